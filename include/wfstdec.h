@@ -1,0 +1,196 @@
+/*
+ * wfstdec: frame-synchronous Viterbi token passing over a WFST decoding graph
+ * with exact lattice generation, lattice pruning and arc posteriors, on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: Chen, Luitjens, Xu, Wang, Povey, Khudanpur, "A GPU-based WFST
+ * Decoder with Exact Lattice Generation", Interspeech 2018 -- token passing
+ * and atomic recombination (Sec. 3.2, Alg. 1), load-balanced arc expansion
+ * (Sec. 3.3), lattice-arc recording (Sec. 3.4), lattice pruning and final
+ * merge (Sec. 3.5), lattice posteriors (Sec. 4.1).
+ *
+ * Conventions for every entry point:
+ *  - Return a wd_status; no exception crosses this boundary.  On a non-OK
+ *    status, wd_last_error() returns a message for the calling thread.
+ *  - "device" pointers are HIP device memory owned by the caller (e.g. torch
+ *    tensors).  The library only borrows them for the duration of the call
+ *    and never allocates device memory itself.
+ *  - Work is enqueued on the caller's stream; wd_decode / wd_decode_batch
+ *    return after the results have been copied to host memory.
+ *  - Results are deterministic: identical inputs give identical outputs,
+ *    bit for bit (posteriors: see wd_lat_arc).
+ */
+#ifndef WFSTDEC_H
+#define WFSTDEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  WD_OK = 0,
+  WD_EINVAL = 1,     /* malformed graph, log-likelihoods or parameters */
+  WD_ECYCLE = 2,     /* the epsilon arcs of the graph contain a cycle */
+  WD_ENOPATH = 3,    /* no token survived some frame */
+  WD_ECAPACITY = 4,  /* the workspace was too small; wd_result_stats reports
+                        the capacities needed, retry with a larger workspace */
+  WD_EDEVICE = 5     /* a HIP call failed */
+} wd_status;
+
+/* Decoding graph (host memory, CSR; arc id = index into the arc arrays).
+ * Arc ids order recombination ties (Sec. 3.2, Alg. 1 packs the arc id under
+ * the cost), so they are part of the result. */
+typedef struct {
+  int32_t num_states;          /* S >= 1 */
+  int64_t num_arcs;            /* A, 0 <= A < 2^32 - 1 */
+  int32_t start_state;         /* 0 <= start < S */
+  const uint32_t* row_ptr;     /* [S+1], row_ptr[0] = 0, non-decreasing, row_ptr[S] = A */
+  const uint32_t* dst;         /* [A] < S */
+  const int32_t* ilabel;       /* [A] 0 = epsilon; k >= 1 reads log-likelihood column k-1 */
+  const int32_t* olabel;       /* [A] >= 0; 0 = no output word */
+  const float* weight;         /* [A] finite, >= 0 */
+  const float* final_weight;   /* [S] >= 0 or +inf (not final); NULL = every state final, cost 0 */
+  int32_t num_pdfs;            /* P: every ilabel must be <= P, 1 <= P < 2^24 */
+} wd_graph_desc;
+
+typedef struct wd_graph wd_graph;
+
+/* Decoding parameters. */
+typedef struct {
+  float beam;          /* > 0, may be +inf: keep tokens within best + beam */
+  int32_t max_active;  /* >= 0; 0 = unlimited; else keep the max_active best (ties kept) */
+  float lattice_beam;  /* >= 0, may be +inf: keep lattice links within this extra cost */
+  uint32_t flags;      /* WD_FLAG_* */
+} wd_params;
+
+/* Return every surviving token of every frame (not only lattice nodes) in
+ * wd_result_tokens; for debugging and tests. */
+#define WD_FLAG_ALL_TOKENS 1u
+
+/* Workspace capacities (per utterance).  0 selects a default.  A decode that
+ * outgrows a capacity fails with WD_ECAPACITY and reports what it needed. */
+typedef struct {
+  int64_t frame_tokens;   /* tokens touched in one frame (<= S) */
+  int64_t frame_arcs;     /* emitting arcs expanded in one frame */
+  int64_t nodes;          /* surviving tokens summed over all frames */
+  int64_t links;          /* lattice links recorded before pruning */
+} wd_caps;
+
+/* One lattice link of the pruned lattice, i.e. one token-passing operation
+ * that survived (Sec. 3.4-3.5).  Links are sorted by (t, arc_id); the pair
+ * is unique.  posterior is computed in fp64 on the pruned lattice; every other
+ * field is exact.  Posteriors agree across runs to within fp64 rounding of the
+ * summation order (<< 1e-9), not necessarily bit for bit. */
+typedef struct {
+  int32_t t;            /* frame of the destination token */
+  uint32_t arc_id;
+  int32_t src_state;    /* source token at frame t-1 (emitting) or t (epsilon) */
+  int32_t dst_state;
+  int32_t ilabel;
+  int32_t olabel;
+  float graph_cost;     /* arc weight */
+  float ac_cost;        /* -loglike[t-1][ilabel-1]; 0 for epsilon links */
+  float fwd_cost;       /* x: cost offered to the destination token */
+  float extra;          /* extra cost of the link (<= lattice_beam) */
+  double posterior;
+} wd_lat_arc;
+
+/* One lattice node: an endpoint of a kept link, or the start token. Sorted by
+ * (t, state). */
+typedef struct {
+  int32_t t;
+  int32_t state;
+  float cost;           /* Viterbi forward cost */
+  float extra;          /* node extra cost */
+} wd_lat_node;
+
+/* One surviving token (WD_FLAG_ALL_TOKENS). Sorted by (t, state). */
+typedef struct {
+  int32_t t;
+  int32_t state;
+  float cost;
+  uint32_t pred_arc;    /* 0xffffffff for the start token */
+} wd_token;
+
+typedef struct {
+  int32_t frames;
+  int32_t final_reached;     /* 1 if final weights were used at the last frame */
+  int64_t arcs_expanded;     /* emitting out-arcs of every surviving token plus the
+                                epsilon out-arcs of every token in the epsilon closure */
+  int64_t tokens;            /* surviving tokens summed over frames */
+  int64_t max_tokens;        /* largest surviving set of one frame */
+  int64_t raw_links;         /* lattice links recorded before pruning */
+  int64_t kept_links;
+  int64_t nodes;             /* lattice nodes returned */
+  wd_caps needed;            /* capacities this decode needed (also on WD_ECAPACITY) */
+} wd_stats;
+
+typedef struct wd_result wd_result;
+
+/* ---- graph ------------------------------------------------------------ */
+
+/* Validate `d` (CSR shape, labels, weights, acyclic epsilon arcs) and return
+ * the device bytes wd_graph_load needs in *bytes.  WD_EINVAL / WD_ECYCLE. */
+wd_status wd_graph_bytes(const wd_graph_desc* d, size_t* bytes);
+
+/* Lay the graph out in `dev_buf` (device, >= wd_graph_bytes, 256-byte
+ * aligned, owned by the caller, must outlive the handle) on `stream`, and
+ * return a host handle in *out.  The graph stays resident in GPU memory
+ * (Sec. 4.3 decodes graphs held entirely in GPU memory).  Synchronous. */
+wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t dev_bytes, void* stream,
+                        wd_graph** out);
+
+/* Frees the host handle only; the caller frees dev_buf. */
+void wd_graph_free(wd_graph* g);
+
+/* Number of epsilon levels (longest epsilon chain + 1, 0 without epsilon arcs). */
+int32_t wd_graph_eps_levels(const wd_graph* g);
+
+/* ---- decoding --------------------------------------------------------- */
+
+/* Device workspace bytes for decoding `lanes` utterances of at most `max_T`
+ * frames each with capacities `caps` (NULL or zero fields: defaults derived
+ * from the graph, max_T and p).  *caps_out (may be NULL) receives the
+ * capacities the layout uses. */
+wd_status wd_workspace_bytes(const wd_graph* g, int32_t lanes, int32_t max_T, const wd_params* p,
+                             const wd_caps* caps, size_t* bytes, wd_caps* caps_out);
+
+/* Decode one utterance.  loglikes: device, T x P row-major fp32 with
+ * P = num_pdfs of the graph; values must not be NaN or +inf and must be
+ * <= 1e30 (-inf marks an impossible pdf).  ws: device workspace of
+ * ws_bytes >= wd_workspace_bytes(g, 1, T, p, caps).  On WD_OK or
+ * WD_ECAPACITY, *out receives a host result to free with wd_result_free. */
+wd_status wd_decode(const wd_graph* g, const float* loglikes, int32_t T, const wd_params* p,
+                    const wd_caps* caps, void* ws, size_t ws_bytes, void* stream, wd_result** out);
+
+/* Decode B independent utterances concurrently against one graph (sequence
+ * parallelism, Sec. 4.2, done as in-process lanes).  loglikes[i] is a device
+ * pointer to T[i] x P fp32.  out[i] receives utterance i's result (lane i
+ * equals wd_decode of utterance i, bit for bit).  The status is the first
+ * non-OK lane status, else WD_OK; every out[i] is filled whenever it is
+ * WD_OK or WD_ECAPACITY for that lane. */
+wd_status wd_decode_batch(const wd_graph* g, int32_t B, const float* const* loglikes,
+                          const int32_t* T, const wd_params* p, const wd_caps* caps, void* ws,
+                          size_t ws_bytes, void* stream, wd_result** out);
+
+/* ---- results (host memory owned by the result) ------------------------ */
+
+wd_status wd_result_status(const wd_result* r);
+float   wd_result_cost(const wd_result* r);
+int32_t wd_result_words(const wd_result* r, const int32_t** words);
+int64_t wd_result_lattice(const wd_result* r, const wd_lat_arc** arcs);
+int64_t wd_result_nodes(const wd_result* r, const wd_lat_node** nodes);
+int64_t wd_result_tokens(const wd_result* r, const wd_token** toks);
+void    wd_result_stats(const wd_result* r, wd_stats* s);
+void    wd_result_free(wd_result* r);
+
+/* Message for the last non-OK status returned on this thread. */
+const char* wd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WFSTDEC_H */
