@@ -66,17 +66,23 @@ typedef struct {
   uint32_t flags;      /* WD_FLAG_* */
 } wd_params;
 
-/* Return every surviving token of every frame (not only lattice nodes) in
- * wd_result_tokens; for debugging and tests. */
-#define WD_FLAG_ALL_TOKENS 1u
+/* Debug output: every surviving token of every frame (wd_result_tokens), the
+ * raw lattice before pruning (wd_result_raw_lattice) and the per-frame cutoffs
+ * (wd_result_cutoffs).  Needs workspace capacity for the raw lattice. */
+#define WD_FLAG_DEBUG 1u
+/* Time the forward (token passing) and lattice kernels with HIP events on the
+ * caller's stream and report them in wd_stats (whole launch: all utterances
+ * of a batch). */
+#define WD_FLAG_TIMING 2u
 
 /* Workspace capacities (per utterance).  0 selects a default.  A decode that
  * outgrows a capacity fails with WD_ECAPACITY and reports what it needed. */
 typedef struct {
   int64_t frame_tokens;   /* tokens touched in one frame (<= S) */
   int64_t frame_arcs;     /* emitting arcs expanded in one frame */
-  int64_t nodes;          /* surviving tokens summed over all frames */
+  int64_t nodes;          /* surviving tokens summed over all frames (< 2^32) */
   int64_t links;          /* lattice links recorded before pruning */
+  int64_t kept_links;     /* lattice links returned (after pruning; raw links with WD_FLAG_DEBUG) */
 } wd_caps;
 
 /* One lattice link of the pruned lattice, i.e. one token-passing operation
@@ -107,7 +113,7 @@ typedef struct {
   float extra;          /* node extra cost */
 } wd_lat_node;
 
-/* One surviving token (WD_FLAG_ALL_TOKENS). Sorted by (t, state). */
+/* One surviving token (WD_FLAG_DEBUG). Sorted by (t, state). */
 typedef struct {
   int32_t t;
   int32_t state;
@@ -125,6 +131,9 @@ typedef struct {
   int64_t raw_links;         /* lattice links recorded before pruning */
   int64_t kept_links;
   int64_t nodes;             /* lattice nodes returned */
+  int64_t eps_arcs_expanded; /* the epsilon part of arcs_expanded */
+  float forward_ms;          /* WD_FLAG_TIMING: token-passing kernel time */
+  float lattice_ms;          /* WD_FLAG_TIMING: lattice kernel time */
   wd_caps needed;            /* capacities this decode needed (also on WD_ECAPACITY) */
 } wd_stats;
 
@@ -183,7 +192,12 @@ float   wd_result_cost(const wd_result* r);
 int32_t wd_result_words(const wd_result* r, const int32_t** words);
 int64_t wd_result_lattice(const wd_result* r, const wd_lat_arc** arcs);
 int64_t wd_result_nodes(const wd_result* r, const wd_lat_node** nodes);
-int64_t wd_result_tokens(const wd_result* r, const wd_token** toks);
+int64_t wd_result_tokens(const wd_result* r, const wd_token** toks);          /* WD_FLAG_DEBUG */
+int64_t wd_result_raw_lattice(const wd_result* r, const wd_lat_arc** arcs);    /* WD_FLAG_DEBUG */
+/* WD_FLAG_DEBUG: per frame t = 0..T the best cost after the emitting step,
+ * the beam cutoff and the final cutoff; returns T+1. */
+int32_t wd_result_cutoffs(const wd_result* r, const float** best, const float** cutoff_beam,
+                          const float** cutoff);
 void    wd_result_stats(const wd_result* r, wd_stats* s);
 void    wd_result_free(wd_result* r);
 

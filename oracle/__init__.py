@@ -56,7 +56,8 @@ class _Stats(ctypes.Structure):
     _fields_ = [("frames", ctypes.c_int32), ("final_reached", ctypes.c_int32),
                 ("arcs_expanded", ctypes.c_int64), ("tokens", ctypes.c_int64),
                 ("max_tokens", ctypes.c_int64), ("raw_links", ctypes.c_int64),
-                ("kept_links", ctypes.c_int64), ("nodes", ctypes.c_int64)]
+                ("kept_links", ctypes.c_int64), ("nodes", ctypes.c_int64),
+                ("eps_arcs_expanded", ctypes.c_int64)]
 
 
 def build(force: bool = False) -> str:

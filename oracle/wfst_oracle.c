@@ -282,7 +282,10 @@ static int finish_frame(dec* d, int32_t t, float best) {
   float cutb = best + d->p.beam;
   prune_list(d, cutb);
   eps_closure(d, cutb);
-  for (int64_t i = 0; i < d->nlist; ++i) d->st.arcs_expanded += eps_deg(g, d->list[i]);
+  for (int64_t i = 0; i < d->nlist; ++i) {
+    d->st.arcs_expanded += eps_deg(g, d->list[i]);
+    d->st.eps_arcs_expanded += eps_deg(g, d->list[i]);
+  }
   float cut = cutb;
   if (d->p.max_active > 0 && d->nlist > d->p.max_active) {
     for (int64_t i = 0; i < d->nlist; ++i) d->sortbuf[i] = d->cost[d->list[i]];

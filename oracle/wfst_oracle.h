@@ -80,6 +80,7 @@ typedef struct {
   int64_t raw_links;        /* links recorded before pruning */
   int64_t kept_links;
   int64_t nodes;
+  int64_t eps_arcs_expanded;  /* the epsilon part of arcs_expanded */
 } wdo_stats;
 
 typedef struct wdo_result wdo_result;

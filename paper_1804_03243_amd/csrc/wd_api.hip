@@ -1,0 +1,405 @@
+// Decode entry points: workspace layout, launches, results.
+//
+// One workgroup decodes one utterance from the first frame to the last inside
+// one launch (no per-frame host round trips; the paper's "other" time of
+// launches and synchronisation, Sec. 4.3, is what this avoids).  A batch runs
+// its utterances as concurrent workgroups sharing the resident graph, which is
+// the paper's sequence parallelism (Sec. 4.2) done in one process.
+#include <algorithm>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "wd_host.h"
+
+namespace wd {
+
+static thread_local std::string g_err;
+
+void set_error(const std::string& msg) { g_err = msg; }
+
+wd_status fail(wd_status st, const std::string& msg) {
+  g_err = msg;
+  return st;
+}
+
+wd_status hip_check(hipError_t e, const char* what) {
+  if (e == hipSuccess) return WD_OK;
+  return fail(WD_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+namespace {
+
+struct Caps {
+  uint64_t frame, arcs, nodes, links, kept, raw, words;
+};
+
+Caps resolve_caps(const wd_graph* g, int32_t max_T, const wd_params* p, const wd_caps* c) {
+  Caps r{};
+  const uint64_t S = (uint64_t)g->S;
+  const uint64_t ma = p->max_active > 0 ? (uint64_t)p->max_active : 0;
+  r.frame = (c && c->frame_tokens > 0) ? (uint64_t)c->frame_tokens
+                                       : (ma ? std::min<uint64_t>(S, std::max<uint64_t>(65536, 16 * ma)) : S);
+  r.frame = std::min<uint64_t>(r.frame, S);
+  r.arcs = (c && c->frame_arcs > 0) ? (uint64_t)c->frame_arcs
+                                    : (ma ? std::min<uint64_t>(g->Ae, std::max<uint64_t>(262144, 64 * ma)) : g->Ae);
+  r.arcs = std::max<uint64_t>(std::min<uint64_t>(r.arcs, g->Ae), 1);
+  const uint64_t T1 = (uint64_t)max_T + 1;
+  r.nodes = (c && c->nodes > 0) ? (uint64_t)c->nodes : T1 * std::min<uint64_t>(S, 1024);
+  r.nodes = std::min<uint64_t>(r.nodes, 0xfffffff0ull);
+  r.links = (c && c->links > 0) ? (uint64_t)c->links : 4 * r.nodes;
+  r.kept = (c && c->kept_links > 0) ? (uint64_t)c->kept_links : std::min<uint64_t>(r.links, 1u << 20);
+  r.raw = (p->flags & WD_FLAG_DEBUG) ? r.links : 0;
+  r.words = T1 * (g->nlevels + 1) + 1;
+  return r;
+}
+
+// Lays every per-utterance array out as one region per array (all lanes side
+// by side) so the per-decode resets are one fill each.  With base == nullptr
+// only sizes the workspace.
+struct Regions {
+  LaneDesc* desc;
+  LaneInfo* info;
+  uint32_t* bad;
+  unsigned long long* slot;
+  uint32_t* bitmap;
+  uint32_t* used;
+  uint64_t bitmap_words, used_words;
+  uint64_t total;
+};
+
+Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base,
+              std::vector<LaneDesc>* lanes) {
+  Regions R{};
+  uint64_t p = 0;
+  auto take = [&](uint64_t per_lane_bytes) -> char* {
+    char* at = base ? base + p : nullptr;
+    p = align_up(p + per_lane_bytes * (uint64_t)B, 256);
+    return at;
+  };
+  const uint64_t S = (uint64_t)g->S;
+  const uint64_t F1 = c.frame + 1;
+  const uint64_t T2 = (uint64_t)max_T + 2;
+  R.desc = (LaneDesc*)take(sizeof(LaneDesc));
+  R.info = (LaneInfo*)take(sizeof(LaneInfo));
+  R.bad = (uint32_t*)take(sizeof(uint32_t));
+  R.bitmap_words = (S + 31) / 32;
+  R.used_words = (c.nodes + 31) / 32 + 1;
+  char* slot = take(8 * S);
+  char* idx = take(4 * S);
+  char* bitmap = take(4 * R.bitmap_words);
+  char* bucket = take(4 * S);
+  char* touched = take(4 * c.frame);
+  char* surv_state = take(4 * c.frame);
+  char* surv_pack = take(8 * c.frame);
+  char* f_state[2], *f_key[2], *f_edeg[2], *f_xdeg[2], *f_cls[2];
+  for (int i = 0; i < 2; ++i) {
+    f_state[i] = take(4 * F1);
+    f_key[i] = take(4 * F1);
+    f_edeg[i] = take(4 * F1);
+    f_xdeg[i] = take(4 * F1);
+    f_cls[i] = take(F1);
+  }
+  char* cand = take(16 * c.arcs);
+  char* n_state = take(4 * c.nodes);
+  char* n_pack = take(8 * c.nodes);
+  char* n_pred = take(4 * c.nodes);
+  char* links = take(16 * c.links);
+  char* link_lvl = take(c.links);
+  char* node_off = take(8 * T2);
+  char* link_off = take(8 * T2);
+  char* link_xoff = take(8 * T2);
+  char* best = take(4 * T2);
+  char* cutb = take(4 * T2);
+  char* cut = take(4 * T2);
+  char* extra_key = take(4 * c.nodes);
+  char* le_key = take(4 * c.links);
+  char* alpha = take(8 * c.nodes);
+  char* beta = take(8 * c.nodes);
+  char* used = take(4 * R.used_words);
+  char* kept_idx = take(8 * c.kept);
+  char* out_links = take(sizeof(OutLink) * c.kept);
+  char* out_raw = take(sizeof(OutLink) * c.raw);
+  char* out_nodes = take(sizeof(OutNode) * (2 * c.kept + 1));
+  char* out_words = take(4 * c.words);
+  R.total = p;
+  R.slot = (unsigned long long*)slot;
+  R.bitmap = (uint32_t*)bitmap;
+  R.used = (uint32_t*)used;
+  if (lanes) {
+    for (int b = 0; b < B; ++b) {
+      LaneDesc& L = (*lanes)[b];
+      auto at = [&](char* region, uint64_t per_lane) { return region + (uint64_t)b * per_lane; };
+      L.frame_cap = c.frame;
+      L.cand_cap = c.arcs;
+      L.node_cap = c.nodes;
+      L.link_cap = c.links;
+      L.kept_cap = c.kept;
+      L.raw_cap = c.raw;
+      L.word_cap = c.words;
+      L.slot = (unsigned long long*)at(slot, 8 * S);
+      L.idx = (uint32_t*)at(idx, 4 * S);
+      L.bitmap = (uint32_t*)at(bitmap, 4 * R.bitmap_words);
+      L.bucket = (uint32_t*)at(bucket, 4 * S);
+      L.touched = (uint32_t*)at(touched, 4 * c.frame);
+      L.surv_state = (uint32_t*)at(surv_state, 4 * c.frame);
+      L.surv_pack = (unsigned long long*)at(surv_pack, 8 * c.frame);
+      for (int i = 0; i < 2; ++i) {
+        L.f_state[i] = (uint32_t*)at(f_state[i], 4 * F1);
+        L.f_key[i] = (uint32_t*)at(f_key[i], 4 * F1);
+        L.f_edeg[i] = (uint32_t*)at(f_edeg[i], 4 * F1);
+        L.f_xdeg[i] = (uint32_t*)at(f_xdeg[i], 4 * F1);
+        L.f_cls[i] = (uint8_t*)at(f_cls[i], F1);
+      }
+      L.cand = (uint4*)at(cand, 16 * c.arcs);
+      L.n_state = (uint32_t*)at(n_state, 4 * c.nodes);
+      L.n_pack = (unsigned long long*)at(n_pack, 8 * c.nodes);
+      L.n_pred = (uint32_t*)at(n_pred, 4 * c.nodes);
+      L.links = (uint4*)at(links, 16 * c.links);
+      L.link_lvl = (uint8_t*)at(link_lvl, c.links);
+      L.node_off = (uint64_t*)at(node_off, 8 * T2);
+      L.link_off = (uint64_t*)at(link_off, 8 * T2);
+      L.link_xoff = (uint64_t*)at(link_xoff, 8 * T2);
+      L.best = (float*)at(best, 4 * T2);
+      L.cutb = (float*)at(cutb, 4 * T2);
+      L.cut = (float*)at(cut, 4 * T2);
+      L.extra_key = (uint32_t*)at(extra_key, 4 * c.nodes);
+      L.le_key = (uint32_t*)at(le_key, 4 * c.links);
+      L.alpha = (double*)at(alpha, 8 * c.nodes);
+      L.beta = (double*)at(beta, 8 * c.nodes);
+      L.used = (uint32_t*)at(used, 4 * R.used_words);
+      L.kept_idx = (uint64_t*)at(kept_idx, 8 * c.kept);
+      L.out_links = (OutLink*)at(out_links, sizeof(OutLink) * c.kept);
+      L.out_raw = (OutLink*)at(out_raw, sizeof(OutLink) * c.raw);
+      L.out_nodes = (OutNode*)at(out_nodes, sizeof(OutNode) * (2 * c.kept + 1));
+      L.out_words = (int32_t*)at(out_words, 4 * c.words);
+      L.info = R.info + b;
+    }
+  }
+  return R;
+}
+
+wd_status check_params(const wd_params* p) {
+  if (!p) return fail(WD_EINVAL, "decode: null params");
+  if (!(p->beam > 0.0f)) return fail(WD_EINVAL, "decode: beam must be > 0");
+  if (p->max_active < 0) return fail(WD_EINVAL, "decode: max_active must be >= 0");
+  if (!(p->lattice_beam >= 0.0f)) return fail(WD_EINVAL, "decode: lattice_beam must be >= 0");
+  return WD_OK;
+}
+
+}  // namespace
+
+}  // namespace wd
+
+struct wd_result {
+  wd_status status = WD_OK;
+  float cost = 0.0f;
+  std::vector<int32_t> words;
+  std::vector<wd_lat_arc> links, raw;
+  std::vector<wd_lat_node> nodes;
+  std::vector<wd_token> tokens;
+  std::vector<float> best, cutb, cut;
+  wd_stats stats{};
+};
+
+static_assert(sizeof(wd_lat_arc) == sizeof(wd::OutLink), "link record layout");
+static_assert(sizeof(wd_lat_node) == sizeof(wd::OutNode), "node record layout");
+
+using namespace wd;
+
+extern "C" wd_status wd_workspace_bytes(const wd_graph* g, int32_t lanes, int32_t max_T, const wd_params* p,
+                                        const wd_caps* caps, size_t* bytes, wd_caps* caps_out) {
+  if (!g || !bytes || lanes < 1 || max_T < 0 || max_T > (1 << 24))
+    return fail(WD_EINVAL, "workspace_bytes: bad arguments");
+  wd_status st = check_params(p);
+  if (st != WD_OK) return st;
+  const Caps c = resolve_caps(g, max_T, p, caps);
+  *bytes = carve(g, lanes, max_T, c, nullptr, nullptr).total;
+  if (caps_out) {
+    caps_out->frame_tokens = (int64_t)c.frame;
+    caps_out->frame_arcs = (int64_t)c.arcs;
+    caps_out->nodes = (int64_t)c.nodes;
+    caps_out->links = (int64_t)c.links;
+    caps_out->kept_links = (int64_t)c.kept;
+  }
+  return WD_OK;
+}
+
+static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* ll, const int32_t* T,
+                             const wd_params* p, const wd_caps* caps, void* ws, size_t ws_bytes,
+                             void* stream, wd_result** out) {
+  if (!g || B < 1 || !ll || !T || !out) return fail(WD_EINVAL, "decode: bad arguments");
+  for (int b = 0; b < B; ++b) out[b] = nullptr;
+  wd_status st = check_params(p);
+  if (st != WD_OK) return st;
+  int32_t max_T = 0;
+  for (int b = 0; b < B; ++b) {
+    if (T[b] < 0 || T[b] > (1 << 24)) return fail(WD_EINVAL, "decode: T out of range");
+    if (T[b] > 0 && !ll[b]) return fail(WD_EINVAL, "decode: null log-likelihoods");
+    max_T = std::max(max_T, T[b]);
+  }
+  if (!ws || ((uintptr_t)ws & 255u)) return fail(WD_EINVAL, "decode: workspace must be 256-byte aligned");
+  const Caps c = resolve_caps(g, max_T, p, caps);
+  std::vector<LaneDesc> lanes((size_t)B);
+  std::memset(lanes.data(), 0, sizeof(LaneDesc) * (size_t)B);
+  const Regions R = carve(g, B, max_T, c, (char*)ws, &lanes);
+  if (ws_bytes < R.total)
+    return fail(WD_EINVAL, "decode: workspace of " + std::to_string(ws_bytes) + " bytes, need " +
+                               std::to_string(R.total));
+  for (int b = 0; b < B; ++b) {
+    lanes[b].ll = ll[b];
+    lanes[b].T = T[b];
+  }
+  hipStream_t s = (hipStream_t)stream;
+  const Params prm{p->beam, p->max_active, p->lattice_beam, p->flags};
+  const uint64_t S = (uint64_t)g->S;
+  if ((st = hip_check(hipMemcpyAsync(R.desc, lanes.data(), sizeof(LaneDesc) * B, hipMemcpyHostToDevice, s),
+                      "lane upload")))
+    return st;
+  launch_fill_u32((uint32_t*)R.info, (uint64_t)B * sizeof(LaneInfo) / 4, 0u, s);
+  launch_fill_u32(R.bad, (uint64_t)B, 0u, s);
+  launch_fill_u64(R.slot, (uint64_t)B * S, kEmpty, s);
+  launch_fill_u32(R.bitmap, (uint64_t)B * R.bitmap_words, 0u, s);
+  launch_fill_u32(R.used, (uint64_t)B * R.used_words, 0u, s);
+  launch_check_loglikes(R.desc, B, g->P, R.bad, s);
+  const bool timing = (p->flags & WD_FLAG_TIMING) != 0;
+  hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
+  if (timing)
+    for (auto& e : ev)
+      if ((st = hip_check(hipEventCreate(&e), "event"))) return st;
+  if (timing) (void)hipEventRecord(ev[0], s);
+  launch_forward(g->dg, R.desc, B, prm, R.bad, s);
+  if (timing) (void)hipEventRecord(ev[1], s);
+  launch_lattice(g->dg, R.desc, B, prm, s);
+  if (timing) (void)hipEventRecord(ev[2], s);
+  if ((st = hip_check(hipGetLastError(), "launch"))) return st;
+  std::vector<LaneInfo> info((size_t)B);
+  if ((st = hip_check(hipMemcpyAsync(info.data(), R.info, sizeof(LaneInfo) * B, hipMemcpyDeviceToHost, s),
+                      "info download")) ||
+      (st = hip_check(hipStreamSynchronize(s), "decode")))
+    return st;
+
+  float fwd_ms = 0.0f, lat_ms = 0.0f;
+  if (timing) {
+    (void)hipEventElapsedTime(&fwd_ms, ev[0], ev[1]);
+    (void)hipEventElapsedTime(&lat_ms, ev[1], ev[2]);
+    for (auto& e : ev) (void)hipEventDestroy(e);
+  }
+  wd_status first_bad = WD_OK;
+  const bool debug = (p->flags & WD_FLAG_DEBUG) != 0;
+  for (int b = 0; b < B; ++b) {
+    const LaneInfo& I = info[b];
+    const LaneDesc& L = lanes[b];
+    const wd_status ls = (wd_status)I.status;
+    if (ls != WD_OK && first_bad == WD_OK) first_bad = ls;
+    if (ls != WD_OK && ls != WD_ECAPACITY) continue;
+    wd_result* r = new wd_result();
+    r->status = ls;
+    r->cost = I.best_cost;
+    wd_stats& stt = r->stats;
+    stt.frames = T[b];
+    stt.final_reached = I.final_used;
+    stt.arcs_expanded = (int64_t)I.arcs_expanded;
+    stt.tokens = (int64_t)I.tokens;
+    stt.max_tokens = (int64_t)I.max_tokens;
+    stt.raw_links = (int64_t)I.links;
+    stt.kept_links = (int64_t)I.kept;
+    stt.nodes = (int64_t)I.out_nodes;
+    stt.eps_arcs_expanded = (int64_t)I.eps_arcs;
+    stt.forward_ms = fwd_ms;
+    stt.lattice_ms = lat_ms;
+    stt.needed.frame_tokens = (int64_t)I.need_frame_tokens;
+    stt.needed.frame_arcs = (int64_t)I.need_frame_arcs;
+    stt.needed.nodes = (int64_t)I.tokens;
+    stt.needed.links = (int64_t)I.links;
+    stt.needed.kept_links = (int64_t)std::max<uint64_t>(I.kept, debug ? I.links : 0);
+    out[b] = r;
+    if (ls != WD_OK) continue;
+    r->words.resize(I.nwords);
+    r->links.resize(I.kept);
+    r->nodes.resize(I.out_nodes);
+    auto d2h = [&](void* dst, const void* src, uint64_t bytes) -> wd_status {
+      if (!bytes) return WD_OK;
+      return hip_check(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s), "result download");
+    };
+    if ((st = d2h(r->words.data(), L.out_words, 4 * I.nwords)) ||
+        (st = d2h(r->links.data(), L.out_links, sizeof(OutLink) * I.kept)) ||
+        (st = d2h(r->nodes.data(), L.out_nodes, sizeof(OutNode) * I.out_nodes)))
+      return st;
+    if (debug) {
+      const uint64_t nn = I.tokens;
+      std::vector<uint32_t> ns(nn);
+      std::vector<unsigned long long> np(nn);
+      std::vector<uint64_t> noff((size_t)T[b] + 2);
+      r->raw.resize(I.out_raw);
+      r->best.resize((size_t)T[b] + 1);
+      r->cutb.resize((size_t)T[b] + 1);
+      r->cut.resize((size_t)T[b] + 1);
+      if ((st = d2h(ns.data(), L.n_state, 4 * nn)) || (st = d2h(np.data(), L.n_pack, 8 * nn)) ||
+          (st = d2h(noff.data(), L.node_off, 8 * ((uint64_t)T[b] + 2))) ||
+          (st = d2h(r->raw.data(), L.out_raw, sizeof(OutLink) * I.out_raw)) ||
+          (st = d2h(r->best.data(), L.best, 4 * ((uint64_t)T[b] + 1))) ||
+          (st = d2h(r->cutb.data(), L.cutb, 4 * ((uint64_t)T[b] + 1))) ||
+          (st = d2h(r->cut.data(), L.cut, 4 * ((uint64_t)T[b] + 1))) ||
+          (st = hip_check(hipStreamSynchronize(s), "debug download")))
+        return st;
+      r->tokens.resize(nn);
+      for (int t = 0; t <= T[b]; ++t)
+        for (uint64_t n = noff[t]; n < noff[t + 1]; ++n)
+          r->tokens[n] = wd_token{t, (int32_t)ns[n], key_cost((uint32_t)(np[n] >> 32)), (uint32_t)np[n]};
+    }
+  }
+  if ((st = hip_check(hipStreamSynchronize(s), "result download"))) return st;
+  if (first_bad != WD_OK) {
+    std::string msg = first_bad == WD_ENOPATH   ? "decode: no token survived a frame"
+                      : first_bad == WD_EINVAL  ? "decode: log-likelihoods contain NaN, +inf or values above 1e30"
+                      : first_bad == WD_ECAPACITY ? "decode: workspace capacity exceeded; see stats.needed"
+                      : first_bad == WD_EDEVICE ? "decode: a kernel's internal consistency check failed"
+                                                : "decode failed";
+    set_error(msg);
+  }
+  return first_bad;
+}
+
+extern "C" wd_status wd_decode(const wd_graph* g, const float* loglikes, int32_t T, const wd_params* p,
+                               const wd_caps* caps, void* ws, size_t ws_bytes, void* stream, wd_result** out) {
+  return decode_impl(g, 1, &loglikes, &T, p, caps, ws, ws_bytes, stream, out);
+}
+
+extern "C" wd_status wd_decode_batch(const wd_graph* g, int32_t B, const float* const* loglikes, const int32_t* T,
+                                     const wd_params* p, const wd_caps* caps, void* ws, size_t ws_bytes,
+                                     void* stream, wd_result** out) {
+  return decode_impl(g, B, loglikes, T, p, caps, ws, ws_bytes, stream, out);
+}
+
+extern "C" wd_status wd_result_status(const wd_result* r) { return r->status; }
+extern "C" float wd_result_cost(const wd_result* r) { return r->cost; }
+extern "C" int32_t wd_result_words(const wd_result* r, const int32_t** w) {
+  *w = r->words.data();
+  return (int32_t)r->words.size();
+}
+extern "C" int64_t wd_result_lattice(const wd_result* r, const wd_lat_arc** a) {
+  *a = r->links.data();
+  return (int64_t)r->links.size();
+}
+extern "C" int64_t wd_result_nodes(const wd_result* r, const wd_lat_node** n) {
+  *n = r->nodes.data();
+  return (int64_t)r->nodes.size();
+}
+extern "C" int64_t wd_result_tokens(const wd_result* r, const wd_token** t) {
+  *t = r->tokens.data();
+  return (int64_t)r->tokens.size();
+}
+extern "C" int64_t wd_result_raw_lattice(const wd_result* r, const wd_lat_arc** a) {
+  *a = r->raw.data();
+  return (int64_t)r->raw.size();
+}
+extern "C" int32_t wd_result_cutoffs(const wd_result* r, const float** b, const float** cb, const float** c) {
+  *b = r->best.data();
+  *cb = r->cutb.data();
+  *c = r->cut.data();
+  return (int32_t)r->best.size();
+}
+extern "C" void wd_result_stats(const wd_result* r, wd_stats* s) { *s = r->stats; }
+extern "C" void wd_result_free(wd_result* r) { delete r; }
+extern "C" const char* wd_last_error(void) { return g_err.c_str(); }

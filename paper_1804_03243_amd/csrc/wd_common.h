@@ -1,0 +1,175 @@
+// Shared definitions of the wfstdec GPU library (host and device).
+//
+// Decoder state follows the paper's token passing (Sec. 3.2): every WFST state
+// holds at most one token per frame; recombination keeps the candidate with the
+// smallest (cost, arc id), packed into one 64-bit word so a single atomicMin
+// decides it (Alg. 1).  Costs are fp32; the packing uses an order-preserving
+// fp32 -> u32 key so negative costs order correctly.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wd {
+
+constexpr uint64_t kEmpty = ~0ull;          // slot holds no token
+constexpr uint32_t kNoArc = 0xffffffffu;    // predecessor of the start token
+constexpr uint32_t kNoEps = 0xffu;          // class byte: state has no epsilon out-arcs
+constexpr int kMaxLevels = 254;             // epsilon levels 0..253
+constexpr int kThreads = 1024;              // one workgroup per utterance
+constexpr int kWaves = kThreads / 64;
+constexpr int kRankMax = 2048;              // survivors sorted in LDS up to this many
+constexpr int kHistBins = 2048;             // 11-bit radix digits for max-active
+constexpr uint32_t kInfKey = 0xff800000u;   // key of +inf
+
+// Order-preserving map of fp32 onto u32 (-0.0 folded onto +0.0): for non-NaN
+// a, b: a < b  <=>  cost_key(a) < cost_key(b).
+__host__ __device__ inline uint32_t cost_key(float x) {
+  union { float f; uint32_t u; } v;
+  v.f = (x == 0.0f) ? 0.0f : x;
+  return (v.u & 0x80000000u) ? ~v.u : (v.u | 0x80000000u);
+}
+
+__host__ __device__ inline float key_cost(uint32_t k) {
+  union { float f; uint32_t u; } v;
+  v.u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+  return v.f;
+}
+
+__host__ __device__ inline uint64_t pack_tok(uint32_t key, uint32_t arc) {
+  return ((uint64_t)key << 32) | arc;
+}
+
+// Device copy of the decoding graph, laid out in one caller-owned buffer.
+//   off[s]  = {first emitting arc, first epsilon arc} of state s (S+1 entries)
+//   earc[i] = {dst, weight bits, ilabel | dst_class << 24, arc id}
+//   xarc[j] = {dst, weight bits, dst_class, arc id}
+// Arcs of a state keep the caller's order, so within a state arc ids ascend.
+// dst_class is the epsilon level of the destination state when it has
+// epsilon out-arcs, else kNoEps.  Epsilon arcs always climb to a strictly
+// higher level, so relaxing levels in order closes a frame exactly.
+struct DevGraph {
+  const uint2* off;
+  const uint4* earc;
+  const uint4* xarc;
+  const uint8_t* sclass;       // [S] class of every state
+  const float* final_w;        // [S] or nullptr
+  const int32_t* ilabel_id;    // [A] by caller arc id
+  const int32_t* olabel_id;    // [A]
+  const float* weight_id;      // [A]
+  const uint32_t* level_base;  // [nlevels + 1] bucket offsets of the epsilon levels
+  uint32_t S;
+  uint32_t start;
+  uint32_t nlevels;
+  uint32_t P;
+  uint64_t Ae;
+  uint64_t Ax;
+  uint64_t A;
+};
+
+struct Params {
+  float beam;
+  int32_t max_active;
+  float lattice_beam;
+  uint32_t flags;
+};
+
+// Per-utterance counters and status, written by the kernels.
+struct LaneInfo {
+  int32_t status;              // WD_* code
+  int32_t frames_done;
+  int32_t final_used;
+  uint32_t overflow;           // bit mask of exceeded capacities (kOvf*)
+  uint64_t arcs_expanded;
+  uint64_t eps_arcs;           // epsilon part of arcs_expanded
+  uint64_t tokens;             // surviving tokens summed over frames (= nodes recorded)
+  uint64_t max_tokens;
+  uint64_t links;              // raw lattice links
+  uint64_t need_frame_tokens;  // largest per-frame touched-state count
+  uint64_t need_frame_arcs;    // largest per-frame emitting work
+  uint64_t kept;               // kept lattice links
+  uint64_t out_nodes;
+  uint64_t nwords;
+  uint64_t out_raw;            // raw links written to the debug output
+  uint32_t start_node;
+  uint32_t best_node;
+  float best_cost;
+  float pad;
+};
+
+enum : uint32_t { kOvfFrame = 1, kOvfArcs = 2, kOvfNodes = 4, kOvfLinks = 8, kOvfKept = 16 };
+// LaneInfo::status value for an internal consistency failure caught by a
+// kernel's own bounds checks (reported as WD_EDEVICE).
+constexpr int32_t kStatusInternal = 5;
+
+// Device output records (match wd_lat_arc / wd_lat_node / wd_token of wfstdec.h).
+struct OutLink {
+  int32_t t;
+  uint32_t arc_id;
+  int32_t src_state;
+  int32_t dst_state;
+  int32_t ilabel;
+  int32_t olabel;
+  float graph_cost;
+  float ac_cost;
+  float fwd_cost;
+  float extra;
+  double posterior;
+};
+struct OutNode {
+  int32_t t;
+  int32_t state;
+  float cost;
+  float extra;
+};
+
+// Everything one utterance needs on the device.  Built on the host; lives in
+// the workspace.
+struct LaneDesc {
+  const float* ll;             // T x P log-likelihoods
+  int32_t T;
+  int32_t pad0;
+  uint64_t frame_cap, cand_cap, node_cap, link_cap, kept_cap, word_cap;
+  // per-frame scratch
+  unsigned long long* slot;    // [S] packed (cost key, arc id); kEmpty between frames
+  uint32_t* idx;               // [S] node id of a state in the current frame / scratch
+  uint32_t* bitmap;            // [ceil(S/32)] zero between frames
+  uint32_t* touched;           // [frame_cap] states touched this frame
+  uint32_t* bucket;            // [S] touched states with epsilon arcs, by level
+  uint32_t* surv_state;        // [frame_cap] tokens within the beam cutoff
+  unsigned long long* surv_pack;
+  uint32_t* f_state[2];        // frontier (surviving tokens of a frame, sorted by state)
+  uint32_t* f_key[2];
+  uint32_t* f_edeg[2];         // exclusive prefix of emitting out-degree
+  uint32_t* f_xdeg[2];         // exclusive prefix of epsilon out-degree
+  uint8_t* f_cls[2];
+  uint4* cand;                 // [cand_cap] emitting candidates {arc, src node, dst, x bits}
+  // history
+  uint32_t* n_state;           // [node_cap]
+  unsigned long long* n_pack;  // [node_cap] (cost key, predecessor arc)
+  uint32_t* n_pred;            // [node_cap] predecessor node
+  uint4* links;                // [link_cap] {arc, src node, dst node, x bits}
+  uint8_t* link_lvl;           // [link_cap] epsilon level of the source (epsilon links)
+  uint64_t* node_off;          // [T+2]
+  uint64_t* link_off;          // [T+2] first link of frame t (emitting run)
+  uint64_t* link_xoff;         // [T+2] first epsilon link of frame t
+  float* best;                 // [T+1]
+  float* cutb;                 // [T+1]
+  float* cut;                  // [T+1]
+  // lattice pass
+  uint32_t* extra_key;         // [node_cap]
+  uint32_t* le_key;            // [link_cap]
+  double* alpha;               // [node_cap]
+  double* beta;                // [node_cap]
+  uint32_t* used;              // [ceil(node_cap/32)+1] lattice-node bitmap
+  uint64_t* kept_idx;          // [kept_cap] kept link ids in link order
+  // outputs
+  OutLink* out_links;          // [kept_cap]
+  OutLink* out_raw;            // [raw_cap] every raw link (debug output)
+  uint64_t raw_cap;
+  OutNode* out_nodes;          // [2*kept_cap+1]
+  int32_t* out_words;          // [word_cap]
+  LaneInfo* info;
+};
+
+}  // namespace wd

@@ -1,0 +1,236 @@
+// Graph loading: validation, epsilon levels, and the device layout.
+//
+// The graph stays resident in GPU memory for every decode (the paper decodes
+// graphs held entirely in GPU memory, Sec. 4.3).  Emitting and epsilon arcs are
+// split into two CSRs of 16-byte records so the emitting expansion reads only
+// the arcs it uses, each with one 16-byte load.  Epsilon levels (longest
+// epsilon path into a state) order the epsilon closure: an epsilon arc always
+// climbs to a higher level.
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "wd_host.h"
+
+namespace wd {
+
+namespace {
+
+struct Prepared {
+  std::vector<uint2> off;
+  std::vector<uint4> earc, xarc;
+  std::vector<uint8_t> sclass;
+  std::vector<uint32_t> level_base;
+  uint32_t nlevels = 0;
+};
+
+struct Layout {
+  uint64_t off, earc, xarc, sclass, final_w, ilabel, olabel, weight, level_base, total;
+};
+
+Layout layout(int64_t S, int64_t A, uint64_t Ae, uint64_t Ax, uint32_t nlevels, bool finals) {
+  Layout l{};
+  uint64_t p = 0;
+  auto take = [&](uint64_t bytes) {
+    uint64_t at = p;
+    p = align_up(p + bytes, 256);
+    return at;
+  };
+  l.off = take(sizeof(uint2) * (uint64_t)(S + 1));
+  l.earc = take(sizeof(uint4) * (Ae ? Ae : 1));
+  l.xarc = take(sizeof(uint4) * (Ax ? Ax : 1));
+  l.sclass = take((uint64_t)S);
+  l.final_w = finals ? take(sizeof(float) * (uint64_t)S) : 0;
+  l.ilabel = take(sizeof(int32_t) * (uint64_t)(A ? A : 1));
+  l.olabel = take(sizeof(int32_t) * (uint64_t)(A ? A : 1));
+  l.weight = take(sizeof(float) * (uint64_t)(A ? A : 1));
+  l.level_base = take(sizeof(uint32_t) * (uint64_t)(nlevels + 1));
+  l.total = p;
+  return l;
+}
+
+wd_status validate(const wd_graph_desc* d) {
+  if (!d) return fail(WD_EINVAL, "graph: null descriptor");
+  const int64_t S = d->num_states, A = d->num_arcs;
+  if (S < 1) return fail(WD_EINVAL, "graph: num_states must be >= 1");
+  if (A < 0 || A >= (int64_t)0xffffffffu) return fail(WD_EINVAL, "graph: num_arcs out of range");
+  if (d->start_state < 0 || d->start_state >= S) return fail(WD_EINVAL, "graph: start_state out of range");
+  if (d->num_pdfs < 1 || d->num_pdfs >= (1 << 24)) return fail(WD_EINVAL, "graph: num_pdfs out of range");
+  if (!d->row_ptr) return fail(WD_EINVAL, "graph: null row_ptr");
+  if (A > 0 && (!d->dst || !d->ilabel || !d->olabel || !d->weight))
+    return fail(WD_EINVAL, "graph: null arc array");
+  if (d->row_ptr[0] != 0 || (int64_t)d->row_ptr[S] != A)
+    return fail(WD_EINVAL, "graph: row_ptr must start at 0 and end at num_arcs");
+  for (int64_t s = 0; s < S; ++s)
+    if (d->row_ptr[s] > d->row_ptr[s + 1]) return fail(WD_EINVAL, "graph: row_ptr decreases");
+  for (int64_t a = 0; a < A; ++a) {
+    if ((int64_t)d->dst[a] >= S) return fail(WD_EINVAL, "graph: dst out of range at arc " + std::to_string(a));
+    if (d->ilabel[a] < 0 || d->ilabel[a] > d->num_pdfs)
+      return fail(WD_EINVAL, "graph: ilabel out of range at arc " + std::to_string(a));
+    if (d->olabel[a] < 0) return fail(WD_EINVAL, "graph: negative olabel at arc " + std::to_string(a));
+    const float w = d->weight[a];
+    if (!(w >= 0.0f) || std::isinf(w))
+      return fail(WD_EINVAL, "graph: weight must be finite and >= 0 at arc " + std::to_string(a));
+  }
+  if (d->final_weight)
+    for (int64_t s = 0; s < S; ++s)
+      if (!(d->final_weight[s] >= 0.0f)) return fail(WD_EINVAL, "graph: final weight must be >= 0 or +inf");
+  return WD_OK;
+}
+
+// Longest epsilon path into every state, by Kahn's order over epsilon arcs;
+// WD_ECYCLE when some state is never freed.
+wd_status eps_levels(const wd_graph_desc* d, std::vector<uint32_t>& level) {
+  const int64_t S = d->num_states;
+  std::vector<uint32_t> indeg((size_t)S, 0);
+  for (int64_t a = 0; a < d->num_arcs; ++a)
+    if (d->ilabel[a] == 0) indeg[d->dst[a]]++;
+  std::vector<uint32_t> queue;
+  queue.reserve((size_t)S);
+  level.assign((size_t)S, 0);
+  for (int64_t s = 0; s < S; ++s)
+    if (!indeg[s]) queue.push_back((uint32_t)s);
+  for (size_t h = 0; h < queue.size(); ++h) {
+    const uint32_t s = queue[h];
+    for (uint32_t a = d->row_ptr[s]; a < d->row_ptr[s + 1]; ++a) {
+      if (d->ilabel[a] != 0) continue;
+      const uint32_t v = d->dst[a];
+      if (level[v] < level[s] + 1) level[v] = level[s] + 1;
+      if (--indeg[v] == 0) queue.push_back(v);
+    }
+  }
+  if ((int64_t)queue.size() != S) return fail(WD_ECYCLE, "graph: epsilon arcs contain a cycle");
+  return WD_OK;
+}
+
+wd_status prepare(const wd_graph_desc* d, Prepared& p, uint64_t* Ae_out, uint64_t* Ax_out) {
+  wd_status st = validate(d);
+  if (st != WD_OK) return st;
+  const int64_t S = d->num_states, A = d->num_arcs;
+  std::vector<uint32_t> level;
+  st = eps_levels(d, level);
+  if (st != WD_OK) return st;
+  p.sclass.assign((size_t)S, (uint8_t)kNoEps);
+  std::vector<uint32_t> count(kMaxLevels + 1, 0);
+  uint32_t maxcls = 0;
+  bool any_eps = false;
+  uint64_t Ae = 0, Ax = 0;
+  p.off.resize((size_t)S + 1);
+  for (int64_t s = 0; s < S; ++s) {
+    p.off[s] = make_uint2((uint32_t)Ae, (uint32_t)Ax);
+    uint32_t ne = 0, nx = 0;
+    for (uint32_t a = d->row_ptr[s]; a < d->row_ptr[s + 1]; ++a) (d->ilabel[a] ? ne : nx)++;
+    Ae += ne;
+    Ax += nx;
+    if (nx) {
+      if (level[s] >= (uint32_t)kMaxLevels)
+        return fail(WD_EINVAL, "graph: epsilon chains deeper than " + std::to_string(kMaxLevels));
+      p.sclass[s] = (uint8_t)level[s];
+      count[level[s]]++;
+      maxcls = level[s] > maxcls ? level[s] : maxcls;
+      any_eps = true;
+    }
+  }
+  p.off[S] = make_uint2((uint32_t)Ae, (uint32_t)Ax);
+  p.nlevels = any_eps ? maxcls + 1 : 0;
+  p.level_base.assign(p.nlevels + 1, 0);
+  for (uint32_t l = 0; l < p.nlevels; ++l) p.level_base[l + 1] = p.level_base[l] + count[l];
+  p.earc.resize(Ae);
+  p.xarc.resize(Ax);
+  uint64_t ie = 0, ix = 0;
+  for (int64_t s = 0; s < S; ++s)
+    for (uint32_t a = d->row_ptr[s]; a < d->row_ptr[s + 1]; ++a) {
+      const uint32_t v = d->dst[a];
+      uint32_t wbits;
+      std::memcpy(&wbits, &d->weight[a], 4);
+      if (d->ilabel[a])
+        p.earc[ie++] = make_uint4(v, wbits, (uint32_t)d->ilabel[a] | ((uint32_t)p.sclass[v] << 24), a);
+      else
+        p.xarc[ix++] = make_uint4(v, wbits, p.sclass[v], a);
+    }
+  (void)A;
+  *Ae_out = Ae;
+  *Ax_out = Ax;
+  return WD_OK;
+}
+
+}  // namespace
+
+}  // namespace wd
+
+using namespace wd;
+
+extern "C" wd_status wd_graph_bytes(const wd_graph_desc* d, size_t* bytes) {
+  if (!bytes) return fail(WD_EINVAL, "graph_bytes: null output");
+  Prepared p;
+  uint64_t Ae, Ax;
+  wd_status st = prepare(d, p, &Ae, &Ax);
+  if (st != WD_OK) return st;
+  *bytes = layout(d->num_states, d->num_arcs, Ae, Ax, p.nlevels, d->final_weight != nullptr).total;
+  return WD_OK;
+}
+
+extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t dev_bytes, void* stream,
+                                   wd_graph** out) {
+  if (!out) return fail(WD_EINVAL, "graph_load: null output");
+  *out = nullptr;
+  if (!dev_buf || ((uintptr_t)dev_buf & 255u)) return fail(WD_EINVAL, "graph_load: dev_buf must be 256-byte aligned");
+  Prepared p;
+  uint64_t Ae, Ax;
+  wd_status st = prepare(d, p, &Ae, &Ax);
+  if (st != WD_OK) return st;
+  const int64_t S = d->num_states, A = d->num_arcs;
+  const bool finals = d->final_weight != nullptr;
+  const Layout l = layout(S, A, Ae, Ax, p.nlevels, finals);
+  if (dev_bytes < l.total) return fail(WD_EINVAL, "graph_load: dev_buf smaller than wd_graph_bytes");
+  hipStream_t s = (hipStream_t)stream;
+  char* base = (char*)dev_buf;
+  auto put = [&](uint64_t at, const void* src, uint64_t bytes) -> wd_status {
+    if (!bytes) return WD_OK;
+    return hip_check(hipMemcpyAsync(base + at, src, bytes, hipMemcpyHostToDevice, s), "graph upload");
+  };
+  if ((st = put(l.off, p.off.data(), sizeof(uint2) * (S + 1))) ||
+      (st = put(l.earc, p.earc.data(), sizeof(uint4) * Ae)) ||
+      (st = put(l.xarc, p.xarc.data(), sizeof(uint4) * Ax)) ||
+      (st = put(l.sclass, p.sclass.data(), (uint64_t)S)) ||
+      (finals && (st = put(l.final_w, d->final_weight, sizeof(float) * S))) ||
+      (st = put(l.ilabel, d->ilabel, sizeof(int32_t) * A)) ||
+      (st = put(l.olabel, d->olabel, sizeof(int32_t) * A)) ||
+      (st = put(l.weight, d->weight, sizeof(float) * A)) ||
+      (st = put(l.level_base, p.level_base.data(), sizeof(uint32_t) * (p.nlevels + 1))))
+    return st;
+  if ((st = hip_check(hipStreamSynchronize(s), "graph upload sync"))) return st;
+  wd_graph* g = new wd_graph();
+  g->S = (int32_t)S;
+  g->A = A;
+  g->Ae = Ae;
+  g->Ax = Ax;
+  g->nlevels = p.nlevels;
+  g->P = (uint32_t)d->num_pdfs;
+  g->level_base = p.level_base;
+  g->bytes = l.total;
+  DevGraph& dg = g->dg;
+  dg.off = (const uint2*)(base + l.off);
+  dg.earc = (const uint4*)(base + l.earc);
+  dg.xarc = (const uint4*)(base + l.xarc);
+  dg.sclass = (const uint8_t*)(base + l.sclass);
+  dg.final_w = finals ? (const float*)(base + l.final_w) : nullptr;
+  dg.ilabel_id = (const int32_t*)(base + l.ilabel);
+  dg.olabel_id = (const int32_t*)(base + l.olabel);
+  dg.weight_id = (const float*)(base + l.weight);
+  dg.level_base = (const uint32_t*)(base + l.level_base);
+  dg.S = (uint32_t)S;
+  dg.start = (uint32_t)d->start_state;
+  dg.nlevels = p.nlevels;
+  dg.P = (uint32_t)d->num_pdfs;
+  dg.Ae = Ae;
+  dg.Ax = Ax;
+  dg.A = (uint64_t)A;
+  *out = g;
+  return WD_OK;
+}
+
+extern "C" void wd_graph_free(wd_graph* g) { delete g; }
+
+extern "C" int32_t wd_graph_eps_levels(const wd_graph* g) { return g ? (int32_t)g->nlevels : 0; }

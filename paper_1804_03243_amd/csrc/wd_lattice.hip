@@ -1,0 +1,394 @@
+// Lattice pass for one utterance per workgroup, after the forward pass.
+//
+// Final costs and the best end token; lattice pruning (Sec. 3.5): the extra
+// cost of a node is the best complete path through it minus the best overall,
+// of a link extra(dst) + (x - cost(dst)); nodes are updated with atomic
+// minima on order-preserving keys, sweeping frames from the last one back (links
+// only run from frame t to t or t+1) and, inside a frame, epsilon links from the
+// highest source level down, so every value is final when it is read.  The
+// 1-best path is traced back during the same sweep.  Then fp64 forward-backward
+// posteriors over the kept links (Sec. 4.1 uses lattice posteriors) and the
+// final merge of the kept links (Sec. 3.5) in (t, arc id) order.
+#include "wd_block.h"
+
+namespace wd {
+
+struct LatShared {
+  BlockScratch bs;
+  unsigned long long nw;   // traceback words collected (thread 0 writes)
+  uint32_t tb_ok;
+};
+
+__device__ __forceinline__ uint64_t search_le64(const uint64_t* a, uint64_t n, uint64_t w) {
+  uint64_t lo = 0, hi = n;
+  while (hi - lo > 1) {
+    uint64_t mid = (lo + hi) >> 1;
+    if (a[mid] <= w) lo = mid;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Number of entries of the sorted a[0..n) below w.
+__device__ __forceinline__ uint64_t lower_bound64(const uint64_t* a, uint64_t n, uint64_t w) {
+  uint64_t lo = 0, hi = n;
+  while (lo < hi) {
+    uint64_t mid = (lo + hi) >> 1;
+    if (a[mid] < w) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// -log(exp(-a) + exp(-b)) accumulated atomically into *p (fp64).
+__device__ __forceinline__ void atomic_logadd(double* p, double v) {
+  if (!(v < INFINITY)) return;
+  unsigned long long* a = reinterpret_cast<unsigned long long*>(p);
+  unsigned long long old = *a;
+  while (true) {
+    const double o = __longlong_as_double((long long)old);
+    double n;
+    if (!(o < INFINITY)) n = v;
+    else n = fmin(o, v) - log1p(exp(-fabs(o - v)));
+    const unsigned long long prev = atomicCAS(a, old, (unsigned long long)__double_as_longlong(n));
+    if (prev == old) break;
+    old = prev;
+  }
+}
+
+__device__ __forceinline__ float node_cost(const LaneDesc& L, uint64_t n) {
+  return key_cost((uint32_t)(L.n_pack[n] >> 32));
+}
+
+struct LinkView {
+  uint32_t arc, src, dst;
+  float x;
+};
+__device__ __forceinline__ LinkView link_at(const LaneDesc& L, uint64_t k) {
+  const uint4 v = L.links[k];
+  return LinkView{v.x, v.y, v.z, __uint_as_float(v.w)};
+}
+
+// Extra cost of link k from the (final) extra cost of its destination.
+__device__ __forceinline__ uint32_t relax_link(const LaneDesc& L, uint64_t k) {
+  const LinkView l = link_at(L, k);
+  const float exd = key_cost(L.extra_key[l.dst]);
+  const float d = l.x - node_cost(L, l.dst);
+  const uint32_t le = cost_key(exd + d);
+  L.le_key[k] = le;
+  atomicMin(&L.extra_key[l.src], le);
+  return le;
+}
+
+__device__ __forceinline__ bool kept(const LaneDesc& L, uint64_t k, uint32_t lb_key) {
+  const uint32_t le = L.le_key[k];
+  return le <= lb_key && le < kInfKey;
+}
+
+__device__ __forceinline__ double link_ac(const LaneDesc& L, const DevGraph& g, int t, uint32_t arc) {
+  const int32_t il = g.ilabel_id[arc];
+  return il ? -(double)L.ll[(size_t)(t - 1) * g.P + (il - 1)] : 0.0;
+}
+
+// Write the selected links (all links, or the kept ones listed in kept_idx)
+// in (t, arc id) order.  Each frame holds an emitting run then an epsilon run,
+// each already ascending in arc id; a link's slot is its rank in its own run
+// plus the number of links of the other run with a smaller arc id.
+__device__ void assemble(const LaneDesc& L, const DevGraph& g, bool all, uint64_t n_sel,
+                         OutLink* out, uint32_t lb_key, double Z, bool with_post, bool mark_nodes) {
+  const int T = L.T;
+  const uint64_t* kid = L.kept_idx;
+  auto sel = [&](uint64_t j) -> uint64_t { return all ? j : kid[j]; };
+  auto below = [&](uint64_t k) -> uint64_t { return all ? k : lower_bound64(kid, n_sel, k); };
+  for (uint64_t j = threadIdx.x; j < n_sel; j += kThreads) {
+    const uint64_t k = sel(j);
+    const int t = (int)search_le64(L.link_off, (uint64_t)T + 2, k);
+    const uint64_t xo = L.link_xoff[t];
+    const bool eps = k >= xo;
+    const uint64_t s0 = below(L.link_off[t]);
+    const uint64_t sx = below(xo);
+    const uint64_t s1 = below(L.link_off[t + 1]);
+    const LinkView l = link_at(L, k);
+    // the other run [o0, o1) in selection order
+    const uint64_t o0 = eps ? s0 : sx, o1 = eps ? sx : s1;
+    uint64_t lo = o0, hi = o1;
+    while (lo < hi) {
+      const uint64_t mid = (lo + hi) >> 1;
+      if (L.links[sel(mid)].x < l.arc) lo = mid + 1;
+      else hi = mid;
+    }
+    const uint64_t rank = eps ? j - sx : j - s0;
+    const uint64_t pos = s0 + rank + (lo - o0);
+    if (pos >= n_sel) continue;  // cannot happen for consistent runs
+    OutLink o;
+    o.t = t;
+    o.arc_id = l.arc;
+    o.src_state = (int32_t)L.n_state[l.src];
+    o.dst_state = (int32_t)L.n_state[l.dst];
+    o.ilabel = g.ilabel_id[l.arc];
+    o.olabel = g.olabel_id[l.arc];
+    o.graph_cost = g.weight_id[l.arc];
+    const double ac = link_ac(L, g, t, l.arc);
+    o.ac_cost = (float)ac;
+    o.fwd_cost = l.x;
+    o.extra = key_cost(L.le_key[k]);
+    o.posterior = 0.0;
+    if (with_post && kept(L, k, lb_key))
+      o.posterior = exp(Z - L.alpha[l.src] - (double)o.graph_cost - ac - L.beta[l.dst]);
+    out[pos] = o;
+    if (mark_nodes) {
+      atomicOr(&L.used[l.src >> 5], 1u << (l.src & 31u));
+      atomicOr(&L.used[l.dst >> 5], 1u << (l.dst & 31u));
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                      Params prm) {
+  __shared__ LatShared sh;
+  const LaneDesc& L = lanes[blockIdx.x];
+  LaneInfo* info = L.info;
+  if (info->status != 0) return;
+  const uint32_t tid = threadIdx.x;
+  const int T = L.T;
+  const uint64_t nT0 = L.node_off[T], nT1 = L.node_off[T + 1];
+  const uint64_t nnodes = nT1;
+  const uint64_t nlinks = L.link_off[T + 1];
+
+  // ------------------------------------------------ final costs, best end token
+  uint32_t any = 0;
+  if (g.final_w)
+    for (uint64_t n = nT0 + tid; n < nT1; n += kThreads) {
+      const float fw = g.final_w[L.n_state[n]];
+      const float c = node_cost(L, n);
+      any |= (fw < INFINITY && (c + fw) < INFINITY) ? 1u : 0u;
+    }
+  const bool final_used = block_or(any, sh.bs) != 0;
+  uint64_t m = kEmpty;
+  for (uint64_t n = nT0 + tid; n < nT1; n += kThreads) {
+    const float c = node_cost(L, n);
+    const float F = final_used ? canon(c + g.final_w[L.n_state[n]]) : c;
+    const uint64_t v = pack_tok(cost_key(F), (uint32_t)(n - nT0));
+    m = v < m ? v : m;
+  }
+  m = block_min64(m, sh.bs);
+  const uint32_t best_key = (uint32_t)(m >> 32);
+  if (best_key >= kInfKey) {
+    if (tid == 0) info->status = 3;
+    return;
+  }
+  const float best_total = key_cost(best_key);
+  const uint64_t bnode = nT0 + (m & 0xffffffffu);
+
+  // ------------------------------------- backward sweep: extra costs + traceback
+  uint64_t tb = bnode;   // traceback position (thread 0)
+  uint64_t nw = 0;
+  bool tb_ok = true;
+  if (tid == 0) {
+    sh.nw = 0;
+    sh.tb_ok = 1;
+  }
+  for (int t = T; t >= 0; --t) {
+    const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
+    for (uint64_t n = n0 + tid; n < n1; n += kThreads) {
+      uint32_t ex = kInfKey;
+      if (t == T) {
+        const float c = node_cost(L, n);
+        const float F = final_used ? canon(c + g.final_w[L.n_state[n]]) : c;
+        if (F < INFINITY) ex = cost_key(F - best_total);
+      }
+      L.extra_key[n] = ex;
+    }
+    if (tid == 0 && tb_ok) {
+      // follow epsilon predecessors inside frame t, then one emitting arc back
+      for (uint32_t steps = 0;; ++steps) {
+        if (tb < n0 || tb >= n1 || steps > g.nlevels) {
+          tb_ok = false;
+          break;
+        }
+        const uint32_t arc = (uint32_t)L.n_pack[tb];
+        if (arc == kNoArc) break;
+        if (arc >= g.A) {
+          tb_ok = false;
+          break;
+        }
+        const int32_t ol = g.olabel_id[arc];
+        if (ol != 0) {
+          if (nw < L.word_cap) L.out_words[nw] = ol;
+          else tb_ok = false;
+          ++nw;
+        }
+        tb = L.n_pred[tb];
+        if (g.ilabel_id[arc] != 0) break;
+      }
+    }
+    __syncthreads();
+    if (t < T) {
+      const uint64_t k0 = L.link_off[t + 1], k1 = L.link_xoff[t + 1];
+      for (uint64_t k = k0 + tid; k < k1; k += kThreads) relax_link(L, k);
+      __syncthreads();
+    }
+    const uint64_t x0 = L.link_xoff[t], x1 = L.link_off[t + 1];
+    if (x1 > x0)
+      for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
+        for (uint64_t k = x0 + tid; k < x1; k += kThreads)
+          if (L.link_lvl[k] == (uint8_t)lvl) relax_link(L, k);
+        __syncthreads();
+      }
+  }
+
+  // ----------------------------------------------------- posteriors (fp64)
+  const uint32_t lb_key = cost_key(prm.lattice_beam);
+  uint64_t start_node = 0;
+  {
+    // the start state among frame 0's tokens (sorted by state)
+    uint64_t lo = 0, hi = L.node_off[1];
+    while (lo < hi) {
+      const uint64_t mid = (lo + hi) >> 1;
+      if (L.n_state[mid] < g.start) lo = mid + 1;
+      else hi = mid;
+    }
+    start_node = lo;
+  }
+  for (int t = 0; t <= T; ++t) {
+    const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
+    for (uint64_t n = n0 + tid; n < n1; n += kThreads) L.alpha[n] = (n == start_node) ? 0.0 : INFINITY;
+    __syncthreads();
+    if (t > 0) {
+      const uint64_t k0 = L.link_off[t], k1 = L.link_xoff[t];
+      for (uint64_t k = k0 + tid; k < k1; k += kThreads) {
+        if (!kept(L, k, lb_key)) continue;
+        const LinkView l = link_at(L, k);
+        atomic_logadd(&L.alpha[l.dst], L.alpha[l.src] + (double)g.weight_id[l.arc] + link_ac(L, g, t, l.arc));
+      }
+      __syncthreads();
+    }
+    const uint64_t x0 = L.link_xoff[t], x1 = L.link_off[t + 1];
+    if (x1 > x0)
+      for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
+        for (uint64_t k = x0 + tid; k < x1; k += kThreads) {
+          if (L.link_lvl[k] != (uint8_t)lvl || !kept(L, k, lb_key)) continue;
+          const LinkView l = link_at(L, k);
+          atomic_logadd(&L.alpha[l.dst], L.alpha[l.src] + (double)g.weight_id[l.arc]);
+        }
+        __syncthreads();
+      }
+  }
+  for (int t = T; t >= 0; --t) {
+    const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
+    for (uint64_t n = n0 + tid; n < n1; n += kThreads) {
+      double b = INFINITY;
+      if (t == T) b = final_used ? (double)g.final_w[L.n_state[n]] : 0.0;
+      L.beta[n] = b;
+    }
+    __syncthreads();
+    if (t < T) {
+      const uint64_t k0 = L.link_off[t + 1], k1 = L.link_xoff[t + 1];
+      for (uint64_t k = k0 + tid; k < k1; k += kThreads) {
+        if (!kept(L, k, lb_key)) continue;
+        const LinkView l = link_at(L, k);
+        atomic_logadd(&L.beta[l.src], (double)g.weight_id[l.arc] + link_ac(L, g, t + 1, l.arc) + L.beta[l.dst]);
+      }
+      __syncthreads();
+    }
+    const uint64_t x0 = L.link_xoff[t], x1 = L.link_off[t + 1];
+    if (x1 > x0)
+      for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
+        for (uint64_t k = x0 + tid; k < x1; k += kThreads) {
+          if (L.link_lvl[k] != (uint8_t)lvl || !kept(L, k, lb_key)) continue;
+          const LinkView l = link_at(L, k);
+          atomic_logadd(&L.beta[l.src], (double)g.weight_id[l.arc] + L.beta[l.dst]);
+        }
+        __syncthreads();
+      }
+  }
+  const double Z = L.beta[start_node];
+  if (tid == 0) {
+    sh.nw = nw;
+    sh.tb_ok = tb_ok ? 1u : 0u;
+  }
+  __syncthreads();
+  nw = sh.nw;
+  tb_ok = sh.tb_ok != 0;
+
+  // ------------------------------------------- final merge of the kept links
+  uint64_t n_kept;
+  {
+    const uint64_t per = (nlinks + kThreads - 1) / kThreads;
+    const uint64_t k0 = tid * per < nlinks ? tid * per : nlinks;
+    const uint64_t k1 = k0 + per < nlinks ? k0 + per : nlinks;
+    uint64_t cnt = 0;
+    for (uint64_t k = k0; k < k1; ++k) cnt += kept(L, k, lb_key);
+    uint64_t pos = block_excl_scan64(cnt, sh.bs, &n_kept);
+    if (n_kept <= L.kept_cap)
+      for (uint64_t k = k0; k < k1; ++k)
+        if (kept(L, k, lb_key)) L.kept_idx[pos++] = k;
+  }
+  __syncthreads();
+  const bool debug = (prm.flags & 1u) != 0;
+  if (n_kept > L.kept_cap || (debug && nlinks > L.raw_cap)) {
+    if (tid == 0) {
+      info->status = 4;
+      info->overflow |= kOvfKept;
+      info->kept = n_kept;
+    }
+    return;
+  }
+  if (!tb_ok) {
+    if (tid == 0) info->status = kStatusInternal;
+    return;
+  }
+  // used-node bitmap is zero on entry (cleared by the host before the launch)
+  if (tid == 0) atomicOr(&L.used[start_node >> 5], 1u << (start_node & 31u));
+  assemble(L, g, false, n_kept, L.out_links, lb_key, Z, true, true);
+  if (debug) assemble(L, g, true, nlinks, L.out_raw, lb_key, Z, true, false);
+  __syncthreads();
+  // lattice nodes in (t, state) order = node id order
+  uint64_t n_out;
+  {
+    const uint64_t nwd = (nnodes + 31) >> 5;
+    const uint64_t per = (nwd + kThreads - 1) / kThreads;
+    const uint64_t w0 = tid * per < nwd ? tid * per : nwd;
+    const uint64_t w1 = w0 + per < nwd ? w0 + per : nwd;
+    uint64_t cnt = 0;
+    for (uint64_t w = w0; w < w1; ++w) cnt += (uint64_t)__popc(L.used[w]);
+    uint64_t pos = block_excl_scan64(cnt, sh.bs, &n_out);
+    for (uint64_t w = w0; w < w1; ++w) {
+      uint32_t word = L.used[w];
+      while (word) {
+        const uint32_t b = (uint32_t)__ffs(word) - 1u;
+        word &= word - 1u;
+        const uint64_t n = (w << 5) | b;
+        OutNode o;
+        o.t = (int32_t)search_le64(L.node_off, (uint64_t)T + 2, n);
+        o.state = (int32_t)L.n_state[n];
+        o.cost = node_cost(L, n);
+        o.extra = key_cost(L.extra_key[n]);
+        L.out_nodes[pos++] = o;
+      }
+    }
+  }
+  __syncthreads();
+  // words were collected last-first
+  for (uint64_t i = tid; i < nw / 2; i += kThreads) {
+    const int32_t a = L.out_words[i];
+    L.out_words[i] = L.out_words[nw - 1 - i];
+    L.out_words[nw - 1 - i] = a;
+  }
+  if (tid == 0) {
+    info->final_used = final_used ? 1 : 0;
+    info->kept = n_kept;
+    info->out_nodes = n_out;
+    info->nwords = nw;
+    info->out_raw = debug ? nlinks : 0;
+    info->start_node = (uint32_t)start_node;
+    info->best_node = (uint32_t)bnode;
+    info->best_cost = best_total;
+  }
+}
+
+void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s) {
+  hipLaunchKernelGGL(k_lattice, dim3(B), dim3(kThreads), 0, s, g, lanes, prm);
+}
+
+}  // namespace wd

@@ -1,0 +1,337 @@
+"""ctypes binding of libwfstdec.so (include/wfstdec.h).
+
+The functions named wd_* mirror the C ABI one to one and only marshal
+arguments.  Graph, decode() and decode_batch() add the bookkeeping a Python
+caller needs: device buffers come from torch (torch is used for device memory
+and streams only), and a decode that reports WD_ECAPACITY is retried once with
+the capacities it reported as needed.  Every step of the decoder runs in the
+library's HIP kernels; if the library is missing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from types import SimpleNamespace
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libwfstdec.so")
+
+WD_OK, WD_EINVAL, WD_ECYCLE, WD_ENOPATH, WD_ECAPACITY, WD_EDEVICE = range(6)
+WD_FLAG_DEBUG = 1
+WD_FLAG_TIMING = 2
+STATUS_NAMES = {0: "WD_OK", 1: "WD_EINVAL", 2: "WD_ECYCLE", 3: "WD_ENOPATH", 4: "WD_ECAPACITY",
+                5: "WD_EDEVICE"}
+
+LINK_DTYPE = np.dtype([("t", "<i4"), ("arc_id", "<u4"), ("src_state", "<i4"), ("dst_state", "<i4"),
+                       ("ilabel", "<i4"), ("olabel", "<i4"), ("graph_cost", "<f4"),
+                       ("ac_cost", "<f4"), ("fwd_cost", "<f4"), ("extra", "<f4"),
+                       ("posterior", "<f8")], align=True)
+NODE_DTYPE = np.dtype([("t", "<i4"), ("state", "<i4"), ("cost", "<f4"), ("extra", "<f4")], align=True)
+TOKEN_DTYPE = np.dtype([("t", "<i4"), ("state", "<i4"), ("cost", "<f4"), ("pred_arc", "<u4")],
+                       align=True)
+
+
+class WdError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class wd_graph_desc(ctypes.Structure):
+    _fields_ = [("num_states", ctypes.c_int32), ("num_arcs", ctypes.c_int64),
+                ("start_state", ctypes.c_int32), ("row_ptr", ctypes.c_void_p),
+                ("dst", ctypes.c_void_p), ("ilabel", ctypes.c_void_p), ("olabel", ctypes.c_void_p),
+                ("weight", ctypes.c_void_p), ("final_weight", ctypes.c_void_p),
+                ("num_pdfs", ctypes.c_int32)]
+
+
+class wd_params(ctypes.Structure):
+    _fields_ = [("beam", ctypes.c_float), ("max_active", ctypes.c_int32),
+                ("lattice_beam", ctypes.c_float), ("flags", ctypes.c_uint32)]
+
+
+class wd_caps(ctypes.Structure):
+    _fields_ = [("frame_tokens", ctypes.c_int64), ("frame_arcs", ctypes.c_int64),
+                ("nodes", ctypes.c_int64), ("links", ctypes.c_int64), ("kept_links", ctypes.c_int64)]
+
+
+class wd_stats(ctypes.Structure):
+    _fields_ = [("frames", ctypes.c_int32), ("final_reached", ctypes.c_int32),
+                ("arcs_expanded", ctypes.c_int64), ("tokens", ctypes.c_int64),
+                ("max_tokens", ctypes.c_int64), ("raw_links", ctypes.c_int64),
+                ("kept_links", ctypes.c_int64), ("nodes", ctypes.c_int64),
+                ("eps_arcs_expanded", ctypes.c_int64), ("forward_ms", ctypes.c_float),
+                ("lattice_ms", ctypes.c_float), ("needed", wd_caps)]
+
+
+EXPORTS = ["wd_graph_bytes", "wd_graph_load", "wd_graph_free", "wd_graph_eps_levels",
+           "wd_workspace_bytes", "wd_decode", "wd_decode_batch", "wd_result_status",
+           "wd_result_cost", "wd_result_words", "wd_result_lattice", "wd_result_nodes",
+           "wd_result_tokens", "wd_result_raw_lattice", "wd_result_cutoffs", "wd_result_stats",
+           "wd_result_free", "wd_last_error"]
+
+_LIB = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -c 'import __graft_entry__ as g; g.build()'`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, VP = ctypes.POINTER, ctypes.c_void_p
+        sig = {
+            "wd_graph_bytes": ([P(wd_graph_desc), P(ctypes.c_size_t)], ctypes.c_int),
+            "wd_graph_load": ([P(wd_graph_desc), VP, ctypes.c_size_t, VP, P(VP)], ctypes.c_int),
+            "wd_graph_free": ([VP], None),
+            "wd_graph_eps_levels": ([VP], ctypes.c_int32),
+            "wd_workspace_bytes": ([VP, ctypes.c_int32, ctypes.c_int32, P(wd_params), P(wd_caps),
+                                    P(ctypes.c_size_t), P(wd_caps)], ctypes.c_int),
+            "wd_decode": ([VP, VP, ctypes.c_int32, P(wd_params), P(wd_caps), VP, ctypes.c_size_t, VP,
+                           P(VP)], ctypes.c_int),
+            "wd_decode_batch": ([VP, ctypes.c_int32, P(VP), P(ctypes.c_int32), P(wd_params),
+                                 P(wd_caps), VP, ctypes.c_size_t, VP, P(VP)], ctypes.c_int),
+            "wd_result_status": ([VP], ctypes.c_int),
+            "wd_result_cost": ([VP], ctypes.c_float),
+            "wd_result_words": ([VP, P(VP)], ctypes.c_int32),
+            "wd_result_lattice": ([VP, P(VP)], ctypes.c_int64),
+            "wd_result_nodes": ([VP, P(VP)], ctypes.c_int64),
+            "wd_result_tokens": ([VP, P(VP)], ctypes.c_int64),
+            "wd_result_raw_lattice": ([VP, P(VP)], ctypes.c_int64),
+            "wd_result_cutoffs": ([VP, P(VP), P(VP), P(VP)], ctypes.c_int32),
+            "wd_result_stats": ([VP, P(wd_stats)], None),
+            "wd_result_free": ([VP], None),
+            "wd_last_error": ([], ctypes.c_char_p),
+        }
+        for name, (args, res) in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _LIB = L
+    return _LIB
+
+
+def _check(st: int):
+    if st != WD_OK:
+        raise WdError(st, lib().wd_last_error().decode())
+
+
+# ------------------------------------------------------------ one-to-one ABI
+
+def wd_graph_bytes(desc: wd_graph_desc) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().wd_graph_bytes(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def wd_graph_load(desc: wd_graph_desc, dev_buf: int, dev_bytes: int, stream: int) -> int:
+    h = ctypes.c_void_p()
+    _check(lib().wd_graph_load(ctypes.byref(desc), dev_buf, dev_bytes, stream, ctypes.byref(h)))
+    return h.value
+
+
+def wd_graph_free(handle: int) -> None:
+    lib().wd_graph_free(handle)
+
+
+def wd_graph_eps_levels(handle: int) -> int:
+    return lib().wd_graph_eps_levels(handle)
+
+
+def wd_workspace_bytes(handle: int, lanes: int, max_T: int, params: wd_params,
+                       caps: wd_caps | None = None) -> tuple[int, wd_caps]:
+    n = ctypes.c_size_t()
+    out = wd_caps()
+    _check(lib().wd_workspace_bytes(handle, lanes, max_T, ctypes.byref(params),
+                                    ctypes.byref(caps) if caps is not None else None,
+                                    ctypes.byref(n), ctypes.byref(out)))
+    return n.value, out
+
+
+def wd_decode(handle: int, loglikes_ptr: int, T: int, params: wd_params, caps: wd_caps | None,
+              ws: int, ws_bytes: int, stream: int) -> tuple[int, int]:
+    """Returns (status, result handle or 0)."""
+    r = ctypes.c_void_p()
+    st = lib().wd_decode(handle, loglikes_ptr, T, ctypes.byref(params),
+                         ctypes.byref(caps) if caps is not None else None, ws, ws_bytes, stream,
+                         ctypes.byref(r))
+    return st, r.value or 0
+
+
+def wd_decode_batch(handle: int, loglikes_ptrs: list[int], Ts: list[int], params: wd_params,
+                    caps: wd_caps | None, ws: int, ws_bytes: int, stream: int) -> tuple[int, list[int]]:
+    B = len(Ts)
+    ptrs = (ctypes.c_void_p * B)(*loglikes_ptrs)
+    ts = (ctypes.c_int32 * B)(*Ts)
+    outs = (ctypes.c_void_p * B)()
+    st = lib().wd_decode_batch(handle, B, ptrs, ts, ctypes.byref(params),
+                               ctypes.byref(caps) if caps is not None else None, ws, ws_bytes, stream,
+                               outs)
+    return st, [o or 0 for o in outs]
+
+
+def _copy(ptr, n, dtype):
+    if n <= 0 or not ptr:
+        return np.zeros(0, dtype=dtype)
+    buf = (ctypes.c_char * (int(n) * dtype.itemsize)).from_address(ptr)
+    return np.frombuffer(bytes(buf), dtype=dtype).copy()
+
+
+def wd_result_read(r: int) -> SimpleNamespace:
+    """Copy everything out of a result handle (wd_result_* accessors)."""
+    L = lib()
+    out = SimpleNamespace()
+    out.status = L.wd_result_status(r)
+    out.cost = np.float32(L.wd_result_cost(r))
+    def get(accessor, dtype):
+        vp = ctypes.c_void_p()
+        n = accessor(r, ctypes.byref(vp))   # sets vp; read it only afterwards
+        return _copy(vp.value, n, dtype)
+
+    out.words = get(L.wd_result_words, np.dtype("<i4"))
+    out.links = get(L.wd_result_lattice, LINK_DTYPE)
+    out.nodes = get(L.wd_result_nodes, NODE_DTYPE)
+    out.tokens = get(L.wd_result_tokens, TOKEN_DTYPE)
+    out.raw_links = get(L.wd_result_raw_lattice, LINK_DTYPE)
+    b, cb, c = ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_void_p()
+    n = L.wd_result_cutoffs(r, ctypes.byref(b), ctypes.byref(cb), ctypes.byref(c))
+    f4 = np.dtype("<f4")
+    out.best, out.cutoff_beam, out.cutoff = (_copy(b.value, n, f4), _copy(cb.value, n, f4),
+                                             _copy(c.value, n, f4))
+    st = wd_stats()
+    L.wd_result_stats(r, ctypes.byref(st))
+    out.stats = {f: getattr(st, f) for f, _ in wd_stats._fields_ if f != "needed"}
+    out.needed = {f: getattr(st.needed, f) for f, _ in wd_caps._fields_}
+    return out
+
+
+def wd_result_free(r: int) -> None:
+    lib().wd_result_free(r)
+
+
+# ---------------------------------------------------------------- helpers
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        raise RuntimeError("wfstdec needs a GPU (torch.cuda.is_available() is False)")
+    return torch
+
+
+def _stream(torch):
+    return torch.cuda.current_stream().cuda_stream
+
+
+class Graph:
+    """A decoding graph resident in GPU memory (buffer owned by a torch tensor)."""
+
+    def __init__(self, g: dict, num_pdfs: int, device: str = "cuda:0"):
+        torch = _torch()
+        self._arrs = dict(row_ptr=np.ascontiguousarray(g["row_ptr"], dtype=np.uint32),
+                          dst=np.ascontiguousarray(g["dst"], dtype=np.uint32),
+                          ilabel=np.ascontiguousarray(g["ilabel"], dtype=np.int32),
+                          olabel=np.ascontiguousarray(g["olabel"], dtype=np.int32),
+                          weight=np.ascontiguousarray(g["weight"], dtype=np.float32))
+        fw = g.get("final_weight")
+        self._fw = None if fw is None else np.ascontiguousarray(fw, dtype=np.float32)
+        a = self._arrs
+        self.desc = wd_graph_desc(int(g["num_states"]), int(a["dst"].size), int(g.get("start_state", 0)),
+                                  a["row_ptr"].ctypes.data, a["dst"].ctypes.data,
+                                  a["ilabel"].ctypes.data, a["olabel"].ctypes.data,
+                                  a["weight"].ctypes.data,
+                                  None if self._fw is None else self._fw.ctypes.data, int(num_pdfs))
+        self.num_pdfs = int(num_pdfs)
+        self.device = torch.device(device)
+        with torch.cuda.device(self.device):
+            nbytes = wd_graph_bytes(self.desc)
+            self.buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
+            base = (self.buf.data_ptr() + 255) // 256 * 256
+            self.handle = wd_graph_load(self.desc, base, nbytes, _stream(torch))
+        self.nbytes = nbytes
+        self.eps_levels = wd_graph_eps_levels(self.handle)
+        self._ws = None
+        self._caps = {}
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h:
+            try:
+                wd_graph_free(h)
+            except Exception:
+                pass
+            self.handle = None
+
+    def workspace(self, lanes: int, max_T: int, params: wd_params, caps: wd_caps | None):
+        """(pointer, bytes) of a workspace large enough; reuses one buffer."""
+        torch = _torch()
+        nbytes, used = wd_workspace_bytes(self.handle, lanes, max_T, params, caps)
+        if self._ws is None or self._ws.numel() < nbytes + 256:
+            self._ws = None
+            self._ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
+        base = (self._ws.data_ptr() + 255) // 256 * 256
+        return base, nbytes, used
+
+
+def _params(beam, max_active, lattice_beam, debug, timing=False):
+    return wd_params(float(beam), int(max_active), float(lattice_beam),
+                     (WD_FLAG_DEBUG if debug else 0) | (WD_FLAG_TIMING if timing else 0))
+
+
+def _grow(caps: wd_caps, needed: dict) -> wd_caps:
+    """Capacities for the next attempt: at least what was needed, and a fast
+    geometric step (an attempt only reveals the first capacity it outgrew)."""
+    c = wd_caps(caps.frame_tokens, caps.frame_arcs, caps.nodes, caps.links, caps.kept_links)
+    for f, _ in wd_caps._fields_:
+        need = needed[f]
+        if need > getattr(c, f):
+            setattr(c, f, int(max(need, 4 * getattr(c, f))))
+    return c
+
+
+def decode_batch(graph: Graph, loglikes: list, beam: float, max_active: int, lattice_beam: float,
+                 debug: bool = False, caps: wd_caps | None = None, max_retries: int = 12,
+                 timing: bool = False):
+    """Decode utterances (device float32 tensors, T_i x P) concurrently.
+    Returns one result namespace per utterance."""
+    torch = _torch()
+    for x in loglikes:
+        if x.dtype != torch.float32 or not x.is_contiguous() or x.device != graph.device:
+            raise ValueError("log-likelihoods must be contiguous float32 tensors on the graph's device")
+        if x.dim() != 2 or x.shape[1] != graph.num_pdfs:
+            raise ValueError(f"log-likelihoods must be T x {graph.num_pdfs}")
+    p = _params(beam, max_active, lattice_beam, debug, timing)
+    Ts = [int(x.shape[0]) for x in loglikes]
+    key = (len(Ts), max(Ts), float(beam), int(max_active), float(lattice_beam), bool(debug))
+    if caps is None:
+        caps = graph._caps.get(key)
+    for attempt in range(max_retries + 1):
+        with torch.cuda.device(graph.device):
+            ws, nbytes, used = graph.workspace(len(Ts), max(Ts), p, caps)
+            st, res = wd_decode_batch(graph.handle, [x.data_ptr() for x in loglikes], Ts, p, used, ws,
+                                      nbytes, _stream(torch))
+        outs = []
+        err = lib().wd_last_error().decode() if st != WD_OK else ""
+        for r in res:
+            outs.append(wd_result_read(r) if r else None)
+            if r:
+                wd_result_free(r)
+        if st == WD_ECAPACITY and attempt < max_retries:
+            need = {f: max(o.needed[f] for o in outs if o is not None) for f, _ in wd_caps._fields_}
+            caps = _grow(used, need)
+            continue
+        if st != WD_OK:
+            raise WdError(st, err)
+        graph._caps[key] = used
+        return outs
+    raise WdError(WD_ECAPACITY, "capacity retries exhausted")
+
+
+def decode(graph: Graph, loglikes, beam: float, max_active: int, lattice_beam: float,
+           debug: bool = False, caps: wd_caps | None = None, timing: bool = False):
+    """Decode one utterance (device float32 tensor, T x P)."""
+    return decode_batch(graph, [loglikes], beam, max_active, lattice_beam, debug, caps,
+                        timing=timing)[0]

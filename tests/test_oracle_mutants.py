@@ -35,7 +35,7 @@ MUTANTS = {
     "posterior_sign": ("post[k] = exp(Z - lse_val(&al[l->src]) - (double)g->weight[l->arc] - ac - lse_val(&be[l->dst]));",
                        "post[k] = exp(Z - lse_val(&al[l->src]) - (double)g->weight[l->arc] + ac - lse_val(&be[l->dst]));"),
     "beam_cutoff_from_zero": ("float cutb = best + d->p.beam;", "float cutb = d->p.beam + 0.0f * best;"),
-    "eps_arcs_not_counted": ("for (int64_t i = 0; i < d->nlist; ++i) d->st.arcs_expanded += eps_deg(g, d->list[i]);", ""),
+    "eps_arcs_not_counted": ("    d->st.arcs_expanded += eps_deg(g, d->list[i]);\n", "\n"),
 }
 
 
