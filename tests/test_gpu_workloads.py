@@ -1,0 +1,71 @@
+"""GPU against the oracle on the full-size workloads: the 30M-state graph,
+the 64-utterance batch on the 5M-state graph (every lane), and the wide-beam
+2M-state graph (a prefix of frames: the oracle needs ~2 s per frame there)."""
+import math
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+import synth
+from gpu_compare import assert_same
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def wf():
+    import torch
+    from paper_1804_03243_amd import wfstdec
+    assert torch.cuda.is_available()
+    wfstdec.lib()
+    return wfstdec
+
+
+def test_lm_30m(wf, oracle_mod):
+    import torch
+    cfg = synth.workload("lm_30m")
+    print("\n[gpu case] lm_30m full (30M states, 80M arcs, 1500 frames)", flush=True)
+    g = synth.make_graph(cfg)
+    L = synth.make_loglikes(cfg)
+    graph = wf.Graph(g, cfg["P"])
+    r = wf.decode(graph, torch.from_numpy(L).to(graph.device), cfg["beam"], cfg["max_active"],
+                  cfg["lattice_beam"])
+    o = oracle_mod.decode(g, L, cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    assert_same(r, o)
+
+
+def test_batch64_hclg_5m(wf, oracle_mod):
+    """All 64 lanes of the batch, each against the oracle on its utterance."""
+    import torch
+    cfg = synth.workload("batch64_hclg_5m")
+    print("\n[gpu case] batch64_hclg_5m (64 utterances, 500-1500 frames)", flush=True)
+    g = synth.make_graph(cfg)
+    Ls = synth.make_batch(cfg)
+    graph = wf.Graph(g, cfg["P"])
+    xs = [torch.from_numpy(x).to(graph.device) for x in Ls]
+    rs = wf.decode_batch(graph, xs, cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    with ThreadPoolExecutor(max_workers=16) as ex:
+        os_ = list(ex.map(lambda x: oracle_mod.decode(g, x, cfg["beam"], cfg["max_active"],
+                                                      cfg["lattice_beam"]), Ls))
+    for i, (r, o) in enumerate(zip(rs, os_)):
+        try:
+            assert_same(r, o)
+        except AssertionError as e:
+            raise AssertionError(f"lane {i} (T={Ls[i].shape[0]}): {e}")
+
+
+@pytest.mark.parametrize("name,T,debug", [("wide_2m", 12, True), ("wide_2m_dyadic", 8, True)])
+def test_wide_2m_prefix(wf, oracle_mod, name, T, debug):
+    """~1M tokens and ~1.5M raw links per frame, epsilon chains of depth 8."""
+    import torch
+    cfg = synth.workload(name)
+    print(f"\n[gpu case] {name} first {T} frames debug={debug}", flush=True)
+    g = synth.make_graph(cfg)
+    L = synth.make_loglikes(cfg)[:T]
+    graph = wf.Graph(g, cfg["P"])
+    r = wf.decode(graph, torch.from_numpy(L).to(graph.device), cfg["beam"], cfg["max_active"],
+                  cfg["lattice_beam"], debug=debug)
+    o = oracle_mod.decode(g, L, cfg["beam"], cfg["max_active"], cfg["lattice_beam"], debug=debug)
+    assert r.stats["max_tokens"] > 100000
+    assert_same(r, o, debug=debug)
