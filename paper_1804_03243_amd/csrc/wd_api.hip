@@ -92,14 +92,14 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
   char* touched = take(4 * c.frame);
   char* surv_state = take(4 * c.frame);
   char* surv_pack = take(8 * c.frame);
-  char* f_state[2], *f_key[2], *f_edeg[2], *f_xdeg[2], *f_cls[2];
-  for (int i = 0; i < 2; ++i) {
-    f_state[i] = take(4 * F1);
-    f_key[i] = take(4 * F1);
-    f_edeg[i] = take(4 * F1);
-    f_xdeg[i] = take(4 * F1);
-    f_cls[i] = take(F1);
-  }
+  char* f_state = take(4 * F1);
+  char* f_key = take(4 * F1);
+  char* f_arc = take(4 * F1);
+  char* f_edeg = take(4 * F1);
+  char* f_xdeg = take(4 * F1);
+  char* f_ebeg = take(4 * F1);
+  char* f_xbeg = take(4 * F1);
+  char* f_cls = take(F1);
   char* cand = take(16 * c.arcs);
   char* n_state = take(4 * c.nodes);
   char* n_pack = take(8 * c.nodes);
@@ -109,6 +109,7 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
   char* node_off = take(8 * T2);
   char* link_off = take(8 * T2);
   char* link_xoff = take(8 * T2);
+  char* xmask = take(4 * T2);
   char* best = take(4 * T2);
   char* cutb = take(4 * T2);
   char* cut = take(4 * T2);
@@ -118,6 +119,7 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
   char* beta = take(8 * c.nodes);
   char* used = take(4 * R.used_words);
   char* kept_idx = take(8 * c.kept);
+  char* kframe = take(16 * T2);
   char* out_links = take(sizeof(OutLink) * c.kept);
   char* out_raw = take(sizeof(OutLink) * c.raw);
   char* out_nodes = take(sizeof(OutNode) * (2 * c.kept + 1));
@@ -144,13 +146,14 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
       L.touched = (uint32_t*)at(touched, 4 * c.frame);
       L.surv_state = (uint32_t*)at(surv_state, 4 * c.frame);
       L.surv_pack = (unsigned long long*)at(surv_pack, 8 * c.frame);
-      for (int i = 0; i < 2; ++i) {
-        L.f_state[i] = (uint32_t*)at(f_state[i], 4 * F1);
-        L.f_key[i] = (uint32_t*)at(f_key[i], 4 * F1);
-        L.f_edeg[i] = (uint32_t*)at(f_edeg[i], 4 * F1);
-        L.f_xdeg[i] = (uint32_t*)at(f_xdeg[i], 4 * F1);
-        L.f_cls[i] = (uint8_t*)at(f_cls[i], F1);
-      }
+      L.f_state = (uint32_t*)at(f_state, 4 * F1);
+      L.f_key = (uint32_t*)at(f_key, 4 * F1);
+      L.f_arc = (uint32_t*)at(f_arc, 4 * F1);
+      L.f_edeg = (uint32_t*)at(f_edeg, 4 * F1);
+      L.f_xdeg = (uint32_t*)at(f_xdeg, 4 * F1);
+      L.f_ebeg = (uint32_t*)at(f_ebeg, 4 * F1);
+      L.f_xbeg = (uint32_t*)at(f_xbeg, 4 * F1);
+      L.f_cls = (uint8_t*)at(f_cls, F1);
       L.cand = (uint4*)at(cand, 16 * c.arcs);
       L.n_state = (uint32_t*)at(n_state, 4 * c.nodes);
       L.n_pack = (unsigned long long*)at(n_pack, 8 * c.nodes);
@@ -160,6 +163,7 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
       L.node_off = (uint64_t*)at(node_off, 8 * T2);
       L.link_off = (uint64_t*)at(link_off, 8 * T2);
       L.link_xoff = (uint64_t*)at(link_xoff, 8 * T2);
+      L.xmask = (uint32_t*)at(xmask, 4 * T2);
       L.best = (float*)at(best, 4 * T2);
       L.cutb = (float*)at(cutb, 4 * T2);
       L.cut = (float*)at(cut, 4 * T2);
@@ -169,6 +173,7 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
       L.beta = (double*)at(beta, 8 * c.nodes);
       L.used = (uint32_t*)at(used, 4 * R.used_words);
       L.kept_idx = (uint64_t*)at(kept_idx, 8 * c.kept);
+      L.kframe = (uint64_t*)at(kframe, 16 * T2);
       L.out_links = (OutLink*)at(out_links, sizeof(OutLink) * c.kept);
       L.out_raw = (OutLink*)at(out_raw, sizeof(OutLink) * c.raw);
       L.out_nodes = (OutNode*)at(out_nodes, sizeof(OutNode) * (2 * c.kept + 1));
@@ -290,7 +295,7 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
   for (int b = 0; b < B; ++b) {
     const LaneInfo& I = info[b];
     const LaneDesc& L = lanes[b];
-    const wd_status ls = (wd_status)I.status;
+    const wd_status ls = (I.status == 0 && I.tb_fail) ? WD_EDEVICE : (wd_status)I.status;
     if (ls != WD_OK && first_bad == WD_OK) first_bad = ls;
     if (ls != WD_OK && ls != WD_ECAPACITY) continue;
     wd_result* r = new wd_result();

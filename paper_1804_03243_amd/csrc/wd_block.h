@@ -43,80 +43,92 @@ __device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int m) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-// Scratch a workgroup needs for its collectives.
+// Scratch a workgroup needs for its collectives.  Two buffers used in turn
+// make each collective cost one barrier: a wave can only come back to a buffer
+// after every wave has passed the barrier of the collective in between, i.e.
+// after every wave has read it.  `par` is per thread, flipped by every
+// collective; all threads call the same sequence of collectives.
 struct BlockScratch {
-  uint32_t w32[kWaves + 1];
-  unsigned long long w64[kWaves + 1];
+  uint32_t w32[2][kWaves];
+  unsigned long long w64[2][kWaves];
 };
 
 // Exclusive prefix sum over the workgroup (thread order); *total = sum.
-__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, BlockScratch& bs, uint32_t* total) {
-  uint32_t inc = wave_incl_scan(v);
-  if (lane_id() == 63) bs.w32[wave_id()] = inc;
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, BlockScratch& bs, uint32_t& par,
+                                                    uint32_t* total) {
+  const uint32_t b = par;
+  par ^= 1u;
+  const uint32_t inc = wave_incl_scan(v);
+  if (lane_id() == 63) bs.w32[b][wave_id()] = inc;
   __syncthreads();
-  if (wave_id() == 0) {
-    uint32_t w = lane_id() < (uint32_t)kWaves ? bs.w32[lane_id()] : 0u;
-    uint32_t wi = wave_incl_scan(w);
-    if (lane_id() < (uint32_t)kWaves) bs.w32[lane_id()] = wi - w;
-    if (lane_id() == (uint32_t)kWaves - 1) bs.w32[kWaves] = wi;
+  uint32_t before = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) {
+    const uint32_t x = bs.w32[b][i];
+    before += (uint32_t)i < wave_id() ? x : 0u;
+    tot += x;
   }
-  __syncthreads();
-  uint32_t r = bs.w32[wave_id()] + inc - v;
-  *total = bs.w32[kWaves];
-  __syncthreads();
-  return r;
+  *total = tot;
+  return before + inc - v;
 }
 
-__device__ __forceinline__ uint64_t block_excl_scan64(uint64_t v, BlockScratch& bs, uint64_t* total) {
-  uint64_t inc = wave_incl_scan64(v);
-  if (lane_id() == 63) bs.w64[wave_id()] = inc;
+__device__ __forceinline__ uint64_t block_excl_scan64(uint64_t v, BlockScratch& bs, uint32_t& par,
+                                                      uint64_t* total) {
+  const uint32_t b = par;
+  par ^= 1u;
+  const uint64_t inc = wave_incl_scan64(v);
+  if (lane_id() == 63) bs.w64[b][wave_id()] = inc;
   __syncthreads();
-  if (wave_id() == 0) {
-    uint64_t w = lane_id() < (uint32_t)kWaves ? bs.w64[lane_id()] : 0ull;
-    uint64_t wi = wave_incl_scan64(w);
-    if (lane_id() < (uint32_t)kWaves) bs.w64[lane_id()] = wi - w;
-    if (lane_id() == (uint32_t)kWaves - 1) bs.w64[kWaves] = wi;
+  uint64_t before = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) {
+    const uint64_t x = bs.w64[b][i];
+    before += (uint32_t)i < wave_id() ? x : 0ull;
+    tot += x;
   }
-  __syncthreads();
-  uint64_t r = bs.w64[wave_id()] + inc - v;
-  *total = bs.w64[kWaves];
-  __syncthreads();
-  return r;
+  *total = tot;
+  return before + inc - v;
 }
 
-__device__ __forceinline__ uint64_t block_min64(uint64_t v, BlockScratch& bs) {
+__device__ __forceinline__ uint64_t block_min64(uint64_t v, BlockScratch& bs, uint32_t& par) {
+  const uint32_t b = par;
+  par ^= 1u;
 #pragma unroll
   for (int m = 32; m > 0; m >>= 1) {
     uint64_t o = shfl_xor64(v, m);
     v = o < v ? o : v;
   }
-  if (lane_id() == 0) bs.w64[wave_id()] = v;
+  if (lane_id() == 0) bs.w64[b][wave_id()] = v;
   __syncthreads();
-  uint64_t r = bs.w64[0];
-  for (int i = 1; i < kWaves; ++i) r = bs.w64[i] < r ? bs.w64[i] : r;
-  __syncthreads();
+  uint64_t r = bs.w64[b][0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) r = bs.w64[b][i] < r ? bs.w64[b][i] : r;
   return r;
 }
 
-__device__ __forceinline__ uint64_t block_sum64(uint64_t v, BlockScratch& bs) {
+__device__ __forceinline__ uint64_t block_sum64(uint64_t v, BlockScratch& bs, uint32_t& par) {
+  const uint32_t b = par;
+  par ^= 1u;
 #pragma unroll
   for (int m = 32; m > 0; m >>= 1) v += shfl_xor64(v, m);
-  if (lane_id() == 0) bs.w64[wave_id()] = v;
+  if (lane_id() == 0) bs.w64[b][wave_id()] = v;
   __syncthreads();
   uint64_t r = 0;
-  for (int i = 0; i < kWaves; ++i) r += bs.w64[i];
-  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) r += bs.w64[b][i];
   return r;
 }
 
-__device__ __forceinline__ uint32_t block_or(uint32_t v, BlockScratch& bs) {
+__device__ __forceinline__ uint32_t block_or(uint32_t v, BlockScratch& bs, uint32_t& par) {
+  const uint32_t b = par;
+  par ^= 1u;
 #pragma unroll
   for (int m = 32; m > 0; m >>= 1) v |= __shfl_xor(v, m, 64);
-  if (lane_id() == 0) bs.w32[wave_id()] = v;
+  if (lane_id() == 0) bs.w32[b][wave_id()] = v;
   __syncthreads();
   uint32_t r = 0;
-  for (int i = 0; i < kWaves; ++i) r |= bs.w32[i];
-  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) r |= bs.w32[b][i];
   return r;
 }
 

@@ -19,6 +19,9 @@ constexpr int kMaxLevels = 254;             // epsilon levels 0..253
 constexpr int kThreads = 1024;              // one workgroup per utterance
 constexpr int kWaves = kThreads / 64;
 constexpr int kRankMax = 2048;              // survivors sorted in LDS up to this many
+constexpr int kHashCap = 4096;              // LDS token table slots (power of two)
+constexpr int kHashMax = 2048;              // LDS token table entries before a frame spills
+constexpr int kFrontCap = 1024;             // frontier tokens held in LDS
 constexpr int kHistBins = 2048;             // 11-bit radix digits for max-active
 constexpr uint32_t kInfKey = 0xff800000u;   // key of +inf
 
@@ -94,7 +97,7 @@ struct LaneInfo {
   uint32_t start_node;
   uint32_t best_node;
   float best_cost;
-  float pad;
+  uint32_t tb_fail;            // traceback met an inconsistent predecessor
 };
 
 enum : uint32_t { kOvfFrame = 1, kOvfArcs = 2, kOvfNodes = 4, kOvfLinks = 8, kOvfKept = 16 };
@@ -138,11 +141,16 @@ struct LaneDesc {
   uint32_t* bucket;            // [S] touched states with epsilon arcs, by level
   uint32_t* surv_state;        // [frame_cap] tokens within the beam cutoff
   unsigned long long* surv_pack;
-  uint32_t* f_state[2];        // frontier (surviving tokens of a frame, sorted by state)
-  uint32_t* f_key[2];
-  uint32_t* f_edeg[2];         // exclusive prefix of emitting out-degree
-  uint32_t* f_xdeg[2];         // exclusive prefix of epsilon out-degree
-  uint8_t* f_cls[2];
+  // frontier: surviving tokens of the last finished frame, sorted by state
+  // (used when a frame has more survivors than the LDS frontier holds)
+  uint32_t* f_state;
+  uint32_t* f_key;             // cost key
+  uint32_t* f_arc;             // predecessor arc
+  uint32_t* f_edeg;            // exclusive prefix of emitting out-degree (+ total)
+  uint32_t* f_xdeg;            // exclusive prefix of epsilon out-degree (+ total)
+  uint32_t* f_ebeg;            // first emitting arc of the state
+  uint32_t* f_xbeg;            // first epsilon arc of the state
+  uint8_t* f_cls;
   uint4* cand;                 // [cand_cap] emitting candidates {arc, src node, dst, x bits}
   // history
   uint32_t* n_state;           // [node_cap]
@@ -153,6 +161,7 @@ struct LaneDesc {
   uint64_t* node_off;          // [T+2]
   uint64_t* link_off;          // [T+2] first link of frame t (emitting run)
   uint64_t* link_xoff;         // [T+2] first epsilon link of frame t
+  uint32_t* xmask;             // [T+2] levels of the epsilon links of frame t (bit 31: 31 or more)
   float* best;                 // [T+1]
   float* cutb;                 // [T+1]
   float* cut;                  // [T+1]
@@ -163,6 +172,7 @@ struct LaneDesc {
   double* beta;                // [node_cap]
   uint32_t* used;              // [ceil(node_cap/32)+1] lattice-node bitmap
   uint64_t* kept_idx;          // [kept_cap] kept link ids in link order
+  uint64_t* kframe;            // [2*(T+2)] per frame: first kept link, first kept epsilon link
   // outputs
   OutLink* out_links;          // [kept_cap]
   OutLink* out_raw;            // [raw_cap] every raw link (debug output)

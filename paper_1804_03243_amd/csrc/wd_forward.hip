@@ -5,27 +5,140 @@
 // oracle): emitting expansion of the surviving tokens of frame t-1 over a flat,
 // prefix-sum load-balanced arc work space (Sec. 3.3 static load balancing);
 // recombination by a 64-bit atomicMin of (cost key, arc id) on the state's
-// slot (Alg. 1); beam cutoff from the best emitting candidate; epsilon closure
-// one epsilon level at a time; exact max-active cutoff by radix select over an
-// LDS histogram; compaction of the survivors into a frontier sorted by state
-// (which numbers the lattice nodes (t, i) of Sec. 3.5); lattice links for every
-// surviving token-passing operation (Sec. 3.4).
+// token slot (Alg. 1); beam cutoff from the best emitting candidate; epsilon
+// closure one epsilon level at a time; exact max-active cutoff by radix select
+// over an LDS histogram; compaction of the survivors into a frontier sorted by
+// state (which numbers the lattice nodes (t, i) of Sec. 3.5); lattice links for
+// every surviving token-passing operation (Sec. 3.4).
+//
+// A frame's token table lives in LDS when the frame is small: an open-addressing
+// hash of the touched states holding the packed tokens, so recombination,
+// epsilon relaxation and the survivor scan are LDS operations.  A frame that
+// touches more states than the table holds is redone from the same frontier on
+// the global per-state slot array (its inputs are unchanged, so the result is
+// identical).  The frontier itself is kept in LDS when it fits.
 #include "wd_block.h"
 
 namespace wd {
 
+constexpr uint32_t kNoKey = 0xffffffffu;
+constexpr uint32_t kLdsWork = 3 * kHashMax;  // emitting work above which a frame starts global
+constexpr uint32_t kBkCap = 1024;            // LDS epsilon bucket entries before a frame spills
+
 struct FwdShared {
   BlockScratch bs;
-  uint32_t n_touched;
-  uint32_t n_surv;
+  uint32_t n_touched;  // global table: touched states
+  uint32_t n_surv;     // survivors of the beam cutoff
   uint32_t n_rank;
   uint32_t sel_b;
   uint32_t sel_before;
-  uint32_t nb[kMaxLevels + 1];
+  uint32_t hcount;     // LDS table: reserved entries
+  uint32_t spill;      // LDS table full: the frame goes global
+  uint32_t n_bk;       // LDS table: epsilon bucket entries
+  uint32_t nb[kMaxLevels + 1];  // global table: bucket sizes per level
+  uint32_t nbl[kMaxLevels + 1]; // LDS table: bucket entries per level
   uint32_t hist[kHistBins];
   uint32_t rs_state[kRankMax];
   unsigned long long rs_pack[kRankMax];
+  uint32_t rs_slot[kRankMax];
+  uint32_t srt[kRankMax];      // states by bucket while sorting survivors
+  uint32_t h_key[kHashCap];
+  unsigned long long h_val[kHashCap];
+  uint4 bk[kBkCap];    // {table slot, first epsilon arc, end epsilon arc, level}
+  uint32_t f_state[kFrontCap + 1];
+  uint32_t f_key[kFrontCap + 1];
+  uint32_t f_arc[kFrontCap + 1];
+  uint32_t f_edeg[kFrontCap + 1];
+  uint32_t f_xdeg[kFrontCap + 1];
+  uint32_t f_ebeg[kFrontCap + 1];
+  uint32_t f_xbeg[kFrontCap + 1];
+  uint8_t f_cls[kFrontCap + 1];
 };
+
+// Frontier arrays of one frame, in LDS or in the workspace.
+struct Front {
+  uint32_t* state;
+  uint32_t* key;
+  uint32_t* arc;
+  uint32_t* edeg;
+  uint32_t* xdeg;
+  uint32_t* ebeg;
+  uint32_t* xbeg;
+  uint8_t* cls;
+};
+
+__device__ __forceinline__ Front front_at(bool lds, FwdShared& sh, const LaneDesc& L) {
+  if (lds) return Front{sh.f_state, sh.f_key, sh.f_arc, sh.f_edeg, sh.f_xdeg, sh.f_ebeg, sh.f_xbeg, sh.f_cls};
+  return Front{L.f_state, L.f_key, L.f_arc, L.f_edeg, L.f_xdeg, L.f_ebeg, L.f_xbeg, L.f_cls};
+}
+
+// ---------------------------------------------------------------- LDS table
+
+__device__ __forceinline__ uint32_t h_home(uint32_t s) { return (s * 0x9E3779B1u) >> 20; }  // 12 bits
+
+// Find or insert state s; returns its slot, or kHashCap when the table is full
+// (sh.spill is then set).  *fresh: this call inserted s.  At most kHashMax
+// entries are ever inserted (< kHashCap), so every probe sequence ends.
+__device__ __forceinline__ uint32_t h_insert(FwdShared& sh, uint32_t s, bool* fresh) {
+  *fresh = false;
+  uint32_t i = h_home(s);
+  while (true) {
+    const uint32_t k = sh.h_key[i];
+    if (k == s) return i;
+    if (k == kNoKey) break;
+    i = (i + 1) & (kHashCap - 1);
+  }
+  if (atomicAdd(&sh.hcount, 1u) >= (uint32_t)kHashMax) {
+    sh.spill = 1;
+    return kHashCap;
+  }
+  while (true) {
+    const uint32_t prev = atomicCAS(&sh.h_key[i], kNoKey, s);
+    if (prev == kNoKey) {
+      *fresh = true;
+      return i;
+    }
+    if (prev == s) return i;
+    i = (i + 1) & (kHashCap - 1);
+  }
+}
+
+__device__ __forceinline__ uint32_t h_find(const FwdShared& sh, uint32_t s) {
+  uint32_t i = h_home(s);
+  while (true) {
+    const uint32_t k = sh.h_key[i];
+    if (k == s) return i;
+    if (k == kNoKey) return kHashCap;
+    i = (i + 1) & (kHashCap - 1);
+  }
+}
+
+__device__ __forceinline__ void h_clear(FwdShared& sh) {
+  for (uint32_t i = threadIdx.x; i < (uint32_t)kHashCap; i += kThreads) {
+    sh.h_key[i] = kNoKey;
+    sh.h_val[i] = kEmpty;
+  }
+  for (uint32_t i = threadIdx.x; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nbl[i] = 0;
+  if (threadIdx.x == 0) {
+    sh.hcount = 0;
+    sh.spill = 0;
+    sh.n_bk = 0;
+  }
+}
+
+// A first touch in the LDS table of a state with epsilon out-arcs: remember
+// its slot, epsilon arc range and level for the epsilon passes.
+__device__ __forceinline__ void lds_bucket(FwdShared& sh, uint32_t slot, uint2 o0, uint2 o1, uint32_t cls) {
+  const uint32_t b = atomicAdd(&sh.n_bk, 1u);
+  if (b < kBkCap) {
+    sh.bk[b] = make_uint4(slot, o0.y, o1.y, cls);
+    atomicAdd(&sh.nbl[cls], 1u);
+  } else {
+    sh.spill = 1;
+  }
+}
+
+// ------------------------------------------------------------- global table
 
 // Record a first touch of `dst` this frame: touched list (ballot-aggregated)
 // and, if the state has epsilon out-arcs, the bucket of its epsilon level.
@@ -53,12 +166,12 @@ __device__ __forceinline__ void note_touch_div(uint32_t dst, uint32_t cls, FwdSh
 }
 
 // Find the bin holding the rank-th smallest key in sh.hist (1-based rank).
-__device__ __forceinline__ void select_bin(uint32_t rank, FwdShared& sh, uint32_t* bin,
+__device__ __forceinline__ void select_bin(uint32_t rank, FwdShared& sh, uint32_t& par, uint32_t* bin,
                                            uint32_t* before, uint32_t* count) {
   const uint32_t tid = threadIdx.x;
   uint32_t h0 = sh.hist[2 * tid], h1 = sh.hist[2 * tid + 1];
   uint32_t tot;
-  uint32_t ex = block_excl_scan(h0 + h1, sh.bs, &tot);
+  uint32_t ex = block_excl_scan(h0 + h1, sh.bs, par, &tot);
   if (ex < rank && rank <= ex + h0) {
     sh.sel_b = 2 * tid;
     sh.sel_before = ex;
@@ -87,23 +200,11 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
 
   for (uint32_t i = tid; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nb[i] = 0;
   for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
+  h_clear(sh);
   if (tid == 0) {
     sh.n_touched = 0;
     sh.n_surv = 0;
     sh.n_rank = 0;
-  }
-  __syncthreads();
-  // frame 0: the start token (cost 0, no predecessor)
-  if (tid == 0) {
-    const uint32_t s0 = g.start;
-    L.slot[s0] = pack_tok(cost_key(0.0f), kNoArc);
-    L.touched[0] = s0;
-    sh.n_touched = 1;
-    const uint32_t c = g.sclass[s0];
-    if (c != kNoEps) {
-      L.bucket[g.level_base[c]] = s0;
-      sh.nb[c] = 1;
-    }
   }
   __syncthreads();
 
@@ -112,13 +213,13 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
   uint32_t best_key = cost_key(0.0f);
   uint64_t node_base = 0, node_base_prev = 0, link_base = 0;
   uint32_t n_prev = 0, W = 0;
-  int cur = 0;
+  bool front_lds = true;  // where the frontier of the last finished frame is
   uint64_t my_arcs = 0, my_eps = 0, tokens = 0, max_tokens = 0, need_frame = 1, need_arcs = 0;
   bool hist_ok = true;  // history (nodes, links) still being stored
+  uint32_t par = 0;     // scratch buffer parity of the workgroup collectives
   int t = 0;
 
   for (t = 0; t <= T; ++t) {
-    // ------------------------------------------------ emitting expansion
     if (t > 0) {
       need_arcs = W > need_arcs ? W : need_arcs;
       if (W > L.cand_cap) {
@@ -126,99 +227,238 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         ovf |= kOvfArcs;
         break;
       }
-      if (tid == 0) my_arcs += W;
-      const int pb = cur ^ 1;
-      const uint32_t* fs = L.f_state[pb];
-      const uint32_t* fk = L.f_key[pb];
-      const uint32_t* fe = L.f_edeg[pb];
-      const float* row = L.ll + (size_t)(t - 1) * P;
-      uint32_t my_best = 0xffffffffu;
-      for (uint32_t base = 0; base < W; base += kThreads) {
-        const uint32_t w = base + tid;
-        bool first = false;
-        uint32_t dst = 0, cls = kNoEps;
-        if (w < W) {
-          const uint32_t i = search_le(fe, n_prev, w);
-          const uint32_t s = fs[i];
-          const float c = key_cost(fk[i]);
-          const uint4 r = g.earc[g.off[s].x + (w - fe[i])];
-          dst = r.x;
-          cls = r.z >> 24;
-          const float ac = -row[(r.z & 0xffffffu) - 1u];
-          float x = c + ac;
-          x = canon(x + __uint_as_float(r.y));
-          const uint32_t xk = cost_key(x);
-          if (xk < kInfKey) {
-            const unsigned long long old = atomicMin(&L.slot[dst], pack_tok(xk, r.w));
-            first = old == kEmpty;
-            my_best = xk < my_best ? xk : my_best;
+    }
+    const Front fp = front_at(front_lds, sh, L);  // frontier of frame t-1
+    const float* row = L.ll + (size_t)(t > 0 ? t - 1 : 0) * P;
+    bool lds = t == 0 || W <= kLdsWork;
+    uint32_t kcutb = 0, ns = 0;
+    uint32_t nbits = 0, shift = 0;
+    uint64_t eps_frame = 0;
+    bool failed = false;
+    // ---------------------------------------------------- token passing
+    for (int attempt = 0; attempt < 2; ++attempt) {
+      eps_frame = 0;
+      if (lds) {
+        // ------------------------------------------ LDS token table
+        if (t == 0) {
+          if (tid == 0) {
+            const uint32_t s0 = g.start;
+            bool fresh;
+            const uint32_t slot = h_insert(sh, s0, &fresh);
+            sh.h_val[slot] = pack_tok(cost_key(0.0f), kNoArc);
+            const uint32_t c = g.sclass[s0];
+            if (c != kNoEps) lds_bucket(sh, slot, g.off[s0], g.off[s0 + 1], c);
           }
-          L.cand[w] = make_uint4(r.w, (uint32_t)(node_base_prev + i), dst, __float_as_uint(x));
+          best_key = cost_key(0.0f);
+        } else {
+          uint32_t my_best = 0xffffffffu;
+          for (uint32_t base = 0; base < W; base += kThreads) {
+            const uint32_t w = base + tid;
+            if (w >= W) break;
+            const uint32_t i = search_le(fp.edeg, n_prev, w);
+            const float c = key_cost(fp.key[i]);
+            const uint4 r = g.earc[fp.ebeg[i] + (w - fp.edeg[i])];
+            const uint32_t dst = r.x, cls = r.z >> 24;
+            // CSR offsets of the destination: the epsilon range for the bucket,
+            // and warm in cache for the degree pass if the token survives
+            const uint2 o0 = g.off[dst], o1 = g.off[dst + 1];
+            const float ac = -row[(r.z & 0xffffffu) - 1u];
+            float x = c + ac;
+            x = canon(x + __uint_as_float(r.y));
+            const uint32_t xk = cost_key(x);
+            if (xk < kInfKey) {
+              my_best = xk < my_best ? xk : my_best;
+              if (!sh.spill) {
+                bool fresh;
+                const uint32_t slot = h_insert(sh, dst, &fresh);
+                if (slot < (uint32_t)kHashCap) {
+                  atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
+                  if (fresh && cls != kNoEps) lds_bucket(sh, slot, o0, o1, cls);
+                }
+              }
+            }
+            L.cand[w] = make_uint4(r.w, (uint32_t)(node_base_prev + i), dst, __float_as_uint(x));
+          }
+          best_key = (uint32_t)block_min64(my_best, sh.bs, par);
+          if (best_key >= kInfKey) {
+            status = 3;  // WD_ENOPATH
+            failed = true;
+            break;
+          }
         }
-        note_touch(first, dst, cls, sh, g, L);
-      }
-      best_key = (uint32_t)block_min64(my_best, sh.bs);
-      if (best_key >= kInfKey) {
-        status = 3;  // WD_ENOPATH
-        break;
-      }
-    }
-    // --------------------------------------------- beam cutoff, epsilon levels
-    const float best = key_cost(best_key);
-    const float cutb = best + prm.beam;
-    const uint32_t kcutb = cost_key(cutb);
-    for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
-      const uint32_t n = sh.nb[lvl];
-      const uint32_t* bk = L.bucket + g.level_base[lvl];
-      for (uint32_t i = tid; i < n; i += kThreads) {
-        const uint32_t s = bk[i];
-        const uint32_t k = (uint32_t)(L.slot[s] >> 32);
-        if (k > kcutb) continue;
-        const float c = key_cost(k);
-        const uint32_t a0 = g.off[s].y, a1 = g.off[s + 1].y;
-        my_eps += a1 - a0;
-        for (uint32_t a = a0; a < a1; ++a) {
-          const uint4 r = g.xarc[a];
-          const float x = canon(c + __uint_as_float(r.y));
-          const uint32_t xk = cost_key(x);
-          if (xk > kcutb || xk >= kInfKey) continue;
-          const unsigned long long old = atomicMin(&L.slot[r.x], pack_tok(xk, r.w));
-          if (old == kEmpty) note_touch_div(r.x, r.z, sh, g, L);
+        __syncthreads();
+        if (sh.spill) {
+          lds = false;
+          continue;
         }
+        const float cutb = key_cost(best_key) + prm.beam;
+        kcutb = cost_key(cutb);
+        for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
+          if (sh.nbl[lvl] == 0) continue;  // uniform: written only by lower levels
+          const uint32_t n = sh.n_bk < kBkCap ? sh.n_bk : kBkCap;
+          for (uint32_t i = tid; i < n; i += kThreads) {
+            const uint4 e = sh.bk[i];
+            if (e.w != lvl) continue;
+            const uint32_t k = (uint32_t)(sh.h_val[e.x] >> 32);
+            if (k > kcutb) continue;
+            const float c = key_cost(k);
+            eps_frame += e.z - e.y;
+            for (uint32_t a = e.y; a < e.z; ++a) {
+              const uint4 r = g.xarc[a];
+              const uint32_t xk = cost_key(canon(c + __uint_as_float(r.y)));
+              if (xk > kcutb || xk >= kInfKey || sh.spill) continue;
+              uint2 o0 = make_uint2(0, 0), o1 = make_uint2(0, 0);
+              if (r.z != kNoEps) {
+                o0 = g.off[r.x];
+                o1 = g.off[r.x + 1];
+              }
+              bool fresh;
+              const uint32_t slot = h_insert(sh, r.x, &fresh);
+              if (slot < (uint32_t)kHashCap) {
+                atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
+                if (fresh && r.z != kNoEps) lds_bucket(sh, slot, o0, o1, r.z);
+              }
+            }
+          }
+          __syncthreads();
+          if (sh.spill) break;
+        }
+        if (sh.spill) {
+          lds = false;
+          continue;
+        }
+        // survivors of the beam cutoff, straight from the table
+        const uint32_t span = kcutb - best_key;
+        nbits = span ? 32u - (uint32_t)__clz(span) : 0u;
+        shift = nbits > 11u ? nbits - 11u : 0u;
+        for (uint32_t base = 0; base < (uint32_t)kHashCap; base += kThreads) {
+          const uint32_t i = base + tid;
+          const uint32_t s = sh.h_key[i];
+          const unsigned long long v = sh.h_val[i];
+          const bool keep = s != kNoKey && (uint32_t)(v >> 32) <= kcutb;
+          const uint32_t pos = wave_append(keep, &sh.n_surv);
+          if (keep) {
+            sh.rs_state[pos] = s;
+            sh.rs_pack[pos] = v;
+            sh.rs_slot[pos] = i;
+            atomicAdd(&sh.hist[((uint32_t)(v >> 32) - best_key) >> shift], 1u);
+          }
+        }
+        __syncthreads();
+        ns = sh.n_surv;
+        need_frame = sh.hcount > need_frame ? sh.hcount : need_frame;
+      } else {
+        // --------------------------------------- global per-state slot array
+        if (t == 0) {
+          if (tid == 0) {
+            const uint32_t s0 = g.start;
+            L.slot[s0] = pack_tok(cost_key(0.0f), kNoArc);
+            L.touched[0] = s0;
+            sh.n_touched = 1;
+            const uint32_t c = g.sclass[s0];
+            if (c != kNoEps) {
+              L.bucket[g.level_base[c]] = s0;
+              sh.nb[c] = 1;
+            }
+          }
+          best_key = cost_key(0.0f);
+          __syncthreads();
+        } else {
+          uint32_t my_best = 0xffffffffu;
+          for (uint32_t base = 0; base < W; base += kThreads) {
+            const uint32_t w = base + tid;
+            bool first = false;
+            uint32_t dst = 0, cls = kNoEps;
+            if (w < W) {
+              const uint32_t i = search_le(fp.edeg, n_prev, w);
+              const float c = key_cost(fp.key[i]);
+              const uint4 r = g.earc[fp.ebeg[i] + (w - fp.edeg[i])];
+              dst = r.x;
+              cls = r.z >> 24;
+              const float ac = -row[(r.z & 0xffffffu) - 1u];
+              float x = c + ac;
+              x = canon(x + __uint_as_float(r.y));
+              const uint32_t xk = cost_key(x);
+              if (xk < kInfKey) {
+                const unsigned long long old = atomicMin(&L.slot[dst], pack_tok(xk, r.w));
+                first = old == kEmpty;
+                my_best = xk < my_best ? xk : my_best;
+              }
+              L.cand[w] = make_uint4(r.w, (uint32_t)(node_base_prev + i), dst, __float_as_uint(x));
+            }
+            note_touch(first, dst, cls, sh, g, L);
+          }
+          best_key = (uint32_t)block_min64(my_best, sh.bs, par);
+          if (best_key >= kInfKey) {
+            status = 3;  // WD_ENOPATH
+            failed = true;
+            break;
+          }
+        }
+        const float cutb = key_cost(best_key) + prm.beam;
+        kcutb = cost_key(cutb);
+        for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
+          const uint32_t n = sh.nb[lvl];
+          if (n == 0) continue;
+          const uint32_t* bk = L.bucket + g.level_base[lvl];
+          for (uint32_t i = tid; i < n; i += kThreads) {
+            const uint32_t s = bk[i];
+            const uint32_t k = (uint32_t)(L.slot[s] >> 32);
+            if (k > kcutb) continue;
+            const float c = key_cost(k);
+            const uint32_t a0 = g.off[s].y, a1 = g.off[s + 1].y;
+            eps_frame += a1 - a0;
+            for (uint32_t a = a0; a < a1; ++a) {
+              const uint4 r = g.xarc[a];
+              const uint32_t xk = cost_key(canon(c + __uint_as_float(r.y)));
+              if (xk > kcutb || xk >= kInfKey) continue;
+              const unsigned long long old = atomicMin(&L.slot[r.x], pack_tok(xk, r.w));
+              if (old == kEmpty) note_touch_div(r.x, r.z, sh, g, L);
+            }
+          }
+          __syncthreads();
+        }
+        const uint32_t nt = sh.n_touched;
+        need_frame = nt > need_frame ? nt : need_frame;
+        if (nt > L.frame_cap) {
+          status = 4;
+          ovf |= kOvfFrame;
+          failed = true;
+          break;
+        }
+        const uint32_t span = kcutb - best_key;
+        nbits = span ? 32u - (uint32_t)__clz(span) : 0u;
+        shift = nbits > 11u ? nbits - 11u : 0u;
+        for (uint32_t base = 0; base < nt; base += kThreads) {
+          const uint32_t i = base + tid;
+          bool keep = false;
+          uint32_t s = 0;
+          unsigned long long v = kEmpty;
+          if (i < nt) {
+            s = L.touched[i];
+            v = L.slot[s];
+            L.slot[s] = kEmpty;
+            keep = (uint32_t)(v >> 32) <= kcutb;
+          }
+          const uint32_t pos = wave_append(keep, &sh.n_surv);
+          if (keep) {
+            L.surv_state[pos] = s;
+            L.surv_pack[pos] = v;
+            atomicAdd(&sh.hist[((uint32_t)(v >> 32) - best_key) >> shift], 1u);
+          }
+        }
+        __syncthreads();
+        ns = sh.n_surv;
       }
-      __syncthreads();
-    }
-    // ------------------------------------ survivors of the beam cutoff + histogram
-    const uint32_t nt = sh.n_touched;
-    need_frame = nt > need_frame ? nt : need_frame;
-    if (nt > L.frame_cap) {
-      status = 4;
-      ovf |= kOvfFrame;
       break;
     }
-    const uint32_t span = kcutb - best_key;
-    const uint32_t nbits = span ? 32u - (uint32_t)__clz(span) : 0u;
-    uint32_t shift = nbits > 11u ? nbits - 11u : 0u;
-    for (uint32_t base = 0; base < nt; base += kThreads) {
-      const uint32_t i = base + tid;
-      bool keep = false;
-      uint32_t s = 0;
-      unsigned long long v = kEmpty;
-      if (i < nt) {
-        s = L.touched[i];
-        v = L.slot[s];
-        L.slot[s] = kEmpty;
-        keep = (uint32_t)(v >> 32) <= kcutb;
-      }
-      const uint32_t pos = wave_append(keep, &sh.n_surv);
-      if (keep) {
-        L.surv_state[pos] = s;
-        L.surv_pack[pos] = v;
-        atomicAdd(&sh.hist[((uint32_t)(v >> 32) - best_key) >> shift], 1u);
-      }
-    }
-    __syncthreads();
-    const uint32_t ns = sh.n_surv;
+    if (failed) break;
+    my_eps += eps_frame;
+    if (t > 0 && tid == 0) my_arcs += W;
+    const float best = key_cost(best_key);
+    const float cutb = key_cost(kcutb);
+    const unsigned long long* spack = lds ? sh.rs_pack : L.surv_pack;
+    const uint32_t* sstate = lds ? sh.rs_state : L.surv_state;
     // ------------------------------------------------ max-active cutoff
     uint32_t cut_key = kcutb;
     uint32_t n_keep = ns;
@@ -227,7 +467,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       uint32_t bits = nbits - shift;
       while (true) {
         uint32_t b, before, cnt;
-        select_bin(rank, sh, &b, &before, &cnt);
+        select_bin(rank, sh, par, &b, &before, &cnt);
         prefix = (prefix << bits) | b;
         less += before;
         rank -= before;
@@ -240,7 +480,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
         __syncthreads();
         for (uint32_t i = tid; i < ns; i += kThreads) {
-          const uint32_t d = (uint32_t)(L.surv_pack[i] >> 32) - best_key;
+          const uint32_t d = (uint32_t)(spack[i] >> 32) - best_key;
           if ((d >> shift) == prefix) atomicAdd(&sh.hist[(d >> nsh) & ((1u << bits) - 1u)], 1u);
         }
         shift = nsh;
@@ -250,8 +490,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       cut_key = vkey < kcutb ? vkey : kcutb;
     }
     // -------------------------------- compaction into a frontier sorted by state
-    uint32_t* fs = L.f_state[cur];
-    uint32_t* fk = L.f_key[cur];
+    const bool fl = n_keep <= (uint32_t)kFrontCap;
+    const Front f = front_at(fl, sh, L);
     if (hist_ok && node_base + n_keep > L.node_cap) {
       hist_ok = false;
       ovf |= kOvfNodes;
@@ -263,43 +503,89 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         L.n_pack[node] = v;
         L.n_pred[node] = kNoArc;
       }
-      L.idx[s] = (uint32_t)node;
-      fs[p] = s;
-      fk[p] = (uint32_t)(v >> 32);
+      f.state[p] = s;
+      f.key[p] = (uint32_t)(v >> 32);
+      f.arc[p] = (uint32_t)v;
     };
-    if (n_keep <= (uint32_t)kRankMax) {
-      for (uint32_t base = 0; base < ns; base += kThreads) {
-        const uint32_t i = base + tid;
-        bool keep = false;
-        uint32_t s = 0;
-        unsigned long long v = 0;
-        if (i < ns) {
-          v = L.surv_pack[i];
-          s = L.surv_state[i];
-          keep = (uint32_t)(v >> 32) <= cut_key;
+    if (lds || n_keep <= (uint32_t)kRankMax) {
+      if (!lds) {
+        // gather the kept survivors of the global table into rs_*
+        for (uint32_t base = 0; base < ns; base += kThreads) {
+          const uint32_t i = base + tid;
+          bool keep = false;
+          uint32_t s = 0;
+          unsigned long long v = 0;
+          if (i < ns) {
+            v = spack[i];
+            s = sstate[i];
+            keep = (uint32_t)(v >> 32) <= cut_key;
+          }
+          const uint32_t pos = wave_append(keep, &sh.n_rank);
+          if (keep && pos < (uint32_t)kRankMax) {
+            sh.rs_state[pos] = s;
+            sh.rs_pack[pos] = v;
+            sh.rs_slot[pos] = kHashCap;
+          }
         }
-        const uint32_t pos = wave_append(keep, &sh.n_rank);
-        if (keep && pos < (uint32_t)kRankMax) {
-          sh.rs_state[pos] = s;
-          sh.rs_pack[pos] = v;
+        __syncthreads();
+        if (sh.n_rank != n_keep) {
+          status = kStatusInternal;
+          break;
         }
       }
+      const uint32_t m = lds ? ns : n_keep;  // entries in rs_* (<= 2 * kThreads)
+      // counting sort on the top 11 bits of the state, then the few states
+      // sharing a bucket are ranked among themselves
+      const uint32_t sbits = 32u - (uint32_t)__clz(g.S > 1 ? g.S - 1 : 1u);
+      const uint32_t ssh = sbits > 11u ? sbits - 11u : 0u;
+      for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
       __syncthreads();
-      if (sh.n_rank != n_keep) {
+      uint32_t bb[2] = {0, 0}, loc[2] = {0, 0}, sv[2] = {0, 0}, sl[2] = {0, 0};
+      unsigned long long vv[2] = {0, 0};
+      bool kp[2] = {false, false};
+      for (int u = 0; u < 2; ++u) {
+        const uint32_t j = tid + (uint32_t)u * kThreads;
+        if (j >= m) continue;
+        vv[u] = sh.rs_pack[j];
+        if ((uint32_t)(vv[u] >> 32) > cut_key) continue;
+        kp[u] = true;
+        sv[u] = sh.rs_state[j];
+        sl[u] = sh.rs_slot[j];
+        bb[u] = sv[u] >> ssh;
+        loc[u] = atomicAdd(&sh.hist[bb[u]], 1u);
+      }
+      __syncthreads();
+      uint32_t nk;
+      {
+        const uint32_t h0 = sh.hist[2 * tid], h1 = sh.hist[2 * tid + 1];
+        const uint32_t ex = block_excl_scan(h0 + h1, sh.bs, par, &nk);
+        __syncthreads();  // every count read before the starts overwrite them
+        sh.hist[2 * tid] = ex;
+        sh.hist[2 * tid + 1] = ex + h0;
+      }
+      if (nk != n_keep) {
         status = kStatusInternal;
         break;
       }
-      for (uint32_t j = tid; j < n_keep; j += kThreads) {
-        const uint32_t s = sh.rs_state[j];
-        uint32_t r = 0;
-        for (uint32_t q = 0; q < n_keep; ++q) r += sh.rs_state[q] < s;
-        place(r, s, sh.rs_pack[j]);
+      __syncthreads();
+      for (int u = 0; u < 2; ++u)
+        if (kp[u]) sh.srt[sh.hist[bb[u]] + loc[u]] = sv[u];
+      __syncthreads();
+      for (int u = 0; u < 2; ++u) {
+        if (!kp[u]) continue;
+        const uint32_t b0 = sh.hist[bb[u]];
+        const uint32_t b1 = bb[u] + 1 < (uint32_t)kHistBins ? sh.hist[bb[u] + 1] : n_keep;
+        uint32_t r = b0;
+        for (uint32_t q = b0; q < b1; ++q) r += sh.srt[q] < sv[u];
+        place(r, sv[u], vv[u]);
+        if (lds) sh.h_val[sl[u]] = node_base + r;  // the table now maps kept states to node ids
+        else L.idx[sv[u]] = (uint32_t)(node_base + r);
       }
     } else {
       for (uint32_t i = tid; i < ns; i += kThreads) {
-        const unsigned long long v = L.surv_pack[i];
+        const unsigned long long v = spack[i];
         if ((uint32_t)(v >> 32) <= cut_key) {
-          const uint32_t s = L.surv_state[i];
+          const uint32_t s = sstate[i];
           L.idx[s] = i;
           atomicOr(&L.bitmap[s >> 5], 1u << (s & 31u));
         }
@@ -312,7 +598,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       uint32_t cnt = 0;
       for (uint32_t w = w0; w < w1; ++w) cnt += (uint32_t)__popc(L.bitmap[w]);
       uint32_t tot;
-      uint32_t p = block_excl_scan(cnt, sh.bs, &tot);
+      uint32_t p = block_excl_scan(cnt, sh.bs, par, &tot);
       for (uint32_t w = w0; w < w1; ++w) {
         uint32_t word = L.bitmap[w];
         if (!word) continue;
@@ -321,15 +607,14 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           const uint32_t b = (uint32_t)__ffs(word) - 1u;
           word &= word - 1u;
           const uint32_t s = (w << 5) | b;
-          place(p++, s, L.surv_pack[L.idx[s]]);
+          place(p, s, spack[L.idx[s]]);
+          L.idx[s] = (uint32_t)(node_base + p);
+          ++p;
         }
       }
     }
     __syncthreads();
-    // ------------------------------------- out-degree prefix sums of the frontier
-    uint32_t* fe = L.f_edeg[cur];
-    uint32_t* fx = L.f_xdeg[cur];
-    uint8_t* fc = L.f_cls[cur];
+    // ------------------------------- arc offsets and degree prefix sums
     uint32_t W_next, W_eps;
     {
       const uint32_t per = (n_keep + kThreads - 1) / kThreads;
@@ -337,25 +622,31 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       const uint32_t p1 = p0 + per < n_keep ? p0 + per : n_keep;
       uint32_t e = 0, x = 0;
       for (uint32_t p = p0; p < p1; ++p) {
-        const uint32_t s = fs[p];
+        const uint32_t s = f.state[p];
         const uint2 o0 = g.off[s], o1 = g.off[s + 1];
         e += o1.x - o0.x;
         x += o1.y - o0.y;
+        f.ebeg[p] = o0.x;
+        f.xbeg[p] = o0.y;
+        f.edeg[p] = o1.x - o0.x;  // degrees for now, prefix sums below
+        f.xdeg[p] = o1.y - o0.y;
+        f.cls[p] = g.sclass[s];
       }
-      uint32_t eb = block_excl_scan(e, sh.bs, &W_next);
-      uint32_t xb = block_excl_scan(x, sh.bs, &W_eps);
+      uint64_t tot2;
+      const uint64_t ex2 = block_excl_scan64(((uint64_t)x << 32) | e, sh.bs, par, &tot2);
+      uint32_t eb = (uint32_t)ex2, xb = (uint32_t)(ex2 >> 32);
+      W_next = (uint32_t)tot2;
+      W_eps = (uint32_t)(tot2 >> 32);
       for (uint32_t p = p0; p < p1; ++p) {
-        const uint32_t s = fs[p];
-        const uint2 o0 = g.off[s], o1 = g.off[s + 1];
-        fe[p] = eb;
-        fx[p] = xb;
-        fc[p] = g.sclass[s];
-        eb += o1.x - o0.x;
-        xb += o1.y - o0.y;
+        const uint32_t de = f.edeg[p], dx = f.xdeg[p];
+        f.edeg[p] = eb;
+        f.xdeg[p] = xb;
+        eb += de;
+        xb += dx;
       }
       if (tid == 0) {
-        fe[n_keep] = W_next;
-        fx[n_keep] = W_eps;
+        f.edeg[n_keep] = W_next;
+        f.xdeg[n_keep] = W_eps;
       }
     }
     __syncthreads();
@@ -369,10 +660,18 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     tokens += n_keep;
     max_tokens = n_keep > max_tokens ? n_keep : max_tokens;
     // -------------------------------------------------- lattice links of frame t
-    // emitting run: candidates in work-item order are in arc-id order
+    // node id of a state that survived frame t
+    auto dst_node = [&](uint32_t s) -> uint64_t {
+      if (lds) {
+        const uint32_t slot = h_find(sh, s);
+        return slot < (uint32_t)kHashCap ? sh.h_val[slot] : kEmpty;
+      }
+      return L.idx[s];
+    };
     uint32_t nE = 0, nX = 0;
-    uint32_t bad_idx = 0;
+    uint32_t bad_idx = 0, xmask = 0;
     {
+      // emitting run: candidates in work-item order are in arc-id order
       const uint32_t Wc = t > 0 ? W : 0;
       const uint32_t per = (Wc + kThreads - 1) / kThreads;
       const uint32_t w0 = tid * per < Wc ? tid * per : Wc;
@@ -382,23 +681,25 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         const uint32_t xk = cost_key(__uint_as_float(L.cand[w].w));
         cnt += xk <= cut_key && xk < kInfKey;
       }
-      uint32_t pos = block_excl_scan(cnt, sh.bs, &nE);
       // epsilon run: every epsilon out-arc of the frontier within the cutoff
       const uint32_t perx = (W_eps + kThreads - 1) / kThreads;
       const uint32_t e0 = tid * perx < W_eps ? tid * perx : W_eps;
       const uint32_t e1 = e0 + perx < W_eps ? e0 + perx : W_eps;
       uint32_t cntx = 0;
       if (e0 < e1) {
-        uint32_t p = search_le(fx, n_keep, e0);
+        uint32_t p = search_le(f.xdeg, n_keep, e0);
         for (uint32_t e = e0; e < e1; ++e) {
-          while (fx[p + 1] <= e) ++p;
-          const uint32_t s = fs[p];
-          const uint4 r = g.xarc[g.off[s].y + (e - fx[p])];
-          const uint32_t xk = cost_key(canon(key_cost(fk[p]) + __uint_as_float(r.y)));
+          while (f.xdeg[p + 1] <= e) ++p;
+          const uint4 r = g.xarc[f.xbeg[p] + (e - f.xdeg[p])];
+          const uint32_t xk = cost_key(canon(key_cost(f.key[p]) + __uint_as_float(r.y)));
           cntx += xk <= cut_key && xk < kInfKey;
         }
       }
-      uint32_t posx = block_excl_scan(cntx, sh.bs, &nX);
+      uint64_t tot2;
+      const uint64_t ex2 = block_excl_scan64(((uint64_t)cntx << 32) | cnt, sh.bs, par, &tot2);
+      uint32_t pos = (uint32_t)ex2, posx = (uint32_t)(ex2 >> 32);
+      nE = (uint32_t)tot2;
+      nX = (uint32_t)(tot2 >> 32);
       if (hist_ok && link_base + nE + nX > L.link_cap) {
         hist_ok = false;
         ovf |= kOvfLinks;
@@ -408,40 +709,43 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           const uint4 c = L.cand[w];
           const uint32_t xk = cost_key(__uint_as_float(c.w));
           if (!(xk <= cut_key && xk < kInfKey)) continue;
-          const uint32_t dn = L.idx[c.z];
+          const uint64_t dn = dst_node(c.z);
           if (dn < node_base || dn >= node_base + n_keep) {
             bad_idx = 1;
             continue;
           }
-          L.links[link_base + pos] = make_uint4(c.x, c.y, dn, c.w);
+          L.links[link_base + pos] = make_uint4(c.x, c.y, (uint32_t)dn, c.w);
           ++pos;
-          if (L.n_pack[dn] == pack_tok(xk, c.x)) L.n_pred[dn] = c.y;
+          const uint32_t q = (uint32_t)(dn - node_base);
+          if (f.key[q] == xk && f.arc[q] == c.x) L.n_pred[dn] = c.y;
         }
         if (e0 < e1) {
-          uint32_t p = search_le(fx, n_keep, e0);
+          uint32_t p = search_le(f.xdeg, n_keep, e0);
           for (uint32_t e = e0; e < e1; ++e) {
-            while (fx[p + 1] <= e) ++p;
-            const uint32_t s = fs[p];
-            const uint4 r = g.xarc[g.off[s].y + (e - fx[p])];
-            const float x = canon(key_cost(fk[p]) + __uint_as_float(r.y));
+            while (f.xdeg[p + 1] <= e) ++p;
+            const uint4 r = g.xarc[f.xbeg[p] + (e - f.xdeg[p])];
+            const float x = canon(key_cost(f.key[p]) + __uint_as_float(r.y));
             const uint32_t xk = cost_key(x);
             if (!(xk <= cut_key && xk < kInfKey)) continue;
-            const uint32_t dn = L.idx[r.x];
+            const uint64_t dn = dst_node(r.x);
             if (dn < node_base || dn >= node_base + n_keep) {
               bad_idx = 1;
               continue;
             }
             const uint32_t sn = (uint32_t)(node_base + p);
             const uint64_t at = link_base + nE + posx;
-            L.links[at] = make_uint4(r.w, sn, dn, __float_as_uint(x));
-            L.link_lvl[at] = fc[p];
+            L.links[at] = make_uint4(r.w, sn, (uint32_t)dn, __float_as_uint(x));
+            L.link_lvl[at] = f.cls[p];
+            xmask |= 1u << (f.cls[p] < 31 ? f.cls[p] : 31);
             ++posx;
-            if (L.n_pack[dn] == pack_tok(xk, r.w)) L.n_pred[dn] = sn;
+            const uint32_t q = (uint32_t)(dn - node_base);
+            if (f.key[q] == xk && f.arc[q] == r.w) L.n_pred[dn] = sn;
           }
         }
       }
     }
-    if (block_or(bad_idx, sh.bs)) {
+    const uint32_t fl_or = block_or((bad_idx ? 0x80000000u : 0u) | xmask, sh.bs, par);
+    if (fl_or & 0x80000000u) {
       status = kStatusInternal;
       break;
     }
@@ -449,6 +753,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       L.link_off[t] = link_base;
       L.link_xoff[t] = link_base + nE;
       L.link_off[t + 1] = link_base + nE + nX;
+      L.xmask[t] = fl_or & 0x7fffffffu;
     }
     link_base += nE + nX;
     // ----------------------------------------------------- next frame
@@ -456,9 +761,10 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     node_base += n_keep;
     n_prev = n_keep;
     W = W_next;
-    cur ^= 1;
+    front_lds = fl;
     for (uint32_t i = tid; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nb[i] = 0;
     for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
+    h_clear(sh);
     __syncthreads();
     if (tid == 0) {
       sh.n_touched = 0;
@@ -468,8 +774,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     __syncthreads();
   }
 
-  const uint64_t eps = block_sum64(my_eps, sh.bs);
-  const uint64_t arcs = block_sum64(my_arcs, sh.bs) + eps;
+  const uint64_t eps = block_sum64(my_eps, sh.bs, par);
+  const uint64_t arcs = block_sum64(my_arcs, sh.bs, par) + eps;
   if (tid == 0) {
     LaneInfo* info = L.info;
     if (status == 0 && (ovf & (kOvfNodes | kOvfLinks))) status = 4;

@@ -15,8 +15,6 @@ namespace wd {
 
 struct LatShared {
   BlockScratch bs;
-  unsigned long long nw;   // traceback words collected (thread 0 writes)
-  uint32_t tb_ok;
 };
 
 __device__ __forceinline__ uint64_t search_le64(const uint64_t* a, uint64_t n, uint64_t w) {
@@ -143,6 +141,14 @@ __device__ void assemble(const LaneDesc& L, const DevGraph& g, bool all, uint64_
   }
 }
 
+// Levels present in a frame's epsilon links, highest first / lowest first.
+__device__ __forceinline__ bool level_present(uint32_t mask, uint32_t lvl) {
+  return (mask >> (lvl < 31u ? lvl : 31u)) & 1u;
+}
+
+// blockIdx.y == 0: pruning, posteriors and the final merge; blockIdx.y == 1:
+// the 1-best traceback (a serial walk over predecessor pointers, run
+// concurrently by its own workgroup).
 __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc* __restrict__ lanes,
                                                       Params prm) {
   __shared__ LatShared sh;
@@ -154,6 +160,7 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
   const uint64_t nT0 = L.node_off[T], nT1 = L.node_off[T + 1];
   const uint64_t nnodes = nT1;
   const uint64_t nlinks = L.link_off[T + 1];
+  uint32_t par = 0;
 
   // ------------------------------------------------ final costs, best end token
   uint32_t any = 0;
@@ -163,7 +170,7 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
       const float c = node_cost(L, n);
       any |= (fw < INFINITY && (c + fw) < INFINITY) ? 1u : 0u;
     }
-  const bool final_used = block_or(any, sh.bs) != 0;
+  const bool final_used = block_or(any, sh.bs, par) != 0;
   uint64_t m = kEmpty;
   for (uint64_t n = nT0 + tid; n < nT1; n += kThreads) {
     const float c = node_cost(L, n);
@@ -171,23 +178,56 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
     const uint64_t v = pack_tok(cost_key(F), (uint32_t)(n - nT0));
     m = v < m ? v : m;
   }
-  m = block_min64(m, sh.bs);
+  m = block_min64(m, sh.bs, par);
   const uint32_t best_key = (uint32_t)(m >> 32);
   if (best_key >= kInfKey) {
-    if (tid == 0) info->status = 3;
+    if (tid == 0 && blockIdx.y == 0) info->status = 3;
     return;
   }
   const float best_total = key_cost(best_key);
   const uint64_t bnode = nT0 + (m & 0xffffffffu);
 
-  // ------------------------------------- backward sweep: extra costs + traceback
-  uint64_t tb = bnode;   // traceback position (thread 0)
-  uint64_t nw = 0;
-  bool tb_ok = true;
-  if (tid == 0) {
-    sh.nw = 0;
-    sh.tb_ok = 1;
+  if (blockIdx.y == 1) {
+    // ------------------------------------------------------------ traceback
+    if (tid != 0) return;
+    uint64_t tb = bnode, nw = 0;
+    bool ok = true;
+    for (int t = T; t >= 0 && ok; --t) {
+      const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
+      // epsilon predecessors stay in frame t; an emitting one goes back a frame
+      for (uint32_t steps = 0;; ++steps) {
+        if (tb < n0 || tb >= n1 || steps > g.nlevels) {
+          ok = false;
+          break;
+        }
+        const uint32_t arc = (uint32_t)L.n_pack[tb];
+        if (arc == kNoArc) break;
+        if (arc >= g.A) {
+          ok = false;
+          break;
+        }
+        const int32_t ol = g.olabel_id[arc];
+        if (ol != 0) {
+          if (nw < L.word_cap) L.out_words[nw] = ol;
+          else ok = false;
+          ++nw;
+        }
+        tb = L.n_pred[tb];
+        if (g.ilabel_id[arc] != 0) break;
+      }
+    }
+    if (ok)
+      for (uint64_t i = 0; i < nw / 2; ++i) {  // collected last-first
+        const int32_t a = L.out_words[i];
+        L.out_words[i] = L.out_words[nw - 1 - i];
+        L.out_words[nw - 1 - i] = a;
+      }
+    info->nwords = nw;
+    info->tb_fail = ok ? 0u : 1u;
+    return;
   }
+
+  // ------------------------------------------------ backward extra-cost sweep
   for (int t = T; t >= 0; --t) {
     const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
     for (uint64_t n = n0 + tid; n < n1; n += kThreads) {
@@ -199,46 +239,60 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
       }
       L.extra_key[n] = ex;
     }
-    if (tid == 0 && tb_ok) {
-      // follow epsilon predecessors inside frame t, then one emitting arc back
-      for (uint32_t steps = 0;; ++steps) {
-        if (tb < n0 || tb >= n1 || steps > g.nlevels) {
-          tb_ok = false;
-          break;
-        }
-        const uint32_t arc = (uint32_t)L.n_pack[tb];
-        if (arc == kNoArc) break;
-        if (arc >= g.A) {
-          tb_ok = false;
-          break;
-        }
-        const int32_t ol = g.olabel_id[arc];
-        if (ol != 0) {
-          if (nw < L.word_cap) L.out_words[nw] = ol;
-          else tb_ok = false;
-          ++nw;
-        }
-        tb = L.n_pred[tb];
-        if (g.ilabel_id[arc] != 0) break;
-      }
-    }
     __syncthreads();
     if (t < T) {
       const uint64_t k0 = L.link_off[t + 1], k1 = L.link_xoff[t + 1];
-      for (uint64_t k = k0 + tid; k < k1; k += kThreads) relax_link(L, k);
-      __syncthreads();
+      if (k1 > k0) {
+        for (uint64_t k = k0 + tid; k < k1; k += kThreads) relax_link(L, k);
+        __syncthreads();
+      }
     }
     const uint64_t x0 = L.link_xoff[t], x1 = L.link_off[t + 1];
+    const uint32_t mask = L.xmask[t];
     if (x1 > x0)
       for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
+        if (!level_present(mask, (uint32_t)lvl)) continue;
         for (uint64_t k = x0 + tid; k < x1; k += kThreads)
           if (L.link_lvl[k] == (uint8_t)lvl) relax_link(L, k);
         __syncthreads();
       }
   }
 
-  // ----------------------------------------------------- posteriors (fp64)
+  // ------------------------------------------ kept links (final merge input)
   const uint32_t lb_key = cost_key(prm.lattice_beam);
+  uint64_t n_kept;
+  {
+    const uint64_t per = (nlinks + kThreads - 1) / kThreads;
+    const uint64_t k0 = tid * per < nlinks ? tid * per : nlinks;
+    const uint64_t k1 = k0 + per < nlinks ? k0 + per : nlinks;
+    uint64_t cnt = 0;
+    for (uint64_t k = k0; k < k1; ++k) cnt += kept(L, k, lb_key);
+    uint64_t pos = block_excl_scan64(cnt, sh.bs, par, &n_kept);
+    if (n_kept <= L.kept_cap)
+      for (uint64_t k = k0; k < k1; ++k)
+        if (kept(L, k, lb_key)) L.kept_idx[pos++] = k;
+  }
+  const bool debug = (prm.flags & 1u) != 0;
+  if (n_kept > L.kept_cap || (debug && nlinks > L.raw_cap)) {
+    if (tid == 0) {
+      info->status = 4;
+      info->overflow |= kOvfKept;
+      info->kept = n_kept;
+    }
+    return;
+  }
+  __syncthreads();
+  const uint64_t* kid = L.kept_idx;
+  // per frame t: kept links start at kf[2t], kept epsilon links at kf[2t+1];
+  // frame t ends where frame t+1 starts
+  uint64_t* kf = L.kframe;
+  for (int t = (int)tid; t <= T + 1; t += kThreads) {
+    kf[2 * t] = lower_bound64(kid, n_kept, L.link_off[t]);
+    kf[2 * t + 1] = t <= T ? lower_bound64(kid, n_kept, L.link_xoff[t]) : n_kept;
+  }
+  __syncthreads();
+
+  // ----------------------------------------------------- posteriors (fp64)
   uint64_t start_node = 0;
   {
     // the start state among frame 0's tokens (sorted by state)
@@ -250,94 +304,66 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
     }
     start_node = lo;
   }
+  for (uint64_t n = tid; n < nnodes; n += kThreads) {
+    L.alpha[n] = (n == start_node) ? 0.0 : INFINITY;
+    double b = INFINITY;
+    if (n >= nT0) b = final_used ? (double)g.final_w[L.n_state[n]] : 0.0;
+    L.beta[n] = b;
+  }
+  __syncthreads();
   for (int t = 0; t <= T; ++t) {
-    const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
-    for (uint64_t n = n0 + tid; n < n1; n += kThreads) L.alpha[n] = (n == start_node) ? 0.0 : INFINITY;
-    __syncthreads();
-    if (t > 0) {
-      const uint64_t k0 = L.link_off[t], k1 = L.link_xoff[t];
-      for (uint64_t k = k0 + tid; k < k1; k += kThreads) {
-        if (!kept(L, k, lb_key)) continue;
-        const LinkView l = link_at(L, k);
+    const uint64_t e0 = kf[2 * t], e1 = kf[2 * t + 1], e2 = kf[2 * t + 2];
+    if (e1 > e0) {
+      for (uint64_t j = e0 + tid; j < e1; j += kThreads) {
+        const LinkView l = link_at(L, kid[j]);
         atomic_logadd(&L.alpha[l.dst], L.alpha[l.src] + (double)g.weight_id[l.arc] + link_ac(L, g, t, l.arc));
       }
       __syncthreads();
     }
-    const uint64_t x0 = L.link_xoff[t], x1 = L.link_off[t + 1];
-    if (x1 > x0)
+    if (e2 > e1) {
+      const uint32_t mask = L.xmask[t];
       for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
-        for (uint64_t k = x0 + tid; k < x1; k += kThreads) {
-          if (L.link_lvl[k] != (uint8_t)lvl || !kept(L, k, lb_key)) continue;
+        if (!level_present(mask, lvl)) continue;
+        for (uint64_t j = e1 + tid; j < e2; j += kThreads) {
+          const uint64_t k = kid[j];
+          if (L.link_lvl[k] != (uint8_t)lvl) continue;
           const LinkView l = link_at(L, k);
           atomic_logadd(&L.alpha[l.dst], L.alpha[l.src] + (double)g.weight_id[l.arc]);
         }
         __syncthreads();
       }
+    }
   }
   for (int t = T; t >= 0; --t) {
-    const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
-    for (uint64_t n = n0 + tid; n < n1; n += kThreads) {
-      double b = INFINITY;
-      if (t == T) b = final_used ? (double)g.final_w[L.n_state[n]] : 0.0;
-      L.beta[n] = b;
-    }
-    __syncthreads();
     if (t < T) {
-      const uint64_t k0 = L.link_off[t + 1], k1 = L.link_xoff[t + 1];
-      for (uint64_t k = k0 + tid; k < k1; k += kThreads) {
-        if (!kept(L, k, lb_key)) continue;
-        const LinkView l = link_at(L, k);
-        atomic_logadd(&L.beta[l.src], (double)g.weight_id[l.arc] + link_ac(L, g, t + 1, l.arc) + L.beta[l.dst]);
+      const uint64_t e0 = kf[2 * t + 2], e1 = kf[2 * t + 3];
+      if (e1 > e0) {
+        for (uint64_t j = e0 + tid; j < e1; j += kThreads) {
+          const LinkView l = link_at(L, kid[j]);
+          atomic_logadd(&L.beta[l.src],
+                        (double)g.weight_id[l.arc] + link_ac(L, g, t + 1, l.arc) + L.beta[l.dst]);
+        }
+        __syncthreads();
       }
-      __syncthreads();
     }
-    const uint64_t x0 = L.link_xoff[t], x1 = L.link_off[t + 1];
-    if (x1 > x0)
+    const uint64_t e1 = kf[2 * t + 1], e2 = kf[2 * t + 2];
+    if (e2 > e1) {
+      const uint32_t mask = L.xmask[t];
       for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
-        for (uint64_t k = x0 + tid; k < x1; k += kThreads) {
-          if (L.link_lvl[k] != (uint8_t)lvl || !kept(L, k, lb_key)) continue;
+        if (!level_present(mask, (uint32_t)lvl)) continue;
+        for (uint64_t j = e1 + tid; j < e2; j += kThreads) {
+          const uint64_t k = kid[j];
+          if (L.link_lvl[k] != (uint8_t)lvl) continue;
           const LinkView l = link_at(L, k);
           atomic_logadd(&L.beta[l.src], (double)g.weight_id[l.arc] + L.beta[l.dst]);
         }
         __syncthreads();
       }
+    }
   }
   const double Z = L.beta[start_node];
-  if (tid == 0) {
-    sh.nw = nw;
-    sh.tb_ok = tb_ok ? 1u : 0u;
-  }
-  __syncthreads();
-  nw = sh.nw;
-  tb_ok = sh.tb_ok != 0;
 
   // ------------------------------------------- final merge of the kept links
-  uint64_t n_kept;
-  {
-    const uint64_t per = (nlinks + kThreads - 1) / kThreads;
-    const uint64_t k0 = tid * per < nlinks ? tid * per : nlinks;
-    const uint64_t k1 = k0 + per < nlinks ? k0 + per : nlinks;
-    uint64_t cnt = 0;
-    for (uint64_t k = k0; k < k1; ++k) cnt += kept(L, k, lb_key);
-    uint64_t pos = block_excl_scan64(cnt, sh.bs, &n_kept);
-    if (n_kept <= L.kept_cap)
-      for (uint64_t k = k0; k < k1; ++k)
-        if (kept(L, k, lb_key)) L.kept_idx[pos++] = k;
-  }
-  __syncthreads();
-  const bool debug = (prm.flags & 1u) != 0;
-  if (n_kept > L.kept_cap || (debug && nlinks > L.raw_cap)) {
-    if (tid == 0) {
-      info->status = 4;
-      info->overflow |= kOvfKept;
-      info->kept = n_kept;
-    }
-    return;
-  }
-  if (!tb_ok) {
-    if (tid == 0) info->status = kStatusInternal;
-    return;
-  }
   // used-node bitmap is zero on entry (cleared by the host before the launch)
   if (tid == 0) atomicOr(&L.used[start_node >> 5], 1u << (start_node & 31u));
   assemble(L, g, false, n_kept, L.out_links, lb_key, Z, true, true);
@@ -352,7 +378,7 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
     const uint64_t w1 = w0 + per < nwd ? w0 + per : nwd;
     uint64_t cnt = 0;
     for (uint64_t w = w0; w < w1; ++w) cnt += (uint64_t)__popc(L.used[w]);
-    uint64_t pos = block_excl_scan64(cnt, sh.bs, &n_out);
+    uint64_t pos = block_excl_scan64(cnt, sh.bs, par, &n_out);
     for (uint64_t w = w0; w < w1; ++w) {
       uint32_t word = L.used[w];
       while (word) {
@@ -368,18 +394,10 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
       }
     }
   }
-  __syncthreads();
-  // words were collected last-first
-  for (uint64_t i = tid; i < nw / 2; i += kThreads) {
-    const int32_t a = L.out_words[i];
-    L.out_words[i] = L.out_words[nw - 1 - i];
-    L.out_words[nw - 1 - i] = a;
-  }
   if (tid == 0) {
     info->final_used = final_used ? 1 : 0;
     info->kept = n_kept;
     info->out_nodes = n_out;
-    info->nwords = nw;
     info->out_raw = debug ? nlinks : 0;
     info->start_node = (uint32_t)start_node;
     info->best_node = (uint32_t)bnode;
@@ -388,7 +406,7 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
 }
 
 void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s) {
-  hipLaunchKernelGGL(k_lattice, dim3(B), dim3(kThreads), 0, s, g, lanes, prm);
+  hipLaunchKernelGGL(k_lattice, dim3(B, 2), dim3(kThreads), 0, s, g, lanes, prm);
 }
 
 }  // namespace wd
