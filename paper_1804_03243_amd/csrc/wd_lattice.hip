@@ -13,8 +13,20 @@
 
 namespace wd {
 
+constexpr uint32_t kWin = 4096;  // nodes of one frame held in LDS
+
+// Two-frame window of per-node values (frame t and t+1, or t-1 and t): extra
+// costs and costs during the pruning sweep, alpha or beta during the
+// posteriors.  Frames with more nodes use the workspace arrays directly.
 struct LatShared {
   BlockScratch bs;
+  union {
+    struct {
+      uint32_t ex[2][kWin];
+      float cost[2][kWin];
+    } p;
+    double ab[2][kWin];
+  } w;
 };
 
 __device__ __forceinline__ uint64_t search_le64(const uint64_t* a, uint64_t n, uint64_t w) {
@@ -65,17 +77,6 @@ struct LinkView {
 __device__ __forceinline__ LinkView link_at(const LaneDesc& L, uint64_t k) {
   const uint4 v = L.links[k];
   return LinkView{v.x, v.y, v.z, __uint_as_float(v.w)};
-}
-
-// Extra cost of link k from the (final) extra cost of its destination.
-__device__ __forceinline__ uint32_t relax_link(const LaneDesc& L, uint64_t k) {
-  const LinkView l = link_at(L, k);
-  const float exd = key_cost(L.extra_key[l.dst]);
-  const float d = l.x - node_cost(L, l.dst);
-  const uint32_t le = cost_key(exd + d);
-  L.le_key[k] = le;
-  atomicMin(&L.extra_key[l.src], le);
-  return le;
 }
 
 __device__ __forceinline__ bool kept(const LaneDesc& L, uint64_t k, uint32_t lb_key) {
@@ -230,20 +231,37 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
   // ------------------------------------------------ backward extra-cost sweep
   for (int t = T; t >= 0; --t) {
     const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
-    for (uint64_t n = n0 + tid; n < n1; n += kThreads) {
-      uint32_t ex = kInfKey;
+    const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
+    const bool win = nt <= kWin;
+    uint32_t* ex = win ? sh.w.p.ex[buf] : L.extra_key + n0;
+    for (uint32_t i = tid; i < nt; i += kThreads) {
+      const float c = node_cost(L, n0 + i);
+      uint32_t e = kInfKey;
       if (t == T) {
-        const float c = node_cost(L, n);
-        const float F = final_used ? canon(c + g.final_w[L.n_state[n]]) : c;
-        if (F < INFINITY) ex = cost_key(F - best_total);
+        const float F = final_used ? canon(c + g.final_w[L.n_state[n0 + i]]) : c;
+        if (F < INFINITY) e = cost_key(F - best_total);
       }
-      L.extra_key[n] = ex;
+      ex[i] = e;
+      if (win) sh.w.p.cost[buf][i] = c;
     }
     __syncthreads();
+    // extra(link) = extra(dst) + (x - cost(dst)); extra(src) = min over links
+    auto relax = [&](uint64_t k, const uint32_t* exd, const float* cd, uint64_t d0) {
+      const LinkView l = link_at(L, k);
+      const uint64_t d = l.dst - d0;
+      const float c = cd ? cd[d] : node_cost(L, l.dst);
+      const uint32_t le = cost_key(key_cost(exd[d]) + (l.x - c));
+      L.le_key[k] = le;
+      atomicMin(&ex[l.src - n0], le);
+    };
     if (t < T) {
       const uint64_t k0 = L.link_off[t + 1], k1 = L.link_xoff[t + 1];
       if (k1 > k0) {
-        for (uint64_t k = k0 + tid; k < k1; k += kThreads) relax_link(L, k);
+        const uint64_t m0 = L.node_off[t + 1];
+        const bool wn = L.node_off[t + 2] - m0 <= kWin;
+        const uint32_t* exn = wn ? sh.w.p.ex[buf ^ 1u] : L.extra_key + m0;
+        const float* cn = wn ? sh.w.p.cost[buf ^ 1u] : nullptr;
+        for (uint64_t k = k0 + tid; k < k1; k += kThreads) relax(k, exn, cn, m0);
         __syncthreads();
       }
     }
@@ -253,10 +271,13 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
       for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
         if (!level_present(mask, (uint32_t)lvl)) continue;
         for (uint64_t k = x0 + tid; k < x1; k += kThreads)
-          if (L.link_lvl[k] == (uint8_t)lvl) relax_link(L, k);
+          if (L.link_lvl[k] == (uint8_t)lvl) relax(k, ex, win ? sh.w.p.cost[buf] : nullptr, n0);
         __syncthreads();
       }
+    if (win)
+      for (uint32_t i = tid; i < nt; i += kThreads) L.extra_key[n0 + i] = ex[i];
   }
+  __syncthreads();
 
   // ------------------------------------------ kept links (final merge input)
   const uint32_t lb_key = cost_key(prm.lattice_beam);
@@ -304,19 +325,21 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
     }
     start_node = lo;
   }
-  for (uint64_t n = tid; n < nnodes; n += kThreads) {
-    L.alpha[n] = (n == start_node) ? 0.0 : INFINITY;
-    double b = INFINITY;
-    if (n >= nT0) b = final_used ? (double)g.final_w[L.n_state[n]] : 0.0;
-    L.beta[n] = b;
-  }
-  __syncthreads();
+  // alpha: frames ascending, epsilon links of a frame by source level
   for (int t = 0; t <= T; ++t) {
+    const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
+    const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
+    const bool win = nt <= kWin;
+    double* a = win ? sh.w.ab[buf] : L.alpha + n0;
+    for (uint32_t i = tid; i < nt; i += kThreads) a[i] = (n0 + i == start_node) ? 0.0 : INFINITY;
+    __syncthreads();
     const uint64_t e0 = kf[2 * t], e1 = kf[2 * t + 1], e2 = kf[2 * t + 2];
     if (e1 > e0) {
+      const uint64_t m0 = L.node_off[t - 1];
+      const double* ap = (n0 - m0 <= kWin) ? sh.w.ab[buf ^ 1u] : L.alpha + m0;
       for (uint64_t j = e0 + tid; j < e1; j += kThreads) {
         const LinkView l = link_at(L, kid[j]);
-        atomic_logadd(&L.alpha[l.dst], L.alpha[l.src] + (double)g.weight_id[l.arc] + link_ac(L, g, t, l.arc));
+        atomic_logadd(&a[l.dst - n0], ap[l.src - m0] + (double)g.weight_id[l.arc] + link_ac(L, g, t, l.arc));
       }
       __syncthreads();
     }
@@ -328,20 +351,33 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
           const uint64_t k = kid[j];
           if (L.link_lvl[k] != (uint8_t)lvl) continue;
           const LinkView l = link_at(L, k);
-          atomic_logadd(&L.alpha[l.dst], L.alpha[l.src] + (double)g.weight_id[l.arc]);
+          atomic_logadd(&a[l.dst - n0], a[l.src - n0] + (double)g.weight_id[l.arc]);
         }
         __syncthreads();
       }
     }
+    if (win)
+      for (uint32_t i = tid; i < nt; i += kThreads) L.alpha[n0 + i] = a[i];
   }
+  __syncthreads();
+  // beta: frames descending, epsilon links of a frame from the highest level
   for (int t = T; t >= 0; --t) {
+    const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
+    const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
+    const bool win = nt <= kWin;
+    double* b = win ? sh.w.ab[buf] : L.beta + n0;
+    for (uint32_t i = tid; i < nt; i += kThreads)
+      b[i] = t == T ? (final_used ? (double)g.final_w[L.n_state[n0 + i]] : 0.0) : INFINITY;
+    __syncthreads();
     if (t < T) {
       const uint64_t e0 = kf[2 * t + 2], e1 = kf[2 * t + 3];
       if (e1 > e0) {
+        const uint64_t m0 = L.node_off[t + 1];
+        const double* bn = (L.node_off[t + 2] - m0 <= kWin) ? sh.w.ab[buf ^ 1u] : L.beta + m0;
         for (uint64_t j = e0 + tid; j < e1; j += kThreads) {
           const LinkView l = link_at(L, kid[j]);
-          atomic_logadd(&L.beta[l.src],
-                        (double)g.weight_id[l.arc] + link_ac(L, g, t + 1, l.arc) + L.beta[l.dst]);
+          atomic_logadd(&b[l.src - n0],
+                        (double)g.weight_id[l.arc] + link_ac(L, g, t + 1, l.arc) + bn[l.dst - m0]);
         }
         __syncthreads();
       }
@@ -355,12 +391,15 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
           const uint64_t k = kid[j];
           if (L.link_lvl[k] != (uint8_t)lvl) continue;
           const LinkView l = link_at(L, k);
-          atomic_logadd(&L.beta[l.src], (double)g.weight_id[l.arc] + L.beta[l.dst]);
+          atomic_logadd(&b[l.src - n0], (double)g.weight_id[l.arc] + b[l.dst - n0]);
         }
         __syncthreads();
       }
     }
+    if (win)
+      for (uint32_t i = tid; i < nt; i += kThreads) L.beta[n0 + i] = b[i];
   }
+  __syncthreads();
   const double Z = L.beta[start_node];
 
   // ------------------------------------------- final merge of the kept links
