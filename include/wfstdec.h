@@ -74,6 +74,16 @@ typedef struct {
  * caller's stream and report them in wd_stats (whole launch: all utterances
  * of a batch). */
 #define WD_FLAG_TIMING 2u
+/* Execution mode.  One workgroup per utterance runs every frame inside one
+ * launch: best while frames hold up to a few thousand tokens.  Chip-wide mode
+ * runs every step of a frame as a kernel over the whole GPU (1024 workgroups
+ * per utterance, launched frame by frame on the caller's stream): for frames
+ * of 10^5..10^6 tokens.  Results are identical.  With neither flag the
+ * library picks chip-wide when max_active is 0 (no limit) or at least
+ * WD_CHIP_WIDE_MAX_ACTIVE, else one workgroup.  Both flags: WD_EINVAL. */
+#define WD_FLAG_ONE_WORKGROUP 4u
+#define WD_FLAG_CHIP_WIDE 8u
+#define WD_CHIP_WIDE_MAX_ACTIVE 32768
 
 /* Workspace capacities (per utterance).  0 selects a default.  A decode that
  * outgrows a capacity fails with WD_ECAPACITY and reports what it needed. */
@@ -132,8 +142,8 @@ typedef struct {
   int64_t kept_links;
   int64_t nodes;             /* lattice nodes returned */
   int64_t eps_arcs_expanded; /* the epsilon part of arcs_expanded */
-  float forward_ms;          /* WD_FLAG_TIMING: token-passing kernel time */
-  float lattice_ms;          /* WD_FLAG_TIMING: lattice kernel time */
+  float forward_ms;          /* WD_FLAG_TIMING: token-passing kernel time(s) */
+  float lattice_ms;          /* WD_FLAG_TIMING: lattice kernel time(s) */
   wd_caps needed;            /* capacities this decode needed (also on WD_ECAPACITY) */
 } wd_stats;
 

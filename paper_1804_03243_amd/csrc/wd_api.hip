@@ -64,6 +64,7 @@ struct Regions {
   unsigned long long* slot;
   uint32_t* bitmap;
   uint32_t* used;
+  void* grid;
   uint64_t bitmap_words, used_words;
   uint64_t total;
 };
@@ -83,6 +84,7 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
   R.desc = (LaneDesc*)take(sizeof(LaneDesc));
   R.info = (LaneInfo*)take(sizeof(LaneInfo));
   R.bad = (uint32_t*)take(sizeof(uint32_t));
+  R.grid = take(grid_lane_bytes());
   R.bitmap_words = (S + 31) / 32;
   R.used_words = (c.nodes + 31) / 32 + 1;
   char* slot = take(8 * S);
@@ -189,6 +191,8 @@ wd_status check_params(const wd_params* p) {
   if (!(p->beam > 0.0f)) return fail(WD_EINVAL, "decode: beam must be > 0");
   if (p->max_active < 0) return fail(WD_EINVAL, "decode: max_active must be >= 0");
   if (!(p->lattice_beam >= 0.0f)) return fail(WD_EINVAL, "decode: lattice_beam must be >= 0");
+  if ((p->flags & WD_FLAG_ONE_WORKGROUP) && (p->flags & WD_FLAG_CHIP_WIDE))
+    return fail(WD_EINVAL, "decode: WD_FLAG_ONE_WORKGROUP and WD_FLAG_CHIP_WIDE are exclusive");
   return WD_OK;
 }
 
@@ -272,10 +276,23 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
   if (timing)
     for (auto& e : ev)
       if ((st = hip_check(hipEventCreate(&e), "event"))) return st;
+  // execution mode: chip-wide kernels per frame for frames too large for one
+  // workgroup (no max-active limit, or a very large one)
+  const bool chip_wide =
+      (p->flags & WD_FLAG_CHIP_WIDE) ||
+      (!(p->flags & WD_FLAG_ONE_WORKGROUP) && (p->max_active == 0 || p->max_active >= WD_CHIP_WIDE_MAX_ACTIVE));
   if (timing) (void)hipEventRecord(ev[0], s);
-  launch_forward(g->dg, R.desc, B, prm, R.bad, s);
+  if (chip_wide) launch_grid_forward(g->dg, R.desc, R.grid, B, prm, R.bad, max_T, s);
+  else launch_forward(g->dg, R.desc, B, prm, R.bad, s);
   if (timing) (void)hipEventRecord(ev[1], s);
-  launch_lattice(g->dg, R.desc, B, prm, s);
+  if (chip_wide) {
+    launch_grid_sweep(g->dg, R.desc, R.grid, B, max_T, s);
+    Params lp = prm;
+    lp.flags |= kFlagSwept;
+    launch_lattice(g->dg, R.desc, B, lp, s);
+  } else {
+    launch_lattice(g->dg, R.desc, B, prm, s);
+  }
   if (timing) (void)hipEventRecord(ev[2], s);
   if ((st = hip_check(hipGetLastError(), "launch"))) return st;
   std::vector<LaneInfo> info((size_t)B);

@@ -101,6 +101,9 @@ struct LaneInfo {
 };
 
 enum : uint32_t { kOvfFrame = 1, kOvfArcs = 2, kOvfNodes = 4, kOvfLinks = 8, kOvfKept = 16 };
+// Params::flags bit set by the host for the lattice kernel when the pruning
+// sweep already ran as chip-wide kernels.
+constexpr uint32_t kFlagSwept = 1u << 30;
 // LaneInfo::status value for an internal consistency failure caught by a
 // kernel's own bounds checks (reported as WD_EDEVICE).
 constexpr int32_t kStatusInternal = 5;

@@ -1,0 +1,853 @@
+// Chip-wide mode for utterances whose frames hold hundreds of thousands of
+// tokens (wide beams, no max-active limit).
+//
+// The same per-frame steps as the one-workgroup forward pass (Sec. 3.2-3.4),
+// each a kernel over 1024 workgroups per utterance, launched frame by frame on
+// the caller's stream: emitting expansion with 64-bit atomicMin recombination
+// on the per-state slot array (Alg. 1) over the prefix-sum work space of
+// Sec. 3.3; one kernel per epsilon level; survivors of the beam cutoff with a
+// global radix histogram for max-active; compaction in state order through the
+// state bitmap; degree prefix sums; lattice links (Sec. 3.4).  Every position
+// (frontier, links) comes from a two-level scan: per-workgroup sums, one
+// workgroup scanning the sums, a per-workgroup rescan.  Frontier and link
+// order are therefore the same as in the one-workgroup pass and the result is
+// identical.  The backward pruning sweep of Sec. 3.5 has a chip-wide form too.
+// Every kernel reads the frame's sizes from device memory, so the host never
+// waits between frames; an utterance whose status is set skips the rest.
+#include "wd_block.h"
+
+namespace wd {
+
+constexpr int kGT = 256;          // threads per workgroup
+constexpr int kGW = kGT / 64;     // wavefronts per workgroup
+constexpr uint32_t kGB = 1024;    // workgroups per utterance
+constexpr uint32_t kSeg = 4096;   // frontier prefix sums a workgroup keeps in LDS
+
+// Per-utterance state carried from kernel to kernel.
+struct GridLane {
+  uint32_t stop;        // nonzero: skip every later kernel
+  int32_t status;
+  uint32_t ovf;
+  uint32_t hist_ok;     // nodes and links still being stored
+  uint32_t bad;         // a consistency check failed
+  uint32_t frames;      // frames finished
+  uint32_t W, n_prev, W_next, W_eps;
+  uint32_t n_touched, n_surv, n_keep;
+  uint32_t best_key, kcutb, cut_key;
+  uint32_t nbits, shift;
+  uint32_t sel_active, sel_rank, sel_prefix, sel_less, sel_bits;
+  uint32_t xmask;
+  uint32_t final_used, best_total_key;
+  uint64_t node_base, node_base_prev, link_base;
+  uint64_t arcs, eps_arcs, tokens, max_tokens, need_frame, need_arcs;
+  uint32_t nb[kMaxLevels + 1];
+  uint32_t hist[kHistBins];
+  // per-workgroup partial sums, then their exclusive prefix (+ total at kGB):
+  // [0] frontier counts, [1] degree sums, [2] link counts
+  unsigned long long part[3][kGB + 1];
+};
+
+// ------------------------------------------------------- workgroup collectives
+
+struct GScratch {
+  unsigned long long w[kGW];
+};
+
+__device__ __forceinline__ unsigned long long gsum64(unsigned long long v, GScratch& s) {
+#pragma unroll
+  for (int m = 32; m > 0; m >>= 1) v += shfl_xor64(v, m);
+  __syncthreads();
+  if (lane_id() == 0) s.w[wave_id()] = v;
+  __syncthreads();
+  unsigned long long r = 0;
+#pragma unroll
+  for (int i = 0; i < kGW; ++i) r += s.w[i];
+  return r;
+}
+
+__device__ __forceinline__ unsigned long long gexcl64(unsigned long long v, GScratch& s,
+                                                      unsigned long long* total) {
+  const unsigned long long inc = wave_incl_scan64(v);
+  __syncthreads();
+  if (lane_id() == 63) s.w[wave_id()] = inc;
+  __syncthreads();
+  unsigned long long before = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kGW; ++i) {
+    before += (uint32_t)i < wave_id() ? s.w[i] : 0ull;
+    tot += s.w[i];
+  }
+  *total = tot;
+  return before + inc - v;
+}
+
+__device__ __forceinline__ unsigned long long gmin64(unsigned long long v, GScratch& s) {
+#pragma unroll
+  for (int m = 32; m > 0; m >>= 1) {
+    const unsigned long long o = shfl_xor64(v, m);
+    v = o < v ? o : v;
+  }
+  __syncthreads();
+  if (lane_id() == 0) s.w[wave_id()] = v;
+  __syncthreads();
+  unsigned long long r = s.w[0];
+#pragma unroll
+  for (int i = 1; i < kGW; ++i) r = s.w[i] < r ? s.w[i] : r;
+  return r;
+}
+
+// [lo, hi) of workgroup b when n items are cut into kGB contiguous chunks.
+__device__ __forceinline__ void chunk(uint64_t n, uint32_t b, uint64_t* lo, uint64_t* hi) {
+  const uint64_t per = (n + kGB - 1) / kGB;
+  const uint64_t a = (uint64_t)b * per;
+  *lo = a < n ? a : n;
+  *hi = a + per < n ? a + per : n;
+}
+
+// [lo, hi) of this thread inside the workgroup's [blo, bhi).
+__device__ __forceinline__ void sub_chunk(uint64_t blo, uint64_t bhi, uint64_t* lo, uint64_t* hi) {
+  const uint64_t n = bhi - blo, per = (n + kGT - 1) / kGT;
+  const uint64_t a = (uint64_t)threadIdx.x * per;
+  *lo = blo + (a < n ? a : n);
+  *hi = blo + (a + per < n ? a + per : n);
+}
+
+// The frontier entries that own the work items [lo, hi) (lo < hi <= a[n]) of
+// the exclusive prefix array a[0..n]: a[pl..pl+m), copied to LDS when it fits.
+struct Seg {
+  uint32_t pl, m;
+  bool lds;
+};
+
+__device__ __forceinline__ Seg load_seg(const uint32_t* a, uint32_t n, uint32_t lo, uint32_t hi,
+                                        uint32_t* seg, uint32_t* rng) {
+  if (threadIdx.x < 2) rng[threadIdx.x] = search_le(a, n, threadIdx.x ? hi - 1u : lo);
+  __syncthreads();
+  Seg r;
+  r.pl = rng[0];
+  r.m = rng[1] - rng[0] + 1u;
+  r.lds = r.m <= kSeg;
+  if (r.lds)
+    for (uint32_t i = threadIdx.x; i < r.m; i += kGT) seg[i] = a[r.pl + i];
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ uint32_t seg_find(const Seg& sg, const uint32_t* seg, const uint32_t* a, uint32_t w) {
+  return sg.pl + (sg.lds ? search_le(seg, sg.m, w) : search_le(a + sg.pl, sg.m, w));
+}
+
+// Exclusive scan of the kGB partial sums part[which] of each utterance.
+__global__ void __launch_bounds__(kGT) k_g_scan(GridLane* gl, int which) {
+  __shared__ GScratch s;
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  unsigned long long* part = G.part[which];
+  constexpr uint32_t per = kGB / kGT;
+  unsigned long long v[per], sum = 0;
+#pragma unroll
+  for (uint32_t i = 0; i < per; ++i) {
+    v[i] = part[threadIdx.x * per + i];
+    sum += v[i];
+  }
+  unsigned long long tot;
+  unsigned long long ex = gexcl64(sum, s, &tot);
+#pragma unroll
+  for (uint32_t i = 0; i < per; ++i) {
+    part[threadIdx.x * per + i] = ex;
+    ex += v[i];
+  }
+  if (threadIdx.x == 0) part[kGB] = tot;
+}
+
+// ---------------------------------------------------------------- forward pass
+
+__global__ void k_g_init(const LaneDesc* __restrict__ lanes, GridLane* gl, const uint32_t* __restrict__ bad) {
+  GridLane& G = gl[blockIdx.y];
+  uint32_t* w = reinterpret_cast<uint32_t*>(&G);
+  for (uint32_t i = threadIdx.x; i < (uint32_t)(sizeof(GridLane) / 4); i += blockDim.x) w[i] = 0;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    G.hist_ok = 1;
+    if (bad[blockIdx.y]) {
+      G.status = 1;  // WD_EINVAL
+      G.stop = 1;
+      lanes[blockIdx.y].info->status = 1;
+    }
+  }
+}
+
+// Frame start: the start token (t = 0) or the emitting work check (t > 0).
+__global__ void k_g_begin(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl, int t) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop || threadIdx.x != 0) return;
+  if (t == 0) {
+    const uint32_t s0 = g.start;
+    L.slot[s0] = pack_tok(cost_key(0.0f), kNoArc);
+    L.touched[0] = s0;
+    G.n_touched = 1;
+    const uint32_t c = g.sclass[s0];
+    if (c != kNoEps) {
+      L.bucket[g.level_base[c]] = s0;
+      G.nb[c] = 1;
+    }
+    G.best_key = cost_key(0.0f);
+    return;
+  }
+  G.need_arcs = G.W > G.need_arcs ? G.W : G.need_arcs;
+  if (G.W > L.cand_cap) {
+    G.status = 4;  // WD_ECAPACITY
+    G.ovf |= kOvfArcs;
+    G.stop = 1;
+    return;
+  }
+  G.arcs += G.W;
+  G.best_key = 0xffffffffu;
+}
+
+// Emitting expansion of frame t: work item w is arc w - edeg[i] of frontier
+// token i of frame t-1.  Writes the candidate of every work item.
+__global__ void __launch_bounds__(kGT) k_g_expand(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                  GridLane* gl, int t) {
+  __shared__ GScratch s;
+  __shared__ uint32_t seg[kSeg];
+  __shared__ uint32_t rng[2];
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop || t == 0) return;
+  const uint32_t W = G.W, n_prev = G.n_prev;
+  const uint64_t nbp = G.node_base_prev;
+  const float* row = L.ll + (size_t)(t - 1) * g.P;
+  uint64_t blo, bhi;
+  chunk(W, blockIdx.x, &blo, &bhi);
+  uint32_t my_best = 0xffffffffu;
+  if (blo < bhi) {
+    const Seg sg = load_seg(L.f_edeg, n_prev, (uint32_t)blo, (uint32_t)bhi, seg, rng);
+    for (uint64_t base = blo; base < bhi; base += kGT) {
+      const uint32_t w = (uint32_t)base + threadIdx.x;
+      bool first = false;
+      uint32_t dst = 0, cls = kNoEps;
+      if (w < bhi) {
+        const uint32_t i = seg_find(sg, seg, L.f_edeg, w);
+        const float c = key_cost(L.f_key[i]);
+        const uint4 r = g.earc[L.f_ebeg[i] + (w - L.f_edeg[i])];
+        dst = r.x;
+        cls = r.z >> 24;
+        const float ac = -row[(r.z & 0xffffffu) - 1u];
+        float x = c + ac;
+        x = canon(x + __uint_as_float(r.y));
+        const uint32_t xk = cost_key(x);
+        if (xk < kInfKey) {
+          const unsigned long long old = atomicMin(&L.slot[dst], pack_tok(xk, r.w));
+          first = old == kEmpty;
+          my_best = xk < my_best ? xk : my_best;
+        }
+        L.cand[w] = make_uint4(r.w, (uint32_t)(nbp + i), dst, __float_as_uint(x));
+      }
+      const uint32_t pos = wave_append(first, &G.n_touched);
+      if (first) {
+        if (pos < L.frame_cap) L.touched[pos] = dst;
+        if (cls != kNoEps) L.bucket[g.level_base[cls] + atomicAdd(&G.nb[cls], 1u)] = dst;
+      }
+    }
+  }
+  my_best = (uint32_t)gmin64(my_best, s);
+  if (threadIdx.x == 0 && my_best != 0xffffffffu) atomicMin(&G.best_key, my_best);
+}
+
+// Beam cutoff from the best emitting candidate (inclusive).
+__global__ void k_g_cut(GridLane* gl, Params prm) {
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop || threadIdx.x != 0) return;
+  if (G.best_key >= kInfKey) {
+    G.status = 3;  // WD_ENOPATH
+    G.stop = 1;
+    return;
+  }
+  G.kcutb = cost_key(key_cost(G.best_key) + prm.beam);
+}
+
+// Epsilon closure, level `lvl`: states of that level within the cutoff relax
+// their epsilon arcs; destinations sit on higher levels.
+__global__ void __launch_bounds__(kGT) k_g_level(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                 GridLane* gl, uint32_t lvl) {
+  __shared__ GScratch s;
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  const uint32_t n = G.nb[lvl];
+  if (n == 0) return;
+  const uint32_t kcutb = G.kcutb;
+  const uint32_t* bk = L.bucket + g.level_base[lvl];
+  unsigned long long eps = 0;
+  for (uint32_t i = blockIdx.x * kGT + threadIdx.x; i < n; i += kGB * kGT) {
+    const uint32_t st = bk[i];
+    const uint32_t k = (uint32_t)(L.slot[st] >> 32);
+    if (k > kcutb) continue;
+    const float c = key_cost(k);
+    const uint32_t a0 = g.off[st].y, a1 = g.off[st + 1].y;
+    eps += a1 - a0;
+    for (uint32_t a = a0; a < a1; ++a) {
+      const uint4 r = g.xarc[a];
+      const uint32_t xk = cost_key(canon(c + __uint_as_float(r.y)));
+      if (xk > kcutb || xk >= kInfKey) continue;
+      const unsigned long long old = atomicMin(&L.slot[r.x], pack_tok(xk, r.w));
+      if (old == kEmpty) {
+        const uint32_t pos = atomicAdd(&G.n_touched, 1u);
+        if (pos < L.frame_cap) L.touched[pos] = r.x;
+        if (r.z != kNoEps) L.bucket[g.level_base[r.z] + atomicAdd(&G.nb[r.z], 1u)] = r.x;
+      }
+    }
+  }
+  eps = gsum64(eps, s);
+  if (threadIdx.x == 0 && eps) atomicAdd((unsigned long long*)&G.eps_arcs, eps);
+}
+
+// After the closure: frame capacity and the digit layout of the histogram.
+__global__ void k_g_check(const LaneDesc* __restrict__ lanes, GridLane* gl) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop || threadIdx.x != 0) return;
+  const uint32_t nt = G.n_touched;
+  G.need_frame = nt > G.need_frame ? nt : G.need_frame;
+  if (nt > L.frame_cap) {
+    G.status = 4;
+    G.ovf |= kOvfFrame;
+    G.stop = 1;
+    return;
+  }
+  const uint32_t span = G.kcutb - G.best_key;
+  G.nbits = span ? 32u - (uint32_t)__clz(span) : 0u;
+  G.shift = G.nbits > 11u ? G.nbits - 11u : 0u;
+}
+
+// Survivors of the beam cutoff; resets the touched slots; histogram of the
+// top cost-key digit when max-active is on.  Costs never fall below the best
+// emitting candidate (weights are >= 0), so the digit is in range.
+__global__ void __launch_bounds__(kGT) k_g_count(const LaneDesc* __restrict__ lanes, GridLane* gl,
+                                                 Params prm) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  const uint32_t nt = G.n_touched, kcutb = G.kcutb, best = G.best_key, shift = G.shift;
+  const bool hist = prm.max_active > 0;
+  for (uint32_t base = blockIdx.x * kGT; base < nt; base += kGB * kGT) {
+    const uint32_t i = base + threadIdx.x;
+    bool keep = false;
+    uint32_t st = 0;
+    unsigned long long v = kEmpty;
+    if (i < nt) {
+      st = L.touched[i];
+      v = L.slot[st];
+      L.slot[st] = kEmpty;
+      keep = (uint32_t)(v >> 32) <= kcutb;
+    }
+    const uint32_t pos = wave_append(keep, &G.n_surv);
+    if (keep) {
+      L.surv_state[pos] = st;
+      L.surv_pack[pos] = v;
+      if (hist) atomicAdd(&G.hist[((uint32_t)(v >> 32) - best) >> shift], 1u);
+    }
+  }
+}
+
+// Max-active by radix select: step 0 decides whether the limit binds; every
+// step finds the histogram bin holding the rank-th smallest key and narrows
+// the prefix by one digit (11, 11 and 10 bits at most).
+__global__ void __launch_bounds__(kGT) k_g_select(GridLane* gl, Params prm, int step) {
+  __shared__ GScratch s;
+  __shared__ uint32_t sel[2];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  if (step == 0) {
+    if (threadIdx.x == 0) {
+      const uint32_t ns = G.n_surv;
+      G.cut_key = G.kcutb;
+      G.n_keep = ns;
+      G.sel_active = prm.max_active > 0 && ns > (uint32_t)prm.max_active;
+      G.sel_rank = (uint32_t)prm.max_active;
+      G.sel_prefix = 0;
+      G.sel_less = 0;
+      G.sel_bits = G.nbits - G.shift;
+    }
+    __syncthreads();
+  }
+  if (!G.sel_active) return;
+  constexpr uint32_t per = kHistBins / kGT;
+  uint32_t h[per], sum = 0;
+#pragma unroll
+  for (uint32_t i = 0; i < per; ++i) {
+    h[i] = G.hist[threadIdx.x * per + i];
+    sum += h[i];
+  }
+  unsigned long long tot;
+  uint32_t ex = (uint32_t)gexcl64(sum, s, &tot);
+  const uint32_t rank = G.sel_rank;
+#pragma unroll
+  for (uint32_t i = 0; i < per; ++i) {
+    if (ex < rank && rank <= ex + h[i]) {
+      sel[0] = threadIdx.x * per + i;
+      sel[1] = ex;
+    }
+    ex += h[i];
+  }
+  __syncthreads();
+  const uint32_t b = sel[0], before = sel[1], cnt = G.hist[b];
+  __syncthreads();
+  for (uint32_t i = threadIdx.x; i < (uint32_t)kHistBins; i += kGT) G.hist[i] = 0;
+  if (threadIdx.x == 0) {
+    G.sel_prefix = (G.sel_prefix << G.sel_bits) | b;
+    G.sel_less += before;
+    G.sel_rank = rank - before;
+    if (G.shift == 0) {
+      const uint32_t vkey = G.best_key + G.sel_prefix;
+      G.cut_key = vkey < G.kcutb ? vkey : G.kcutb;
+      G.n_keep = G.sel_less + cnt;
+      G.sel_active = 0;
+    } else {
+      const uint32_t nsh = G.shift > 11u ? G.shift - 11u : 0u;
+      G.sel_bits = G.shift - nsh;
+      G.shift = nsh;
+    }
+  }
+}
+
+// Histogram of the next digit over the survivors matching the prefix.
+__global__ void __launch_bounds__(kGT) k_g_select_hist(const LaneDesc* __restrict__ lanes, GridLane* gl) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop || !G.sel_active) return;
+  const uint32_t ns = G.n_surv, best = G.best_key, prefix = G.sel_prefix, bits = G.sel_bits;
+  const uint32_t nsh = G.shift, osh = nsh + bits;
+  for (uint32_t i = blockIdx.x * kGT + threadIdx.x; i < ns; i += kGB * kGT) {
+    const uint32_t d = (uint32_t)(L.surv_pack[i] >> 32) - best;
+    if ((d >> osh) == prefix) atomicAdd(&G.hist[(d >> nsh) & ((1u << bits) - 1u)], 1u);
+  }
+}
+
+// Kept tokens mark their state in the bitmap; idx[state] = survivor index.
+__global__ void __launch_bounds__(kGT) k_g_mark(const LaneDesc* __restrict__ lanes, GridLane* gl) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  const uint32_t ns = G.n_surv, cut = G.cut_key;
+  if (blockIdx.x == 0 && threadIdx.x == 0 && G.hist_ok && G.node_base + G.n_keep > L.node_cap) {
+    G.hist_ok = 0;
+    G.ovf |= kOvfNodes;
+  }
+  for (uint32_t i = blockIdx.x * kGT + threadIdx.x; i < ns; i += kGB * kGT) {
+    const unsigned long long v = L.surv_pack[i];
+    if ((uint32_t)(v >> 32) <= cut) {
+      const uint32_t st = L.surv_state[i];
+      L.idx[st] = i;
+      atomicOr(&L.bitmap[st >> 5], 1u << (st & 31u));
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kGT) k_g_bits(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl) {
+  __shared__ GScratch s;
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  uint64_t blo, bhi, lo, hi;
+  chunk((g.S + 31u) >> 5, blockIdx.x, &blo, &bhi);
+  sub_chunk(blo, bhi, &lo, &hi);
+  unsigned long long c = 0;
+  for (uint64_t w = lo; w < hi; ++w) c += (uint32_t)__popc(L.bitmap[w]);
+  c = gsum64(c, s);
+  if (threadIdx.x == 0) G.part[0][blockIdx.x] = c;
+}
+
+// The frontier in state order: node store, frontier arrays, idx[state] = node
+// id; per-workgroup (emitting, epsilon) out-degree sums of its frontier range.
+__global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                   GridLane* gl) {
+  __shared__ GScratch s;
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  uint64_t blo, bhi, lo, hi;
+  chunk((g.S + 31u) >> 5, blockIdx.x, &blo, &bhi);
+  sub_chunk(blo, bhi, &lo, &hi);
+  unsigned long long c = 0;
+  for (uint64_t w = lo; w < hi; ++w) c += (uint32_t)__popc(L.bitmap[w]);
+  unsigned long long tot;
+  uint64_t p = G.part[0][blockIdx.x] + gexcl64(c, s, &tot);
+  const uint64_t nb = G.node_base;
+  const bool store = G.hist_ok != 0;
+  unsigned long long deg = 0;
+  for (uint64_t w = lo; w < hi; ++w) {
+    uint32_t word = L.bitmap[w];
+    if (!word) continue;
+    L.bitmap[w] = 0;
+    while (word) {
+      const uint32_t b = (uint32_t)__ffs(word) - 1u;
+      word &= word - 1u;
+      const uint32_t st = ((uint32_t)w << 5) | b;
+      const unsigned long long v = L.surv_pack[L.idx[st]];
+      const uint64_t node = nb + p;
+      if (store) {
+        L.n_state[node] = st;
+        L.n_pack[node] = v;
+        L.n_pred[node] = kNoArc;
+      }
+      L.idx[st] = (uint32_t)node;
+      L.f_state[p] = st;
+      L.f_key[p] = (uint32_t)(v >> 32);
+      L.f_arc[p] = (uint32_t)v;
+      const uint2 o0 = g.off[st], o1 = g.off[st + 1];
+      deg += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
+      ++p;
+    }
+  }
+  deg = gsum64(deg, s);
+  if (threadIdx.x == 0) G.part[1][blockIdx.x] = deg;
+}
+
+// Degree prefix sums of the frontier: each workgroup rescans the frontier range
+// it compacted.
+__global__ void __launch_bounds__(kGT) k_g_degrees(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                   GridLane* gl) {
+  __shared__ GScratch s;
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  const uint64_t blo = G.part[0][blockIdx.x], bhi = G.part[0][blockIdx.x + 1];
+  const uint32_t n = (uint32_t)G.part[0][kGB];
+  uint64_t lo, hi;
+  sub_chunk(blo, bhi, &lo, &hi);
+  unsigned long long c = 0;
+  for (uint64_t p = lo; p < hi; ++p) {
+    const uint32_t st = L.f_state[p];
+    const uint2 o0 = g.off[st], o1 = g.off[st + 1];
+    c += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
+  }
+  unsigned long long tot;
+  unsigned long long q = G.part[1][blockIdx.x] + gexcl64(c, s, &tot);
+  for (uint64_t p = lo; p < hi; ++p) {
+    const uint32_t st = L.f_state[p];
+    const uint2 o0 = g.off[st], o1 = g.off[st + 1];
+    L.f_edeg[p] = (uint32_t)q;
+    L.f_xdeg[p] = (uint32_t)(q >> 32);
+    L.f_ebeg[p] = o0.x;
+    L.f_xbeg[p] = o0.y;
+    L.f_cls[p] = g.sclass[st];
+    q += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    const unsigned long long all = G.part[1][kGB];
+    if (n != G.n_keep) G.bad = 1;
+    G.W_next = (uint32_t)all;
+    G.W_eps = (uint32_t)(all >> 32);
+    L.f_edeg[n] = (uint32_t)all;
+    L.f_xdeg[n] = (uint32_t)(all >> 32);
+  }
+}
+
+// Lattice links of frame t over one item space: [0, W) the emitting
+// candidates (arc-id order), [W, W + W_eps) the epsilon out-arcs of the
+// frontier (arc-id order).  A link exists where the candidate is within the
+// final cutoff.
+struct LinkItem {
+  uint32_t arc, src, dst, xbits, lvl;
+};
+
+__device__ __forceinline__ bool link_item(const DevGraph& g, const LaneDesc& L, uint32_t W, uint32_t cut,
+                                          uint32_t it, const Seg& sg, const uint32_t* seg, LinkItem* o) {
+  if (it < W) {
+    const uint4 c = L.cand[it];
+    const uint32_t xk = cost_key(__uint_as_float(c.w));
+    *o = LinkItem{c.x, c.y, c.z, c.w, 0};
+    return xk <= cut && xk < kInfKey;
+  }
+  const uint32_t e = it - W;
+  const uint32_t p = seg_find(sg, seg, L.f_xdeg, e);
+  const uint4 r = g.xarc[L.f_xbeg[p] + (e - L.f_xdeg[p])];
+  const float x = canon(key_cost(L.f_key[p]) + __uint_as_float(r.y));
+  const uint32_t xk = cost_key(x);
+  *o = LinkItem{r.w, p, r.x, __float_as_uint(x), L.f_cls[p]};  // src: frontier position
+  return xk <= cut && xk < kInfKey;
+}
+
+// Epsilon segment of a workgroup's item range [blo, bhi) (none below W).
+__device__ __forceinline__ Seg link_seg(const LaneDesc& L, uint32_t W, uint32_t n, uint64_t blo, uint64_t bhi,
+                                        uint32_t* seg, uint32_t* rng) {
+  if (bhi <= W) return Seg{0, 0, true};
+  const uint32_t e0 = (uint32_t)(blo > W ? blo - W : 0), e1 = (uint32_t)(bhi - W);
+  return load_seg(L.f_xdeg, n, e0, e1, seg, rng);
+}
+
+__global__ void __launch_bounds__(kGT) k_g_link_count(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                      GridLane* gl, int t) {
+  __shared__ GScratch s;
+  __shared__ uint32_t seg[kSeg];
+  __shared__ uint32_t rng[2];
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  const uint32_t W = t > 0 ? G.W : 0, n = G.n_keep, cut = G.cut_key;
+  uint64_t blo, bhi;
+  chunk((uint64_t)W + G.W_eps, blockIdx.x, &blo, &bhi);
+  unsigned long long c = 0;
+  if (blo < bhi) {
+    const Seg sg = link_seg(L, W, n, blo, bhi, seg, rng);
+    for (uint64_t it = blo + threadIdx.x; it < bhi; it += kGT) {
+      LinkItem o;
+      if (link_item(g, L, W, cut, (uint32_t)it, sg, seg, &o)) c += it < W ? 1ull : (1ull << 32);
+    }
+  }
+  c = gsum64(c, s);
+  if (threadIdx.x == 0) G.part[2][blockIdx.x] = c;
+}
+
+// Writes the links in item order: per 256-item tile a workgroup scan of the
+// (emitting, epsilon) flags.  Sets the predecessor node of each token from
+// the link that produced it (same cost key and arc id).
+__global__ void __launch_bounds__(kGT) k_g_link_write(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                      GridLane* gl, int t) {
+  __shared__ GScratch s;
+  __shared__ uint32_t seg[kSeg];
+  __shared__ uint32_t rng[2];
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  const uint32_t W = t > 0 ? G.W : 0, n = G.n_keep, cut = G.cut_key;
+  const unsigned long long all = G.part[2][kGB];
+  const uint64_t nE = (uint32_t)all;
+  const uint64_t lb = G.link_base, nb = G.node_base;
+  if (!G.hist_ok || lb + nE + (all >> 32) > L.link_cap) return;
+  uint64_t blo, bhi;
+  chunk((uint64_t)W + G.W_eps, blockIdx.x, &blo, &bhi);
+  if (blo >= bhi) return;
+  const Seg sg = link_seg(L, W, n, blo, bhi, seg, rng);
+  unsigned long long run = G.part[2][blockIdx.x];
+  uint32_t xm = 0, bad = 0;
+  for (uint64_t base = blo; base < bhi; base += kGT) {
+    const uint64_t it = base + threadIdx.x;
+    LinkItem o;
+    const bool on = it < bhi && link_item(g, L, W, cut, (uint32_t)it, sg, seg, &o);
+    const unsigned long long f = on ? (it < W ? 1ull : (1ull << 32)) : 0ull;
+    unsigned long long tile;
+    const unsigned long long ex = run + gexcl64(f, s, &tile);
+    run += tile;
+    if (!on) continue;
+    const uint32_t dn = L.idx[o.dst];
+    const uint32_t q = dn - (uint32_t)nb;
+    if ((uint64_t)dn < nb || q >= n) {
+      bad = 1;
+      continue;
+    }
+    const uint32_t xk = cost_key(__uint_as_float(o.xbits));
+    if (it < W) {
+      L.links[lb + (uint32_t)ex] = make_uint4(o.arc, o.src, dn, o.xbits);
+      if (L.f_key[q] == xk && L.f_arc[q] == o.arc) L.n_pred[dn] = o.src;
+    } else {
+      const uint64_t at = lb + nE + (ex >> 32);
+      const uint32_t sn = (uint32_t)(nb + o.src);
+      L.links[at] = make_uint4(o.arc, sn, dn, o.xbits);
+      L.link_lvl[at] = (uint8_t)o.lvl;
+      xm |= 1u << (o.lvl < 31u ? o.lvl : 31u);
+      if (L.f_key[q] == xk && L.f_arc[q] == o.arc) L.n_pred[dn] = sn;
+    }
+  }
+  if (xm) atomicOr(&G.xmask, xm);
+  if (bad) atomicOr(&G.bad, 1u);
+}
+
+// End of frame t: per-frame records, counters, and the state of frame t+1.
+__global__ void __launch_bounds__(kGT) k_g_end(const LaneDesc* __restrict__ lanes, GridLane* gl, int t) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop) return;
+  for (uint32_t i = threadIdx.x; i <= (uint32_t)kMaxLevels; i += kGT) G.nb[i] = 0;
+  for (uint32_t i = threadIdx.x; i < (uint32_t)kHistBins; i += kGT) G.hist[i] = 0;
+  if (threadIdx.x != 0) return;
+  if (G.bad) {
+    G.status = kStatusInternal;
+    G.stop = 1;
+    return;
+  }
+  const uint32_t n = G.n_keep;
+  const unsigned long long all = G.part[2][kGB];
+  const uint64_t nE = (uint32_t)all, nX = all >> 32;
+  if (G.hist_ok && G.link_base + nE + nX > L.link_cap) {
+    G.hist_ok = 0;
+    G.ovf |= kOvfLinks;
+  }
+  L.node_off[t] = G.node_base;
+  L.node_off[t + 1] = G.node_base + n;
+  L.link_off[t] = G.link_base;
+  L.link_xoff[t] = G.link_base + nE;
+  L.link_off[t + 1] = G.link_base + nE + nX;
+  L.xmask[t] = G.xmask;
+  L.best[t] = key_cost(G.best_key);
+  L.cutb[t] = key_cost(G.kcutb);
+  L.cut[t] = key_cost(G.cut_key);
+  G.tokens += n;
+  G.max_tokens = n > G.max_tokens ? n : G.max_tokens;
+  G.link_base += nE + nX;
+  G.node_base_prev = G.node_base;
+  G.node_base += n;
+  G.n_prev = n;
+  G.W = G.W_next;
+  G.n_touched = 0;
+  G.n_surv = 0;
+  G.xmask = 0;
+  G.frames = (uint32_t)t + 1u;
+  if (t == L.T) G.stop = 1;
+}
+
+// Final counters into the utterance's LaneInfo.
+__global__ void k_g_finish(const LaneDesc* __restrict__ lanes, GridLane* gl) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  const GridLane& G = gl[blockIdx.y];
+  if (threadIdx.x != 0 || G.status == 1) return;
+  LaneInfo* info = L.info;
+  int32_t status = G.status;
+  if (status == 0 && (G.ovf & (kOvfNodes | kOvfLinks))) status = 4;
+  info->status = status;
+  info->frames_done = (int32_t)G.frames;
+  info->overflow = G.ovf;
+  info->arcs_expanded = G.arcs + G.eps_arcs;
+  info->eps_arcs = G.eps_arcs;
+  info->tokens = G.tokens;
+  info->max_tokens = G.max_tokens;
+  info->links = G.link_base;
+  info->need_frame_tokens = G.need_frame;
+  info->need_frame_arcs = G.need_arcs;
+}
+
+// ------------------------------------------------------------- pruning sweep
+
+// Whether a final state was reached in the last frame, and the best final
+// cost.  One workgroup per utterance.
+__global__ void __launch_bounds__(kGT) k_gs_final(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                  GridLane* gl) {
+  __shared__ GScratch s;
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (L.info->status != 0) return;
+  const int T = L.T;
+  const uint64_t n0 = L.node_off[T], n1 = L.node_off[T + 1];
+  unsigned long long any = 0;
+  if (g.final_w)
+    for (uint64_t n = n0 + threadIdx.x; n < n1; n += kGT) {
+      const float fw = g.final_w[L.n_state[n]];
+      const float c = key_cost((uint32_t)(L.n_pack[n] >> 32));
+      any |= (fw < INFINITY && (c + fw) < INFINITY) ? 1ull : 0ull;
+    }
+  any = gsum64(any, s);
+  unsigned long long m = kEmpty;
+  for (uint64_t n = n0 + threadIdx.x; n < n1; n += kGT) {
+    const float c = key_cost((uint32_t)(L.n_pack[n] >> 32));
+    const float F = any ? canon(c + g.final_w[L.n_state[n]]) : c;
+    const unsigned long long v = pack_tok(cost_key(F), (uint32_t)(n - n0));
+    m = v < m ? v : m;
+  }
+  m = gmin64(m, s);
+  if (threadIdx.x == 0) {
+    G.final_used = any ? 1u : 0u;
+    G.best_total_key = (uint32_t)(m >> 32);
+  }
+}
+
+// Extra costs of frame t's nodes before relaxation: final extra cost for the
+// last frame, +inf otherwise.
+__global__ void __launch_bounds__(kGT) k_gs_init(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                 const GridLane* gl, int t) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  const GridLane& G = gl[blockIdx.y];
+  if (L.info->status != 0 || t > L.T || G.best_total_key >= kInfKey) return;
+  const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
+  const bool last = t == L.T;
+  const float best = key_cost(G.best_total_key);
+  for (uint64_t n = n0 + blockIdx.x * kGT + threadIdx.x; n < n1; n += (uint64_t)kGB * kGT) {
+    uint32_t e = kInfKey;
+    if (last) {
+      const float c = key_cost((uint32_t)(L.n_pack[n] >> 32));
+      const float F = G.final_used ? canon(c + g.final_w[L.n_state[n]]) : c;
+      if (F < INFINITY) e = cost_key(F - best);
+    }
+    L.extra_key[n] = e;
+  }
+}
+
+// Relaxes links into their source's extra cost: the emitting links that
+// leave frame t (emit != 0), or frame t's epsilon links whose source is on
+// level `lvl`.  extra(link) = extra(dst) + (x - cost(dst)).
+__global__ void __launch_bounds__(kGT) k_gs_relax(const LaneDesc* __restrict__ lanes, const GridLane* gl,
+                                                  int t, int emit, int lvl) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  if (L.info->status != 0 || t > L.T || gl[blockIdx.y].best_total_key >= kInfKey) return;
+  uint64_t k0, k1;
+  if (emit) {
+    if (t == L.T) return;
+    k0 = L.link_off[t + 1];
+    k1 = L.link_xoff[t + 1];
+  } else {
+    if (((L.xmask[t] >> (lvl < 31 ? lvl : 31)) & 1u) == 0) return;
+    k0 = L.link_xoff[t];
+    k1 = L.link_off[t + 1];
+  }
+  for (uint64_t k = k0 + blockIdx.x * kGT + threadIdx.x; k < k1; k += (uint64_t)kGB * kGT) {
+    if (!emit && L.link_lvl[k] != (uint8_t)lvl) continue;
+    const uint4 v = L.links[k];
+    const float exd = key_cost(L.extra_key[v.z]);
+    const float c = key_cost((uint32_t)(L.n_pack[v.z] >> 32));
+    const uint32_t le = cost_key(exd + (__uint_as_float(v.w) - c));
+    L.le_key[k] = le;
+    atomicMin(&L.extra_key[v.y], le);
+  }
+}
+
+// -------------------------------------------------------------------- launches
+
+size_t grid_lane_bytes() { return sizeof(GridLane); }
+
+void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, int B, const Params& prm,
+                         const uint32_t* bad, int maxT, hipStream_t st) {
+  GridLane* gl = (GridLane*)glv;
+  const dim3 one(1, B), all(kGB, B), blk(kGT);
+  hipLaunchKernelGGL(k_g_init, one, blk, 0, st, lanes, gl, bad);
+  for (int t = 0; t <= maxT; ++t) {
+    hipLaunchKernelGGL(k_g_begin, one, dim3(64), 0, st, g, lanes, gl, t);
+    hipLaunchKernelGGL(k_g_expand, all, blk, 0, st, g, lanes, gl, t);
+    hipLaunchKernelGGL(k_g_cut, one, dim3(64), 0, st, gl, prm);
+    for (uint32_t l = 0; l < g.nlevels; ++l) hipLaunchKernelGGL(k_g_level, all, blk, 0, st, g, lanes, gl, l);
+    hipLaunchKernelGGL(k_g_check, one, dim3(64), 0, st, lanes, gl);
+    hipLaunchKernelGGL(k_g_count, all, blk, 0, st, lanes, gl, prm);
+    hipLaunchKernelGGL(k_g_select, one, blk, 0, st, gl, prm, 0);
+    if (prm.max_active > 0)
+      for (int step = 1; step < 3; ++step) {
+        hipLaunchKernelGGL(k_g_select_hist, all, blk, 0, st, lanes, gl);
+        hipLaunchKernelGGL(k_g_select, one, blk, 0, st, gl, prm, step);
+      }
+    hipLaunchKernelGGL(k_g_mark, all, blk, 0, st, lanes, gl);
+    hipLaunchKernelGGL(k_g_bits, all, blk, 0, st, g, lanes, gl);
+    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, gl, 0);
+    hipLaunchKernelGGL(k_g_compact, all, blk, 0, st, g, lanes, gl);
+    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, gl, 1);
+    hipLaunchKernelGGL(k_g_degrees, all, blk, 0, st, g, lanes, gl);
+    hipLaunchKernelGGL(k_g_link_count, all, blk, 0, st, g, lanes, gl, t);
+    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, gl, 2);
+    hipLaunchKernelGGL(k_g_link_write, all, blk, 0, st, g, lanes, gl, t);
+    hipLaunchKernelGGL(k_g_end, one, blk, 0, st, lanes, gl, t);
+  }
+  hipLaunchKernelGGL(k_g_finish, one, dim3(64), 0, st, lanes, gl);
+}
+
+void launch_grid_sweep(const DevGraph& g, const LaneDesc* lanes, void* glv, int B, int maxT, hipStream_t st) {
+  GridLane* gl = (GridLane*)glv;
+  const dim3 one(1, B), all(kGB, B), blk(kGT);
+  hipLaunchKernelGGL(k_gs_final, one, blk, 0, st, g, lanes, gl);
+  for (int t = maxT; t >= 0; --t) {
+    hipLaunchKernelGGL(k_gs_init, all, blk, 0, st, g, lanes, gl, t);
+    hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, t, 1, 0);
+    for (int l = (int)g.nlevels - 1; l >= 0; --l)
+      hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, t, 0, l);
+  }
+}
+
+}  // namespace wd

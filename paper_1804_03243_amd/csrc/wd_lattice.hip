@@ -229,7 +229,8 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
   }
 
   // ------------------------------------------------ backward extra-cost sweep
-  for (int t = T; t >= 0; --t) {
+  const bool swept = (prm.flags & kFlagSwept) != 0;
+  for (int t = swept ? -1 : T; t >= 0; --t) {
     const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
     const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
     const bool win = nt <= kWin;

@@ -21,6 +21,10 @@ LIB_PATH = os.path.join(_HERE, "libwfstdec.so")
 WD_OK, WD_EINVAL, WD_ECYCLE, WD_ENOPATH, WD_ECAPACITY, WD_EDEVICE = range(6)
 WD_FLAG_DEBUG = 1
 WD_FLAG_TIMING = 2
+WD_FLAG_ONE_WORKGROUP = 4
+WD_FLAG_CHIP_WIDE = 8
+WD_CHIP_WIDE_MAX_ACTIVE = 32768
+_MODE_FLAGS = {"auto": 0, "workgroup": WD_FLAG_ONE_WORKGROUP, "chip": WD_FLAG_CHIP_WIDE}
 STATUS_NAMES = {0: "WD_OK", 1: "WD_EINVAL", 2: "WD_ECYCLE", 3: "WD_ENOPATH", 4: "WD_ECAPACITY",
                 5: "WD_EDEVICE"}
 
@@ -276,9 +280,12 @@ class Graph:
         return base, nbytes, used
 
 
-def _params(beam, max_active, lattice_beam, debug, timing=False):
+def _params(beam, max_active, lattice_beam, debug, timing=False, mode="auto"):
+    if mode not in _MODE_FLAGS:
+        raise ValueError(f"mode must be one of {sorted(_MODE_FLAGS)}")
     return wd_params(float(beam), int(max_active), float(lattice_beam),
-                     (WD_FLAG_DEBUG if debug else 0) | (WD_FLAG_TIMING if timing else 0))
+                     (WD_FLAG_DEBUG if debug else 0) | (WD_FLAG_TIMING if timing else 0) |
+                     _MODE_FLAGS[mode])
 
 
 def _grow(caps: wd_caps, needed: dict) -> wd_caps:
@@ -294,16 +301,18 @@ def _grow(caps: wd_caps, needed: dict) -> wd_caps:
 
 def decode_batch(graph: Graph, loglikes: list, beam: float, max_active: int, lattice_beam: float,
                  debug: bool = False, caps: wd_caps | None = None, max_retries: int = 12,
-                 timing: bool = False):
+                 timing: bool = False, mode: str = "auto"):
     """Decode utterances (device float32 tensors, T_i x P) concurrently.
-    Returns one result namespace per utterance."""
+    `mode`: "workgroup" (one workgroup per utterance), "chip" (chip-wide
+    kernels per frame) or "auto" (the library's choice).  Returns one result
+    namespace per utterance."""
     torch = _torch()
     for x in loglikes:
         if x.dtype != torch.float32 or not x.is_contiguous() or x.device != graph.device:
             raise ValueError("log-likelihoods must be contiguous float32 tensors on the graph's device")
         if x.dim() != 2 or x.shape[1] != graph.num_pdfs:
             raise ValueError(f"log-likelihoods must be T x {graph.num_pdfs}")
-    p = _params(beam, max_active, lattice_beam, debug, timing)
+    p = _params(beam, max_active, lattice_beam, debug, timing, mode)
     Ts = [int(x.shape[0]) for x in loglikes]
     key = (len(Ts), max(Ts), float(beam), int(max_active), float(lattice_beam), bool(debug))
     if caps is None:
@@ -331,7 +340,8 @@ def decode_batch(graph: Graph, loglikes: list, beam: float, max_active: int, lat
 
 
 def decode(graph: Graph, loglikes, beam: float, max_active: int, lattice_beam: float,
-           debug: bool = False, caps: wd_caps | None = None, timing: bool = False):
+           debug: bool = False, caps: wd_caps | None = None, timing: bool = False,
+           mode: str = "auto"):
     """Decode one utterance (device float32 tensor, T x P)."""
     return decode_batch(graph, [loglikes], beam, max_active, lattice_beam, debug, caps,
-                        timing=timing)[0]
+                        timing=timing, mode=mode)[0]

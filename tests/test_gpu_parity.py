@@ -3,7 +3,8 @@ inputs: 1-best words, cost, every lattice link and node bit for bit,
 posteriors within 1e-4; with the debug flag also every frame's surviving
 tokens, cutoffs and the raw lattice.  Sizes span several tiles of the
 1024-thread workgroup, both compaction paths (LDS rank sort, state bitmap)
-and ragged frames."""
+and ragged frames.  Every case runs in both execution modes: one workgroup
+per utterance, and chip-wide kernels per frame."""
 import math
 
 import numpy as np
@@ -16,6 +17,7 @@ from gpu_compare import assert_same
 
 pytestmark = pytest.mark.gpu
 INF = math.inf
+MODES = ["workgroup", "chip"]
 
 
 @pytest.fixture(scope="module")
@@ -27,30 +29,32 @@ def wf():
     return wfstdec
 
 
-def _run(wf, oracle_mod, g, L, P, beam, ma, lb, debug=True, graph=None, case=""):
+def _run(wf, oracle_mod, g, L, P, beam, ma, lb, debug=True, graph=None, case="", mode="auto"):
     import torch
     print(f"\n[gpu case] {case} S={g['num_states']} A={g['dst'].size} T={L.shape[0]} "
-          f"beam={beam} max_active={ma} lattice_beam={lb} debug={debug}", flush=True)
+          f"beam={beam} max_active={ma} lattice_beam={lb} debug={debug} mode={mode}", flush=True)
     graph = graph or wf.Graph(g, P)
     x = torch.from_numpy(np.ascontiguousarray(L)).to(graph.device)
-    r = wf.decode(graph, x, beam, ma, lb, debug=debug)
+    r = wf.decode(graph, x, beam, ma, lb, debug=debug, mode=mode)
     o = oracle_mod.decode(g, L, beam, ma, lb, debug=debug)
     assert_same(r, o, debug=debug)
     return r, o, graph
 
 
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("name", ["hand_worked_1.json", "hand_worked_2.json"])
-def test_golden(wf, oracle_mod, name):
+def test_golden(wf, oracle_mod, name, mode):
     d, g, L = golden_cases.load(name)
     r, o, _ = _run(wf, oracle_mod, g, L, L.shape[1], d["beam"], d["max_active"], d["lattice_beam"],
-                   case=name)
+                   case=name, mode=mode)
     e = d["expect"]
     assert float(r.cost) == e["cost"] and list(r.words) == e["words"]
     assert r.stats["arcs_expanded"] == e["arcs_expanded"]
 
 
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("seed", range(24))
-def test_tiny_random(wf, oracle_mod, seed):
+def test_tiny_random(wf, oracle_mod, seed, mode):
     dy = seed % 2 == 0
     g = synth.tiny_graph(4000 + seed, S=4 + seed % 6, A=12 + seed % 11, eps_frac=0.35, P=3,
                          finals=seed % 3 == 0, dyadic=dy)
@@ -62,17 +66,19 @@ def test_tiny_random(wf, oracle_mod, seed):
         oracle_mod.decode(g, L, beam, ma, lb)
     except oracle_mod.OracleError:
         pytest.skip("no path")
-    _run(wf, oracle_mod, g, L, 3, beam, ma, lb, case=f"tiny seed {seed}")
+    _run(wf, oracle_mod, g, L, 3, beam, ma, lb, case=f"tiny seed {seed}", mode=mode)
 
 
-def test_zero_frames(wf, oracle_mod):
+@pytest.mark.parametrize("mode", MODES)
+def test_zero_frames(wf, oracle_mod, mode):
     g = synth.tiny_graph(77, S=6, A=14, eps_frac=0.6, P=3, finals=True)
     L = np.zeros((0, 3), np.float32)
-    _run(wf, oracle_mod, g, L, 3, INF, 0, INF, case="T=0")
+    _run(wf, oracle_mod, g, L, 3, INF, 0, INF, case="T=0", mode=mode)
 
 
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("seed", range(8))
-def test_medium_random(wf, oracle_mod, seed):
+def test_medium_random(wf, oracle_mod, seed, mode):
     rng = np.random.default_rng(seed)
     dy = seed % 3 == 0
     g = synth.tiny_graph(500 + seed, S=150, A=520, eps_frac=0.25, P=12, V=20,
@@ -81,7 +87,7 @@ def test_medium_random(wf, oracle_mod, seed):
     beam = float(rng.choice([2.0, 5.0, 9.0, INF]))
     ma = int(rng.choice([0, 5, 30]))
     lb = float(rng.choice([0.0, 1.0, 4.0, INF]))
-    r, _, _ = _run(wf, oracle_mod, g, L, 12, beam, ma, lb, case=f"medium seed {seed}")
+    r, _, _ = _run(wf, oracle_mod, g, L, 12, beam, ma, lb, case=f"medium seed {seed}", mode=mode)
     invariants.check_all(g, L, beam, ma, lb, r)
 
 
@@ -96,20 +102,22 @@ def tiny10k(wf):
     return cfg, g, synth.make_loglikes(cfg), wf.Graph(g, cfg["P"])
 
 
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("beam,ma,lb", TINY_PARAMS)
-def test_tiny_10k(wf, oracle_mod, tiny10k, beam, ma, lb):
+def test_tiny_10k(wf, oracle_mod, tiny10k, beam, ma, lb, mode):
     cfg, g, L, graph = tiny10k
     r, _, _ = _run(wf, oracle_mod, g, L, cfg["P"], beam, ma, lb, graph=graph,
-                   case=f"tiny_10k {beam}/{ma}/{lb}")
+                   case=f"tiny_10k {beam}/{ma}/{lb}", mode=mode)
     invariants.check_all(g, L, beam, ma, lb, r)
 
 
-def test_determinism(wf, oracle_mod, tiny10k):
+@pytest.mark.parametrize("mode", MODES)
+def test_determinism(wf, oracle_mod, tiny10k, mode):
     import torch
     cfg, g, L, graph = tiny10k
     x = torch.from_numpy(L).to(graph.device)
-    print("\n[gpu case] determinism tiny_10k x3", flush=True)
-    rs = [wf.decode(graph, x, 10.0, 40, 6.0, debug=True) for _ in range(3)]
+    print(f"\n[gpu case] determinism tiny_10k x3 mode={mode}", flush=True)
+    rs = [wf.decode(graph, x, 10.0, 40, 6.0, debug=True, mode=mode) for _ in range(3)]
     for r in rs[1:]:
         assert r.cost == rs[0].cost and list(r.words) == list(rs[0].words)
         assert np.array_equal(r.links[["t", "arc_id", "fwd_cost", "extra"]],
@@ -118,7 +126,8 @@ def test_determinism(wf, oracle_mod, tiny10k):
         assert np.abs(r.links["posterior"] - rs[0].links["posterior"]).max(initial=0) < 1e-12
 
 
-def test_batch_lanes_equal_single(wf, oracle_mod, tiny10k):
+@pytest.mark.parametrize("mode", MODES)
+def test_batch_lanes_equal_single(wf, oracle_mod, tiny10k, mode):
     """Lane i of a batch equals a single decode of utterance i, bit for bit,
     for utterances of different lengths."""
     import torch
@@ -128,66 +137,81 @@ def test_batch_lanes_equal_single(wf, oracle_mod, tiny10k):
           enumerate([50, 1, 120, 0, 77])]
     Ls = [np.ascontiguousarray(x, dtype=np.float32) for x in Ls]
     xs = [torch.from_numpy(x).to(graph.device) for x in Ls]
-    print("\n[gpu case] batch of 5 tiny_10k utterances", flush=True)
-    rb = wf.decode_batch(graph, xs, 10.0, 40, 6.0, debug=True)
+    print(f"\n[gpu case] batch of 5 tiny_10k utterances mode={mode}", flush=True)
+    rb = wf.decode_batch(graph, xs, 10.0, 40, 6.0, debug=True, mode=mode)
     for i, x in enumerate(xs):
-        rs = wf.decode(graph, x, 10.0, 40, 6.0, debug=True)
+        rs = wf.decode(graph, x, 10.0, 40, 6.0, debug=True, mode=mode)
         o = oracle_mod.decode(g, Ls[i], 10.0, 40, 6.0, debug=True)
         assert_same(rb[i], o, debug=True)
         assert_same(rs, o, debug=True)
     del rng
 
 
-def test_wide_2m_dyadic_prefix(wf, oracle_mod):
+@pytest.mark.parametrize("mode", MODES)
+def test_wide_2m_dyadic_prefix(wf, oracle_mod, mode):
     """Tens of thousands of tokens per frame (state-bitmap compaction), exact
     ties, epsilon chains of depth 8."""
     cfg = synth.workload("wide_2m_dyadic")
     g = synth.make_graph(cfg)
     L = synth.make_loglikes(cfg)[:3]
     r, _, _ = _run(wf, oracle_mod, g, L, cfg["P"], cfg["beam"], cfg["max_active"], cfg["lattice_beam"],
-                   case="wide_2m_dyadic T=3")
+                   case="wide_2m_dyadic T=3", mode=mode)
     assert r.stats["max_tokens"] > 2048
 
 
-def test_hclg_5m(wf, oracle_mod):
+@pytest.fixture(scope="module")
+def hclg5m(wf, oracle_mod):
     cfg = synth.workload("hclg_5m")
     g = synth.make_graph(cfg)
     L = synth.make_loglikes(cfg)
-    _run(wf, oracle_mod, g, L, cfg["P"], cfg["beam"], cfg["max_active"], cfg["lattice_beam"],
-         debug=False, case="hclg_5m full")
+    o = oracle_mod.decode(g, L, cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    return cfg, g, L, wf.Graph(g, cfg["P"]), o
 
 
-def test_invalid_loglikes(wf, tiny10k):
+@pytest.mark.parametrize("mode", MODES)
+def test_hclg_5m(wf, hclg5m, mode):
+    import torch
+    cfg, g, L, graph, o = hclg5m
+    print(f"\n[gpu case] hclg_5m full mode={mode}", flush=True)
+    x = torch.from_numpy(L).to(graph.device)
+    r = wf.decode(graph, x, cfg["beam"], cfg["max_active"], cfg["lattice_beam"], mode=mode)
+    assert_same(r, o)
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_invalid_loglikes(wf, tiny10k, mode):
     import torch
     cfg, g, L, graph = tiny10k
     bad = L[:20].copy()
     bad[7, 3] = np.nan
-    print("\n[gpu case] NaN log-likelihood", flush=True)
+    print(f"\n[gpu case] NaN log-likelihood mode={mode}", flush=True)
     with pytest.raises(wf.WdError) as e:
-        wf.decode(graph, torch.from_numpy(bad).to(graph.device), 10.0, 0, 5.0)
+        wf.decode(graph, torch.from_numpy(bad).to(graph.device), 10.0, 0, 5.0, mode=mode)
     assert e.value.status == wf.WD_EINVAL
 
 
-def test_no_path(wf, tiny10k):
+@pytest.mark.parametrize("mode", MODES)
+def test_no_path(wf, tiny10k, mode):
     import torch
     cfg, g, L, graph = tiny10k
     bad = L[:20].copy()
     bad[5, :] = -np.inf
-    print("\n[gpu case] all pdfs impossible at one frame", flush=True)
+    print(f"\n[gpu case] all pdfs impossible at one frame mode={mode}", flush=True)
     with pytest.raises(wf.WdError) as e:
-        wf.decode(graph, torch.from_numpy(bad).to(graph.device), INF, 0, 5.0)
+        wf.decode(graph, torch.from_numpy(bad).to(graph.device), INF, 0, 5.0, mode=mode)
     assert e.value.status == wf.WD_ENOPATH
 
 
-def test_capacity_retry(wf, oracle_mod, tiny10k):
+@pytest.mark.parametrize("mode", MODES)
+def test_capacity_retry(wf, oracle_mod, tiny10k, mode):
     """Deliberately small capacities: the decode reports WD_ECAPACITY with the
     sizes it needs, and the retries end with the oracle's result."""
     import torch
     cfg, g, L, graph = tiny10k
     x = torch.from_numpy(L[:80]).to(graph.device)
     small = wf.wd_caps(64, 64, 500, 500, 16)
-    print("\n[gpu case] capacity retry", flush=True)
-    p = wf.wd_params(10.0, 2000, 6.0, 0)
+    print(f"\n[gpu case] capacity retry mode={mode}", flush=True)
+    p = wf.wd_params(10.0, 2000, 6.0, wf._MODE_FLAGS[mode])
     ws, nbytes, used = graph.workspace(1, 80, p, small)
     st, res = wf.wd_decode(graph.handle, x.data_ptr(), 80, p, used, ws, nbytes,
                            torch.cuda.current_stream().cuda_stream)
@@ -195,6 +219,18 @@ def test_capacity_retry(wf, oracle_mod, tiny10k):
     r0 = wf.wd_result_read(res)
     wf.wd_result_free(res)
     assert any(r0.needed[f] > getattr(used, f) for f, _ in wf.wd_caps._fields_), r0.needed
-    r = wf.decode(graph, x, 10.0, 2000, 6.0, caps=small)
+    r = wf.decode(graph, x, 10.0, 2000, 6.0, caps=small, mode=mode)
     o = oracle_mod.decode(g, L[:80], 10.0, 2000, 6.0)
     assert_same(r, o)
+
+
+def test_mode_flags_exclusive(wf, tiny10k):
+    import torch
+    cfg, g, L, graph = tiny10k
+    x = torch.from_numpy(L[:10]).to(graph.device)
+    p = wf.wd_params(10.0, 40, 6.0, wf.WD_FLAG_ONE_WORKGROUP | wf.WD_FLAG_CHIP_WIDE)
+    ws, nbytes, used = graph.workspace(1, 10, wf.wd_params(10.0, 40, 6.0, 0), None)
+    print("\n[gpu case] both mode flags", flush=True)
+    st, res = wf.wd_decode(graph.handle, x.data_ptr(), 10, p, used, ws, nbytes,
+                           torch.cuda.current_stream().cuda_stream)
+    assert st == wf.WD_EINVAL and not res

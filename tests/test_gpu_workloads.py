@@ -55,17 +55,18 @@ def test_batch64_hclg_5m(wf, oracle_mod):
             raise AssertionError(f"lane {i} (T={Ls[i].shape[0]}): {e}")
 
 
+@pytest.mark.parametrize("mode", ["chip", "workgroup"])
 @pytest.mark.parametrize("name,T,debug", [("wide_2m", 12, True), ("wide_2m_dyadic", 8, True)])
-def test_wide_2m_prefix(wf, oracle_mod, name, T, debug):
+def test_wide_2m_prefix(wf, oracle_mod, name, T, debug, mode):
     """~1M tokens and ~1.5M raw links per frame, epsilon chains of depth 8."""
     import torch
     cfg = synth.workload(name)
-    print(f"\n[gpu case] {name} first {T} frames debug={debug}", flush=True)
+    print(f"\n[gpu case] {name} first {T} frames debug={debug} mode={mode}", flush=True)
     g = synth.make_graph(cfg)
     L = synth.make_loglikes(cfg)[:T]
     graph = wf.Graph(g, cfg["P"])
     r = wf.decode(graph, torch.from_numpy(L).to(graph.device), cfg["beam"], cfg["max_active"],
-                  cfg["lattice_beam"], debug=debug)
+                  cfg["lattice_beam"], debug=debug, mode=mode)
     o = oracle_mod.decode(g, L, cfg["beam"], cfg["max_active"], cfg["lattice_beam"], debug=debug)
     assert r.stats["max_tokens"] > 100000
     assert_same(r, o, debug=debug)
