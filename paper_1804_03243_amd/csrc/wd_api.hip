@@ -286,7 +286,7 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
   else launch_forward(g->dg, R.desc, B, prm, R.bad, s);
   if (timing) (void)hipEventRecord(ev[1], s);
   if (chip_wide) {
-    launch_grid_sweep(g->dg, R.desc, R.grid, B, max_T, s);
+    launch_grid_sweep(g->dg, R.desc, R.grid, B, max_T, p->lattice_beam, s);
     Params lp = prm;
     lp.flags |= kFlagSwept;
     launch_lattice(g->dg, R.desc, B, lp, s);

@@ -98,6 +98,7 @@ struct LaneInfo {
   uint32_t best_node;
   float best_cost;
   uint32_t tb_fail;            // traceback met an inconsistent predecessor
+  double Z;                    // total cost of the kept lattice (-log of its path sum)
 };
 
 enum : uint32_t { kOvfFrame = 1, kOvfArcs = 2, kOvfNodes = 4, kOvfLinks = 8, kOvfKept = 16 };

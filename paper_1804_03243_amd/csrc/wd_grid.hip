@@ -38,13 +38,14 @@ struct GridLane {
   uint32_t sel_active, sel_rank, sel_prefix, sel_less, sel_bits;
   uint32_t xmask;
   uint32_t final_used, best_total_key;
+  unsigned long long best_total;  // (final cost key, node offset) of the best end token
   uint64_t node_base, node_base_prev, link_base;
   uint64_t arcs, eps_arcs, tokens, max_tokens, need_frame, need_arcs;
   uint32_t nb[kMaxLevels + 1];
   uint32_t hist[kHistBins];
   // per-workgroup partial sums, then their exclusive prefix (+ total at kGB):
-  // [0] frontier counts, [1] degree sums, [2] link counts
-  unsigned long long part[3][kGB + 1];
+  // [0] frontier counts, [1] degree sums, [2] link counts, [3] kept links
+  unsigned long long part[4][kGB + 1];
 };
 
 // ------------------------------------------------------- workgroup collectives
@@ -137,11 +138,12 @@ __device__ __forceinline__ uint32_t seg_find(const Seg& sg, const uint32_t* seg,
   return sg.pl + (sg.lds ? search_le(seg, sg.m, w) : search_le(a + sg.pl, sg.m, w));
 }
 
-// Exclusive scan of the kGB partial sums part[which] of each utterance.
-__global__ void __launch_bounds__(kGT) k_g_scan(GridLane* gl, int which) {
+// Exclusive scan of the kGB partial sums part[which] of each utterance
+// (which = 3: the lattice pass, after the forward pass has stopped).
+__global__ void __launch_bounds__(kGT) k_g_scan(const LaneDesc* __restrict__ lanes, GridLane* gl, int which) {
   __shared__ GScratch s;
   GridLane& G = gl[blockIdx.y];
-  if (G.stop) return;
+  if (which < 3 ? G.stop != 0 : lanes[blockIdx.y].info->status != 0) return;
   unsigned long long* part = G.part[which];
   constexpr uint32_t per = kGB / kGT;
   unsigned long long v[per], sum = 0;
@@ -206,6 +208,70 @@ __global__ void k_g_begin(DevGraph g, const LaneDesc* __restrict__ lanes, GridLa
   G.best_key = 0xffffffffu;
 }
 
+// First touches of a workgroup staged in LDS and published with one global
+// reservation per list and round (touched states; the epsilon bucket of each
+// level) instead of one atomic per wavefront or thread on a counter that every
+// workgroup shares.  Entries that do not fit are appended directly.
+constexpr uint32_t kStage = 1024;
+
+struct TouchStage {
+  uint32_t nt, nbk, gt;
+  uint32_t touched[kStage];
+  uint32_t bk_state[kStage];
+  uint32_t bk_tag[kStage];  // level << 16 | index among the level's staged entries
+  uint32_t lcnt[kMaxLevels + 1];
+  uint32_t lbase[kMaxLevels + 1];
+};
+
+__device__ __forceinline__ void stage_reset(TouchStage& ts, uint32_t nlevels) {
+  for (uint32_t l = threadIdx.x; l < nlevels; l += kGT) ts.lcnt[l] = 0;
+  if (threadIdx.x == 0) {
+    ts.nt = 0;
+    ts.nbk = 0;
+  }
+}
+
+__device__ __forceinline__ void stage_touch(TouchStage& ts, GridLane& G, const LaneDesc& L, const DevGraph& g,
+                                            uint32_t dst, uint32_t cls) {
+  const uint32_t p = atomicAdd(&ts.nt, 1u);
+  if (p < kStage) {
+    ts.touched[p] = dst;
+  } else {
+    const uint32_t pos = atomicAdd(&G.n_touched, 1u);
+    if (pos < L.frame_cap) L.touched[pos] = dst;
+  }
+  if (cls != kNoEps) {
+    const uint32_t q = atomicAdd(&ts.nbk, 1u);
+    if (q < kStage) {
+      ts.bk_state[q] = dst;
+      ts.bk_tag[q] = (cls << 16) | atomicAdd(&ts.lcnt[cls], 1u);
+    } else {
+      L.bucket[g.level_base[cls] + atomicAdd(&G.nb[cls], 1u)] = dst;
+    }
+  }
+}
+
+// Publishes the staged entries and empties the stage.  Whole workgroup.
+__device__ __forceinline__ void stage_flush(TouchStage& ts, GridLane& G, const LaneDesc& L, const DevGraph& g) {
+  __syncthreads();
+  const uint32_t nt = ts.nt < kStage ? ts.nt : kStage, nbk = ts.nbk < kStage ? ts.nbk : kStage;
+  if (threadIdx.x == 0 && nt) ts.gt = atomicAdd(&G.n_touched, nt);
+  for (uint32_t l = threadIdx.x; l < g.nlevels; l += kGT)
+    if (ts.lcnt[l]) ts.lbase[l] = atomicAdd(&G.nb[l], ts.lcnt[l]);
+  __syncthreads();
+  for (uint32_t i = threadIdx.x; i < nt; i += kGT) {
+    const uint32_t pos = ts.gt + i;
+    if (pos < L.frame_cap) L.touched[pos] = ts.touched[i];
+  }
+  for (uint32_t i = threadIdx.x; i < nbk; i += kGT) {
+    const uint32_t tag = ts.bk_tag[i], l = tag >> 16;
+    L.bucket[g.level_base[l] + ts.lbase[l] + (tag & 0xffffu)] = ts.bk_state[i];
+  }
+  __syncthreads();
+  stage_reset(ts, g.nlevels);
+  __syncthreads();
+}
+
 // Emitting expansion of frame t: work item w is arc w - edeg[i] of frontier
 // token i of frame t-1.  Writes the candidate of every work item.
 __global__ void __launch_bounds__(kGT) k_g_expand(DevGraph g, const LaneDesc* __restrict__ lanes,
@@ -213,6 +279,7 @@ __global__ void __launch_bounds__(kGT) k_g_expand(DevGraph g, const LaneDesc* __
   __shared__ GScratch s;
   __shared__ uint32_t seg[kSeg];
   __shared__ uint32_t rng[2];
+  __shared__ TouchStage ts;
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop || t == 0) return;
@@ -223,33 +290,28 @@ __global__ void __launch_bounds__(kGT) k_g_expand(DevGraph g, const LaneDesc* __
   chunk(W, blockIdx.x, &blo, &bhi);
   uint32_t my_best = 0xffffffffu;
   if (blo < bhi) {
+    stage_reset(ts, g.nlevels);
     const Seg sg = load_seg(L.f_edeg, n_prev, (uint32_t)blo, (uint32_t)bhi, seg, rng);
-    for (uint64_t base = blo; base < bhi; base += kGT) {
-      const uint32_t w = (uint32_t)base + threadIdx.x;
-      bool first = false;
-      uint32_t dst = 0, cls = kNoEps;
-      if (w < bhi) {
+    for (uint64_t r0 = blo; r0 < bhi; r0 += kStage) {
+      const uint64_t r1 = r0 + kStage < bhi ? r0 + kStage : bhi;
+      for (uint64_t base = r0; base < r1; base += kGT) {
+        const uint32_t w = (uint32_t)base + threadIdx.x;
+        if (w >= r1) continue;
         const uint32_t i = seg_find(sg, seg, L.f_edeg, w);
         const float c = key_cost(L.f_key[i]);
         const uint4 r = g.earc[L.f_ebeg[i] + (w - L.f_edeg[i])];
-        dst = r.x;
-        cls = r.z >> 24;
         const float ac = -row[(r.z & 0xffffffu) - 1u];
         float x = c + ac;
         x = canon(x + __uint_as_float(r.y));
         const uint32_t xk = cost_key(x);
         if (xk < kInfKey) {
-          const unsigned long long old = atomicMin(&L.slot[dst], pack_tok(xk, r.w));
-          first = old == kEmpty;
+          const unsigned long long old = atomicMin(&L.slot[r.x], pack_tok(xk, r.w));
           my_best = xk < my_best ? xk : my_best;
+          if (old == kEmpty) stage_touch(ts, G, L, g, r.x, r.z >> 24);
         }
-        L.cand[w] = make_uint4(r.w, (uint32_t)(nbp + i), dst, __float_as_uint(x));
+        L.cand[w] = make_uint4(r.w, (uint32_t)(nbp + i), r.x, __float_as_uint(x));
       }
-      const uint32_t pos = wave_append(first, &G.n_touched);
-      if (first) {
-        if (pos < L.frame_cap) L.touched[pos] = dst;
-        if (cls != kNoEps) L.bucket[g.level_base[cls] + atomicAdd(&G.nb[cls], 1u)] = dst;
-      }
+      stage_flush(ts, G, L, g);
     }
   }
   my_best = (uint32_t)gmin64(my_best, s);
@@ -269,38 +331,52 @@ __global__ void k_g_cut(GridLane* gl, Params prm) {
 }
 
 // Epsilon closure, level `lvl`: states of that level within the cutoff relax
-// their epsilon arcs; destinations sit on higher levels.
+// their epsilon arcs; destinations sit on higher levels.  Per tile of 256
+// bucket states the workgroup spreads the tile's arcs over its threads (a
+// prefix sum of the states' epsilon degrees in LDS), so a state with many
+// epsilon arcs does not serialise the kernel.
 __global__ void __launch_bounds__(kGT) k_g_level(DevGraph g, const LaneDesc* __restrict__ lanes,
                                                  GridLane* gl, uint32_t lvl) {
   __shared__ GScratch s;
+  __shared__ TouchStage ts;
+  __shared__ uint32_t t_beg[kGT], t_ex[kGT], t_key[kGT];
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
   const uint32_t n = G.nb[lvl];
-  if (n == 0) return;
+  if (n == 0 || blockIdx.x * kGT >= n) return;
   const uint32_t kcutb = G.kcutb;
   const uint32_t* bk = L.bucket + g.level_base[lvl];
+  stage_reset(ts, g.nlevels);
   unsigned long long eps = 0;
-  for (uint32_t i = blockIdx.x * kGT + threadIdx.x; i < n; i += kGB * kGT) {
-    const uint32_t st = bk[i];
-    const uint32_t k = (uint32_t)(L.slot[st] >> 32);
-    if (k > kcutb) continue;
-    const float c = key_cost(k);
-    const uint32_t a0 = g.off[st].y, a1 = g.off[st + 1].y;
-    eps += a1 - a0;
-    for (uint32_t a = a0; a < a1; ++a) {
-      const uint4 r = g.xarc[a];
-      const uint32_t xk = cost_key(canon(c + __uint_as_float(r.y)));
-      if (xk > kcutb || xk >= kInfKey) continue;
-      const unsigned long long old = atomicMin(&L.slot[r.x], pack_tok(xk, r.w));
-      if (old == kEmpty) {
-        const uint32_t pos = atomicAdd(&G.n_touched, 1u);
-        if (pos < L.frame_cap) L.touched[pos] = r.x;
-        if (r.z != kNoEps) L.bucket[g.level_base[r.z] + atomicAdd(&G.nb[r.z], 1u)] = r.x;
+  for (uint32_t base = blockIdx.x * kGT; base < n; base += kGB * kGT) {
+    const uint32_t i = base + threadIdx.x;
+    uint32_t deg = 0, a0 = 0, k = 0;
+    if (i < n) {
+      const uint32_t st = bk[i];
+      k = (uint32_t)(L.slot[st] >> 32);
+      if (k <= kcutb) {
+        a0 = g.off[st].y;
+        deg = g.off[st + 1].y - a0;
       }
     }
+    unsigned long long tot;
+    const uint32_t ex = (uint32_t)gexcl64(deg, s, &tot);
+    t_beg[threadIdx.x] = a0;
+    t_ex[threadIdx.x] = ex;
+    t_key[threadIdx.x] = k;
+    eps += tot;
+    __syncthreads();
+    for (uint32_t w = threadIdx.x; w < (uint32_t)tot; w += kGT) {
+      const uint32_t j = search_le(t_ex, kGT, w);
+      const uint4 r = g.xarc[t_beg[j] + (w - t_ex[j])];
+      const uint32_t xk = cost_key(canon(key_cost(t_key[j]) + __uint_as_float(r.y)));
+      if (xk > kcutb || xk >= kInfKey) continue;
+      const unsigned long long old = atomicMin(&L.slot[r.x], pack_tok(xk, r.w));
+      if (old == kEmpty) stage_touch(ts, G, L, g, r.x, r.z);
+    }
+    stage_flush(ts, G, L, g);
   }
-  eps = gsum64(eps, s);
   if (threadIdx.x == 0 && eps) atomicAdd((unsigned long long*)&G.eps_arcs, eps);
 }
 
@@ -324,32 +400,58 @@ __global__ void k_g_check(const LaneDesc* __restrict__ lanes, GridLane* gl) {
 
 // Survivors of the beam cutoff; resets the touched slots; histogram of the
 // top cost-key digit when max-active is on.  Costs never fall below the best
-// emitting candidate (weights are >= 0), so the digit is in range.
+// emitting candidate (weights are >= 0), so the digit is in range.  Survivors
+// and histogram counts are staged in LDS per workgroup.
 __global__ void __launch_bounds__(kGT) k_g_count(const LaneDesc* __restrict__ lanes, GridLane* gl,
                                                  Params prm) {
+  __shared__ uint32_t n_st, gbase;
+  __shared__ uint32_t st_state[kStage];
+  __shared__ unsigned long long st_pack[kStage];
+  __shared__ uint32_t hist[kHistBins];
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
   const uint32_t nt = G.n_touched, kcutb = G.kcutb, best = G.best_key, shift = G.shift;
-  const bool hist = prm.max_active > 0;
-  for (uint32_t base = blockIdx.x * kGT; base < nt; base += kGB * kGT) {
-    const uint32_t i = base + threadIdx.x;
-    bool keep = false;
-    uint32_t st = 0;
-    unsigned long long v = kEmpty;
-    if (i < nt) {
-      st = L.touched[i];
-      v = L.slot[st];
+  if (blockIdx.x * kStage >= nt) return;
+  const bool use_hist = prm.max_active > 0;
+  if (use_hist)
+    for (uint32_t i = threadIdx.x; i < (uint32_t)kHistBins; i += kGT) hist[i] = 0;
+  if (threadIdx.x == 0) n_st = 0;
+  __syncthreads();
+  for (uint32_t r0 = blockIdx.x * kStage; r0 < nt; r0 += kGB * kStage) {
+    const uint32_t r1 = r0 + kStage < nt ? r0 + kStage : nt;
+    for (uint32_t i = r0 + threadIdx.x; i < r1; i += kGT) {
+      const uint32_t st = L.touched[i];
+      const unsigned long long v = L.slot[st];
       L.slot[st] = kEmpty;
-      keep = (uint32_t)(v >> 32) <= kcutb;
+      if ((uint32_t)(v >> 32) <= kcutb) {
+        const uint32_t p = atomicAdd(&n_st, 1u);
+        st_state[p] = st;
+        st_pack[p] = v;
+        if (use_hist) atomicAdd(&hist[((uint32_t)(v >> 32) - best) >> shift], 1u);
+      }
     }
-    const uint32_t pos = wave_append(keep, &G.n_surv);
-    if (keep) {
-      L.surv_state[pos] = st;
-      L.surv_pack[pos] = v;
-      if (hist) atomicAdd(&G.hist[((uint32_t)(v >> 32) - best) >> shift], 1u);
+    __syncthreads();
+    const uint32_t m = n_st;
+    if (threadIdx.x == 0 && m) gbase = atomicAdd(&G.n_surv, m);
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < m; i += kGT) {
+      const uint32_t st = st_state[i];
+      L.surv_state[gbase + i] = st;
+      L.surv_pack[gbase + i] = st_pack[i];
+      if (!use_hist) {
+        // no max-active: every survivor is kept (what k_g_mark does otherwise)
+        L.idx[st] = gbase + i;
+        atomicOr(&L.bitmap[st >> 5], 1u << (st & 31u));
+      }
     }
+    __syncthreads();
+    if (threadIdx.x == 0) n_st = 0;
+    __syncthreads();
   }
+  if (use_hist)
+    for (uint32_t i = threadIdx.x; i < (uint32_t)kHistBins; i += kGT)
+      if (hist[i]) atomicAdd(&G.hist[i], hist[i]);
 }
 
 // Max-active by radix select: step 0 decides whether the limit binds; every
@@ -413,29 +515,34 @@ __global__ void __launch_bounds__(kGT) k_g_select(GridLane* gl, Params prm, int 
   }
 }
 
-// Histogram of the next digit over the survivors matching the prefix.
+// Histogram of the next digit over the survivors matching the prefix (per
+// workgroup in LDS, then added to the utterance's histogram).
 __global__ void __launch_bounds__(kGT) k_g_select_hist(const LaneDesc* __restrict__ lanes, GridLane* gl) {
+  __shared__ uint32_t hist[kHistBins];
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop || !G.sel_active) return;
   const uint32_t ns = G.n_surv, best = G.best_key, prefix = G.sel_prefix, bits = G.sel_bits;
   const uint32_t nsh = G.shift, osh = nsh + bits;
+  if (blockIdx.x * kGT >= ns) return;
+  for (uint32_t i = threadIdx.x; i < (uint32_t)kHistBins; i += kGT) hist[i] = 0;
+  __syncthreads();
   for (uint32_t i = blockIdx.x * kGT + threadIdx.x; i < ns; i += kGB * kGT) {
     const uint32_t d = (uint32_t)(L.surv_pack[i] >> 32) - best;
-    if ((d >> osh) == prefix) atomicAdd(&G.hist[(d >> nsh) & ((1u << bits) - 1u)], 1u);
+    if ((d >> osh) == prefix) atomicAdd(&hist[(d >> nsh) & ((1u << bits) - 1u)], 1u);
   }
+  __syncthreads();
+  for (uint32_t i = threadIdx.x; i < (uint32_t)kHistBins; i += kGT)
+    if (hist[i]) atomicAdd(&G.hist[i], hist[i]);
 }
 
-// Kept tokens mark their state in the bitmap; idx[state] = survivor index.
+// Kept tokens mark their state in the bitmap; idx[state] = survivor index
+// (max-active on; without it the survivor kernel marks them).
 __global__ void __launch_bounds__(kGT) k_g_mark(const LaneDesc* __restrict__ lanes, GridLane* gl) {
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
   const uint32_t ns = G.n_surv, cut = G.cut_key;
-  if (blockIdx.x == 0 && threadIdx.x == 0 && G.hist_ok && G.node_base + G.n_keep > L.node_cap) {
-    G.hist_ok = 0;
-    G.ovf |= kOvfNodes;
-  }
   for (uint32_t i = blockIdx.x * kGT + threadIdx.x; i < ns; i += kGB * kGT) {
     const unsigned long long v = L.surv_pack[i];
     if ((uint32_t)(v >> 32) <= cut) {
@@ -446,11 +553,16 @@ __global__ void __launch_bounds__(kGT) k_g_mark(const LaneDesc* __restrict__ lan
   }
 }
 
+// Kept states per workgroup chunk of the bitmap; node capacity check.
 __global__ void __launch_bounds__(kGT) k_g_bits(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl) {
   __shared__ GScratch s;
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
+  if (blockIdx.x == 0 && threadIdx.x == 0 && G.hist_ok && G.node_base + G.n_keep > L.node_cap) {
+    G.hist_ok = 0;
+    G.ovf |= kOvfNodes;
+  }
   uint64_t blo, bhi, lo, hi;
   chunk((g.S + 31u) >> 5, blockIdx.x, &blo, &bhi);
   sub_chunk(blo, bhi, &lo, &hi);
@@ -462,30 +574,49 @@ __global__ void __launch_bounds__(kGT) k_g_bits(DevGraph g, const LaneDesc* __re
 
 // The frontier in state order: node store, frontier arrays, idx[state] = node
 // id; per-workgroup (emitting, epsilon) out-degree sums of its frontier range.
+// A workgroup takes its bitmap chunk 1024 words at a time into LDS with the
+// words' exclusive bit counts, then one thread per state bit.
+constexpr uint32_t kCW = 1024;
+
 __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* __restrict__ lanes,
                                                    GridLane* gl) {
   __shared__ GScratch s;
+  __shared__ uint32_t wd[kCW], wp[kCW];
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
-  uint64_t blo, bhi, lo, hi;
+  uint64_t blo, bhi;
   chunk((g.S + 31u) >> 5, blockIdx.x, &blo, &bhi);
-  sub_chunk(blo, bhi, &lo, &hi);
-  unsigned long long c = 0;
-  for (uint64_t w = lo; w < hi; ++w) c += (uint32_t)__popc(L.bitmap[w]);
-  unsigned long long tot;
-  uint64_t p = G.part[0][blockIdx.x] + gexcl64(c, s, &tot);
+  uint64_t pos0 = G.part[0][blockIdx.x];
   const uint64_t nb = G.node_base;
   const bool store = G.hist_ok != 0;
   unsigned long long deg = 0;
-  for (uint64_t w = lo; w < hi; ++w) {
-    uint32_t word = L.bitmap[w];
-    if (!word) continue;
-    L.bitmap[w] = 0;
-    while (word) {
-      const uint32_t b = (uint32_t)__ffs(word) - 1u;
-      word &= word - 1u;
-      const uint32_t st = ((uint32_t)w << 5) | b;
+  constexpr uint32_t per = kCW / kGT;
+  for (uint64_t r0 = blo; r0 < bhi; r0 += kCW) {
+    const uint32_t m = (uint32_t)(bhi - r0 < kCW ? bhi - r0 : kCW);
+    uint32_t c = 0;
+#pragma unroll
+    for (uint32_t j = 0; j < per; ++j) {
+      const uint32_t q = threadIdx.x * per + j;
+      uint32_t w = 0;
+      if (q < m) {
+        w = L.bitmap[r0 + q];
+        if (w) L.bitmap[r0 + q] = 0;
+      }
+      wd[q] = w;
+      wp[q] = c;
+      c += (uint32_t)__popc(w);
+    }
+    unsigned long long tot;
+    const uint32_t ex = (uint32_t)gexcl64(c, s, &tot);
+#pragma unroll
+    for (uint32_t j = 0; j < per; ++j) wp[threadIdx.x * per + j] += ex;
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < m * 32u; j += kGT) {
+      const uint32_t word = wd[j >> 5], b = j & 31u;
+      if (!((word >> b) & 1u)) continue;
+      const uint64_t p = pos0 + wp[j >> 5] + (uint32_t)__popc(word & ((1u << b) - 1u));
+      const uint32_t st = (uint32_t)((r0 << 5) + j);
       const unsigned long long v = L.surv_pack[L.idx[st]];
       const uint64_t node = nb + p;
       if (store) {
@@ -499,8 +630,9 @@ __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* _
       L.f_arc[p] = (uint32_t)v;
       const uint2 o0 = g.off[st], o1 = g.off[st + 1];
       deg += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
-      ++p;
     }
+    pos0 += tot;
+    __syncthreads();
   }
   deg = gsum64(deg, s);
   if (threadIdx.x == 0) G.part[1][blockIdx.x] = deg;
@@ -721,36 +853,54 @@ __global__ void k_g_finish(const LaneDesc* __restrict__ lanes, GridLane* gl) {
 
 // ------------------------------------------------------------- pruning sweep
 
-// Whether a final state was reached in the last frame, and the best final
-// cost.  One workgroup per utterance.
-__global__ void __launch_bounds__(kGT) k_gs_final(DevGraph g, const LaneDesc* __restrict__ lanes,
-                                                  GridLane* gl) {
+// Whether a final state with a finite total cost was reached in the last frame.
+__global__ void __launch_bounds__(kGT) k_gs_final_any(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                      GridLane* gl) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (L.info->status != 0) return;
+  if (blockIdx.x == 0 && threadIdx.x == 0) G.best_total = kEmpty;
+  if (!g.final_w) return;
+  const uint64_t n0 = L.node_off[L.T], n1 = L.node_off[L.T + 1];
+  bool any = false;
+  for (uint64_t n = n0 + blockIdx.x * kGT + threadIdx.x; n < n1; n += (uint64_t)kGB * kGT) {
+    const float fw = g.final_w[L.n_state[n]];
+    const float c = key_cost((uint32_t)(L.n_pack[n] >> 32));
+    any |= fw < INFINITY && (c + fw) < INFINITY;
+  }
+  if (__ballot(any) && lane_id() == 0) atomicOr(&G.final_used, 1u);
+}
+
+// The best final cost (lowest node on ties) of the last frame.
+__global__ void __launch_bounds__(kGT) k_gs_final_min(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                      GridLane* gl) {
   __shared__ GScratch s;
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (L.info->status != 0) return;
-  const int T = L.T;
-  const uint64_t n0 = L.node_off[T], n1 = L.node_off[T + 1];
-  unsigned long long any = 0;
-  if (g.final_w)
-    for (uint64_t n = n0 + threadIdx.x; n < n1; n += kGT) {
-      const float fw = g.final_w[L.n_state[n]];
-      const float c = key_cost((uint32_t)(L.n_pack[n] >> 32));
-      any |= (fw < INFINITY && (c + fw) < INFINITY) ? 1ull : 0ull;
-    }
-  any = gsum64(any, s);
+  const uint64_t n0 = L.node_off[L.T], n1 = L.node_off[L.T + 1];
+  if (n0 + blockIdx.x * kGT >= n1) return;
+  const bool any = G.final_used != 0;
   unsigned long long m = kEmpty;
-  for (uint64_t n = n0 + threadIdx.x; n < n1; n += kGT) {
+  for (uint64_t n = n0 + blockIdx.x * kGT + threadIdx.x; n < n1; n += (uint64_t)kGB * kGT) {
     const float c = key_cost((uint32_t)(L.n_pack[n] >> 32));
     const float F = any ? canon(c + g.final_w[L.n_state[n]]) : c;
     const unsigned long long v = pack_tok(cost_key(F), (uint32_t)(n - n0));
     m = v < m ? v : m;
   }
   m = gmin64(m, s);
-  if (threadIdx.x == 0) {
-    G.final_used = any ? 1u : 0u;
-    G.best_total_key = (uint32_t)(m >> 32);
-  }
+  if (threadIdx.x == 0) atomicMin(&G.best_total, m);
+}
+
+// Publishes the final-cost results for the lattice kernel.
+__global__ void k_gs_final(const LaneDesc* __restrict__ lanes, GridLane* gl) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (threadIdx.x != 0 || L.info->status != 0) return;
+  G.best_total_key = (uint32_t)(G.best_total >> 32);
+  L.info->final_used = G.final_used ? 1 : 0;
+  L.info->best_node = (uint32_t)(L.node_off[L.T] + (G.best_total & 0xffffffffu));
+  L.info->best_cost = key_cost(G.best_total_key);
 }
 
 // Extra costs of frame t's nodes before relaxation: final extra cost for the
@@ -802,6 +952,62 @@ __global__ void __launch_bounds__(kGT) k_gs_relax(const LaneDesc* __restrict__ l
   }
 }
 
+// Kept links (extra cost within the lattice beam) in link order: per-workgroup
+// counts, then per 256-link tile a workgroup scan.  The count goes to the
+// utterance's LaneInfo; the list is written only when it fits.
+__device__ __forceinline__ bool kept_link(const LaneDesc& L, uint64_t k, uint32_t lb_key) {
+  const uint32_t le = L.le_key[k];
+  return le <= lb_key && le < kInfKey;
+}
+
+__global__ void __launch_bounds__(kGT) k_gk_count(const LaneDesc* __restrict__ lanes, GridLane* gl,
+                                                  uint32_t lb_key) {
+  __shared__ GScratch s;
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (L.info->status != 0) return;
+  uint64_t blo, bhi;
+  chunk(L.link_off[L.T + 1], blockIdx.x, &blo, &bhi);
+  unsigned long long c = 0;
+  for (uint64_t k = blo + threadIdx.x; k < bhi; k += kGT) c += kept_link(L, k, lb_key);
+  c = gsum64(c, s);
+  if (threadIdx.x == 0) G.part[3][blockIdx.x] = c;
+}
+
+__global__ void __launch_bounds__(kGT) k_gk_write(const LaneDesc* __restrict__ lanes, GridLane* gl,
+                                                  uint32_t lb_key) {
+  __shared__ GScratch s;
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (L.info->status != 0) return;
+  const uint64_t n_kept = G.part[3][kGB];
+  if (blockIdx.x == 0 && threadIdx.x == 0) L.info->kept = n_kept;
+  if (n_kept > L.kept_cap) return;
+  uint64_t blo, bhi;
+  chunk(L.link_off[L.T + 1], blockIdx.x, &blo, &bhi);
+  unsigned long long run = G.part[3][blockIdx.x];
+  for (uint64_t base = blo; base < bhi; base += kGT) {
+    const uint64_t k = base + threadIdx.x;
+    const bool on = k < bhi && kept_link(L, k, lb_key);
+    unsigned long long tile;
+    const unsigned long long ex = run + gexcl64(on ? 1ull : 0ull, s, &tile);
+    run += tile;
+    if (on) L.kept_idx[ex] = k;
+  }
+}
+
+// alpha and beta of every node start at +inf (the lattice kernel then only
+// writes the nodes that kept links reach).
+__global__ void __launch_bounds__(kGT) k_gs_fill_ab(const LaneDesc* __restrict__ lanes) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  if (L.info->status != 0) return;
+  const uint64_t n = L.node_off[L.T + 1];
+  for (uint64_t i = (uint64_t)blockIdx.x * kGT + threadIdx.x; i < n; i += (uint64_t)kGB * kGT) {
+    L.alpha[i] = INFINITY;
+    L.beta[i] = INFINITY;
+  }
+}
+
 // -------------------------------------------------------------------- launches
 
 size_t grid_lane_bytes() { return sizeof(GridLane); }
@@ -824,30 +1030,38 @@ void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, in
         hipLaunchKernelGGL(k_g_select_hist, all, blk, 0, st, lanes, gl);
         hipLaunchKernelGGL(k_g_select, one, blk, 0, st, gl, prm, step);
       }
-    hipLaunchKernelGGL(k_g_mark, all, blk, 0, st, lanes, gl);
+    if (prm.max_active > 0) hipLaunchKernelGGL(k_g_mark, all, blk, 0, st, lanes, gl);
     hipLaunchKernelGGL(k_g_bits, all, blk, 0, st, g, lanes, gl);
-    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, gl, 0);
+    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 0);
     hipLaunchKernelGGL(k_g_compact, all, blk, 0, st, g, lanes, gl);
-    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, gl, 1);
+    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 1);
     hipLaunchKernelGGL(k_g_degrees, all, blk, 0, st, g, lanes, gl);
     hipLaunchKernelGGL(k_g_link_count, all, blk, 0, st, g, lanes, gl, t);
-    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, gl, 2);
+    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 2);
     hipLaunchKernelGGL(k_g_link_write, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_g_end, one, blk, 0, st, lanes, gl, t);
   }
   hipLaunchKernelGGL(k_g_finish, one, dim3(64), 0, st, lanes, gl);
 }
 
-void launch_grid_sweep(const DevGraph& g, const LaneDesc* lanes, void* glv, int B, int maxT, hipStream_t st) {
+void launch_grid_sweep(const DevGraph& g, const LaneDesc* lanes, void* glv, int B, int maxT, float lattice_beam,
+                       hipStream_t st) {
   GridLane* gl = (GridLane*)glv;
   const dim3 one(1, B), all(kGB, B), blk(kGT);
-  hipLaunchKernelGGL(k_gs_final, one, blk, 0, st, g, lanes, gl);
+  hipLaunchKernelGGL(k_gs_final_any, all, blk, 0, st, g, lanes, gl);
+  hipLaunchKernelGGL(k_gs_final_min, all, blk, 0, st, g, lanes, gl);
+  hipLaunchKernelGGL(k_gs_final, one, dim3(64), 0, st, lanes, gl);
   for (int t = maxT; t >= 0; --t) {
     hipLaunchKernelGGL(k_gs_init, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, t, 1, 0);
     for (int l = (int)g.nlevels - 1; l >= 0; --l)
       hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, t, 0, l);
   }
+  const uint32_t lb_key = cost_key(lattice_beam);
+  hipLaunchKernelGGL(k_gk_count, all, blk, 0, st, lanes, gl, lb_key);
+  hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 3);
+  hipLaunchKernelGGL(k_gk_write, all, blk, 0, st, lanes, gl, lb_key);
+  hipLaunchKernelGGL(k_gs_fill_ab, all, blk, 0, st, lanes);
 }
 
 }  // namespace wd

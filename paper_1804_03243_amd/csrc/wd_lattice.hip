@@ -92,21 +92,24 @@ __device__ __forceinline__ double link_ac(const LaneDesc& L, const DevGraph& g, 
 // Write the selected links (all links, or the kept ones listed in kept_idx)
 // in (t, arc id) order.  Each frame holds an emitting run then an epsilon run,
 // each already ascending in arc id; a link's slot is its rank in its own run
-// plus the number of links of the other run with a smaller arc id.
+// plus the number of links of the other run with a smaller arc id.  The runs'
+// bounds in selection order are the frame's link offsets (all links) or the
+// per-frame kept-link boundaries kf.
 __device__ void assemble(const LaneDesc& L, const DevGraph& g, bool all, uint64_t n_sel,
-                         OutLink* out, uint32_t lb_key, double Z, bool with_post, bool mark_nodes) {
+                         OutLink* out, uint32_t lb_key, double Z, bool with_post, bool mark_nodes,
+                         uint64_t first, uint64_t stride) {
   const int T = L.T;
   const uint64_t* kid = L.kept_idx;
+  const uint64_t* kf = L.kframe;
   auto sel = [&](uint64_t j) -> uint64_t { return all ? j : kid[j]; };
-  auto below = [&](uint64_t k) -> uint64_t { return all ? k : lower_bound64(kid, n_sel, k); };
-  for (uint64_t j = threadIdx.x; j < n_sel; j += kThreads) {
+  for (uint64_t j = first; j < n_sel; j += stride) {
     const uint64_t k = sel(j);
     const int t = (int)search_le64(L.link_off, (uint64_t)T + 2, k);
     const uint64_t xo = L.link_xoff[t];
     const bool eps = k >= xo;
-    const uint64_t s0 = below(L.link_off[t]);
-    const uint64_t sx = below(xo);
-    const uint64_t s1 = below(L.link_off[t + 1]);
+    const uint64_t s0 = all ? L.link_off[t] : kf[2 * t];
+    const uint64_t sx = all ? xo : kf[2 * t + 1];
+    const uint64_t s1 = all ? L.link_off[t + 1] : kf[2 * t + 2];
     const LinkView l = link_at(L, k);
     // the other run [o0, o1) in selection order
     const uint64_t o0 = eps ? s0 : sx, o1 = eps ? sx : s1;
@@ -142,6 +145,34 @@ __device__ void assemble(const LaneDesc& L, const DevGraph& g, bool all, uint64_
   }
 }
 
+// Lattice nodes (those marked in the used bitmap) in (t, state) order, which
+// is node id order; returns their number.  Whole workgroup.
+__device__ uint64_t write_nodes(const LaneDesc& L, uint64_t nnodes, BlockScratch& bs, uint32_t& par) {
+  const uint32_t tid = threadIdx.x;
+  const uint64_t nwd = (nnodes + 31) >> 5;
+  const uint64_t per = (nwd + kThreads - 1) / kThreads;
+  const uint64_t w0 = tid * per < nwd ? tid * per : nwd;
+  const uint64_t w1 = w0 + per < nwd ? w0 + per : nwd;
+  uint64_t cnt = 0, n_out;
+  for (uint64_t w = w0; w < w1; ++w) cnt += (uint64_t)__popc(L.used[w]);
+  uint64_t pos = block_excl_scan64(cnt, bs, par, &n_out);
+  for (uint64_t w = w0; w < w1; ++w) {
+    uint32_t word = L.used[w];
+    while (word) {
+      const uint32_t b = (uint32_t)__ffs(word) - 1u;
+      word &= word - 1u;
+      const uint64_t n = (w << 5) | b;
+      OutNode o;
+      o.t = (int32_t)search_le64(L.node_off, (uint64_t)L.T + 2, n);
+      o.state = (int32_t)L.n_state[n];
+      o.cost = node_cost(L, n);
+      o.extra = key_cost(L.extra_key[n]);
+      L.out_nodes[pos++] = o;
+    }
+  }
+  return n_out;
+}
+
 // Levels present in a frame's epsilon links, highest first / lowest first.
 __device__ __forceinline__ bool level_present(uint32_t mask, uint32_t lvl) {
   return (mask >> (lvl < 31u ? lvl : 31u)) & 1u;
@@ -164,29 +195,40 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
   uint32_t par = 0;
 
   // ------------------------------------------------ final costs, best end token
-  uint32_t any = 0;
-  if (g.final_w)
+  const bool swept = (prm.flags & kFlagSwept) != 0;
+  bool final_used;
+  uint32_t best_key;
+  uint64_t bnode;
+  if (swept) {
+    // found by the chip-wide kernels
+    final_used = info->final_used != 0;
+    best_key = cost_key(info->best_cost);
+    bnode = info->best_node;
+  } else {
+    uint32_t any = 0;
+    if (g.final_w)
+      for (uint64_t n = nT0 + tid; n < nT1; n += kThreads) {
+        const float fw = g.final_w[L.n_state[n]];
+        const float c = node_cost(L, n);
+        any |= (fw < INFINITY && (c + fw) < INFINITY) ? 1u : 0u;
+      }
+    final_used = block_or(any, sh.bs, par) != 0;
+    uint64_t m = kEmpty;
     for (uint64_t n = nT0 + tid; n < nT1; n += kThreads) {
-      const float fw = g.final_w[L.n_state[n]];
       const float c = node_cost(L, n);
-      any |= (fw < INFINITY && (c + fw) < INFINITY) ? 1u : 0u;
+      const float F = final_used ? canon(c + g.final_w[L.n_state[n]]) : c;
+      const uint64_t v = pack_tok(cost_key(F), (uint32_t)(n - nT0));
+      m = v < m ? v : m;
     }
-  const bool final_used = block_or(any, sh.bs, par) != 0;
-  uint64_t m = kEmpty;
-  for (uint64_t n = nT0 + tid; n < nT1; n += kThreads) {
-    const float c = node_cost(L, n);
-    const float F = final_used ? canon(c + g.final_w[L.n_state[n]]) : c;
-    const uint64_t v = pack_tok(cost_key(F), (uint32_t)(n - nT0));
-    m = v < m ? v : m;
+    m = block_min64(m, sh.bs, par);
+    best_key = (uint32_t)(m >> 32);
+    bnode = nT0 + (m & 0xffffffffu);
   }
-  m = block_min64(m, sh.bs, par);
-  const uint32_t best_key = (uint32_t)(m >> 32);
   if (best_key >= kInfKey) {
     if (tid == 0 && blockIdx.y == 0) info->status = 3;
     return;
   }
   const float best_total = key_cost(best_key);
-  const uint64_t bnode = nT0 + (m & 0xffffffffu);
 
   if (blockIdx.y == 1) {
     // ------------------------------------------------------------ traceback
@@ -229,7 +271,6 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
   }
 
   // ------------------------------------------------ backward extra-cost sweep
-  const bool swept = (prm.flags & kFlagSwept) != 0;
   for (int t = swept ? -1 : T; t >= 0; --t) {
     const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
     const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
@@ -282,8 +323,8 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
 
   // ------------------------------------------ kept links (final merge input)
   const uint32_t lb_key = cost_key(prm.lattice_beam);
-  uint64_t n_kept;
-  {
+  uint64_t n_kept = info->kept;  // counted and listed by the chip-wide kernels when swept
+  if (!swept) {
     const uint64_t per = (nlinks + kThreads - 1) / kThreads;
     const uint64_t k0 = tid * per < nlinks ? tid * per : nlinks;
     const uint64_t k1 = k0 + per < nlinks ? k0 + per : nlinks;
@@ -332,7 +373,11 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
     const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
     const bool win = nt <= kWin;
     double* a = win ? sh.w.ab[buf] : L.alpha + n0;
-    for (uint32_t i = tid; i < nt; i += kThreads) a[i] = (n0 + i == start_node) ? 0.0 : INFINITY;
+    if (win || !swept) {
+      for (uint32_t i = tid; i < nt; i += kThreads) a[i] = (n0 + i == start_node) ? 0.0 : INFINITY;
+    } else if (tid == 0 && start_node >= n0 && start_node < n1) {
+      a[start_node - n0] = 0.0;  // the rest is +inf already
+    }
     __syncthreads();
     const uint64_t e0 = kf[2 * t], e1 = kf[2 * t + 1], e2 = kf[2 * t + 2];
     if (e1 > e0) {
@@ -367,8 +412,9 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
     const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
     const bool win = nt <= kWin;
     double* b = win ? sh.w.ab[buf] : L.beta + n0;
-    for (uint32_t i = tid; i < nt; i += kThreads)
-      b[i] = t == T ? (final_used ? (double)g.final_w[L.n_state[n0 + i]] : 0.0) : INFINITY;
+    if (win || !swept || t == T)
+      for (uint32_t i = tid; i < nt; i += kThreads)
+        b[i] = t == T ? (final_used ? (double)g.final_w[L.n_state[n0 + i]] : 0.0) : INFINITY;
     __syncthreads();
     if (t < T) {
       const uint64_t e0 = kf[2 * t + 2], e1 = kf[2 * t + 3];
@@ -402,51 +448,58 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
   }
   __syncthreads();
   const double Z = L.beta[start_node];
-
-  // ------------------------------------------- final merge of the kept links
-  // used-node bitmap is zero on entry (cleared by the host before the launch)
-  if (tid == 0) atomicOr(&L.used[start_node >> 5], 1u << (start_node & 31u));
-  assemble(L, g, false, n_kept, L.out_links, lb_key, Z, true, true);
-  if (debug) assemble(L, g, true, nlinks, L.out_raw, lb_key, Z, true, false);
-  __syncthreads();
-  // lattice nodes in (t, state) order = node id order
-  uint64_t n_out;
-  {
-    const uint64_t nwd = (nnodes + 31) >> 5;
-    const uint64_t per = (nwd + kThreads - 1) / kThreads;
-    const uint64_t w0 = tid * per < nwd ? tid * per : nwd;
-    const uint64_t w1 = w0 + per < nwd ? w0 + per : nwd;
-    uint64_t cnt = 0;
-    for (uint64_t w = w0; w < w1; ++w) cnt += (uint64_t)__popc(L.used[w]);
-    uint64_t pos = block_excl_scan64(cnt, sh.bs, par, &n_out);
-    for (uint64_t w = w0; w < w1; ++w) {
-      uint32_t word = L.used[w];
-      while (word) {
-        const uint32_t b = (uint32_t)__ffs(word) - 1u;
-        word &= word - 1u;
-        const uint64_t n = (w << 5) | b;
-        OutNode o;
-        o.t = (int32_t)search_le64(L.node_off, (uint64_t)T + 2, n);
-        o.state = (int32_t)L.n_state[n];
-        o.cost = node_cost(L, n);
-        o.extra = key_cost(L.extra_key[n]);
-        L.out_nodes[pos++] = o;
-      }
-    }
-  }
   if (tid == 0) {
     info->final_used = final_used ? 1 : 0;
     info->kept = n_kept;
-    info->out_nodes = n_out;
     info->out_raw = debug ? nlinks : 0;
     info->start_node = (uint32_t)start_node;
     info->best_node = (uint32_t)bnode;
     info->best_cost = best_total;
+    info->Z = Z;
   }
+  // used-node bitmap is zero on entry (cleared by the host before the launch)
+  if (tid == 0) atomicOr(&L.used[start_node >> 5], 1u << (start_node & 31u));
+  if (swept) return;  // the merge and the node list run as chip-wide kernels
+
+  // ------------------------------------------- final merge of the kept links
+  assemble(L, g, false, n_kept, L.out_links, lb_key, Z, true, true, tid, kThreads);
+  if (debug) assemble(L, g, true, nlinks, L.out_raw, lb_key, Z, true, false, tid, kThreads);
+  __syncthreads();
+  const uint64_t n_out = write_nodes(L, nnodes, sh.bs, par);
+  if (tid == 0) info->out_nodes = n_out;
+}
+
+// Chip-wide merge of the kept links (and of every raw link with the debug
+// flag), after the lattice kernel has produced the posteriors' inputs.
+__global__ void __launch_bounds__(256) k_lat_assemble(DevGraph g, const LaneDesc* __restrict__ lanes, Params prm) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  const LaneInfo* info = L.info;
+  if (info->status != 0) return;
+  const uint32_t lb_key = cost_key(prm.lattice_beam);
+  const uint64_t first = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  assemble(L, g, false, info->kept, L.out_links, lb_key, info->Z, true, true, first, stride);
+  if (prm.flags & 1u)
+    assemble(L, g, true, L.link_off[L.T + 1], L.out_raw, lb_key, info->Z, true, false, first, stride);
+}
+
+// The lattice node list after the chip-wide merge.
+__global__ void __launch_bounds__(kThreads) k_lat_nodes(const LaneDesc* __restrict__ lanes) {
+  __shared__ BlockScratch bs;
+  const LaneDesc& L = lanes[blockIdx.x];
+  LaneInfo* info = L.info;
+  if (info->status != 0) return;
+  uint32_t par = 0;
+  const uint64_t n_out = write_nodes(L, L.node_off[L.T + 1], bs, par);
+  if (threadIdx.x == 0) info->out_nodes = n_out;
 }
 
 void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s) {
   hipLaunchKernelGGL(k_lattice, dim3(B, 2), dim3(kThreads), 0, s, g, lanes, prm);
+  if (prm.flags & kFlagSwept) {
+    hipLaunchKernelGGL(k_lat_assemble, dim3(1024, B), dim3(256), 0, s, g, lanes, prm);
+    hipLaunchKernelGGL(k_lat_nodes, dim3(B), dim3(kThreads), 0, s, lanes);
+  }
 }
 
 }  // namespace wd
