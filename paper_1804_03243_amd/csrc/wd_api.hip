@@ -290,6 +290,7 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
     Params lp = prm;
     lp.flags |= kFlagSwept;
     launch_lattice(g->dg, R.desc, B, lp, s);
+    launch_grid_nodes(R.desc, R.grid, B, s);
   } else {
     launch_lattice(g->dg, R.desc, B, prm, s);
   }

@@ -139,11 +139,13 @@ __device__ __forceinline__ uint32_t seg_find(const Seg& sg, const uint32_t* seg,
 }
 
 // Exclusive scan of the kGB partial sums part[which] of each utterance
-// (which = 3: the lattice pass, after the forward pass has stopped).
-__global__ void __launch_bounds__(kGT) k_g_scan(const LaneDesc* __restrict__ lanes, GridLane* gl, int which) {
+// (lattice != 0: after the forward pass has stopped, for utterances whose
+// status is still WD_OK).
+__global__ void __launch_bounds__(kGT) k_g_scan(const LaneDesc* __restrict__ lanes, GridLane* gl, int which,
+                                                int lattice) {
   __shared__ GScratch s;
   GridLane& G = gl[blockIdx.y];
-  if (which < 3 ? G.stop != 0 : lanes[blockIdx.y].info->status != 0) return;
+  if (lattice ? lanes[blockIdx.y].info->status != 0 : G.stop != 0) return;
   unsigned long long* part = G.part[which];
   constexpr uint32_t per = kGB / kGT;
   unsigned long long v[per], sum = 0;
@@ -903,19 +905,18 @@ __global__ void k_gs_final(const LaneDesc* __restrict__ lanes, GridLane* gl) {
   L.info->best_cost = key_cost(G.best_total_key);
 }
 
-// Extra costs of frame t's nodes before relaxation: final extra cost for the
-// last frame, +inf otherwise.
+// Extra costs of all nodes before relaxation: the final extra cost for the
+// last frame's nodes, +inf for the others.
 __global__ void __launch_bounds__(kGT) k_gs_init(DevGraph g, const LaneDesc* __restrict__ lanes,
-                                                 const GridLane* gl, int t) {
+                                                 const GridLane* gl) {
   const LaneDesc& L = lanes[blockIdx.y];
   const GridLane& G = gl[blockIdx.y];
-  if (L.info->status != 0 || t > L.T || G.best_total_key >= kInfKey) return;
-  const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
-  const bool last = t == L.T;
+  if (L.info->status != 0 || G.best_total_key >= kInfKey) return;
+  const uint64_t nT = L.node_off[L.T], n1 = L.node_off[L.T + 1];
   const float best = key_cost(G.best_total_key);
-  for (uint64_t n = n0 + blockIdx.x * kGT + threadIdx.x; n < n1; n += (uint64_t)kGB * kGT) {
+  for (uint64_t n = (uint64_t)blockIdx.x * kGT + threadIdx.x; n < n1; n += (uint64_t)kGB * kGT) {
     uint32_t e = kInfKey;
-    if (last) {
+    if (n >= nT) {
       const float c = key_cost((uint32_t)(L.n_pack[n] >> 32));
       const float F = G.final_used ? canon(c + g.final_w[L.n_state[n]]) : c;
       if (F < INFINITY) e = cost_key(F - best);
@@ -1008,6 +1009,75 @@ __global__ void __launch_bounds__(kGT) k_gs_fill_ab(const LaneDesc* __restrict__
   }
 }
 
+// The lattice node list: nodes marked in the used bitmap, in node id order,
+// which is (t, state) order.  Per-workgroup counts over bitmap chunks, a scan,
+// then one thread per bit as in the frontier compaction.
+__global__ void __launch_bounds__(kGT) k_gn_count(const LaneDesc* __restrict__ lanes, GridLane* gl) {
+  __shared__ GScratch s;
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (L.info->status != 0) return;
+  uint64_t blo, bhi;
+  chunk((L.node_off[L.T + 1] + 31) >> 5, blockIdx.x, &blo, &bhi);
+  unsigned long long c = 0;
+  for (uint64_t w = blo + threadIdx.x; w < bhi; w += kGT) c += (uint32_t)__popc(L.used[w]);
+  c = gsum64(c, s);
+  if (threadIdx.x == 0) G.part[0][blockIdx.x] = c;
+}
+
+__global__ void __launch_bounds__(kGT) k_gn_write(const LaneDesc* __restrict__ lanes, GridLane* gl) {
+  __shared__ GScratch s;
+  __shared__ uint32_t wd[kCW], wp[kCW];
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  LaneInfo* info = L.info;
+  if (info->status != 0) return;
+  if (blockIdx.x == 0 && threadIdx.x == 0) info->out_nodes = G.part[0][kGB];
+  const uint64_t T2 = (uint64_t)L.T + 2;
+  uint64_t blo, bhi;
+  chunk((L.node_off[L.T + 1] + 31) >> 5, blockIdx.x, &blo, &bhi);
+  uint64_t pos0 = G.part[0][blockIdx.x];
+  constexpr uint32_t per = kCW / kGT;
+  for (uint64_t r0 = blo; r0 < bhi; r0 += kCW) {
+    const uint32_t m = (uint32_t)(bhi - r0 < kCW ? bhi - r0 : kCW);
+    uint32_t c = 0;
+#pragma unroll
+    for (uint32_t j = 0; j < per; ++j) {
+      const uint32_t q = threadIdx.x * per + j;
+      const uint32_t w = q < m ? L.used[r0 + q] : 0u;
+      wd[q] = w;
+      wp[q] = c;
+      c += (uint32_t)__popc(w);
+    }
+    unsigned long long tot;
+    const uint32_t ex = (uint32_t)gexcl64(c, s, &tot);
+#pragma unroll
+    for (uint32_t j = 0; j < per; ++j) wp[threadIdx.x * per + j] += ex;
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < m * 32u; j += kGT) {
+      const uint32_t word = wd[j >> 5], b = j & 31u;
+      if (!((word >> b) & 1u)) continue;
+      const uint64_t p = pos0 + wp[j >> 5] + (uint32_t)__popc(word & ((1u << b) - 1u));
+      const uint64_t n = (r0 << 5) + j;
+      // frame of node n: last t with node_off[t] <= n
+      uint64_t lo = 0, hi = T2;
+      while (hi - lo > 1) {
+        const uint64_t mid = (lo + hi) >> 1;
+        if (L.node_off[mid] <= n) lo = mid;
+        else hi = mid;
+      }
+      OutNode o;
+      o.t = (int32_t)lo;
+      o.state = (int32_t)L.n_state[n];
+      o.cost = key_cost((uint32_t)(L.n_pack[n] >> 32));
+      o.extra = key_cost(L.extra_key[n]);
+      L.out_nodes[p] = o;
+    }
+    pos0 += tot;
+    __syncthreads();
+  }
+}
+
 // -------------------------------------------------------------------- launches
 
 size_t grid_lane_bytes() { return sizeof(GridLane); }
@@ -1032,16 +1102,24 @@ void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, in
       }
     if (prm.max_active > 0) hipLaunchKernelGGL(k_g_mark, all, blk, 0, st, lanes, gl);
     hipLaunchKernelGGL(k_g_bits, all, blk, 0, st, g, lanes, gl);
-    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 0);
+    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 0, 0);
     hipLaunchKernelGGL(k_g_compact, all, blk, 0, st, g, lanes, gl);
-    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 1);
+    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 1, 0);
     hipLaunchKernelGGL(k_g_degrees, all, blk, 0, st, g, lanes, gl);
     hipLaunchKernelGGL(k_g_link_count, all, blk, 0, st, g, lanes, gl, t);
-    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 2);
+    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 2, 0);
     hipLaunchKernelGGL(k_g_link_write, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_g_end, one, blk, 0, st, lanes, gl, t);
   }
   hipLaunchKernelGGL(k_g_finish, one, dim3(64), 0, st, lanes, gl);
+}
+
+void launch_grid_nodes(const LaneDesc* lanes, void* glv, int B, hipStream_t st) {
+  GridLane* gl = (GridLane*)glv;
+  const dim3 one(1, B), all(kGB, B), blk(kGT);
+  hipLaunchKernelGGL(k_gn_count, all, blk, 0, st, lanes, gl);
+  hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 0, 1);
+  hipLaunchKernelGGL(k_gn_write, all, blk, 0, st, lanes, gl);
 }
 
 void launch_grid_sweep(const DevGraph& g, const LaneDesc* lanes, void* glv, int B, int maxT, float lattice_beam,
@@ -1051,15 +1129,15 @@ void launch_grid_sweep(const DevGraph& g, const LaneDesc* lanes, void* glv, int 
   hipLaunchKernelGGL(k_gs_final_any, all, blk, 0, st, g, lanes, gl);
   hipLaunchKernelGGL(k_gs_final_min, all, blk, 0, st, g, lanes, gl);
   hipLaunchKernelGGL(k_gs_final, one, dim3(64), 0, st, lanes, gl);
+  hipLaunchKernelGGL(k_gs_init, all, blk, 0, st, g, lanes, gl);
   for (int t = maxT; t >= 0; --t) {
-    hipLaunchKernelGGL(k_gs_init, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, t, 1, 0);
     for (int l = (int)g.nlevels - 1; l >= 0; --l)
       hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, t, 0, l);
   }
   const uint32_t lb_key = cost_key(lattice_beam);
   hipLaunchKernelGGL(k_gk_count, all, blk, 0, st, lanes, gl, lb_key);
-  hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 3);
+  hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 3, 1);
   hipLaunchKernelGGL(k_gk_write, all, blk, 0, st, lanes, gl, lb_key);
   hipLaunchKernelGGL(k_gs_fill_ab, all, blk, 0, st, lanes);
 }

@@ -32,6 +32,7 @@ void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* grid, i
                          const uint32_t* bad, int maxT, hipStream_t s);
 void launch_grid_sweep(const DevGraph& g, const LaneDesc* lanes, void* grid, int B, int maxT, float lattice_beam,
                        hipStream_t s);
+void launch_grid_nodes(const LaneDesc* lanes, void* grid, int B, hipStream_t s);
 void launch_check_loglikes(const LaneDesc* lanes, int B, uint32_t P, uint32_t* bad, hipStream_t s);
 void launch_fill_u64(unsigned long long* p, uint64_t n, unsigned long long v, hipStream_t s);
 void launch_fill_u32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t s);

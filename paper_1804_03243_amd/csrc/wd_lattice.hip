@@ -483,22 +483,10 @@ __global__ void __launch_bounds__(256) k_lat_assemble(DevGraph g, const LaneDesc
     assemble(L, g, true, L.link_off[L.T + 1], L.out_raw, lb_key, info->Z, true, false, first, stride);
 }
 
-// The lattice node list after the chip-wide merge.
-__global__ void __launch_bounds__(kThreads) k_lat_nodes(const LaneDesc* __restrict__ lanes) {
-  __shared__ BlockScratch bs;
-  const LaneDesc& L = lanes[blockIdx.x];
-  LaneInfo* info = L.info;
-  if (info->status != 0) return;
-  uint32_t par = 0;
-  const uint64_t n_out = write_nodes(L, L.node_off[L.T + 1], bs, par);
-  if (threadIdx.x == 0) info->out_nodes = n_out;
-}
-
 void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s) {
   hipLaunchKernelGGL(k_lattice, dim3(B, 2), dim3(kThreads), 0, s, g, lanes, prm);
   if (prm.flags & kFlagSwept) {
     hipLaunchKernelGGL(k_lat_assemble, dim3(1024, B), dim3(256), 0, s, g, lanes, prm);
-    hipLaunchKernelGGL(k_lat_nodes, dim3(B), dim3(kThreads), 0, s, lanes);
   }
 }
 
