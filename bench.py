@@ -7,10 +7,19 @@ lattice pruning, posteriors and the final merge, results copied to the host.
 Inputs (graph and log-likelihoods) are resident in GPU memory before timing.
 
 Prints one JSON line.  `python bench.py [--gpus 1] [--steps K] [--warmup W]`.
+
+Besides the headline line's fields: `roofline.traffic` is the HBM traffic of
+one k_forward launch measured with hardware counters (FETCH_SIZE + WRITE_SIZE,
+each scaled by what the same counter reads for a plain device copy of known
+size), reported only while the kernel sources hash to the ones the counters
+were taken on; `other_workloads` times the chip-wide mode on the wide-beam
+2M-state graph.  `--copy-kernel-bytes N` only runs a plain N-byte device copy
+(the counter calibration run) and exits.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -35,13 +44,77 @@ BYTES_TOKEN = 8 + 12 + 12
 BYTES_LINK = 16
 
 
+# HBM traffic of one k_forward launch on this workload, from rocprofv3 --pmc
+# runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
+# divided by the counter's reading per byte of a plain device copy of known
+# size (bench.py --copy-kernel-bytes).  Valid for the sources with this hash.
+TRAFFIC = {"sources_sha256": "9605d9a9ba029f4fc1d6be23e29d075a2872664dfc8759dbfd56eaae3a6e0886",
+           "bytes_per_launch": 53148409}
+
+
+def sources_sha256() -> str:
+    d = os.path.join(ROOT, "paper_1804_03243_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def copy_kernel(nbytes: int) -> int:
+    """A plain device-to-device copy of nbytes, five times (counter calibration)."""
+    import torch
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_kernel_bytes": nbytes, "launches": 5}), flush=True)
+    return 0
+
+
+def wide_chip(wfstdec, steps: int = 3) -> dict:
+    """Chip-wide mode on the wide-beam 2M-state graph (800 frames, beam 20,
+    no max-active): full decodes, lattice and posteriors included."""
+    import synth
+    import torch
+    cfg = synth.workload("wide_2m")
+    g = synth.make_graph(cfg)
+    L = synth.make_loglikes(cfg)
+    graph = wfstdec.Graph(g, cfg["P"], "cuda:0")
+    x = torch.from_numpy(L).to(graph.device)
+    args = (cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    r = wfstdec.decode(graph, x, *args, timing=True, mode="chip")  # sizes the workspace
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    fwd, lat = [], []
+    for _ in range(steps):
+        r = wfstdec.decode(graph, x, *args, timing=True, mode="chip")
+        fwd.append(r.stats["forward_ms"])
+        lat.append(r.stats["lattice_ms"])
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    T = L.shape[0]
+    st = r.stats
+    out = {"workload": "wide_2m", "mode": "chip", "frames": T, "steps": steps,
+           "frames_per_s": round(T / wall, 1), "ms_per_step": round(1e3 * wall, 2),
+           "arcs_expanded_per_s": round(st["arcs_expanded"] / wall, 1),
+           "tokens_per_frame": round(st["tokens"] / (T + 1), 1),
+           "raw_links": st["raw_links"], "kept_links": st["kept_links"],
+           "kernel_ms": {"forward": round(sum(fwd) / steps, 2), "lattice": round(sum(lat) / steps, 2)}}
+    del graph
+    torch.cuda.empty_cache()
+    return out
+
+
 def algorithmic_bytes(stats: dict) -> int:
     emit = stats["arcs_expanded"] - stats["eps_arcs_expanded"]
     return (stats["arcs_expanded"] * BYTES_ARC + emit * BYTES_LOGLIKE +
             stats["tokens"] * BYTES_TOKEN + stats["raw_links"] * BYTES_LINK)
 
 
-def cpu_baseline(g, L, cfg, min_seconds: float = 10.0) -> dict:
+def cpu_baseline(g, L, cfg, workload, min_seconds: float = 10.0) -> dict:
     """The CPU oracle (plain sequential C, one thread) on the same utterance,
     repeated until about `min_seconds` of CPU work."""
     import oracle
@@ -54,7 +127,7 @@ def cpu_baseline(g, L, cfg, min_seconds: float = 10.0) -> dict:
         if dt >= min_seconds:
             break
     return {"value": round(runs * L.shape[0] / dt, 2), "unit": "frames/s", "cores": 1, "kind": "oracle",
-            "sample": f"{WORKLOAD} full utterance ({L.shape[0]} frames) x {runs} runs, one thread, "
+            "sample": f"{workload} full utterance ({L.shape[0]} frames) x {runs} runs, one thread, "
                       f"{dt:.1f} s"}
 
 
@@ -64,11 +137,18 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true", help="skip other_workloads")
+    ap.add_argument("--copy-kernel-bytes", type=int, default=0)
+    ap.add_argument("--workload", default=WORKLOAD,
+                    help="workload timed (the headline line is hclg_5m; others are for profiling)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this decoder runs on one GPU; --gpus {args.gpus} is not supported "
               "(utterances shard across GPUs with no exchange, see DESIGN.md)", file=sys.stderr)
         return 2
+
+    if args.copy_kernel_bytes:
+        return copy_kernel(args.copy_kernel_bytes)
 
     import numpy as np
     import torch
@@ -76,7 +156,8 @@ def main() -> int:
     import synth
     from paper_1804_03243_amd import wfstdec
 
-    cfg = synth.workload(WORKLOAD)
+    workload = args.workload
+    cfg = synth.workload(workload)
     g = synth.make_graph(cfg)
     L = synth.make_loglikes(cfg)
     dev = torch.device("cuda:0")
@@ -103,6 +184,10 @@ def main() -> int:
     fwd = float(np.mean(fwd_ms))
     bytes_launch = algorithmic_bytes(st)
     achieved = bytes_launch / (fwd * 1e-3) / 1e9
+    traffic = (TRAFFIC["bytes_per_launch"]
+               if TRAFFIC and workload == WORKLOAD and TRAFFIC["sources_sha256"] == sources_sha256()
+               else None)
+    chip = cfg["max_active"] == 0 or cfg["max_active"] >= wfstdec.WD_CHIP_WIDE_MAX_ACTIVE
     out = {
         "metric": METRIC,
         "value": round(fps, 2),
@@ -116,19 +201,23 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": WORKLOAD, "states": cfg["S"], "arcs": cfg["A"], "frames": T,
+        "config": {"workload": workload, "states": cfg["S"], "arcs": cfg["A"], "frames": T,
                    "pdfs": cfg["P"], "beam": beam, "max_active": ma, "lattice_beam": lb,
                    "utterances_per_step": 1},
         "arcs_expanded_per_s": round(st["arcs_expanded"] * args.steps / wall, 1),
         "rtf": round((wall / args.steps) / (T / FRAME_RATE), 7),
         "tokens_per_frame": round(st["tokens"] / (T + 1), 1),
         "kernel_ms": {"forward": round(fwd, 3), "lattice": round(float(np.mean(lat_ms)), 3)},
-        "roofline": {"bound": "hbm", "kernel": "k_forward", "achieved": round(achieved, 3),
+        "roofline": {"bound": "hbm", "kernel": "chip-wide forward kernels" if chip else "k_forward", "achieved": round(achieved, 3),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
-                     "traffic": None, "algorithmic_bytes_per_launch": int(bytes_launch)},
+                     "traffic": traffic, "algorithmic_bytes_per_launch": int(bytes_launch)},
     }
+    if not args.no_extra and workload == WORKLOAD:
+        del graph, x
+        torch.cuda.empty_cache()
+        out["other_workloads"] = [wide_chip(wfstdec)]
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(g, L, cfg)
+        out["cpu_baseline"] = cpu_baseline(g, L, cfg, workload)
     print(json.dumps(out), flush=True)
     return 0
 
