@@ -34,6 +34,8 @@ struct GridLane {
   uint32_t W, n_prev, W_next, W_eps;
   uint32_t n_touched, n_surv, n_keep;
   uint32_t best_key, kcutb, cut_key;
+  uint32_t best_pos;    // frontier position of a token with the frame's best cost
+  uint32_t ub;          // cutoff prefilter bound of the frame being expanded (a key)
   uint32_t nbits, shift;
   uint32_t sel_active, sel_rank, sel_prefix, sel_less, sel_bits;
   uint32_t xmask;
@@ -181,11 +183,41 @@ __global__ void k_g_init(const LaneDesc* __restrict__ lanes, GridLane* gl, const
   }
 }
 
-// Frame start: the start token (t = 0) or the emitting work check (t > 0).
-__global__ void k_g_begin(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl, int t) {
+// Frame start: the start token (t = 0), or the emitting work check and the
+// cutoff prefilter bound (t > 0).  The bound (Sec. 4.3 prunes each transition
+// against a beam as it is made): the best emitting candidate of one best token
+// of frame t-1, plus the beam.  That candidate is one of all the frame's
+// candidates, so the exact beam cutoff (best of all, plus the beam) is not
+// above the bound, and a candidate above the bound can never survive or
+// become a lattice link: expansion skips its recombination.  One wavefront.
+__global__ void k_g_begin(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl, Params prm, int t) {
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
-  if (G.stop || threadIdx.x != 0) return;
+  if (G.stop) return;
+  if (t > 0) {
+    const uint32_t p = G.best_pos;
+    uint32_t m = 0xffffffffu;
+    if (p < G.n_prev) {
+      const float c = key_cost(L.f_key[p]);
+      const uint32_t a0 = L.f_ebeg[p], deg = L.f_edeg[p + 1] - L.f_edeg[p];
+      const float* row = L.ll + (size_t)(t - 1) * g.P;
+      for (uint32_t j = threadIdx.x; j < deg; j += 64) {
+        const uint4 r = g.earc[a0 + j];
+        const float ac = -row[(r.z & 0xffffffu) - 1u];
+        float x = c + ac;
+        x = canon(x + __uint_as_float(r.y));
+        const uint32_t xk = cost_key(x);
+        m = xk < m ? xk : m;
+      }
+    }
+#pragma unroll
+    for (int k = 32; k > 0; k >>= 1) {
+      const uint32_t o = __shfl_xor(m, k, 64);
+      m = o < m ? o : m;
+    }
+    if (threadIdx.x == 0) G.ub = m < kInfKey ? cost_key(key_cost(m) + prm.beam) : 0xffffffffu;
+  }
+  if (threadIdx.x != 0) return;
   if (t == 0) {
     const uint32_t s0 = g.start;
     L.slot[s0] = pack_tok(cost_key(0.0f), kNoArc);
@@ -285,7 +317,7 @@ __global__ void __launch_bounds__(kGT) k_g_expand(DevGraph g, const LaneDesc* __
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop || t == 0) return;
-  const uint32_t W = G.W, n_prev = G.n_prev;
+  const uint32_t W = G.W, n_prev = G.n_prev, ub = G.ub;
   const uint64_t nbp = G.node_base_prev;
   const float* row = L.ll + (size_t)(t - 1) * g.P;
   uint64_t blo, bhi;
@@ -306,7 +338,7 @@ __global__ void __launch_bounds__(kGT) k_g_expand(DevGraph g, const LaneDesc* __
         float x = c + ac;
         x = canon(x + __uint_as_float(r.y));
         const uint32_t xk = cost_key(x);
-        if (xk < kInfKey) {
+        if (xk < kInfKey && xk <= ub) {
           const unsigned long long old = atomicMin(&L.slot[r.x], pack_tok(xk, r.w));
           my_best = xk < my_best ? xk : my_best;
           if (old == kEmpty) stage_touch(ts, G, L, g, r.x, r.z >> 24);
@@ -324,6 +356,7 @@ __global__ void __launch_bounds__(kGT) k_g_expand(DevGraph g, const LaneDesc* __
 __global__ void k_g_cut(GridLane* gl, Params prm) {
   GridLane& G = gl[blockIdx.y];
   if (G.stop || threadIdx.x != 0) return;
+  G.best_pos = 0xffffffffu;  // set again by this frame's compaction
   if (G.best_key >= kInfKey) {
     G.status = 3;  // WD_ENOPATH
     G.stop = 1;
@@ -592,6 +625,7 @@ __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* _
   uint64_t pos0 = G.part[0][blockIdx.x];
   const uint64_t nb = G.node_base;
   const bool store = G.hist_ok != 0;
+  const uint32_t best = G.best_key;
   unsigned long long deg = 0;
   constexpr uint32_t per = kCW / kGT;
   for (uint64_t r0 = blo; r0 < bhi; r0 += kCW) {
@@ -630,6 +664,7 @@ __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* _
       L.f_state[p] = st;
       L.f_key[p] = (uint32_t)(v >> 32);
       L.f_arc[p] = (uint32_t)v;
+      if ((uint32_t)(v >> 32) == best) atomicMin(&G.best_pos, (uint32_t)p);
       const uint2 o0 = g.off[st], o1 = g.off[st + 1];
       deg += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
     }
@@ -1088,7 +1123,7 @@ void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, in
   const dim3 one(1, B), all(kGB, B), blk(kGT);
   hipLaunchKernelGGL(k_g_init, one, blk, 0, st, lanes, gl, bad);
   for (int t = 0; t <= maxT; ++t) {
-    hipLaunchKernelGGL(k_g_begin, one, dim3(64), 0, st, g, lanes, gl, t);
+    hipLaunchKernelGGL(k_g_begin, one, dim3(64), 0, st, g, lanes, gl, prm, t);
     hipLaunchKernelGGL(k_g_expand, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_g_cut, one, dim3(64), 0, st, gl, prm);
     for (uint32_t l = 0; l < g.nlevels; ++l) hipLaunchKernelGGL(k_g_level, all, blk, 0, st, g, lanes, gl, l);
