@@ -47,18 +47,20 @@ BYTES_LINK = 16
 # HBM traffic of one k_forward launch on this workload, from rocprofv3 --pmc
 # runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
 # divided by the counter's reading per byte of a plain device copy of known
-# size (bench.py --copy-kernel-bytes).  Valid for the sources with this hash.
-TRAFFIC = {"sources_sha256": "9605d9a9ba029f4fc1d6be23e29d075a2872664dfc8759dbfd56eaae3a6e0886",
+# size (bench.py --copy-kernel-bytes).  Valid while k_forward's sources hash to this.
+TRAFFIC = {"sources_sha256": "da63e369ba08b1970dcb59ab63aa5d50d582edf2d4ccc41ca9e96e45718a0355",
            "bytes_per_launch": 53148409}
+
+
+FORWARD_SOURCES = ("wd_block.h", "wd_common.h", "wd_forward.hip")  # what k_forward is built from
 
 
 def sources_sha256() -> str:
     d = os.path.join(ROOT, "paper_1804_03243_amd", "csrc")
     h = hashlib.sha256()
-    for name in sorted(os.listdir(d)):
-        if name.endswith((".hip", ".h")):
-            with open(os.path.join(d, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for name in FORWARD_SOURCES:
+        with open(os.path.join(d, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
 
 
