@@ -70,3 +70,23 @@ def test_wide_2m_prefix(wf, oracle_mod, name, T, debug, mode):
     o = oracle_mod.decode(g, L, cfg["beam"], cfg["max_active"], cfg["lattice_beam"], debug=debug)
     assert r.stats["max_tokens"] > 100000
     assert_same(r, o, debug=debug)
+
+
+@pytest.mark.parametrize("name", ["wide_2m", "wide_2m_dyadic"])
+def test_wide_2m_full(wf, name):
+    """All 800 frames in chip-wide mode, as bench.py times them: the oracle
+    needs ~2 s per frame here, so the result is checked by the properties
+    that define it (tests/lattice_props.py, pinned on oracle results); the
+    first frames are compared with the oracle bit for bit above."""
+    import torch
+    import lattice_props
+    cfg = synth.workload(name)
+    print(f"\n[gpu case] {name} full ({cfg['T']} frames) mode=chip", flush=True)
+    g = synth.make_graph(cfg)
+    L = synth.make_loglikes(cfg)
+    graph = wf.Graph(g, cfg["P"])
+    r = wf.decode(graph, torch.from_numpy(L).to(graph.device), cfg["beam"], cfg["max_active"],
+                  cfg["lattice_beam"], mode="chip")
+    assert r.stats["max_tokens"] > 500000 and r.stats["raw_links"] > 500_000_000
+    unique = lattice_props.check(g, L, cfg["lattice_beam"], r)
+    assert unique or name.endswith("dyadic")
