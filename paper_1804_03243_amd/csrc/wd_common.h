@@ -47,6 +47,7 @@ __host__ __device__ inline uint64_t pack_tok(uint32_t key, uint32_t arc) {
 //   off[s]  = {first emitting arc, first epsilon arc} of state s (S+1 entries)
 //   earc[i] = {dst, weight bits, ilabel | dst_class << 24, arc id}
 //   xarc[j] = {dst, weight bits, dst_class, arc id}
+//   xnext[j] = epsilon arc range {first, end} of xarc[j]'s destination
 // Arcs of a state keep the caller's order, so within a state arc ids ascend.
 // dst_class is the epsilon level of the destination state when it has
 // epsilon out-arcs, else kNoEps.  Epsilon arcs always climb to a strictly
@@ -55,6 +56,7 @@ struct DevGraph {
   const uint2* off;
   const uint4* earc;
   const uint4* xarc;
+  const uint2* xnext;
   const uint8_t* sclass;       // [S] class of every state
   const float* final_w;        // [S] or nullptr
   const int32_t* ilabel_id;    // [A] by caller arc id

@@ -24,9 +24,12 @@ namespace wd {
 constexpr uint32_t kNoKey = 0xffffffffu;
 constexpr uint32_t kLdsWork = 3 * kHashMax;  // emitting work above which a frame starts global
 constexpr uint32_t kBkCap = 1024;            // LDS epsilon bucket entries before a frame spills
+static_assert(kBkCap == (uint32_t)kThreads, "one bucket entry per thread in the epsilon level scan");
 
 struct FwdShared {
   BlockScratch bs;
+  // utterance counters, kept by thread 0 (in LDS to spare registers)
+  unsigned long long c_arcs, c_tokens, c_max_tokens, c_need_frame, c_need_arcs;
   uint32_t n_touched;  // global table: touched states
   uint32_t n_surv;     // survivors of the beam cutoff
   uint32_t n_rank;
@@ -45,6 +48,7 @@ struct FwdShared {
   uint32_t h_key[kHashCap];
   unsigned long long h_val[kHashCap];
   uint4 bk[kBkCap];    // {table slot, first epsilon arc, end epsilon arc, level}
+  uint32_t xp[kBkCap]; // epsilon arcs of the bucket entries before entry i (one level)
   uint32_t f_state[kFrontCap + 1];
   uint32_t f_key[kFrontCap + 1];
   uint32_t f_arc[kFrontCap + 1];
@@ -214,14 +218,21 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
   uint64_t node_base = 0, node_base_prev = 0, link_base = 0;
   uint32_t n_prev = 0, W = 0;
   bool front_lds = true;  // where the frontier of the last finished frame is
-  uint64_t my_arcs = 0, my_eps = 0, tokens = 0, max_tokens = 0, need_frame = 1, need_arcs = 0;
+  uint64_t my_eps = 0;
+  if (tid == 0) {
+    sh.c_arcs = 0;
+    sh.c_tokens = 0;
+    sh.c_max_tokens = 0;
+    sh.c_need_frame = 1;
+    sh.c_need_arcs = 0;
+  }
   bool hist_ok = true;  // history (nodes, links) still being stored
   uint32_t par = 0;     // scratch buffer parity of the workgroup collectives
   int t = 0;
 
   for (t = 0; t <= T; ++t) {
     if (t > 0) {
-      need_arcs = W > need_arcs ? W : need_arcs;
+      if (tid == 0 && W > sh.c_need_arcs) sh.c_need_arcs = W;
       if (W > L.cand_cap) {
         status = 4;  // WD_ECAPACITY
         ovf |= kOvfArcs;
@@ -235,6 +246,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     uint32_t nbits = 0, shift = 0;
     uint64_t eps_frame = 0;
     bool failed = false;
+    uint4 my_c = make_uint4(0, 0, 0, 0);  // this thread's first candidate (work item tid)
     // ---------------------------------------------------- token passing
     for (int attempt = 0; attempt < 2; ++attempt) {
       eps_frame = 0;
@@ -277,7 +289,9 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
                 }
               }
             }
-            L.cand[w] = make_uint4(r.w, (uint32_t)(node_base_prev + i), dst, __float_as_uint(x));
+            const uint4 cv = make_uint4(r.w, (uint32_t)(node_base_prev + i), dst, __float_as_uint(x));
+            L.cand[w] = cv;
+            if (base == 0) my_c = cv;
           }
           best_key = (uint32_t)block_min64(my_best, sh.bs, par);
           if (best_key >= kInfKey) {
@@ -295,29 +309,35 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         kcutb = cost_key(cutb);
         for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
           if (sh.nbl[lvl] == 0) continue;  // uniform: written only by lower levels
+          // this level's entries within the cutoff spread their epsilon arcs
+          // over the workgroup: entry i (one per thread) owns arcs
+          // [xp[i], xp[i] + its degree) of the level's work space.  Every
+          // thread reads the entry count before the scan's barrier; entries
+          // appended below (higher levels) come after it.
           const uint32_t n = sh.n_bk < kBkCap ? sh.n_bk : kBkCap;
-          for (uint32_t i = tid; i < n; i += kThreads) {
-            const uint4 e = sh.bk[i];
-            if (e.w != lvl) continue;
-            const uint32_t k = (uint32_t)(sh.h_val[e.x] >> 32);
-            if (k > kcutb) continue;
-            const float c = key_cost(k);
-            eps_frame += e.z - e.y;
-            for (uint32_t a = e.y; a < e.z; ++a) {
-              const uint4 r = g.xarc[a];
-              const uint32_t xk = cost_key(canon(c + __uint_as_float(r.y)));
-              if (xk > kcutb || xk >= kInfKey || sh.spill) continue;
-              uint2 o0 = make_uint2(0, 0), o1 = make_uint2(0, 0);
-              if (r.z != kNoEps) {
-                o0 = g.off[r.x];
-                o1 = g.off[r.x + 1];
-              }
-              bool fresh;
-              const uint32_t slot = h_insert(sh, r.x, &fresh);
-              if (slot < (uint32_t)kHashCap) {
-                atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
-                if (fresh && r.z != kNoEps) lds_bucket(sh, slot, o0, o1, r.z);
-              }
+          uint32_t d = 0;
+          if (tid < n) {
+            const uint4 e = sh.bk[tid];
+            if (e.w == lvl && (uint32_t)(sh.h_val[e.x] >> 32) <= kcutb) d = e.z - e.y;
+          }
+          eps_frame += d;
+          uint32_t tot;
+          sh.xp[tid] = block_excl_scan(d, sh.bs, par, &tot);
+          __syncthreads();
+          for (uint32_t w = tid; w < tot; w += kThreads) {
+            const uint32_t j = search_le(sh.xp, n, w);
+            const uint4 e = sh.bk[j];
+            const uint32_t a = e.y + (w - sh.xp[j]);
+            const uint4 r = g.xarc[a];
+            const uint2 nx = g.xnext[a];  // the destination's epsilon arcs
+            const float c = key_cost((uint32_t)(sh.h_val[e.x] >> 32));
+            const uint32_t xk = cost_key(canon(c + __uint_as_float(r.y)));
+            if (xk > kcutb || xk >= kInfKey || sh.spill) continue;
+            bool fresh;
+            const uint32_t slot = h_insert(sh, r.x, &fresh);
+            if (slot < (uint32_t)kHashCap) {
+              atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
+              if (fresh && r.z != kNoEps) lds_bucket(sh, slot, make_uint2(0, nx.x), make_uint2(0, nx.y), r.z);
             }
           }
           __syncthreads();
@@ -346,7 +366,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         }
         __syncthreads();
         ns = sh.n_surv;
-        need_frame = sh.hcount > need_frame ? sh.hcount : need_frame;
+        if (tid == 0 && sh.hcount > sh.c_need_frame) sh.c_need_frame = sh.hcount;
       } else {
         // --------------------------------------- global per-state slot array
         if (t == 0) {
@@ -384,7 +404,9 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
                 first = old == kEmpty;
                 my_best = xk < my_best ? xk : my_best;
               }
-              L.cand[w] = make_uint4(r.w, (uint32_t)(node_base_prev + i), dst, __float_as_uint(x));
+              const uint4 cv = make_uint4(r.w, (uint32_t)(node_base_prev + i), dst, __float_as_uint(x));
+              L.cand[w] = cv;
+              if (base == 0) my_c = cv;
             }
             note_touch(first, dst, cls, sh, g, L);
           }
@@ -419,7 +441,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           __syncthreads();
         }
         const uint32_t nt = sh.n_touched;
-        need_frame = nt > need_frame ? nt : need_frame;
+        if (tid == 0 && nt > sh.c_need_frame) sh.c_need_frame = nt;
         if (nt > L.frame_cap) {
           status = 4;
           ovf |= kOvfFrame;
@@ -454,7 +476,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     }
     if (failed) break;
     my_eps += eps_frame;
-    if (t > 0 && tid == 0) my_arcs += W;
+    if (t > 0 && tid == 0) sh.c_arcs += W;
     const float best = key_cost(best_key);
     const float cutb = key_cost(kcutb);
     const unsigned long long* spack = lds ? sh.rs_pack : L.surv_pack;
@@ -657,8 +679,10 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       L.cutb[t] = cutb;
       L.cut[t] = key_cost(cut_key);
     }
-    tokens += n_keep;
-    max_tokens = n_keep > max_tokens ? n_keep : max_tokens;
+    if (tid == 0) {
+      sh.c_tokens += n_keep;
+      if (n_keep > sh.c_max_tokens) sh.c_max_tokens = n_keep;
+    }
     // -------------------------------------------------- lattice links of frame t
     // node id of a state that survived frame t
     auto dst_node = [&](uint32_t s) -> uint64_t {
@@ -676,9 +700,11 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       const uint32_t per = (Wc + kThreads - 1) / kThreads;
       const uint32_t w0 = tid * per < Wc ? tid * per : Wc;
       const uint32_t w1 = w0 + per < Wc ? w0 + per : Wc;
+      // with one item per thread, the item is the thread's own candidate
       uint32_t cnt = 0;
       for (uint32_t w = w0; w < w1; ++w) {
-        const uint32_t xk = cost_key(__uint_as_float(L.cand[w].w));
+        const uint32_t xb = per == 1 ? my_c.w : L.cand[w].w;
+        const uint32_t xk = cost_key(__uint_as_float(xb));
         cnt += xk <= cut_key && xk < kInfKey;
       }
       // epsilon run: every epsilon out-arc of the frontier within the cutoff
@@ -686,11 +712,15 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       const uint32_t e0 = tid * perx < W_eps ? tid * perx : W_eps;
       const uint32_t e1 = e0 + perx < W_eps ? e0 + perx : W_eps;
       uint32_t cntx = 0;
+      uint4 rx0 = make_uint4(0, 0, 0, 0);  // the thread's first epsilon arc, reused below
+      uint32_t px0 = 0;
       if (e0 < e1) {
         uint32_t p = search_le(f.xdeg, n_keep, e0);
+        px0 = p;
         for (uint32_t e = e0; e < e1; ++e) {
           while (f.xdeg[p + 1] <= e) ++p;
           const uint4 r = g.xarc[f.xbeg[p] + (e - f.xdeg[p])];
+          if (e == e0) rx0 = r;
           const uint32_t xk = cost_key(canon(key_cost(f.key[p]) + __uint_as_float(r.y)));
           cntx += xk <= cut_key && xk < kInfKey;
         }
@@ -706,7 +736,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       }
       if (hist_ok) {
         for (uint32_t w = w0; w < w1; ++w) {
-          const uint4 c = L.cand[w];
+          uint4 c = my_c;
+          if (per != 1) c = L.cand[w];
           const uint32_t xk = cost_key(__uint_as_float(c.w));
           if (!(xk <= cut_key && xk < kInfKey)) continue;
           const uint64_t dn = dst_node(c.z);
@@ -720,10 +751,11 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           if (f.key[q] == xk && f.arc[q] == c.x) L.n_pred[dn] = c.y;
         }
         if (e0 < e1) {
-          uint32_t p = search_le(f.xdeg, n_keep, e0);
+          uint32_t p = px0;
           for (uint32_t e = e0; e < e1; ++e) {
             while (f.xdeg[p + 1] <= e) ++p;
-            const uint4 r = g.xarc[f.xbeg[p] + (e - f.xdeg[p])];
+            uint4 r = rx0;
+            if (e != e0) r = g.xarc[f.xbeg[p] + (e - f.xdeg[p])];
             const float x = canon(key_cost(f.key[p]) + __uint_as_float(r.y));
             const uint32_t xk = cost_key(x);
             if (!(xk <= cut_key && xk < kInfKey)) continue;
@@ -775,7 +807,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
   }
 
   const uint64_t eps = block_sum64(my_eps, sh.bs, par);
-  const uint64_t arcs = block_sum64(my_arcs, sh.bs, par) + eps;
+  const uint64_t arcs = sh.c_arcs + eps;  // thread 0's own write; read by thread 0 below
   if (tid == 0) {
     LaneInfo* info = L.info;
     if (status == 0 && (ovf & (kOvfNodes | kOvfLinks))) status = 4;
@@ -784,11 +816,11 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     info->overflow = ovf;
     info->arcs_expanded = arcs;
     info->eps_arcs = eps;
-    info->tokens = tokens;
-    info->max_tokens = max_tokens;
+    info->tokens = sh.c_tokens;
+    info->max_tokens = sh.c_max_tokens;
     info->links = link_base;
-    info->need_frame_tokens = need_frame;
-    info->need_frame_arcs = need_arcs;
+    info->need_frame_tokens = sh.c_need_frame;
+    info->need_frame_arcs = sh.c_need_arcs;
   }
 }
 

@@ -5,7 +5,9 @@
 // split into two CSRs of 16-byte records so the emitting expansion reads only
 // the arcs it uses, each with one 16-byte load.  Epsilon levels (longest
 // epsilon path into a state) order the epsilon closure: an epsilon arc always
-// climbs to a higher level.
+// climbs to a higher level.  Beside each epsilon arc sits its destination's
+// epsilon arc range, so a closure step that reaches a state with epsilon arcs
+// needs no second, dependent read of the offsets.
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -20,13 +22,14 @@ namespace {
 struct Prepared {
   std::vector<uint2> off;
   std::vector<uint4> earc, xarc;
+  std::vector<uint2> xnext;
   std::vector<uint8_t> sclass;
   std::vector<uint32_t> level_base;
   uint32_t nlevels = 0;
 };
 
 struct Layout {
-  uint64_t off, earc, xarc, sclass, final_w, ilabel, olabel, weight, level_base, total;
+  uint64_t off, earc, xarc, xnext, sclass, final_w, ilabel, olabel, weight, level_base, total;
 };
 
 Layout layout(int64_t S, int64_t A, uint64_t Ae, uint64_t Ax, uint32_t nlevels, bool finals) {
@@ -40,6 +43,7 @@ Layout layout(int64_t S, int64_t A, uint64_t Ae, uint64_t Ax, uint32_t nlevels, 
   l.off = take(sizeof(uint2) * (uint64_t)(S + 1));
   l.earc = take(sizeof(uint4) * (Ae ? Ae : 1));
   l.xarc = take(sizeof(uint4) * (Ax ? Ax : 1));
+  l.xnext = take(sizeof(uint2) * (Ax ? Ax : 1));
   l.sclass = take((uint64_t)S);
   l.final_w = finals ? take(sizeof(float) * (uint64_t)S) : 0;
   l.ilabel = take(sizeof(int32_t) * (uint64_t)(A ? A : 1));
@@ -149,6 +153,11 @@ wd_status prepare(const wd_graph_desc* d, Prepared& p, uint64_t* Ae_out, uint64_
       else
         p.xarc[ix++] = make_uint4(v, wbits, p.sclass[v], a);
     }
+  p.xnext.resize(Ax);
+  for (uint64_t j = 0; j < Ax; ++j) {
+    const uint32_t v = p.xarc[j].x;
+    p.xnext[j] = make_uint2(p.off[v].y, p.off[v + 1].y);
+  }
   (void)A;
   *Ae_out = Ae;
   *Ax_out = Ax;
@@ -193,6 +202,7 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
   if ((st = put(l.off, p.off.data(), sizeof(uint2) * (S + 1))) ||
       (st = put(l.earc, p.earc.data(), sizeof(uint4) * Ae)) ||
       (st = put(l.xarc, p.xarc.data(), sizeof(uint4) * Ax)) ||
+      (st = put(l.xnext, p.xnext.data(), sizeof(uint2) * Ax)) ||
       (st = put(l.sclass, p.sclass.data(), (uint64_t)S)) ||
       (finals && (st = put(l.final_w, d->final_weight, sizeof(float) * S))) ||
       (st = put(l.ilabel, d->ilabel, sizeof(int32_t) * A)) ||
@@ -214,6 +224,7 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
   dg.off = (const uint2*)(base + l.off);
   dg.earc = (const uint4*)(base + l.earc);
   dg.xarc = (const uint4*)(base + l.xarc);
+  dg.xnext = (const uint2*)(base + l.xnext);
   dg.sclass = (const uint8_t*)(base + l.sclass);
   dg.final_w = finals ? (const float*)(base + l.final_w) : nullptr;
   dg.ilabel_id = (const int32_t*)(base + l.ilabel);
