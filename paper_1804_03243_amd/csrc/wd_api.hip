@@ -121,6 +121,7 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
   char* beta = take(8 * c.nodes);
   char* used = take(4 * R.used_words);
   char* kept_idx = take(8 * c.kept);
+  char* post = take(16 * c.kept);
   char* kframe = take(16 * T2);
   char* out_links = take(sizeof(OutLink) * c.kept);
   char* out_raw = take(sizeof(OutLink) * c.raw);
@@ -175,6 +176,7 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
       L.beta = (double*)at(beta, 8 * c.nodes);
       L.used = (uint32_t*)at(used, 4 * R.used_words);
       L.kept_idx = (uint64_t*)at(kept_idx, 8 * c.kept);
+      L.post = (uint4*)at(post, 16 * c.kept);
       L.kframe = (uint64_t*)at(kframe, 16 * T2);
       L.out_links = (OutLink*)at(out_links, sizeof(OutLink) * c.kept);
       L.out_raw = (OutLink*)at(out_raw, sizeof(OutLink) * c.raw);

@@ -47,13 +47,15 @@ __device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int m) {
 // make each collective cost one barrier: a wave can only come back to a buffer
 // after every wave has passed the barrier of the collective in between, i.e.
 // after every wave has read it.  `par` is per thread, flipped by every
-// collective; all threads call the same sequence of collectives.
+// collective; all threads call the same sequence of collectives.  NW is the
+// workgroup's wavefront count (the scratch holds up to kWaves).
 struct BlockScratch {
   uint32_t w32[2][kWaves];
   unsigned long long w64[2][kWaves];
 };
 
 // Exclusive prefix sum over the workgroup (thread order); *total = sum.
+template <int NW = kWaves>
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, BlockScratch& bs, uint32_t& par,
                                                     uint32_t* total) {
   const uint32_t b = par;
@@ -63,7 +65,7 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, BlockScratch& bs
   __syncthreads();
   uint32_t before = 0, tot = 0;
 #pragma unroll
-  for (int i = 0; i < kWaves; ++i) {
+  for (int i = 0; i < NW; ++i) {
     const uint32_t x = bs.w32[b][i];
     before += (uint32_t)i < wave_id() ? x : 0u;
     tot += x;
@@ -72,6 +74,7 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, BlockScratch& bs
   return before + inc - v;
 }
 
+template <int NW = kWaves>
 __device__ __forceinline__ uint64_t block_excl_scan64(uint64_t v, BlockScratch& bs, uint32_t& par,
                                                       uint64_t* total) {
   const uint32_t b = par;
@@ -81,7 +84,7 @@ __device__ __forceinline__ uint64_t block_excl_scan64(uint64_t v, BlockScratch& 
   __syncthreads();
   uint64_t before = 0, tot = 0;
 #pragma unroll
-  for (int i = 0; i < kWaves; ++i) {
+  for (int i = 0; i < NW; ++i) {
     const uint64_t x = bs.w64[b][i];
     before += (uint32_t)i < wave_id() ? x : 0ull;
     tot += x;
@@ -90,6 +93,7 @@ __device__ __forceinline__ uint64_t block_excl_scan64(uint64_t v, BlockScratch& 
   return before + inc - v;
 }
 
+template <int NW = kWaves>
 __device__ __forceinline__ uint64_t block_min64(uint64_t v, BlockScratch& bs, uint32_t& par) {
   const uint32_t b = par;
   par ^= 1u;
@@ -102,10 +106,11 @@ __device__ __forceinline__ uint64_t block_min64(uint64_t v, BlockScratch& bs, ui
   __syncthreads();
   uint64_t r = bs.w64[b][0];
 #pragma unroll
-  for (int i = 1; i < kWaves; ++i) r = bs.w64[b][i] < r ? bs.w64[b][i] : r;
+  for (int i = 1; i < NW; ++i) r = bs.w64[b][i] < r ? bs.w64[b][i] : r;
   return r;
 }
 
+template <int NW = kWaves>
 __device__ __forceinline__ uint64_t block_sum64(uint64_t v, BlockScratch& bs, uint32_t& par) {
   const uint32_t b = par;
   par ^= 1u;
@@ -115,10 +120,11 @@ __device__ __forceinline__ uint64_t block_sum64(uint64_t v, BlockScratch& bs, ui
   __syncthreads();
   uint64_t r = 0;
 #pragma unroll
-  for (int i = 0; i < kWaves; ++i) r += bs.w64[b][i];
+  for (int i = 0; i < NW; ++i) r += bs.w64[b][i];
   return r;
 }
 
+template <int NW = kWaves>
 __device__ __forceinline__ uint32_t block_or(uint32_t v, BlockScratch& bs, uint32_t& par) {
   const uint32_t b = par;
   par ^= 1u;
@@ -128,7 +134,7 @@ __device__ __forceinline__ uint32_t block_or(uint32_t v, BlockScratch& bs, uint3
   __syncthreads();
   uint32_t r = 0;
 #pragma unroll
-  for (int i = 0; i < kWaves; ++i) r |= bs.w32[b][i];
+  for (int i = 0; i < NW; ++i) r |= bs.w32[b][i];
   return r;
 }
 

@@ -178,6 +178,8 @@ struct LaneDesc {
   double* beta;                // [node_cap]
   uint32_t* used;              // [ceil(node_cap/32)+1] lattice-node bitmap
   uint64_t* kept_idx;          // [kept_cap] kept link ids in link order
+  uint4* post;                 // [kept_cap] kept links for forward-backward:
+                               //   {src node, dst node, weight bits, -loglike bits | source level}
   uint64_t* kframe;            // [2*(T+2)] per frame: first kept link, first kept epsilon link
   // outputs
   OutLink* out_links;          // [kept_cap]

@@ -1010,7 +1010,10 @@ __global__ void __launch_bounds__(kGT) k_gk_count(const LaneDesc* __restrict__ l
   if (threadIdx.x == 0) G.part[3][blockIdx.x] = c;
 }
 
-__global__ void __launch_bounds__(kGT) k_gk_write(const LaneDesc* __restrict__ lanes, GridLane* gl,
+// Also writes each kept link's record for the forward-backward pass: {src
+// node, dst node, graph cost bits, acoustic cost bits (emitting link) or
+// source level (epsilon link)}.
+__global__ void __launch_bounds__(kGT) k_gk_write(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl,
                                                   uint32_t lb_key) {
   __shared__ GScratch s;
   const LaneDesc& L = lanes[blockIdx.y];
@@ -1028,7 +1031,19 @@ __global__ void __launch_bounds__(kGT) k_gk_write(const LaneDesc* __restrict__ l
     unsigned long long tile;
     const unsigned long long ex = run + gexcl64(on ? 1ull : 0ull, s, &tile);
     run += tile;
-    if (on) L.kept_idx[ex] = k;
+    if (!on) continue;
+    L.kept_idx[ex] = k;
+    uint64_t lo = 0, hi = (uint64_t)L.T + 1;  // frame of link k: last t with link_off[t] <= k
+    while (hi - lo > 1) {
+      const uint64_t mid = (lo + hi) >> 1;
+      if (L.link_off[mid] <= k) lo = mid;
+      else hi = mid;
+    }
+    const uint4 v = L.links[k];
+    uint32_t aux;
+    if (k >= L.link_xoff[lo]) aux = L.link_lvl[k];
+    else aux = __float_as_uint(-L.ll[(size_t)(lo - 1) * g.P + (g.ilabel_id[v.x] - 1)]);
+    L.post[ex] = make_uint4(v.y, v.z, __float_as_uint(g.weight_id[v.x]), aux);
   }
 }
 
@@ -1173,7 +1188,7 @@ void launch_grid_sweep(const DevGraph& g, const LaneDesc* lanes, void* glv, int 
   const uint32_t lb_key = cost_key(lattice_beam);
   hipLaunchKernelGGL(k_gk_count, all, blk, 0, st, lanes, gl, lb_key);
   hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 3, 1);
-  hipLaunchKernelGGL(k_gk_write, all, blk, 0, st, lanes, gl, lb_key);
+  hipLaunchKernelGGL(k_gk_write, all, blk, 0, st, g, lanes, gl, lb_key);
   hipLaunchKernelGGL(k_gs_fill_ab, all, blk, 0, st, lanes);
 }
 

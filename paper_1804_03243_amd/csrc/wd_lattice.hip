@@ -14,6 +14,11 @@
 namespace wd {
 
 constexpr uint32_t kWin = 4096;  // nodes of one frame held in LDS
+// The lattice pass is a chain of small per-frame steps: 512 threads (8
+// wavefronts, up to 256 VGPRs each) hold a frame's inputs loaded a frame
+// ahead in registers and meet at cheaper barriers than 1024 would.
+constexpr int kLT = 512;
+constexpr int kLW = kLT / 64;
 
 // Two-frame window of per-node values (frame t and t+1, or t-1 and t): extra
 // costs and costs during the pruning sweep, alpha or beta during the
@@ -22,10 +27,13 @@ struct LatShared {
   BlockScratch bs;
   union {
     struct {
-      uint32_t ex[2][kWin];
-      float cost[2][kWin];
+      uint32_t ex[3][kWin];  // three frames: t+1 (read), t (relaxed), t-1 (being initialised)
+      float cost[3][kWin];
     } p;
-    double ab[2][kWin];
+    struct {
+      double a[2][kWin];  // alpha (wavefront 0)
+      double b[2][kWin];  // beta (wavefront 1, concurrently)
+    } ab;
   } w;
 };
 
@@ -150,12 +158,12 @@ __device__ void assemble(const LaneDesc& L, const DevGraph& g, bool all, uint64_
 __device__ uint64_t write_nodes(const LaneDesc& L, uint64_t nnodes, BlockScratch& bs, uint32_t& par) {
   const uint32_t tid = threadIdx.x;
   const uint64_t nwd = (nnodes + 31) >> 5;
-  const uint64_t per = (nwd + kThreads - 1) / kThreads;
+  const uint64_t per = (nwd + kLT - 1) / kLT;
   const uint64_t w0 = tid * per < nwd ? tid * per : nwd;
   const uint64_t w1 = w0 + per < nwd ? w0 + per : nwd;
   uint64_t cnt = 0, n_out;
   for (uint64_t w = w0; w < w1; ++w) cnt += (uint64_t)__popc(L.used[w]);
-  uint64_t pos = block_excl_scan64(cnt, bs, par, &n_out);
+  uint64_t pos = block_excl_scan64<kLW>(cnt, bs, par, &n_out);
   for (uint64_t w = w0; w < w1; ++w) {
     uint32_t word = L.used[w];
     while (word) {
@@ -178,10 +186,395 @@ __device__ __forceinline__ bool level_present(uint32_t mask, uint32_t lvl) {
   return (mask >> (lvl < 31u ? lvl : 31u)) & 1u;
 }
 
+// The per-frame chains (pruning sweep, alpha, beta) run on single
+// wavefronts: a frame is a handful of dependent steps over tens of items, and
+// the lanes of one wavefront need no workgroup barrier between steps.  Inputs
+// of a frame that do not depend on the chain are loaded a frame ahead into
+// registers, kAhead items per lane and run; further items are loaded in place.
+constexpr int kAhead = 2;
+
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Loads of values other lanes update with atomics in device memory (frames
+// too large for the LDS windows): served by L2, never by a stale L1 line.
+__device__ __forceinline__ uint32_t load_fresh(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double load_fresh(const double* p) {
+  const unsigned long long v = __hip_atomic_load(reinterpret_cast<const unsigned long long*>(p),
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __longlong_as_double((long long)v);
+}
+
+// A frame's offsets (scalar loads, mostly scalar-cache hits) are read when
+// its items are prefetched, a frame ahead of its processing.
+struct SweepScal {
+  uint64_t n0, n1, k0, k1, x0, x1;
+  uint32_t mask;
+};
+__device__ __forceinline__ void sweep_scal(const LaneDesc& L, int t, SweepScal& a) {
+  a.n0 = L.node_off[t];
+  a.n1 = L.node_off[t + 1];
+  a.x0 = L.link_xoff[t];
+  a.x1 = L.link_off[t + 1];
+  a.mask = L.xmask[t];
+  a.k0 = t < L.T ? L.link_off[t + 1] : 0;
+  a.k1 = t < L.T ? L.link_xoff[t + 1] : 0;
+}
+
+// extra(link) = extra(dst) + (x - cost(dst)) into le_key; extra(src) = min.
+// exd/cd: the destination frame's window, or device memory (cd == nullptr).
+__device__ __forceinline__ void sweep_relax(const LaneDesc& L, uint64_t k, uint4 v, const uint32_t* exd,
+                                            const float* cd, uint64_t d0, uint32_t* ex, uint64_t n0) {
+  const uint64_t d = v.z - d0;
+  const float c = cd ? cd[d] : node_cost(L, v.z);
+  const uint32_t e = cd ? exd[d] : load_fresh(&exd[d]);
+  const uint32_t le = cost_key(key_cost(e) + (__uint_as_float(v.w) - c));
+  L.le_key[k] = le;
+  atomicMin(&ex[v.y - n0], le);
+}
+
+// The sweep: per frame the emitting links out of the frame (tens to
+// hundreds) are relaxed by the whole workgroup; then wavefront 0 walks the
+// frame's epsilon levels (a few tens of links) without workgroup barriers,
+// while the other wavefronts write back frame t+1's window and initialise
+// frame t-1's (three windows in turn).  Two workgroup barriers per frame.
+struct SweepOne {
+  uint32_t lvl, c;
+  uint4 e, x;
+};
+
+__device__ __forceinline__ void sweep_one(const LaneDesc& L, const SweepScal& a, uint32_t tid, SweepOne& it) {
+  if (tid < a.k1 - a.k0) it.e = L.links[a.k0 + tid];
+  if (tid < a.x1 - a.x0) {
+    it.x = L.links[a.x0 + tid];
+    it.lvl = L.link_lvl[a.x0 + tid];
+  }
+}
+
+// Extra costs (+inf, or the final extra cost for the last frame) and costs
+// of frame t's nodes, by threads first, first + stride, ...; c0: the cost key
+// of node `first`, loaded ahead (kNoKeyAhead: load it here).
+constexpr uint32_t kNoKeyAhead = 0u;
+__device__ __forceinline__ void sweep_init(const LaneDesc& L, const DevGraph& g, LatShared& sh, int t,
+                                           const SweepScal& a, uint32_t first, uint32_t stride, bool final_used,
+                                           float best_total, uint32_t c0) {
+  const uint64_t n0 = a.n0;
+  const uint32_t nt = (uint32_t)(a.n1 - n0), buf = (uint32_t)t % 3u;
+  const bool win = nt <= kWin;
+  uint32_t* ex = win ? sh.w.p.ex[buf] : L.extra_key + n0;
+  for (uint32_t i = first; i < nt; i += stride) {
+    const float c = (i == first && c0 != kNoKeyAhead) ? key_cost(c0) : node_cost(L, n0 + i);
+    uint32_t e = kInfKey;
+    if (t == L.T) {
+      const float F = final_used ? canon(c + g.final_w[L.n_state[n0 + i]]) : c;
+      if (F < INFINITY) e = cost_key(F - best_total);
+    }
+    ex[i] = e;
+    if (win) sh.w.p.cost[buf][i] = c;
+  }
+}
+
+__device__ __forceinline__ void sweep_writeback(const LaneDesc& L, LatShared& sh, int t, const SweepScal& a,
+                                                uint32_t first, uint32_t stride) {
+  const uint32_t nt = (uint32_t)(a.n1 - a.n0);
+  if (nt > kWin) return;  // relaxed in device memory directly
+  const uint32_t* ex = sh.w.p.ex[(uint32_t)t % 3u];
+  for (uint32_t i = first; i < nt; i += stride) L.extra_key[a.n0 + i] = ex[i];
+}
+
+// Frame t: `cur` holds this thread's links of frame t (loaded during frame
+// t+1) and the cost key of its node of frame t-1 (loaded during t+1); frame
+// t-1's links and frame t-2's node cost are loaded into `nxt` now.  The
+// caller alternates two sets, so no register with a load in flight is copied.
+__device__ __forceinline__ void sweep_step(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t tid, int t,
+                                           bool final_used, float best_total, const SweepOne& cur,
+                                           SweepOne& nxt) {
+  const int T = L.T;
+  SweepScal sa, sp{}, sn{};
+  sweep_scal(L, t, sa);
+  if (t < T) sweep_scal(L, t + 1, sp);
+  if (t > 0) {
+    sweep_scal(L, t - 1, sn);
+    sweep_one(L, sn, tid, nxt);
+  }
+  nxt.c = kNoKeyAhead;
+  if (t > 1 && tid >= 64) {
+    const uint64_t m0 = L.node_off[t - 2], m1 = L.node_off[t - 1];
+    if (tid - 64 < m1 - m0) nxt.c = (uint32_t)(L.n_pack[m0 + tid - 64] >> 32);
+  }
+  const uint64_t n0 = sa.n0, n1 = sa.n1;
+  const uint32_t buf = (uint32_t)t % 3u;
+  const bool win = n1 - n0 <= kWin;
+  uint32_t* ex = win ? sh.w.p.ex[buf] : L.extra_key + n0;
+  float* cw = win ? sh.w.p.cost[buf] : nullptr;
+  if (sa.k1 > sa.k0) {
+    const uint64_t m0 = n1;
+    const bool wn = sp.n1 - m0 <= kWin;
+    const uint32_t nb = (uint32_t)(t + 1) % 3u;
+    const uint32_t* exn = wn ? sh.w.p.ex[nb] : L.extra_key + m0;
+    const float* cn = wn ? sh.w.p.cost[nb] : nullptr;
+    if (sa.k0 + tid < sa.k1) sweep_relax(L, sa.k0 + tid, cur.e, exn, cn, m0, ex, n0);
+    for (uint64_t k = sa.k0 + tid + kLT; k < sa.k1; k += kLT) sweep_relax(L, k, L.links[k], exn, cn, m0, ex, n0);
+  }
+  __syncthreads();
+  if (tid < 64) {
+    if (sa.x1 > sa.x0)
+      for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
+        if (!level_present(sa.mask, (uint32_t)lvl)) continue;
+        if (sa.x0 + tid < sa.x1 && cur.lvl == (uint32_t)lvl) sweep_relax(L, sa.x0 + tid, cur.x, ex, cw, n0, ex, n0);
+        for (uint64_t k = sa.x0 + tid + 64; k < sa.x1; k += 64)
+          if (L.link_lvl[k] == (uint8_t)lvl) sweep_relax(L, k, L.links[k], ex, cw, n0, ex, n0);
+        wave_sync();
+      }
+  } else {
+    if (t < T) sweep_writeback(L, sh, t + 1, sp, tid - 64, kLT - 64);
+    if (t > 0) sweep_init(L, g, sh, t - 1, sn, tid - 64, kLT - 64, final_used, best_total, cur.c);
+  }
+  __syncthreads();
+}
+
+// Backward extra-cost sweep over every frame.
+__device__ __forceinline__ void sweep_block(const LaneDesc& L, const DevGraph& g, LatShared& sh,
+                                            uint32_t tid, bool final_used, float best_total) {
+  const int T = L.T;
+  SweepOne x{}, y{};
+  {
+    SweepScal s0;
+    sweep_scal(L, T, s0);
+    sweep_one(L, s0, tid, x);
+    sweep_init(L, g, sh, T, s0, tid, kLT, final_used, best_total, kNoKeyAhead);
+    // node cost of frame T-1 for the first step's initialisation
+    x.c = kNoKeyAhead;
+    if (T > 0 && tid >= 64) {
+      const uint64_t m0 = L.node_off[T - 1], m1 = L.node_off[T];
+      if (tid - 64 < m1 - m0) x.c = (uint32_t)(L.n_pack[m0 + tid - 64] >> 32);
+    }
+  }
+  __syncthreads();
+  for (int t = T; t >= 0; t -= 2) {
+    sweep_step(L, g, sh, tid, t, final_used, best_total, x, y);
+    if (t >= 1) sweep_step(L, g, sh, tid, t - 1, final_used, best_total, y, x);
+  }
+  SweepScal s0;
+  sweep_scal(L, 0, s0);
+  sweep_writeback(L, sh, 0, s0, tid, kLT);
+}
+
+// Kept link j for the forward-backward pass: {src node, dst node, graph cost
+// bits, acoustic cost bits (emitting) or source level (epsilon)}.
+__device__ __forceinline__ uint4 post_link(const LaneDesc& L, uint64_t j) { return L.post[j]; }
+
+// Record of kept link j (link k) of frame t; `eps`: an epsilon link.
+__device__ __forceinline__ uint4 post_record(const LaneDesc& L, const DevGraph& g, uint64_t k, int t, bool eps) {
+  const uint4 v = L.links[k];
+  uint32_t aux;
+  if (eps) aux = L.link_lvl[k];
+  else aux = __float_as_uint(-L.ll[(size_t)(t - 1) * g.P + (g.ilabel_id[v.x] - 1)]);
+  return make_uint4(v.y, v.z, __float_as_uint(g.weight_id[v.x]), aux);
+}
+
+struct PostScal {
+  uint64_t n0, n1, m0, m1, e0, e1, x0, x1;
+  uint32_t mask;
+};
+struct PostItems {
+  uint4 e[kAhead], x[kAhead];
+  float fw[kAhead];
+};
+
+// Frame t of the alpha pass: emitting kept links into t (from t-1), epsilon
+// kept links of t.
+__device__ __forceinline__ void alpha_scal(const LaneDesc& L, int t, PostScal& a) {
+  a.n0 = L.node_off[t];
+  a.n1 = L.node_off[t + 1];
+  a.m0 = t > 0 ? L.node_off[t - 1] : 0;
+  a.e0 = L.kframe[2 * t];
+  a.e1 = L.kframe[2 * t + 1];
+  a.x0 = a.e1;
+  a.x1 = L.kframe[2 * t + 2];
+  a.mask = L.xmask[t];
+}
+
+// Frame t of the beta pass: emitting kept links out of t (into t+1), epsilon
+// kept links of t.
+__device__ __forceinline__ void beta_scal(const LaneDesc& L, int t, PostScal& a) {
+  const int T = L.T;
+  a.n0 = L.node_off[t];
+  a.n1 = L.node_off[t + 1];
+  a.m0 = t < T ? L.node_off[t + 1] : 0;
+  a.m1 = t < T ? L.node_off[t + 2] : 0;
+  a.e0 = t < T ? L.kframe[2 * t + 2] : 0;
+  a.e1 = t < T ? L.kframe[2 * t + 3] : 0;
+  a.x0 = L.kframe[2 * t + 1];
+  a.x1 = L.kframe[2 * t + 2];
+  a.mask = L.xmask[t];
+}
+
+// Items of a frame; `fin`: the last frame of the beta pass (final weights).
+__device__ __forceinline__ void post_items(const LaneDesc& L, const DevGraph& g, const PostScal& a, uint32_t lane,
+                                           bool fin, PostItems& it) {
+#pragma unroll
+  for (int q = 0; q < kAhead; ++q) {
+    const uint64_t i = lane + 64u * (uint32_t)q;
+    if (i < a.e1 - a.e0) it.e[q] = post_link(L, a.e0 + i);
+    if (i < a.x1 - a.x0) it.x[q] = post_link(L, a.x0 + i);
+    if (fin && i < a.n1 - a.n0) it.fw[q] = g.final_w[L.n_state[a.n0 + i]];
+  }
+}
+
+// Frame t of the alpha pass on one wavefront (items of t in `cur`; those of
+// t+1 are loaded into `nxt`).  `swept`: device-memory alpha is +inf already.
+__device__ __forceinline__ void alpha_step(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
+                                           int t, bool swept, uint64_t start_node, const PostItems& cur,
+                                           PostItems& nxt) {
+  const int T = L.T;
+  PostScal pa;
+  alpha_scal(L, t, pa);
+  if (t < T) {
+    PostScal pb;
+    alpha_scal(L, t + 1, pb);
+    post_items(L, g, pb, lane, false, nxt);
+  }
+  const uint64_t n0 = pa.n0, n1 = pa.n1;
+  const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
+  const bool win = nt <= kWin;
+  double* a = win ? sh.w.ab.a[buf] : L.alpha + n0;
+  if (win || !swept) {
+    for (uint32_t i = lane; i < nt; i += 64) a[i] = (n0 + i == start_node) ? 0.0 : INFINITY;
+  } else if (lane == 0 && start_node >= n0 && start_node < n1) {
+    a[start_node - n0] = 0.0;  // the rest is +inf already
+  }
+  wave_sync();
+  if (pa.e1 > pa.e0) {
+    const uint64_t m0 = pa.m0;
+    const bool wp = n0 - m0 <= kWin;
+    const double* ap = wp ? sh.w.ab.a[buf ^ 1u] : L.alpha + m0;
+#pragma unroll
+    for (int q = 0; q <= kAhead; ++q)
+      for (uint64_t j = pa.e0 + lane + 64u * (uint32_t)q; j < pa.e1; j += (q < kAhead ? pa.e1 : 64u)) {
+        const uint4 l = q < kAhead ? cur.e[q < kAhead ? q : 0] : post_link(L, j);
+        const double av = wp ? ap[l.x - m0] : load_fresh(&ap[l.x - m0]);
+        atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w));
+      }
+    wave_sync();
+  }
+  if (pa.x1 > pa.x0)
+    for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
+      if (!level_present(pa.mask, lvl)) continue;
+#pragma unroll
+      for (int q = 0; q <= kAhead; ++q)
+        for (uint64_t j = pa.x0 + lane + 64u * (uint32_t)q; j < pa.x1; j += (q < kAhead ? pa.x1 : 64u)) {
+          const uint4 l = q < kAhead ? cur.x[q < kAhead ? q : 0] : post_link(L, j);
+          if (l.w != lvl) continue;
+          const double av = win ? a[l.x - n0] : load_fresh(&a[l.x - n0]);
+          atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z));
+        }
+      wave_sync();
+    }
+  if (win)
+    for (uint32_t i = lane; i < nt; i += 64) L.alpha[n0 + i] = a[i];
+}
+
+// alpha over every frame, ascending; epsilon links of a frame by source
+// level.  One wavefront.
+__device__ __forceinline__ void alpha_wave(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
+                                           bool swept, uint64_t start_node) {
+  const int T = L.T;
+  PostItems x{}, y{};
+  {
+    PostScal p0;
+    alpha_scal(L, 0, p0);
+    post_items(L, g, p0, lane, false, x);
+  }
+  for (int t = 0; t <= T; t += 2) {
+    alpha_step(L, g, sh, lane, t, swept, start_node, x, y);
+    if (t + 1 <= T) alpha_step(L, g, sh, lane, t + 1, swept, start_node, y, x);
+  }
+}
+
+// Frame t of the beta pass on one wavefront (items of t in `cur`; those of
+// t-1 are loaded into `nxt`).
+__device__ __forceinline__ void beta_step(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
+                                          int t, bool swept, bool final_used, const PostItems& cur, PostItems& nxt) {
+  const int T = L.T;
+  PostScal pa;
+  beta_scal(L, t, pa);
+  if (t > 0) {
+    PostScal pb;
+    beta_scal(L, t - 1, pb);
+    post_items(L, g, pb, lane, false, nxt);
+  }
+  const uint64_t n0 = pa.n0, n1 = pa.n1;
+  const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
+  const bool win = nt <= kWin;
+  double* b = win ? sh.w.ab.b[buf] : L.beta + n0;
+  if (win || !swept || t == T) {
+#pragma unroll
+    for (int q = 0; q <= kAhead; ++q)
+      for (uint32_t i = lane + 64u * (uint32_t)q; i < nt; i += (q < kAhead ? nt : 64u)) {
+        double v = INFINITY;
+        if (t == T)
+          v = final_used ? (double)(q < kAhead ? cur.fw[q < kAhead ? q : 0] : g.final_w[L.n_state[n0 + i]]) : 0.0;
+        b[i] = v;
+      }
+  }
+  wave_sync();
+  if (pa.e1 > pa.e0) {
+    const uint64_t m0 = pa.m0;
+    const bool wn = pa.m1 - m0 <= kWin;
+    const double* bn = wn ? sh.w.ab.b[buf ^ 1u] : L.beta + m0;
+#pragma unroll
+    for (int q = 0; q <= kAhead; ++q)
+      for (uint64_t j = pa.e0 + lane + 64u * (uint32_t)q; j < pa.e1; j += (q < kAhead ? pa.e1 : 64u)) {
+        const uint4 l = q < kAhead ? cur.e[q < kAhead ? q : 0] : post_link(L, j);
+        const double bv = wn ? bn[l.y - m0] : load_fresh(&bn[l.y - m0]);
+        atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w) + bv);
+      }
+    wave_sync();
+  }
+  if (pa.x1 > pa.x0)
+    for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
+      if (!level_present(pa.mask, (uint32_t)lvl)) continue;
+#pragma unroll
+      for (int q = 0; q <= kAhead; ++q)
+        for (uint64_t j = pa.x0 + lane + 64u * (uint32_t)q; j < pa.x1; j += (q < kAhead ? pa.x1 : 64u)) {
+          const uint4 l = q < kAhead ? cur.x[q < kAhead ? q : 0] : post_link(L, j);
+          if (l.w != (uint32_t)lvl) continue;
+          const double bv = win ? b[l.y - n0] : load_fresh(&b[l.y - n0]);
+          atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + bv);
+        }
+      wave_sync();
+    }
+  if (win)
+    for (uint32_t i = lane; i < nt; i += 64) L.beta[n0 + i] = b[i];
+}
+
+// beta over every frame, descending; epsilon links of a frame from the
+// highest source level.  One wavefront.
+__device__ __forceinline__ void beta_wave(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
+                                          bool swept, bool final_used) {
+  const int T = L.T;
+  PostItems x{}, y{};
+  {
+    PostScal p0;
+    beta_scal(L, T, p0);
+    post_items(L, g, p0, lane, final_used, x);
+  }
+  for (int t = T; t >= 0; t -= 2) {
+    beta_step(L, g, sh, lane, t, swept, final_used, x, y);
+    if (t >= 1) beta_step(L, g, sh, lane, t - 1, swept, final_used, y, x);
+  }
+}
+
 // blockIdx.y == 0: pruning, posteriors and the final merge; blockIdx.y == 1:
 // the 1-best traceback (a serial walk over predecessor pointers, run
 // concurrently by its own workgroup).
-__global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc* __restrict__ lanes,
+__global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __restrict__ lanes,
                                                       Params prm) {
   __shared__ LatShared sh;
   const LaneDesc& L = lanes[blockIdx.x];
@@ -207,20 +600,20 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
   } else {
     uint32_t any = 0;
     if (g.final_w)
-      for (uint64_t n = nT0 + tid; n < nT1; n += kThreads) {
+      for (uint64_t n = nT0 + tid; n < nT1; n += kLT) {
         const float fw = g.final_w[L.n_state[n]];
         const float c = node_cost(L, n);
         any |= (fw < INFINITY && (c + fw) < INFINITY) ? 1u : 0u;
       }
-    final_used = block_or(any, sh.bs, par) != 0;
+    final_used = block_or<kLW>(any, sh.bs, par) != 0;
     uint64_t m = kEmpty;
-    for (uint64_t n = nT0 + tid; n < nT1; n += kThreads) {
+    for (uint64_t n = nT0 + tid; n < nT1; n += kLT) {
       const float c = node_cost(L, n);
       const float F = final_used ? canon(c + g.final_w[L.n_state[n]]) : c;
       const uint64_t v = pack_tok(cost_key(F), (uint32_t)(n - nT0));
       m = v < m ? v : m;
     }
-    m = block_min64(m, sh.bs, par);
+    m = block_min64<kLW>(m, sh.bs, par);
     best_key = (uint32_t)(m >> 32);
     bnode = nT0 + (m & 0xffffffffu);
   }
@@ -271,66 +664,19 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
   }
 
   // ------------------------------------------------ backward extra-cost sweep
-  for (int t = swept ? -1 : T; t >= 0; --t) {
-    const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
-    const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
-    const bool win = nt <= kWin;
-    uint32_t* ex = win ? sh.w.p.ex[buf] : L.extra_key + n0;
-    for (uint32_t i = tid; i < nt; i += kThreads) {
-      const float c = node_cost(L, n0 + i);
-      uint32_t e = kInfKey;
-      if (t == T) {
-        const float F = final_used ? canon(c + g.final_w[L.n_state[n0 + i]]) : c;
-        if (F < INFINITY) e = cost_key(F - best_total);
-      }
-      ex[i] = e;
-      if (win) sh.w.p.cost[buf][i] = c;
-    }
-    __syncthreads();
-    // extra(link) = extra(dst) + (x - cost(dst)); extra(src) = min over links
-    auto relax = [&](uint64_t k, const uint32_t* exd, const float* cd, uint64_t d0) {
-      const LinkView l = link_at(L, k);
-      const uint64_t d = l.dst - d0;
-      const float c = cd ? cd[d] : node_cost(L, l.dst);
-      const uint32_t le = cost_key(key_cost(exd[d]) + (l.x - c));
-      L.le_key[k] = le;
-      atomicMin(&ex[l.src - n0], le);
-    };
-    if (t < T) {
-      const uint64_t k0 = L.link_off[t + 1], k1 = L.link_xoff[t + 1];
-      if (k1 > k0) {
-        const uint64_t m0 = L.node_off[t + 1];
-        const bool wn = L.node_off[t + 2] - m0 <= kWin;
-        const uint32_t* exn = wn ? sh.w.p.ex[buf ^ 1u] : L.extra_key + m0;
-        const float* cn = wn ? sh.w.p.cost[buf ^ 1u] : nullptr;
-        for (uint64_t k = k0 + tid; k < k1; k += kThreads) relax(k, exn, cn, m0);
-        __syncthreads();
-      }
-    }
-    const uint64_t x0 = L.link_xoff[t], x1 = L.link_off[t + 1];
-    const uint32_t mask = L.xmask[t];
-    if (x1 > x0)
-      for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
-        if (!level_present(mask, (uint32_t)lvl)) continue;
-        for (uint64_t k = x0 + tid; k < x1; k += kThreads)
-          if (L.link_lvl[k] == (uint8_t)lvl) relax(k, ex, win ? sh.w.p.cost[buf] : nullptr, n0);
-        __syncthreads();
-      }
-    if (win)
-      for (uint32_t i = tid; i < nt; i += kThreads) L.extra_key[n0 + i] = ex[i];
-  }
+  if (!swept) sweep_block(L, g, sh, tid, final_used, best_total);
   __syncthreads();
 
   // ------------------------------------------ kept links (final merge input)
   const uint32_t lb_key = cost_key(prm.lattice_beam);
   uint64_t n_kept = info->kept;  // counted and listed by the chip-wide kernels when swept
   if (!swept) {
-    const uint64_t per = (nlinks + kThreads - 1) / kThreads;
+    const uint64_t per = (nlinks + kLT - 1) / kLT;
     const uint64_t k0 = tid * per < nlinks ? tid * per : nlinks;
     const uint64_t k1 = k0 + per < nlinks ? k0 + per : nlinks;
     uint64_t cnt = 0;
     for (uint64_t k = k0; k < k1; ++k) cnt += kept(L, k, lb_key);
-    uint64_t pos = block_excl_scan64(cnt, sh.bs, par, &n_kept);
+    uint64_t pos = block_excl_scan64<kLW>(cnt, sh.bs, par, &n_kept);
     if (n_kept <= L.kept_cap)
       for (uint64_t k = k0; k < k1; ++k)
         if (kept(L, k, lb_key)) L.kept_idx[pos++] = k;
@@ -349,11 +695,33 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
   // per frame t: kept links start at kf[2t], kept epsilon links at kf[2t+1];
   // frame t ends where frame t+1 starts
   uint64_t* kf = L.kframe;
-  for (int t = (int)tid; t <= T + 1; t += kThreads) {
+  for (int t = (int)tid; t <= T + 1; t += kLT) {
     kf[2 * t] = lower_bound64(kid, n_kept, L.link_off[t]);
     kf[2 * t + 1] = t <= T ? lower_bound64(kid, n_kept, L.link_xoff[t]) : n_kept;
   }
   __syncthreads();
+  if (!swept) {
+    // records of the kept links for forward-backward (chip-wide mode writes
+    // them while listing the kept links): a thread takes a contiguous range,
+    // finds the frame of its first link and walks the frame boundaries
+    const uint64_t per = (n_kept + kLT - 1) / kLT;
+    const uint64_t j0 = tid * per < n_kept ? tid * per : n_kept;
+    const uint64_t j1 = j0 + per < n_kept ? j0 + per : n_kept;
+    if (j0 < j1) {
+      int lo = 0, hi = T + 1;  // last t with kf[2t] <= j0 (kf[2(T+1)] = n_kept)
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (kf[2 * mid] <= j0) lo = mid;
+        else hi = mid;
+      }
+      int t = lo;
+      for (uint64_t j = j0; j < j1; ++j) {
+        while (kf[2 * t + 2] <= j) ++t;
+        L.post[j] = post_record(L, g, kid[j], t, j >= kf[2 * t + 1]);
+      }
+    }
+    __syncthreads();
+  }
 
   // ----------------------------------------------------- posteriors (fp64)
   uint64_t start_node = 0;
@@ -367,85 +735,9 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
     }
     start_node = lo;
   }
-  // alpha: frames ascending, epsilon links of a frame by source level
-  for (int t = 0; t <= T; ++t) {
-    const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
-    const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
-    const bool win = nt <= kWin;
-    double* a = win ? sh.w.ab[buf] : L.alpha + n0;
-    if (win || !swept) {
-      for (uint32_t i = tid; i < nt; i += kThreads) a[i] = (n0 + i == start_node) ? 0.0 : INFINITY;
-    } else if (tid == 0 && start_node >= n0 && start_node < n1) {
-      a[start_node - n0] = 0.0;  // the rest is +inf already
-    }
-    __syncthreads();
-    const uint64_t e0 = kf[2 * t], e1 = kf[2 * t + 1], e2 = kf[2 * t + 2];
-    if (e1 > e0) {
-      const uint64_t m0 = L.node_off[t - 1];
-      const double* ap = (n0 - m0 <= kWin) ? sh.w.ab[buf ^ 1u] : L.alpha + m0;
-      for (uint64_t j = e0 + tid; j < e1; j += kThreads) {
-        const LinkView l = link_at(L, kid[j]);
-        atomic_logadd(&a[l.dst - n0], ap[l.src - m0] + (double)g.weight_id[l.arc] + link_ac(L, g, t, l.arc));
-      }
-      __syncthreads();
-    }
-    if (e2 > e1) {
-      const uint32_t mask = L.xmask[t];
-      for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
-        if (!level_present(mask, lvl)) continue;
-        for (uint64_t j = e1 + tid; j < e2; j += kThreads) {
-          const uint64_t k = kid[j];
-          if (L.link_lvl[k] != (uint8_t)lvl) continue;
-          const LinkView l = link_at(L, k);
-          atomic_logadd(&a[l.dst - n0], a[l.src - n0] + (double)g.weight_id[l.arc]);
-        }
-        __syncthreads();
-      }
-    }
-    if (win)
-      for (uint32_t i = tid; i < nt; i += kThreads) L.alpha[n0 + i] = a[i];
-  }
-  __syncthreads();
-  // beta: frames descending, epsilon links of a frame from the highest level
-  for (int t = T; t >= 0; --t) {
-    const uint64_t n0 = L.node_off[t], n1 = L.node_off[t + 1];
-    const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
-    const bool win = nt <= kWin;
-    double* b = win ? sh.w.ab[buf] : L.beta + n0;
-    if (win || !swept || t == T)
-      for (uint32_t i = tid; i < nt; i += kThreads)
-        b[i] = t == T ? (final_used ? (double)g.final_w[L.n_state[n0 + i]] : 0.0) : INFINITY;
-    __syncthreads();
-    if (t < T) {
-      const uint64_t e0 = kf[2 * t + 2], e1 = kf[2 * t + 3];
-      if (e1 > e0) {
-        const uint64_t m0 = L.node_off[t + 1];
-        const double* bn = (L.node_off[t + 2] - m0 <= kWin) ? sh.w.ab[buf ^ 1u] : L.beta + m0;
-        for (uint64_t j = e0 + tid; j < e1; j += kThreads) {
-          const LinkView l = link_at(L, kid[j]);
-          atomic_logadd(&b[l.src - n0],
-                        (double)g.weight_id[l.arc] + link_ac(L, g, t + 1, l.arc) + bn[l.dst - m0]);
-        }
-        __syncthreads();
-      }
-    }
-    const uint64_t e1 = kf[2 * t + 1], e2 = kf[2 * t + 2];
-    if (e2 > e1) {
-      const uint32_t mask = L.xmask[t];
-      for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
-        if (!level_present(mask, (uint32_t)lvl)) continue;
-        for (uint64_t j = e1 + tid; j < e2; j += kThreads) {
-          const uint64_t k = kid[j];
-          if (L.link_lvl[k] != (uint8_t)lvl) continue;
-          const LinkView l = link_at(L, k);
-          atomic_logadd(&b[l.src - n0], (double)g.weight_id[l.arc] + b[l.dst - n0]);
-        }
-        __syncthreads();
-      }
-    }
-    if (win)
-      for (uint32_t i = tid; i < nt; i += kThreads) L.beta[n0 + i] = b[i];
-  }
+  // alpha on wavefront 0 and beta on wavefront 1, concurrently
+  if (tid < 64) alpha_wave(L, g, sh, tid, swept, start_node);
+  else if (tid < 128) beta_wave(L, g, sh, tid - 64, swept, final_used);
   __syncthreads();
   const double Z = L.beta[start_node];
   if (tid == 0) {
@@ -462,8 +754,8 @@ __global__ void __launch_bounds__(kThreads) k_lattice(DevGraph g, const LaneDesc
   if (swept) return;  // the merge and the node list run as chip-wide kernels
 
   // ------------------------------------------- final merge of the kept links
-  assemble(L, g, false, n_kept, L.out_links, lb_key, Z, true, true, tid, kThreads);
-  if (debug) assemble(L, g, true, nlinks, L.out_raw, lb_key, Z, true, false, tid, kThreads);
+  assemble(L, g, false, n_kept, L.out_links, lb_key, Z, true, true, tid, kLT);
+  if (debug) assemble(L, g, true, nlinks, L.out_raw, lb_key, Z, true, false, tid, kLT);
   __syncthreads();
   const uint64_t n_out = write_nodes(L, nnodes, sh.bs, par);
   if (tid == 0) info->out_nodes = n_out;
@@ -484,7 +776,7 @@ __global__ void __launch_bounds__(256) k_lat_assemble(DevGraph g, const LaneDesc
 }
 
 void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s) {
-  hipLaunchKernelGGL(k_lattice, dim3(B, 2), dim3(kThreads), 0, s, g, lanes, prm);
+  hipLaunchKernelGGL(k_lattice, dim3(B, 2), dim3(kLT), 0, s, g, lanes, prm);
   if (prm.flags & kFlagSwept) {
     hipLaunchKernelGGL(k_lat_assemble, dim3(1024, B), dim3(256), 0, s, g, lanes, prm);
   }
