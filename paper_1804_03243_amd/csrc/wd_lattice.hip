@@ -103,7 +103,7 @@ __device__ __forceinline__ double link_ac(const LaneDesc& L, const DevGraph& g, 
 // plus the number of links of the other run with a smaller arc id.  The runs'
 // bounds in selection order are the frame's link offsets (all links) or the
 // per-frame kept-link boundaries kf.
-__device__ void assemble(const LaneDesc& L, const DevGraph& g, bool all, uint64_t n_sel,
+__device__ __forceinline__ void assemble(const LaneDesc& L, const DevGraph& g, bool all, uint64_t n_sel,
                          OutLink* out, uint32_t lb_key, double Z, bool with_post, bool mark_nodes,
                          uint64_t first, uint64_t stride) {
   const int T = L.T;
@@ -155,7 +155,7 @@ __device__ void assemble(const LaneDesc& L, const DevGraph& g, bool all, uint64_
 
 // Lattice nodes (those marked in the used bitmap) in (t, state) order, which
 // is node id order; returns their number.  Whole workgroup.
-__device__ uint64_t write_nodes(const LaneDesc& L, uint64_t nnodes, BlockScratch& bs, uint32_t& par) {
+__device__ __forceinline__ uint64_t write_nodes(const LaneDesc& L, uint64_t nnodes, BlockScratch& bs, uint32_t& par) {
   const uint32_t tid = threadIdx.x;
   const uint64_t nwd = (nnodes + 31) >> 5;
   const uint64_t per = (nwd + kLT - 1) / kLT;
@@ -197,6 +197,14 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Synchronisation of the threads running a per-frame chain: one wavefront
+// (GS = 64) or the whole workgroup.
+template <int GS>
+__device__ __forceinline__ void group_sync() {
+  if (GS == 64) wave_sync();
+  else __syncthreads();
 }
 
 // Loads of values other lanes update with atomics in device memory (frames
@@ -378,6 +386,23 @@ __device__ __forceinline__ uint4 post_record(const LaneDesc& L, const DevGraph& 
   return make_uint4(v.y, v.z, __float_as_uint(g.weight_id[v.x]), aux);
 }
 
+// Kept links of a run beyond the prefetched ones, kBatch per lane per round
+// trip: the loads of a batch are issued together, then the batch is applied.
+constexpr int kBatch = 4;
+
+template <int GS, typename F>
+__device__ __forceinline__ void post_tail(const LaneDesc& L, uint64_t j0, uint64_t j1, uint32_t lane, F&& apply) {
+  for (uint64_t jb = j0 + lane + (uint64_t)GS * kAhead; jb < j1; jb += (uint64_t)GS * kBatch) {
+    uint4 lb[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      if (jb + (uint64_t)GS * u < j1) lb[u] = post_link(L, jb + (uint64_t)GS * u);
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      if (jb + (uint64_t)GS * u < j1) apply(lb[u]);
+  }
+}
+
 struct PostScal {
   uint64_t n0, n1, m0, m1, e0, e1, x0, x1;
   uint32_t mask;
@@ -416,19 +441,21 @@ __device__ __forceinline__ void beta_scal(const LaneDesc& L, int t, PostScal& a)
 }
 
 // Items of a frame; `fin`: the last frame of the beta pass (final weights).
+template <int GS>
 __device__ __forceinline__ void post_items(const LaneDesc& L, const DevGraph& g, const PostScal& a, uint32_t lane,
                                            bool fin, PostItems& it) {
 #pragma unroll
   for (int q = 0; q < kAhead; ++q) {
-    const uint64_t i = lane + 64u * (uint32_t)q;
+    const uint64_t i = lane + (uint64_t)GS * q;
     if (i < a.e1 - a.e0) it.e[q] = post_link(L, a.e0 + i);
     if (i < a.x1 - a.x0) it.x[q] = post_link(L, a.x0 + i);
     if (fin && i < a.n1 - a.n0) it.fw[q] = g.final_w[L.n_state[a.n0 + i]];
   }
 }
 
-// Frame t of the alpha pass on one wavefront (items of t in `cur`; those of
+// Frame t of the alpha pass on a group of GS threads (items of t in `cur`; those of
 // t+1 are loaded into `nxt`).  `swept`: device-memory alpha is +inf already.
+template <int GS>
 __device__ __forceinline__ void alpha_step(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
                                            int t, bool swept, uint64_t start_node, const PostItems& cur,
                                            PostItems& nxt) {
@@ -438,50 +465,53 @@ __device__ __forceinline__ void alpha_step(const LaneDesc& L, const DevGraph& g,
   if (t < T) {
     PostScal pb;
     alpha_scal(L, t + 1, pb);
-    post_items(L, g, pb, lane, false, nxt);
+    post_items<GS>(L, g, pb, lane, false, nxt);
   }
   const uint64_t n0 = pa.n0, n1 = pa.n1;
   const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
   const bool win = nt <= kWin;
   double* a = win ? sh.w.ab.a[buf] : L.alpha + n0;
   if (win || !swept) {
-    for (uint32_t i = lane; i < nt; i += 64) a[i] = (n0 + i == start_node) ? 0.0 : INFINITY;
+    for (uint32_t i = lane; i < nt; i += GS) a[i] = (n0 + i == start_node) ? 0.0 : INFINITY;
   } else if (lane == 0 && start_node >= n0 && start_node < n1) {
     a[start_node - n0] = 0.0;  // the rest is +inf already
   }
-  wave_sync();
+  group_sync<GS>();
   if (pa.e1 > pa.e0) {
     const uint64_t m0 = pa.m0;
     const bool wp = n0 - m0 <= kWin;
     const double* ap = wp ? sh.w.ab.a[buf ^ 1u] : L.alpha + m0;
+    auto emit = [&](uint4 l) {
+      const double av = wp ? ap[l.x - m0] : load_fresh(&ap[l.x - m0]);
+      atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w));
+    };
 #pragma unroll
-    for (int q = 0; q <= kAhead; ++q)
-      for (uint64_t j = pa.e0 + lane + 64u * (uint32_t)q; j < pa.e1; j += (q < kAhead ? pa.e1 : 64u)) {
-        const uint4 l = q < kAhead ? cur.e[q < kAhead ? q : 0] : post_link(L, j);
-        const double av = wp ? ap[l.x - m0] : load_fresh(&ap[l.x - m0]);
-        atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w));
-      }
-    wave_sync();
+    for (int q = 0; q < kAhead; ++q)
+      if (pa.e0 + lane + (uint64_t)GS * q < pa.e1) emit(cur.e[q]);
+    post_tail<GS>(L, pa.e0, pa.e1, lane, emit);
+    group_sync<GS>();
   }
   if (pa.x1 > pa.x0)
     for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
       if (!level_present(pa.mask, lvl)) continue;
+      auto eps = [&](uint4 l) {
+        if (l.w != lvl) return;
+        const double av = win ? a[l.x - n0] : load_fresh(&a[l.x - n0]);
+        atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z));
+      };
 #pragma unroll
-      for (int q = 0; q <= kAhead; ++q)
-        for (uint64_t j = pa.x0 + lane + 64u * (uint32_t)q; j < pa.x1; j += (q < kAhead ? pa.x1 : 64u)) {
-          const uint4 l = q < kAhead ? cur.x[q < kAhead ? q : 0] : post_link(L, j);
-          if (l.w != lvl) continue;
-          const double av = win ? a[l.x - n0] : load_fresh(&a[l.x - n0]);
-          atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z));
-        }
-      wave_sync();
+      for (int q = 0; q < kAhead; ++q)
+        if (pa.x0 + lane + (uint64_t)GS * q < pa.x1) eps(cur.x[q]);
+      post_tail<GS>(L, pa.x0, pa.x1, lane, eps);
+      group_sync<GS>();
     }
   if (win)
-    for (uint32_t i = lane; i < nt; i += 64) L.alpha[n0 + i] = a[i];
+    for (uint32_t i = lane; i < nt; i += GS) L.alpha[n0 + i] = a[i];
 }
 
 // alpha over every frame, ascending; epsilon links of a frame by source
-// level.  One wavefront.
+// level, on GS threads.
+template <int GS>
 __device__ __forceinline__ void alpha_wave(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
                                            bool swept, uint64_t start_node) {
   const int T = L.T;
@@ -489,16 +519,17 @@ __device__ __forceinline__ void alpha_wave(const LaneDesc& L, const DevGraph& g,
   {
     PostScal p0;
     alpha_scal(L, 0, p0);
-    post_items(L, g, p0, lane, false, x);
+    post_items<GS>(L, g, p0, lane, false, x);
   }
   for (int t = 0; t <= T; t += 2) {
-    alpha_step(L, g, sh, lane, t, swept, start_node, x, y);
-    if (t + 1 <= T) alpha_step(L, g, sh, lane, t + 1, swept, start_node, y, x);
+    alpha_step<GS>(L, g, sh, lane, t, swept, start_node, x, y);
+    if (t + 1 <= T) alpha_step<GS>(L, g, sh, lane, t + 1, swept, start_node, y, x);
   }
 }
 
-// Frame t of the beta pass on one wavefront (items of t in `cur`; those of
+// Frame t of the beta pass on a group of GS threads (items of t in `cur`; those of
 // t-1 are loaded into `nxt`).
+template <int GS>
 __device__ __forceinline__ void beta_step(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
                                           int t, bool swept, bool final_used, const PostItems& cur, PostItems& nxt) {
   const int T = L.T;
@@ -507,7 +538,7 @@ __device__ __forceinline__ void beta_step(const LaneDesc& L, const DevGraph& g, 
   if (t > 0) {
     PostScal pb;
     beta_scal(L, t - 1, pb);
-    post_items(L, g, pb, lane, false, nxt);
+    post_items<GS>(L, g, pb, lane, false, nxt);
   }
   const uint64_t n0 = pa.n0, n1 = pa.n1;
   const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
@@ -516,46 +547,49 @@ __device__ __forceinline__ void beta_step(const LaneDesc& L, const DevGraph& g, 
   if (win || !swept || t == T) {
 #pragma unroll
     for (int q = 0; q <= kAhead; ++q)
-      for (uint32_t i = lane + 64u * (uint32_t)q; i < nt; i += (q < kAhead ? nt : 64u)) {
+      for (uint32_t i = lane + (uint32_t)(GS * q); i < nt; i += (q < kAhead ? nt : (uint32_t)GS)) {
         double v = INFINITY;
         if (t == T)
           v = final_used ? (double)(q < kAhead ? cur.fw[q < kAhead ? q : 0] : g.final_w[L.n_state[n0 + i]]) : 0.0;
         b[i] = v;
       }
   }
-  wave_sync();
+  group_sync<GS>();
   if (pa.e1 > pa.e0) {
     const uint64_t m0 = pa.m0;
     const bool wn = pa.m1 - m0 <= kWin;
     const double* bn = wn ? sh.w.ab.b[buf ^ 1u] : L.beta + m0;
+    auto emit = [&](uint4 l) {
+      const double bv = wn ? bn[l.y - m0] : load_fresh(&bn[l.y - m0]);
+      atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w) + bv);
+    };
 #pragma unroll
-    for (int q = 0; q <= kAhead; ++q)
-      for (uint64_t j = pa.e0 + lane + 64u * (uint32_t)q; j < pa.e1; j += (q < kAhead ? pa.e1 : 64u)) {
-        const uint4 l = q < kAhead ? cur.e[q < kAhead ? q : 0] : post_link(L, j);
-        const double bv = wn ? bn[l.y - m0] : load_fresh(&bn[l.y - m0]);
-        atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w) + bv);
-      }
-    wave_sync();
+    for (int q = 0; q < kAhead; ++q)
+      if (pa.e0 + lane + (uint64_t)GS * q < pa.e1) emit(cur.e[q]);
+    post_tail<GS>(L, pa.e0, pa.e1, lane, emit);
+    group_sync<GS>();
   }
   if (pa.x1 > pa.x0)
     for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
       if (!level_present(pa.mask, (uint32_t)lvl)) continue;
+      auto eps = [&](uint4 l) {
+        if (l.w != (uint32_t)lvl) return;
+        const double bv = win ? b[l.y - n0] : load_fresh(&b[l.y - n0]);
+        atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + bv);
+      };
 #pragma unroll
-      for (int q = 0; q <= kAhead; ++q)
-        for (uint64_t j = pa.x0 + lane + 64u * (uint32_t)q; j < pa.x1; j += (q < kAhead ? pa.x1 : 64u)) {
-          const uint4 l = q < kAhead ? cur.x[q < kAhead ? q : 0] : post_link(L, j);
-          if (l.w != (uint32_t)lvl) continue;
-          const double bv = win ? b[l.y - n0] : load_fresh(&b[l.y - n0]);
-          atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + bv);
-        }
-      wave_sync();
+      for (int q = 0; q < kAhead; ++q)
+        if (pa.x0 + lane + (uint64_t)GS * q < pa.x1) eps(cur.x[q]);
+      post_tail<GS>(L, pa.x0, pa.x1, lane, eps);
+      group_sync<GS>();
     }
   if (win)
-    for (uint32_t i = lane; i < nt; i += 64) L.beta[n0 + i] = b[i];
+    for (uint32_t i = lane; i < nt; i += GS) L.beta[n0 + i] = b[i];
 }
 
 // beta over every frame, descending; epsilon links of a frame from the
-// highest source level.  One wavefront.
+// highest source level, on GS threads.
+template <int GS>
 __device__ __forceinline__ void beta_wave(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
                                           bool swept, bool final_used) {
   const int T = L.T;
@@ -563,11 +597,11 @@ __device__ __forceinline__ void beta_wave(const LaneDesc& L, const DevGraph& g, 
   {
     PostScal p0;
     beta_scal(L, T, p0);
-    post_items(L, g, p0, lane, final_used, x);
+    post_items<GS>(L, g, p0, lane, final_used, x);
   }
   for (int t = T; t >= 0; t -= 2) {
-    beta_step(L, g, sh, lane, t, swept, final_used, x, y);
-    if (t >= 1) beta_step(L, g, sh, lane, t - 1, swept, final_used, y, x);
+    beta_step<GS>(L, g, sh, lane, t, swept, final_used, x, y);
+    if (t >= 1) beta_step<GS>(L, g, sh, lane, t - 1, swept, final_used, y, x);
   }
 }
 
@@ -735,9 +769,17 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
     }
     start_node = lo;
   }
-  // alpha on wavefront 0 and beta on wavefront 1, concurrently
-  if (tid < 64) alpha_wave(L, g, sh, tid, swept, start_node);
-  else if (tid < 128) beta_wave(L, g, sh, tid - 64, swept, final_used);
+  // small kept lattices: alpha on wavefront 0 and beta on wavefront 1,
+  // concurrently; large ones (more than 64 kept links per frame on average):
+  // the whole workgroup, alpha then beta
+  if (n_kept <= 64 * ((uint64_t)T + 1)) {
+    if (tid < 64) alpha_wave<64>(L, g, sh, tid, swept, start_node);
+    else if (tid < 128) beta_wave<64>(L, g, sh, tid - 64, swept, final_used);
+  } else {
+    alpha_wave<kLT>(L, g, sh, tid, swept, start_node);
+    __syncthreads();
+    beta_wave<kLT>(L, g, sh, tid, swept, final_used);
+  }
   __syncthreads();
   const double Z = L.beta[start_node];
   if (tid == 0) {
