@@ -48,8 +48,8 @@ BYTES_LINK = 16
 # runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
 # divided by the counter's reading per byte of a plain device copy of known
 # size (bench.py --copy-kernel-bytes).  Valid while k_forward's sources hash to this.
-TRAFFIC = {"sources_sha256": "da63e369ba08b1970dcb59ab63aa5d50d582edf2d4ccc41ca9e96e45718a0355",
-           "bytes_per_launch": 53148409}
+TRAFFIC = {"sources_sha256": "0fcd903e396109939359d56d8fb4f6b603dc04f50124c4282e3dba76429b33d8",
+           "bytes_per_launch": 54145369}
 
 
 FORWARD_SOURCES = ("wd_block.h", "wd_common.h", "wd_forward.hip")  # what k_forward is built from
