@@ -76,9 +76,11 @@ def copy_kernel(nbytes: int) -> int:
     return 0
 
 
-def wide_chip(wfstdec, steps: int = 3) -> dict:
+def wide_chip(wfstdec, steps: int = 3, mode: str = "chip") -> dict:
     """Chip-wide mode on the wide-beam 2M-state graph (800 frames, beam 20,
-    no max-active): full decodes, lattice and posteriors included."""
+    no max-active): full decodes, lattice and posteriors included.
+    mode "chip_dyn": the same with dynamic load balancing of the emitting
+    arcs (the A/B against the prefix-sum work space)."""
     import synth
     import torch
     cfg = synth.workload("wide_2m")
@@ -87,19 +89,19 @@ def wide_chip(wfstdec, steps: int = 3) -> dict:
     graph = wfstdec.Graph(g, cfg["P"], "cuda:0")
     x = torch.from_numpy(L).to(graph.device)
     args = (cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
-    r = wfstdec.decode(graph, x, *args, timing=True, mode="chip")  # sizes the workspace
+    r = wfstdec.decode(graph, x, *args, timing=True, mode=mode)  # sizes the workspace
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     fwd, lat = [], []
     for _ in range(steps):
-        r = wfstdec.decode(graph, x, *args, timing=True, mode="chip")
+        r = wfstdec.decode(graph, x, *args, timing=True, mode=mode)
         fwd.append(r.stats["forward_ms"])
         lat.append(r.stats["lattice_ms"])
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
     T = L.shape[0]
     st = r.stats
-    out = {"workload": "wide_2m", "mode": "chip", "frames": T, "steps": steps,
+    out = {"workload": "wide_2m", "mode": mode, "frames": T, "steps": steps,
            "frames_per_s": round(T / wall, 1), "ms_per_step": round(1e3 * wall, 2),
            "arcs_expanded_per_s": round(st["arcs_expanded"] / wall, 1),
            "tokens_per_frame": round(st["tokens"] / (T + 1), 1),
@@ -217,7 +219,7 @@ def main() -> int:
     if not args.no_extra and workload == WORKLOAD:
         del graph, x
         torch.cuda.empty_cache()
-        out["other_workloads"] = [wide_chip(wfstdec)]
+        out["other_workloads"] = [wide_chip(wfstdec, mode="chip"), wide_chip(wfstdec, mode="chip_dyn")]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(g, L, cfg, workload)
     print(json.dumps(out), flush=True)

@@ -84,6 +84,12 @@ typedef struct {
 #define WD_FLAG_ONE_WORKGROUP 4u
 #define WD_FLAG_CHIP_WIDE 8u
 #define WD_CHIP_WIDE_MAX_ACTIVE 32768
+/* Chip-wide mode only (ignored by one-workgroup decodes): expand emitting
+ * arcs with the paper's dynamic load balancing (Alg. 2, Sec. 3.3: a
+ * dispatcher counter hands out frontier tokens; a group of lanes expands all
+ * arcs of one token) instead of the static prefix-sum work space.  The
+ * result is identical; the flag exists for the A/B comparison. */
+#define WD_FLAG_DYNAMIC_LB 16u
 
 /* Workspace capacities (per utterance).  0 selects a default.  A decode that
  * outgrows a capacity fails with WD_ECAPACITY and reports what it needed. */

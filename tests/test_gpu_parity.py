@@ -3,8 +3,9 @@ inputs: 1-best words, cost, every lattice link and node bit for bit,
 posteriors within 1e-4; with the debug flag also every frame's surviving
 tokens, cutoffs and the raw lattice.  Sizes span several tiles of the
 1024-thread workgroup, both compaction paths (LDS rank sort, state bitmap)
-and ragged frames.  Every case runs in both execution modes: one workgroup
-per utterance, and chip-wide kernels per frame."""
+and ragged frames.  Every case runs in every execution mode: one workgroup
+per utterance, chip-wide kernels per frame, and chip-wide with dynamic load
+balancing of the emitting arcs."""
 import math
 
 import numpy as np
@@ -17,7 +18,7 @@ from gpu_compare import assert_same
 
 pytestmark = pytest.mark.gpu
 INF = math.inf
-MODES = ["workgroup", "chip"]
+MODES = ["workgroup", "chip", "chip_dyn"]
 
 
 @pytest.fixture(scope="module")

@@ -55,7 +55,7 @@ def test_batch64_hclg_5m(wf, oracle_mod):
             raise AssertionError(f"lane {i} (T={Ls[i].shape[0]}): {e}")
 
 
-@pytest.mark.parametrize("mode", ["chip", "workgroup"])
+@pytest.mark.parametrize("mode", ["chip", "chip_dyn", "workgroup"])
 @pytest.mark.parametrize("name,T,debug", [("wide_2m", 12, True), ("wide_2m_dyadic", 8, True)])
 def test_wide_2m_prefix(wf, oracle_mod, name, T, debug, mode):
     """~1M tokens and ~1.5M raw links per frame, epsilon chains of depth 8."""
@@ -72,8 +72,8 @@ def test_wide_2m_prefix(wf, oracle_mod, name, T, debug, mode):
     assert_same(r, o, debug=debug)
 
 
-@pytest.mark.parametrize("name", ["wide_2m", "wide_2m_dyadic"])
-def test_wide_2m_full(wf, name):
+@pytest.mark.parametrize("name,mode", [("wide_2m", "chip"), ("wide_2m_dyadic", "chip"), ("wide_2m", "chip_dyn")])
+def test_wide_2m_full(wf, name, mode):
     """All 800 frames in chip-wide mode, as bench.py times them: the oracle
     needs ~2 s per frame here, so the result is checked by the properties
     that define it (tests/lattice_props.py, pinned on oracle results); the
@@ -81,12 +81,12 @@ def test_wide_2m_full(wf, name):
     import torch
     import lattice_props
     cfg = synth.workload(name)
-    print(f"\n[gpu case] {name} full ({cfg['T']} frames) mode=chip", flush=True)
+    print(f"\n[gpu case] {name} full ({cfg['T']} frames) mode={mode}", flush=True)
     g = synth.make_graph(cfg)
     L = synth.make_loglikes(cfg)
     graph = wf.Graph(g, cfg["P"])
     r = wf.decode(graph, torch.from_numpy(L).to(graph.device), cfg["beam"], cfg["max_active"],
-                  cfg["lattice_beam"], mode="chip")
+                  cfg["lattice_beam"], mode=mode)
     assert r.stats["max_tokens"] > 500000 and r.stats["raw_links"] > 500_000_000
     unique = lattice_props.check(g, L, cfg["lattice_beam"], r)
     assert unique or name.endswith("dyadic")
