@@ -507,12 +507,31 @@ __global__ void __launch_bounds__(kGT) k_g_count(const LaneDesc* __restrict__ la
   __shared__ uint32_t st_state[kStage];
   __shared__ unsigned long long st_pack[kStage];
   __shared__ uint32_t hist[kHistBins];
+  __shared__ GScratch s;
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
   const uint32_t nt = G.n_touched, kcutb = G.kcutb, best = G.best_key, shift = G.shift;
+  if (prm.max_active == 0) {
+    // every survivor is kept: mark its state; its token stays in the slot,
+    // where the compaction reads and resets it
+    if (blockIdx.x * kGT >= nt) return;
+    unsigned long long cnt = 0;
+    for (uint32_t i = blockIdx.x * kGT + threadIdx.x; i < nt; i += kGB * kGT) {
+      const uint32_t st = L.touched[i];
+      if ((uint32_t)(L.slot[st] >> 32) <= kcutb) {
+        atomicOr(&L.bitmap[st >> 5], 1u << (st & 31u));
+        ++cnt;
+      } else {
+        L.slot[st] = kEmpty;
+      }
+    }
+    cnt = gsum64(cnt, s);
+    if (threadIdx.x == 0 && cnt) atomicAdd(&G.n_surv, (uint32_t)cnt);
+    return;
+  }
   if (blockIdx.x * kStage >= nt) return;
-  const bool use_hist = prm.max_active > 0;
+  const bool use_hist = true;
   if (use_hist)
     for (uint32_t i = threadIdx.x; i < (uint32_t)kHistBins; i += kGT) hist[i] = 0;
   if (threadIdx.x == 0) n_st = 0;
@@ -535,14 +554,8 @@ __global__ void __launch_bounds__(kGT) k_g_count(const LaneDesc* __restrict__ la
     if (threadIdx.x == 0 && m) gbase = atomicAdd(&G.n_surv, m);
     __syncthreads();
     for (uint32_t i = threadIdx.x; i < m; i += kGT) {
-      const uint32_t st = st_state[i];
-      L.surv_state[gbase + i] = st;
+      L.surv_state[gbase + i] = st_state[i];
       L.surv_pack[gbase + i] = st_pack[i];
-      if (!use_hist) {
-        // no max-active: every survivor is kept (what k_g_mark does otherwise)
-        L.idx[st] = gbase + i;
-        atomicOr(&L.bitmap[st >> 5], 1u << (st & 31u));
-      }
     }
     __syncthreads();
     if (threadIdx.x == 0) n_st = 0;
@@ -636,7 +649,8 @@ __global__ void __launch_bounds__(kGT) k_g_select_hist(const LaneDesc* __restric
 }
 
 // Kept tokens mark their state in the bitmap; idx[state] = survivor index
-// (max-active on; without it the survivor kernel marks them).
+// (max-active on; without it the survivor kernel marks them and the tokens
+// stay in their slots).
 __global__ void __launch_bounds__(kGT) k_g_mark(const LaneDesc* __restrict__ lanes, GridLane* gl) {
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
@@ -678,7 +692,7 @@ __global__ void __launch_bounds__(kGT) k_g_bits(DevGraph g, const LaneDesc* __re
 constexpr uint32_t kCW = 1024;
 
 __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* __restrict__ lanes,
-                                                   GridLane* gl) {
+                                                   GridLane* gl, Params prm) {
   __shared__ GScratch s;
   __shared__ uint32_t wd[kCW], wp[kCW];
   const LaneDesc& L = lanes[blockIdx.y];
@@ -690,6 +704,7 @@ __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* _
   const uint64_t nb = G.node_base;
   const bool store = G.hist_ok != 0;
   const uint32_t best = G.best_key;
+  const bool in_slot = prm.max_active == 0;  // the kept tokens are still in their slots
   unsigned long long deg = 0;
   constexpr uint32_t per = kCW / kGT;
   for (uint64_t r0 = blo; r0 < bhi; r0 += kCW) {
@@ -717,7 +732,13 @@ __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* _
       if (!((word >> b) & 1u)) continue;
       const uint64_t p = pos0 + wp[j >> 5] + (uint32_t)__popc(word & ((1u << b) - 1u));
       const uint32_t st = (uint32_t)((r0 << 5) + j);
-      const unsigned long long v = L.surv_pack[L.idx[st]];
+      unsigned long long v;
+      if (in_slot) {
+        v = L.slot[st];
+        L.slot[st] = kEmpty;
+      } else {
+        v = L.surv_pack[L.idx[st]];
+      }
       const uint64_t node = nb + p;
       if (store) {
         L.n_state[node] = st;
@@ -1218,7 +1239,7 @@ void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, in
     if (prm.max_active > 0) hipLaunchKernelGGL(k_g_mark, all, blk, 0, st, lanes, gl);
     hipLaunchKernelGGL(k_g_bits, all, blk, 0, st, g, lanes, gl);
     hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 0, 0);
-    hipLaunchKernelGGL(k_g_compact, all, blk, 0, st, g, lanes, gl);
+    hipLaunchKernelGGL(k_g_compact, all, blk, 0, st, g, lanes, gl, prm);
     hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 1, 0);
     hipLaunchKernelGGL(k_g_degrees, all, blk, 0, st, g, lanes, gl);
     hipLaunchKernelGGL(k_g_link_count, all, blk, 0, st, g, lanes, gl, t);
