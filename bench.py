@@ -105,7 +105,7 @@ def wide_chip(wfstdec, steps: int = 3, mode: str = "chip") -> dict:
            "frames_per_s": round(T / wall, 1), "ms_per_step": round(1e3 * wall, 2),
            "arcs_expanded_per_s": round(st["arcs_expanded"] / wall, 1),
            "tokens_per_frame": round(st["tokens"] / (T + 1), 1),
-           "raw_links": st["raw_links"], "kept_links": st["kept_links"],
+           "raw_links": st["raw_links"], "kept_links": st["kept_links"], "link_store_peak": r.needed["links"],
            "kernel_ms": {"forward": round(sum(fwd) / steps, 2), "lattice": round(sum(lat) / steps, 2)}}
     del graph
     torch.cuda.empty_cache()
@@ -219,7 +219,7 @@ def main() -> int:
     if not args.no_extra and workload == WORKLOAD:
         del graph, x
         torch.cuda.empty_cache()
-        out["other_workloads"] = [wide_chip(wfstdec, mode="chip"), wide_chip(wfstdec, mode="chip_dyn")]
+        out["other_workloads"] = [wide_chip(wfstdec, mode=m) for m in ("chip", "chip_noprune", "chip_dyn")]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(g, L, cfg, workload)
     print(json.dumps(out), flush=True)

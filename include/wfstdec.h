@@ -90,6 +90,12 @@ typedef struct {
  * arcs of one token) instead of the static prefix-sum work space.  The
  * result is identical; the flag exists for the A/B comparison. */
 #define WD_FLAG_DYNAMIC_LB 16u
+/* Chip-wide mode prunes the lattice conservatively while decoding (every 32
+ * frames; Fig. 1 of the paper prunes on a second stream as decoding goes), so
+ * the link store holds roughly the surviving lattice plus the last window
+ * instead of every raw link.  The result is identical.  This flag turns it
+ * off (A/B).  Never done with WD_FLAG_DEBUG, which returns the raw lattice. */
+#define WD_FLAG_NO_INCREMENTAL_PRUNE 32u
 
 /* Workspace capacities (per utterance).  0 selects a default.  A decode that
  * outgrows a capacity fails with WD_ECAPACITY and reports what it needed. */

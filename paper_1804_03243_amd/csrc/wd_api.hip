@@ -336,7 +336,7 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
     stt.needed.frame_tokens = (int64_t)I.need_frame_tokens;
     stt.needed.frame_arcs = (int64_t)I.need_frame_arcs;
     stt.needed.nodes = (int64_t)I.tokens;
-    stt.needed.links = (int64_t)I.links;
+    stt.needed.links = (int64_t)I.need_links;
     stt.needed.kept_links = (int64_t)std::max<uint64_t>(I.kept, debug ? I.links : 0);
     out[b] = r;
     if (ls != WD_OK) continue;

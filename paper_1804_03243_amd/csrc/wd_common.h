@@ -89,7 +89,8 @@ struct LaneInfo {
   uint64_t eps_arcs;           // epsilon part of arcs_expanded
   uint64_t tokens;             // surviving tokens summed over frames (= nodes recorded)
   uint64_t max_tokens;
-  uint64_t links;              // raw lattice links
+  uint64_t links;              // raw lattice links (all ever recorded)
+  uint64_t need_links;         // link store capacity the decode needed (peak)
   uint64_t need_frame_tokens;  // largest per-frame touched-state count
   uint64_t need_frame_arcs;    // largest per-frame emitting work
   uint64_t kept;               // kept lattice links

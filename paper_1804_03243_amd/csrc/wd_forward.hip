@@ -819,6 +819,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     info->tokens = sh.c_tokens;
     info->max_tokens = sh.c_max_tokens;
     info->links = link_base;
+    info->need_links = link_base;
     info->need_frame_tokens = sh.c_need_frame;
     info->need_frame_arcs = sh.c_need_arcs;
   }

@@ -45,6 +45,9 @@ struct GridLane {
   unsigned long long best_total;  // (final cost key, node offset) of the best end token
   uint64_t node_base, node_base_prev, link_base;
   uint64_t arcs, eps_arcs, tokens, max_tokens, need_frame, need_arcs;
+  uint64_t raw_total, need_links;  // links ever recorded; peak store occupancy
+  uint64_t pbase, pend;            // incremental pruning: window of the link store
+  uint32_t pok, pad2;              // the window is pruned this pass
   uint32_t nb[kMaxLevels + 1];
   uint32_t hist[kHistBins];
   // per-workgroup partial sums, then their exclusive prefix (+ total at kGB):
@@ -926,6 +929,8 @@ __global__ void __launch_bounds__(kGT) k_g_end(const LaneDesc* __restrict__ lane
   const uint32_t n = G.n_keep;
   const unsigned long long all = G.part[2][kGB];
   const uint64_t nE = (uint32_t)all, nX = all >> 32;
+  G.raw_total += nE + nX;
+  if (G.link_base + nE + nX > G.need_links) G.need_links = G.link_base + nE + nX;
   if (G.hist_ok && G.link_base + nE + nX > L.link_cap) {
     G.hist_ok = 0;
     G.ovf |= kOvfLinks;
@@ -968,7 +973,8 @@ __global__ void k_g_finish(const LaneDesc* __restrict__ lanes, GridLane* gl) {
   info->eps_arcs = G.eps_arcs;
   info->tokens = G.tokens;
   info->max_tokens = G.max_tokens;
-  info->links = G.link_base;
+  info->links = G.raw_total;
+  info->need_links = G.need_links;
   info->need_frame_tokens = G.need_frame;
   info->need_frame_arcs = G.need_arcs;
 }
@@ -1048,10 +1054,12 @@ __global__ void __launch_bounds__(kGT) k_gs_init(DevGraph g, const LaneDesc* __r
 // Relaxes links into their source's extra cost: the emitting links that
 // leave frame t (emit != 0), or frame t's epsilon links whose source is on
 // level `lvl`.  extra(link) = extra(dst) + (x - cost(dst)).
+// `prune`: the conservative sweep of incremental pruning, while decoding.
 __global__ void __launch_bounds__(kGT) k_gs_relax(const LaneDesc* __restrict__ lanes, const GridLane* gl,
-                                                  int t, int emit, int lvl) {
+                                                  int t, int emit, int lvl, int prune) {
   const LaneDesc& L = lanes[blockIdx.y];
-  if (L.info->status != 0 || t > L.T || gl[blockIdx.y].best_total_key >= kInfKey) return;
+  const GridLane& G = gl[blockIdx.y];
+  if (prune ? (G.stop || !G.hist_ok) : (L.info->status != 0 || t > L.T || G.best_total_key >= kInfKey)) return;
   uint64_t k0, k1;
   if (emit) {
     if (t == L.T) return;
@@ -1213,6 +1221,122 @@ __global__ void __launch_bounds__(kGT) k_gn_write(const LaneDesc* __restrict__ l
   }
 }
 
+// ------------------------------------------------------ incremental pruning
+//
+// After frame t, every kPruneEvery frames: the window of frames [t0, t].  The
+// nodes of frame t get extra cost 0, the lowest an extra cost can be; the
+// sweep of Sec. 3.5 over the window then gives every node and link of the
+// window a lower bound of its final extra cost (the recursion is monotone in
+// the frame-t values).  A link whose bound is above the lattice beam (or
+// +inf: it leads nowhere) cannot be kept by the final pruning, and nothing it
+// could decide survives either: a node's final extra cost is the minimum over
+// its out-links, reached by a link within the beam whenever it matters.  Those
+// links are dropped and the window's part of the link store is compacted in
+// order, through scratch space right after the live links (done only when the
+// store has room for it).
+constexpr int kPruneEvery = 32;
+
+__global__ void __launch_bounds__(kGT) k_gp_init(const LaneDesc* __restrict__ lanes, const GridLane* gl,
+                                                 int t0, int t) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  const GridLane& G = gl[blockIdx.y];
+  if (G.stop || !G.hist_ok) return;
+  const uint64_t n0 = L.node_off[t0], nt = L.node_off[t], n1 = L.node_off[t + 1];
+  for (uint64_t n = n0 + (uint64_t)blockIdx.x * kGT + threadIdx.x; n < n1; n += (uint64_t)kGB * kGT)
+    L.extra_key[n] = n >= nt ? cost_key(0.0f) : kInfKey;
+}
+
+__device__ __forceinline__ bool gp_window(const LaneDesc& L, const GridLane& G, int t0, uint64_t* base,
+                                          uint64_t* end) {
+  *base = L.link_off[t0];
+  *end = G.link_base;
+  return 2 * *end - *base <= L.link_cap;
+}
+
+__global__ void __launch_bounds__(kGT) k_gp_count(const LaneDesc* __restrict__ lanes, GridLane* gl, int t0,
+                                                  uint32_t lb_key) {
+  __shared__ GScratch s;
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop || !G.hist_ok) return;
+  uint64_t base, end;
+  const bool ok = gp_window(L, G, t0, &base, &end);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    G.pbase = base;
+    G.pend = end;
+    G.pok = ok ? 1u : 0u;
+    if (2 * end - base > G.need_links) G.need_links = 2 * end - base;
+  }
+  if (!ok) return;
+  uint64_t blo, bhi;
+  chunk(end - base, blockIdx.x, &blo, &bhi);
+  unsigned long long c = 0;
+  for (uint64_t k = base + blo + threadIdx.x; k < base + bhi; k += kGT) {
+    const uint32_t le = L.le_key[k];
+    c += le <= lb_key && le < kInfKey;
+  }
+  c = gsum64(c, s);
+  if (threadIdx.x == 0) G.part[3][blockIdx.x] = c;
+}
+
+// Kept links to the scratch space in order; le_key[k] := kept links before k.
+__global__ void __launch_bounds__(kGT) k_gp_write(const LaneDesc* __restrict__ lanes, GridLane* gl,
+                                                  uint32_t lb_key) {
+  __shared__ GScratch s;
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop || !G.hist_ok || !G.pok) return;
+  const uint64_t base = G.pbase, end = G.pend;
+  uint64_t blo, bhi;
+  chunk(end - base, blockIdx.x, &blo, &bhi);
+  unsigned long long run = G.part[3][blockIdx.x];
+  for (uint64_t b0 = base + blo; b0 < base + bhi; b0 += kGT) {
+    const uint64_t k = b0 + threadIdx.x;
+    bool on = false;
+    if (k < base + bhi) {
+      const uint32_t le = L.le_key[k];
+      on = le <= lb_key && le < kInfKey;
+    }
+    unsigned long long tile;
+    const unsigned long long ex = run + gexcl64(on ? 1ull : 0ull, s, &tile);
+    run += tile;
+    if (k >= base + bhi) continue;
+    L.le_key[k] = (uint32_t)ex;
+    if (on) {
+      L.links[end + ex] = L.links[k];
+      L.link_lvl[end + ex] = L.link_lvl[k];
+    }
+  }
+}
+
+// New frame offsets of the window and the new end of the store.
+__global__ void __launch_bounds__(kGT) k_gp_fix(const LaneDesc* __restrict__ lanes, GridLane* gl, int t0, int t) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (G.stop || !G.hist_ok || !G.pok) return;
+  const uint64_t base = G.pbase, end = G.pend, nk = G.part[3][kGB];
+  for (int f = t0 + (int)threadIdx.x; f <= t + 1; f += kGT) {
+    const uint64_t o = L.link_off[f];
+    L.link_off[f] = base + (o < end ? L.le_key[o] : nk);
+    if (f <= t) {
+      const uint64_t x = L.link_xoff[f];
+      L.link_xoff[f] = base + (x < end ? L.le_key[x] : nk);
+    }
+  }
+  if (threadIdx.x == 0) G.link_base = base + nk;
+}
+
+__global__ void __launch_bounds__(kGT) k_gp_move(const LaneDesc* __restrict__ lanes, const GridLane* gl) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  const GridLane& G = gl[blockIdx.y];
+  if (G.stop || !G.hist_ok || !G.pok) return;
+  const uint64_t base = G.pbase, end = G.pend, nk = G.part[3][kGB];
+  for (uint64_t i = (uint64_t)blockIdx.x * kGT + threadIdx.x; i < nk; i += (uint64_t)kGB * kGT) {
+    L.links[base + i] = L.links[end + i];
+    L.link_lvl[base + i] = L.link_lvl[end + i];
+  }
+}
+
 // -------------------------------------------------------------------- launches
 
 size_t grid_lane_bytes() { return sizeof(GridLane); }
@@ -1221,6 +1345,8 @@ void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, in
                          const uint32_t* bad, int maxT, hipStream_t st) {
   GridLane* gl = (GridLane*)glv;
   const dim3 one(1, B), all(kGB, B), blk(kGT);
+  const bool prune = !(prm.flags & (WD_FLAG_DEBUG | WD_FLAG_NO_INCREMENTAL_PRUNE));
+  const uint32_t lb_key = cost_key(prm.lattice_beam);
   hipLaunchKernelGGL(k_g_init, one, blk, 0, st, lanes, gl, bad);
   for (int t = 0; t <= maxT; ++t) {
     hipLaunchKernelGGL(k_g_begin, one, dim3(64), 0, st, g, lanes, gl, prm, t);
@@ -1246,6 +1372,24 @@ void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, in
     hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 2, 0);
     hipLaunchKernelGGL(k_g_link_write, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_g_end, one, blk, 0, st, lanes, gl, t);
+    if (prune && (t + 1) % kPruneEvery == 0 && t < maxT) {
+      const int t0 = t + 1 - kPruneEvery;
+      hipLaunchKernelGGL(k_gp_init, all, blk, 0, st, lanes, gl, t0, t);
+      // frame f: the emitting links leaving it, then its epsilon levels; down
+      // to f = t0 - 1 for the emitting links into t0 (the window's first run;
+      // the extra costs this leaves on frame t0 - 1 are never read)
+      for (int f = t; f >= t0 - 1 && f >= 0; --f) {
+        if (f < t) hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, f, 1, 0, 1);
+        if (f >= t0)
+          for (int l = (int)g.nlevels - 1; l >= 0; --l)
+            hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, f, 0, l, 1);
+      }
+      hipLaunchKernelGGL(k_gp_count, all, blk, 0, st, lanes, gl, t0, lb_key);
+      hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 3, 0);
+      hipLaunchKernelGGL(k_gp_write, all, blk, 0, st, lanes, gl, lb_key);
+      hipLaunchKernelGGL(k_gp_fix, one, blk, 0, st, lanes, gl, t0, t);
+      hipLaunchKernelGGL(k_gp_move, all, blk, 0, st, lanes, gl);
+    }
   }
   hipLaunchKernelGGL(k_g_finish, one, dim3(64), 0, st, lanes, gl);
 }
@@ -1267,9 +1411,9 @@ void launch_grid_sweep(const DevGraph& g, const LaneDesc* lanes, void* glv, int 
   hipLaunchKernelGGL(k_gs_final, one, dim3(64), 0, st, lanes, gl);
   hipLaunchKernelGGL(k_gs_init, all, blk, 0, st, g, lanes, gl);
   for (int t = maxT; t >= 0; --t) {
-    hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, t, 1, 0);
+    hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, t, 1, 0, 0);
     for (int l = (int)g.nlevels - 1; l >= 0; --l)
-      hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, t, 0, l);
+      hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, t, 0, l, 0);
   }
   const uint32_t lb_key = cost_key(lattice_beam);
   hipLaunchKernelGGL(k_gk_count, all, blk, 0, st, lanes, gl, lb_key);

@@ -25,8 +25,10 @@ WD_FLAG_ONE_WORKGROUP = 4
 WD_FLAG_CHIP_WIDE = 8
 WD_CHIP_WIDE_MAX_ACTIVE = 32768
 WD_FLAG_DYNAMIC_LB = 16
+WD_FLAG_NO_INCREMENTAL_PRUNE = 32
 _MODE_FLAGS = {"auto": 0, "workgroup": WD_FLAG_ONE_WORKGROUP, "chip": WD_FLAG_CHIP_WIDE,
-               "chip_dyn": WD_FLAG_CHIP_WIDE | WD_FLAG_DYNAMIC_LB}
+               "chip_dyn": WD_FLAG_CHIP_WIDE | WD_FLAG_DYNAMIC_LB,
+               "chip_noprune": WD_FLAG_CHIP_WIDE | WD_FLAG_NO_INCREMENTAL_PRUNE}
 STATUS_NAMES = {0: "WD_OK", 1: "WD_EINVAL", 2: "WD_ECYCLE", 3: "WD_ENOPATH", 4: "WD_ECAPACITY",
                 5: "WD_EDEVICE"}
 
@@ -307,7 +309,8 @@ def decode_batch(graph: Graph, loglikes: list, beam: float, max_active: int, lat
     """Decode utterances (device float32 tensors, T_i x P) concurrently.
     `mode`: "workgroup" (one workgroup per utterance), "chip" (chip-wide
     kernels per frame), "chip_dyn" (chip-wide with dynamic load balancing of
-    the emitting arcs) or "auto" (the library's choice).  Returns one result
+    the emitting arcs), "chip_noprune" (chip-wide without incremental lattice
+    pruning) or "auto" (the library's choice).  Returns one result
     namespace per utterance."""
     torch = _torch()
     for x in loglikes:

@@ -112,6 +112,23 @@ def test_tiny_10k(wf, oracle_mod, tiny10k, beam, ma, lb, mode):
     invariants.check_all(g, L, beam, ma, lb, r)
 
 
+@pytest.mark.parametrize("mode", ["chip", "chip_noprune", "chip_dyn"])
+@pytest.mark.parametrize("beam,ma,lb", TINY_PARAMS)
+def test_incremental_prune(wf, oracle_mod, tiny10k, beam, ma, lb, mode):
+    """Chip-wide decodes without the debug flag prune the lattice every 32
+    frames while decoding (conservatively); the result still equals the
+    oracle's, and with a finite lattice beam the link store peaks below the
+    raw lattice."""
+    cfg, g, L, graph = tiny10k
+    r, o, _ = _run(wf, oracle_mod, g, L, cfg["P"], beam, ma, lb, debug=False, graph=graph,
+                   case=f"tiny_10k incremental prune {beam}/{ma}/{lb}", mode=mode)
+    assert r.stats["raw_links"] == o.stats["raw_links"]
+    if mode == "chip_noprune" or math.isinf(lb):
+        assert r.needed["links"] <= r.stats["raw_links"]
+    else:
+        assert r.needed["links"] < r.stats["raw_links"]
+
+
 @pytest.mark.parametrize("mode", MODES)
 def test_determinism(wf, oracle_mod, tiny10k, mode):
     import torch

@@ -88,5 +88,7 @@ def test_wide_2m_full(wf, name, mode):
     r = wf.decode(graph, torch.from_numpy(L).to(graph.device), cfg["beam"], cfg["max_active"],
                   cfg["lattice_beam"], mode=mode)
     assert r.stats["max_tokens"] > 500000 and r.stats["raw_links"] > 500_000_000
+    # incremental pruning keeps the link store far below the raw lattice
+    assert r.needed["links"] < r.stats["raw_links"] // 2
     unique = lattice_props.check(g, L, cfg["lattice_beam"], r)
     assert unique or name.endswith("dyadic")
