@@ -90,11 +90,19 @@ typedef struct {
  * arcs of one token) instead of the static prefix-sum work space.  The
  * result is identical; the flag exists for the A/B comparison. */
 #define WD_FLAG_DYNAMIC_LB 16u
-/* Chip-wide mode prunes the lattice conservatively while decoding (every 32
- * frames; Fig. 1 of the paper prunes on a second stream as decoding goes), so
- * the link store holds roughly the surviving lattice plus the last window
- * instead of every raw link.  The result is identical.  This flag turns it
- * off (A/B).  Never done with WD_FLAG_DEBUG, which returns the raw lattice. */
+/* Chip-wide mode prunes the lattice conservatively while decoding, on a
+ * second stream of the library's own (Fig. 1 of the paper prunes on a second
+ * stream as decoding goes): frames are recorded in windows of 32 into two raw
+ * window slots taken in turn; once a window is complete, its links are swept
+ * with the lowest possible extra cost (0) on its last frame's tokens, and the
+ * links that cannot be kept by the final pruning are dropped while the rest
+ * are appended to the compacted region of the link store.  Decoding goes on
+ * meanwhile and only waits for a window's pruning before it reuses that
+ * window's slot.  The link store then holds the compacted region (capacity
+ * `links`) plus the two slots (`window_links` each) instead of every raw
+ * link.  The result is identical.  This flag turns it off (A/B).  Never done
+ * with WD_FLAG_DEBUG, which returns the raw lattice.  Decodes on one device
+ * share the library's pruning stream and are ordered on it by events. */
 #define WD_FLAG_NO_INCREMENTAL_PRUNE 32u
 
 /* Workspace capacities (per utterance).  0 selects a default.  A decode that
@@ -103,8 +111,11 @@ typedef struct {
   int64_t frame_tokens;   /* tokens touched in one frame (<= S) */
   int64_t frame_arcs;     /* emitting arcs expanded in one frame */
   int64_t nodes;          /* surviving tokens summed over all frames (< 2^32) */
-  int64_t links;          /* lattice links recorded before pruning */
+  int64_t links;          /* lattice links recorded before pruning (the link store; with
+                             chip-wide incremental pruning its compacted region) */
   int64_t kept_links;     /* lattice links returned (after pruning; raw links with WD_FLAG_DEBUG) */
+  int64_t window_links;   /* chip-wide incremental pruning: raw links of one 32-frame window
+                             (`links` is then the compacted region); unused otherwise */
 } wd_caps;
 
 /* One lattice link of the pruned lattice, i.e. one token-passing operation

@@ -31,8 +31,19 @@ wd_status hip_check(hipError_t e, const char* what) {
 namespace {
 
 struct Caps {
-  uint64_t frame, arcs, nodes, links, kept, raw, words;
+  uint64_t frame, arcs, nodes, links, kept, raw, words, win;
 };
+
+// Execution mode: chip-wide kernels per frame for frames too large for one
+// workgroup (no max-active limit, or a very large one).
+bool chip_wide_mode(const wd_params* p) {
+  return (p->flags & WD_FLAG_CHIP_WIDE) ||
+         (!(p->flags & WD_FLAG_ONE_WORKGROUP) && (p->max_active == 0 || p->max_active >= WD_CHIP_WIDE_MAX_ACTIVE));
+}
+
+bool incremental_prune(const wd_params* p) {
+  return chip_wide_mode(p) && !(p->flags & (WD_FLAG_DEBUG | WD_FLAG_NO_INCREMENTAL_PRUNE));
+}
 
 Caps resolve_caps(const wd_graph* g, int32_t max_T, const wd_params* p, const wd_caps* c) {
   Caps r{};
@@ -50,6 +61,9 @@ Caps resolve_caps(const wd_graph* g, int32_t max_T, const wd_params* p, const wd
   r.links = (c && c->links > 0) ? (uint64_t)c->links : 4 * r.nodes;
   r.kept = (c && c->kept_links > 0) ? (uint64_t)c->kept_links : std::min<uint64_t>(r.links, 1u << 20);
   r.raw = (p->flags & WD_FLAG_DEBUG) ? r.links : 0;
+  r.win = 0;
+  if (incremental_prune(p))
+    r.win = (c && c->window_links > 0) ? (uint64_t)c->window_links : std::max<uint64_t>(r.links / 4, 1);
   r.words = T1 * (g->nlevels + 1) + 1;
   return r;
 }
@@ -106,17 +120,19 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
   char* n_state = take(4 * c.nodes);
   char* n_pack = take(8 * c.nodes);
   char* n_pred = take(4 * c.nodes);
-  char* links = take(16 * c.links);
-  char* link_lvl = take(c.links);
+  const uint64_t nlink = c.links + 2 * c.win;
+  char* links = take(16 * nlink);
+  char* link_lvl = take(nlink);
   char* node_off = take(8 * T2);
   char* link_off = take(8 * T2);
   char* link_xoff = take(8 * T2);
+  char* link_end = take(8 * T2);
   char* xmask = take(4 * T2);
   char* best = take(4 * T2);
   char* cutb = take(4 * T2);
   char* cut = take(4 * T2);
   char* extra_key = take(4 * c.nodes);
-  char* le_key = take(4 * c.links);
+  char* le_key = take(4 * nlink);
   char* alpha = take(8 * c.nodes);
   char* beta = take(8 * c.nodes);
   char* used = take(4 * R.used_words);
@@ -139,6 +155,7 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
       L.cand_cap = c.arcs;
       L.node_cap = c.nodes;
       L.link_cap = c.links;
+      L.win_cap = c.win;
       L.kept_cap = c.kept;
       L.raw_cap = c.raw;
       L.word_cap = c.words;
@@ -161,17 +178,18 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
       L.n_state = (uint32_t*)at(n_state, 4 * c.nodes);
       L.n_pack = (unsigned long long*)at(n_pack, 8 * c.nodes);
       L.n_pred = (uint32_t*)at(n_pred, 4 * c.nodes);
-      L.links = (uint4*)at(links, 16 * c.links);
-      L.link_lvl = (uint8_t*)at(link_lvl, c.links);
+      L.links = (uint4*)at(links, 16 * nlink);
+      L.link_lvl = (uint8_t*)at(link_lvl, nlink);
       L.node_off = (uint64_t*)at(node_off, 8 * T2);
       L.link_off = (uint64_t*)at(link_off, 8 * T2);
       L.link_xoff = (uint64_t*)at(link_xoff, 8 * T2);
+      L.link_end = (uint64_t*)at(link_end, 8 * T2);
       L.xmask = (uint32_t*)at(xmask, 4 * T2);
       L.best = (float*)at(best, 4 * T2);
       L.cutb = (float*)at(cutb, 4 * T2);
       L.cut = (float*)at(cut, 4 * T2);
       L.extra_key = (uint32_t*)at(extra_key, 4 * c.nodes);
-      L.le_key = (uint32_t*)at(le_key, 4 * c.links);
+      L.le_key = (uint32_t*)at(le_key, 4 * nlink);
       L.alpha = (double*)at(alpha, 8 * c.nodes);
       L.beta = (double*)at(beta, 8 * c.nodes);
       L.used = (uint32_t*)at(used, 4 * R.used_words);
@@ -232,6 +250,7 @@ extern "C" wd_status wd_workspace_bytes(const wd_graph* g, int32_t lanes, int32_
     caps_out->nodes = (int64_t)c.nodes;
     caps_out->links = (int64_t)c.links;
     caps_out->kept_links = (int64_t)c.kept;
+    caps_out->window_links = (int64_t)c.win;
   }
   return WD_OK;
 }
@@ -278,14 +297,14 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
   if (timing)
     for (auto& e : ev)
       if ((st = hip_check(hipEventCreate(&e), "event"))) return st;
-  // execution mode: chip-wide kernels per frame for frames too large for one
-  // workgroup (no max-active limit, or a very large one)
-  const bool chip_wide =
-      (p->flags & WD_FLAG_CHIP_WIDE) ||
-      (!(p->flags & WD_FLAG_ONE_WORKGROUP) && (p->max_active == 0 || p->max_active >= WD_CHIP_WIDE_MAX_ACTIVE));
+  const bool chip_wide = chip_wide_mode(p);
   if (timing) (void)hipEventRecord(ev[0], s);
-  if (chip_wide) launch_grid_forward(g->dg, R.desc, R.grid, B, prm, R.bad, max_T, s);
-  else launch_forward(g->dg, R.desc, B, prm, R.bad, s);
+  if (chip_wide) {
+    if ((st = launch_grid_forward(g->dg, R.desc, R.grid, B, prm, incremental_prune(p), R.bad, max_T, s)))
+      return st;
+  } else {
+    launch_forward(g->dg, R.desc, B, prm, R.bad, s);
+  }
   if (timing) (void)hipEventRecord(ev[1], s);
   if (chip_wide) {
     launch_grid_sweep(g->dg, R.desc, R.grid, B, max_T, p->lattice_beam, s);
@@ -337,6 +356,7 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
     stt.needed.frame_arcs = (int64_t)I.need_frame_arcs;
     stt.needed.nodes = (int64_t)I.tokens;
     stt.needed.links = (int64_t)I.need_links;
+    stt.needed.window_links = (int64_t)I.need_window;
     stt.needed.kept_links = (int64_t)std::max<uint64_t>(I.kept, debug ? I.links : 0);
     out[b] = r;
     if (ls != WD_OK) continue;

@@ -90,7 +90,9 @@ struct LaneInfo {
   uint64_t tokens;             // surviving tokens summed over frames (= nodes recorded)
   uint64_t max_tokens;
   uint64_t links;              // raw lattice links (all ever recorded)
-  uint64_t need_links;         // link store capacity the decode needed (peak)
+  uint64_t need_links;         // link store capacity the decode needed (peak; with
+                               // incremental pruning: the compacted region)
+  uint64_t need_window;        // incremental pruning: raw links of the largest window
   uint64_t need_frame_tokens;  // largest per-frame touched-state count
   uint64_t need_frame_arcs;    // largest per-frame emitting work
   uint64_t kept;               // kept lattice links
@@ -140,6 +142,7 @@ struct LaneDesc {
   int32_t T;
   int32_t pad0;
   uint64_t frame_cap, cand_cap, node_cap, link_cap, kept_cap, word_cap;
+  uint64_t win_cap;            // incremental pruning: links of one raw window slot (0: off)
   // per-frame scratch
   unsigned long long* slot;    // [S] packed (cost key, arc id); kEmpty between frames
   uint32_t* idx;               // [S] node id of a state in the current frame / scratch
@@ -163,18 +166,21 @@ struct LaneDesc {
   uint32_t* n_state;           // [node_cap]
   unsigned long long* n_pack;  // [node_cap] (cost key, predecessor arc)
   uint32_t* n_pred;            // [node_cap] predecessor node
-  uint4* links;                // [link_cap] {arc, src node, dst node, x bits}
-  uint8_t* link_lvl;           // [link_cap] epsilon level of the source (epsilon links)
+  // link store [link_cap + 2*win_cap]: with incremental pruning, the compacted
+  // region [0, link_cap) then two raw window slots of win_cap links each
+  uint4* links;                // {arc, src node, dst node, x bits}
+  uint8_t* link_lvl;           // epsilon level of the source (epsilon links)
   uint64_t* node_off;          // [T+2]
   uint64_t* link_off;          // [T+2] first link of frame t (emitting run)
   uint64_t* link_xoff;         // [T+2] first epsilon link of frame t
+  uint64_t* link_end;          // [T+2] one past the last link of frame t
   uint32_t* xmask;             // [T+2] levels of the epsilon links of frame t (bit 31: 31 or more)
   float* best;                 // [T+1]
   float* cutb;                 // [T+1]
   float* cut;                  // [T+1]
   // lattice pass
   uint32_t* extra_key;         // [node_cap]
-  uint32_t* le_key;            // [link_cap]
+  uint32_t* le_key;            // [link_cap + 2*win_cap]
   double* alpha;               // [node_cap]
   double* beta;                // [node_cap]
   uint32_t* used;              // [ceil(node_cap/32)+1] lattice-node bitmap

@@ -14,7 +14,10 @@
 // identical.  The backward pruning sweep of Sec. 3.5 has a chip-wide form too.
 // Every kernel reads the frame's sizes from device memory, so the host never
 // waits between frames; an utterance whose status is set skips the rest.
+#include <mutex>
+
 #include "wd_block.h"
+#include "wd_host.h"
 #include "../../include/wfstdec.h"
 
 namespace wd {
@@ -23,6 +26,21 @@ constexpr int kGT = 256;          // threads per workgroup
 constexpr int kGW = kGT / 64;     // wavefronts per workgroup
 constexpr uint32_t kGB = 1024;    // workgroups per utterance
 constexpr uint32_t kSeg = 4096;   // frontier prefix sums a workgroup keeps in LDS
+
+// Incremental pruning runs in windows of this many frames; its sweep kernels
+// use a quarter of the workgroups, leaving room for the decoding kernels.
+constexpr int kPruneEvery = 32;
+constexpr uint32_t kPB = kGB / 4;
+
+// Incremental pruning state of one utterance, written only by the kernels on
+// the pruning stream and, once the host has made the decoding stream wait for
+// them, by the last window's gather.
+struct PruneLane {
+  uint64_t kend;      // links in the compacted region (still counted after an overflow)
+  uint32_t go;        // the current window is pruned
+  uint32_t ovf;       // the compacted region overflowed
+  unsigned long long part[kGB + 1];  // kept links per workgroup, then their prefix
+};
 
 // Per-utterance state carried from kernel to kernel.
 struct GridLane {
@@ -45,9 +63,10 @@ struct GridLane {
   unsigned long long best_total;  // (final cost key, node offset) of the best end token
   uint64_t node_base, node_base_prev, link_base;
   uint64_t arcs, eps_arcs, tokens, max_tokens, need_frame, need_arcs;
-  uint64_t raw_total, need_links;  // links ever recorded; peak store occupancy
-  uint64_t pbase, pend;            // incremental pruning: window of the link store
-  uint32_t pok, pad2;              // the window is pruned this pass
+  uint64_t raw_total;              // links ever recorded
+  uint64_t slot_lo, slot_hi;       // where links go: the whole store, or the window's slot
+  uint64_t need_win;               // largest occupancy of the store (or of a slot)
+  PruneLane pr;
   uint32_t nb[kMaxLevels + 1];
   uint32_t hist[kHistBins];
   // per-workgroup partial sums, then their exclusive prefix (+ total at kGB):
@@ -145,15 +164,8 @@ __device__ __forceinline__ uint32_t seg_find(const Seg& sg, const uint32_t* seg,
   return sg.pl + (sg.lds ? search_le(seg, sg.m, w) : search_le(a + sg.pl, sg.m, w));
 }
 
-// Exclusive scan of the kGB partial sums part[which] of each utterance
-// (lattice != 0: after the forward pass has stopped, for utterances whose
-// status is still WD_OK).
-__global__ void __launch_bounds__(kGT) k_g_scan(const LaneDesc* __restrict__ lanes, GridLane* gl, int which,
-                                                int lattice) {
-  __shared__ GScratch s;
-  GridLane& G = gl[blockIdx.y];
-  if (lattice ? lanes[blockIdx.y].info->status != 0 : G.stop != 0) return;
-  unsigned long long* part = G.part[which];
+// Exclusive scan of one utterance's kGB per-workgroup sums (+ total at kGB).
+__device__ __forceinline__ void scan_parts(unsigned long long* part, GScratch& s) {
   constexpr uint32_t per = kGB / kGT;
   unsigned long long v[per], sum = 0;
 #pragma unroll
@@ -171,15 +183,31 @@ __global__ void __launch_bounds__(kGT) k_g_scan(const LaneDesc* __restrict__ lan
   if (threadIdx.x == 0) part[kGB] = tot;
 }
 
+// Exclusive scan of the kGB partial sums part[which] of each utterance
+// (lattice != 0: after the forward pass has stopped, for utterances whose
+// status is still WD_OK).
+__global__ void __launch_bounds__(kGT) k_g_scan(const LaneDesc* __restrict__ lanes, GridLane* gl, int which,
+                                                int lattice) {
+  __shared__ GScratch s;
+  GridLane& G = gl[blockIdx.y];
+  if (lattice ? lanes[blockIdx.y].info->status != 0 : G.stop != 0) return;
+  scan_parts(G.part[which], s);
+}
+
 // ---------------------------------------------------------------- forward pass
 
 __global__ void k_g_init(const LaneDesc* __restrict__ lanes, GridLane* gl, const uint32_t* __restrict__ bad) {
+  const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   uint32_t* w = reinterpret_cast<uint32_t*>(&G);
   for (uint32_t i = threadIdx.x; i < (uint32_t)(sizeof(GridLane) / 4); i += blockDim.x) w[i] = 0;
   __syncthreads();
   if (threadIdx.x == 0) {
     G.hist_ok = 1;
+    // with incremental pruning, frames 0..31 go to the first window slot
+    G.slot_lo = L.win_cap ? L.link_cap : 0;
+    G.slot_hi = L.win_cap ? L.link_cap + L.win_cap : L.link_cap;
+    G.link_base = G.slot_lo;
     if (bad[blockIdx.y]) {
       G.status = 1;  // WD_EINVAL
       G.stop = 1;
@@ -874,7 +902,7 @@ __global__ void __launch_bounds__(kGT) k_g_link_write(DevGraph g, const LaneDesc
   const unsigned long long all = G.part[2][kGB];
   const uint64_t nE = (uint32_t)all;
   const uint64_t lb = G.link_base, nb = G.node_base;
-  if (!G.hist_ok || lb + nE + (all >> 32) > L.link_cap) return;
+  if (!G.hist_ok || lb + nE + (all >> 32) > G.slot_hi) return;
   uint64_t blo, bhi;
   chunk((uint64_t)W + G.W_eps, blockIdx.x, &blo, &bhi);
   if (blo >= bhi) return;
@@ -929,9 +957,10 @@ __global__ void __launch_bounds__(kGT) k_g_end(const LaneDesc* __restrict__ lane
   const uint32_t n = G.n_keep;
   const unsigned long long all = G.part[2][kGB];
   const uint64_t nE = (uint32_t)all, nX = all >> 32;
+  const uint64_t end = G.link_base + nE + nX;
   G.raw_total += nE + nX;
-  if (G.link_base + nE + nX > G.need_links) G.need_links = G.link_base + nE + nX;
-  if (G.hist_ok && G.link_base + nE + nX > L.link_cap) {
+  if (end - G.slot_lo > G.need_win) G.need_win = end - G.slot_lo;
+  if (G.hist_ok && end > G.slot_hi) {
     G.hist_ok = 0;
     G.ovf |= kOvfLinks;
   }
@@ -939,14 +968,20 @@ __global__ void __launch_bounds__(kGT) k_g_end(const LaneDesc* __restrict__ lane
   L.node_off[t + 1] = G.node_base + n;
   L.link_off[t] = G.link_base;
   L.link_xoff[t] = G.link_base + nE;
-  L.link_off[t + 1] = G.link_base + nE + nX;
+  L.link_end[t] = end;
+  L.link_off[t + 1] = end;
   L.xmask[t] = G.xmask;
   L.best[t] = key_cost(G.best_key);
   L.cutb[t] = key_cost(G.kcutb);
   L.cut[t] = key_cost(G.cut_key);
   G.tokens += n;
   G.max_tokens = n > G.max_tokens ? n : G.max_tokens;
-  G.link_base += nE + nX;
+  G.link_base = end;
+  if (L.win_cap && (t + 1) % kPruneEvery == 0) {  // next window: the other slot
+    G.slot_lo = L.link_cap + (((uint32_t)(t + 1) / kPruneEvery) & 1u) * L.win_cap;
+    G.slot_hi = G.slot_lo + L.win_cap;
+    G.link_base = G.slot_lo;
+  }
   G.node_base_prev = G.node_base;
   G.node_base += n;
   G.n_prev = n;
@@ -965,16 +1000,18 @@ __global__ void k_g_finish(const LaneDesc* __restrict__ lanes, GridLane* gl) {
   if (threadIdx.x != 0 || G.status == 1) return;
   LaneInfo* info = L.info;
   int32_t status = G.status;
-  if (status == 0 && (G.ovf & (kOvfNodes | kOvfLinks))) status = 4;
+  const uint32_t ovf = G.ovf | (G.pr.ovf ? (uint32_t)kOvfLinks : 0u);
+  if (status == 0 && (ovf & (kOvfNodes | kOvfLinks))) status = 4;
   info->status = status;
   info->frames_done = (int32_t)G.frames;
-  info->overflow = G.ovf;
+  info->overflow = ovf;
   info->arcs_expanded = G.arcs + G.eps_arcs;
   info->eps_arcs = G.eps_arcs;
   info->tokens = G.tokens;
   info->max_tokens = G.max_tokens;
   info->links = G.raw_total;
-  info->need_links = G.need_links;
+  info->need_links = L.win_cap ? G.pr.kend : G.need_win;
+  info->need_window = L.win_cap ? G.need_win : 0;
   info->need_frame_tokens = G.need_frame;
   info->need_frame_arcs = G.need_arcs;
 }
@@ -1059,7 +1096,7 @@ __global__ void __launch_bounds__(kGT) k_gs_relax(const LaneDesc* __restrict__ l
                                                   int t, int emit, int lvl, int prune) {
   const LaneDesc& L = lanes[blockIdx.y];
   const GridLane& G = gl[blockIdx.y];
-  if (prune ? (G.stop || !G.hist_ok) : (L.info->status != 0 || t > L.T || G.best_total_key >= kInfKey)) return;
+  if (prune ? !G.pr.go : (L.info->status != 0 || t > L.T || G.best_total_key >= kInfKey)) return;
   uint64_t k0, k1;
   if (emit) {
     if (t == L.T) return;
@@ -1068,9 +1105,9 @@ __global__ void __launch_bounds__(kGT) k_gs_relax(const LaneDesc* __restrict__ l
   } else {
     if (((L.xmask[t] >> (lvl < 31 ? lvl : 31)) & 1u) == 0) return;
     k0 = L.link_xoff[t];
-    k1 = L.link_off[t + 1];
+    k1 = L.link_end[t];
   }
-  for (uint64_t k = k0 + blockIdx.x * kGT + threadIdx.x; k < k1; k += (uint64_t)kGB * kGT) {
+  for (uint64_t k = k0 + blockIdx.x * kGT + threadIdx.x; k < k1; k += (uint64_t)gridDim.x * kGT) {
     if (!emit && L.link_lvl[k] != (uint8_t)lvl) continue;
     const uint4 v = L.links[k];
     const float exd = key_cost(L.extra_key[v.z]);
@@ -1223,117 +1260,168 @@ __global__ void __launch_bounds__(kGT) k_gn_write(const LaneDesc* __restrict__ l
 
 // ------------------------------------------------------ incremental pruning
 //
-// After frame t, every kPruneEvery frames: the window of frames [t0, t].  The
-// nodes of frame t get extra cost 0, the lowest an extra cost can be; the
+// Frames are recorded in windows of kPruneEvery frames, window j in raw slot
+// j mod 2 of the link store.  Once frame t, the last of window [t0, t], is
+// done, the pruning stream sweeps the window while decoding goes on: the
+// nodes of frame t get extra cost 0, the lowest an extra cost can be, and the
 // sweep of Sec. 3.5 over the window then gives every node and link of the
 // window a lower bound of its final extra cost (the recursion is monotone in
 // the frame-t values).  A link whose bound is above the lattice beam (or
 // +inf: it leads nowhere) cannot be kept by the final pruning, and nothing it
 // could decide survives either: a node's final extra cost is the minimum over
-// its out-links, reached by a link within the beam whenever it matters.  Those
-// links are dropped and the window's part of the link store is compacted in
-// order, through scratch space right after the live links (done only when the
-// store has room for it).
-constexpr int kPruneEvery = 32;
+// its out-links, reached by a link within the beam whenever it matters.  The
+// other links are appended, in order, to the compacted region [0, link_cap),
+// and the window's frame offsets move with them.  Decoding waits for window
+// j's pruning only before frame 32 (j + 2) reuses its slot.  The last window
+// of an utterance is never pruned (the final sweep follows): the gather moves
+// it behind the compacted region, which then holds every frame in order, as
+// the link store does without incremental pruning.
+//
+// Decoding and pruning touch disjoint data while they overlap: the window's
+// links, link offsets, extra costs and le_key belong to the pruning stream;
+// node offsets and costs of the window are final and only read.  The gate
+// `go` is taken once per window from the decoding state (status and
+// hist_ok only ever change to a failure, whose result is not returned).
+
+__global__ void k_gp_go(const LaneDesc* __restrict__ lanes, GridLane* gl, int t) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  if (threadIdx.x != 0) return;
+  const int32_t status = __hip_atomic_load(&G.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint32_t ok = __hip_atomic_load(&G.hist_ok, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  G.pr.go = (t < L.T && status == 0 && ok) ? 1u : 0u;
+}
 
 __global__ void __launch_bounds__(kGT) k_gp_init(const LaneDesc* __restrict__ lanes, const GridLane* gl,
                                                  int t0, int t) {
   const LaneDesc& L = lanes[blockIdx.y];
   const GridLane& G = gl[blockIdx.y];
-  if (G.stop || !G.hist_ok) return;
+  if (!G.pr.go) return;
   const uint64_t n0 = L.node_off[t0], nt = L.node_off[t], n1 = L.node_off[t + 1];
-  for (uint64_t n = n0 + (uint64_t)blockIdx.x * kGT + threadIdx.x; n < n1; n += (uint64_t)kGB * kGT)
+  for (uint64_t n = n0 + (uint64_t)blockIdx.x * kGT + threadIdx.x; n < n1; n += (uint64_t)gridDim.x * kGT)
     L.extra_key[n] = n >= nt ? cost_key(0.0f) : kInfKey;
 }
 
-__device__ __forceinline__ bool gp_window(const LaneDesc& L, const GridLane& G, int t0, uint64_t* base,
-                                          uint64_t* end) {
-  *base = L.link_off[t0];
-  *end = G.link_base;
-  return 2 * *end - *base <= L.link_cap;
+__device__ __forceinline__ bool gp_kept(const LaneDesc& L, uint64_t k, uint32_t lb_key) {
+  const uint32_t le = L.le_key[k];
+  return le <= lb_key && le < kInfKey;
 }
 
 __global__ void __launch_bounds__(kGT) k_gp_count(const LaneDesc* __restrict__ lanes, GridLane* gl, int t0,
-                                                  uint32_t lb_key) {
+                                                  int t, uint32_t lb_key) {
   __shared__ GScratch s;
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
-  if (G.stop || !G.hist_ok) return;
-  uint64_t base, end;
-  const bool ok = gp_window(L, G, t0, &base, &end);
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    G.pbase = base;
-    G.pend = end;
-    G.pok = ok ? 1u : 0u;
-    if (2 * end - base > G.need_links) G.need_links = 2 * end - base;
-  }
-  if (!ok) return;
+  if (!G.pr.go) return;
+  const uint64_t base = L.link_off[t0], end = L.link_end[t];
   uint64_t blo, bhi;
   chunk(end - base, blockIdx.x, &blo, &bhi);
   unsigned long long c = 0;
-  for (uint64_t k = base + blo + threadIdx.x; k < base + bhi; k += kGT) {
-    const uint32_t le = L.le_key[k];
-    c += le <= lb_key && le < kInfKey;
-  }
+  for (uint64_t k = base + blo + threadIdx.x; k < base + bhi; k += kGT) c += gp_kept(L, k, lb_key);
   c = gsum64(c, s);
-  if (threadIdx.x == 0) G.part[3][blockIdx.x] = c;
+  if (threadIdx.x == 0) G.pr.part[blockIdx.x] = c;
 }
 
-// Kept links to the scratch space in order; le_key[k] := kept links before k.
-__global__ void __launch_bounds__(kGT) k_gp_write(const LaneDesc* __restrict__ lanes, GridLane* gl,
-                                                  uint32_t lb_key) {
+__global__ void __launch_bounds__(kGT) k_gp_scan(GridLane* gl) {
+  __shared__ GScratch s;
+  GridLane& G = gl[blockIdx.y];
+  if (!G.pr.go) return;
+  scan_parts(G.pr.part, s);
+}
+
+// Kept links to the compacted region in order (when they fit); le_key[k] :=
+// kept links of the window before k, for the offsets.
+__global__ void __launch_bounds__(kGT) k_gp_write(const LaneDesc* __restrict__ lanes, GridLane* gl, int t0,
+                                                  int t, uint32_t lb_key) {
   __shared__ GScratch s;
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
-  if (G.stop || !G.hist_ok || !G.pok) return;
-  const uint64_t base = G.pbase, end = G.pend;
+  if (!G.pr.go) return;
+  const uint64_t base = L.link_off[t0], end = L.link_end[t];
+  const uint64_t k0 = G.pr.kend, nk = G.pr.part[kGB];
+  const bool fits = !G.pr.ovf && k0 + nk <= L.link_cap;
   uint64_t blo, bhi;
   chunk(end - base, blockIdx.x, &blo, &bhi);
-  unsigned long long run = G.part[3][blockIdx.x];
+  unsigned long long run = G.pr.part[blockIdx.x];
   for (uint64_t b0 = base + blo; b0 < base + bhi; b0 += kGT) {
     const uint64_t k = b0 + threadIdx.x;
-    bool on = false;
-    if (k < base + bhi) {
-      const uint32_t le = L.le_key[k];
-      on = le <= lb_key && le < kInfKey;
-    }
+    const bool on = k < base + bhi && gp_kept(L, k, lb_key);
     unsigned long long tile;
     const unsigned long long ex = run + gexcl64(on ? 1ull : 0ull, s, &tile);
     run += tile;
     if (k >= base + bhi) continue;
     L.le_key[k] = (uint32_t)ex;
-    if (on) {
-      L.links[end + ex] = L.links[k];
-      L.link_lvl[end + ex] = L.link_lvl[k];
+    if (on && fits) {
+      L.links[k0 + ex] = L.links[k];
+      L.link_lvl[k0 + ex] = L.link_lvl[k];
     }
   }
 }
 
-// New frame offsets of the window and the new end of the store.
+// The window's frame offsets in the compacted region, and its new end.
 __global__ void __launch_bounds__(kGT) k_gp_fix(const LaneDesc* __restrict__ lanes, GridLane* gl, int t0, int t) {
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
-  if (G.stop || !G.hist_ok || !G.pok) return;
-  const uint64_t base = G.pbase, end = G.pend, nk = G.part[3][kGB];
-  for (int f = t0 + (int)threadIdx.x; f <= t + 1; f += kGT) {
-    const uint64_t o = L.link_off[f];
-    L.link_off[f] = base + (o < end ? L.le_key[o] : nk);
-    if (f <= t) {
-      const uint64_t x = L.link_xoff[f];
-      L.link_xoff[f] = base + (x < end ? L.le_key[x] : nk);
-    }
+  if (!G.pr.go) return;
+  const uint64_t end = L.link_end[t], k0 = G.pr.kend, nk = G.pr.part[kGB];
+  __syncthreads();  // every thread has read link_end[t] before it moves
+  auto moved = [&](uint64_t o) -> uint64_t { return k0 + (o < end ? (uint64_t)L.le_key[o] : nk); };
+  for (int f = t0 + (int)threadIdx.x; f <= t; f += kGT) {
+    L.link_off[f] = moved(L.link_off[f]);
+    L.link_xoff[f] = moved(L.link_xoff[f]);
+    L.link_end[f] = moved(L.link_end[f]);
   }
-  if (threadIdx.x == 0) G.link_base = base + nk;
+  if (threadIdx.x == 0) {
+    if (k0 + nk > L.link_cap) G.pr.ovf = 1;
+    G.pr.kend = k0 + nk;
+  }
 }
 
-__global__ void __launch_bounds__(kGT) k_gp_move(const LaneDesc* __restrict__ lanes, const GridLane* gl) {
+// The utterance's last window (frames from t0 = T rounded down to the window
+// size, to T), behind the compacted region.  On the decoding stream, after it
+// has waited for the pruning stream.
+__device__ __forceinline__ bool gather_range(const LaneDesc& L, const GridLane& G, int* t0, uint64_t* src,
+                                             uint64_t* n) {
+  if (!L.win_cap || G.status != 0 || !G.hist_ok) return false;
+  *t0 = (L.T / kPruneEvery) * kPruneEvery;
+  *src = L.link_off[*t0];
+  *n = L.link_end[L.T] - *src;
+  return true;
+}
+
+__global__ void __launch_bounds__(kGT) k_gp_gather(const LaneDesc* __restrict__ lanes, const GridLane* gl) {
   const LaneDesc& L = lanes[blockIdx.y];
   const GridLane& G = gl[blockIdx.y];
-  if (G.stop || !G.hist_ok || !G.pok) return;
-  const uint64_t base = G.pbase, end = G.pend, nk = G.part[3][kGB];
-  for (uint64_t i = (uint64_t)blockIdx.x * kGT + threadIdx.x; i < nk; i += (uint64_t)kGB * kGT) {
-    L.links[base + i] = L.links[end + i];
-    L.link_lvl[base + i] = L.link_lvl[end + i];
+  int t0;
+  uint64_t src, n;
+  if (!gather_range(L, G, &t0, &src, &n)) return;
+  const uint64_t k0 = G.pr.kend;
+  if (G.pr.ovf || k0 + n > L.link_cap) return;
+  for (uint64_t i = (uint64_t)blockIdx.x * kGT + threadIdx.x; i < n; i += (uint64_t)kGB * kGT) {
+    L.links[k0 + i] = L.links[src + i];
+    L.link_lvl[k0 + i] = L.link_lvl[src + i];
+  }
+}
+
+__global__ void __launch_bounds__(kGT) k_gp_gather_fix(const LaneDesc* __restrict__ lanes, GridLane* gl) {
+  const LaneDesc& L = lanes[blockIdx.y];
+  GridLane& G = gl[blockIdx.y];
+  int t0;
+  uint64_t src, n;
+  if (!gather_range(L, G, &t0, &src, &n)) return;
+  const uint64_t k0 = G.pr.kend;
+  const bool fits = !G.pr.ovf && k0 + n <= L.link_cap;
+  __syncthreads();  // every thread has read link_off[t0] before it moves
+  if (fits)
+    for (int f = t0 + (int)threadIdx.x; f <= L.T; f += kGT) {
+      L.link_off[f] = L.link_off[f] - src + k0;
+      L.link_xoff[f] = L.link_xoff[f] - src + k0;
+      L.link_end[f] = L.link_end[f] - src + k0;
+    }
+  if (threadIdx.x == 0) {
+    if (fits) L.link_off[L.T + 1] = k0 + n;
+    else G.pr.ovf = 1;
+    G.pr.kend = k0 + n;
   }
 }
 
@@ -1341,14 +1429,62 @@ __global__ void __launch_bounds__(kGT) k_gp_move(const LaneDesc* __restrict__ la
 
 size_t grid_lane_bytes() { return sizeof(GridLane); }
 
-void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, int B, const Params& prm,
-                         const uint32_t* bad, int maxT, hipStream_t st) {
+namespace {
+
+// The pruning stream of one device and the events that order it against the
+// decoding streams: ready[j % 4] after window j is decoded, done[j % 4] after
+// it is pruned.  A wait is enqueued before its event is recorded again, and
+// the mutex keeps one decode's launch sequence whole.
+struct PruneSync {
+  std::mutex m;
+  hipStream_t s = nullptr;
+  hipEvent_t ready[4] = {}, done[4] = {};
+};
+
+constexpr int kMaxDevices = 64;
+
+hipError_t prune_sync(PruneSync** out) {
+  static std::mutex create;
+  static PruneSync* per_dev[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(create);
+  if (!per_dev[dev]) {
+    PruneSync* p = new PruneSync();
+    e = hipStreamCreateWithFlags(&p->s, hipStreamNonBlocking);
+    for (int i = 0; i < 4 && e == hipSuccess; ++i) {
+      e = hipEventCreateWithFlags(&p->ready[i], hipEventDisableTiming);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&p->done[i], hipEventDisableTiming);
+    }
+    if (e != hipSuccess) return e;  // a partial set is kept out of use (and leaked)
+    per_dev[dev] = p;
+  }
+  *out = per_dev[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+wd_status launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, int B, const Params& prm,
+                              bool prune, const uint32_t* bad, int maxT, hipStream_t st) {
   GridLane* gl = (GridLane*)glv;
-  const dim3 one(1, B), all(kGB, B), blk(kGT);
-  const bool prune = !(prm.flags & (WD_FLAG_DEBUG | WD_FLAG_NO_INCREMENTAL_PRUNE));
+  const dim3 one(1, B), all(kGB, B), part(kPB, B), blk(kGT);
   const uint32_t lb_key = cost_key(prm.lattice_beam);
+  PruneSync* ps = nullptr;
+  std::unique_lock<std::mutex> lk;
+  hipError_t e = hipSuccess;
+  if (prune) {
+    if ((e = prune_sync(&ps)) != hipSuccess) return hip_check(e, "pruning stream");
+    lk = std::unique_lock<std::mutex>(ps->m);
+  }
+  int nwin = 0;  // windows handed to the pruning stream
   hipLaunchKernelGGL(k_g_init, one, blk, 0, st, lanes, gl, bad);
-  for (int t = 0; t <= maxT; ++t) {
+  for (int t = 0; t <= maxT && e == hipSuccess; ++t) {
+    // frame t starts window t / 32, whose slot held window t / 32 - 2
+    if (prune && t % kPruneEvery == 0 && t / kPruneEvery - 2 >= 0 && t / kPruneEvery - 2 < nwin)
+      e = hipStreamWaitEvent(st, ps->done[(t / kPruneEvery - 2) % 4], 0);
     hipLaunchKernelGGL(k_g_begin, one, dim3(64), 0, st, g, lanes, gl, prm, t);
     if (prm.flags & WD_FLAG_DYNAMIC_LB) hipLaunchKernelGGL(k_g_expand_dyn, all, blk, 0, st, g, lanes, gl, t);
     else hipLaunchKernelGGL(k_g_expand, all, blk, 0, st, g, lanes, gl, t);
@@ -1373,25 +1509,36 @@ void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, in
     hipLaunchKernelGGL(k_g_link_write, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_g_end, one, blk, 0, st, lanes, gl, t);
     if (prune && (t + 1) % kPruneEvery == 0 && t < maxT) {
-      const int t0 = t + 1 - kPruneEvery;
-      hipLaunchKernelGGL(k_gp_init, all, blk, 0, st, lanes, gl, t0, t);
+      const int t0 = t + 1 - kPruneEvery, j = nwin++;
+      hipStream_t q = ps->s;
+      e = hipEventRecord(ps->ready[j % 4], st);
+      if (e == hipSuccess) e = hipStreamWaitEvent(q, ps->ready[j % 4], 0);
+      if (e != hipSuccess) break;
+      hipLaunchKernelGGL(k_gp_go, one, dim3(64), 0, q, lanes, gl, t);
+      hipLaunchKernelGGL(k_gp_init, part, blk, 0, q, lanes, gl, t0, t);
       // frame f: the emitting links leaving it, then its epsilon levels; down
       // to f = t0 - 1 for the emitting links into t0 (the window's first run;
       // the extra costs this leaves on frame t0 - 1 are never read)
       for (int f = t; f >= t0 - 1 && f >= 0; --f) {
-        if (f < t) hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, f, 1, 0, 1);
+        if (f < t) hipLaunchKernelGGL(k_gs_relax, part, blk, 0, q, lanes, gl, f, 1, 0, 1);
         if (f >= t0)
           for (int l = (int)g.nlevels - 1; l >= 0; --l)
-            hipLaunchKernelGGL(k_gs_relax, all, blk, 0, st, lanes, gl, f, 0, l, 1);
+            hipLaunchKernelGGL(k_gs_relax, part, blk, 0, q, lanes, gl, f, 0, l, 1);
       }
-      hipLaunchKernelGGL(k_gp_count, all, blk, 0, st, lanes, gl, t0, lb_key);
-      hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 3, 0);
-      hipLaunchKernelGGL(k_gp_write, all, blk, 0, st, lanes, gl, lb_key);
-      hipLaunchKernelGGL(k_gp_fix, one, blk, 0, st, lanes, gl, t0, t);
-      hipLaunchKernelGGL(k_gp_move, all, blk, 0, st, lanes, gl);
+      hipLaunchKernelGGL(k_gp_count, all, blk, 0, q, lanes, gl, t0, t, lb_key);
+      hipLaunchKernelGGL(k_gp_scan, one, blk, 0, q, gl);
+      hipLaunchKernelGGL(k_gp_write, all, blk, 0, q, lanes, gl, t0, t, lb_key);
+      hipLaunchKernelGGL(k_gp_fix, one, blk, 0, q, lanes, gl, t0, t);
+      e = hipEventRecord(ps->done[j % 4], q);
     }
   }
+  if (prune && e == hipSuccess) {
+    if (nwin > 0) e = hipStreamWaitEvent(st, ps->done[(nwin - 1) % 4], 0);
+    hipLaunchKernelGGL(k_gp_gather, all, blk, 0, st, lanes, gl);
+    hipLaunchKernelGGL(k_gp_gather_fix, one, blk, 0, st, lanes, gl);
+  }
   hipLaunchKernelGGL(k_g_finish, one, dim3(64), 0, st, lanes, gl);
+  return hip_check(e, "pruning stream");
 }
 
 void launch_grid_nodes(const LaneDesc* lanes, void* glv, int B, hipStream_t st) {

@@ -28,8 +28,11 @@ void launch_forward(const DevGraph& g, const LaneDesc* lanes, int B, const Param
                     const uint32_t* bad, hipStream_t s);
 void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s);
 size_t grid_lane_bytes();
-void launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* grid, int B, const Params& prm,
-                         const uint32_t* bad, int maxT, hipStream_t s);
+// `prune`: incremental lattice pruning on the library's pruning stream of the
+// current device (ordered against `s` by events).  Fails only on a HIP error
+// of that stream or its events.
+wd_status launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* grid, int B, const Params& prm,
+                              bool prune, const uint32_t* bad, int maxT, hipStream_t s);
 void launch_grid_sweep(const DevGraph& g, const LaneDesc* lanes, void* grid, int B, int maxT, float lattice_beam,
                        hipStream_t s);
 void launch_grid_nodes(const LaneDesc* lanes, void* grid, int B, hipStream_t s);

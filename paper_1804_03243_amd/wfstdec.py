@@ -62,7 +62,8 @@ class wd_params(ctypes.Structure):
 
 class wd_caps(ctypes.Structure):
     _fields_ = [("frame_tokens", ctypes.c_int64), ("frame_arcs", ctypes.c_int64),
-                ("nodes", ctypes.c_int64), ("links", ctypes.c_int64), ("kept_links", ctypes.c_int64)]
+                ("nodes", ctypes.c_int64), ("links", ctypes.c_int64), ("kept_links", ctypes.c_int64),
+                ("window_links", ctypes.c_int64)]
 
 
 class wd_stats(ctypes.Structure):
@@ -295,7 +296,7 @@ def _params(beam, max_active, lattice_beam, debug, timing=False, mode="auto"):
 def _grow(caps: wd_caps, needed: dict) -> wd_caps:
     """Capacities for the next attempt: at least what was needed, and a fast
     geometric step (an attempt only reveals the first capacity it outgrew)."""
-    c = wd_caps(caps.frame_tokens, caps.frame_arcs, caps.nodes, caps.links, caps.kept_links)
+    c = wd_caps(*(getattr(caps, f) for f, _ in wd_caps._fields_))
     for f, _ in wd_caps._fields_:
         need = needed[f]
         if need > getattr(c, f):

@@ -58,7 +58,7 @@ def test_record_layouts():
     assert wfstdec.LINK_DTYPE.itemsize == 48
     assert wfstdec.NODE_DTYPE.itemsize == 16
     assert wfstdec.TOKEN_DTYPE.itemsize == 16
-    assert ctypes.sizeof(wfstdec.wd_stats) == 8 + 7 * 8 + 8 + 5 * 8
+    assert ctypes.sizeof(wfstdec.wd_stats) == 8 + 7 * 8 + 8 + 6 * 8  # wd_caps: 6 x int64
 
 
 def test_oracle_is_not_imported_by_the_library():

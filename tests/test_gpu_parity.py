@@ -129,6 +129,28 @@ def test_incremental_prune(wf, oracle_mod, tiny10k, beam, ma, lb, mode):
         assert r.needed["links"] < r.stats["raw_links"]
 
 
+@pytest.mark.parametrize("mode", ["chip", "chip_dyn"])
+def test_incremental_prune_batch(wf, oracle_mod, tiny10k, mode):
+    """Pruning windows of 32 frames with utterances of different lengths in
+    one batch: shorter than a window, ending on a window's last frame (that
+    window is never pruned), one frame into the next window, several windows.
+    Every lane equals the oracle and its own single decode."""
+    import torch
+    cfg, g, L, graph = tiny10k
+    lens = [0, 1, 31, 32, 33, 63, 64, 95, 120]
+    Ls = [np.ascontiguousarray(synth.tiny_loglikes(700 + i, n, cfg["P"]) * 3 - 10, dtype=np.float32)
+          for i, n in enumerate(lens)]
+    xs = [torch.from_numpy(x).to(graph.device) for x in Ls]
+    print(f"\n[gpu case] incremental prune batch lens={lens} mode={mode}", flush=True)
+    rb = wf.decode_batch(graph, xs, 10.0, 40, 6.0, mode=mode)
+    for i, x in enumerate(xs):
+        rs = wf.decode(graph, x, 10.0, 40, 6.0, mode=mode)
+        o = oracle_mod.decode(g, Ls[i], 10.0, 40, 6.0)
+        assert_same(rb[i], o)
+        assert_same(rs, o)
+        assert rb[i].stats["raw_links"] == o.stats["raw_links"]
+
+
 @pytest.mark.parametrize("mode", MODES)
 def test_determinism(wf, oracle_mod, tiny10k, mode):
     import torch
@@ -227,7 +249,7 @@ def test_capacity_retry(wf, oracle_mod, tiny10k, mode):
     import torch
     cfg, g, L, graph = tiny10k
     x = torch.from_numpy(L[:80]).to(graph.device)
-    small = wf.wd_caps(64, 64, 500, 500, 16)
+    small = wf.wd_caps(64, 64, 500, 500, 16, 40)
     print(f"\n[gpu case] capacity retry mode={mode}", flush=True)
     p = wf.wd_params(10.0, 2000, 6.0, wf._MODE_FLAGS[mode])
     ws, nbytes, used = graph.workspace(1, 80, p, small)
