@@ -218,6 +218,41 @@ wd_status wd_decode_batch(const wd_graph* g, int32_t B, const float* const* logl
                           const int32_t* T, const wd_params* p, const wd_caps* caps, void* ws,
                           size_t ws_bytes, void* stream, wd_result** out);
 
+/* ---- streaming -------------------------------------------------------- */
+
+/* Frame-synchronous decoding as the log-likelihoods arrive, e.g. chunk by
+ * chunk from an acoustic model on the same stream (the paper's closing
+ * sections name the integration of acoustic inference with decoding on the
+ * GPU as future work).  The result equals wd_decode_batch of the complete
+ * utterances, bit for bit.
+ *
+ * wd_stream_begin: B utterances of at most max_T frames each.  frames[i] is
+ * utterance i's frame store: device, max_T x P fp32 row-major, owned by the
+ * caller and valid until wd_stream_end/free returns; row t-1 holds frame t.
+ * A row must be written (on `stream`, or before) before the advance that
+ * covers it and left unchanged afterwards.  ws: as for wd_decode_batch with
+ * (B, max_T).  Chip-wide mode (see the mode flags) takes B = 1.  The decoder
+ * carries each utterance's frontier and counters in the workspace between
+ * launches.  *out receives the stream handle.
+ *
+ * wd_stream_advance: n_frames[i] >= 0 more rows of utterance i are ready;
+ * decodes them (asynchronously on `stream`: the call only enqueues work).
+ * WD_EINVAL if a count would pass max_T.  Decoding errors (invalid values,
+ * no surviving token, capacity) are reported by wd_stream_end.
+ *
+ * wd_stream_end: the utterances end after the frames received; final costs,
+ * lattice pruning and posteriors as in wd_decode_batch, whose status and
+ * out[i] rules apply.  Synchronises and frees the handle.
+ *
+ * wd_stream_free: abandons a stream (waits for its work, frees the handle). */
+typedef struct wd_stream wd_stream;
+wd_status wd_stream_begin(const wd_graph* g, int32_t B, const float* const* frames, int32_t max_T,
+                          const wd_params* p, const wd_caps* caps, void* ws, size_t ws_bytes, void* stream,
+                          wd_stream** out);
+wd_status wd_stream_advance(wd_stream* s, const int32_t* n_frames);
+wd_status wd_stream_end(wd_stream* s, wd_result** out);
+void      wd_stream_free(wd_stream* s);
+
 /* ---- results (host memory owned by the result) ------------------------ */
 
 wd_status wd_result_status(const wd_result* r);

@@ -255,67 +255,120 @@ extern "C" wd_status wd_workspace_bytes(const wd_graph* g, int32_t lanes, int32_
   return WD_OK;
 }
 
-static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* ll, const int32_t* T,
-                             const wd_params* p, const wd_caps* caps, void* ws, size_t ws_bytes,
-                             void* stream, wd_result** out) {
-  if (!g || B < 1 || !ll || !T || !out) return fail(WD_EINVAL, "decode: bad arguments");
-  for (int b = 0; b < B; ++b) out[b] = nullptr;
-  wd_status st = check_params(p);
-  if (st != WD_OK) return st;
+// One decode of B utterances from setup to results: wd_decode_batch runs it
+// in one call, a stream over several (begin, advances, end).
+struct wd_stream {
+  const wd_graph* g = nullptr;
+  int B = 0;
   int32_t max_T = 0;
-  for (int b = 0; b < B; ++b) {
-    if (T[b] < 0 || T[b] > (1 << 24)) return fail(WD_EINVAL, "decode: T out of range");
-    if (T[b] > 0 && !ll[b]) return fail(WD_EINVAL, "decode: null log-likelihoods");
-    max_T = std::max(max_T, T[b]);
+  wd_params p{};
+  Params prm{};
+  Caps c{};
+  Regions R{};
+  std::vector<LaneDesc> lanes;
+  std::vector<int32_t> T;     // frames received per utterance
+  std::vector<int32_t> next;  // first frame not yet decoded
+  hipStream_t s = nullptr;
+  bool chip = false, open = false;
+  GridRun gr;
+  hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
+
+  ~wd_stream() {
+    grid_release(&gr);
+    for (auto& e : ev)
+      if (e) (void)hipEventDestroy(e);
   }
-  if (!ws || ((uintptr_t)ws & 255u)) return fail(WD_EINVAL, "decode: workspace must be 256-byte aligned");
-  const Caps c = resolve_caps(g, max_T, p, caps);
-  std::vector<LaneDesc> lanes((size_t)B);
-  std::memset(lanes.data(), 0, sizeof(LaneDesc) * (size_t)B);
-  const Regions R = carve(g, B, max_T, c, (char*)ws, &lanes);
+};
+
+// Workspace layout, resets, the per-utterance state of the chosen mode.
+static wd_status run_setup(wd_stream* run, const wd_graph* g, int32_t B, const float* const* ll, const int32_t* T,
+                           int32_t max_T, const wd_params* p, const wd_caps* caps, void* ws, size_t ws_bytes,
+                           void* stream, bool open) {
+  run->g = g;
+  run->B = B;
+  run->max_T = max_T;
+  run->p = *p;
+  run->prm = Params{p->beam, p->max_active, p->lattice_beam, p->flags};
+  run->c = resolve_caps(g, max_T, p, caps);
+  run->lanes.assign((size_t)B, LaneDesc{});
+  std::memset(run->lanes.data(), 0, sizeof(LaneDesc) * (size_t)B);
+  run->R = carve(g, B, max_T, run->c, (char*)ws, &run->lanes);
+  const Regions& R = run->R;
   if (ws_bytes < R.total)
     return fail(WD_EINVAL, "decode: workspace of " + std::to_string(ws_bytes) + " bytes, need " +
                                std::to_string(R.total));
+  run->T.assign(T, T + B);
+  run->next.assign((size_t)B, 0);
+  run->open = open;
   for (int b = 0; b < B; ++b) {
-    lanes[b].ll = ll[b];
-    lanes[b].T = T[b];
+    run->lanes[b].ll = ll[b];
+    run->lanes[b].T = T[b];
+    run->lanes[b].t0 = 0;
+    run->lanes[b].open = open ? 1 : 0;
   }
-  hipStream_t s = (hipStream_t)stream;
-  const Params prm{p->beam, p->max_active, p->lattice_beam, p->flags};
-  const uint64_t S = (uint64_t)g->S;
-  if ((st = hip_check(hipMemcpyAsync(R.desc, lanes.data(), sizeof(LaneDesc) * B, hipMemcpyHostToDevice, s),
+  run->s = (hipStream_t)stream;
+  hipStream_t s = run->s;
+  wd_status st;
+  if ((st = hip_check(hipMemcpyAsync(R.desc, run->lanes.data(), sizeof(LaneDesc) * B, hipMemcpyHostToDevice, s),
                       "lane upload")))
     return st;
+  const uint64_t S = (uint64_t)g->S;
   launch_fill_u32((uint32_t*)R.info, (uint64_t)B * sizeof(LaneInfo) / 4, 0u, s);
   launch_fill_u32(R.bad, (uint64_t)B, 0u, s);
   launch_fill_u64(R.slot, (uint64_t)B * S, kEmpty, s);
   launch_fill_u32(R.bitmap, (uint64_t)B * R.bitmap_words, 0u, s);
   launch_fill_u32(R.used, (uint64_t)B * R.used_words, 0u, s);
-  launch_check_loglikes(R.desc, B, g->P, R.bad, s);
-  const bool timing = (p->flags & WD_FLAG_TIMING) != 0;
-  hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
-  if (timing)
-    for (auto& e : ev)
+  if (p->flags & WD_FLAG_TIMING)
+    for (auto& e : run->ev)
       if ((st = hip_check(hipEventCreate(&e), "event"))) return st;
-  const bool chip_wide = chip_wide_mode(p);
-  if (timing) (void)hipEventRecord(ev[0], s);
-  if (chip_wide) {
-    if ((st = launch_grid_forward(g->dg, R.desc, R.grid, B, prm, incremental_prune(p), R.bad, max_T, s)))
-      return st;
+  if (run->ev[0]) (void)hipEventRecord(run->ev[0], s);
+  run->chip = chip_wide_mode(p);
+  if (run->chip) return grid_begin(&run->gr, R.desc, R.grid, B, incremental_prune(p), R.bad, s);
+  return WD_OK;
+}
+
+// Decodes every received frame not decoded yet (frame 0 in the first call).
+static wd_status run_frames(wd_stream* run, bool update) {
+  const Regions& R = run->R;
+  hipStream_t s = run->s;
+  const int B = run->B;
+  if (update) launch_set_frames(R.desc, B, run->T.data(), run->next.data(), run->open ? 1 : 0, s);
+  launch_check_loglikes(R.desc, B, run->g->P, R.bad, s);
+  wd_status st = WD_OK;
+  if (run->chip) {
+    int lo = run->max_T + 1, hi = -1;
+    for (int b = 0; b < B; ++b) {
+      lo = std::min(lo, run->next[b]);
+      hi = std::max(hi, run->T[b]);
+    }
+    st = grid_frames(&run->gr, run->g->dg, R.desc, R.grid, B, run->prm, R.bad, lo, hi, s);
   } else {
-    launch_forward(g->dg, R.desc, B, prm, R.bad, s);
+    launch_forward(run->g->dg, R.desc, B, run->prm, R.bad, s);
   }
-  if (timing) (void)hipEventRecord(ev[1], s);
-  if (chip_wide) {
-    launch_grid_sweep(g->dg, R.desc, R.grid, B, max_T, p->lattice_beam, s);
-    Params lp = prm;
+  for (int b = 0; b < B; ++b) run->next[b] = run->T[b] + 1;
+  if (st == WD_OK) st = hip_check(hipGetLastError(), "launch");
+  return st;
+}
+
+// Lattice pass, then the results of every utterance (synchronises).
+static wd_status run_finish(wd_stream* run, wd_result** out) {
+  const Regions& R = run->R;
+  hipStream_t s = run->s;
+  const int B = run->B;
+  const wd_params* p = &run->p;
+  wd_status st;
+  if (run->chip && (st = grid_end(&run->gr, R.desc, R.grid, B, s))) return st;
+  if (run->ev[1]) (void)hipEventRecord(run->ev[1], s);
+  if (run->chip) {
+    launch_grid_sweep(run->g->dg, R.desc, R.grid, B, run->max_T, p->lattice_beam, s);
+    Params lp = run->prm;
     lp.flags |= kFlagSwept;
-    launch_lattice(g->dg, R.desc, B, lp, s);
+    launch_lattice(run->g->dg, R.desc, B, lp, s);
     launch_grid_nodes(R.desc, R.grid, B, s);
   } else {
-    launch_lattice(g->dg, R.desc, B, prm, s);
+    launch_lattice(run->g->dg, R.desc, B, run->prm, s);
   }
-  if (timing) (void)hipEventRecord(ev[2], s);
+  if (run->ev[2]) (void)hipEventRecord(run->ev[2], s);
   if ((st = hip_check(hipGetLastError(), "launch"))) return st;
   std::vector<LaneInfo> info((size_t)B);
   if ((st = hip_check(hipMemcpyAsync(info.data(), R.info, sizeof(LaneInfo) * B, hipMemcpyDeviceToHost, s),
@@ -324,16 +377,16 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
     return st;
 
   float fwd_ms = 0.0f, lat_ms = 0.0f;
-  if (timing) {
-    (void)hipEventElapsedTime(&fwd_ms, ev[0], ev[1]);
-    (void)hipEventElapsedTime(&lat_ms, ev[1], ev[2]);
-    for (auto& e : ev) (void)hipEventDestroy(e);
+  if (run->ev[0]) {
+    (void)hipEventElapsedTime(&fwd_ms, run->ev[0], run->ev[1]);
+    (void)hipEventElapsedTime(&lat_ms, run->ev[1], run->ev[2]);
   }
   wd_status first_bad = WD_OK;
   const bool debug = (p->flags & WD_FLAG_DEBUG) != 0;
   for (int b = 0; b < B; ++b) {
     const LaneInfo& I = info[b];
-    const LaneDesc& L = lanes[b];
+    const LaneDesc& L = run->lanes[b];
+    const int32_t Tb = run->T[b];
     const wd_status ls = (I.status == 0 && I.tb_fail) ? WD_EDEVICE : (wd_status)I.status;
     if (ls != WD_OK && first_bad == WD_OK) first_bad = ls;
     if (ls != WD_OK && ls != WD_ECAPACITY) continue;
@@ -341,7 +394,7 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
     r->status = ls;
     r->cost = I.best_cost;
     wd_stats& stt = r->stats;
-    stt.frames = T[b];
+    stt.frames = Tb;
     stt.final_reached = I.final_used;
     stt.arcs_expanded = (int64_t)I.arcs_expanded;
     stt.tokens = (int64_t)I.tokens;
@@ -375,21 +428,21 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
       const uint64_t nn = I.tokens;
       std::vector<uint32_t> ns(nn);
       std::vector<unsigned long long> np(nn);
-      std::vector<uint64_t> noff((size_t)T[b] + 2);
+      std::vector<uint64_t> noff((size_t)Tb + 2);
       r->raw.resize(I.out_raw);
-      r->best.resize((size_t)T[b] + 1);
-      r->cutb.resize((size_t)T[b] + 1);
-      r->cut.resize((size_t)T[b] + 1);
+      r->best.resize((size_t)Tb + 1);
+      r->cutb.resize((size_t)Tb + 1);
+      r->cut.resize((size_t)Tb + 1);
       if ((st = d2h(ns.data(), L.n_state, 4 * nn)) || (st = d2h(np.data(), L.n_pack, 8 * nn)) ||
-          (st = d2h(noff.data(), L.node_off, 8 * ((uint64_t)T[b] + 2))) ||
+          (st = d2h(noff.data(), L.node_off, 8 * ((uint64_t)Tb + 2))) ||
           (st = d2h(r->raw.data(), L.out_raw, sizeof(OutLink) * I.out_raw)) ||
-          (st = d2h(r->best.data(), L.best, 4 * ((uint64_t)T[b] + 1))) ||
-          (st = d2h(r->cutb.data(), L.cutb, 4 * ((uint64_t)T[b] + 1))) ||
-          (st = d2h(r->cut.data(), L.cut, 4 * ((uint64_t)T[b] + 1))) ||
+          (st = d2h(r->best.data(), L.best, 4 * ((uint64_t)Tb + 1))) ||
+          (st = d2h(r->cutb.data(), L.cutb, 4 * ((uint64_t)Tb + 1))) ||
+          (st = d2h(r->cut.data(), L.cut, 4 * ((uint64_t)Tb + 1))) ||
           (st = hip_check(hipStreamSynchronize(s), "debug download")))
         return st;
       r->tokens.resize(nn);
-      for (int t = 0; t <= T[b]; ++t)
+      for (int t = 0; t <= Tb; ++t)
         for (uint64_t n = noff[t]; n < noff[t + 1]; ++n)
           r->tokens[n] = wd_token{t, (int32_t)ns[n], key_cost((uint32_t)(np[n] >> 32)), (uint32_t)np[n]};
     }
@@ -406,6 +459,35 @@ static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* l
   return first_bad;
 }
 
+static wd_status check_lanes(const wd_graph* g, int32_t B, const float* const* ll, const int32_t* T,
+                             wd_result** out) {
+  if (!g || B < 1 || !ll || !T || !out) return fail(WD_EINVAL, "decode: bad arguments");
+  for (int b = 0; b < B; ++b) out[b] = nullptr;
+  for (int b = 0; b < B; ++b) {
+    if (T[b] < 0 || T[b] > (1 << 24)) return fail(WD_EINVAL, "decode: T out of range");
+    if (T[b] > 0 && !ll[b]) return fail(WD_EINVAL, "decode: null log-likelihoods");
+  }
+  return WD_OK;
+}
+
+static wd_status decode_impl(const wd_graph* g, int32_t B, const float* const* ll, const int32_t* T,
+                             const wd_params* p, const wd_caps* caps, void* ws, size_t ws_bytes,
+                             void* stream, wd_result** out) {
+  wd_status st = check_lanes(g, B, ll, T, out);
+  if (st != WD_OK) return st;
+  if ((st = check_params(p)) != WD_OK) return st;
+  int32_t max_T = 0;
+  for (int b = 0; b < B; ++b) max_T = std::max(max_T, T[b]);
+  if (!ws || ((uintptr_t)ws & 255u)) return fail(WD_EINVAL, "decode: workspace must be 256-byte aligned");
+  wd_stream run;
+  if ((st = run_setup(&run, g, B, ll, T, max_T, p, caps, ws, ws_bytes, stream, false)) ||
+      (st = run_frames(&run, false))) {
+    (void)hipStreamSynchronize(run.s);
+    return st;
+  }
+  return run_finish(&run, out);
+}
+
 extern "C" wd_status wd_decode(const wd_graph* g, const float* loglikes, int32_t T, const wd_params* p,
                                const wd_caps* caps, void* ws, size_t ws_bytes, void* stream, wd_result** out) {
   return decode_impl(g, 1, &loglikes, &T, p, caps, ws, ws_bytes, stream, out);
@@ -415,6 +497,56 @@ extern "C" wd_status wd_decode_batch(const wd_graph* g, int32_t B, const float* 
                                      const wd_params* p, const wd_caps* caps, void* ws, size_t ws_bytes,
                                      void* stream, wd_result** out) {
   return decode_impl(g, B, loglikes, T, p, caps, ws, ws_bytes, stream, out);
+}
+
+extern "C" wd_status wd_stream_begin(const wd_graph* g, int32_t B, const float* const* frames, int32_t max_T,
+                                     const wd_params* p, const wd_caps* caps, void* ws, size_t ws_bytes,
+                                     void* stream, wd_stream** out) {
+  if (!out) return fail(WD_EINVAL, "stream_begin: null output");
+  *out = nullptr;
+  if (!g || B < 1 || !frames || max_T < 0 || max_T > (1 << 24))
+    return fail(WD_EINVAL, "stream_begin: bad arguments");
+  for (int b = 0; b < B; ++b)
+    if (max_T > 0 && !frames[b]) return fail(WD_EINVAL, "stream_begin: null frame store");
+  wd_status st = check_params(p);
+  if (st != WD_OK) return st;
+  if (chip_wide_mode(p) && B != 1) return fail(WD_EINVAL, "stream_begin: chip-wide streams hold one utterance");
+  if (!ws || ((uintptr_t)ws & 255u)) return fail(WD_EINVAL, "stream_begin: workspace must be 256-byte aligned");
+  wd_stream* run = new wd_stream();
+  std::vector<int32_t> zero((size_t)B, 0);
+  if ((st = run_setup(run, g, B, frames, zero.data(), max_T, p, caps, ws, ws_bytes, stream, true))) {
+    (void)hipStreamSynchronize((hipStream_t)stream);
+    delete run;
+    return st;
+  }
+  *out = run;
+  return WD_OK;
+}
+
+extern "C" wd_status wd_stream_advance(wd_stream* run, const int32_t* n_frames) {
+  if (!run || !n_frames) return fail(WD_EINVAL, "stream_advance: bad arguments");
+  for (int b = 0; b < run->B; ++b)
+    if (n_frames[b] < 0 || (int64_t)run->T[b] + n_frames[b] > run->max_T)
+      return fail(WD_EINVAL, "stream_advance: frame count beyond max_T");
+  for (int b = 0; b < run->B; ++b) run->T[b] += n_frames[b];
+  return run_frames(run, true);
+}
+
+extern "C" wd_status wd_stream_end(wd_stream* run, wd_result** out) {
+  if (!run || !out) return fail(WD_EINVAL, "stream_end: bad arguments");
+  for (int b = 0; b < run->B; ++b) out[b] = nullptr;
+  run->open = false;
+  wd_status st = run_frames(run, true);
+  if (st == WD_OK) st = run_finish(run, out);
+  (void)hipStreamSynchronize(run->s);  // nothing of the stream's may run after it is freed
+  delete run;
+  return st;
+}
+
+extern "C" void wd_stream_free(wd_stream* run) {
+  if (!run) return;
+  (void)hipStreamSynchronize(run->s);
+  delete run;
 }
 
 extern "C" wd_status wd_result_status(const wd_result* r) { return r->status; }

@@ -103,6 +103,8 @@ struct LaneInfo {
   uint32_t best_node;
   float best_cost;
   uint32_t tb_fail;            // traceback met an inconsistent predecessor
+  uint32_t last_tokens;        // surviving tokens of the last decoded frame
+  uint32_t pad0;
   double Z;                    // total cost of the kept lattice (-log of its path sum)
 };
 
@@ -138,8 +140,10 @@ struct OutNode {
 // Everything one utterance needs on the device.  Built on the host; lives in
 // the workspace.
 struct LaneDesc {
-  const float* ll;             // T x P log-likelihoods
-  int32_t T;
+  const float* ll;             // T x P log-likelihoods (row t-1 belongs to frame t)
+  int32_t T;                   // last frame (streaming: the last frame received so far)
+  int32_t t0;                  // first frame this launch decodes; > 0 resumes a stream
+  int32_t open;                // streaming: more frames may follow
   int32_t pad0;
   uint64_t frame_cap, cand_cap, node_cap, link_cap, kept_cap, word_cap;
   uint64_t win_cap;            // incremental pruning: links of one raw window slot (0: off)

@@ -190,6 +190,11 @@ __device__ __forceinline__ void select_bin(uint32_t rank, FwdShared& sh, uint32_
   __syncthreads();
 }
 
+__device__ __forceinline__ uint64_t uniform64(uint64_t v) {
+  return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
+         (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+}
+
 __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc* __restrict__ lanes,
                                                       Params prm, const uint32_t* __restrict__ bad) {
   __shared__ FwdShared sh;
@@ -228,9 +233,37 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
   }
   bool hist_ok = true;  // history (nodes, links) still being stored
   uint32_t par = 0;     // scratch buffer parity of the workgroup collectives
-  int t = 0;
+  int t = L.t0;
+  if (t > 0) {
+    // a stream resumes after frame t - 1: the state the last launch left in
+    // LaneInfo, the frontier in the workspace.  A full node or link store
+    // goes on (the decode still measures what it needs); a frame that
+    // outgrew the per-frame capacities stopped mid-frame and stays stopped.
+    // The values are the same in every lane; saying so keeps them out of
+    // vector registers.
+    const LaneInfo& I = *L.info;
+    const bool go_on = I.status == 4 && (I.overflow & (kOvfFrame | kOvfArcs)) == 0;
+    status = __builtin_amdgcn_readfirstlane(go_on ? 0 : I.status);
+    if (status != 0) return;
+    ovf = __builtin_amdgcn_readfirstlane(I.overflow);
+    hist_ok = (ovf & (kOvfNodes | kOvfLinks)) == 0;
+    node_base = uniform64(I.tokens);
+    n_prev = __builtin_amdgcn_readfirstlane(I.last_tokens);
+    node_base_prev = node_base - n_prev;
+    link_base = uniform64(I.links);
+    W = __builtin_amdgcn_readfirstlane(L.f_edeg[n_prev]);
+    front_lds = false;
+    my_eps = tid == 0 ? I.eps_arcs : 0;
+    if (tid == 0) {
+      sh.c_arcs = I.arcs_expanded - I.eps_arcs;
+      sh.c_tokens = I.tokens;
+      sh.c_max_tokens = I.max_tokens;
+      sh.c_need_frame = I.need_frame_tokens;
+      sh.c_need_arcs = I.need_frame_arcs;
+    }
+  }
 
-  for (t = 0; t <= T; ++t) {
+  for (; t <= T; ++t) {
     if (t > 0) {
       if (tid == 0 && W > sh.c_need_arcs) sh.c_need_arcs = W;
       if (W > L.cand_cap) {
@@ -806,6 +839,19 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     __syncthreads();
   }
 
+  if (L.open && front_lds) {  // an open stream resumes from the workspace frontier
+    for (uint32_t i = tid; i <= n_prev; i += kThreads) {
+      L.f_edeg[i] = sh.f_edeg[i];
+      L.f_xdeg[i] = sh.f_xdeg[i];
+      if (i == n_prev) continue;
+      L.f_state[i] = sh.f_state[i];
+      L.f_key[i] = sh.f_key[i];
+      L.f_arc[i] = sh.f_arc[i];
+      L.f_ebeg[i] = sh.f_ebeg[i];
+      L.f_xbeg[i] = sh.f_xbeg[i];
+      L.f_cls[i] = sh.f_cls[i];
+    }
+  }
   const uint64_t eps = block_sum64(my_eps, sh.bs, par);
   const uint64_t arcs = sh.c_arcs + eps;  // thread 0's own write; read by thread 0 below
   if (tid == 0) {
@@ -822,14 +868,17 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     info->need_links = link_base;
     info->need_frame_tokens = sh.c_need_frame;
     info->need_frame_arcs = sh.c_need_arcs;
+    info->last_tokens = n_prev;
   }
 }
 
 // Log-likelihood check: NaN, +inf and values above 1e30 are rejected.
+// Rows of the frames this launch decodes, t0..T (frame t reads row t - 1).
 __global__ void k_check_loglikes(const LaneDesc* __restrict__ lanes, uint32_t P, uint32_t* bad) {
   const LaneDesc L = lanes[blockIdx.y];
   const uint64_t n = (uint64_t)L.T * P;
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+  const uint64_t r0 = (uint64_t)(L.t0 > 0 ? L.t0 - 1 : 0) * P;
+  for (uint64_t i = r0 + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (uint64_t)gridDim.x * blockDim.x) {
     const float v = L.ll[i];
     if (v != v || v > 1e30f) {
@@ -849,6 +898,36 @@ __global__ void k_fill_u32(uint32_t* p, uint64_t n, uint32_t v) {
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (uint64_t)gridDim.x * blockDim.x)
     p[i] = v;
+}
+
+constexpr int kSetLanes = 128;
+struct FrameSet {
+  int32_t T[kSetLanes];
+  int32_t t0[kSetLanes];
+  int32_t b0, n, open;
+};
+
+__global__ void k_set_frames(LaneDesc* lanes, FrameSet f) {
+  for (int i = (int)threadIdx.x; i < f.n; i += (int)blockDim.x) {
+    LaneDesc& L = lanes[f.b0 + i];
+    L.T = f.T[i];
+    L.t0 = f.t0[i];
+    L.open = f.open;
+  }
+}
+
+void launch_set_frames(LaneDesc* lanes, int B, const int32_t* T, const int32_t* t0, int32_t open, hipStream_t s) {
+  for (int b0 = 0; b0 < B; b0 += kSetLanes) {
+    FrameSet f{};
+    f.b0 = b0;
+    f.n = B - b0 < kSetLanes ? B - b0 : kSetLanes;
+    f.open = open;
+    for (int i = 0; i < f.n; ++i) {
+      f.T[i] = T[b0 + i];
+      f.t0[i] = t0[b0 + i];
+    }
+    hipLaunchKernelGGL(k_set_frames, dim3(1), dim3(kSetLanes), 0, s, lanes, f);
+  }
 }
 
 void launch_forward(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm,

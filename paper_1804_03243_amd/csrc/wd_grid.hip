@@ -39,6 +39,8 @@ struct PruneLane {
   uint64_t kend;      // links in the compacted region (still counted after an overflow)
   uint32_t go;        // the current window is pruned
   uint32_t ovf;       // the compacted region overflowed
+  uint32_t next;      // first frame not yet pruned
+  uint32_t pad0;
   unsigned long long part[kGB + 1];  // kept links per workgroup, then their prefix
 };
 
@@ -990,7 +992,7 @@ __global__ void __launch_bounds__(kGT) k_g_end(const LaneDesc* __restrict__ lane
   G.n_surv = 0;
   G.xmask = 0;
   G.frames = (uint32_t)t + 1u;
-  if (t == L.T) G.stop = 1;
+  if (t == L.T && !L.open) G.stop = 1;
 }
 
 // Final counters into the utterance's LaneInfo.
@@ -1272,16 +1274,19 @@ __global__ void __launch_bounds__(kGT) k_gn_write(const LaneDesc* __restrict__ l
 // its out-links, reached by a link within the beam whenever it matters.  The
 // other links are appended, in order, to the compacted region [0, link_cap),
 // and the window's frame offsets move with them.  Decoding waits for window
-// j's pruning only before frame 32 (j + 2) reuses its slot.  The last window
-// of an utterance is never pruned (the final sweep follows): the gather moves
-// it behind the compacted region, which then holds every frame in order, as
-// the link store does without incremental pruning.
+// j's pruning only before frame 32 (j + 2) reuses its slot.  At the end, the
+// frames after the last complete window are gathered behind the compacted
+// region, which then holds every frame in order, as the link store does
+// without incremental pruning.  (A window that ends on the last frame is
+// pruned too: the bound holds whether or not frames follow, so a stream can
+// prune each window as soon as it is complete.)
 //
 // Decoding and pruning touch disjoint data while they overlap: the window's
 // links, link offsets, extra costs and le_key belong to the pruning stream;
 // node offsets and costs of the window are final and only read.  The gate
-// `go` is taken once per window from the decoding state (status and
-// hist_ok only ever change to a failure, whose result is not returned).
+// `go` is taken once per window from the decoding state: the window's frames
+// are decoded (frames only grows), and status and hist_ok still say OK (they
+// only ever change to a failure, whose result is not returned).
 
 __global__ void k_gp_go(const LaneDesc* __restrict__ lanes, GridLane* gl, int t) {
   const LaneDesc& L = lanes[blockIdx.y];
@@ -1289,7 +1294,8 @@ __global__ void k_gp_go(const LaneDesc* __restrict__ lanes, GridLane* gl, int t)
   if (threadIdx.x != 0) return;
   const int32_t status = __hip_atomic_load(&G.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const uint32_t ok = __hip_atomic_load(&G.hist_ok, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  G.pr.go = (t < L.T && status == 0 && ok) ? 1u : 0u;
+  const uint32_t done = __hip_atomic_load(&G.frames, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  G.pr.go = ((uint32_t)t < done && status == 0 && ok) ? 1u : 0u;
 }
 
 __global__ void __launch_bounds__(kGT) k_gp_init(const LaneDesc* __restrict__ lanes, const GridLane* gl,
@@ -1374,18 +1380,19 @@ __global__ void __launch_bounds__(kGT) k_gp_fix(const LaneDesc* __restrict__ lan
   if (threadIdx.x == 0) {
     if (k0 + nk > L.link_cap) G.pr.ovf = 1;
     G.pr.kend = k0 + nk;
+    G.pr.next = (uint32_t)t + 1u;
   }
 }
 
-// The utterance's last window (frames from t0 = T rounded down to the window
-// size, to T), behind the compacted region.  On the decoding stream, after it
-// has waited for the pruning stream.
+// The frames after the last pruned window (t0 .. T, all in one slot; none
+// when the last window ended at T), behind the compacted region.  On the
+// decoding stream, after it has waited for the pruning stream.
 __device__ __forceinline__ bool gather_range(const LaneDesc& L, const GridLane& G, int* t0, uint64_t* src,
                                              uint64_t* n) {
   if (!L.win_cap || G.status != 0 || !G.hist_ok) return false;
-  *t0 = (L.T / kPruneEvery) * kPruneEvery;
-  *src = L.link_off[*t0];
-  *n = L.link_end[L.T] - *src;
+  *t0 = (int)G.pr.next;
+  *src = *t0 <= L.T ? L.link_off[*t0] : 0;
+  *n = *t0 <= L.T ? L.link_end[L.T] - *src : 0;
   return true;
 }
 
@@ -1429,37 +1436,31 @@ __global__ void __launch_bounds__(kGT) k_gp_gather_fix(const LaneDesc* __restric
 
 size_t grid_lane_bytes() { return sizeof(GridLane); }
 
+// Decoding-state update for a stream's utterances: a workgroup per lane.
+__global__ void k_g_bad(const LaneDesc* __restrict__ lanes, GridLane* gl, const uint32_t* __restrict__ bad) {
+  GridLane& G = gl[blockIdx.y];
+  if (threadIdx.x != 0 || !bad[blockIdx.y] || G.status != 0) return;
+  G.status = 1;  // WD_EINVAL
+  G.stop = 1;
+  lanes[blockIdx.y].info->status = 1;
+}
+
 namespace {
 
-// The pruning stream of one device and the events that order it against the
-// decoding streams: ready[j % 4] after window j is decoded, done[j % 4] after
-// it is pruned.  A wait is enqueued before its event is recorded again, and
-// the mutex keeps one decode's launch sequence whole.
-struct PruneSync {
-  std::mutex m;
-  hipStream_t s = nullptr;
-  hipEvent_t ready[4] = {}, done[4] = {};
-};
-
-constexpr int kMaxDevices = 64;
-
-hipError_t prune_sync(PruneSync** out) {
+// The library's pruning stream of each device (default priority, never
+// blocking on the null stream).
+hipError_t prune_stream(hipStream_t* out) {
   static std::mutex create;
-  static PruneSync* per_dev[kMaxDevices] = {};
+  static hipStream_t per_dev[64] = {};
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
   std::lock_guard<std::mutex> lk(create);
   if (!per_dev[dev]) {
-    PruneSync* p = new PruneSync();
-    e = hipStreamCreateWithFlags(&p->s, hipStreamNonBlocking);
-    for (int i = 0; i < 4 && e == hipSuccess; ++i) {
-      e = hipEventCreateWithFlags(&p->ready[i], hipEventDisableTiming);
-      if (e == hipSuccess) e = hipEventCreateWithFlags(&p->done[i], hipEventDisableTiming);
-    }
-    if (e != hipSuccess) return e;  // a partial set is kept out of use (and leaked)
-    per_dev[dev] = p;
+    hipStream_t q = nullptr;
+    if ((e = hipStreamCreateWithFlags(&q, hipStreamNonBlocking)) != hipSuccess) return e;
+    per_dev[dev] = q;
   }
   *out = per_dev[dev];
   return hipSuccess;
@@ -1467,24 +1468,50 @@ hipError_t prune_sync(PruneSync** out) {
 
 }  // namespace
 
-wd_status launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* glv, int B, const Params& prm,
-                              bool prune, const uint32_t* bad, int maxT, hipStream_t st) {
+void grid_release(GridRun* run) {
+  // a run that did not reach grid_end may still have windows being pruned
+  if (run->q && !run->ended && run->nwin > 0) (void)hipStreamSynchronize(run->q);
+  for (int i = 0; i < 4; ++i) {
+    if (run->ready[i]) (void)hipEventDestroy(run->ready[i]);
+    if (run->done[i]) (void)hipEventDestroy(run->done[i]);
+    run->ready[i] = run->done[i] = nullptr;
+  }
+  run->q = nullptr;
+}
+
+wd_status grid_begin(GridRun* run, const LaneDesc* lanes, void* glv, int B, bool prune, const uint32_t* bad,
+                     hipStream_t st) {
+  *run = GridRun{};
+  if (prune) {
+    hipError_t e = prune_stream(&run->q);
+    for (int i = 0; i < 4 && e == hipSuccess; ++i) {
+      e = hipEventCreateWithFlags(&run->ready[i], hipEventDisableTiming);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&run->done[i], hipEventDisableTiming);
+    }
+    if (e != hipSuccess) {
+      grid_release(run);
+      return hip_check(e, "pruning stream");
+    }
+  }
+  hipLaunchKernelGGL(k_g_init, dim3(1, B), dim3(kGT), 0, st, lanes, (GridLane*)glv, bad);
+  return WD_OK;
+}
+
+// Frames t_from..t_to.  Window j's links go to slot j % 2: the first frame of
+// window j waits for the pruning of window j - 2; after the last frame of a
+// window, an event hands it to the pruning stream (ready[j % 4] / done[j % 4];
+// every wait is enqueued before its event is recorded again).
+wd_status grid_frames(GridRun* run, const DevGraph& g, const LaneDesc* lanes, void* glv, int B, const Params& prm,
+                      const uint32_t* bad, int t_from, int t_to, hipStream_t st) {
   GridLane* gl = (GridLane*)glv;
   const dim3 one(1, B), all(kGB, B), part(kPB, B), blk(kGT);
   const uint32_t lb_key = cost_key(prm.lattice_beam);
-  PruneSync* ps = nullptr;
-  std::unique_lock<std::mutex> lk;
   hipError_t e = hipSuccess;
-  if (prune) {
-    if ((e = prune_sync(&ps)) != hipSuccess) return hip_check(e, "pruning stream");
-    lk = std::unique_lock<std::mutex>(ps->m);
-  }
-  int nwin = 0;  // windows handed to the pruning stream
-  hipLaunchKernelGGL(k_g_init, one, blk, 0, st, lanes, gl, bad);
-  for (int t = 0; t <= maxT && e == hipSuccess; ++t) {
-    // frame t starts window t / 32, whose slot held window t / 32 - 2
-    if (prune && t % kPruneEvery == 0 && t / kPruneEvery - 2 >= 0 && t / kPruneEvery - 2 < nwin)
-      e = hipStreamWaitEvent(st, ps->done[(t / kPruneEvery - 2) % 4], 0);
+  hipLaunchKernelGGL(k_g_bad, one, dim3(64), 0, st, lanes, gl, bad);
+  for (int t = t_from; t <= t_to && e == hipSuccess; ++t) {
+    const int reuse = t / kPruneEvery - 2;
+    if (run->q && t % kPruneEvery == 0 && reuse >= 0 && reuse < run->nwin)
+      e = hipStreamWaitEvent(st, run->done[reuse % 4], 0);
     hipLaunchKernelGGL(k_g_begin, one, dim3(64), 0, st, g, lanes, gl, prm, t);
     if (prm.flags & WD_FLAG_DYNAMIC_LB) hipLaunchKernelGGL(k_g_expand_dyn, all, blk, 0, st, g, lanes, gl, t);
     else hipLaunchKernelGGL(k_g_expand, all, blk, 0, st, g, lanes, gl, t);
@@ -1508,11 +1535,11 @@ wd_status launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* gl
     hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 2, 0);
     hipLaunchKernelGGL(k_g_link_write, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_g_end, one, blk, 0, st, lanes, gl, t);
-    if (prune && (t + 1) % kPruneEvery == 0 && t < maxT) {
-      const int t0 = t + 1 - kPruneEvery, j = nwin++;
-      hipStream_t q = ps->s;
-      e = hipEventRecord(ps->ready[j % 4], st);
-      if (e == hipSuccess) e = hipStreamWaitEvent(q, ps->ready[j % 4], 0);
+    if (run->q && (t + 1) % kPruneEvery == 0) {
+      const int t0 = t + 1 - kPruneEvery, j = run->nwin++;
+      hipStream_t q = run->q;
+      e = hipEventRecord(run->ready[j % 4], st);
+      if (e == hipSuccess) e = hipStreamWaitEvent(q, run->ready[j % 4], 0);
       if (e != hipSuccess) break;
       hipLaunchKernelGGL(k_gp_go, one, dim3(64), 0, q, lanes, gl, t);
       hipLaunchKernelGGL(k_gp_init, part, blk, 0, q, lanes, gl, t0, t);
@@ -1529,15 +1556,25 @@ wd_status launch_grid_forward(const DevGraph& g, const LaneDesc* lanes, void* gl
       hipLaunchKernelGGL(k_gp_scan, one, blk, 0, q, gl);
       hipLaunchKernelGGL(k_gp_write, all, blk, 0, q, lanes, gl, t0, t, lb_key);
       hipLaunchKernelGGL(k_gp_fix, one, blk, 0, q, lanes, gl, t0, t);
-      e = hipEventRecord(ps->done[j % 4], q);
+      e = hipEventRecord(run->done[j % 4], q);
     }
   }
-  if (prune && e == hipSuccess) {
-    if (nwin > 0) e = hipStreamWaitEvent(st, ps->done[(nwin - 1) % 4], 0);
+  return hip_check(e, "pruning stream");
+}
+
+// After the last frame: wait for the pruning stream, gather the frames after
+// the last pruned window, final counters.
+wd_status grid_end(GridRun* run, const LaneDesc* lanes, void* glv, int B, hipStream_t st) {
+  GridLane* gl = (GridLane*)glv;
+  const dim3 one(1, B), all(kGB, B), blk(kGT);
+  hipError_t e = hipSuccess;
+  if (run->q) {
+    if (run->nwin > 0) e = hipStreamWaitEvent(st, run->done[(run->nwin - 1) % 4], 0);
     hipLaunchKernelGGL(k_gp_gather, all, blk, 0, st, lanes, gl);
     hipLaunchKernelGGL(k_gp_gather_fix, one, blk, 0, st, lanes, gl);
   }
   hipLaunchKernelGGL(k_g_finish, one, dim3(64), 0, st, lanes, gl);
+  run->ended = e == hipSuccess;
   return hip_check(e, "pruning stream");
 }
 

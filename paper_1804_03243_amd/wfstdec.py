@@ -76,7 +76,8 @@ class wd_stats(ctypes.Structure):
 
 
 EXPORTS = ["wd_graph_bytes", "wd_graph_load", "wd_graph_free", "wd_graph_eps_levels",
-           "wd_workspace_bytes", "wd_decode", "wd_decode_batch", "wd_result_status",
+           "wd_workspace_bytes", "wd_decode", "wd_decode_batch", "wd_stream_begin",
+           "wd_stream_advance", "wd_stream_end", "wd_stream_free", "wd_result_status",
            "wd_result_cost", "wd_result_words", "wd_result_lattice", "wd_result_nodes",
            "wd_result_tokens", "wd_result_raw_lattice", "wd_result_cutoffs", "wd_result_stats",
            "wd_result_free", "wd_last_error"]
@@ -104,6 +105,11 @@ def lib():
                            P(VP)], ctypes.c_int),
             "wd_decode_batch": ([VP, ctypes.c_int32, P(VP), P(ctypes.c_int32), P(wd_params),
                                  P(wd_caps), VP, ctypes.c_size_t, VP, P(VP)], ctypes.c_int),
+            "wd_stream_begin": ([VP, ctypes.c_int32, P(VP), ctypes.c_int32, P(wd_params), P(wd_caps),
+                                 VP, ctypes.c_size_t, VP, P(VP)], ctypes.c_int),
+            "wd_stream_advance": ([VP, P(ctypes.c_int32)], ctypes.c_int),
+            "wd_stream_end": ([VP, P(VP)], ctypes.c_int),
+            "wd_stream_free": ([VP], None),
             "wd_result_status": ([VP], ctypes.c_int),
             "wd_result_cost": ([VP], ctypes.c_float),
             "wd_result_words": ([VP, P(VP)], ctypes.c_int32),
@@ -181,6 +187,34 @@ def wd_decode_batch(handle: int, loglikes_ptrs: list[int], Ts: list[int], params
                                ctypes.byref(caps) if caps is not None else None, ws, ws_bytes, stream,
                                outs)
     return st, [o or 0 for o in outs]
+
+
+def wd_stream_begin(handle: int, frame_ptrs: list[int], max_T: int, params: wd_params,
+                    caps: wd_caps | None, ws: int, ws_bytes: int, stream: int) -> int:
+    """Returns the stream handle; raises WdError on a non-OK status."""
+    B = len(frame_ptrs)
+    ptrs = (ctypes.c_void_p * B)(*frame_ptrs)
+    h = ctypes.c_void_p()
+    _check(lib().wd_stream_begin(handle, B, ptrs, max_T, ctypes.byref(params),
+                                 ctypes.byref(caps) if caps is not None else None, ws, ws_bytes, stream,
+                                 ctypes.byref(h)))
+    return h.value
+
+
+def wd_stream_advance(sh: int, n_frames: list[int]) -> None:
+    ns = (ctypes.c_int32 * len(n_frames))(*n_frames)
+    _check(lib().wd_stream_advance(sh, ns))
+
+
+def wd_stream_end(sh: int, B: int) -> tuple[int, list[int]]:
+    """Returns (status, result handles or 0); frees the stream."""
+    outs = (ctypes.c_void_p * B)()
+    st = lib().wd_stream_end(sh, outs)
+    return st, [o or 0 for o in outs]
+
+
+def wd_stream_free(sh: int) -> None:
+    lib().wd_stream_free(sh)
 
 
 def _copy(ptr, n, dtype):
@@ -352,3 +386,81 @@ def decode(graph: Graph, loglikes, beam: float, max_active: int, lattice_beam: f
     """Decode one utterance (device float32 tensor, T x P)."""
     return decode_batch(graph, [loglikes], beam, max_active, lattice_beam, debug, caps,
                         timing=timing, mode=mode)[0]
+
+
+class Stream:
+    """Streaming decode of B utterances whose log-likelihoods arrive in chunks
+    (wd_stream_begin / wd_stream_advance / wd_stream_end).  `frames[i]` is
+    utterance i's frame store (max_T x P device tensor); `push` copies chunks
+    into it on the current stream and decodes them.  `end` returns the same
+    results as decode_batch of the complete utterances; if the workspace
+    turns out too small it decodes them again from the frame stores with the
+    capacities the stream reported (decode_batch's retry)."""
+
+    def __init__(self, graph: Graph, B: int, max_T: int, beam: float, max_active: int,
+                 lattice_beam: float, debug: bool = False, timing: bool = False, mode: str = "auto",
+                 caps: wd_caps | None = None):
+        torch = _torch()
+        self.graph, self.B, self.max_T = graph, int(B), int(max_T)
+        self.args = (beam, max_active, lattice_beam)
+        self.debug, self.timing, self.mode = debug, timing, mode
+        self.params = _params(beam, max_active, lattice_beam, debug, timing, mode)
+        self.T = [0] * self.B
+        with torch.cuda.device(graph.device):
+            self.frames = torch.empty((self.B, max(self.max_T, 1), graph.num_pdfs), dtype=torch.float32,
+                                      device=graph.device)
+            nbytes, used = wd_workspace_bytes(graph.handle, self.B, self.max_T, self.params, caps)
+            self._ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=graph.device)
+            ws = (self._ws.data_ptr() + 255) // 256 * 256
+            self.handle = wd_stream_begin(graph.handle, [self.frames[i].data_ptr() for i in range(self.B)],
+                                          self.max_T, self.params, used, ws, nbytes, _stream(torch))
+        self.caps = used
+
+    def push(self, chunks: list) -> None:
+        """chunks[i]: None or a device float32 tensor (n_i x P) of utterance
+        i's next frames."""
+        torch = _torch()
+        counts = [0] * self.B
+        with torch.cuda.device(self.graph.device):
+            for i, x in enumerate(chunks):
+                if x is None:
+                    continue
+                n = int(x.shape[0])
+                if x.dim() != 2 or x.shape[1] != self.graph.num_pdfs or x.dtype != torch.float32:
+                    raise ValueError(f"chunk {i} must be n x {self.graph.num_pdfs} float32")
+                if self.T[i] + n > self.max_T:
+                    raise ValueError(f"utterance {i} would pass max_T = {self.max_T}")
+                if n:
+                    self.frames[i, self.T[i]:self.T[i] + n].copy_(x)
+                counts[i] = n
+            wd_stream_advance(self.handle, counts)
+        for i, n in enumerate(counts):
+            self.T[i] += n
+
+    def end(self) -> list:
+        torch = _torch()
+        with torch.cuda.device(self.graph.device):
+            st, res = wd_stream_end(self.handle, self.B)
+        self.handle = None
+        outs, err = [], lib().wd_last_error().decode() if st != WD_OK else ""
+        for r in res:
+            outs.append(wd_result_read(r) if r else None)
+            if r:
+                wd_result_free(r)
+        if st == WD_ECAPACITY:
+            need = {f: max(o.needed[f] for o in outs if o is not None) for f, _ in wd_caps._fields_}
+            xs = [self.frames[i, :self.T[i]] for i in range(self.B)]
+            return decode_batch(self.graph, xs, *self.args, debug=self.debug, caps=_grow(self.caps, need),
+                                timing=self.timing, mode=self.mode)
+        if st != WD_OK:
+            raise WdError(st, err)
+        return outs
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h:
+            try:
+                wd_stream_free(h)
+            except Exception:
+                pass
+            self.handle = None
