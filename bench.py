@@ -12,8 +12,10 @@ Besides the headline line's fields: `roofline.traffic` is the HBM traffic of
 one k_forward launch measured with hardware counters (FETCH_SIZE + WRITE_SIZE,
 each scaled by what the same counter reads for a plain device copy of known
 size), reported only while the kernel sources hash to the ones the counters
-were taken on; `other_workloads` times the chip-wide mode on the wide-beam
-2M-state graph.  `--copy-kernel-bytes N` only runs a plain N-byte device copy
+were taken on; `other_workloads` times the same utterance streamed in chunks
+of 32 and 8 frames, and the chip-wide mode on the wide-beam 2M-state graph
+(with and without incremental lattice pruning, and with dynamic load
+balancing).  `--copy-kernel-bytes N` only runs a plain N-byte device copy
 (the counter calibration run) and exits.
 """
 from __future__ import annotations
@@ -105,11 +107,47 @@ def wide_chip(wfstdec, steps: int = 3, mode: str = "chip") -> dict:
            "frames_per_s": round(T / wall, 1), "ms_per_step": round(1e3 * wall, 2),
            "arcs_expanded_per_s": round(st["arcs_expanded"] / wall, 1),
            "tokens_per_frame": round(st["tokens"] / (T + 1), 1),
-           "raw_links": st["raw_links"], "kept_links": st["kept_links"], "link_store_peak": r.needed["links"],
+           "raw_links": st["raw_links"], "kept_links": st["kept_links"], "link_store_links": r.needed["links"] + 2 * r.needed["window_links"],
            "kernel_ms": {"forward": round(sum(fwd) / steps, 2), "lattice": round(sum(lat) / steps, 2)}}
     del graph
     torch.cuda.empty_cache()
     return out
+
+
+def stream_hclg(wfstdec, graph, x, cfg, chunk: int, steps: int = 3) -> dict:
+    """The headline utterance streamed in chunks of `chunk` frames
+    (wd_stream_*): throughput with every chunk pushed without waiting (begin
+    to end, lattice included), and the latency of one chunk's decode when
+    each push is waited for."""
+    import numpy as np
+    import torch
+    T = int(x.shape[0])
+    args = (cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+
+    def run(wait: bool):
+        s = wfstdec.Stream(graph, 1, T, *args, mode="workgroup")
+        lat = []
+        for t0 in range(0, T, chunk):
+            a = time.perf_counter()
+            s.push([x[t0:t0 + chunk]])
+            if wait:
+                torch.cuda.synchronize()
+                lat.append(1e3 * (time.perf_counter() - a))
+        return s.end()[0], lat
+
+    run(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        r, _ = run(False)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    _, lat = run(True)
+    return {"workload": f"{WORKLOAD}_stream", "chunk_frames": chunk, "frames": T, "steps": steps,
+            "frames_per_s": round(T / wall, 1), "ms_per_utterance": round(1e3 * wall, 2),
+            "chunk_latency_ms": {"mean": round(float(np.mean(lat)), 3),
+                                 "p95": round(float(np.percentile(lat, 95)), 3)},
+            "cost": float(r.cost)}
 
 
 def algorithmic_bytes(stats: dict) -> int:
@@ -217,9 +255,11 @@ def main() -> int:
                      "traffic": traffic, "algorithmic_bytes_per_launch": int(bytes_launch)},
     }
     if not args.no_extra and workload == WORKLOAD:
+        streamed = [stream_hclg(wfstdec, graph, x, cfg, chunk) for chunk in (32, 8)]
         del graph, x
         torch.cuda.empty_cache()
-        out["other_workloads"] = [wide_chip(wfstdec, mode=m) for m in ("chip", "chip_noprune", "chip_dyn")]
+        out["other_workloads"] = streamed + [wide_chip(wfstdec, mode=m)
+                                             for m in ("chip", "chip_noprune", "chip_dyn")]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(g, L, cfg, workload)
     print(json.dumps(out), flush=True)
