@@ -50,8 +50,8 @@ BYTES_LINK = 16
 # runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
 # divided by the counter's reading per byte of a plain device copy of known
 # size (bench.py --copy-kernel-bytes).  Valid while k_forward's sources hash to this.
-TRAFFIC = {"sources_sha256": "0fcd903e396109939359d56d8fb4f6b603dc04f50124c4282e3dba76429b33d8",
-           "bytes_per_launch": 54145369}
+TRAFFIC = {"sources_sha256": "b9ff87f8ee3429a5870b2fa6ee94579b1d75a84587365c5f20ce3e8b705885ef",
+           "bytes_per_launch": 54150642}
 
 
 FORWARD_SOURCES = ("wd_block.h", "wd_common.h", "wd_forward.hip")  # what k_forward is built from
@@ -183,6 +183,7 @@ def main() -> int:
     ap.add_argument("--copy-kernel-bytes", type=int, default=0)
     ap.add_argument("--workload", default=WORKLOAD,
                     help="workload timed (the headline line is hclg_5m; others are for profiling)")
+    ap.add_argument("--mode", default="auto", help="execution mode of the timed decodes (for profiling)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this decoder runs on one GPU; --gpus {args.gpus} is not supported "
@@ -208,12 +209,12 @@ def main() -> int:
     beam, ma, lb = cfg["beam"], cfg["max_active"], cfg["lattice_beam"]
 
     for _ in range(max(1, args.warmup)):
-        r = wfstdec.decode(graph, x, beam, ma, lb, timing=True)
+        r = wfstdec.decode(graph, x, beam, ma, lb, timing=True, mode=args.mode)
     torch.cuda.synchronize()
     fwd_ms, lat_ms = [], []
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        r = wfstdec.decode(graph, x, beam, ma, lb, timing=True)
+        r = wfstdec.decode(graph, x, beam, ma, lb, timing=True, mode=args.mode)
         fwd_ms.append(r.stats["forward_ms"])
         lat_ms.append(r.stats["lattice_ms"])
     torch.cuda.synchronize()
@@ -229,7 +230,8 @@ def main() -> int:
     traffic = (TRAFFIC["bytes_per_launch"]
                if TRAFFIC and workload == WORKLOAD and TRAFFIC["sources_sha256"] == sources_sha256()
                else None)
-    chip = cfg["max_active"] == 0 or cfg["max_active"] >= wfstdec.WD_CHIP_WIDE_MAX_ACTIVE
+    chip = args.mode.startswith("chip") or (args.mode == "auto" and (
+        cfg["max_active"] == 0 or cfg["max_active"] >= wfstdec.WD_CHIP_WIDE_MAX_ACTIVE))
     out = {
         "metric": METRIC,
         "value": round(fps, 2),
@@ -245,7 +247,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": workload, "states": cfg["S"], "arcs": cfg["A"], "frames": T,
                    "pdfs": cfg["P"], "beam": beam, "max_active": ma, "lattice_beam": lb,
-                   "utterances_per_step": 1},
+                   "utterances_per_step": 1, "mode": args.mode},
         "arcs_expanded_per_s": round(st["arcs_expanded"] * args.steps / wall, 1),
         "rtf": round((wall / args.steps) / (T / FRAME_RATE), 7),
         "tokens_per_frame": round(st["tokens"] / (T + 1), 1),
