@@ -13,9 +13,9 @@ one k_forward launch measured with hardware counters (FETCH_SIZE + WRITE_SIZE,
 each scaled by what the same counter reads for a plain device copy of known
 size), reported only while the kernel sources hash to the ones the counters
 were taken on; `other_workloads` times the same utterance streamed in chunks
-of 32 and 8 frames, and the chip-wide mode on the wide-beam 2M-state graph
-(with and without incremental lattice pruning, and with dynamic load
-balancing).  `--copy-kernel-bytes N` only runs a plain N-byte device copy
+of 32 and 8 frames, the host determinisation of its lattice, and the
+chip-wide mode on the wide-beam 2M-state graph (with and without incremental
+lattice pruning, and with dynamic load balancing).  `--copy-kernel-bytes N` only runs a plain N-byte device copy
 (the counter calibration run) and exits.
 """
 from __future__ import annotations
@@ -150,6 +150,20 @@ def stream_hclg(wfstdec, graph, x, cfg, chunk: int, steps: int = 3) -> dict:
             "cost": float(r.cost)}
 
 
+def determinize_hclg(wfstdec, r, g, T: int, reps: int = 20) -> dict:
+    """Host determinisation of the headline utterance's lattice (the compact
+    exact lattice), timed over `reps` runs; lattice density (arcs per frame)
+    before and after."""
+    s0, fw = int(g.get("start_state", 0)), g.get("final_weight")
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        c = wfstdec.determinize(r, s0, fw)
+    dt = (time.perf_counter() - t0) / reps
+    return {"workload": f"{WORKLOAD}_determinize", "where": "host, one thread", "ms": round(1e3 * dt, 3),
+            "lattice_arcs_per_frame": round(len(r.links) / T, 3),
+            "compact_arcs_per_frame": round(len(c.arcs) / T, 3), "compact_states": int(c.states)}
+
+
 def algorithmic_bytes(stats: dict) -> int:
     emit = stats["arcs_expanded"] - stats["eps_arcs_expanded"]
     return (stats["arcs_expanded"] * BYTES_ARC + emit * BYTES_LOGLIKE +
@@ -258,6 +272,7 @@ def main() -> int:
     }
     if not args.no_extra and workload == WORKLOAD:
         streamed = [stream_hclg(wfstdec, graph, x, cfg, chunk) for chunk in (32, 8)]
+        streamed.append(determinize_hclg(wfstdec, r, g, T))
         del graph, x
         torch.cuda.empty_cache()
         out["other_workloads"] = streamed + [wide_chip(wfstdec, mode=m)

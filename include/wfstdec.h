@@ -253,6 +253,51 @@ wd_status wd_stream_advance(wd_stream* s, const int32_t* n_frames);
 wd_status wd_stream_end(wd_stream* s, wd_result** out);
 void      wd_stream_free(wd_stream* s);
 
+/* ---- lattice determinisation (host) ----------------------------------- */
+
+/* The compact "exact lattice" (Sec. 3.4, after Povey et al. 2012) of a pruned
+ * state-level lattice, computed on the CPU as the paper does after the copy
+ * to the host.  Input: the links and nodes of a result (wd_result_lattice,
+ * wd_result_nodes: nodes sorted by (t, state); a link runs from node
+ * (t-1, src_state) if ilabel != 0, else (t, src_state), to (t, dst_state)),
+ * the start state (its node at t = 0 starts every path), and node_final[i],
+ * the final graph cost of node i (+inf: not final; NULL: the nodes of the
+ * last frame, cost 0).  A path's weight is the pair (sum of graph costs, sum
+ * of acoustic costs), in double; its string is the ilabels of its emitting
+ * links in order; its words are its nonzero olabels.
+ * Output: a lattice deterministic on words (state 0 starts; no arc has word
+ * 0; arcs sorted by (source state, word)) with exactly one path per word
+ * sequence of the input; that path's weight and string are those of the best
+ * input path with the same words (best: lower graph + acoustic total, then
+ * the lexicographically smaller string, then the lower graph cost).  An arc's
+ * alignment is its part of the path's string; a final state's alignment
+ * ends it.  WD_EINVAL for unsorted nodes, dangling links or a cycle;
+ * WD_ECAPACITY beyond max_states output states (<= 0: 4M).  Residual
+ * weights are kept in double; output states whose residuals differ in their
+ * last bits are not merged (the lattice stays deterministic and exact). */
+typedef struct {
+  int32_t src, dst;
+  int32_t word;         /* olabel, never 0 */
+  int32_t align_len;
+  double graph_cost, ac_cost;
+  int64_t align_off;    /* into wd_clat_alignment */
+} wd_clat_arc;
+typedef struct {
+  int32_t state;
+  int32_t align_len;
+  double graph_cost, ac_cost;
+  int64_t align_off;
+} wd_clat_final;
+typedef struct wd_clat wd_clat;
+wd_status wd_lattice_determinize(const wd_lat_arc* arcs, int64_t n_arcs, const wd_lat_node* nodes,
+                                 int64_t n_nodes, int32_t start_state, const float* node_final,
+                                 int64_t max_states, wd_clat** out);
+int32_t wd_clat_states(const wd_clat* c);
+int64_t wd_clat_arcs(const wd_clat* c, const wd_clat_arc** arcs);
+int64_t wd_clat_finals(const wd_clat* c, const wd_clat_final** finals);
+int64_t wd_clat_alignment(const wd_clat* c, const int32_t** labels);
+void    wd_clat_free(wd_clat* c);
+
 /* ---- results (host memory owned by the result) ------------------------ */
 
 wd_status wd_result_status(const wd_result* r);

@@ -36,6 +36,10 @@ LINK_DTYPE = np.dtype([("t", "<i4"), ("arc_id", "<u4"), ("src_state", "<i4"), ("
                        ("ilabel", "<i4"), ("olabel", "<i4"), ("graph_cost", "<f4"),
                        ("ac_cost", "<f4"), ("fwd_cost", "<f4"), ("extra", "<f4"),
                        ("posterior", "<f8")], align=True)
+CLAT_ARC_DTYPE = np.dtype([("src", "<i4"), ("dst", "<i4"), ("word", "<i4"), ("align_len", "<i4"),
+                           ("graph_cost", "<f8"), ("ac_cost", "<f8"), ("align_off", "<i8")], align=True)
+CLAT_FINAL_DTYPE = np.dtype([("state", "<i4"), ("align_len", "<i4"), ("graph_cost", "<f8"),
+                             ("ac_cost", "<f8"), ("align_off", "<i8")], align=True)
 NODE_DTYPE = np.dtype([("t", "<i4"), ("state", "<i4"), ("cost", "<f4"), ("extra", "<f4")], align=True)
 TOKEN_DTYPE = np.dtype([("t", "<i4"), ("state", "<i4"), ("cost", "<f4"), ("pred_arc", "<u4")],
                        align=True)
@@ -77,7 +81,9 @@ class wd_stats(ctypes.Structure):
 
 EXPORTS = ["wd_graph_bytes", "wd_graph_load", "wd_graph_free", "wd_graph_eps_levels",
            "wd_workspace_bytes", "wd_decode", "wd_decode_batch", "wd_stream_begin",
-           "wd_stream_advance", "wd_stream_end", "wd_stream_free", "wd_result_status",
+           "wd_stream_advance", "wd_stream_end", "wd_stream_free", "wd_lattice_determinize",
+           "wd_clat_states", "wd_clat_arcs", "wd_clat_finals", "wd_clat_alignment", "wd_clat_free",
+           "wd_result_status",
            "wd_result_cost", "wd_result_words", "wd_result_lattice", "wd_result_nodes",
            "wd_result_tokens", "wd_result_raw_lattice", "wd_result_cutoffs", "wd_result_stats",
            "wd_result_free", "wd_last_error"]
@@ -110,6 +116,13 @@ def lib():
             "wd_stream_advance": ([VP, P(ctypes.c_int32)], ctypes.c_int),
             "wd_stream_end": ([VP, P(VP)], ctypes.c_int),
             "wd_stream_free": ([VP], None),
+            "wd_lattice_determinize": ([VP, ctypes.c_int64, VP, ctypes.c_int64, ctypes.c_int32, VP,
+                                        ctypes.c_int64, P(VP)], ctypes.c_int),
+            "wd_clat_states": ([VP], ctypes.c_int32),
+            "wd_clat_arcs": ([VP, P(VP)], ctypes.c_int64),
+            "wd_clat_finals": ([VP, P(VP)], ctypes.c_int64),
+            "wd_clat_alignment": ([VP, P(VP)], ctypes.c_int64),
+            "wd_clat_free": ([VP], None),
             "wd_result_status": ([VP], ctypes.c_int),
             "wd_result_cost": ([VP], ctypes.c_float),
             "wd_result_words": ([VP, P(VP)], ctypes.c_int32),
@@ -215,6 +228,53 @@ def wd_stream_end(sh: int, B: int) -> tuple[int, list[int]]:
 
 def wd_stream_free(sh: int) -> None:
     lib().wd_stream_free(sh)
+
+
+def wd_lattice_determinize(links, nodes, start_state: int, node_final=None,
+                           max_states: int = 0) -> SimpleNamespace:
+    """Host lattice determinisation of (links, nodes) arrays; returns
+    states, arcs (CLAT_ARC_DTYPE), finals (CLAT_FINAL_DTYPE) and the
+    alignment label pool."""
+    L = lib()
+    la = np.zeros(len(links), LINK_DTYPE)
+    for f in LINK_DTYPE.names:
+        la[f] = links[f]
+    na = np.zeros(len(nodes), NODE_DTYPE)
+    for f in NODE_DTYPE.names:
+        na[f] = nodes[f]
+    nf = None if node_final is None else np.ascontiguousarray(node_final, dtype=np.float32)
+    if nf is not None and nf.size != len(nodes):
+        raise ValueError("node_final needs one value per node")
+    h = ctypes.c_void_p()
+    _check(L.wd_lattice_determinize(la.ctypes.data if la.size else None, la.size,
+                                    na.ctypes.data if na.size else None, na.size, int(start_state),
+                                    None if nf is None else nf.ctypes.data, int(max_states), ctypes.byref(h)))
+    try:
+        out = SimpleNamespace(states=L.wd_clat_states(h))
+        for name, acc, dt in (("arcs", L.wd_clat_arcs, CLAT_ARC_DTYPE),
+                              ("finals", L.wd_clat_finals, CLAT_FINAL_DTYPE),
+                              ("align", L.wd_clat_alignment, np.dtype("<i4"))):
+            vp = ctypes.c_void_p()
+            n = acc(h, ctypes.byref(vp))
+            setattr(out, name, _copy(vp.value, n, dt))
+    finally:
+        L.wd_clat_free(h)
+    return out
+
+
+def determinize(result, start_state: int = 0, final_weight=None, max_states: int = 0) -> SimpleNamespace:
+    """The compact lattice of a decode result (this library's or the
+    oracle's): the last frame's nodes are final with the graph's final
+    weights when the decode used them (stats final_reached), else cost 0."""
+    nodes = result.nodes
+    T = int(result.stats["frames"])
+    nf = np.full(len(nodes), np.inf, np.float32)
+    last = nodes["t"] == T
+    if final_weight is not None and result.stats["final_reached"]:
+        nf[last] = np.asarray(final_weight, np.float32)[nodes["state"][last]]
+    else:
+        nf[last] = 0.0
+    return wd_lattice_determinize(result.links, nodes, start_state, nf, max_states)
 
 
 def _copy(ptr, n, dtype):
