@@ -13,9 +13,11 @@ one k_forward launch measured with hardware counters (FETCH_SIZE + WRITE_SIZE,
 each scaled by what the same counter reads for a plain device copy of known
 size), reported only while the kernel sources hash to the ones the counters
 were taken on; `other_workloads` times the same utterance streamed in chunks
-of 32 and 8 frames, the host determinisation of its lattice, and the
+of 32 and 8 frames, the host determinisation of its lattice, the
+64-utterance batch on the same graph (with its own roofline), and the
 chip-wide mode on the wide-beam 2M-state graph (with and without incremental
-lattice pruning, and with dynamic load balancing).  `--copy-kernel-bytes N` only runs a plain N-byte device copy
+lattice pruning, and with dynamic load balancing); `roofline.copy_ceiling_gbs`
+is what a plain device copy reaches.  `--copy-kernel-bytes N` only runs a plain N-byte device copy
 (the counter calibration run) and exits.
 """
 from __future__ import annotations
@@ -164,6 +166,76 @@ def determinize_hclg(wfstdec, r, g, T: int, reps: int = 20) -> dict:
             "compact_arcs_per_frame": round(len(c.arcs) / T, 3), "compact_states": int(c.states)}
 
 
+def batch64(wfstdec, graph, steps: int = 3) -> dict:
+    """The 64-utterance batch on the same graph (one workgroup per utterance,
+    one launch for the batch): aggregate frames/s and the roofline of the
+    batch's k_forward launch.  Algorithmic bytes are summed over the lanes
+    (arcs that several lanes expand in the same step count once per lane, so
+    this is an upper bound of the unique-arc figure)."""
+    import numpy as np
+    import synth
+    import torch
+    cfg = synth.workload("batch64_hclg_5m")
+    xs = [torch.from_numpy(x).to(graph.device) for x in synth.make_batch(cfg)]
+    args = (cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    wfstdec.decode_batch(graph, xs, *args, timing=True)
+    torch.cuda.synchronize()
+    fwd, lat = [], []
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        rs = wfstdec.decode_batch(graph, xs, *args, timing=True)
+        fwd.append(rs[0].stats["forward_ms"])
+        lat.append(rs[0].stats["lattice_ms"])
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    frames = sum(int(x.shape[0]) for x in xs)
+    f_ms = float(np.mean(fwd))
+    nbytes = sum(algorithmic_bytes(r.stats) for r in rs)
+    achieved = nbytes / (f_ms * 1e-3) / 1e9
+    out = {"workload": "batch64_hclg_5m", "utterances": len(xs), "frames": frames, "steps": steps,
+           "frames_per_s": round(frames / wall, 1), "ms_per_step": round(1e3 * wall, 2),
+           "arcs_expanded_per_s": round(sum(r.stats["arcs_expanded"] for r in rs) / wall, 1),
+           "kernel_ms": {"forward": round(f_ms, 3), "lattice": round(float(np.mean(lat)), 3)},
+           "roofline": {"bound": "hbm", "kernel": "k_forward (64 workgroups)", "achieved": round(achieved, 3),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
+                        "algorithmic_bytes_per_launch": int(nbytes)}}
+    del xs
+    torch.cuda.empty_cache()
+    return out
+
+
+def copy_ceiling(nbytes: int = 1 << 30, reps: int = 10) -> float:
+    """GB/s (bytes read + written) of a plain device-to-device copy: the
+    bandwidth a streaming kernel reaches on this GPU."""
+    import torch
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2 * nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return round(gbs, 1)
+
+
+def host_info() -> dict:
+    import torch
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpu": model, "gpu": torch.cuda.get_device_name(0)}
+
+
 def algorithmic_bytes(stats: dict) -> int:
     emit = stats["arcs_expanded"] - stats["eps_arcs_expanded"]
     return (stats["arcs_expanded"] * BYTES_ARC + emit * BYTES_LOGLIKE +
@@ -273,10 +345,14 @@ def main() -> int:
     if not args.no_extra and workload == WORKLOAD:
         streamed = [stream_hclg(wfstdec, graph, x, cfg, chunk) for chunk in (32, 8)]
         streamed.append(determinize_hclg(wfstdec, r, g, T))
+        streamed.append(batch64(wfstdec, graph))
         del graph, x
         torch.cuda.empty_cache()
         out["other_workloads"] = streamed + [wide_chip(wfstdec, mode=m)
                                              for m in ("chip", "chip_noprune", "chip_dyn")]
+    if not args.no_extra:
+        out["roofline"]["copy_ceiling_gbs"] = copy_ceiling()
+    out["host"] = host_info()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(g, L, cfg, workload)
     print(json.dumps(out), flush=True)
