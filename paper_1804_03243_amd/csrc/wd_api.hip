@@ -383,6 +383,27 @@ static wd_status run_finish(wd_stream* run, wd_result** out) {
   }
   wd_status first_bad = WD_OK;
   const bool debug = (p->flags & WD_FLAG_DEBUG) != 0;
+  // Without the debug outputs, the finished lanes' links, nodes and words
+  // are packed on the device (into the candidate buffer, free after the
+  // forward pass) and copied with one transfer instead of three per lane.
+  std::vector<uint64_t> poff((size_t)B + 1, 0);
+  for (int b = 0; b < B; ++b) {
+    const LaneInfo& I = info[b];
+    const uint64_t n = (I.status != 0 || I.tb_fail) ? 0
+                       : sizeof(OutLink) * I.kept + sizeof(OutNode) * I.out_nodes + ((4 * I.nwords + 15) & ~15ull);
+    poff[b + 1] = poff[b] + n;
+  }
+  const bool packed = !debug && poff[B] > 0 && poff[B] <= (uint64_t)B * run->c.arcs * 16;
+  std::vector<char> pack;
+  if (packed) {
+    pack.resize(poff[B]);
+    launch_pack_results(R.desc, B, run->lanes[0].cand, s);
+    if ((st = hip_check(hipGetLastError(), "launch")) ||
+        (st = hip_check(hipMemcpyAsync(pack.data(), run->lanes[0].cand, poff[B], hipMemcpyDeviceToHost, s),
+                        "result download")) ||
+        (st = hip_check(hipStreamSynchronize(s), "result download")))
+      return st;
+  }
   for (int b = 0; b < B; ++b) {
     const LaneInfo& I = info[b];
     const LaneDesc& L = run->lanes[b];
@@ -416,6 +437,7 @@ static wd_status run_finish(wd_stream* run, wd_result** out) {
     r->words.resize(I.nwords);
     r->links.resize(I.kept);
     r->nodes.resize(I.out_nodes);
+    if (packed) continue;  // copied below, all lanes at once
     auto d2h = [&](void* dst, const void* src, uint64_t bytes) -> wd_status {
       if (!bytes) return WD_OK;
       return hip_check(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s), "result download");
@@ -447,6 +469,17 @@ static wd_status run_finish(wd_stream* run, wd_result** out) {
           r->tokens[n] = wd_token{t, (int32_t)ns[n], key_cost((uint32_t)(np[n] >> 32)), (uint32_t)np[n]};
     }
   }
+  if (packed)
+    for (int b = 0; b < B; ++b) {
+      wd_result* r = out[b];
+      if (!r || r->status != WD_OK) continue;
+      const char* src = pack.data() + poff[b];
+      std::memcpy(r->links.data(), src, sizeof(OutLink) * r->links.size());
+      src += sizeof(OutLink) * r->links.size();
+      std::memcpy(r->nodes.data(), src, sizeof(OutNode) * r->nodes.size());
+      src += sizeof(OutNode) * r->nodes.size();
+      std::memcpy(r->words.data(), src, 4 * r->words.size());
+    }
   if ((st = hip_check(hipStreamSynchronize(s), "result download"))) return st;
   if (first_bad != WD_OK) {
     std::string msg = first_bad == WD_ENOPATH   ? "decode: no token survived a frame"

@@ -900,6 +900,37 @@ __global__ void k_fill_u32(uint32_t* p, uint64_t n, uint32_t v) {
     p[i] = v;
 }
 
+// Results of every finished utterance (links, nodes, words) packed into one
+// contiguous buffer, so that the host copies them with one transfer: lane b
+// starts after the lanes before it, each lane's part is its links, its nodes
+// and its words padded to 16 bytes (packed_bytes; the host computes the same
+// offsets).  One workgroup per lane.
+__device__ __forceinline__ uint64_t packed_bytes(const LaneInfo& I) {
+  if (I.status != 0 || I.tb_fail) return 0;
+  return sizeof(OutLink) * I.kept + sizeof(OutNode) * I.out_nodes + ((4 * I.nwords + 15) & ~15ull);
+}
+
+__global__ void k_pack_results(const LaneDesc* __restrict__ lanes, int B, char* __restrict__ dst) {
+  const int b = blockIdx.x;
+  uint64_t off = 0;
+  for (int k = 0; k < b; ++k) off += packed_bytes(*lanes[k].info);
+  const LaneDesc& L = lanes[b];
+  const LaneInfo& I = *L.info;
+  if (!packed_bytes(I)) return;
+  uint4* out = reinterpret_cast<uint4*>(dst + off);
+  const uint64_t nl = I.kept * (sizeof(OutLink) / 16), nn = I.out_nodes;
+  const uint4* ls = reinterpret_cast<const uint4*>(L.out_links);
+  const uint4* ns = reinterpret_cast<const uint4*>(L.out_nodes);
+  for (uint64_t i = threadIdx.x; i < nl; i += blockDim.x) out[i] = ls[i];
+  for (uint64_t i = threadIdx.x; i < nn; i += blockDim.x) out[nl + i] = ns[i];
+  uint32_t* w = reinterpret_cast<uint32_t*>(out + nl + nn);
+  for (uint64_t i = threadIdx.x; i < I.nwords; i += blockDim.x) w[i] = (uint32_t)L.out_words[i];
+}
+
+void launch_pack_results(const LaneDesc* lanes, int B, void* dst, hipStream_t s) {
+  hipLaunchKernelGGL(k_pack_results, dim3(B), dim3(256), 0, s, lanes, B, (char*)dst);
+}
+
 constexpr int kSetLanes = 128;
 struct FrameSet {
   int32_t T[kSetLanes];

@@ -51,6 +51,9 @@ void launch_grid_sweep(const DevGraph& g, const LaneDesc* lanes, void* grid, int
                        hipStream_t s);
 void launch_grid_nodes(const LaneDesc* lanes, void* grid, int B, hipStream_t s);
 void launch_check_loglikes(const LaneDesc* lanes, int B, uint32_t P, uint32_t* bad, hipStream_t s);
+// Packs the links, nodes and words of every finished lane into dst (device),
+// lane after lane, each lane's part 16-byte aligned.
+void launch_pack_results(const LaneDesc* lanes, int B, void* dst, hipStream_t s);
 // Sets T, t0 and open of lanes[0..B) (streaming) from host values passed as
 // kernel arguments.
 void launch_set_frames(LaneDesc* lanes, int B, const int32_t* T, const int32_t* t0, int32_t open, hipStream_t s);

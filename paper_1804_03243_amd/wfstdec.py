@@ -278,10 +278,11 @@ def determinize(result, start_state: int = 0, final_weight=None, max_states: int
 
 
 def _copy(ptr, n, dtype):
-    if n <= 0 or not ptr:
-        return np.zeros(0, dtype=dtype)
-    buf = (ctypes.c_char * (int(n) * dtype.itemsize)).from_address(ptr)
-    return np.frombuffer(bytes(buf), dtype=dtype).copy()
+    """n records of `dtype` at host address ptr, copied into a new array."""
+    out = np.empty(max(int(n), 0), dtype=dtype)
+    if out.size and ptr:
+        ctypes.memmove(out.ctypes.data, ptr, out.nbytes)
+    return out
 
 
 def wd_result_read(r: int) -> SimpleNamespace:
