@@ -24,6 +24,7 @@ namespace wd {
 constexpr uint32_t kNoKey = 0xffffffffu;
 constexpr uint32_t kLdsWork = 3 * kHashMax;  // emitting work above which a frame starts global
 constexpr uint32_t kBkCap = 1024;            // LDS epsilon bucket entries before a frame spills
+constexpr uint32_t kDirectRank = 256;        // survivors ranked directly, without the counting sort
 static_assert(kBkCap == (uint32_t)kThreads, "one bucket entry per thread in the epsilon level scan");
 
 struct FwdShared {
@@ -44,7 +45,7 @@ struct FwdShared {
   uint32_t rs_state[kRankMax];
   unsigned long long rs_pack[kRankMax];
   uint32_t rs_slot[kRankMax];
-  uint32_t srt[kRankMax];      // states by bucket while sorting survivors
+  alignas(16) uint32_t srt[kRankMax];  // states by bucket while sorting survivors
   uint32_t h_key[kHashCap];
   unsigned long long h_val[kHashCap];
   uint4 bk[kBkCap];    // {table slot, first epsilon arc, end epsilon arc, level}
@@ -280,6 +281,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     uint64_t eps_frame = 0;
     bool failed = false;
     uint4 my_c = make_uint4(0, 0, 0, 0);  // this thread's first candidate (work item tid)
+    float warm = 0.0f;  // values of cache-warming loads, read at the end of the frame
     // ---------------------------------------------------- token passing
     for (int attempt = 0; attempt < 2; ++attempt) {
       eps_frame = 0;
@@ -340,6 +342,12 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         }
         const float cutb = key_cost(best_key) + prm.beam;
         kcutb = cost_key(cutb);
+        // the upper wavefronts warm the first epsilon arcs of the entries the
+        // expansion bucketed (read by the level passes below)
+        if (tid >= 512u && tid - 512u < (sh.n_bk < kBkCap ? sh.n_bk : kBkCap)) {
+          const uint4 e = sh.bk[tid - 512u];
+          if (e.z > e.y) warm = __uint_as_float(g.xarc[e.y].y);
+        }
         for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
           if (sh.nbl[lvl] == 0) continue;  // uniform: written only by lower levels
           // this level's entries within the cutoff spread their epsilon arcs
@@ -589,52 +597,75 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         }
       }
       const uint32_t m = lds ? ns : n_keep;  // entries in rs_* (<= 2 * kThreads)
-      // counting sort on the top 11 bits of the state, then the few states
-      // sharing a bucket are ranked among themselves
-      const uint32_t sbits = 32u - (uint32_t)__clz(g.S > 1 ? g.S - 1 : 1u);
-      const uint32_t ssh = sbits > 11u ? sbits - 11u : 0u;
-      for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
-      __syncthreads();
-      uint32_t bb[2] = {0, 0}, loc[2] = {0, 0}, sv[2] = {0, 0}, sl[2] = {0, 0};
-      unsigned long long vv[2] = {0, 0};
-      bool kp[2] = {false, false};
-      for (int u = 0; u < 2; ++u) {
-        const uint32_t j = tid + (uint32_t)u * kThreads;
-        if (j >= m) continue;
-        vv[u] = sh.rs_pack[j];
-        if ((uint32_t)(vv[u] >> 32) > cut_key) continue;
-        kp[u] = true;
-        sv[u] = sh.rs_state[j];
-        sl[u] = sh.rs_slot[j];
-        bb[u] = sv[u] >> ssh;
-        loc[u] = atomicAdd(&sh.hist[bb[u]], 1u);
-      }
-      __syncthreads();
-      uint32_t nk;
-      {
-        const uint32_t h0 = sh.hist[2 * tid], h1 = sh.hist[2 * tid + 1];
-        const uint32_t ex = block_excl_scan(h0 + h1, sh.bs, par, &nk);
-        __syncthreads();  // every count read before the starts overwrite them
-        sh.hist[2 * tid] = ex;
-        sh.hist[2 * tid + 1] = ex + h0;
-      }
-      if (nk != n_keep) {
-        status = kStatusInternal;
-        break;
-      }
-      __syncthreads();
-      for (int u = 0; u < 2; ++u)
-        if (kp[u]) sh.srt[sh.hist[bb[u]] + loc[u]] = sv[u];
-      __syncthreads();
-      for (int u = 0; u < 2; ++u) {
-        if (!kp[u]) continue;
-        const uint32_t b0 = sh.hist[bb[u]];
-        const uint32_t b1 = bb[u] + 1 < (uint32_t)kHistBins ? sh.hist[bb[u] + 1] : n_keep;
-        uint32_t r = b0;
-        for (uint32_t q = b0; q < b1; ++q) r += sh.srt[q] < sv[u];
-        place(r, sv[u], vv[u]);
-        if (lds) sh.h_val[sl[u]] = node_base + r;  // the table now maps kept states to node ids
-        else L.idx[sv[u]] = (uint32_t)(node_base + r);
+      if (m <= kDirectRank) {
+        // few entries: each kept state's rank is the number of kept states
+        // below it (non-kept entries and the padding to 4 read as ~0)
+        if (tid < ((m + 3u) & ~3u)) {
+          uint32_t s = kNoKey;
+          if (tid < m && (uint32_t)(sh.rs_pack[tid] >> 32) <= cut_key) s = sh.rs_state[tid];
+          sh.srt[tid] = s;
+        }
+        __syncthreads();
+        if (tid < m && sh.srt[tid] != kNoKey) {
+          const uint32_t s = sh.srt[tid];
+          const uint4* q4 = reinterpret_cast<const uint4*>(sh.srt);
+          uint32_t r = 0;
+          for (uint32_t q = 0; q < (m + 3u) / 4u; ++q) {
+            const uint4 v = q4[q];
+            r += (v.x < s) + (v.y < s) + (v.z < s) + (v.w < s);
+          }
+          place(r, s, sh.rs_pack[tid]);
+          if (lds) sh.h_val[sh.rs_slot[tid]] = node_base + r;  // the table now maps kept states to node ids
+          else L.idx[s] = (uint32_t)(node_base + r);
+        }
+      } else {
+        // counting sort on the top 11 bits of the state, then the few states
+        // sharing a bucket are ranked among themselves
+        const uint32_t sbits = 32u - (uint32_t)__clz(g.S > 1 ? g.S - 1 : 1u);
+        const uint32_t ssh = sbits > 11u ? sbits - 11u : 0u;
+        for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
+        __syncthreads();
+        uint32_t bb[2] = {0, 0}, loc[2] = {0, 0}, sv[2] = {0, 0}, sl[2] = {0, 0};
+        unsigned long long vv[2] = {0, 0};
+        bool kp[2] = {false, false};
+        for (int u = 0; u < 2; ++u) {
+          const uint32_t j = tid + (uint32_t)u * kThreads;
+          if (j >= m) continue;
+          vv[u] = sh.rs_pack[j];
+          if ((uint32_t)(vv[u] >> 32) > cut_key) continue;
+          kp[u] = true;
+          sv[u] = sh.rs_state[j];
+          sl[u] = sh.rs_slot[j];
+          bb[u] = sv[u] >> ssh;
+          loc[u] = atomicAdd(&sh.hist[bb[u]], 1u);
+        }
+        __syncthreads();
+        uint32_t nk;
+        {
+          const uint32_t h0 = sh.hist[2 * tid], h1 = sh.hist[2 * tid + 1];
+          const uint32_t ex = block_excl_scan(h0 + h1, sh.bs, par, &nk);
+          __syncthreads();  // every count read before the starts overwrite them
+          sh.hist[2 * tid] = ex;
+          sh.hist[2 * tid + 1] = ex + h0;
+        }
+        if (nk != n_keep) {
+          status = kStatusInternal;
+          break;
+        }
+        __syncthreads();
+        for (int u = 0; u < 2; ++u)
+          if (kp[u]) sh.srt[sh.hist[bb[u]] + loc[u]] = sv[u];
+        __syncthreads();
+        for (int u = 0; u < 2; ++u) {
+          if (!kp[u]) continue;
+          const uint32_t b0 = sh.hist[bb[u]];
+          const uint32_t b1 = bb[u] + 1 < (uint32_t)kHistBins ? sh.hist[bb[u] + 1] : n_keep;
+          uint32_t r = b0;
+          for (uint32_t q = b0; q < b1; ++q) r += sh.srt[q] < sv[u];
+          place(r, sv[u], vv[u]);
+          if (lds) sh.h_val[sl[u]] = node_base + r;  // the table now maps kept states to node ids
+          else L.idx[sv[u]] = (uint32_t)(node_base + r);
+        }
       }
     } else {
       for (uint32_t i = tid; i < ns; i += kThreads) {
@@ -715,6 +746,21 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     if (tid == 0) {
       sh.c_tokens += n_keep;
       if (n_keep > sh.c_max_tokens) sh.c_max_tokens = n_keep;
+    }
+    // Warm the caches for frame t+1 while the links are written: one load
+    // per 128-byte line of its log-likelihood row and one per work item of
+    // its first 256 emitting arcs.  The upper wavefronts issue them: in small
+    // frames they have no link items, and a wavefront's loads complete in
+    // order, so loads issued by a busy wavefront would make its own link
+    // loads wait for them.  The values are read only after the link pass.
+    if (t < T) {
+      if (tid >= 768u) {
+        const uint32_t k = (tid - 768u) * 32u;
+        if (k < P) warm += L.ll[(size_t)t * P + k];
+      } else if (tid >= 512u && tid - 512u < W_next) {
+        const uint32_t w = tid - 512u, p = search_le(f.edeg, n_keep, w);
+        warm += __uint_as_float(g.earc[f.ebeg[p] + (w - f.edeg[p])].y);
+      }
     }
     // -------------------------------------------------- lattice links of frame t
     // node id of a state that survived frame t
@@ -809,6 +855,9 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         }
       }
     }
+    // a payload no sum of a finite weight and a log-likelihood has: keeps the
+    // warming loads without waiting for them earlier
+    if (__float_as_uint(warm) == 0x7fc00001u) bad_idx |= 2u;
     const uint32_t fl_or = block_or((bad_idx ? 0x80000000u : 0u) | xmask, sh.bs, par);
     if (fl_or & 0x80000000u) {
       status = kStatusInternal;
