@@ -6,15 +6,21 @@
  * Method: Chen, Luitjens, Xu, Wang, Povey, Khudanpur, "A GPU-based WFST
  * Decoder with Exact Lattice Generation", Interspeech 2018 -- token passing
  * and atomic recombination (Sec. 3.2, Alg. 1), load-balanced arc expansion
- * (Sec. 3.3), lattice-arc recording (Sec. 3.4), lattice pruning and final
- * merge (Sec. 3.5), lattice posteriors (Sec. 4.1).
+ * (Sec. 3.3, Alg. 2), lattice-arc recording (Sec. 3.4), lattice pruning and
+ * final merge (Sec. 3.5, also incrementally on a second stream, Sec. 3.1),
+ * lattice posteriors (Sec. 4.1), the compact exact lattice (Sec. 3.4, on the
+ * host), streaming decodes (the integration with acoustic inference the
+ * paper leaves to future work, Sec. 5).
  *
  * Conventions for every entry point:
  *  - Return a wd_status; no exception crosses this boundary.  On a non-OK
  *    status, wd_last_error() returns a message for the calling thread.
  *  - "device" pointers are HIP device memory owned by the caller (e.g. torch
- *    tensors).  The library only borrows them for the duration of the call
- *    and never allocates device memory itself.
+ *    tensors).  The library borrows them for the duration of the call (a
+ *    stream: until wd_stream_end / wd_stream_free returns) and never
+ *    allocates device memory itself; its only device resources are one
+ *    pruning stream per device (created on first use, kept for the process)
+ *    and a few events per chip-wide decode.
  *  - Work is enqueued on the caller's stream; wd_decode / wd_decode_batch
  *    return after the results have been copied to host memory.
  *  - Results are deterministic: identical inputs give identical outputs,

@@ -1,11 +1,14 @@
 """ctypes binding of libwfstdec.so (include/wfstdec.h).
 
 The functions named wd_* mirror the C ABI one to one and only marshal
-arguments.  Graph, decode() and decode_batch() add the bookkeeping a Python
-caller needs: device buffers come from torch (torch is used for device memory
-and streams only), and a decode that reports WD_ECAPACITY is retried once with
-the capacities it reported as needed.  Every step of the decoder runs in the
-library's HIP kernels; if the library is missing this module raises.
+arguments.  Graph, decode(), decode_batch(), Stream and determinize() add the
+bookkeeping a Python caller needs: device buffers come from torch (torch is
+used for device memory and streams only), and a decode that reports
+WD_ECAPACITY is run again with the capacities it reported as needed (growing
+at least fourfold per attempt).  A Graph keeps one workspace for its decodes,
+so decodes on one Graph object must not run from several threads at once.
+Every step of the decoder runs in the library's HIP kernels; if the library
+is missing this module raises.
 """
 from __future__ import annotations
 
