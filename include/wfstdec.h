@@ -277,10 +277,18 @@ void      wd_stream_free(wd_stream* s);
  * input path with the same words (best: lower graph + acoustic total, then
  * the lexicographically smaller string, then the lower graph cost).  An arc's
  * alignment is its part of the path's string; a final state's alignment
- * ends it.  WD_EINVAL for unsorted nodes, dangling links or a cycle;
- * WD_ECAPACITY beyond max_states output states (<= 0: 4M).  Residual
- * weights are kept in double; output states whose residuals differ in their
- * last bits are not merged (the lattice stays deterministic and exact). */
+ * ends it.  beam (>= 0, +inf: none) prunes inside the construction: output
+ * states are built best first (forward cost plus the exact best completion
+ * of their lattice nodes) and a state whose best complete path costs more
+ * than the lattice's best path plus beam is not built, and the subsets
+ * leave out lattice nodes that no path within the beam crosses.  Every word
+ * sequence within the beam is then kept, with its exact best path; a
+ * sequence beyond it may be kept too, with some path of its words beyond
+ * the beam.  State numbers follow the construction order.  WD_EINVAL for unsorted nodes,
+ * dangling links, a cycle or a negative or NaN beam; WD_ECAPACITY beyond
+ * max_states output states (<= 0: 4M).  Residual weights are kept in double;
+ * output states whose residuals differ in their last bits are not merged
+ * (the lattice stays deterministic and exact). */
 typedef struct {
   int32_t src, dst;
   int32_t word;         /* olabel, never 0 */
@@ -297,7 +305,7 @@ typedef struct {
 typedef struct wd_clat wd_clat;
 wd_status wd_lattice_determinize(const wd_lat_arc* arcs, int64_t n_arcs, const wd_lat_node* nodes,
                                  int64_t n_nodes, int32_t start_state, const float* node_final,
-                                 int64_t max_states, wd_clat** out);
+                                 double beam, int64_t max_states, wd_clat** out);
 int32_t wd_clat_states(const wd_clat* c);
 int64_t wd_clat_arcs(const wd_clat* c, const wd_clat_arc** arcs);
 int64_t wd_clat_finals(const wd_clat* c, const wd_clat_final** finals);

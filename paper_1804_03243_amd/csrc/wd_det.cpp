@@ -75,8 +75,31 @@ bool better(double g1, double a1, const Str& s1, double g2, double a2, const Str
 
 bool better(const Elem& x, const Elem& y) { return better(x.g, x.a, x.s, y.g, y.a, y.s); }
 
+// Best completion cost of every node (graph + acoustic + final), by the
+// reverse of the topological order; +inf for a node that reaches no final.
+std::vector<double> completion(const Input& in) {
+  std::vector<int32_t> order((size_t)in.n);
+  for (int32_t u = 0; u < in.n; ++u) order[(size_t)in.rank[u]] = u;
+  std::vector<double> beta((size_t)in.n, INFINITY);
+  for (int32_t h = in.n - 1; h >= 0; --h) {
+    const int32_t u = order[(size_t)h];
+    double b = in.fin[u];
+    for (int64_t k = in.off[u]; k < in.off[u + 1]; ++k) {
+      const InArc& a = in.arcs[k];
+      const double c = a.g + a.a + beta[a.dst];
+      b = c < b ? c : b;
+    }
+    beta[u] = b;
+  }
+  return beta;
+}
+
 // Closure of `m` (input node -> element) under the links without a word.
-void closure(const Input& in, std::unordered_map<int32_t, Elem>& m) {
+// With a finite `limit`, an element whose residual plus its node's best
+// completion exceeds it is neither added nor followed (no path through it
+// is within the beam).
+void closure(const Input& in, std::unordered_map<int32_t, Elem>& m, const std::vector<double>& beta,
+             double limit) {
   using Item = std::pair<int32_t, int32_t>;  // (rank, node)
   std::priority_queue<Item, std::vector<Item>, std::greater<Item>> q;
   for (auto& kv : m) q.push({in.rank[kv.first], kv.first});
@@ -90,6 +113,7 @@ void closure(const Input& in, std::unordered_map<int32_t, Elem>& m) {
     for (int64_t k = in.off[u]; k < in.off[u + 1]; ++k) {
       const InArc& r = in.arcs[k];
       if (r.word != 0) continue;
+      if (e.g + r.g + e.a + r.a + beta[r.dst] > limit) continue;
       Elem c{r.dst, e.g + r.g, e.a + r.a, e.s};
       if (r.ilabel != 0) c.s.push_back(r.ilabel);
       auto it = m.find(r.dst);
@@ -195,12 +219,21 @@ wd_status build_input(const wd_lat_arc* arcs, int64_t n_arcs, const wd_lat_node*
   return WD_OK;
 }
 
+double best_rest(const std::vector<Elem>& S, const std::vector<double>& beta) {
+  double m = INFINITY;
+  for (const Elem& e : S) {
+    const double c = e.g + e.a + beta[e.node];
+    m = c < m ? c : m;
+  }
+  return m;
+}
+
 }  // namespace
 
 extern "C" wd_status wd_lattice_determinize(const wd_lat_arc* arcs, int64_t n_arcs, const wd_lat_node* nodes,
                                             int64_t n_nodes, int32_t start_state, const float* node_final,
-                                            int64_t max_states, wd_clat** out) {
-  if (!out || n_arcs < 0 || n_nodes < 0 || (n_arcs && !arcs) || (n_nodes && !nodes))
+                                            double beam, int64_t max_states, wd_clat** out) {
+  if (!out || n_arcs < 0 || n_nodes < 0 || (n_arcs && !arcs) || (n_nodes && !nodes) || !(beam >= 0.0))
     return wd::fail(WD_EINVAL, "determinize: bad arguments");
   *out = nullptr;
   Input in;
@@ -212,16 +245,38 @@ extern "C" wd_status wd_lattice_determinize(const wd_lat_arc* arcs, int64_t n_ar
     return WD_OK;
   }
   if (max_states <= 0) max_states = 1 << 22;
+  const std::vector<double> beta = completion(in);
+  // Output states are expanded in the order of (forward cost of the best
+  // output path reaching them + best completion of their elements): the
+  // completion cost is exact, so this order never decreases along an arc
+  // and a state's forward cost is final when it is expanded.  With a finite
+  // beam, word links and closure elements whose best complete path costs
+  // more than the best path plus `beam` are left out, so no state beyond
+  // the beam is created and subsets hold only nodes within it; the paths
+  // within the beam are all still there, each with its own best weight.
   std::unordered_map<std::vector<int64_t>, int32_t, KeyHash> ids;
   std::vector<std::vector<Elem>> todo;  // subsets by state id, freed once expanded
+  std::vector<double> fwd;              // forward cost (graph + acoustic) of each state
+  using Item = std::pair<double, int32_t>;
+  std::priority_queue<Item, std::vector<Item>, std::greater<Item>> heap;
+  double cutoff;
   {
     std::unordered_map<int32_t, Elem> m;
     m.emplace(in.start, Elem{in.start, 0.0, 0.0, {}});
-    closure(in, m);
+    const double f0 = beta[in.start];
+    cutoff = f0 + beam;
+    closure(in, m, beta, cutoff);
     todo.push_back(sorted(m));
     ids.emplace(key_of(todo[0]), 0);
+    fwd.push_back(0.0);
+    heap.push({f0, 0});
   }
-  for (int32_t id = 0; id < (int32_t)todo.size(); ++id) {
+  std::vector<char> done(1, 0);
+  while (!heap.empty()) {
+    const int32_t id = heap.top().second;
+    heap.pop();
+    if (done[(size_t)id]) continue;
+    done[(size_t)id] = 1;
     const std::vector<Elem> S = std::move(todo[id]);
     todo[id].clear();
     todo[id].shrink_to_fit();
@@ -240,26 +295,34 @@ extern "C" wd_status wd_lattice_determinize(const wd_lat_arc* arcs, int64_t n_ar
       r->finals.push_back(wd_clat_final{id, (int32_t)fe.s.size(), fe.g, fe.a, (int64_t)r->align.size()});
       r->align.insert(r->align.end(), fe.s.begin(), fe.s.end());
     }
-    // words leaving the set, in increasing order
-    std::vector<int32_t> words;
-    for (const Elem& e : S)
-      for (int64_t k = in.off[e.node]; k < in.off[e.node + 1]; ++k)
-        if (in.arcs[k].word != 0) words.push_back(in.arcs[k].word);
-    std::sort(words.begin(), words.end());
-    words.erase(std::unique(words.begin(), words.end()), words.end());
-    for (int32_t w : words) {
+    // the word links leaving the set, by word (then element and link order);
+    // links that cannot be within the beam are left out
+    const double limit = cutoff - fwd[(size_t)id];
+    std::vector<std::pair<int32_t, std::pair<uint32_t, int64_t>>> out_links;  // (word, (elem, link))
+    for (uint32_t ei = 0; ei < (uint32_t)S.size(); ++ei) {
+      const Elem& e = S[ei];
+      for (int64_t k = in.off[e.node]; k < in.off[e.node + 1]; ++k) {
+        const InArc& a = in.arcs[k];
+        if (a.word != 0 && !(e.g + a.g + e.a + a.a + beta[a.dst] > limit)) out_links.push_back({a.word, {ei, k}});
+      }
+    }
+    std::sort(out_links.begin(), out_links.end());
+    for (size_t q0 = 0; q0 < out_links.size();) {
+      const int32_t w = out_links[q0].first;
+      size_t q1 = q0;
+      while (q1 < out_links.size() && out_links[q1].first == w) ++q1;
       std::unordered_map<int32_t, Elem> m;
-      for (const Elem& e : S)
-        for (int64_t k = in.off[e.node]; k < in.off[e.node + 1]; ++k) {
-          const InArc& a = in.arcs[k];
-          if (a.word != w) continue;
-          Elem c{a.dst, e.g + a.g, e.a + a.a, e.s};
-          if (a.ilabel != 0) c.s.push_back(a.ilabel);
-          auto it = m.find(a.dst);
-          if (it == m.end()) m.emplace(a.dst, std::move(c));
-          else if (better(c, it->second)) it->second = std::move(c);
-        }
-      closure(in, m);
+      for (size_t q = q0; q < q1; ++q) {
+        const Elem& e = S[out_links[q].second.first];
+        const InArc& a = in.arcs[out_links[q].second.second];
+        Elem c{a.dst, e.g + a.g, e.a + a.a, e.s};
+        if (a.ilabel != 0) c.s.push_back(a.ilabel);
+        auto it = m.find(a.dst);
+        if (it == m.end()) m.emplace(a.dst, std::move(c));
+        else if (better(c, it->second)) it->second = std::move(c);
+      }
+      q0 = q1;
+      closure(in, m, beta, limit);
       std::vector<Elem> T = sorted(m);
       // divide by the common part: best weight, longest common string prefix
       const Elem* b = &T[0];
@@ -278,11 +341,17 @@ extern "C" wd_status wd_lattice_determinize(const wd_lat_arc* arcs, int64_t n_ar
         e.a -= a0;
         e.s.erase(e.s.begin(), e.s.begin() + (std::ptrdiff_t)pre);
       }
+      const double fT = fwd[(size_t)id] + (g0 + a0);
+      const double f = fT + best_rest(T, beta);
       std::vector<int64_t> k = key_of(T);
       auto it = ids.find(k);
       int32_t to;
       if (it != ids.end()) {
         to = it->second;
+        if (!done[(size_t)to] && fT < fwd[(size_t)to]) {
+          fwd[(size_t)to] = fT;
+          heap.push({f, to});
+        }
       } else {
         if ((int64_t)todo.size() >= max_states) {
           delete r;
@@ -291,12 +360,20 @@ extern "C" wd_status wd_lattice_determinize(const wd_lat_arc* arcs, int64_t n_ar
         to = (int32_t)todo.size();
         ids.emplace(std::move(k), to);
         todo.push_back(std::move(T));
+        fwd.push_back(fT);
+        done.push_back(0);
+        heap.push({f, to});
       }
       r->arcs.push_back(wd_clat_arc{id, to, w, (int32_t)common.size(), g0, a0, (int64_t)r->align.size()});
       r->align.insert(r->align.end(), common.begin(), common.end());
     }
   }
   r->states = (int32_t)todo.size();
+  std::sort(r->arcs.begin(), r->arcs.end(), [](const wd_clat_arc& x, const wd_clat_arc& y) {
+    return x.src != y.src ? x.src < y.src : x.word < y.word;
+  });
+  std::sort(r->finals.begin(), r->finals.end(),
+            [](const wd_clat_final& x, const wd_clat_final& y) { return x.state < y.state; });
   *out = r;
   return WD_OK;
 }

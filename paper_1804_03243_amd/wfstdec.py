@@ -120,7 +120,7 @@ def lib():
             "wd_stream_end": ([VP, P(VP)], ctypes.c_int),
             "wd_stream_free": ([VP], None),
             "wd_lattice_determinize": ([VP, ctypes.c_int64, VP, ctypes.c_int64, ctypes.c_int32, VP,
-                                        ctypes.c_int64, P(VP)], ctypes.c_int),
+                                        ctypes.c_double, ctypes.c_int64, P(VP)], ctypes.c_int),
             "wd_clat_states": ([VP], ctypes.c_int32),
             "wd_clat_arcs": ([VP, P(VP)], ctypes.c_int64),
             "wd_clat_finals": ([VP, P(VP)], ctypes.c_int64),
@@ -233,7 +233,7 @@ def wd_stream_free(sh: int) -> None:
     lib().wd_stream_free(sh)
 
 
-def wd_lattice_determinize(links, nodes, start_state: int, node_final=None,
+def wd_lattice_determinize(links, nodes, start_state: int, node_final=None, beam: float = float("inf"),
                            max_states: int = 0) -> SimpleNamespace:
     """Host lattice determinisation of (links, nodes) arrays; returns
     states, arcs (CLAT_ARC_DTYPE), finals (CLAT_FINAL_DTYPE) and the
@@ -251,7 +251,8 @@ def wd_lattice_determinize(links, nodes, start_state: int, node_final=None,
     h = ctypes.c_void_p()
     _check(L.wd_lattice_determinize(la.ctypes.data if la.size else None, la.size,
                                     na.ctypes.data if na.size else None, na.size, int(start_state),
-                                    None if nf is None else nf.ctypes.data, int(max_states), ctypes.byref(h)))
+                                    None if nf is None else nf.ctypes.data, float(beam), int(max_states),
+                                    ctypes.byref(h)))
     try:
         out = SimpleNamespace(states=L.wd_clat_states(h))
         for name, acc, dt in (("arcs", L.wd_clat_arcs, CLAT_ARC_DTYPE),
@@ -265,7 +266,8 @@ def wd_lattice_determinize(links, nodes, start_state: int, node_final=None,
     return out
 
 
-def determinize(result, start_state: int = 0, final_weight=None, max_states: int = 0) -> SimpleNamespace:
+def determinize(result, start_state: int = 0, final_weight=None, beam: float = float("inf"),
+                max_states: int = 0) -> SimpleNamespace:
     """The compact lattice of a decode result (this library's or the
     oracle's): the last frame's nodes are final with the graph's final
     weights when the decode used them (stats final_reached), else cost 0."""
@@ -277,7 +279,7 @@ def determinize(result, start_state: int = 0, final_weight=None, max_states: int
         nf[last] = np.asarray(final_weight, np.float32)[nodes["state"][last]]
     else:
         nf[last] = 0.0
-    return wd_lattice_determinize(result.links, nodes, start_state, nf, max_states)
+    return wd_lattice_determinize(result.links, nodes, start_state, nf, beam, max_states)
 
 
 def _copy(ptr, n, dtype):

@@ -171,3 +171,58 @@ def test_errors(wf):
     assert e.value.status == wf.WD_EINVAL
     c = wf.wd_lattice_determinize(links[:0], nodes[:0], 0, nf[:0])
     assert c.states == 0 and len(c.arcs) == 0
+
+
+@pytest.mark.parametrize("beam", [0.0, 0.5, 2.0, 5.0])
+@pytest.mark.parametrize("seed", range(20))
+def test_beam_keeps_every_sequence_within_it(wf, seed, beam):
+    """Pruned determinisation: every word sequence whose best path is within
+    the beam of the best path is kept, with that best path (dyadic inputs:
+    exact); a sequence beyond the beam may appear, with a path beyond it."""
+    g = synth.tiny_graph(seed, dyadic=True, finals=seed % 2 == 1)
+    L = synth.tiny_loglikes(seed, 6 + seed % 5, 4, dyadic=True)
+    try:
+        o = oracle.decode(g, L, 8.0, 0, 5.0)
+    except oracle.OracleError:
+        pytest.skip("no surviving path")
+    s0, fw = g.get("start_state", 0), g.get("final_weight")
+    nf = lp.node_final_costs(o, fw)
+    try:
+        best, _ = lp.best_by_words(o.links, o.nodes, s0, nf)
+    except lp.TooManyPaths:
+        pytest.skip("too many paths to enumerate")
+    c = wf.determinize(o, s0, fw, beam=beam)
+    check_structure(c)
+    got = paths(c)
+    top = min(v[0] + v[1] for v in best.values())
+    within = {w for w, v in best.items() if v[0] + v[1] <= top + beam}
+    assert within <= set(got)
+    for w, v in got.items():
+        if w in within:
+            assert v == best[w], (w, v, best[w])
+        else:
+            assert v[0] + v[1] > top + beam and v[0] + v[1] >= best[w][0] + best[w][1]
+
+
+def test_beam_on_a_longer_lattice(wf):
+    cfg = synth.workload("tiny_10k")
+    g = synth.make_graph(cfg)
+    L = synth.make_loglikes(cfg)
+    o = oracle.decode(g, L, cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    s0, fw = g.get("start_state", 0), g.get("final_weight")
+    c = wf.determinize(o, s0, fw, beam=1.0)
+    check_structure(c)
+    total, words = best_path(c)
+    assert list(words) == list(o.words)
+    assert math.isclose(total, float(o.cost), rel_tol=1e-5, abs_tol=1e-3)
+
+
+def test_beam_errors(wf):
+    d, links, nodes, nf = load_fixture("det_hand_1.json")
+    for beam in (-1.0, float("nan")):
+        with pytest.raises(wf.WdError) as e:
+            wf.wd_lattice_determinize(links, nodes, 0, nf, beam=beam)
+        assert e.value.status == wf.WD_EINVAL
+    # beam 0 on the hand-worked lattice: (10, 11) costs 4.25, (10,) 5.5
+    c = wf.wd_lattice_determinize(links, nodes, 0, nf, beam=0.0)
+    assert set(paths(c)) >= {(10, 11)}
