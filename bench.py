@@ -242,7 +242,10 @@ def host_info() -> dict:
                 break
     except OSError:
         pass
-    return {"nproc": os.cpu_count(), "cpu": model, "gpu": torch.cuda.get_device_name(0)}
+    props = torch.cuda.get_device_properties(0)
+    return {"nproc": os.cpu_count(), "cpu": model, "gpu": torch.cuda.get_device_name(0),
+            "gpu_arch": getattr(props, "gcnArchName", ""), "gpu_cus": props.multi_processor_count,
+            "gpu_mem_gib": round(props.total_memory / 2 ** 30, 1)}
 
 
 def algorithmic_bytes(stats: dict) -> int:
