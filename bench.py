@@ -175,7 +175,51 @@ def determinize_hclg(wfstdec, r, g, T: int, reps: int = 20) -> dict:
             "compact_arcs_per_frame": round(len(c.arcs) / T, 3), "compact_states": int(c.states)}
 
 
-def batch64(wfstdec, graph, steps: int = 3) -> dict:
+_CPU_GRAPH = None
+
+
+def _cpu_init(workload: str) -> None:
+    global _CPU_GRAPH
+    import oracle
+    import synth
+    oracle.build()
+    cfg = synth.workload(workload)
+    _CPU_GRAPH = (cfg, synth.make_graph(cfg))
+
+
+def _cpu_decode(i: int) -> tuple:
+    import oracle
+    import synth
+    cfg, g = _CPU_GRAPH
+    if i < 0:
+        return (0, os.getpid(), 0.0)  # warm-up task: the worker is initialised
+    L = synth.make_loglikes(cfg, i)
+    t0 = time.perf_counter()
+    oracle.decode(g, L, cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    return (int(L.shape[0]), os.getpid(), time.perf_counter() - t0)
+
+
+def cpu_batch_baseline(workload: str, n_utts: int) -> dict:
+    """The CPU oracle on the batch, one utterance per task over a pool of
+    processes (started fresh, they never touch the GPU), one per host core.
+    Throughput = frames / the longest per-process sum of decode times (the
+    log-likelihood generation of each task is not counted)."""
+    import multiprocessing as mp
+    n = os.cpu_count() or 1
+    with mp.get_context("spawn").Pool(n, initializer=_cpu_init, initargs=(workload,)) as pool:
+        pool.map(_cpu_decode, [-1] * n, chunksize=1)
+        res = pool.map(_cpu_decode, range(n_utts), chunksize=1)
+    frames = sum(r[0] for r in res)
+    busy = {}
+    for _, pid, dt in res:
+        busy[pid] = busy.get(pid, 0.0) + dt
+    span = max(busy.values())
+    return {"value": round(frames / span, 1), "unit": "frames/s", "cores": len(busy), "kind": "oracle",
+            "sample": f"all {n_utts} utterances of {workload} ({frames} frames) over {len(busy)} processes; "
+                      f"longest per-process decode time {span:.1f} s, {sum(busy.values()):.1f} s of CPU work"}
+
+
+def batch64(wfstdec, graph, steps: int = 3, cpu: bool = True) -> dict:
     """The 64-utterance batch on the same graph (one workgroup per utterance,
     one launch for the batch): aggregate frames/s and the roofline of the
     batch's k_forward launch.  Algorithmic bytes are summed over the lanes
@@ -210,6 +254,8 @@ def batch64(wfstdec, graph, steps: int = 3) -> dict:
                         "algorithmic_bytes_per_launch": int(nbytes)}}
     del xs
     torch.cuda.empty_cache()
+    if cpu:
+        out["cpu_baseline"] = cpu_batch_baseline("batch64_hclg_5m", len(rs))
     return out
 
 
@@ -357,7 +403,7 @@ def main() -> int:
     if not args.no_extra and workload == WORKLOAD:
         streamed = [stream_hclg(wfstdec, graph, x, cfg, chunk) for chunk in (32, 8)]
         streamed.append(determinize_hclg(wfstdec, r, g, T))
-        streamed.append(batch64(wfstdec, graph))
+        streamed.append(batch64(wfstdec, graph, cpu=not args.no_cpu_baseline))
         del graph, x
         torch.cuda.empty_cache()
         out["other_workloads"] = streamed + [wide_chip(wfstdec, mode=m)
