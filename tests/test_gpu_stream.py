@@ -208,3 +208,40 @@ def test_stream_capacity_fallback(wf, oracle_mod, tiny10k, mode):
     r = s.end()[0]
     assert_same(r, oracle_mod.decode(g, L80, 10.0, 2000, 6.0))
     assert not math.isnan(float(r.cost))
+
+
+def test_concurrent_chip_decodes(wf, oracle_mod, tiny10k):
+    """Chip-wide decodes from two host threads on two HIP streams share the
+    library's pruning stream (each decode orders it with its own events):
+    every result equals the oracle's.  Each thread has its own Graph (a
+    Graph's workspace serves one decode at a time)."""
+    import threading
+    import torch
+    cfg, g, L, _ = tiny10k
+    args = (10.0, 0, 6.0)
+    L1, L2 = L[:150], L[100:300]
+    o1, o2 = oracle_mod.decode(g, L1, *args), oracle_mod.decode(g, L2, *args)
+    graphs = [wf.Graph(g, cfg["P"]), wf.Graph(g, cfg["P"])]
+    xs = [torch.from_numpy(np.ascontiguousarray(a)).to(graphs[0].device) for a in (L1, L2)]
+    print("\n[gpu case] two threads x 3 chip-wide decodes on two streams", flush=True)
+    results, errors = [[], []], []
+
+    def work(k):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                for _ in range(3):
+                    results[k].append(wf.decode(graphs[k], xs[k], *args, mode="chip"))
+        except Exception as e:  # reported below
+            errors.append(e)
+
+    th = [threading.Thread(target=work, args=(k,)) for k in range(2)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    assert not errors, errors
+    for r in results[0]:
+        assert_same(r, o1)
+    for r in results[1]:
+        assert_same(r, o2)
