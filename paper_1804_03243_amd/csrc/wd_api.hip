@@ -159,48 +159,48 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
       L.kept_cap = c.kept;
       L.raw_cap = c.raw;
       L.word_cap = c.words;
-      L.slot = (unsigned long long*)at(slot, 8 * S);
-      L.idx = (uint32_t*)at(idx, 4 * S);
-      L.bitmap = (uint32_t*)at(bitmap, 4 * R.bitmap_words);
-      L.bucket = (uint32_t*)at(bucket, 4 * S);
-      L.touched = (uint32_t*)at(touched, 4 * c.frame);
-      L.surv_state = (uint32_t*)at(surv_state, 4 * c.frame);
-      L.surv_pack = (unsigned long long*)at(surv_pack, 8 * c.frame);
-      L.f_state = (uint32_t*)at(f_state, 4 * F1);
-      L.f_key = (uint32_t*)at(f_key, 4 * F1);
-      L.f_arc = (uint32_t*)at(f_arc, 4 * F1);
-      L.f_edeg = (uint32_t*)at(f_edeg, 4 * F1);
-      L.f_xdeg = (uint32_t*)at(f_xdeg, 4 * F1);
-      L.f_ebeg = (uint32_t*)at(f_ebeg, 4 * F1);
-      L.f_xbeg = (uint32_t*)at(f_xbeg, 4 * F1);
-      L.f_cls = (uint8_t*)at(f_cls, F1);
-      L.cand = (uint4*)at(cand, 16 * c.arcs);
-      L.n_state = (uint32_t*)at(n_state, 4 * c.nodes);
-      L.n_pack = (unsigned long long*)at(n_pack, 8 * c.nodes);
-      L.n_pred = (uint32_t*)at(n_pred, 4 * c.nodes);
-      L.links = (uint4*)at(links, 16 * nlink);
-      L.link_lvl = (uint8_t*)at(link_lvl, nlink);
-      L.node_off = (uint64_t*)at(node_off, 8 * T2);
-      L.link_off = (uint64_t*)at(link_off, 8 * T2);
-      L.link_xoff = (uint64_t*)at(link_xoff, 8 * T2);
-      L.link_end = (uint64_t*)at(link_end, 8 * T2);
-      L.xmask = (uint32_t*)at(xmask, 4 * T2);
-      L.best = (float*)at(best, 4 * T2);
-      L.cutb = (float*)at(cutb, 4 * T2);
-      L.cut = (float*)at(cut, 4 * T2);
-      L.extra_key = (uint32_t*)at(extra_key, 4 * c.nodes);
-      L.le_key = (uint32_t*)at(le_key, 4 * nlink);
-      L.alpha = (double*)at(alpha, 8 * c.nodes);
-      L.beta = (double*)at(beta, 8 * c.nodes);
-      L.used = (uint32_t*)at(used, 4 * R.used_words);
-      L.kept_idx = (uint64_t*)at(kept_idx, 8 * c.kept);
-      L.post = (uint4*)at(post, 16 * c.kept);
-      L.kframe = (uint64_t*)at(kframe, 16 * T2);
-      L.out_links = (OutLink*)at(out_links, sizeof(OutLink) * c.kept);
-      L.out_raw = (OutLink*)at(out_raw, sizeof(OutLink) * c.raw);
-      L.out_nodes = (OutNode*)at(out_nodes, sizeof(OutNode) * (2 * c.kept + 1));
-      L.out_words = (int32_t*)at(out_words, 4 * c.words);
-      L.info = R.info + b;
+      L.slot = (decltype(L.slot))at(slot, 8 * S);
+      L.idx = (decltype(L.idx))at(idx, 4 * S);
+      L.bitmap = (decltype(L.bitmap))at(bitmap, 4 * R.bitmap_words);
+      L.bucket = (decltype(L.bucket))at(bucket, 4 * S);
+      L.touched = (decltype(L.touched))at(touched, 4 * c.frame);
+      L.surv_state = (decltype(L.surv_state))at(surv_state, 4 * c.frame);
+      L.surv_pack = (decltype(L.surv_pack))at(surv_pack, 8 * c.frame);
+      L.f_state = (decltype(L.f_state))at(f_state, 4 * F1);
+      L.f_key = (decltype(L.f_key))at(f_key, 4 * F1);
+      L.f_arc = (decltype(L.f_arc))at(f_arc, 4 * F1);
+      L.f_edeg = (decltype(L.f_edeg))at(f_edeg, 4 * F1);
+      L.f_xdeg = (decltype(L.f_xdeg))at(f_xdeg, 4 * F1);
+      L.f_ebeg = (decltype(L.f_ebeg))at(f_ebeg, 4 * F1);
+      L.f_xbeg = (decltype(L.f_xbeg))at(f_xbeg, 4 * F1);
+      L.f_cls = (decltype(L.f_cls))at(f_cls, F1);
+      L.cand = (decltype(L.cand))at(cand, 16 * c.arcs);
+      L.n_state = (decltype(L.n_state))at(n_state, 4 * c.nodes);
+      L.n_pack = (decltype(L.n_pack))at(n_pack, 8 * c.nodes);
+      L.n_pred = (decltype(L.n_pred))at(n_pred, 4 * c.nodes);
+      L.links = (decltype(L.links))at(links, 16 * nlink);
+      L.link_lvl = (decltype(L.link_lvl))at(link_lvl, nlink);
+      L.node_off = (decltype(L.node_off))at(node_off, 8 * T2);
+      L.link_off = (decltype(L.link_off))at(link_off, 8 * T2);
+      L.link_xoff = (decltype(L.link_xoff))at(link_xoff, 8 * T2);
+      L.link_end = (decltype(L.link_end))at(link_end, 8 * T2);
+      L.xmask = (decltype(L.xmask))at(xmask, 4 * T2);
+      L.best = (decltype(L.best))at(best, 4 * T2);
+      L.cutb = (decltype(L.cutb))at(cutb, 4 * T2);
+      L.cut = (decltype(L.cut))at(cut, 4 * T2);
+      L.extra_key = (decltype(L.extra_key))at(extra_key, 4 * c.nodes);
+      L.le_key = (decltype(L.le_key))at(le_key, 4 * nlink);
+      L.alpha = (decltype(L.alpha))at(alpha, 8 * c.nodes);
+      L.beta = (decltype(L.beta))at(beta, 8 * c.nodes);
+      L.used = (decltype(L.used))at(used, 4 * R.used_words);
+      L.kept_idx = (decltype(L.kept_idx))at(kept_idx, 8 * c.kept);
+      L.post = (decltype(L.post))at(post, 16 * c.kept);
+      L.kframe = (decltype(L.kframe))at(kframe, 16 * T2);
+      L.out_links = (decltype(L.out_links))at(out_links, sizeof(OutLink) * c.kept);
+      L.out_raw = (decltype(L.out_raw))at(out_raw, sizeof(OutLink) * c.raw);
+      L.out_nodes = (decltype(L.out_nodes))at(out_nodes, sizeof(OutNode) * (2 * c.kept + 1));
+      L.out_words = (decltype(L.out_words))at(out_words, 4 * c.words);
+      L.info = (decltype(L.info))(R.info + b);
     }
   }
   return R;
@@ -301,7 +301,7 @@ static wd_status run_setup(wd_stream* run, const wd_graph* g, int32_t B, const f
   run->next.assign((size_t)B, 0);
   run->open = open;
   for (int b = 0; b < B; ++b) {
-    run->lanes[b].ll = ll[b];
+    run->lanes[b].ll = (decltype(run->lanes[b].ll))ll[b];
     run->lanes[b].T = T[b];
     run->lanes[b].t0 = 0;
     run->lanes[b].open = open ? 1 : 0;

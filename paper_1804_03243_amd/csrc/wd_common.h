@@ -137,10 +137,22 @@ struct OutNode {
   float extra;
 };
 
+// Pointers into device memory seen from device code: in the global address
+// space, so that every access through them is a global memory instruction.
+// (A pointer of unknown address space compiles to flat instructions, and a
+// wait for a flat load waits for every load in flight, which would stall the
+// loads the kernels issue a frame ahead.)  Host code sees plain pointers;
+// both views have the same layout.
+#if defined(__HIP_DEVICE_COMPILE__)
+#define WD_GLOBAL __attribute__((address_space(1)))
+#else
+#define WD_GLOBAL
+#endif
+
 // Everything one utterance needs on the device.  Built on the host; lives in
 // the workspace.
 struct LaneDesc {
-  const float* ll;             // T x P log-likelihoods (row t-1 belongs to frame t)
+  const WD_GLOBAL float* ll;             // T x P log-likelihoods (row t-1 belongs to frame t)
   int32_t T;                   // last frame (streaming: the last frame received so far)
   int32_t t0;                  // first frame this launch decodes; > 0 resumes a stream
   int32_t open;                // streaming: more frames may follow
@@ -148,57 +160,57 @@ struct LaneDesc {
   uint64_t frame_cap, cand_cap, node_cap, link_cap, kept_cap, word_cap;
   uint64_t win_cap;            // incremental pruning: links of one raw window slot (0: off)
   // per-frame scratch
-  unsigned long long* slot;    // [S] packed (cost key, arc id); kEmpty between frames
-  uint32_t* idx;               // [S] node id of a state in the current frame / scratch
-  uint32_t* bitmap;            // [ceil(S/32)] zero between frames
-  uint32_t* touched;           // [frame_cap] states touched this frame
-  uint32_t* bucket;            // [S] touched states with epsilon arcs, by level
-  uint32_t* surv_state;        // [frame_cap] tokens within the beam cutoff
-  unsigned long long* surv_pack;
+  WD_GLOBAL unsigned long long* slot;    // [S] packed (cost key, arc id); kEmpty between frames
+  WD_GLOBAL uint32_t* idx;               // [S] node id of a state in the current frame / scratch
+  WD_GLOBAL uint32_t* bitmap;            // [ceil(S/32)] zero between frames
+  WD_GLOBAL uint32_t* touched;           // [frame_cap] states touched this frame
+  WD_GLOBAL uint32_t* bucket;            // [S] touched states with epsilon arcs, by level
+  WD_GLOBAL uint32_t* surv_state;        // [frame_cap] tokens within the beam cutoff
+  WD_GLOBAL unsigned long long* surv_pack;
   // frontier: surviving tokens of the last finished frame, sorted by state
   // (used when a frame has more survivors than the LDS frontier holds)
-  uint32_t* f_state;
-  uint32_t* f_key;             // cost key
-  uint32_t* f_arc;             // predecessor arc
-  uint32_t* f_edeg;            // exclusive prefix of emitting out-degree (+ total)
-  uint32_t* f_xdeg;            // exclusive prefix of epsilon out-degree (+ total)
-  uint32_t* f_ebeg;            // first emitting arc of the state
-  uint32_t* f_xbeg;            // first epsilon arc of the state
-  uint8_t* f_cls;
-  uint4* cand;                 // [cand_cap] emitting candidates {arc, src node, dst, x bits}
+  WD_GLOBAL uint32_t* f_state;
+  WD_GLOBAL uint32_t* f_key;             // cost key
+  WD_GLOBAL uint32_t* f_arc;             // predecessor arc
+  WD_GLOBAL uint32_t* f_edeg;            // exclusive prefix of emitting out-degree (+ total)
+  WD_GLOBAL uint32_t* f_xdeg;            // exclusive prefix of epsilon out-degree (+ total)
+  WD_GLOBAL uint32_t* f_ebeg;            // first emitting arc of the state
+  WD_GLOBAL uint32_t* f_xbeg;            // first epsilon arc of the state
+  WD_GLOBAL uint8_t* f_cls;
+  WD_GLOBAL uint4* cand;                 // [cand_cap] emitting candidates {arc, src node, dst, x bits}
   // history
-  uint32_t* n_state;           // [node_cap]
-  unsigned long long* n_pack;  // [node_cap] (cost key, predecessor arc)
-  uint32_t* n_pred;            // [node_cap] predecessor node
+  WD_GLOBAL uint32_t* n_state;           // [node_cap]
+  WD_GLOBAL unsigned long long* n_pack;  // [node_cap] (cost key, predecessor arc)
+  WD_GLOBAL uint32_t* n_pred;            // [node_cap] predecessor node
   // link store [link_cap + 2*win_cap]: with incremental pruning, the compacted
   // region [0, link_cap) then two raw window slots of win_cap links each
-  uint4* links;                // {arc, src node, dst node, x bits}
-  uint8_t* link_lvl;           // epsilon level of the source (epsilon links)
-  uint64_t* node_off;          // [T+2]
-  uint64_t* link_off;          // [T+2] first link of frame t (emitting run)
-  uint64_t* link_xoff;         // [T+2] first epsilon link of frame t
-  uint64_t* link_end;          // [T+2] one past the last link of frame t
-  uint32_t* xmask;             // [T+2] levels of the epsilon links of frame t (bit 31: 31 or more)
-  float* best;                 // [T+1]
-  float* cutb;                 // [T+1]
-  float* cut;                  // [T+1]
+  WD_GLOBAL uint4* links;                // {arc, src node, dst node, x bits}
+  WD_GLOBAL uint8_t* link_lvl;           // epsilon level of the source (epsilon links)
+  WD_GLOBAL uint64_t* node_off;          // [T+2]
+  WD_GLOBAL uint64_t* link_off;          // [T+2] first link of frame t (emitting run)
+  WD_GLOBAL uint64_t* link_xoff;         // [T+2] first epsilon link of frame t
+  WD_GLOBAL uint64_t* link_end;          // [T+2] one past the last link of frame t
+  WD_GLOBAL uint32_t* xmask;             // [T+2] levels of the epsilon links of frame t (bit 31: 31 or more)
+  WD_GLOBAL float* best;                 // [T+1]
+  WD_GLOBAL float* cutb;                 // [T+1]
+  WD_GLOBAL float* cut;                  // [T+1]
   // lattice pass
-  uint32_t* extra_key;         // [node_cap]
-  uint32_t* le_key;            // [link_cap + 2*win_cap]
-  double* alpha;               // [node_cap]
-  double* beta;                // [node_cap]
-  uint32_t* used;              // [ceil(node_cap/32)+1] lattice-node bitmap
-  uint64_t* kept_idx;          // [kept_cap] kept link ids in link order
-  uint4* post;                 // [kept_cap] kept links for forward-backward:
+  WD_GLOBAL uint32_t* extra_key;         // [node_cap]
+  WD_GLOBAL uint32_t* le_key;            // [link_cap + 2*win_cap]
+  WD_GLOBAL double* alpha;               // [node_cap]
+  WD_GLOBAL double* beta;                // [node_cap]
+  WD_GLOBAL uint32_t* used;              // [ceil(node_cap/32)+1] lattice-node bitmap
+  WD_GLOBAL uint64_t* kept_idx;          // [kept_cap] kept link ids in link order
+  WD_GLOBAL uint4* post;                 // [kept_cap] kept links for forward-backward:
                                //   {src node, dst node, weight bits, -loglike bits | source level}
-  uint64_t* kframe;            // [2*(T+2)] per frame: first kept link, first kept epsilon link
+  WD_GLOBAL uint64_t* kframe;            // [2*(T+2)] per frame: first kept link, first kept epsilon link
   // outputs
-  OutLink* out_links;          // [kept_cap]
-  OutLink* out_raw;            // [raw_cap] every raw link (debug output)
+  WD_GLOBAL OutLink* out_links;          // [kept_cap]
+  WD_GLOBAL OutLink* out_raw;            // [raw_cap] every raw link (debug output)
   uint64_t raw_cap;
-  OutNode* out_nodes;          // [2*kept_cap+1]
-  int32_t* out_words;          // [word_cap]
-  LaneInfo* info;
+  WD_GLOBAL OutNode* out_nodes;          // [2*kept_cap+1]
+  WD_GLOBAL int32_t* out_words;          // [word_cap]
+  WD_GLOBAL LaneInfo* info;
 };
 
 }  // namespace wd

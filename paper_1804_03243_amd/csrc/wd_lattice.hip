@@ -220,18 +220,54 @@ __device__ __forceinline__ double load_fresh(const double* p) {
 
 // A frame's offsets (scalar loads, mostly scalar-cache hits) are read when
 // its items are prefetched, a frame ahead of its processing.
-struct SweepScal {
-  uint64_t n0, n1, k0, k1, x0, x1;
-  uint32_t mask;
+// Offsets of frame u for the sweep, loaded two frames ahead of their use as
+// vector loads: their waits count in issue order with the other loads, so a
+// frame never waits for a load issued for a later one.
+struct SweepFrame {
+  uint64_t n0, n1, p0;  // nodes of frame u: [n0, n1); p0: first node of frame u-1 (n0 for u = 0)
+  uint64_t k0, k1;      // emitting links out of frame u (empty for the last frame)
+  uint64_t x0, x1;      // epsilon links of frame u
+  uint32_t mask;        // their source levels
 };
-__device__ __forceinline__ void sweep_scal(const LaneDesc& L, int t, SweepScal& a) {
-  a.n0 = L.node_off[t];
-  a.n1 = L.node_off[t + 1];
-  a.x0 = L.link_xoff[t];
-  a.x1 = L.link_off[t + 1];
-  a.mask = L.xmask[t];
-  a.k0 = t < L.T ? L.link_off[t + 1] : 0;
-  a.k1 = t < L.T ? L.link_xoff[t + 1] : 0;
+// A zero the compiler cannot see through.  Loads indexed with it are not known
+// to be uniform, so their results stay in vector registers until `uniform`
+// takes them; a load known to be uniform is moved to a scalar register, and
+// waited for, right where it is issued.
+__device__ __forceinline__ uint32_t opaque_zero() {
+  uint32_t z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+  return z;
+}
+__device__ __forceinline__ uint64_t uni64(uint64_t v) {
+  return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
+         (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+}
+
+__device__ __forceinline__ void sweep_frame(const LaneDesc& L, int u, uint32_t z, SweepFrame& f) {
+  const int T = L.T;
+  const uint64_t* no = L.node_off + z;
+  f.n0 = no[u];
+  f.n1 = no[u + 1];
+  f.p0 = no[u > 0 ? u - 1 : 0];
+  f.x0 = L.link_xoff[u + z];
+  f.x1 = L.link_off[u + 1 + z];
+  f.k0 = f.x1;
+  // the last frame's (empty) emitting run ends where it starts
+  f.k1 = (u < T ? &L.link_xoff[u + 1] : &L.link_off[T + 1])[z];
+  f.mask = L.xmask[u + z];
+}
+// The frame's offsets in scalar registers (their loads must have arrived).
+__device__ __forceinline__ SweepFrame uniform(const SweepFrame& f) {
+  SweepFrame u;
+  u.n0 = uni64(f.n0);
+  u.n1 = uni64(f.n1);
+  u.p0 = uni64(f.p0);
+  u.k0 = uni64(f.k0);
+  u.k1 = uni64(f.k1);
+  u.x0 = uni64(f.x0);
+  u.x1 = u.k0;
+  u.mask = __builtin_amdgcn_readfirstlane(f.mask);
+  return u;
 }
 
 // extra(link) = extra(dst) + (x - cost(dst)) into le_key; extra(src) = min.
@@ -256,12 +292,21 @@ struct SweepOne {
   uint4 e, x;
 };
 
-__device__ __forceinline__ void sweep_one(const LaneDesc& L, const SweepScal& a, uint32_t tid, SweepOne& it) {
-  if (tid < a.k1 - a.k0) it.e = L.links[a.k0 + tid];
-  if (tid < a.x1 - a.x0) {
-    it.x = L.links[a.x0 + tid];
-    it.lvl = L.link_lvl[a.x0 + tid];
-  }
+// Index base + i when i < n, else some valid index (base + n - 1, or 0 for an
+// empty range: every array holds at least one element).  Prefetches load
+// unconditionally so that no merge copy waits for them.
+__device__ __forceinline__ uint64_t safe_idx(uint64_t base, uint64_t i, uint64_t n) {
+  return n ? base + (i < n ? i : n - 1) : 0;
+}
+
+// Links of frame u for this thread and the cost key of its node of frame
+// u-1 (used only where that node exists).
+__device__ __forceinline__ void sweep_one(const LaneDesc& L, const SweepFrame& f, uint32_t tid, SweepOne& it) {
+  it.e = L.links[safe_idx(f.k0, tid, f.k1 - f.k0)];
+  const uint64_t kx = safe_idx(f.x0, tid, f.x1 - f.x0);
+  it.x = L.links[kx];
+  it.lvl = L.link_lvl[kx];
+  it.c = (uint32_t)(L.n_pack[safe_idx(f.p0, tid - 64, tid >= 64 ? f.n0 - f.p0 : 0)] >> 32);
 }
 
 // Extra costs (+inf, or the final extra cost for the last frame) and costs
@@ -269,25 +314,27 @@ __device__ __forceinline__ void sweep_one(const LaneDesc& L, const SweepScal& a,
 // of node `first`, loaded ahead (kNoKeyAhead: load it here).
 constexpr uint32_t kNoKeyAhead = 0u;
 __device__ __forceinline__ void sweep_init(const LaneDesc& L, const DevGraph& g, LatShared& sh, int t,
-                                           const SweepScal& a, uint32_t first, uint32_t stride, bool final_used,
+                                           const SweepFrame& a, uint32_t first, uint32_t stride, bool final_used,
                                            float best_total, uint32_t c0) {
   const uint64_t n0 = a.n0;
   const uint32_t nt = (uint32_t)(a.n1 - n0), buf = (uint32_t)t % 3u;
-  const bool win = nt <= kWin;
-  uint32_t* ex = win ? sh.w.p.ex[buf] : L.extra_key + n0;
-  for (uint32_t i = first; i < nt; i += stride) {
-    const float c = (i == first && c0 != kNoKeyAhead) ? key_cost(c0) : node_cost(L, n0 + i);
-    uint32_t e = kInfKey;
-    if (t == L.T) {
-      const float F = final_used ? canon(c + g.final_w[L.n_state[n0 + i]]) : c;
-      if (F < INFINITY) e = cost_key(F - best_total);
+  auto init = [&](uint32_t* ex, float* cw) {
+    for (uint32_t i = first; i < nt; i += stride) {
+      const float c = (i == first && c0 != kNoKeyAhead) ? key_cost(c0) : node_cost(L, n0 + i);
+      uint32_t e = kInfKey;
+      if (t == L.T) {
+        const float F = final_used ? canon(c + g.final_w[L.n_state[n0 + i]]) : c;
+        if (F < INFINITY) e = cost_key(F - best_total);
+      }
+      ex[i] = e;
+      if (cw) cw[i] = c;
     }
-    ex[i] = e;
-    if (win) sh.w.p.cost[buf][i] = c;
-  }
+  };
+  if (nt <= kWin) init(sh.w.p.ex[buf], sh.w.p.cost[buf]);
+  else init(L.extra_key + n0, nullptr);
 }
 
-__device__ __forceinline__ void sweep_writeback(const LaneDesc& L, LatShared& sh, int t, const SweepScal& a,
+__device__ __forceinline__ void sweep_writeback(const LaneDesc& L, LatShared& sh, int t, const SweepFrame& a,
                                                 uint32_t first, uint32_t stride) {
   const uint32_t nt = (uint32_t)(a.n1 - a.n0);
   if (nt > kWin) return;  // relaxed in device memory directly
@@ -295,43 +342,41 @@ __device__ __forceinline__ void sweep_writeback(const LaneDesc& L, LatShared& sh
   for (uint32_t i = first; i < nt; i += stride) L.extra_key[a.n0 + i] = ex[i];
 }
 
-// Frame t: `cur` holds this thread's links of frame t (loaded during frame
-// t+1) and the cost key of its node of frame t-1 (loaded during t+1); frame
-// t-1's links and frame t-2's node cost are loaded into `nxt` now.  The
-// caller alternates two sets, so no register with a load in flight is copied.
+// Frame t.  sp, sa, sn: offsets of frames t+1, t and t-1 (t+1 unused for the
+// last frame); those of frame t-2 are loaded into snn now.  cur: this
+// thread's links of frame t and its node cost of frame t-1, loaded during
+// frame t+1; those of frame t-1 (and t-2) are loaded into nxt now.  The
+// caller rotates the sets, so no register with a load in flight is copied.
 __device__ __forceinline__ void sweep_step(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t tid, int t,
-                                           bool final_used, float best_total, const SweepOne& cur,
-                                           SweepOne& nxt) {
+                                           bool final_used, float best_total, const SweepFrame& sp_v,
+                                           const SweepFrame& sa_v, const SweepFrame& sn_v, SweepFrame& snn,
+                                           const SweepOne& cur, SweepOne& nxt, uint32_t z) {
   const int T = L.T;
-  SweepScal sa, sp{}, sn{};
-  sweep_scal(L, t, sa);
-  if (t < T) sweep_scal(L, t + 1, sp);
-  if (t > 0) {
-    sweep_scal(L, t - 1, sn);
-    sweep_one(L, sn, tid, nxt);
-  }
-  nxt.c = kNoKeyAhead;
-  if (t > 1 && tid >= 64) {
-    const uint64_t m0 = L.node_off[t - 2], m1 = L.node_off[t - 1];
-    if (tid - 64 < m1 - m0) nxt.c = (uint32_t)(L.n_pack[m0 + tid - 64] >> 32);
-  }
+  const SweepFrame sp = uniform(sp_v), sa = uniform(sa_v), sn = uniform(sn_v);
+  sweep_frame(L, t > 1 ? t - 2 : 0, z, snn);
+  sweep_one(L, sn, tid, nxt);
   const uint64_t n0 = sa.n0, n1 = sa.n1;
   const uint32_t buf = (uint32_t)t % 3u;
   const bool win = n1 - n0 <= kWin;
-  uint32_t* ex = win ? sh.w.p.ex[buf] : L.extra_key + n0;
-  float* cw = win ? sh.w.p.cost[buf] : nullptr;
+  // Each relaxation is written once per kind of window (LDS, device memory),
+  // so that LDS windows are addressed as LDS: through a pointer that may be
+  // either, every access would wait for all loads in flight.
   if (sa.k1 > sa.k0) {
     const uint64_t m0 = n1;
     const bool wn = sp.n1 - m0 <= kWin;
     const uint32_t nb = (uint32_t)(t + 1) % 3u;
-    const uint32_t* exn = wn ? sh.w.p.ex[nb] : L.extra_key + m0;
-    const float* cn = wn ? sh.w.p.cost[nb] : nullptr;
-    if (sa.k0 + tid < sa.k1) sweep_relax(L, sa.k0 + tid, cur.e, exn, cn, m0, ex, n0);
-    for (uint64_t k = sa.k0 + tid + kLT; k < sa.k1; k += kLT) sweep_relax(L, k, L.links[k], exn, cn, m0, ex, n0);
+    auto emitting = [&](const uint32_t* exn, const float* cn, uint32_t* ex) {
+      if (sa.k0 + tid < sa.k1) sweep_relax(L, sa.k0 + tid, cur.e, exn, cn, m0, ex, n0);
+      for (uint64_t k = sa.k0 + tid + kLT; k < sa.k1; k += kLT) sweep_relax(L, k, L.links[k], exn, cn, m0, ex, n0);
+    };
+    if (win && wn) emitting(sh.w.p.ex[nb], sh.w.p.cost[nb], sh.w.p.ex[buf]);
+    else
+      emitting(wn ? sh.w.p.ex[nb] : L.extra_key + m0, wn ? sh.w.p.cost[nb] : nullptr,
+               win ? sh.w.p.ex[buf] : L.extra_key + n0);
   }
   __syncthreads();
   if (tid < 64) {
-    if (sa.x1 > sa.x0)
+    auto epsilon = [&](uint32_t* ex, const float* cw) {
       for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
         if (!level_present(sa.mask, (uint32_t)lvl)) continue;
         if (sa.x0 + tid < sa.x1 && cur.lvl == (uint32_t)lvl) sweep_relax(L, sa.x0 + tid, cur.x, ex, cw, n0, ex, n0);
@@ -339,6 +384,11 @@ __device__ __forceinline__ void sweep_step(const LaneDesc& L, const DevGraph& g,
           if (L.link_lvl[k] == (uint8_t)lvl) sweep_relax(L, k, L.links[k], ex, cw, n0, ex, n0);
         wave_sync();
       }
+    };
+    if (sa.x1 > sa.x0) {
+      if (win) epsilon(sh.w.p.ex[buf], sh.w.p.cost[buf]);
+      else epsilon(L.extra_key + n0, nullptr);
+    }
   } else {
     if (t < T) sweep_writeback(L, sh, t + 1, sp, tid - 64, kLT - 64);
     if (t > 0) sweep_init(L, g, sh, t - 1, sn, tid - 64, kLT - 64, final_used, best_total, cur.c);
@@ -346,31 +396,33 @@ __device__ __forceinline__ void sweep_step(const LaneDesc& L, const DevGraph& g,
   __syncthreads();
 }
 
-// Backward extra-cost sweep over every frame.
+// Backward extra-cost sweep over every frame: four sets of frame offsets and
+// two of links in rotation (a loop of four frames, then up to three more).
 __device__ __forceinline__ void sweep_block(const LaneDesc& L, const DevGraph& g, LatShared& sh,
                                             uint32_t tid, bool final_used, float best_total) {
   const int T = L.T;
-  SweepOne x{}, y{};
-  {
-    SweepScal s0;
-    sweep_scal(L, T, s0);
-    sweep_one(L, s0, tid, x);
-    sweep_init(L, g, sh, T, s0, tid, kLT, final_used, best_total, kNoKeyAhead);
-    // node cost of frame T-1 for the first step's initialisation
-    x.c = kNoKeyAhead;
-    if (T > 0 && tid >= 64) {
-      const uint64_t m0 = L.node_off[T - 1], m1 = L.node_off[T];
-      if (tid - 64 < m1 - m0) x.c = (uint32_t)(L.n_pack[m0 + tid - 64] >> 32);
-    }
-  }
+  const uint32_t z = opaque_zero();
+  SweepFrame A{}, B, C, D;
+  SweepOne x, y;
+  sweep_frame(L, T, z, B);
+  sweep_frame(L, T > 0 ? T - 1 : 0, z, C);
+  const SweepFrame fT = uniform(B);
+  sweep_one(L, fT, tid, x);
+  sweep_init(L, g, sh, T, fT, tid, kLT, final_used, best_total, kNoKeyAhead);
   __syncthreads();
-  for (int t = T; t >= 0; t -= 2) {
-    sweep_step(L, g, sh, tid, t, final_used, best_total, x, y);
-    if (t >= 1) sweep_step(L, g, sh, tid, t - 1, final_used, best_total, y, x);
+  int t = T;
+  for (; t >= 3; t -= 4) {
+    sweep_step(L, g, sh, tid, t, final_used, best_total, A, B, C, D, x, y, z);
+    sweep_step(L, g, sh, tid, t - 1, final_used, best_total, B, C, D, A, y, x, z);
+    sweep_step(L, g, sh, tid, t - 2, final_used, best_total, C, D, A, B, x, y, z);
+    sweep_step(L, g, sh, tid, t - 3, final_used, best_total, D, A, B, C, y, x, z);
   }
-  SweepScal s0;
-  sweep_scal(L, 0, s0);
-  sweep_writeback(L, sh, 0, s0, tid, kLT);
+  if (t >= 0) sweep_step(L, g, sh, tid, t, final_used, best_total, A, B, C, D, x, y, z);
+  if (t >= 1) sweep_step(L, g, sh, tid, t - 1, final_used, best_total, B, C, D, A, y, x, z);
+  if (t >= 2) sweep_step(L, g, sh, tid, t - 2, final_used, best_total, C, D, A, B, x, y, z);
+  SweepFrame f0;
+  sweep_frame(L, 0, z, f0);
+  sweep_writeback(L, sh, 0, uniform(f0), tid, kLT);
 }
 
 // Kept link j for the forward-backward pass: {src node, dst node, graph cost
@@ -403,188 +455,216 @@ __device__ __forceinline__ void post_tail(const LaneDesc& L, uint64_t j0, uint64
   }
 }
 
-struct PostScal {
-  uint64_t n0, n1, m0, m1, e0, e1, x0, x1;
-  uint32_t mask;
+// Offsets of frame u for a posterior pass, loaded two frames ahead of their
+// use like the sweep's.
+struct PostFrame {
+  uint64_t n0, n1;  // nodes of frame u
+  uint64_t m0, m1;  // nodes of the frame the emitting links come from (alpha: u-1) or go to (beta: u+1)
+  uint64_t e0, e1;  // kept emitting links into u (alpha) or out of u (beta)
+  uint64_t x0, x1;  // kept epsilon links of u
+  uint32_t mask;    // their source levels
 };
 struct PostItems {
   uint4 e[kAhead], x[kAhead];
   float fw[kAhead];
 };
 
-// Frame t of the alpha pass: emitting kept links into t (from t-1), epsilon
-// kept links of t.
-__device__ __forceinline__ void alpha_scal(const LaneDesc& L, int t, PostScal& a) {
-  a.n0 = L.node_off[t];
-  a.n1 = L.node_off[t + 1];
-  a.m0 = t > 0 ? L.node_off[t - 1] : 0;
-  a.e0 = L.kframe[2 * t];
-  a.e1 = L.kframe[2 * t + 1];
-  a.x0 = a.e1;
-  a.x1 = L.kframe[2 * t + 2];
-  a.mask = L.xmask[t];
+__device__ __forceinline__ PostFrame uniform(const PostFrame& f) {
+  PostFrame u;
+  u.n0 = uni64(f.n0);
+  u.n1 = uni64(f.n1);
+  u.m0 = uni64(f.m0);
+  u.m1 = uni64(f.m1);
+  u.e0 = uni64(f.e0);
+  u.e1 = uni64(f.e1);
+  u.x0 = uni64(f.x0);
+  u.x1 = uni64(f.x1);
+  u.mask = __builtin_amdgcn_readfirstlane(f.mask);
+  return u;
 }
 
-// Frame t of the beta pass: emitting kept links out of t (into t+1), epsilon
-// kept links of t.
-__device__ __forceinline__ void beta_scal(const LaneDesc& L, int t, PostScal& a) {
+// Frame u of the alpha pass: emitting kept links into u (from u-1), epsilon
+// kept links of u.
+__device__ __forceinline__ void alpha_frame(const LaneDesc& L, int u, uint32_t z, PostFrame& f) {
+  const uint64_t* no = L.node_off + z;
+  const uint64_t* kf = L.kframe + z;
+  f.n0 = no[u];
+  f.n1 = no[u + 1];
+  f.m0 = no[u > 0 ? u - 1 : 0];
+  f.m1 = f.n0;
+  f.e0 = kf[2 * u];
+  f.e1 = kf[2 * u + 1];
+  f.x0 = f.e1;
+  f.x1 = kf[2 * u + 2];
+  f.mask = L.xmask[u + z];
+}
+
+// Frame u of the beta pass: emitting kept links out of u (into u+1), epsilon
+// kept links of u.
+__device__ __forceinline__ void beta_frame(const LaneDesc& L, int u, uint32_t z, PostFrame& f) {
   const int T = L.T;
-  a.n0 = L.node_off[t];
-  a.n1 = L.node_off[t + 1];
-  a.m0 = t < T ? L.node_off[t + 1] : 0;
-  a.m1 = t < T ? L.node_off[t + 2] : 0;
-  a.e0 = t < T ? L.kframe[2 * t + 2] : 0;
-  a.e1 = t < T ? L.kframe[2 * t + 3] : 0;
-  a.x0 = L.kframe[2 * t + 1];
-  a.x1 = L.kframe[2 * t + 2];
-  a.mask = L.xmask[t];
+  const uint64_t* no = L.node_off + z;
+  const uint64_t* kf = L.kframe + z;
+  f.n0 = no[u];
+  f.n1 = no[u + 1];
+  f.m0 = f.n1;
+  f.m1 = no[u < T ? u + 2 : u + 1];
+  f.x0 = kf[2 * u + 1];
+  f.x1 = kf[2 * u + 2];
+  f.e0 = f.x1;
+  f.e1 = kf[u < T ? 2 * u + 3 : 2 * u + 2];  // none out of the last frame
+  f.mask = L.xmask[u + z];
 }
 
-// Items of a frame; `fin`: the last frame of the beta pass (final weights).
+// Kept links of a frame for this lane (loaded unconditionally, like the
+// sweep's links); `fin`: also the final weights of the frame's first nodes
+// (the last frame of the beta pass).
 template <int GS>
-__device__ __forceinline__ void post_items(const LaneDesc& L, const DevGraph& g, const PostScal& a, uint32_t lane,
+__device__ __forceinline__ void post_items(const LaneDesc& L, const DevGraph& g, const PostFrame& a, uint32_t lane,
                                            bool fin, PostItems& it) {
 #pragma unroll
   for (int q = 0; q < kAhead; ++q) {
     const uint64_t i = lane + (uint64_t)GS * q;
-    if (i < a.e1 - a.e0) it.e[q] = post_link(L, a.e0 + i);
-    if (i < a.x1 - a.x0) it.x[q] = post_link(L, a.x0 + i);
+    it.e[q] = post_link(L, safe_idx(a.e0, i, a.e1 - a.e0));
+    it.x[q] = post_link(L, safe_idx(a.x0, i, a.x1 - a.x0));
     if (fin && i < a.n1 - a.n0) it.fw[q] = g.final_w[L.n_state[a.n0 + i]];
   }
 }
 
-// Frame t of the alpha pass on a group of GS threads (items of t in `cur`; those of
-// t+1 are loaded into `nxt`).  `swept`: device-memory alpha is +inf already.
+// Frame t of the alpha pass on a group of GS threads.  sa, sn: offsets of
+// frames t and t+1; those of t+2 are loaded into snn now.  cur: kept links
+// of frame t (loaded during t-1); those of t+1 are loaded into nxt now.
+// `swept`: device-memory alpha is +inf already.
 template <int GS>
 __device__ __forceinline__ void alpha_step(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
-                                           int t, bool swept, uint64_t start_node, const PostItems& cur,
-                                           PostItems& nxt) {
+                                           int t, bool swept, uint64_t start_node, const PostFrame& sa_v,
+                                           const PostFrame& sn_v, PostFrame& snn, const PostItems& cur,
+                                           PostItems& nxt, uint32_t z) {
   const int T = L.T;
-  PostScal pa;
-  alpha_scal(L, t, pa);
-  if (t < T) {
-    PostScal pb;
-    alpha_scal(L, t + 1, pb);
-    post_items<GS>(L, g, pb, lane, false, nxt);
-  }
-  const uint64_t n0 = pa.n0, n1 = pa.n1;
+  const PostFrame pa = uniform(sa_v), pn = uniform(sn_v);
+  alpha_frame(L, t + 2 <= T ? t + 2 : T, z, snn);
+  post_items<GS>(L, g, pn, lane, false, nxt);
+  const uint64_t n0 = pa.n0, n1 = pa.n1, m0 = pa.m0;
   const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
-  const bool win = nt <= kWin;
-  double* a = win ? sh.w.ab.a[buf] : L.alpha + n0;
-  if (win || !swept) {
-    for (uint32_t i = lane; i < nt; i += GS) a[i] = (n0 + i == start_node) ? 0.0 : INFINITY;
-  } else if (lane == 0 && start_node >= n0 && start_node < n1) {
-    a[start_node - n0] = 0.0;  // the rest is +inf already
-  }
-  group_sync<GS>();
-  if (pa.e1 > pa.e0) {
-    const uint64_t m0 = pa.m0;
-    const bool wp = n0 - m0 <= kWin;
-    const double* ap = wp ? sh.w.ab.a[buf ^ 1u] : L.alpha + m0;
-    auto emit = [&](uint4 l) {
-      const double av = wp ? ap[l.x - m0] : load_fresh(&ap[l.x - m0]);
-      atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w));
-    };
-#pragma unroll
-    for (int q = 0; q < kAhead; ++q)
-      if (pa.e0 + lane + (uint64_t)GS * q < pa.e1) emit(cur.e[q]);
-    post_tail<GS>(L, pa.e0, pa.e1, lane, emit);
+  const bool win = nt <= kWin, wp = n0 - m0 <= kWin;
+  // written once per kind of window, as in the sweep
+  auto frame = [&](double* a, const double* ap, bool lds_a, bool lds_ap) {
+    if (lds_a || !swept) {
+      for (uint32_t i = lane; i < nt; i += GS) a[i] = (n0 + i == start_node) ? 0.0 : INFINITY;
+    } else if (lane == 0 && start_node >= n0 && start_node < n1) {
+      a[start_node - n0] = 0.0;  // the rest is +inf already
+    }
     group_sync<GS>();
-  }
-  if (pa.x1 > pa.x0)
-    for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
-      if (!level_present(pa.mask, lvl)) continue;
-      auto eps = [&](uint4 l) {
-        if (l.w != lvl) return;
-        const double av = win ? a[l.x - n0] : load_fresh(&a[l.x - n0]);
-        atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z));
+    if (pa.e1 > pa.e0) {
+      auto emit = [&](uint4 l) {
+        const double av = lds_ap ? ap[l.x - m0] : load_fresh(&ap[l.x - m0]);
+        atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w));
       };
 #pragma unroll
       for (int q = 0; q < kAhead; ++q)
-        if (pa.x0 + lane + (uint64_t)GS * q < pa.x1) eps(cur.x[q]);
-      post_tail<GS>(L, pa.x0, pa.x1, lane, eps);
+        if (pa.e0 + lane + (uint64_t)GS * q < pa.e1) emit(cur.e[q]);
+      post_tail<GS>(L, pa.e0, pa.e1, lane, emit);
       group_sync<GS>();
     }
-  if (win)
-    for (uint32_t i = lane; i < nt; i += GS) L.alpha[n0 + i] = a[i];
+    if (pa.x1 > pa.x0)
+      for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
+        if (!level_present(pa.mask, lvl)) continue;
+        auto eps = [&](uint4 l) {
+          if (l.w != lvl) return;
+          const double av = lds_a ? a[l.x - n0] : load_fresh(&a[l.x - n0]);
+          atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z));
+        };
+#pragma unroll
+        for (int q = 0; q < kAhead; ++q)
+          if (pa.x0 + lane + (uint64_t)GS * q < pa.x1) eps(cur.x[q]);
+        post_tail<GS>(L, pa.x0, pa.x1, lane, eps);
+        group_sync<GS>();
+      }
+    if (lds_a)
+      for (uint32_t i = lane; i < nt; i += GS) L.alpha[n0 + i] = a[i];
+  };
+  if (win && wp) frame(sh.w.ab.a[buf], sh.w.ab.a[buf ^ 1u], true, true);
+  else frame(win ? sh.w.ab.a[buf] : L.alpha + n0, wp ? sh.w.ab.a[buf ^ 1u] : L.alpha + m0, win, wp);
 }
 
 // alpha over every frame, ascending; epsilon links of a frame by source
-// level, on GS threads.
+// level, on GS threads.  The look-ahead sets move down at the end of a step,
+// when their loads (issued at its start) have had the step to arrive.
 template <int GS>
 __device__ __forceinline__ void alpha_wave(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
                                            bool swept, uint64_t start_node) {
   const int T = L.T;
-  PostItems x{}, y{};
-  {
-    PostScal p0;
-    alpha_scal(L, 0, p0);
-    post_items<GS>(L, g, p0, lane, false, x);
-  }
-  for (int t = 0; t <= T; t += 2) {
-    alpha_step<GS>(L, g, sh, lane, t, swept, start_node, x, y);
-    if (t + 1 <= T) alpha_step<GS>(L, g, sh, lane, t + 1, swept, start_node, y, x);
+  const uint32_t z = opaque_zero();
+  PostFrame sa, sn, snn;
+  PostItems cur{}, nxt{};
+  alpha_frame(L, 0, z, sa);
+  alpha_frame(L, T >= 1 ? 1 : 0, z, sn);
+  post_items<GS>(L, g, uniform(sa), lane, false, cur);
+  for (int t = 0; t <= T; ++t) {
+    alpha_step<GS>(L, g, sh, lane, t, swept, start_node, sa, sn, snn, cur, nxt, z);
+    sa = sn;
+    sn = snn;
+    cur = nxt;
   }
 }
 
-// Frame t of the beta pass on a group of GS threads (items of t in `cur`; those of
-// t-1 are loaded into `nxt`).
+// Frame t of the beta pass on a group of GS threads.  sa, sn: offsets of
+// frames t and t-1; those of t-2 are loaded into snn now.  cur: kept links
+// of frame t (loaded during t+1); those of t-1 are loaded into nxt now.
 template <int GS>
 __device__ __forceinline__ void beta_step(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
-                                          int t, bool swept, bool final_used, const PostItems& cur, PostItems& nxt) {
+                                          int t, bool swept, bool final_used, const PostFrame& sa_v,
+                                          const PostFrame& sn_v, PostFrame& snn, const PostItems& cur,
+                                          PostItems& nxt, uint32_t z) {
   const int T = L.T;
-  PostScal pa;
-  beta_scal(L, t, pa);
-  if (t > 0) {
-    PostScal pb;
-    beta_scal(L, t - 1, pb);
-    post_items<GS>(L, g, pb, lane, false, nxt);
-  }
-  const uint64_t n0 = pa.n0, n1 = pa.n1;
+  const PostFrame pa = uniform(sa_v), pn = uniform(sn_v);
+  beta_frame(L, t > 1 ? t - 2 : 0, z, snn);
+  post_items<GS>(L, g, pn, lane, false, nxt);
+  const uint64_t n0 = pa.n0, n1 = pa.n1, m0 = pa.m0;
   const uint32_t nt = (uint32_t)(n1 - n0), buf = (uint32_t)t & 1u;
-  const bool win = nt <= kWin;
-  double* b = win ? sh.w.ab.b[buf] : L.beta + n0;
-  if (win || !swept || t == T) {
+  const bool win = nt <= kWin, wn = pa.m1 - m0 <= kWin;
+  auto frame = [&](double* b, const double* bn, bool lds_b, bool lds_bn) {
+    if (lds_b || !swept || t == T) {
 #pragma unroll
-    for (int q = 0; q <= kAhead; ++q)
-      for (uint32_t i = lane + (uint32_t)(GS * q); i < nt; i += (q < kAhead ? nt : (uint32_t)GS)) {
-        double v = INFINITY;
-        if (t == T)
-          v = final_used ? (double)(q < kAhead ? cur.fw[q < kAhead ? q : 0] : g.final_w[L.n_state[n0 + i]]) : 0.0;
-        b[i] = v;
-      }
-  }
-  group_sync<GS>();
-  if (pa.e1 > pa.e0) {
-    const uint64_t m0 = pa.m0;
-    const bool wn = pa.m1 - m0 <= kWin;
-    const double* bn = wn ? sh.w.ab.b[buf ^ 1u] : L.beta + m0;
-    auto emit = [&](uint4 l) {
-      const double bv = wn ? bn[l.y - m0] : load_fresh(&bn[l.y - m0]);
-      atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w) + bv);
-    };
-#pragma unroll
-    for (int q = 0; q < kAhead; ++q)
-      if (pa.e0 + lane + (uint64_t)GS * q < pa.e1) emit(cur.e[q]);
-    post_tail<GS>(L, pa.e0, pa.e1, lane, emit);
+      for (int q = 0; q <= kAhead; ++q)
+        for (uint32_t i = lane + (uint32_t)(GS * q); i < nt; i += (q < kAhead ? nt : (uint32_t)GS)) {
+          double v = INFINITY;
+          if (t == T)
+            v = final_used ? (double)(q < kAhead ? cur.fw[q < kAhead ? q : 0] : g.final_w[L.n_state[n0 + i]]) : 0.0;
+          b[i] = v;
+        }
+    }
     group_sync<GS>();
-  }
-  if (pa.x1 > pa.x0)
-    for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
-      if (!level_present(pa.mask, (uint32_t)lvl)) continue;
-      auto eps = [&](uint4 l) {
-        if (l.w != (uint32_t)lvl) return;
-        const double bv = win ? b[l.y - n0] : load_fresh(&b[l.y - n0]);
-        atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + bv);
+    if (pa.e1 > pa.e0) {
+      auto emit = [&](uint4 l) {
+        const double bv = lds_bn ? bn[l.y - m0] : load_fresh(&bn[l.y - m0]);
+        atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w) + bv);
       };
 #pragma unroll
       for (int q = 0; q < kAhead; ++q)
-        if (pa.x0 + lane + (uint64_t)GS * q < pa.x1) eps(cur.x[q]);
-      post_tail<GS>(L, pa.x0, pa.x1, lane, eps);
+        if (pa.e0 + lane + (uint64_t)GS * q < pa.e1) emit(cur.e[q]);
+      post_tail<GS>(L, pa.e0, pa.e1, lane, emit);
       group_sync<GS>();
     }
-  if (win)
-    for (uint32_t i = lane; i < nt; i += GS) L.beta[n0 + i] = b[i];
+    if (pa.x1 > pa.x0)
+      for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
+        if (!level_present(pa.mask, (uint32_t)lvl)) continue;
+        auto eps = [&](uint4 l) {
+          if (l.w != (uint32_t)lvl) return;
+          const double bv = lds_b ? b[l.y - n0] : load_fresh(&b[l.y - n0]);
+          atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + bv);
+        };
+#pragma unroll
+        for (int q = 0; q < kAhead; ++q)
+          if (pa.x0 + lane + (uint64_t)GS * q < pa.x1) eps(cur.x[q]);
+        post_tail<GS>(L, pa.x0, pa.x1, lane, eps);
+        group_sync<GS>();
+      }
+    if (lds_b)
+      for (uint32_t i = lane; i < nt; i += GS) L.beta[n0 + i] = b[i];
+  };
+  if (win && wn) frame(sh.w.ab.b[buf], sh.w.ab.b[buf ^ 1u], true, true);
+  else frame(win ? sh.w.ab.b[buf] : L.beta + n0, wn ? sh.w.ab.b[buf ^ 1u] : L.beta + m0, win, wn);
 }
 
 // beta over every frame, descending; epsilon links of a frame from the
@@ -593,15 +673,17 @@ template <int GS>
 __device__ __forceinline__ void beta_wave(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
                                           bool swept, bool final_used) {
   const int T = L.T;
-  PostItems x{}, y{};
-  {
-    PostScal p0;
-    beta_scal(L, T, p0);
-    post_items<GS>(L, g, p0, lane, final_used, x);
-  }
-  for (int t = T; t >= 0; t -= 2) {
-    beta_step<GS>(L, g, sh, lane, t, swept, final_used, x, y);
-    if (t >= 1) beta_step<GS>(L, g, sh, lane, t - 1, swept, final_used, y, x);
+  const uint32_t z = opaque_zero();
+  PostFrame sa, sn, snn;
+  PostItems cur{}, nxt{};
+  beta_frame(L, T, z, sa);
+  beta_frame(L, T >= 1 ? T - 1 : 0, z, sn);
+  post_items<GS>(L, g, uniform(sa), lane, final_used, cur);
+  for (int t = T; t >= 0; --t) {
+    beta_step<GS>(L, g, sh, lane, t, swept, final_used, sa, sn, snn, cur, nxt, z);
+    sa = sn;
+    sn = snn;
+    cur = nxt;
   }
 }
 
