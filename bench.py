@@ -52,8 +52,8 @@ BYTES_LINK = 16
 # runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
 # divided by the counter's reading per byte of a plain device copy of known
 # size (bench.py --copy-kernel-bytes).  Valid while k_forward's sources hash to this.
-TRAFFIC = {"sources_sha256": "8752586c6e70d5290f7e99814147fdb33162fc71df862baea51461f6d7904af4",
-           "bytes_per_launch": 67211285}
+TRAFFIC = {"sources_sha256": "418ce1aa7bbda167b0b39ea840b65b070417b4fcb1246753f426aba7f3f44a89",
+           "bytes_per_launch": 67206996}
 
 
 FORWARD_SOURCES = ("wd_block.h", "wd_common.h", "wd_forward.hip")  # what k_forward is built from
