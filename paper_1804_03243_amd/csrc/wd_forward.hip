@@ -363,10 +363,18 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           }
           eps_frame += d;
           uint32_t tot;
-          sh.xp[tid] = block_excl_scan(d, sh.bs, par, &tot);
+          const uint32_t ex = block_excl_scan(d, sh.bs, par, &tot);
+          sh.xp[tid] = ex;
+          // each entry writes its index at its work items, so a work item
+          // finds its entry with one LDS read (the survivor arrays are free
+          // until the closure ends)
+          uint16_t* own = reinterpret_cast<uint16_t*>(sh.srt);
+          const bool by_owner = tot <= 2u * (uint32_t)kRankMax;
+          if (by_owner)
+            for (uint32_t k = 0; k < d; ++k) own[ex + k] = (uint16_t)tid;
           __syncthreads();
           for (uint32_t w = tid; w < tot; w += kThreads) {
-            const uint32_t j = search_le(sh.xp, n, w);
+            const uint32_t j = by_owner ? (uint32_t)own[w] : search_le(sh.xp, n, w);
             const uint4 e = sh.bk[j];
             const uint32_t a = e.y + (w - sh.xp[j]);
             const uint4 r = g.xarc[a];
