@@ -884,10 +884,11 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     n_prev = n_keep;
     W = W_next;
     front_lds = fl;
+    // (the frame's last reads of these counters came before the link
+    // pass's closing collective)
     for (uint32_t i = tid; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nb[i] = 0;
     for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
     h_clear(sh);
-    __syncthreads();
     if (tid == 0) {
       sh.n_touched = 0;
       sh.n_surv = 0;

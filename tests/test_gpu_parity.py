@@ -274,3 +274,39 @@ def test_mode_flags_exclusive(wf, tiny10k):
     st, res = wf.wd_decode(graph.handle, x.data_ptr(), 10, p, used, ws, nbytes,
                            torch.cuda.current_stream().cuda_stream)
     assert st == wf.WD_EINVAL and not res
+
+
+def fanin_graph(n_spread: int, n_hub: int = 8, P: int = 16, seed: int = 0) -> dict:
+    """Start state -> n_spread states by emitting arcs; each of those has an
+    epsilon arc to every one of n_hub hub states; each hub goes back to the
+    start by an emitting arc.  Every other frame, the epsilon closure has
+    one level of n_spread * n_hub work items over only n_spread + n_hub
+    table entries."""
+    rng = np.random.default_rng(seed)
+    S = 1 + n_spread + n_hub
+    src, dst, il = [], [], []
+    for i in range(n_spread):
+        src.append(0), dst.append(1 + i), il.append(1 + i % P)
+    for i in range(n_spread):
+        for h in range(n_hub):
+            src.append(1 + i), dst.append(1 + n_spread + h), il.append(0)
+    for h in range(n_hub):
+        src.append(1 + n_spread + h), dst.append(0), il.append(1 + h % P)
+    src = np.asarray(src)
+    A = src.size
+    row_ptr = np.zeros(S + 1, np.int64)
+    np.cumsum(np.bincount(src, minlength=S), out=row_ptr[1:])
+    olabel = np.where(rng.random(A) < 0.3, rng.integers(1, 50, A), 0)
+    return synth._pack(dict(row_ptr=row_ptr, dst=np.asarray(dst), ilabel=np.asarray(il), olabel=olabel,
+                            weight=rng.exponential(1.0, A).astype(np.float32)), S)
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("n_spread", [500, 600])
+def test_epsilon_fanin_level(wf, oracle_mod, n_spread, mode):
+    """One epsilon level with 4000 (500 x 8) and 4800 (600 x 8) work items:
+    in one-workgroup mode below and above the number whose owners fit the
+    owner array (4096), so both the owner lookup and the search fallback run."""
+    g = fanin_graph(n_spread)
+    L = synth.tiny_loglikes(31 + n_spread, 7, 16) * 3 - 6
+    _run(wf, oracle_mod, g, L, 16, INF, 2000, 4.0, case=f"epsilon fan-in {n_spread}", mode=mode)
