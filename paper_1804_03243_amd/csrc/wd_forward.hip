@@ -297,6 +297,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             if (c != kNoEps) lds_bucket(sh, slot, g.off[s0], g.off[s0 + 1], c);
           }
           best_key = cost_key(0.0f);
+          __syncthreads();
         } else {
           uint32_t my_best = 0xffffffffu;
           for (uint32_t base = 0; base < W; base += kThreads) {
@@ -328,6 +329,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             L.cand[w] = cv;
             if (base == 0) my_c = cv;
           }
+          // (the collective's barrier also publishes the table writes)
           best_key = (uint32_t)block_min64(my_best, sh.bs, par);
           if (best_key >= kInfKey) {
             status = 3;  // WD_ENOPATH
@@ -335,7 +337,6 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             break;
           }
         }
-        __syncthreads();
         if (sh.spill) {
           lds = false;
           continue;
