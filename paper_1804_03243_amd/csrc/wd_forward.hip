@@ -36,6 +36,7 @@ struct FwdShared {
   uint32_t n_rank;
   uint32_t sel_b;
   uint32_t sel_before;
+  uint32_t lvl_tot;    // LDS table: work items of the current epsilon level
   uint32_t hcount;     // LDS table: reserved entries
   uint32_t spill;      // LDS table full: the frame goes global
   uint32_t n_bk;       // LDS table: epsilon bucket entries
@@ -363,17 +364,33 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             if (e.w == lvl && (uint32_t)(sh.h_val[e.x] >> 32) <= kcutb) d = e.z - e.y;
           }
           eps_frame += d;
-          uint32_t tot;
-          const uint32_t ex = block_excl_scan(d, sh.bs, par, &tot);
-          sh.xp[tid] = ex;
           // each entry writes its index at its work items, so a work item
-          // finds its entry with one LDS read (the survivor arrays are free
-          // until the closure ends)
-          uint16_t* own = reinterpret_cast<uint16_t*>(sh.srt);
-          const bool by_owner = tot <= 2u * (uint32_t)kRankMax;
-          if (by_owner)
-            for (uint32_t k = 0; k < d; ++k) own[ex + k] = (uint16_t)tid;
-          __syncthreads();
+          // finds its entry with one LDS read (rs_slot is free until the
+          // closure ends)
+          uint16_t* own = reinterpret_cast<uint16_t*>(sh.rs_slot);
+          constexpr uint32_t kOwnCap = 2u * (uint32_t)kRankMax;
+          uint32_t tot;
+          if (n <= 64u) {
+            // every entry in the first wavefront: its scan needs no
+            // workgroup barrier, and one barrier publishes the result
+            if (tid < 64u) {
+              const uint32_t inc = wave_incl_scan(d), ex = inc - d;
+              const uint32_t all = __shfl(inc, 63, 64);
+              sh.xp[tid] = ex;
+              if (all <= kOwnCap)
+                for (uint32_t k = 0; k < d; ++k) own[ex + k] = (uint16_t)tid;
+              if (tid == 63u) sh.lvl_tot = all;
+            }
+            __syncthreads();
+            tot = sh.lvl_tot;
+          } else {
+            const uint32_t ex = block_excl_scan(d, sh.bs, par, &tot);
+            sh.xp[tid] = ex;
+            if (tot <= kOwnCap)
+              for (uint32_t k = 0; k < d; ++k) own[ex + k] = (uint16_t)tid;
+            __syncthreads();
+          }
+          const bool by_owner = tot <= kOwnCap;
           for (uint32_t w = tid; w < tot; w += kThreads) {
             const uint32_t j = by_owner ? (uint32_t)own[w] : search_le(sh.xp, n, w);
             const uint4 e = sh.bk[j];
@@ -411,6 +428,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             sh.rs_state[pos] = s;
             sh.rs_pack[pos] = v;
             sh.rs_slot[pos] = i;
+            sh.srt[pos] = s;  // the direct ranking's input when no max-active cut follows
             atomicAdd(&sh.hist[((uint32_t)(v >> 32) - best_key) >> shift], 1u);
           }
         }
@@ -608,21 +626,25 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       const uint32_t m = lds ? ns : n_keep;  // entries in rs_* (<= 2 * kThreads)
       if (m <= kDirectRank) {
         // few entries: each kept state's rank is the number of kept states
-        // below it (non-kept entries and the padding to 4 read as ~0)
-        if (tid < ((m + 3u) & ~3u)) {
-          uint32_t s = kNoKey;
-          if (tid < m && (uint32_t)(sh.rs_pack[tid] >> 32) <= cut_key) s = sh.rs_state[tid];
-          sh.srt[tid] = s;
+        // below it.  Without a max-active cut the survivor pass has put every
+        // entry into srt already; otherwise the entries it drops read as ~0.
+        if (!(lds && cut_key == kcutb)) {
+          if (tid < m) {
+            uint32_t s = kNoKey;
+            if ((uint32_t)(sh.rs_pack[tid] >> 32) <= cut_key) s = sh.rs_state[tid];
+            sh.srt[tid] = s;
+          }
+          __syncthreads();
         }
-        __syncthreads();
         if (tid < m && sh.srt[tid] != kNoKey) {
           const uint32_t s = sh.srt[tid];
           const uint4* q4 = reinterpret_cast<const uint4*>(sh.srt);
           uint32_t r = 0;
-          for (uint32_t q = 0; q < (m + 3u) / 4u; ++q) {
+          for (uint32_t q = 0; q < m / 4u; ++q) {
             const uint4 v = q4[q];
             r += (v.x < s) + (v.y < s) + (v.z < s) + (v.w < s);
           }
+          for (uint32_t q = m & ~3u; q < m; ++q) r += sh.srt[q] < s;
           place(r, s, sh.rs_pack[tid]);
           if (lds) sh.h_val[sh.rs_slot[tid]] = node_base + r;  // the table now maps kept states to node ids
           else L.idx[s] = (uint32_t)(node_base + r);
