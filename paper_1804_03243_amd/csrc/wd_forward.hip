@@ -37,6 +37,7 @@ struct FwdShared {
   uint32_t sel_b;
   uint32_t sel_before;
   uint32_t lvl_tot;    // LDS table: work items of the current epsilon level
+  unsigned long long deg_tot;  // frontier out-degree totals (epsilon << 32 | emitting), small frames
   uint32_t hcount;     // LDS table: reserved entries
   uint32_t spill;      // LDS table full: the frame goes global
   uint32_t n_bk;       // LDS table: epsilon bucket entries
@@ -582,6 +583,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     // -------------------------------- compaction into a frontier sorted by state
     const bool fl = n_keep <= (uint32_t)kFrontCap;
     const Front f = front_at(fl, sh, L);
+    bool deg_ready = false;  // the compaction filled the frontier's offsets and degrees
     if (hist_ok && node_base + n_keep > L.node_cap) {
       hist_ok = false;
       ovf |= kOvfNodes;
@@ -628,6 +630,9 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         // few entries: each kept state's rank is the number of kept states
         // below it.  Without a max-active cut the survivor pass has put every
         // entry into srt already; otherwise the entries it drops read as ~0.
+        // The ranking thread also fills the frontier entry's arc offsets,
+        // degrees and level (its loads overlap the ranking).
+        deg_ready = true;
         if (!(lds && cut_key == kcutb)) {
           if (tid < m) {
             uint32_t s = kNoKey;
@@ -638,6 +643,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         }
         if (tid < m && sh.srt[tid] != kNoKey) {
           const uint32_t s = sh.srt[tid];
+          const uint2 o0 = g.off[s], o1 = g.off[s + 1];
+          const uint8_t cls = g.sclass[s];
           const uint4* q4 = reinterpret_cast<const uint4*>(sh.srt);
           uint32_t r = 0;
           for (uint32_t q = 0; q < m / 4u; ++q) {
@@ -648,6 +655,11 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           place(r, s, sh.rs_pack[tid]);
           if (lds) sh.h_val[sh.rs_slot[tid]] = node_base + r;  // the table now maps kept states to node ids
           else L.idx[s] = (uint32_t)(node_base + r);
+          f.ebeg[r] = o0.x;
+          f.xbeg[r] = o0.y;
+          f.edeg[r] = o1.x - o0.x;  // degrees for now, prefix sums below
+          f.xdeg[r] = o1.y - o0.y;
+          f.cls[r] = cls;
         }
       } else {
         // counting sort on the top 11 bits of the state, then the few states
@@ -733,7 +745,42 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     __syncthreads();
     // ------------------------------- arc offsets and degree prefix sums
     uint32_t W_next, W_eps;
-    {
+    if (deg_ready) {
+      // at most kDirectRank tokens with their degrees in place: the first
+      // wavefront sums them, four per lane, and publishes the totals
+      static_assert(kDirectRank <= 4 * 64, "four tokens per lane");
+      if (tid < 64u) {
+        uint32_t de[4], dx[4];
+        uint64_t sum = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t p = 4u * tid + (uint32_t)k;
+          de[k] = p < n_keep ? f.edeg[p] : 0u;
+          dx[k] = p < n_keep ? f.xdeg[p] : 0u;
+          sum += ((uint64_t)dx[k] << 32) | de[k];
+        }
+        const uint64_t inc = wave_incl_scan64(sum);
+        uint32_t eb = (uint32_t)(inc - sum), xb = (uint32_t)((inc - sum) >> 32);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t p = 4u * tid + (uint32_t)k;
+          if (p < n_keep) {
+            f.edeg[p] = eb;
+            f.xdeg[p] = xb;
+          }
+          eb += de[k];
+          xb += dx[k];
+        }
+        if (tid == 63u) {
+          sh.deg_tot = inc;
+          f.edeg[n_keep] = (uint32_t)inc;
+          f.xdeg[n_keep] = (uint32_t)(inc >> 32);
+        }
+      }
+      __syncthreads();
+      W_next = (uint32_t)sh.deg_tot;
+      W_eps = (uint32_t)(sh.deg_tot >> 32);
+    } else {
       const uint32_t per = (n_keep + kThreads - 1) / kThreads;
       const uint32_t p0 = tid * per < n_keep ? tid * per : n_keep;
       const uint32_t p1 = p0 + per < n_keep ? p0 + per : n_keep;
@@ -765,8 +812,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         f.edeg[n_keep] = W_next;
         f.xdeg[n_keep] = W_eps;
       }
+      __syncthreads();
     }
-    __syncthreads();
     if (tid == 0) {
       L.node_off[t] = node_base;
       L.node_off[t + 1] = node_base + n_keep;
