@@ -22,6 +22,7 @@
 namespace wd {
 
 constexpr uint32_t kNoKey = 0xffffffffu;
+constexpr uint16_t kNoSlot = 0xffffu;
 constexpr uint32_t kLdsWork = 3 * kHashMax;  // emitting work above which a frame starts global
 constexpr uint32_t kBkCap = 1024;            // LDS epsilon bucket entries before a frame spills
 constexpr uint32_t kDirectRank = 256;        // survivors ranked directly, without the counting sort
@@ -50,6 +51,7 @@ struct FwdShared {
   alignas(16) uint32_t srt[kRankMax];  // states by bucket while sorting survivors
   uint32_t h_key[kHashCap];
   unsigned long long h_val[kHashCap];
+  uint16_t h_used[kHashMax];  // slot claimed by the n-th insertion (kNoSlot: the state was there)
   uint4 bk[kBkCap];    // {table slot, first epsilon arc, end epsilon arc, level}
   uint32_t xp[kBkCap]; // epsilon arcs of the bucket entries before entry i (one level)
   uint32_t f_state[kFrontCap + 1];
@@ -95,17 +97,22 @@ __device__ __forceinline__ uint32_t h_insert(FwdShared& sh, uint32_t s, bool* fr
     if (k == kNoKey) break;
     i = (i + 1) & (kHashCap - 1);
   }
-  if (atomicAdd(&sh.hcount, 1u) >= (uint32_t)kHashMax) {
+  const uint32_t c = atomicAdd(&sh.hcount, 1u);
+  if (c >= (uint32_t)kHashMax) {
     sh.spill = 1;
     return kHashCap;
   }
   while (true) {
     const uint32_t prev = atomicCAS(&sh.h_key[i], kNoKey, s);
     if (prev == kNoKey) {
+      sh.h_used[c] = (uint16_t)i;
       *fresh = true;
       return i;
     }
-    if (prev == s) return i;
+    if (prev == s) {
+      sh.h_used[c] = kNoSlot;
+      return i;
+    }
     i = (i + 1) & (kHashCap - 1);
   }
 }
@@ -120,10 +127,23 @@ __device__ __forceinline__ uint32_t h_find(const FwdShared& sh, uint32_t s) {
   }
 }
 
-__device__ __forceinline__ void h_clear(FwdShared& sh) {
-  for (uint32_t i = threadIdx.x; i < (uint32_t)kHashCap; i += kThreads) {
-    sh.h_key[i] = kNoKey;
-    sh.h_val[i] = kEmpty;
+// Empties the table: every slot (used = kHashCap: its first use), or the
+// slots claimed by the first `used` insertions (the count read before the
+// last barrier; a frame claims at most kHashMax slots).
+__device__ __forceinline__ void h_clear(FwdShared& sh, uint32_t used) {
+  if (used == (uint32_t)kHashCap) {
+    for (uint32_t i = threadIdx.x; i < (uint32_t)kHashCap; i += kThreads) {
+      sh.h_key[i] = kNoKey;
+      sh.h_val[i] = kEmpty;
+    }
+  } else {
+    for (uint32_t i = threadIdx.x; i < used; i += kThreads) {
+      const uint32_t slot = sh.h_used[i];
+      if (slot != kNoSlot) {
+        sh.h_key[slot] = kNoKey;
+        sh.h_val[slot] = kEmpty;
+      }
+    }
   }
   for (uint32_t i = threadIdx.x; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nbl[i] = 0;
   if (threadIdx.x == 0) {
@@ -212,7 +232,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
 
   for (uint32_t i = tid; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nb[i] = 0;
   for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
-  h_clear(sh);
+  h_clear(sh, kHashCap);
   if (tid == 0) {
     sh.n_touched = 0;
     sh.n_surv = 0;
@@ -419,16 +439,23 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         const uint32_t span = kcutb - best_key;
         nbits = span ? 32u - (uint32_t)__clz(span) : 0u;
         shift = nbits > 11u ? nbits - 11u : 0u;
-        for (uint32_t base = 0; base < (uint32_t)kHashCap; base += kThreads) {
+        // (the table's entries are the slots its insertions claimed)
+        const uint32_t hc = sh.hcount;  // <= kHashMax: the frame did not spill
+        for (uint32_t base = 0; base < hc; base += kThreads) {
           const uint32_t i = base + tid;
-          const uint32_t s = sh.h_key[i];
-          const unsigned long long v = sh.h_val[i];
+          const uint32_t slot = i < hc ? (uint32_t)sh.h_used[i] : (uint32_t)kNoSlot;
+          uint32_t s = kNoKey;
+          unsigned long long v = kEmpty;
+          if (slot != kNoSlot) {
+            s = sh.h_key[slot];
+            v = sh.h_val[slot];
+          }
           const bool keep = s != kNoKey && (uint32_t)(v >> 32) <= kcutb;
           const uint32_t pos = wave_append(keep, &sh.n_surv);
           if (keep) {
             sh.rs_state[pos] = s;
             sh.rs_pack[pos] = v;
-            sh.rs_slot[pos] = i;
+            sh.rs_slot[pos] = slot;
             sh.srt[pos] = s;  // the direct ranking's input when no max-active cut follows
             atomicAdd(&sh.hist[((uint32_t)(v >> 32) - best_key) >> shift], 1u);
           }
@@ -936,6 +963,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     // a payload no sum of a finite weight and a log-likelihood has: keeps the
     // warming loads without waiting for them earlier
     if (__float_as_uint(warm) == 0x7fc00001u) bad_idx |= 2u;
+    // insertions to undo, read before the barrier after which thread 0 resets the count
+    const uint32_t h_used_n = sh.hcount < (uint32_t)kHashMax ? sh.hcount : (uint32_t)kHashMax;
     const uint32_t fl_or = block_or((bad_idx ? 0x80000000u : 0u) | xmask, sh.bs, par);
     if (fl_or & 0x80000000u) {
       status = kStatusInternal;
@@ -958,7 +987,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     // pass's closing collective)
     for (uint32_t i = tid; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nb[i] = 0;
     for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
-    h_clear(sh);
+    h_clear(sh, h_used_n);
     if (tid == 0) {
       sh.n_touched = 0;
       sh.n_surv = 0;
