@@ -246,6 +246,11 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
   uint64_t node_base = 0, node_base_prev = 0, link_base = 0;
   uint32_t n_prev = 0, W = 0;
   bool front_lds = true;  // where the frontier of the last finished frame is
+  bool front_own = false; // its emitting work items' owners are in own_e
+  // owners of the frontier's emitting work items, 16-bit, in rs_pack (free
+  // from the degree pass until the next frame's survivor pass)
+  uint16_t* const own_e = reinterpret_cast<uint16_t*>(sh.rs_pack);
+  constexpr uint32_t kOwnE = 4u * (uint32_t)kRankMax;
   uint64_t my_eps = 0;
   if (tid == 0) {
     sh.c_arcs = 0;
@@ -325,7 +330,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           for (uint32_t base = 0; base < W; base += kThreads) {
             const uint32_t w = base + tid;
             if (w >= W) break;
-            const uint32_t i = search_le(fp.edeg, n_prev, w);
+            const uint32_t i = front_own ? (uint32_t)own_e[w] : search_le(fp.edeg, n_prev, w);
             const float c = key_cost(fp.key[i]);
             const uint4 r = g.earc[fp.ebeg[i] + (w - fp.edeg[i])];
             const uint32_t dst = r.x, cls = r.z >> 24;
@@ -486,7 +491,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             bool first = false;
             uint32_t dst = 0, cls = kNoEps;
             if (w < W) {
-              const uint32_t i = search_le(fp.edeg, n_prev, w);
+              const uint32_t i = front_own ? (uint32_t)own_e[w] : search_le(fp.edeg, n_prev, w);
               const float c = key_cost(fp.key[i]);
               const uint4 r = g.earc[fp.ebeg[i] + (w - fp.edeg[i])];
               dst = r.x;
@@ -841,6 +846,14 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       }
       __syncthreads();
     }
+    // owners of the next frame's emitting work items, written by threads
+    // 256..511 (idle in the link pass of small frames)
+    const bool own_e_ok = fl && W_next <= kOwnE;
+    if (own_e_ok && tid >= 256u && tid < 512u)
+      for (uint32_t p = tid - 256u; p < n_keep; p += 256u) {
+        const uint32_t k1 = f.edeg[p + 1];
+        for (uint32_t k = f.edeg[p]; k < k1; ++k) own_e[k] = (uint16_t)p;
+      }
     if (tid == 0) {
       L.node_off[t] = node_base;
       L.node_off[t + 1] = node_base + n_keep;
@@ -983,6 +996,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     n_prev = n_keep;
     W = W_next;
     front_lds = fl;
+    front_own = own_e_ok;
     // (the frame's last reads of these counters came before the link
     // pass's closing collective)
     for (uint32_t i = tid; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nb[i] = 0;
