@@ -6,18 +6,23 @@ namespace wd {
 
 // Log-likelihood check: NaN, +inf and values above 1e30 are rejected.
 // Rows of the frames this launch decodes, t0..T (frame t reads row t - 1).
+// A streaming read: four independent loads per thread per step keep enough
+// of them in flight to run at HBM speed.
+__device__ __forceinline__ bool bad_loglike(float v) { return v != v || v > 1e30f; }
+
 __global__ void k_check_loglikes(const LaneDesc* __restrict__ lanes, uint32_t P, uint32_t* bad) {
   const LaneDesc L = lanes[blockIdx.y];
   const uint64_t n = (uint64_t)L.T * P;
   const uint64_t r0 = (uint64_t)(L.t0 > 0 ? L.t0 - 1 : 0) * P;
-  for (uint64_t i = r0 + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (uint64_t)gridDim.x * blockDim.x) {
-    const float v = L.ll[i];
-    if (v != v || v > 1e30f) {
-      atomicOr(&bad[blockIdx.y], 1u);
-      break;
-    }
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  uint64_t i = r0 + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  bool b = false;
+  for (; i + 3 * stride < n; i += 4 * stride) {
+    const float v0 = L.ll[i], v1 = L.ll[i + stride], v2 = L.ll[i + 2 * stride], v3 = L.ll[i + 3 * stride];
+    b |= bad_loglike(v0) | bad_loglike(v1) | bad_loglike(v2) | bad_loglike(v3);
   }
+  for (; i < n; i += stride) b |= bad_loglike(L.ll[i]);
+  if (b) atomicOr(&bad[blockIdx.y], 1u);
 }
 
 __global__ void k_fill_u64(unsigned long long* p, uint64_t n, unsigned long long v) {
@@ -95,7 +100,9 @@ void launch_set_frames(LaneDesc* lanes, int B, const int32_t* T, const int32_t* 
 
 
 void launch_check_loglikes(const LaneDesc* lanes, int B, uint32_t P, uint32_t* bad, hipStream_t s) {
-  hipLaunchKernelGGL(k_check_loglikes, dim3(64, B), dim3(256), 0, s, lanes, P, bad);
+  // ~2048 workgroups in all (at least 16 per utterance)
+  const int gx = B >= 128 ? 16 : 2048 / B;
+  hipLaunchKernelGGL(k_check_loglikes, dim3(gx, B), dim3(256), 0, s, lanes, P, bad);
 }
 
 void launch_fill_u64(unsigned long long* p, uint64_t n, unsigned long long v, hipStream_t s) {
