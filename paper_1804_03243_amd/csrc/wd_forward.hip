@@ -309,6 +309,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     bool failed = false;
     uint4 my_c = make_uint4(0, 0, 0, 0);  // this thread's first candidate (work item tid)
     float warm = 0.0f;  // values of cache-warming loads, read at the end of the frame
+    float warm_x = 0.0f;
     // ---------------------------------------------------- token passing
     for (int attempt = 0; attempt < 2; ++attempt) {
       eps_frame = 0;
@@ -687,6 +688,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           place(r, s, sh.rs_pack[tid]);
           if (lds) sh.h_val[sh.rs_slot[tid]] = node_base + r;  // the table now maps kept states to node ids
           else L.idx[s] = (uint32_t)(node_base + r);
+          // the link pass reads the token's epsilon arcs
+          if (o1.y > o0.y) warm_x = __uint_as_float(g.xarc[o0.y].y);
           f.ebeg[r] = o0.x;
           f.xbeg[r] = o0.y;
           f.edeg[r] = o1.x - o0.x;  // degrees for now, prefix sums below
@@ -975,7 +978,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     }
     // a payload no sum of a finite weight and a log-likelihood has: keeps the
     // warming loads without waiting for them earlier
-    if (__float_as_uint(warm) == 0x7fc00001u) bad_idx |= 2u;
+    if (__float_as_uint(warm) == 0x7fc00001u || __float_as_uint(warm_x) == 0x7fc00001u) bad_idx |= 2u;
     // insertions to undo, read before the barrier after which thread 0 resets the count
     const uint32_t h_used_n = sh.hcount < (uint32_t)kHashMax ? sh.hcount : (uint32_t)kHashMax;
     const uint32_t fl_or = block_or((bad_idx ? 0x80000000u : 0u) | xmask, sh.bs, par);
