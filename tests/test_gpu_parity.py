@@ -187,6 +187,26 @@ def test_batch_lanes_equal_single(wf, oracle_mod, tiny10k, mode):
     del rng
 
 
+def test_batch_more_lanes_than_cus(wf, oracle_mod, tiny10k):
+    """300 utterances in one call (more workgroups than the chip's 256 CUs),
+    lengths 0..80 frames, results through the packed single transfer: every
+    lane equals the oracle's decode of its utterance."""
+    import torch
+    cfg, g, L, graph = tiny10k
+    rng = np.random.default_rng(17)
+    lens = [0, 1] + [int(n) for n in rng.integers(2, 81, 298)]
+    Ls = [np.ascontiguousarray(synth.tiny_loglikes(5000 + i, n, cfg["P"]) * 3 - 10, dtype=np.float32)
+          for i, n in enumerate(lens)]
+    xs = [torch.from_numpy(x).to(graph.device) for x in Ls]
+    args = (10.0, 200, 6.0)
+    print(f"\n[gpu case] batch of {len(lens)} tiny_10k utterances, {sum(lens)} frames, mode=workgroup",
+          flush=True)
+    rb = wf.decode_batch(graph, xs, *args, mode="workgroup")
+    assert len(rb) == len(lens)
+    for i, x in enumerate(Ls):
+        assert_same(rb[i], oracle_mod.decode(g, x, *args))
+
+
 @pytest.mark.parametrize("mode", MODES)
 def test_wide_2m_dyadic_prefix(wf, oracle_mod, mode):
     """Tens of thousands of tokens per frame (state-bitmap compaction), exact
