@@ -945,10 +945,13 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             bad_idx = 1;
             continue;
           }
+          // the frontier reads come before the stores: a wait for a flat load
+          // also waits for every store in flight
+          const uint32_t q = (uint32_t)(dn - node_base);
+          const uint32_t fk = f.key[q], fa = f.arc[q];
           L.links[link_base + pos] = make_uint4(c.x, c.y, (uint32_t)dn, c.w);
           ++pos;
-          const uint32_t q = (uint32_t)(dn - node_base);
-          if (f.key[q] == xk && f.arc[q] == c.x) L.n_pred[dn] = c.y;
+          if (fk == xk && fa == c.x) L.n_pred[dn] = c.y;
         }
         if (e0 < e1) {
           uint32_t p = px0;
@@ -966,12 +969,13 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             }
             const uint32_t sn = (uint32_t)(node_base + p);
             const uint64_t at = link_base + nE + posx;
-            L.links[at] = make_uint4(r.w, sn, (uint32_t)dn, __float_as_uint(x));
-            L.link_lvl[at] = f.cls[p];
-            xmask |= 1u << (f.cls[p] < 31 ? f.cls[p] : 31);
-            ++posx;
             const uint32_t q = (uint32_t)(dn - node_base);
-            if (f.key[q] == xk && f.arc[q] == r.w) L.n_pred[dn] = sn;
+            const uint32_t cls = f.cls[p], fk = f.key[q], fa = f.arc[q];  // before the stores
+            L.links[at] = make_uint4(r.w, sn, (uint32_t)dn, __float_as_uint(x));
+            L.link_lvl[at] = (uint8_t)cls;
+            xmask |= 1u << (cls < 31 ? cls : 31);
+            ++posx;
+            if (fk == xk && fa == r.w) L.n_pred[dn] = sn;
           }
         }
       }
