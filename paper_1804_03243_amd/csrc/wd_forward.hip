@@ -23,6 +23,8 @@ namespace wd {
 
 constexpr uint32_t kNoKey = 0xffffffffu;
 constexpr uint16_t kNoSlot = 0xffffu;
+// s_waitcnt operand: vector memory count 0, the export and LDS counts left open
+constexpr int kWaitVm0 = 0x0f70;
 constexpr uint32_t kLdsWork = 3 * kHashMax;  // emitting work above which a frame starts global
 constexpr uint32_t kBkCap = 1024;            // LDS epsilon bucket entries before a frame spills
 constexpr uint32_t kDirectRank = 256;        // survivors ranked directly, without the counting sort
@@ -674,6 +676,9 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           }
           __syncthreads();
         }
+        // the frontier's earlier stores have landed by now; saying so lets the
+        // ranking loop read LDS without first waiting for the loads below
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
         if (tid < m && sh.srt[tid] != kNoKey) {
           const uint32_t s = sh.srt[tid];
           const uint2 o0 = g.off[s], o1 = g.off[s + 1];
