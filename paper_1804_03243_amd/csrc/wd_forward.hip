@@ -40,6 +40,7 @@ struct FwdShared {
   uint32_t sel_b;
   uint32_t sel_before;
   uint32_t lvl_tot;    // LDS table: work items of the current epsilon level
+  uint32_t lvl_wide;   // LDS table: first epsilon level the whole workgroup runs
   unsigned long long deg_tot;  // frontier out-degree totals (epsilon << 32 | emitting), small frames
   uint32_t hcount;     // LDS table: reserved entries
   uint32_t spill;      // LDS table full: the frame goes global
@@ -379,7 +380,62 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           const uint4 e = sh.bk[tid - 512u];
           if (e.z > e.y) warm = __uint_as_float(g.xarc[e.y].y);
         }
-        for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
+        // one epsilon arc of a level: work item w of bucket entry j
+        auto relax_eps = [&](uint32_t j, uint32_t w) {
+          const uint4 e = sh.bk[j];
+          const uint32_t a = e.y + (w - sh.xp[j]);
+          const uint4 r = g.xarc[a];
+          const uint2 nx = g.xnext[a];  // the destination's epsilon arcs
+          const float c = key_cost((uint32_t)(sh.h_val[e.x] >> 32));
+          const uint32_t xk = cost_key(canon(c + __uint_as_float(r.y)));
+          if (xk > kcutb || xk >= kInfKey || sh.spill) return;
+          bool fresh;
+          const uint32_t slot = h_insert(sh, r.x, &fresh);
+          if (slot < (uint32_t)kHashCap) {
+            atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
+            if (fresh && r.z != kNoEps) lds_bucket(sh, slot, make_uint2(0, nx.x), make_uint2(0, nx.y), r.z);
+          }
+        };
+        // each entry writes its index at its work items, so a work item
+        // finds its entry with one LDS read (rs_slot is free until the
+        // closure ends)
+        uint16_t* own = reinterpret_cast<uint16_t*>(sh.rs_slot);
+        constexpr uint32_t kOwnCap = 2u * (uint32_t)kRankMax;
+        // Levels whose bucket entries and epsilon arcs each fit in one
+        // wavefront run in wavefront 0 alone, one after another, with no
+        // workgroup barrier: a wavefront's LDS accesses take effect in
+        // program order, so each level sees the previous one's tokens.  The
+        // first level that does not fit, and the levels after it, run on the
+        // whole workgroup below.
+        if (tid < 64u) {
+          uint32_t lvl = 0;
+          for (; lvl < g.nlevels; ++lvl) {
+            if (sh.spill) {
+              lvl = g.nlevels;
+              break;
+            }
+            if (sh.nbl[lvl] == 0) continue;
+            const uint32_t n = sh.n_bk < kBkCap ? sh.n_bk : kBkCap;
+            if (n > 64u) break;
+            uint32_t d = 0;
+            if (tid < n) {
+              const uint4 e = sh.bk[tid];
+              if (e.w == lvl && (uint32_t)(sh.h_val[e.x] >> 32) <= kcutb) d = e.z - e.y;
+            }
+            const uint32_t inc = wave_incl_scan(d), ex = inc - d;
+            const uint32_t all = __shfl(inc, 63, 64);
+            if (all > 64u) break;  // (nothing of this level done yet)
+            eps_frame += d;
+            sh.xp[tid] = ex;
+            for (uint32_t k = 0; k < d; ++k) own[ex + k] = (uint16_t)tid;
+            __builtin_amdgcn_wave_barrier();
+            if (tid < all) relax_eps(own[tid], tid);
+            __builtin_amdgcn_wave_barrier();
+          }
+          if (tid == 0) sh.lvl_wide = lvl;
+        }
+        __syncthreads();
+        for (uint32_t lvl = sh.lvl_wide; lvl < g.nlevels; ++lvl) {
           if (sh.nbl[lvl] == 0) continue;  // uniform: written only by lower levels
           // this level's entries within the cutoff spread their epsilon arcs
           // over the workgroup: entry i (one per thread) owns arcs
@@ -393,11 +449,6 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             if (e.w == lvl && (uint32_t)(sh.h_val[e.x] >> 32) <= kcutb) d = e.z - e.y;
           }
           eps_frame += d;
-          // each entry writes its index at its work items, so a work item
-          // finds its entry with one LDS read (rs_slot is free until the
-          // closure ends)
-          uint16_t* own = reinterpret_cast<uint16_t*>(sh.rs_slot);
-          constexpr uint32_t kOwnCap = 2u * (uint32_t)kRankMax;
           uint32_t tot;
           if (n <= 64u) {
             // every entry in the first wavefront: its scan needs no
@@ -420,22 +471,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             __syncthreads();
           }
           const bool by_owner = tot <= kOwnCap;
-          for (uint32_t w = tid; w < tot; w += kThreads) {
-            const uint32_t j = by_owner ? (uint32_t)own[w] : search_le(sh.xp, n, w);
-            const uint4 e = sh.bk[j];
-            const uint32_t a = e.y + (w - sh.xp[j]);
-            const uint4 r = g.xarc[a];
-            const uint2 nx = g.xnext[a];  // the destination's epsilon arcs
-            const float c = key_cost((uint32_t)(sh.h_val[e.x] >> 32));
-            const uint32_t xk = cost_key(canon(c + __uint_as_float(r.y)));
-            if (xk > kcutb || xk >= kInfKey || sh.spill) continue;
-            bool fresh;
-            const uint32_t slot = h_insert(sh, r.x, &fresh);
-            if (slot < (uint32_t)kHashCap) {
-              atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
-              if (fresh && r.z != kNoEps) lds_bucket(sh, slot, make_uint2(0, nx.x), make_uint2(0, nx.y), r.z);
-            }
-          }
+          for (uint32_t w = tid; w < tot; w += kThreads)
+            relax_eps(by_owner ? (uint32_t)own[w] : search_le(sh.xp, n, w), w);
           __syncthreads();
           if (sh.spill) break;
         }
