@@ -352,7 +352,11 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
                 const uint32_t slot = h_insert(sh, dst, &fresh);
                 if (slot < (uint32_t)kHashCap) {
                   atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
-                  if (fresh && cls != kNoEps) lds_bucket(sh, slot, o0, o1, cls);
+                  if (fresh && cls != kNoEps) {
+                    lds_bucket(sh, slot, o0, o1, cls);
+                    // start the state's first epsilon arc on its way for the closure
+                    warm = __uint_as_float(g.xarc[o0.y].y);
+                  }
                 }
               }
             }
@@ -374,12 +378,6 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         }
         const float cutb = key_cost(best_key) + prm.beam;
         kcutb = cost_key(cutb);
-        // the upper wavefronts warm the first epsilon arcs of the entries the
-        // expansion bucketed (read by the level passes below)
-        if (tid >= 512u && tid - 512u < (sh.n_bk < kBkCap ? sh.n_bk : kBkCap)) {
-          const uint4 e = sh.bk[tid - 512u];
-          if (e.z > e.y) warm = __uint_as_float(g.xarc[e.y].y);
-        }
         // one epsilon arc of a level: work item w of bucket entry j
         auto relax_eps = [&](uint32_t j, uint32_t w) {
           const uint4 e = sh.bk[j];
