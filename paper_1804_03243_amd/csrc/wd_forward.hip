@@ -311,6 +311,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     uint64_t eps_frame = 0;
     bool failed = false;
     uint4 my_c = make_uint4(0, 0, 0, 0);  // this thread's first candidate (work item tid)
+    uint32_t my_slot = kHashCap;          // its destination's slot in the LDS table
     float warm = 0.0f;  // values of cache-warming loads, read at the end of the frame
     float warm_x = 0.0f;
     // ---------------------------------------------------- token passing
@@ -345,11 +346,13 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             float x = c + ac;
             x = canon(x + __uint_as_float(r.y));
             const uint32_t xk = cost_key(x);
+            uint32_t cslot = kHashCap;
             if (xk < kInfKey) {
               my_best = xk < my_best ? xk : my_best;
               if (!sh.spill) {
                 bool fresh;
                 const uint32_t slot = h_insert(sh, dst, &fresh);
+                cslot = slot;
                 if (slot < (uint32_t)kHashCap) {
                   atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
                   if (fresh && cls != kNoEps) {
@@ -362,7 +365,10 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             }
             const uint4 cv = make_uint4(r.w, (uint32_t)(node_base_prev + i), dst, __float_as_uint(x));
             L.cand[w] = cv;
-            if (base == 0) my_c = cv;
+            if (base == 0) {
+              my_c = cv;
+              my_slot = cslot;
+            }
           }
           // (the collective's barrier also publishes the table writes)
           best_key = (uint32_t)block_min64(my_best, sh.bs, par);
@@ -980,7 +986,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           if (per != 1) c = L.cand[w];
           const uint32_t xk = cost_key(__uint_as_float(c.w));
           if (!(xk <= cut_key && xk < kInfKey)) continue;
-          const uint64_t dn = dst_node(c.z);
+          // the thread's own candidate: its insertion left the slot
+          const uint64_t dn = per == 1 && lds && my_slot < (uint32_t)kHashCap ? sh.h_val[my_slot] : dst_node(c.z);
           if (dn < node_base || dn >= node_base + n_keep) {
             bad_idx = 1;
             continue;
