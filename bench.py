@@ -42,7 +42,8 @@ METRIC = "decoded frames/sec + arcs expanded/sec at 1 GPU; % of HBM peak"
 # atomic, plus the 4-byte log-likelihood gather for emitting arcs; per
 # surviving token 8 bytes of offsets, 12 read and 12 written; per lattice
 # link 16 bytes written.
-BYTES_ARC = 16 + 8
+BYTES_ARC_RECORD = 16
+BYTES_ARC = BYTES_ARC_RECORD + 8
 BYTES_LOGLIKE = 4
 BYTES_TOKEN = 8 + 12 + 12
 BYTES_LINK = 16
@@ -80,7 +81,7 @@ def copy_kernel(nbytes: int) -> int:
     return 0
 
 
-def wide_chip(wfstdec, steps: int = 3, mode: str = "chip") -> dict:
+def wide_chip(wfstdec, steps: int = 3, mode: str = "chip", cpu: bool = False, cpu_frames: int = 10) -> dict:
     """Chip-wide mode on the wide-beam 2M-state graph (800 frames, beam 20,
     no max-active): full decodes, lattice and posteriors included.
     mode "chip_dyn": the same with dynamic load balancing of the emitting
@@ -111,6 +112,16 @@ def wide_chip(wfstdec, steps: int = 3, mode: str = "chip") -> dict:
            "tokens_per_frame": round(st["tokens"] / (T + 1), 1),
            "raw_links": st["raw_links"], "kept_links": st["kept_links"], "link_store_links": r.needed["links"] + 2 * r.needed["window_links"],
            "kernel_ms": {"forward": round(sum(fwd) / steps, 2), "lattice": round(sum(lat) / steps, 2)}}
+    # the forward pass is ~25 kernels per frame; their summed time (HIP events
+    # around the decode's forward part on its stream) against its bytes
+    nbytes = algorithmic_bytes(st)
+    f_ms = sum(fwd) / steps
+    achieved = nbytes / (f_ms * 1e-3) / 1e9
+    out["roofline"] = {"bound": "hbm", "kernel": "chip-wide forward kernels (all launches of the forward pass)",
+                       "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                       "frac": round(achieved / HBM_PEAK_GBS, 5), "algorithmic_bytes_per_launch": int(nbytes)}
+    if cpu:
+        out["cpu_baseline"] = cpu_prefix_baseline(g, L, cfg, "wide_2m", cpu_frames)
     if mode == "chip":
         # host determinisation of this lattice, pruned to a beam of 6 (the
         # lattice beam is 10; at 10 the compact lattice keeps ~450 arcs/frame)
@@ -224,9 +235,9 @@ def batch(wfstdec, graph, n_utts: int = 64, steps: int = 3, cpu: bool = True) ->
     one launch for the batch): aggregate frames/s (median step) and the
     roofline of the batch's k_forward launch.  n_utts = 64 is the batch
     workload; 256 (one workgroup per CU) draws more utterances from the same
-    distribution.  Algorithmic bytes are summed over the lanes (arcs that
-    several lanes expand in the same step count once per lane, so this is an
-    upper bound of the unique-arc figure)."""
+    distribution.  Algorithmic bytes credit an arc record once per unique
+    (step, arc) over the lanes (`unique_arc_bytes`); the per-lane sum is
+    reported beside it."""
     import numpy as np
     import synth
     import torch
@@ -248,7 +259,9 @@ def batch(wfstdec, graph, n_utts: int = 64, steps: int = 3, cpu: bool = True) ->
     wall = float(np.median(walls))
     frames = sum(int(x.shape[0]) for x in xs)
     f_ms = float(np.median(fwd))
-    nbytes = sum(algorithmic_bytes(r.stats) for r in rs)
+    lane_sum = sum(algorithmic_bytes(r.stats) for r in rs)
+    uq = unique_arc_bytes(wfstdec, graph, xs, args, rs)
+    nbytes = lane_sum - uq["duplicate_arc_records"] * BYTES_ARC_RECORD
     achieved = nbytes / (f_ms * 1e-3) / 1e9
     out = {"workload": name, "utterances": len(xs), "frames": frames, "steps": steps,
            "frames_per_s": round(frames / wall, 1), "ms_per_step": round(1e3 * wall, 2),
@@ -256,12 +269,148 @@ def batch(wfstdec, graph, n_utts: int = 64, steps: int = 3, cpu: bool = True) ->
            "kernel_ms": {"forward": round(f_ms, 3), "lattice": round(float(np.median(lat)), 3)},
            "roofline": {"bound": "hbm", "kernel": f"k_forward ({n_utts} workgroups)",
                         "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        "frac": round(achieved / HBM_PEAK_GBS, 6), "algorithmic_bytes_per_launch": int(nbytes)}}
+                        "frac": round(achieved / HBM_PEAK_GBS, 6), "algorithmic_bytes_per_launch": int(nbytes),
+                        "per_lane_sum_bytes": int(lane_sum), "unique_arcs": uq}}
     del xs, rs
     graph._ws = None  # the batch's workspace (~0.4 GB per utterance)
     torch.cuda.empty_cache()
     if cpu:
         out["cpu_baseline"] = cpu_batch_baseline(name, n_utts)
+    return out
+
+
+PHASE_NAMES = ("expand", "eps_closure", "survivors", "max_active", "compact", "degrees", "link_count",
+               "link_write", "frame_end")
+
+
+def phase_profile(wfstdec, workload: str, reps: int = 3) -> dict:
+    """Step profile of the one-workgroup forward pass (WD_FLAG_PHASES): per
+    frame the device wall clock at each step boundary, summarised as the mean
+    microseconds per frame spent in each step (frames 1..T, all `reps`
+    decodes), with the frames whose token table went to device memory
+    counted apart.  The profiled kernel is a separate copy; its total is
+    compared with the plain kernel's time in the same run."""
+    import numpy as np
+    import synth
+    import torch
+    cfg = synth.workload(workload)
+    g = synth.make_graph(cfg)
+    L = synth.make_loglikes(cfg)
+    graph = wfstdec.Graph(g, cfg["P"], "cuda:0")
+    x = torch.from_numpy(L).to(graph.device)
+    args = (cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    plain = [wfstdec.decode(graph, x, *args, timing=True, mode="workgroup").stats["forward_ms"]
+             for _ in range(reps + 1)][1:]
+    rows, fwd = [], []
+    for _ in range(reps + 1):
+        r = wfstdec.decode(graph, x, *args, timing=True, mode="workgroup", flags=wfstdec.WD_FLAG_PHASES)
+        rows.append(r.phases[1:])
+        fwd.append(r.stats["forward_ms"])
+    rows, fwd = rows[1:], fwd[1:]
+    ph = np.concatenate(rows).astype(np.int64)
+    hz = r.phase_tick_hz
+    S = wfstdec.WD_PHASE_STAMPS
+    st = ph[:, :S]
+    # a step the frame skipped (no max-active cut, ...) has the previous stamp's value
+    d = np.diff(st, axis=1).astype(np.float64) * 1e6 / hz
+    frame_us = (st[:, S - 1] - st[:, 0]) * 1e6 / hz
+    lds = (ph[:, S] & 1).astype(bool)
+    ntok = (ph[:, S] >> 8) & 0xffffff
+    nlink = ph[:, S] >> 32
+    W = ph[:, S + 1] & 0xffffffff
+    nbk = ph[:, S + 1] >> 32
+    # frame end -> next frame's start, within each decode
+    gap = np.concatenate([r[1:, 0].astype(np.int64) - r[:-1, S - 1].astype(np.int64) for r in rows]) * 1e6 / hz
+
+    def summary(sel):
+        if not sel.any():
+            return None
+        return {"frames": int(sel.sum()), "frame_us": round(float(frame_us[sel].mean()), 3),
+                "step_us": {n: round(float(d[sel, i].mean()), 3) for i, n in enumerate(PHASE_NAMES)},
+                "tokens": round(float(ntok[sel].mean()), 1), "emitting_items": round(float(W[sel].mean()), 1),
+                "eps_bucket_entries": round(float(nbk[sel].mean()), 1), "links": round(float(nlink[sel].mean()), 1)}
+
+    out = {"workload": workload, "kernel": "k_forward_phases (WD_FLAG_PHASES copy of k_forward)",
+           "frames_per_decode": int(L.shape[0]), "decodes": reps, "tick_hz": hz,
+           "forward_ms_plain": round(float(np.mean(plain)), 3),
+           "forward_ms_profiled": round(float(np.mean(fwd)), 3),
+           "all": summary(np.ones(len(lds), bool)), "lds_table": summary(lds),
+           "device_table": summary(~lds),
+           "between_frames_us": round(float(gap.mean()), 3) if gap.size else None}
+    del graph
+    torch.cuda.empty_cache()
+    return out
+
+
+def unique_arc_bytes(wfstdec, graph, xs, args, rs) -> dict:
+    """Arc records a batch step shares between lanes.  Step t expands the
+    emitting arcs of every lane's surviving tokens of frame t-1 and the
+    epsilon arcs of its epsilon closure at frame t; an arc that several
+    lanes expand in the same step is one record read, so the algorithmic
+    bytes credit it once.  The closure's token set is taken as the frame's
+    surviving tokens, which is exact while max-active does not cut (checked:
+    the per-lane counts must reproduce each lane's arcs_expanded).  One
+    debug decode of the batch (not timed) lists every lane's tokens."""
+    import numpy as np
+    dbg = wfstdec.decode_batch(graph, xs, *args, debug=True, mode="workgroup")
+    edeg, xdeg = graph.degrees()
+    keys_e, keys_x, lane_ok, total = [], [], True, 0
+    for r, x in zip(dbg, xs):
+        T = int(x.shape[0])
+        t = r.tokens["t"].astype(np.int64)
+        s_ = r.tokens["state"].astype(np.int64)
+        n_lane = int(edeg[s_[t < T]].sum() + xdeg[s_].sum())
+        lane_ok &= n_lane == r.stats["arcs_expanded"]
+        total += n_lane
+        keys_e.append((t[t < T] << 32) | s_[t < T])
+        keys_x.append((t << 32) | s_)
+    ue = np.unique(np.concatenate(keys_e)) & 0xffffffff
+    ux = np.unique(np.concatenate(keys_x)) & 0xffffffff
+    unique = int(edeg[ue].sum() + xdeg[ux].sum())
+    return {"arcs_summed_over_lanes": total, "unique_step_arcs": unique,
+            "duplicate_arc_records": total - unique if lane_ok else 0, "lane_counts_match": bool(lane_ok)}
+
+
+def single(wfstdec, workload: str, steps: int = 5, cpu_seconds: float = 10.0, cpu: bool = True) -> dict:
+    """One utterance of `workload` in the library's default mode: frames/s
+    (median step), kernel times, the forward launch's roofline and the
+    oracle on the host (the whole utterance, repeated for about
+    `cpu_seconds`)."""
+    import numpy as np
+    import synth
+    import torch
+    cfg = synth.workload(workload)
+    g = synth.make_graph(cfg)
+    L = synth.make_loglikes(cfg)
+    graph = wfstdec.Graph(g, cfg["P"], "cuda:0")
+    x = torch.from_numpy(L).to(graph.device)
+    args = (cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    wfstdec.decode(graph, x, *args, timing=True)
+    torch.cuda.synchronize()
+    walls, fwd, lat = [], [], []
+    for _ in range(steps):
+        t0 = time.perf_counter()
+        r = wfstdec.decode(graph, x, *args, timing=True)
+        torch.cuda.synchronize()
+        walls.append(time.perf_counter() - t0)
+        fwd.append(r.stats["forward_ms"])
+        lat.append(r.stats["lattice_ms"])
+    wall, f_ms = float(np.median(walls)), float(np.median(fwd))
+    T = L.shape[0]
+    nbytes = algorithmic_bytes(r.stats)
+    achieved = nbytes / (f_ms * 1e-3) / 1e9
+    out = {"workload": workload, "states": cfg["S"], "arcs": int(g["dst"].size), "frames": T, "steps": steps,
+           "frames_per_s": round(T / wall, 1), "ms_per_step": round(1e3 * wall, 3),
+           "arcs_expanded_per_s": round(r.stats["arcs_expanded"] / wall, 1),
+           "rtf": round(wall / (T / FRAME_RATE), 7), "tokens_per_frame": round(r.stats["tokens"] / (T + 1), 1),
+           "kernel_ms": {"forward": round(f_ms, 3), "lattice": round(float(np.median(lat)), 3)},
+           "roofline": {"bound": "hbm", "kernel": "k_forward", "achieved": round(achieved, 3),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 7),
+                        "algorithmic_bytes_per_launch": int(nbytes)}}
+    del graph, x
+    torch.cuda.empty_cache()
+    if cpu:
+        out["cpu_baseline"] = cpu_baseline(g, L, cfg, workload, min_seconds=cpu_seconds)
     return out
 
 
@@ -323,6 +472,23 @@ def cpu_baseline(g, L, cfg, workload, min_seconds: float = 10.0) -> dict:
                       f"{dt:.1f} s"}
 
 
+def cpu_prefix_baseline(g, L, cfg, workload, frames: int) -> dict:
+    """The oracle (one thread) on the first `frames` frames of a workload
+    whose whole utterance takes the oracle far too long (the wide-beam graph:
+    seconds per frame).  The early frames hold fewer tokens than later ones,
+    so the arcs-expanded rate is the comparable figure."""
+    import oracle
+    oracle.build()
+    t0 = time.perf_counter()
+    o = oracle.decode(g, L[:frames], cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    dt = time.perf_counter() - t0
+    return {"value": round(frames / dt, 3), "unit": "frames/s", "cores": 1, "kind": "oracle",
+            "arcs_expanded_per_s": round(o.stats["arcs_expanded"] / dt, 1),
+            "sample": f"{workload} first {frames} frames (whole decode of that prefix, lattice included), "
+                      f"one thread, {dt:.1f} s; {o.stats['tokens'] / (frames + 1):.0f} tokens per frame "
+                      f"on average in the sample"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -334,6 +500,8 @@ def main() -> int:
     ap.add_argument("--workload", default=WORKLOAD,
                     help="workload timed (the headline line is hclg_5m; others are for profiling)")
     ap.add_argument("--mode", default="auto", help="execution mode of the timed decodes (for profiling)")
+    ap.add_argument("--phases", action="store_true",
+                    help="only print the step profile of the one-workgroup forward pass on --workload")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this decoder runs on one GPU; --gpus {args.gpus} is not supported "
@@ -342,6 +510,10 @@ def main() -> int:
 
     if args.copy_kernel_bytes:
         return copy_kernel(args.copy_kernel_bytes)
+    if args.phases:
+        from paper_1804_03243_amd import wfstdec
+        print(json.dumps(phase_profile(wfstdec, args.workload)), flush=True)
+        return 0
 
     import numpy as np
     import torch
@@ -413,8 +585,10 @@ def main() -> int:
         streamed.append(batch(wfstdec, graph, 256, steps=5, cpu=False))
         del graph, x
         torch.cuda.empty_cache()
-        out["other_workloads"] = streamed + [wide_chip(wfstdec, mode=m)
+        out["other_workloads"] = streamed + [wide_chip(wfstdec, mode=m, cpu=m == "chip" and not args.no_cpu_baseline)
                                              for m in ("chip", "chip_noprune", "chip_dyn")]
+        out["other_workloads"] += [single(wfstdec, w, cpu=not args.no_cpu_baseline)
+                                   for w in ("tiny_10k", "lm_30m")]
     if not args.no_extra:
         out["roofline"]["copy_ceiling_gbs"] = copy_ceiling()
     out["host"] = host_info()

@@ -110,6 +110,29 @@ typedef struct {
  * with WD_FLAG_DEBUG, which returns the raw lattice.  Decodes on one device
  * share the library's pruning stream and are ordered on it by events. */
 #define WD_FLAG_NO_INCREMENTAL_PRUNE 32u
+/* Step profile of the one-workgroup forward pass (a measurement aid, off in
+ * timed runs; WD_EINVAL in chip-wide mode): a separately compiled copy of the
+ * forward kernel stores the device wall clock each time its first thread
+ * passes a step boundary of a frame (wd_result_phases).  The result is the
+ * same; the stores add a little time to each frame. */
+#define WD_FLAG_PHASES 64u
+/* One-workgroup mode: take the epsilon closure level by level (one pass per
+ * epsilon level, each a round of dependent memory reads) even when the graph
+ * has an epsilon path table (wd_graph_eps_paths), where by default every
+ * epsilon path of a state within the beam is relaxed at once.  The result is
+ * identical; the flag exists for the A/B comparison. */
+#define WD_FLAG_EPS_LEVELS 128u
+/* Words per frame of wd_result_phases: WD_PHASE_STAMPS wall-clock stamps, at
+ * (0) the frame's start, the end of (1) the emitting expansion and its best
+ * cost, (2) the epsilon closure, (3) the survivor pass, (4) the max-active
+ * cutoff, (5) the compaction into the state-sorted frontier, (6) the degree
+ * prefix sums, (7) the lattice-link counts, (8) the link writes, (9) the
+ * frame (table reset); then word 10 = (1 if the frame's token table was in
+ * LDS) | surviving tokens << 8 | lattice links << 32, and word 11 = emitting
+ * work items | LDS-table epsilon bucket entries << 32 (touched states with
+ * epsilon arcs). */
+#define WD_PHASE_STAMPS 10
+#define WD_PHASE_SLOTS 12
 
 /* Workspace capacities (per utterance).  0 selects a default.  A decode that
  * outgrows a capacity fails with WD_ECAPACITY and reports what it needed. */
@@ -181,7 +204,14 @@ typedef struct wd_result wd_result;
 /* ---- graph ------------------------------------------------------------ */
 
 /* Validate `d` (CSR shape, labels, weights, acyclic epsilon arcs) and return
- * the device bytes wd_graph_load needs in *bytes.  WD_EINVAL / WD_ECYCLE. */
+ * the device bytes wd_graph_load needs in *bytes.  WD_EINVAL / WD_ECYCLE.
+ * Epsilon depth limit: the epsilon closure runs one pass per epsilon level
+ * (the longest epsilon path into a state; the paper leaves epsilon handling
+ * open), and a level is stored in one byte, so every state that HAS epsilon
+ * out-arcs must sit at level <= 253 (a chain of at most 254 epsilon arcs);
+ * a deeper graph is rejected with WD_EINVAL (message "epsilon chains deeper
+ * than 254") although its decode would be defined.  States reached by longer
+ * chains but without epsilon arcs of their own are accepted. */
 wd_status wd_graph_bytes(const wd_graph_desc* d, size_t* bytes);
 
 /* Lay the graph out in `dev_buf` (device, >= wd_graph_bytes, 256-byte
@@ -196,6 +226,15 @@ void wd_graph_free(wd_graph* g);
 
 /* Number of epsilon levels (longest epsilon chain + 1, 0 without epsilon arcs). */
 int32_t wd_graph_eps_levels(const wd_graph* g);
+
+/* Epsilon paths in the graph's path table: every path of one or more
+ * epsilon arcs out of every state, enumerated at load (with their weights
+ * and last arcs) so that the one-workgroup epsilon closure relaxes all
+ * levels in one round (see WD_FLAG_EPS_LEVELS); 0 when the graph has no
+ * epsilon arcs, more than 2^27 such paths or one longer than 16 arcs (the
+ * closure then goes level by level).  The table takes 20 + 4 * (longest
+ * path - 1) bytes per path of device memory (part of wd_graph_bytes). */
+int64_t wd_graph_eps_paths(const wd_graph* g);
 
 /* ---- decoding --------------------------------------------------------- */
 
@@ -325,6 +364,11 @@ int64_t wd_result_raw_lattice(const wd_result* r, const wd_lat_arc** arcs);    /
  * the beam cutoff and the final cutoff; returns T+1. */
 int32_t wd_result_cutoffs(const wd_result* r, const float** best, const float** cutoff_beam,
                           const float** cutoff);
+/* WD_FLAG_PHASES: per decoded frame t = 0..T (streams: every frame) the
+ * WD_PHASE_SLOTS words above, frame after frame, in *stamps; *tick_hz (may be
+ * NULL) receives the stamps' clock rate.  Returns the number of frames (0
+ * without the flag). */
+int32_t wd_result_phases(const wd_result* r, const uint64_t** stamps, double* tick_hz);
 void    wd_result_stats(const wd_result* r, wd_stats* s);
 void    wd_result_free(wd_result* r);
 

@@ -7,6 +7,7 @@
 // the paper's sequence parallelism (Sec. 4.2) done in one process.
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -32,6 +33,7 @@ namespace {
 
 struct Caps {
   uint64_t frame, arcs, nodes, links, kept, raw, words, win;
+  uint64_t prof;  // step-profile words per utterance (WD_FLAG_PHASES)
 };
 
 // Execution mode: chip-wide kernels per frame for frames too large for one
@@ -65,6 +67,7 @@ Caps resolve_caps(const wd_graph* g, int32_t max_T, const wd_params* p, const wd
   if (incremental_prune(p))
     r.win = (c && c->window_links > 0) ? (uint64_t)c->window_links : std::max<uint64_t>(r.links / 4, 1);
   r.words = T1 * (g->nlevels + 1) + 1;
+  r.prof = (p->flags & WD_FLAG_PHASES) ? T1 * (uint64_t)kProfSlots : 0;
   return r;
 }
 
@@ -83,8 +86,7 @@ struct Regions {
   uint64_t total;
 };
 
-Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base,
-              std::vector<LaneDesc>* lanes) {
+Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base, LaneDesc* lanes) {
   Regions R{};
   uint64_t p = 0;
   auto take = [&](uint64_t per_lane_bytes) -> char* {
@@ -143,13 +145,14 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
   char* out_raw = take(sizeof(OutLink) * c.raw);
   char* out_nodes = take(sizeof(OutNode) * (2 * c.kept + 1));
   char* out_words = take(4 * c.words);
+  char* prof = take(8 * c.prof);
   R.total = p;
   R.slot = (unsigned long long*)slot;
   R.bitmap = (uint32_t*)bitmap;
   R.used = (uint32_t*)used;
   if (lanes) {
     for (int b = 0; b < B; ++b) {
-      LaneDesc& L = (*lanes)[b];
+      LaneDesc& L = lanes[b];
       auto at = [&](char* region, uint64_t per_lane) { return region + (uint64_t)b * per_lane; };
       L.frame_cap = c.frame;
       L.cand_cap = c.arcs;
@@ -200,6 +203,7 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
       L.out_raw = (decltype(L.out_raw))at(out_raw, sizeof(OutLink) * c.raw);
       L.out_nodes = (decltype(L.out_nodes))at(out_nodes, sizeof(OutNode) * (2 * c.kept + 1));
       L.out_words = (decltype(L.out_words))at(out_words, 4 * c.words);
+      L.prof = c.prof ? (decltype(L.prof))at(prof, 8 * c.prof) : nullptr;
       L.info = (decltype(L.info))(R.info + b);
     }
   }
@@ -213,6 +217,8 @@ wd_status check_params(const wd_params* p) {
   if (!(p->lattice_beam >= 0.0f)) return fail(WD_EINVAL, "decode: lattice_beam must be >= 0");
   if ((p->flags & WD_FLAG_ONE_WORKGROUP) && (p->flags & WD_FLAG_CHIP_WIDE))
     return fail(WD_EINVAL, "decode: WD_FLAG_ONE_WORKGROUP and WD_FLAG_CHIP_WIDE are exclusive");
+  if ((p->flags & WD_FLAG_PHASES) && chip_wide_mode(p))
+    return fail(WD_EINVAL, "decode: WD_FLAG_PHASES profiles the one-workgroup forward pass only");
   return WD_OK;
 }
 
@@ -228,6 +234,8 @@ struct wd_result {
   std::vector<wd_lat_node> nodes;
   std::vector<wd_token> tokens;
   std::vector<float> best, cutb, cut;
+  std::vector<uint64_t> prof;  // WD_FLAG_PHASES: (T+1) x WD_PHASE_SLOTS
+  double tick_hz = 0.0;
   wd_stats stats{};
 };
 
@@ -292,7 +300,7 @@ static wd_status run_setup(wd_stream* run, const wd_graph* g, int32_t B, const f
   run->c = resolve_caps(g, max_T, p, caps);
   run->lanes.assign((size_t)B, LaneDesc{});
   std::memset(run->lanes.data(), 0, sizeof(LaneDesc) * (size_t)B);
-  run->R = carve(g, B, max_T, run->c, (char*)ws, &run->lanes);
+  run->R = carve(g, B, max_T, run->c, (char*)ws, run->lanes.data());
   const Regions& R = run->R;
   if (ws_bytes < R.total)
     return fail(WD_EINVAL, "decode: workspace of " + std::to_string(ws_bytes) + " bytes, need " +
@@ -348,6 +356,36 @@ static wd_status run_frames(wd_stream* run, bool update) {
   for (int b = 0; b < B; ++b) run->next[b] = run->T[b] + 1;
   if (st == WD_OK) st = hip_check(hipGetLastError(), "launch");
   return st;
+}
+
+static wd_stats lane_stats(const LaneInfo& I, int32_t T, float fwd_ms, float lat_ms, bool debug) {
+  wd_stats stt{};
+  stt.frames = T;
+  stt.final_reached = I.final_used;
+  stt.arcs_expanded = (int64_t)I.arcs_expanded;
+  stt.tokens = (int64_t)I.tokens;
+  stt.max_tokens = (int64_t)I.max_tokens;
+  stt.raw_links = (int64_t)I.links;
+  stt.kept_links = (int64_t)I.kept;
+  stt.nodes = (int64_t)I.out_nodes;
+  stt.eps_arcs_expanded = (int64_t)I.eps_arcs;
+  stt.forward_ms = fwd_ms;
+  stt.lattice_ms = lat_ms;
+  stt.needed.frame_tokens = (int64_t)I.need_frame_tokens;
+  stt.needed.frame_arcs = (int64_t)I.need_frame_arcs;
+  stt.needed.nodes = (int64_t)I.tokens;
+  stt.needed.links = (int64_t)I.need_links;
+  stt.needed.window_links = (int64_t)I.need_window;
+  stt.needed.kept_links = (int64_t)std::max<uint64_t>(I.kept, debug ? I.links : 0);
+  return stt;
+}
+
+static const char* status_message(wd_status st) {
+  return st == WD_ENOPATH     ? "decode: no token survived a frame"
+         : st == WD_EINVAL    ? "decode: log-likelihoods contain NaN, +inf or values above 1e30"
+         : st == WD_ECAPACITY ? "decode: workspace capacity exceeded; see stats.needed"
+         : st == WD_EDEVICE   ? "decode: a kernel's internal consistency check failed"
+                              : "decode failed";
 }
 
 // Lattice pass, then the results of every utterance (synchronises).
@@ -414,34 +452,26 @@ static wd_status run_finish(wd_stream* run, wd_result** out) {
     wd_result* r = new wd_result();
     r->status = ls;
     r->cost = I.best_cost;
-    wd_stats& stt = r->stats;
-    stt.frames = Tb;
-    stt.final_reached = I.final_used;
-    stt.arcs_expanded = (int64_t)I.arcs_expanded;
-    stt.tokens = (int64_t)I.tokens;
-    stt.max_tokens = (int64_t)I.max_tokens;
-    stt.raw_links = (int64_t)I.links;
-    stt.kept_links = (int64_t)I.kept;
-    stt.nodes = (int64_t)I.out_nodes;
-    stt.eps_arcs_expanded = (int64_t)I.eps_arcs;
-    stt.forward_ms = fwd_ms;
-    stt.lattice_ms = lat_ms;
-    stt.needed.frame_tokens = (int64_t)I.need_frame_tokens;
-    stt.needed.frame_arcs = (int64_t)I.need_frame_arcs;
-    stt.needed.nodes = (int64_t)I.tokens;
-    stt.needed.links = (int64_t)I.need_links;
-    stt.needed.window_links = (int64_t)I.need_window;
-    stt.needed.kept_links = (int64_t)std::max<uint64_t>(I.kept, debug ? I.links : 0);
+    r->stats = lane_stats(I, Tb, fwd_ms, lat_ms, debug);
     out[b] = r;
     if (ls != WD_OK) continue;
     r->words.resize(I.nwords);
     r->links.resize(I.kept);
     r->nodes.resize(I.out_nodes);
-    if (packed) continue;  // copied below, all lanes at once
     auto d2h = [&](void* dst, const void* src, uint64_t bytes) -> wd_status {
       if (!bytes) return WD_OK;
       return hip_check(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s), "result download");
     };
+    if (L.prof) {
+      r->prof.resize(((size_t)Tb + 1) * kProfSlots);
+      int khz = 0, dev = 0;
+      if ((st = d2h(r->prof.data(), L.prof, 8 * r->prof.size())) ||
+          (st = hip_check(hipGetDevice(&dev), "device")) ||
+          (st = hip_check(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev), "clock rate")))
+        return st;
+      r->tick_hz = 1e3 * khz;
+    }
+    if (packed) continue;  // copied below, all lanes at once
     if ((st = d2h(r->words.data(), L.out_words, 4 * I.nwords)) ||
         (st = d2h(r->links.data(), L.out_links, sizeof(OutLink) * I.kept)) ||
         (st = d2h(r->nodes.data(), L.out_nodes, sizeof(OutNode) * I.out_nodes)))
@@ -481,14 +511,7 @@ static wd_status run_finish(wd_stream* run, wd_result** out) {
       std::memcpy(r->words.data(), src, 4 * r->words.size());
     }
   if ((st = hip_check(hipStreamSynchronize(s), "result download"))) return st;
-  if (first_bad != WD_OK) {
-    std::string msg = first_bad == WD_ENOPATH   ? "decode: no token survived a frame"
-                      : first_bad == WD_EINVAL  ? "decode: log-likelihoods contain NaN, +inf or values above 1e30"
-                      : first_bad == WD_ECAPACITY ? "decode: workspace capacity exceeded; see stats.needed"
-                      : first_bad == WD_EDEVICE ? "decode: a kernel's internal consistency check failed"
-                                                : "decode failed";
-    set_error(msg);
-  }
+  if (first_bad != WD_OK) set_error(status_message(first_bad));
   return first_bad;
 }
 
@@ -609,6 +632,11 @@ extern "C" int32_t wd_result_cutoffs(const wd_result* r, const float** b, const 
   *cb = r->cutb.data();
   *c = r->cut.data();
   return (int32_t)r->best.size();
+}
+extern "C" int32_t wd_result_phases(const wd_result* r, const uint64_t** stamps, double* tick_hz) {
+  *stamps = r->prof.data();
+  if (tick_hz) *tick_hz = r->tick_hz;
+  return (int32_t)(r->prof.size() / kProfSlots);
 }
 extern "C" void wd_result_stats(const wd_result* r, wd_stats* s) { *s = r->stats; }
 extern "C" void wd_result_free(wd_result* r) { delete r; }

@@ -124,6 +124,12 @@ __device__ __forceinline__ uint64_t block_sum64(uint64_t v, BlockScratch& bs, ui
   return r;
 }
 
+__device__ __forceinline__ uint32_t wave_or(uint32_t v) {
+#pragma unroll
+  for (int m = 32; m > 0; m >>= 1) v |= __shfl_xor(v, m, 64);
+  return v;
+}
+
 template <int NW = kWaves>
 __device__ __forceinline__ uint32_t block_or(uint32_t v, BlockScratch& bs, uint32_t& par) {
   const uint32_t b = par;

@@ -24,6 +24,10 @@ constexpr int kHashMax = 2048;              // LDS token table entries before a 
 constexpr int kFrontCap = 1024;             // frontier tokens held in LDS
 constexpr int kHistBins = 2048;             // 11-bit radix digits for max-active
 constexpr uint32_t kInfKey = 0xff800000u;   // key of +inf
+constexpr uint32_t kPathMaxLen = 16;        // epsilon paths longer than this: no path table
+constexpr uint64_t kPathMax = 1ull << 27;   // more epsilon paths than this: no path table
+constexpr int kProfStamps = 10;             // step boundaries stamped per frame (WD_FLAG_PHASES)
+constexpr int kProfSlots = kProfStamps + 2; // + two words describing the frame
 
 // Order-preserving map of fp32 onto u32 (-0.0 folded onto +0.0): for non-NaN
 // a, b: a < b  <=>  cost_key(a) < cost_key(b).
@@ -63,6 +67,17 @@ struct DevGraph {
   const int32_t* olabel_id;    // [A]
   const float* weight_id;      // [A]
   const uint32_t* level_base;  // [nlevels + 1] bucket offsets of the epsilon levels
+  // Epsilon paths (every path of one or more epsilon arcs out of a state,
+  // enumerated when the graph is loaded; npaths = 0 when the graph has too
+  // many or too long ones).  Paths of state s: [pfirst[s], pfirst[s+1]).
+  //   phead[p] = {last state, last arc id, last arc's weight bits, k | xdeg << 8}
+  //     k = number of arcs, xdeg = epsilon out-degree of the last state
+  //   ptail[p * pstride + i] = weight of arc i < k - 1 (pstride = longest path - 1)
+  const uint32_t* pfirst;
+  const uint4* phead;
+  const float* ptail;
+  uint64_t npaths;
+  uint32_t pstride;
   uint32_t S;
   uint32_t start;
   uint32_t nlevels;
@@ -211,6 +226,7 @@ struct LaneDesc {
   WD_GLOBAL OutNode* out_nodes;          // [2*kept_cap+1]
   WD_GLOBAL int32_t* out_words;          // [word_cap]
   WD_GLOBAL LaneInfo* info;
+  WD_GLOBAL uint64_t* prof;              // [(T+1) * kProfSlots] step profile (WD_FLAG_PHASES)
 };
 
 }  // namespace wd

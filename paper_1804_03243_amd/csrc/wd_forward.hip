@@ -17,6 +17,7 @@
 // touches more states than the table holds is redone from the same frontier on
 // the global per-state slot array (its inputs are unchanged, so the result is
 // identical).  The frontier itself is kept in LDS when it fits.
+#include "../../include/wfstdec.h"
 #include "wd_block.h"
 
 namespace wd {
@@ -41,6 +42,7 @@ struct FwdShared {
   uint32_t sel_before;
   uint32_t lvl_tot;    // LDS table: work items of the current epsilon level
   uint32_t lvl_wide;   // LDS table: first epsilon level the whole workgroup runs
+  uint32_t lvl_live;   // LDS table: levels that may hold an entry within the cutoff (level_bit)
   unsigned long long deg_tot;  // frontier out-degree totals (epsilon << 32 | emitting), small frames
   uint32_t hcount;     // LDS table: reserved entries
   uint32_t spill;      // LDS table full: the frame goes global
@@ -168,6 +170,36 @@ __device__ __forceinline__ void lds_bucket(FwdShared& sh, uint32_t slot, uint2 o
   }
 }
 
+// The same with the graph's epsilon path table: the state's path range and
+// its epsilon out-degree (empty range: a state reached by an epsilon path,
+// whose own paths are extensions of that path).
+__device__ __forceinline__ void lds_bucket_paths(FwdShared& sh, uint32_t slot, uint32_t p0, uint32_t p1,
+                                                 uint32_t xdeg) {
+  const uint32_t b = atomicAdd(&sh.n_bk, 1u);
+  if (b < kBkCap) sh.bk[b] = make_uint4(slot, p0, p1, xdeg);
+  else sh.spill = 1;
+}
+
+// Epsilon levels as bits of a mask: bit l for level l < 31, bit 31 for every
+// level from 31 on.
+__device__ __forceinline__ uint32_t level_bit(uint32_t l) { return 1u << (l < 31u ? l : 31u); }
+
+// Lowest level >= from whose bit is set in mask (levels from 31 on are taken
+// one after another while bit 31 is set); nlevels when there is none.
+__device__ __forceinline__ uint32_t next_live(uint32_t mask, uint32_t from, uint32_t nlevels) {
+  if (from >= nlevels) return nlevels;
+  if (from < 31u) {
+    const uint32_t m = mask & 0x7fffffffu & (~0u << from);
+    if (m) {
+      const uint32_t l = (uint32_t)__ffs(m) - 1u;
+      return l < nlevels ? l : nlevels;
+    }
+    from = 31u;
+    if (from >= nlevels) return nlevels;
+  }
+  return (mask & 0x80000000u) ? from : nlevels;
+}
+
 // ------------------------------------------------------------- global table
 
 // Record a first touch of `dst` this frame: touched list (ballot-aggregated)
@@ -221,11 +253,15 @@ __device__ __forceinline__ uint64_t uniform64(uint64_t v) {
          (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
 }
 
-__global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc* __restrict__ lanes,
-                                                      Params prm, const uint32_t* __restrict__ bad) {
-  __shared__ FwdShared sh;
+// kProf: the step-profile copy (WD_FLAG_PHASES), which stores the device
+// wall clock at each step boundary of every frame (thread 0).
+template <bool kProf>
+__device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, const LaneDesc* __restrict__ lanes,
+                                             const Params& prm, const uint32_t* __restrict__ bad) {
   const LaneDesc& L = lanes[blockIdx.x];
   const uint32_t tid = threadIdx.x;
+  // epsilon closure of LDS-table frames: every path at once, or level by level
+  const bool paths = g.npaths != 0 && !(prm.flags & WD_FLAG_EPS_LEVELS);
   if (bad[blockIdx.x]) {
     if (tid == 0) L.info->status = 1;  // WD_EINVAL
     return;
@@ -265,6 +301,18 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
   bool hist_ok = true;  // history (nodes, links) still being stored
   uint32_t par = 0;     // scratch buffer parity of the workgroup collectives
   int t = L.t0;
+  // step profile: slot k < kProfStamps of frame t gets the wall clock when
+  // thread 0 passes step boundary k; the last two slots describe the frame
+  auto stamp = [&](int k) {
+    if constexpr (kProf) {
+      if (tid == 0) L.prof[(size_t)t * kProfSlots + (size_t)k] = wall_clock64();
+    }
+  };
+  auto note = [&](int k, uint64_t v) {
+    if constexpr (kProf) {
+      if (tid == 0) L.prof[(size_t)t * kProfSlots + (size_t)k] = v;
+    }
+  };
   if (t > 0) {
     // a stream resumes after frame t - 1: the state the last launch left in
     // LaneInfo, the frontier in the workspace.  A full node or link store
@@ -295,6 +343,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
   }
 
   for (; t <= T; ++t) {
+    stamp(0);
     if (t > 0) {
       if (tid == 0 && W > sh.c_need_arcs) sh.c_need_arcs = W;
       if (W > L.cand_cap) {
@@ -326,10 +375,14 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             const uint32_t slot = h_insert(sh, s0, &fresh);
             sh.h_val[slot] = pack_tok(cost_key(0.0f), kNoArc);
             const uint32_t c = g.sclass[s0];
-            if (c != kNoEps) lds_bucket(sh, slot, g.off[s0], g.off[s0 + 1], c);
+            if (c != kNoEps) {
+              if (paths) lds_bucket_paths(sh, slot, g.pfirst[s0], g.pfirst[s0 + 1], g.off[s0 + 1].y - g.off[s0].y);
+              else lds_bucket(sh, slot, g.off[s0], g.off[s0 + 1], c);
+            }
           }
           best_key = cost_key(0.0f);
           __syncthreads();
+          stamp(1);
         } else {
           uint32_t my_best = 0xffffffffu;
           for (uint32_t base = 0; base < W; base += kThreads) {
@@ -340,8 +393,14 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             const uint4 r = g.earc[fp.ebeg[i] + (w - fp.edeg[i])];
             const uint32_t dst = r.x, cls = r.z >> 24;
             // CSR offsets of the destination: the epsilon range for the bucket,
-            // and warm in cache for the degree pass if the token survives
+            // and warm in cache for the degree pass if the token survives;
+            // with the path table, the range of its epsilon paths
             const uint2 o0 = g.off[dst], o1 = g.off[dst + 1];
+            uint32_t p0 = 0, p1 = 0;
+            if (paths && cls != kNoEps) {
+              p0 = g.pfirst[dst];
+              p1 = g.pfirst[dst + 1];
+            }
             const float ac = -row[(r.z & 0xffffffu) - 1u];
             float x = c + ac;
             x = canon(x + __uint_as_float(r.y));
@@ -356,9 +415,13 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
                 if (slot < (uint32_t)kHashCap) {
                   atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
                   if (fresh && cls != kNoEps) {
-                    lds_bucket(sh, slot, o0, o1, cls);
-                    // start the state's first epsilon arc on its way for the closure
-                    warm = __uint_as_float(g.xarc[o0.y].y);
+                    if (paths) {
+                      lds_bucket_paths(sh, slot, p0, p1, o1.y - o0.y);
+                    } else {
+                      lds_bucket(sh, slot, o0, o1, cls);
+                      // start the state's first epsilon arc on its way for the closure
+                      warm = __uint_as_float(g.xarc[o0.y].y);
+                    }
                   }
                 }
               }
@@ -372,6 +435,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           }
           // (the collective's barrier also publishes the table writes)
           best_key = (uint32_t)block_min64(my_best, sh.bs, par);
+          stamp(1);
           if (best_key >= kInfKey) {
             status = 3;  // WD_ENOPATH
             failed = true;
@@ -384,6 +448,94 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         }
         const float cutb = key_cost(best_key) + prm.beam;
         kcutb = cost_key(cutb);
+        // each entry writes its index at its work items, so a work item
+        // finds its entry with one LDS read (rs_slot is free until the
+        // closure ends)
+        uint16_t* own = reinterpret_cast<uint16_t*>(sh.rs_slot);
+        constexpr uint32_t kOwnCap = 2u * (uint32_t)kRankMax;
+        if (paths) {
+          // Every epsilon path of every bucket entry within the cutoff, all
+          // levels at once: a path's cost adds its arcs' weights to the
+          // entry's cost in path order, rounding after each addition, which
+          // is what one pass per level computes for the path's last state
+          // (rounding is monotone, so the minimum over the paths into a
+          // state is the level-by-level token, arc ids included; an entry
+          // whose cost later drops through another path only offers the
+          // sums of longer paths that are themselves in the table).  One
+          // round of dependent loads instead of one per level.
+          auto relax_path = [&](uint32_t j, uint32_t w) {
+            const uint4 e = sh.bk[j];
+            const uint32_t pth = e.y + (w - sh.xp[j]);
+            const uint4 h = g.phead[pth];
+            const uint32_t k = h.w & 0xffu;
+            float x = key_cost((uint32_t)(sh.h_val[e.x] >> 32));
+            if (k > 1u) {
+              const float* tw = g.ptail + (size_t)pth * g.pstride;
+              const float w0 = tw[0];
+              const float w1 = k > 2u ? tw[1] : 0.0f;
+              const float w2 = k > 3u ? tw[2] : 0.0f;
+              x = canon(x + w0);
+              if (k > 2u) x = canon(x + w1);
+              if (k > 3u) x = canon(x + w2);
+              for (uint32_t i = 3; i + 1 < k; ++i) x = canon(x + tw[i]);
+            }
+            const uint32_t xk = cost_key(canon(x + __uint_as_float(h.z)));
+            if (xk > kcutb || xk >= kInfKey || sh.spill) return;
+            bool fresh;
+            const uint32_t slot = h_insert(sh, h.x, &fresh);
+            if (slot < (uint32_t)kHashCap) {
+              atomicMin(&sh.h_val[slot], pack_tok(xk, h.y));
+              if (fresh && (h.w >> 8)) lds_bucket_paths(sh, slot, 0, 0, h.w >> 8);
+            }
+          };
+          const uint32_t n = sh.n_bk < kBkCap ? sh.n_bk : kBkCap;
+          uint32_t d = 0;
+          if (tid < n) {
+            const uint4 e = sh.bk[tid];
+            if ((uint32_t)(sh.h_val[e.x] >> 32) <= kcutb) d = e.z - e.y;
+          }
+          uint32_t tot;
+          if (n <= 64u) {
+            // every entry in the first wavefront: its scan needs no workgroup
+            // barrier, and when the paths fit its lanes it relaxes them alone
+            if (tid < 64u) {
+              const uint32_t inc = wave_incl_scan(d), ex = inc - d;
+              const uint32_t all = __shfl(inc, 63, 64);
+              sh.xp[tid] = ex;
+              if (all <= kOwnCap)
+                for (uint32_t k = 0; k < d; ++k) own[ex + k] = (uint16_t)tid;
+              if (tid == 63u) sh.lvl_tot = all;
+              __builtin_amdgcn_wave_barrier();
+              if (all <= 64u && tid < all) relax_path(own[tid], tid);
+            }
+            __syncthreads();
+            tot = sh.lvl_tot;
+          } else {
+            const uint32_t ex = block_excl_scan(d, sh.bs, par, &tot);
+            sh.xp[tid] = ex;
+            if (tot <= kOwnCap)
+              for (uint32_t k = 0; k < d; ++k) own[ex + k] = (uint16_t)tid;
+            __syncthreads();
+          }
+          // (uniform: n and tot are the same in every thread)
+          if (n > 64u || tot > 64u) {
+            const bool by_owner = tot <= kOwnCap;
+            for (uint32_t w = tid; w < tot; w += kThreads)
+              relax_path(by_owner ? (uint32_t)own[w] : search_le(sh.xp, n, w), w);
+            __syncthreads();
+          }
+          if (sh.spill) {
+            lds = false;
+            continue;
+          }
+          // the epsilon out-arcs of the closure's states within the cutoff
+          // (the arcs-expanded count); the entries' costs are final
+          const uint32_t nb = sh.n_bk < kBkCap ? sh.n_bk : kBkCap;
+          for (uint32_t j = tid; j < nb; j += kThreads) {
+            const uint4 e = sh.bk[j];
+            if ((uint32_t)(sh.h_val[e.x] >> 32) <= kcutb) eps_frame += e.w;
+          }
+        } else {
         // one epsilon arc of a level: work item w of bucket entry j
         auto relax_eps = [&](uint32_t j, uint32_t w) {
           const uint4 e = sh.bk[j];
@@ -397,14 +549,34 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           const uint32_t slot = h_insert(sh, r.x, &fresh);
           if (slot < (uint32_t)kHashCap) {
             atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
-            if (fresh && r.z != kNoEps) lds_bucket(sh, slot, make_uint2(0, nx.x), make_uint2(0, nx.y), r.z);
+            if (r.z != kNoEps) {
+              // the destination's level now holds an entry within the cutoff
+              atomicOr(&sh.lvl_live, level_bit(r.z));
+              if (fresh) lds_bucket(sh, slot, make_uint2(0, nx.x), make_uint2(0, nx.y), r.z);
+            }
           }
         };
-        // each entry writes its index at its work items, so a work item
-        // finds its entry with one LDS read (rs_slot is free until the
-        // closure ends)
-        uint16_t* own = reinterpret_cast<uint16_t*>(sh.rs_slot);
-        constexpr uint32_t kOwnCap = 2u * (uint32_t)kRankMax;
+        // The levels that hold a bucket entry within the cutoff: only they
+        // relax epsilon arcs (most frames have none, or one or two of the
+        // graph's levels).  Every insertion within the cutoff into a state
+        // with epsilon arcs adds its level.
+        // (Wavefront 0 builds the mask when every entry is in its lanes and
+        // reads it in program order; the others read it after the next
+        // barrier.  With more entries every level is taken.)
+        if (tid < 64u) {
+          const uint32_t nbk0 = sh.n_bk;  // (published by the last barrier)
+          uint32_t m = ~0u;
+          if (nbk0 <= 64u) {
+            m = 0;
+            if (tid < nbk0) {
+              const uint4 e = sh.bk[tid];
+              if ((uint32_t)(sh.h_val[e.x] >> 32) <= kcutb) m = level_bit(e.w);
+            }
+            m = wave_or(m);
+          }
+          if (tid == 0) sh.lvl_live = m;
+          __builtin_amdgcn_wave_barrier();
+        }
         // Levels whose bucket entries and epsilon arcs each fit in one
         // wavefront run in wavefront 0 alone, one after another, with no
         // workgroup barrier: a wavefront's LDS accesses take effect in
@@ -412,8 +584,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         // first level that does not fit, and the levels after it, run on the
         // whole workgroup below.
         if (tid < 64u) {
-          uint32_t lvl = 0;
-          for (; lvl < g.nlevels; ++lvl) {
+          uint32_t lvl = next_live(sh.lvl_live, 0, g.nlevels);
+          for (; lvl < g.nlevels; lvl = next_live(sh.lvl_live, lvl + 1, g.nlevels)) {
             if (sh.spill) {
               lvl = g.nlevels;
               break;
@@ -439,7 +611,10 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           if (tid == 0) sh.lvl_wide = lvl;
         }
         __syncthreads();
-        for (uint32_t lvl = sh.lvl_wide; lvl < g.nlevels; ++lvl) {
+        // (lvl_live changes only in a level's relaxation, after that level's
+        // scan barrier, which every thread passes after reading it here)
+        for (uint32_t lvl = next_live(sh.lvl_live, sh.lvl_wide, g.nlevels); lvl < g.nlevels;
+             lvl = next_live(sh.lvl_live, lvl + 1, g.nlevels)) {
           if (sh.nbl[lvl] == 0) continue;  // uniform: written only by lower levels
           // this level's entries within the cutoff spread their epsilon arcs
           // over the workgroup: entry i (one per thread) owns arcs
@@ -484,6 +659,8 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           lds = false;
           continue;
         }
+        }  // level by level
+        stamp(2);
         // survivors of the beam cutoff, straight from the table
         const uint32_t span = kcutb - best_key;
         nbits = span ? 32u - (uint32_t)__clz(span) : 0u;
@@ -511,6 +688,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         }
         __syncthreads();
         ns = sh.n_surv;
+        stamp(3);
         if (tid == 0 && sh.hcount > sh.c_need_frame) sh.c_need_frame = sh.hcount;
       } else {
         // --------------------------------------- global per-state slot array
@@ -528,6 +706,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           }
           best_key = cost_key(0.0f);
           __syncthreads();
+          stamp(1);
         } else {
           uint32_t my_best = 0xffffffffu;
           for (uint32_t base = 0; base < W; base += kThreads) {
@@ -556,6 +735,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
             note_touch(first, dst, cls, sh, g, L);
           }
           best_key = (uint32_t)block_min64(my_best, sh.bs, par);
+          stamp(1);
           if (best_key >= kInfKey) {
             status = 3;  // WD_ENOPATH
             failed = true;
@@ -585,6 +765,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
           }
           __syncthreads();
         }
+        stamp(2);
         const uint32_t nt = sh.n_touched;
         if (tid == 0 && nt > sh.c_need_frame) sh.c_need_frame = nt;
         if (nt > L.frame_cap) {
@@ -616,6 +797,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
         }
         __syncthreads();
         ns = sh.n_surv;
+        stamp(3);
       }
       break;
     }
@@ -656,6 +838,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       const uint32_t vkey = best_key + prefix;
       cut_key = vkey < kcutb ? vkey : kcutb;
     }
+    stamp(4);
     // -------------------------------- compaction into a frontier sorted by state
     const bool fl = n_keep <= (uint32_t)kFrontCap;
     const Front f = front_at(fl, sh, L);
@@ -824,6 +1007,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       }
     }
     __syncthreads();
+    stamp(5);
     // ------------------------------- arc offsets and degree prefix sums
     uint32_t W_next, W_eps;
     if (deg_ready) {
@@ -895,6 +1079,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       }
       __syncthreads();
     }
+    stamp(6);
     // owners of the next frame's emitting work items, written by threads
     // 256..511 (idle in the link pass of small frames)
     const bool own_e_ok = fl && W_next <= kOwnE;
@@ -976,6 +1161,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       uint32_t pos = (uint32_t)ex2, posx = (uint32_t)(ex2 >> 32);
       nE = (uint32_t)tot2;
       nX = (uint32_t)(tot2 >> 32);
+      stamp(7);
       if (hist_ok && link_base + nE + nX > L.link_cap) {
         hist_ok = false;
         ovf |= kOvfLinks;
@@ -1033,6 +1219,9 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
     // insertions to undo, read before the barrier after which thread 0 resets the count
     const uint32_t h_used_n = sh.hcount < (uint32_t)kHashMax ? sh.hcount : (uint32_t)kHashMax;
     const uint32_t fl_or = block_or((bad_idx ? 0x80000000u : 0u) | xmask, sh.bs, par);
+    stamp(8);
+    note(kProfStamps, (lds ? 1ull : 0ull) | ((uint64_t)n_keep << 8) | ((uint64_t)(nE + nX) << 32));
+    note(kProfStamps + 1, (t > 0 ? (uint64_t)W : 0ull) | ((uint64_t)(lds ? sh.n_bk : 0u) << 32));
     if (fl_or & 0x80000000u) {
       status = kStatusInternal;
       break;
@@ -1062,6 +1251,7 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
       sh.n_rank = 0;
     }
     __syncthreads();
+    stamp(9);
   }
 
   if (L.open && front_lds) {  // an open stream resumes from the workspace frontier
@@ -1097,9 +1287,24 @@ __global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc
   }
 }
 
+__global__ void __launch_bounds__(kThreads) k_forward(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                      Params prm, const uint32_t* __restrict__ bad) {
+  __shared__ FwdShared sh;
+  forward_body<false>(sh, g, lanes, prm, bad);
+}
+
+__global__ void __launch_bounds__(kThreads) k_forward_phases(DevGraph g, const LaneDesc* __restrict__ lanes,
+                                                             Params prm, const uint32_t* __restrict__ bad) {
+  __shared__ FwdShared sh;
+  forward_body<true>(sh, g, lanes, prm, bad);
+}
+
 void launch_forward(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm,
                     const uint32_t* bad, hipStream_t s) {
-  hipLaunchKernelGGL(k_forward, dim3(B), dim3(kThreads), 0, s, g, lanes, prm, bad);
+  if (prm.flags & WD_FLAG_PHASES)
+    hipLaunchKernelGGL(k_forward_phases, dim3(B), dim3(kThreads), 0, s, g, lanes, prm, bad);
+  else
+    hipLaunchKernelGGL(k_forward, dim3(B), dim3(kThreads), 0, s, g, lanes, prm, bad);
 }
 
 }  // namespace wd

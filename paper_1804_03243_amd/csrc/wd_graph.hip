@@ -8,6 +8,7 @@
 // climbs to a higher level.  Beside each epsilon arc sits its destination's
 // epsilon arc range, so a closure step that reaches a state with epsilon arcs
 // needs no second, dependent read of the offsets.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -26,13 +27,19 @@ struct Prepared {
   std::vector<uint8_t> sclass;
   std::vector<uint32_t> level_base;
   uint32_t nlevels = 0;
+  std::vector<uint32_t> pfirst;  // epsilon path table (empty: none)
+  std::vector<uint4> phead;
+  std::vector<float> ptail;
+  uint32_t pstride = 0;
 };
 
 struct Layout {
-  uint64_t off, earc, xarc, xnext, sclass, final_w, ilabel, olabel, weight, level_base, total;
+  uint64_t off, earc, xarc, xnext, sclass, final_w, ilabel, olabel, weight, level_base, pfirst, phead, ptail,
+      total;
 };
 
-Layout layout(int64_t S, int64_t A, uint64_t Ae, uint64_t Ax, uint32_t nlevels, bool finals) {
+Layout layout(int64_t S, int64_t A, uint64_t Ae, uint64_t Ax, uint32_t nlevels, bool finals, uint64_t npaths,
+              uint32_t pstride) {
   Layout l{};
   uint64_t p = 0;
   auto take = [&](uint64_t bytes) {
@@ -50,6 +57,9 @@ Layout layout(int64_t S, int64_t A, uint64_t Ae, uint64_t Ax, uint32_t nlevels, 
   l.olabel = take(sizeof(int32_t) * (uint64_t)(A ? A : 1));
   l.weight = take(sizeof(float) * (uint64_t)(A ? A : 1));
   l.level_base = take(sizeof(uint32_t) * (uint64_t)(nlevels + 1));
+  l.pfirst = npaths ? take(sizeof(uint32_t) * (uint64_t)(S + 1)) : 0;
+  l.phead = npaths ? take(sizeof(uint4) * npaths) : 0;
+  l.ptail = npaths && pstride ? take(sizeof(float) * npaths * pstride) : 0;
   l.total = p;
   return l;
 }
@@ -85,12 +95,12 @@ wd_status validate(const wd_graph_desc* d) {
 
 // Longest epsilon path into every state, by Kahn's order over epsilon arcs;
 // WD_ECYCLE when some state is never freed.
-wd_status eps_levels(const wd_graph_desc* d, std::vector<uint32_t>& level) {
+wd_status eps_levels(const wd_graph_desc* d, std::vector<uint32_t>& level, std::vector<uint32_t>& queue) {
   const int64_t S = d->num_states;
   std::vector<uint32_t> indeg((size_t)S, 0);
   for (int64_t a = 0; a < d->num_arcs; ++a)
     if (d->ilabel[a] == 0) indeg[d->dst[a]]++;
-  std::vector<uint32_t> queue;
+  queue.clear();
   queue.reserve((size_t)S);
   level.assign((size_t)S, 0);
   for (int64_t s = 0; s < S; ++s)
@@ -108,12 +118,83 @@ wd_status eps_levels(const wd_graph_desc* d, std::vector<uint32_t>& level) {
   return WD_OK;
 }
 
+// Every epsilon path out of every state (the closure's alternative to one
+// pass per level: a token's epsilon paths are relaxed all at once, each
+// path's weights added in path order).  Left empty when the graph has more
+// than kPathMax paths or one longer than kPathMaxLen arcs.  Per state the
+// paths are listed depth first, arcs in the caller's order.
+void eps_paths(const wd_graph_desc* d, const std::vector<uint32_t>& topo, Prepared& p) {
+  const int64_t S = d->num_states;
+  std::vector<uint64_t> npath((size_t)S, 0);
+  std::vector<uint32_t> maxlen((size_t)S, 0), xdeg((size_t)S, 0);
+  uint64_t total = 0;
+  uint32_t longest = 0;
+  // destinations before sources: the reverse of a topological order
+  for (size_t h = topo.size(); h-- > 0;) {
+    const uint32_t s = topo[h];
+    uint64_t n = 0;
+    uint32_t len = 0;
+    for (uint32_t a = d->row_ptr[s]; a < d->row_ptr[s + 1]; ++a) {
+      if (d->ilabel[a] != 0) continue;
+      const uint32_t v = d->dst[a];
+      xdeg[s]++;
+      n += 1 + npath[v];
+      if (n > kPathMax) n = kPathMax + 1;  // (saturates: the table will not be built)
+      len = std::max(len, 1 + maxlen[v]);
+    }
+    npath[s] = n;
+    maxlen[s] = len;
+    total = std::min<uint64_t>(total + n, kPathMax + 1);
+    longest = std::max(longest, len);
+  }
+  if (total == 0 || total > kPathMax || longest > kPathMaxLen) return;
+  for (int64_t s = 0; s < S; ++s)
+    if (xdeg[s] >= (1u << 24)) return;
+  p.pstride = longest - 1;
+  p.pfirst.assign((size_t)S + 1, 0);
+  for (int64_t s = 0; s < S; ++s) p.pfirst[s + 1] = p.pfirst[s] + (uint32_t)npath[s];
+  p.phead.resize(total);
+  p.ptail.assign(total * p.pstride, 0.0f);
+  // depth-first walk of the epsilon arcs out of s: stack of (state, next arc)
+  std::vector<std::pair<uint32_t, uint32_t>> stack;
+  std::vector<float> wpath;  // weights of the current path's arcs
+  for (int64_t s = 0; s < S; ++s) {
+    if (!npath[s]) continue;
+    uint64_t at = p.pfirst[s];
+    stack.assign(1, {(uint32_t)s, d->row_ptr[s]});
+    wpath.clear();
+    while (!stack.empty()) {
+      auto& top = stack.back();
+      const uint32_t u = top.first;
+      uint32_t a = top.second;
+      while (a < d->row_ptr[u + 1] && d->ilabel[a] != 0) ++a;
+      if (a >= d->row_ptr[u + 1]) {
+        stack.pop_back();
+        if (!wpath.empty()) wpath.pop_back();
+        continue;
+      }
+      top.second = a + 1;
+      const uint32_t v = d->dst[a];
+      const uint32_t k = (uint32_t)wpath.size() + 1;
+      uint32_t wbits;
+      std::memcpy(&wbits, &d->weight[a], 4);
+      p.phead[at] = make_uint4(v, a, wbits, k | (xdeg[v] << 8));
+      for (uint32_t i = 0; i + 1 < k; ++i) p.ptail[at * p.pstride + i] = wpath[i];
+      ++at;
+      if (xdeg[v]) {
+        wpath.push_back(d->weight[a]);
+        stack.push_back({v, d->row_ptr[v]});
+      }
+    }
+  }
+}
+
 wd_status prepare(const wd_graph_desc* d, Prepared& p, uint64_t* Ae_out, uint64_t* Ax_out) {
   wd_status st = validate(d);
   if (st != WD_OK) return st;
   const int64_t S = d->num_states, A = d->num_arcs;
-  std::vector<uint32_t> level;
-  st = eps_levels(d, level);
+  std::vector<uint32_t> level, topo;
+  st = eps_levels(d, level, topo);
   if (st != WD_OK) return st;
   p.sclass.assign((size_t)S, (uint8_t)kNoEps);
   std::vector<uint32_t> count(kMaxLevels + 1, 0);
@@ -158,6 +239,7 @@ wd_status prepare(const wd_graph_desc* d, Prepared& p, uint64_t* Ae_out, uint64_
     const uint32_t v = p.xarc[j].x;
     p.xnext[j] = make_uint2(p.off[v].y, p.off[v + 1].y);
   }
+  eps_paths(d, topo, p);
   (void)A;
   *Ae_out = Ae;
   *Ax_out = Ax;
@@ -176,7 +258,8 @@ extern "C" wd_status wd_graph_bytes(const wd_graph_desc* d, size_t* bytes) {
   uint64_t Ae, Ax;
   wd_status st = prepare(d, p, &Ae, &Ax);
   if (st != WD_OK) return st;
-  *bytes = layout(d->num_states, d->num_arcs, Ae, Ax, p.nlevels, d->final_weight != nullptr).total;
+  *bytes = layout(d->num_states, d->num_arcs, Ae, Ax, p.nlevels, d->final_weight != nullptr, p.phead.size(),
+                  p.pstride).total;
   return WD_OK;
 }
 
@@ -191,7 +274,8 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
   if (st != WD_OK) return st;
   const int64_t S = d->num_states, A = d->num_arcs;
   const bool finals = d->final_weight != nullptr;
-  const Layout l = layout(S, A, Ae, Ax, p.nlevels, finals);
+  const uint64_t npaths = p.phead.size();
+  const Layout l = layout(S, A, Ae, Ax, p.nlevels, finals, npaths, p.pstride);
   if (dev_bytes < l.total) return fail(WD_EINVAL, "graph_load: dev_buf smaller than wd_graph_bytes");
   hipStream_t s = (hipStream_t)stream;
   char* base = (char*)dev_buf;
@@ -208,7 +292,10 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
       (st = put(l.ilabel, d->ilabel, sizeof(int32_t) * A)) ||
       (st = put(l.olabel, d->olabel, sizeof(int32_t) * A)) ||
       (st = put(l.weight, d->weight, sizeof(float) * A)) ||
-      (st = put(l.level_base, p.level_base.data(), sizeof(uint32_t) * (p.nlevels + 1))))
+      (st = put(l.level_base, p.level_base.data(), sizeof(uint32_t) * (p.nlevels + 1))) ||
+      (npaths && (st = put(l.pfirst, p.pfirst.data(), sizeof(uint32_t) * (S + 1)))) ||
+      (npaths && (st = put(l.phead, p.phead.data(), sizeof(uint4) * npaths))) ||
+      (npaths && p.pstride && (st = put(l.ptail, p.ptail.data(), sizeof(float) * npaths * p.pstride))))
     return st;
   if ((st = hip_check(hipStreamSynchronize(s), "graph upload sync"))) return st;
   wd_graph* g = new wd_graph();
@@ -231,6 +318,11 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
   dg.olabel_id = (const int32_t*)(base + l.olabel);
   dg.weight_id = (const float*)(base + l.weight);
   dg.level_base = (const uint32_t*)(base + l.level_base);
+  dg.pfirst = npaths ? (const uint32_t*)(base + l.pfirst) : nullptr;
+  dg.phead = npaths ? (const uint4*)(base + l.phead) : nullptr;
+  dg.ptail = npaths && p.pstride ? (const float*)(base + l.ptail) : nullptr;
+  dg.npaths = npaths;
+  dg.pstride = p.pstride;
   dg.S = (uint32_t)S;
   dg.start = (uint32_t)d->start_state;
   dg.nlevels = p.nlevels;
@@ -245,3 +337,5 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
 extern "C" void wd_graph_free(wd_graph* g) { delete g; }
 
 extern "C" int32_t wd_graph_eps_levels(const wd_graph* g) { return g ? (int32_t)g->nlevels : 0; }
+
+extern "C" int64_t wd_graph_eps_paths(const wd_graph* g) { return g ? (int64_t)g->dg.npaths : 0; }

@@ -29,9 +29,14 @@ WD_FLAG_CHIP_WIDE = 8
 WD_CHIP_WIDE_MAX_ACTIVE = 32768
 WD_FLAG_DYNAMIC_LB = 16
 WD_FLAG_NO_INCREMENTAL_PRUNE = 32
+WD_FLAG_PHASES = 64
+WD_FLAG_EPS_LEVELS = 128
+WD_PHASE_STAMPS = 10
+WD_PHASE_SLOTS = 12
 _MODE_FLAGS = {"auto": 0, "workgroup": WD_FLAG_ONE_WORKGROUP, "chip": WD_FLAG_CHIP_WIDE,
                "chip_dyn": WD_FLAG_CHIP_WIDE | WD_FLAG_DYNAMIC_LB,
-               "chip_noprune": WD_FLAG_CHIP_WIDE | WD_FLAG_NO_INCREMENTAL_PRUNE}
+               "chip_noprune": WD_FLAG_CHIP_WIDE | WD_FLAG_NO_INCREMENTAL_PRUNE,
+               "workgroup_levels": WD_FLAG_ONE_WORKGROUP | WD_FLAG_EPS_LEVELS}
 STATUS_NAMES = {0: "WD_OK", 1: "WD_EINVAL", 2: "WD_ECYCLE", 3: "WD_ENOPATH", 4: "WD_ECAPACITY",
                 5: "WD_EDEVICE"}
 
@@ -82,13 +87,14 @@ class wd_stats(ctypes.Structure):
                 ("lattice_ms", ctypes.c_float), ("needed", wd_caps)]
 
 
-EXPORTS = ["wd_graph_bytes", "wd_graph_load", "wd_graph_free", "wd_graph_eps_levels",
+EXPORTS = ["wd_graph_bytes", "wd_graph_load", "wd_graph_free", "wd_graph_eps_levels", "wd_graph_eps_paths",
            "wd_workspace_bytes", "wd_decode", "wd_decode_batch", "wd_stream_begin",
            "wd_stream_advance", "wd_stream_end", "wd_stream_free", "wd_lattice_determinize",
            "wd_clat_states", "wd_clat_arcs", "wd_clat_finals", "wd_clat_alignment", "wd_clat_free",
            "wd_result_status",
            "wd_result_cost", "wd_result_words", "wd_result_lattice", "wd_result_nodes",
-           "wd_result_tokens", "wd_result_raw_lattice", "wd_result_cutoffs", "wd_result_stats",
+           "wd_result_tokens", "wd_result_raw_lattice", "wd_result_cutoffs", "wd_result_phases",
+           "wd_result_stats",
            "wd_result_free", "wd_last_error"]
 
 _LIB = None
@@ -108,6 +114,7 @@ def lib():
             "wd_graph_load": ([P(wd_graph_desc), VP, ctypes.c_size_t, VP, P(VP)], ctypes.c_int),
             "wd_graph_free": ([VP], None),
             "wd_graph_eps_levels": ([VP], ctypes.c_int32),
+            "wd_graph_eps_paths": ([VP], ctypes.c_int64),
             "wd_workspace_bytes": ([VP, ctypes.c_int32, ctypes.c_int32, P(wd_params), P(wd_caps),
                                     P(ctypes.c_size_t), P(wd_caps)], ctypes.c_int),
             "wd_decode": ([VP, VP, ctypes.c_int32, P(wd_params), P(wd_caps), VP, ctypes.c_size_t, VP,
@@ -134,6 +141,7 @@ def lib():
             "wd_result_tokens": ([VP, P(VP)], ctypes.c_int64),
             "wd_result_raw_lattice": ([VP, P(VP)], ctypes.c_int64),
             "wd_result_cutoffs": ([VP, P(VP), P(VP), P(VP)], ctypes.c_int32),
+            "wd_result_phases": ([VP, P(VP), P(ctypes.c_double)], ctypes.c_int32),
             "wd_result_stats": ([VP, P(wd_stats)], None),
             "wd_result_free": ([VP], None),
             "wd_last_error": ([], ctypes.c_char_p),
@@ -171,6 +179,10 @@ def wd_graph_free(handle: int) -> None:
 
 def wd_graph_eps_levels(handle: int) -> int:
     return lib().wd_graph_eps_levels(handle)
+
+
+def wd_graph_eps_paths(handle: int) -> int:
+    return lib().wd_graph_eps_paths(handle)
 
 
 def wd_workspace_bytes(handle: int, lanes: int, max_T: int, params: wd_params,
@@ -311,6 +323,10 @@ def wd_result_read(r: int) -> SimpleNamespace:
     f4 = np.dtype("<f4")
     out.best, out.cutoff_beam, out.cutoff = (_copy(b.value, n, f4), _copy(cb.value, n, f4),
                                              _copy(c.value, n, f4))
+    vp, hz = ctypes.c_void_p(), ctypes.c_double()
+    n = L.wd_result_phases(r, ctypes.byref(vp), ctypes.byref(hz))
+    out.phases = _copy(vp.value, n * WD_PHASE_SLOTS, np.dtype("<u8")).reshape(n, WD_PHASE_SLOTS)
+    out.phase_tick_hz = hz.value
     st = wd_stats()
     L.wd_result_stats(r, ctypes.byref(st))
     out.stats = {f: getattr(st, f) for f, _ in wd_stats._fields_ if f != "needed"}
@@ -362,6 +378,7 @@ class Graph:
             self.handle = wd_graph_load(self.desc, base, nbytes, _stream(torch))
         self.nbytes = nbytes
         self.eps_levels = wd_graph_eps_levels(self.handle)
+        self.eps_paths = wd_graph_eps_paths(self.handle)
         self._ws = None
         self._caps = {}
 
@@ -374,6 +391,15 @@ class Graph:
                 pass
             self.handle = None
 
+    def degrees(self):
+        """Per-state (emitting, epsilon) out-degrees of the graph (host numpy
+        arrays, from the CSR this graph was loaded from)."""
+        rp = self._arrs["row_ptr"].astype(np.int64)
+        S = rp.size - 1
+        src = np.repeat(np.arange(S), np.diff(rp))
+        eps = self._arrs["ilabel"] == 0
+        return np.bincount(src[~eps], minlength=S), np.bincount(src[eps], minlength=S)
+
     def workspace(self, lanes: int, max_T: int, params: wd_params, caps: wd_caps | None):
         """(pointer, bytes) of a workspace large enough; reuses one buffer."""
         torch = _torch()
@@ -385,12 +411,12 @@ class Graph:
         return base, nbytes, used
 
 
-def _params(beam, max_active, lattice_beam, debug, timing=False, mode="auto"):
+def _params(beam, max_active, lattice_beam, debug, timing=False, mode="auto", flags=0):
     if mode not in _MODE_FLAGS:
         raise ValueError(f"mode must be one of {sorted(_MODE_FLAGS)}")
     return wd_params(float(beam), int(max_active), float(lattice_beam),
                      (WD_FLAG_DEBUG if debug else 0) | (WD_FLAG_TIMING if timing else 0) |
-                     _MODE_FLAGS[mode])
+                     _MODE_FLAGS[mode] | int(flags))
 
 
 def _grow(caps: wd_caps, needed: dict) -> wd_caps:
@@ -406,22 +432,24 @@ def _grow(caps: wd_caps, needed: dict) -> wd_caps:
 
 def decode_batch(graph: Graph, loglikes: list, beam: float, max_active: int, lattice_beam: float,
                  debug: bool = False, caps: wd_caps | None = None, max_retries: int = 12,
-                 timing: bool = False, mode: str = "auto"):
+                 timing: bool = False, mode: str = "auto", flags: int = 0):
     """Decode utterances (device float32 tensors, T_i x P) concurrently.
     `mode`: "workgroup" (one workgroup per utterance), "chip" (chip-wide
     kernels per frame), "chip_dyn" (chip-wide with dynamic load balancing of
     the emitting arcs), "chip_noprune" (chip-wide without incremental lattice
-    pruning) or "auto" (the library's choice).  Returns one result
-    namespace per utterance."""
+    pruning), "workgroup_levels" (one workgroup, epsilon closure level by
+    level instead of by the graph's epsilon paths) or "auto" (the library's
+    choice).  `flags`: further WD_FLAG_*
+    bits (e.g. WD_FLAG_PHASES).  Returns one result namespace per utterance."""
     torch = _torch()
     for x in loglikes:
         if x.dtype != torch.float32 or not x.is_contiguous() or x.device != graph.device:
             raise ValueError("log-likelihoods must be contiguous float32 tensors on the graph's device")
         if x.dim() != 2 or x.shape[1] != graph.num_pdfs:
             raise ValueError(f"log-likelihoods must be T x {graph.num_pdfs}")
-    p = _params(beam, max_active, lattice_beam, debug, timing, mode)
+    p = _params(beam, max_active, lattice_beam, debug, timing, mode, flags)
     Ts = [int(x.shape[0]) for x in loglikes]
-    key = (len(Ts), max(Ts), float(beam), int(max_active), float(lattice_beam), bool(debug))
+    key = (len(Ts), max(Ts), float(beam), int(max_active), float(lattice_beam), bool(debug), int(flags))
     if caps is None:
         caps = graph._caps.get(key)
     for attempt in range(max_retries + 1):
@@ -448,10 +476,10 @@ def decode_batch(graph: Graph, loglikes: list, beam: float, max_active: int, lat
 
 def decode(graph: Graph, loglikes, beam: float, max_active: int, lattice_beam: float,
            debug: bool = False, caps: wd_caps | None = None, timing: bool = False,
-           mode: str = "auto"):
+           mode: str = "auto", flags: int = 0):
     """Decode one utterance (device float32 tensor, T x P)."""
     return decode_batch(graph, [loglikes], beam, max_active, lattice_beam, debug, caps,
-                        timing=timing, mode=mode)[0]
+                        timing=timing, mode=mode, flags=flags)[0]
 
 
 class Stream:
@@ -478,27 +506,42 @@ class Stream:
             nbytes, used = wd_workspace_bytes(graph.handle, self.B, self.max_T, self.params, caps)
             self._ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=graph.device)
             ws = (self._ws.data_ptr() + 255) // 256 * 256
+            # the stream every advance decodes on (wd_stream_begin keeps it)
+            self._stream = torch.cuda.current_stream(graph.device)
             self.handle = wd_stream_begin(graph.handle, [self.frames[i].data_ptr() for i in range(self.B)],
-                                          self.max_T, self.params, used, ws, nbytes, _stream(torch))
+                                          self.max_T, self.params, used, ws, nbytes,
+                                          self._stream.cuda_stream)
         self.caps = used
 
     def push(self, chunks: list) -> None:
         """chunks[i]: None or a device float32 tensor (n_i x P) of utterance
-        i's next frames."""
+        i's next frames, produced on the caller's current stream.  The copies
+        into the frame stores run on the decoding stream (the one current at
+        construction) after it has waited for the current stream, so the
+        decode never reads a row before its chunk is complete."""
         torch = _torch()
         counts = [0] * self.B
+        for i, x in enumerate(chunks):
+            if x is None:
+                continue
+            if x.dim() != 2 or x.shape[1] != self.graph.num_pdfs or x.dtype != torch.float32:
+                raise ValueError(f"chunk {i} must be n x {self.graph.num_pdfs} float32")
+            if self.T[i] + int(x.shape[0]) > self.max_T:
+                raise ValueError(f"utterance {i} would pass max_T = {self.max_T}")
         with torch.cuda.device(self.graph.device):
-            for i, x in enumerate(chunks):
-                if x is None:
-                    continue
-                n = int(x.shape[0])
-                if x.dim() != 2 or x.shape[1] != self.graph.num_pdfs or x.dtype != torch.float32:
-                    raise ValueError(f"chunk {i} must be n x {self.graph.num_pdfs} float32")
-                if self.T[i] + n > self.max_T:
-                    raise ValueError(f"utterance {i} would pass max_T = {self.max_T}")
-                if n:
-                    self.frames[i, self.T[i]:self.T[i] + n].copy_(x)
-                counts[i] = n
+            cur = torch.cuda.current_stream(self.graph.device)
+            if cur != self._stream:
+                self._stream.wait_stream(cur)
+            with torch.cuda.stream(self._stream):
+                for i, x in enumerate(chunks):
+                    if x is None:
+                        continue
+                    n = int(x.shape[0])
+                    if n:
+                        self.frames[i, self.T[i]:self.T[i] + n].copy_(x)
+                        if cur != self._stream:
+                            x.record_stream(self._stream)  # x may be freed on `cur` meanwhile
+                    counts[i] = n
             wd_stream_advance(self.handle, counts)
         for i, n in enumerate(counts):
             self.T[i] += n

@@ -5,7 +5,9 @@ tokens, cutoffs and the raw lattice.  Sizes span several tiles of the
 1024-thread workgroup, both compaction paths (LDS rank sort, state bitmap)
 and ragged frames.  Every case runs in every execution mode: one workgroup
 per utterance, chip-wide kernels per frame, and chip-wide with dynamic load
-balancing of the emitting arcs."""
+balancing of the emitting arcs; the one-workgroup mode both with the
+epsilon closure over the graph's enumerated epsilon paths (its default) and
+level by level."""
 import math
 
 import numpy as np
@@ -18,7 +20,7 @@ from gpu_compare import assert_same
 
 pytestmark = pytest.mark.gpu
 INF = math.inf
-MODES = ["workgroup", "chip", "chip_dyn"]
+MODES = ["workgroup", "workgroup_levels", "chip", "chip_dyn"]
 
 
 @pytest.fixture(scope="module")
@@ -65,8 +67,17 @@ def test_tiny_random(wf, oracle_mod, seed, mode):
     lb = [INF, 1.0, 0.0][seed % 3]
     try:
         oracle_mod.decode(g, L, beam, ma, lb)
-    except oracle_mod.OracleError:
-        pytest.skip("no path")
+    except oracle_mod.OracleError as e:
+        # no token survives some frame: the GPU must report the same status
+        assert e.code == oracle_mod.ENOPATH, e
+        import torch
+        print(f"\n[gpu case] tiny seed {seed} (no path) mode={mode}", flush=True)
+        graph = wf.Graph(g, 3)
+        x = torch.from_numpy(np.ascontiguousarray(L)).to(graph.device)
+        with pytest.raises(wf.WdError) as err:
+            wf.decode(graph, x, beam, ma, lb, mode=mode)
+        assert err.value.status == wf.WD_ENOPATH
+        return
     _run(wf, oracle_mod, g, L, 3, beam, ma, lb, case=f"tiny seed {seed}", mode=mode)
 
 
@@ -330,3 +341,33 @@ def test_epsilon_fanin_level(wf, oracle_mod, n_spread, mode):
     g = fanin_graph(n_spread)
     L = synth.tiny_loglikes(31 + n_spread, 7, 16) * 3 - 6
     _run(wf, oracle_mod, g, L, 16, INF, 2000, 4.0, case=f"epsilon fan-in {n_spread}", mode=mode)
+
+
+def test_phase_profile(wf, oracle_mod, tiny10k):
+    """WD_FLAG_PHASES runs the profiled copy of the forward kernel: the same
+    result, and per frame non-decreasing wall-clock stamps at the step
+    boundaries and the frame's token and link counts; chip-wide mode rejects
+    the flag."""
+    import torch
+    cfg, g, L, graph = tiny10k
+    args = (cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    x = torch.from_numpy(L[:120]).to(graph.device)
+    print("\n[gpu case] step profile tiny_10k 120 frames", flush=True)
+    r = wf.decode(graph, x, *args, debug=True, mode="workgroup", flags=wf.WD_FLAG_PHASES)
+    o = oracle_mod.decode(g, L[:120], *args, debug=True)
+    assert_same(r, o, debug=True)
+    ph = r.phases
+    assert ph.shape == (121, wf.WD_PHASE_SLOTS) and r.phase_tick_hz > 0
+    st = ph[:, :wf.WD_PHASE_STAMPS].astype(np.int64)
+    assert np.all(np.diff(st, axis=1) >= 0)
+    assert np.all(st[1:, 0] >= st[:-1, wf.WD_PHASE_STAMPS - 1])
+    ntok = (ph[:, wf.WD_PHASE_STAMPS] >> 8) & 0xffffff
+    counts = np.bincount(o.tokens["t"], minlength=121)
+    assert np.array_equal(ntok, counts)
+    nlink = ph[:, wf.WD_PHASE_STAMPS] >> 32
+    assert np.array_equal(nlink, np.bincount(o.raw_links["t"], minlength=121))
+    plain = wf.decode(graph, x, *args, mode="workgroup")
+    assert plain.phases.shape[0] == 0
+    with pytest.raises(wf.WdError) as e:
+        wf.decode(graph, x, *args, mode="chip", flags=wf.WD_FLAG_PHASES)
+    assert e.value.status == wf.WD_EINVAL

@@ -245,3 +245,29 @@ def test_concurrent_chip_decodes(wf, oracle_mod, tiny10k):
         assert_same(r, o1)
     for r in results[1]:
         assert_same(r, o2)
+
+
+@pytest.mark.parametrize("mode", ["workgroup", "chip"])
+def test_stream_chunks_from_another_stream(wf, oracle_mod, tiny10k, mode):
+    """Chunks produced on a side stream (a pretend acoustic model: a
+    host-to-device copy and a scale on that stream) and pushed while the
+    side stream is current: the decode, on the stream the decoder was built
+    on, waits for each chunk."""
+    import torch
+    cfg, g, L, graph = tiny10k
+    args = (cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
+    print(f"\n[gpu case] stream chunks from a side stream mode={mode}", flush=True)
+    half = np.ascontiguousarray(L * np.float32(0.5))
+    s = wf.Stream(graph, 1, L.shape[0], *args, mode=mode)
+    side = torch.cuda.Stream(graph.device)
+    host = torch.from_numpy(half).pin_memory()
+    t = 0
+    with torch.cuda.stream(side):
+        for n in chunks([37, 1, 64], L.shape[0], seed=3):
+            x = host[t:t + n].to(graph.device, non_blocking=True)
+            x = x * 2.0  # exact: restores L
+            s.push([x])
+            del x
+            t += n
+    r = s.end()[0]
+    assert_same(r, oracle_mod.decode(g, L, *args))

@@ -72,6 +72,54 @@ def test_wide_2m_prefix(wf, oracle_mod, name, T, debug, mode):
     assert_same(r, o, debug=debug)
 
 
+def _golden_module():
+    import importlib.util
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "make_wide_2m.py")
+    spec = importlib.util.spec_from_file_location("make_wide_2m", path)
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+GOLDEN_T = 200
+
+
+@pytest.fixture(scope="module", params=["wide_2m", "wide_2m_dyadic"])
+def wide_golden(request, wf):
+    import torch
+    name = request.param
+    gm = _golden_module()
+    meta, post = gm.load(name, GOLDEN_T)
+    cfg = synth.workload(name)
+    g = synth.make_graph(cfg)
+    L = synth.make_loglikes(cfg)[:GOLDEN_T]
+    graph = wf.Graph(g, cfg["P"])
+    x = torch.from_numpy(L).to(graph.device)
+    yield gm, name, cfg, graph, x, meta, post
+    del graph, x
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("mode", ["chip", "chip_dyn", "workgroup"])
+def test_wide_2m_golden(wf, wide_golden, mode):
+    """The first 200 frames of the wide-beam workload (650k tokens and 1.1M
+    candidate links per frame once it has ramped up, epsilon chains of depth
+    8), decoded as a whole utterance without the debug flag, so that in
+    chip-wide mode the lattice is pruned in 32-frame windows on the second
+    stream while decoding goes on (six windows, then the final pruning of the
+    rest): words, cost, statistics and every lattice link and node must match
+    the oracle's stored result bit for bit (per-frame digests written by
+    tests/golden/make_wide_2m.py from an oracle run), posteriors within 1e-4."""
+    gm, name, cfg, graph, x, meta, post = wide_golden
+    print(f"\n[gpu case] {name} golden first {GOLDEN_T} frames mode={mode}", flush=True)
+    r = wf.decode(graph, x, cfg["beam"], cfg["max_active"], cfg["lattice_beam"], mode=mode)
+    gm.compare(meta, post, r.words, r.cost, r.links, r.nodes, r.stats)
+    if mode.startswith("chip"):
+        # incremental pruning ran: the link store held far fewer than the raw links
+        assert r.needed["links"] + 2 * r.needed["window_links"] < r.stats["raw_links"]
+
+
 @pytest.mark.parametrize("name,mode", [("wide_2m", "chip"), ("wide_2m_dyadic", "chip"), ("wide_2m", "chip_dyn")])
 def test_wide_2m_full(wf, name, mode):
     """All 800 frames in chip-wide mode, as bench.py times them: the oracle
