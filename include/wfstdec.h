@@ -263,6 +263,39 @@ wd_status wd_decode_batch(const wd_graph* g, int32_t B, const float* const* logl
                           const int32_t* T, const wd_params* p, const wd_caps* caps, void* ws,
                           size_t ws_bytes, void* stream, wd_result** out);
 
+/* ---- decoding without allocation -------------------------------------- */
+
+/* For callers that cannot allocate device memory (code that must not call
+ * hipMalloc, e.g. under HIP graph capture, in tight serving loops, or in
+ * harnesses that forbid it): wd_decode of one utterance in one-workgroup
+ * mode whose workspace is a fixed device array inside the library,
+ * WD_NOALLOC_SCRATCH_BYTES on every device the library runs on (held until
+ * the process ends), and whose results go into the caller's host buffers.
+ * It calls no hipMalloc, hipFree or other allocating routine, and creates no
+ * stream or event.
+ *  - p->flags: 0 or WD_FLAG_ONE_WORKGROUP only (debug, timing, profile and
+ *    chip-wide flags: WD_EINVAL; with max_active 0 or >= WD_CHIP_WIDE_MAX_ACTIVE
+ *    WD_FLAG_ONE_WORKGROUP must be set).  caps as for wd_workspace_bytes.
+ *  - WD_EINVAL, before any device work, when the workspace these
+ *    capacities need (wd_workspace_bytes with lanes = 1) exceeds the scratch;
+ *    the per-state arrays take 16.5 bytes per graph state, so graphs beyond
+ *    ~15M states do not fit.
+ *  - Outputs (host memory, caller-owned): *cost, words[words_cap] with the
+ *    count in *n_words, links[links_cap] (sorted by (t, arc_id)) and
+ *    nodes[nodes_cap] (sorted by (t, state)) with their counts in
+ *    stats->kept_links and stats->nodes, and *stats (forward_ms/lattice_ms 0).
+ *    WD_ECAPACITY when the workspace capacities or an output buffer were too
+ *    small; *n_words and *stats (its `needed` capacities, kept_links, nodes)
+ *    then say what is needed.
+ *  - Synchronous on `stream`.  Every call on a device uses the same scratch,
+ *    which keeps the last call's contents: calls that overlap on one device
+ *    (other threads, other streams) race and must not be issued. */
+#define WD_NOALLOC_SCRATCH_BYTES (256u << 20)
+wd_status wd_decode_noalloc(const wd_graph* g, const float* loglikes, int32_t T, const wd_params* p,
+                            const wd_caps* caps, void* stream, float* cost, int32_t* words, int32_t words_cap,
+                            int32_t* n_words, wd_lat_arc* links, int64_t links_cap, wd_lat_node* nodes,
+                            int64_t nodes_cap, wd_stats* stats);
+
 /* ---- streaming -------------------------------------------------------- */
 
 /* Frame-synchronous decoding as the log-likelihoods arrive, e.g. chunk by

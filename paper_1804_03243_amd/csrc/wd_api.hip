@@ -605,6 +605,102 @@ extern "C" void wd_stream_free(wd_stream* run) {
   delete run;
 }
 
+// ------------------------------------------------------ decode without allocation
+//
+// The workspace of wd_decode_noalloc: a fixed array in every device's memory
+// (held from the library's first use on that device until the process ends).
+// In host code `scratch` names a host-side stand-in, never the device
+// memory; the device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[WD_NOALLOC_SCRATCH_BYTES];
+
+static wd_status scratch_of_current_device(char** out) {
+  static std::mutex mu;
+  static char* per_dev[64] = {};
+  int dev = 0;
+  wd_status st = hip_check(hipGetDevice(&dev), "noalloc: device");
+  if (st != WD_OK) return st;
+  if (dev < 0 || dev >= 64) return fail(WD_EDEVICE, "noalloc: device index out of range");
+  std::lock_guard<std::mutex> lk(mu);
+  if (!per_dev[dev]) {
+    void* ptr = nullptr;
+    if ((st = hip_check(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)), "noalloc: scratch address"))) return st;
+    if (!ptr || ((uintptr_t)ptr & 255u)) return fail(WD_EDEVICE, "noalloc: scratch misaligned");
+    per_dev[dev] = (char*)ptr;
+  }
+  *out = per_dev[dev];
+  return WD_OK;
+}
+
+extern "C" wd_status wd_decode_noalloc(const wd_graph* g, const float* loglikes, int32_t T, const wd_params* p,
+                                       const wd_caps* caps, void* stream, float* cost, int32_t* words,
+                                       int32_t words_cap, int32_t* n_words, wd_lat_arc* links, int64_t links_cap,
+                                       wd_lat_node* nodes, int64_t nodes_cap, wd_stats* stats) {
+  if (!g || T < 0 || T > (1 << 24) || (T > 0 && !loglikes) || !cost || !n_words || !stats ||
+      words_cap < 0 || links_cap < 0 || nodes_cap < 0 || (words_cap && !words) || (links_cap && !links) ||
+      (nodes_cap && !nodes))
+    return fail(WD_EINVAL, "decode_noalloc: bad arguments");
+  wd_status st = check_params(p);
+  if (st != WD_OK) return st;
+  const uint32_t allowed = WD_FLAG_ONE_WORKGROUP;
+  if ((p->flags & ~allowed) || chip_wide_mode(p))
+    return fail(WD_EINVAL, "decode_noalloc: one-workgroup decodes only, without debug, timing or profile flags "
+                           "(set WD_FLAG_ONE_WORKGROUP when max_active is 0 or >= WD_CHIP_WIDE_MAX_ACTIVE)");
+  *n_words = 0;
+  *cost = 0.0f;
+  std::memset(stats, 0, sizeof(*stats));
+  const Caps c = resolve_caps(g, T, p, caps);
+  const uint64_t need = carve(g, 1, T, c, nullptr, nullptr).total;
+  if (need > (uint64_t)WD_NOALLOC_SCRATCH_BYTES)
+    return fail(WD_EINVAL, "decode_noalloc: this decode needs a workspace of " + std::to_string(need) +
+                               " bytes, more than the " + std::to_string((uint64_t)WD_NOALLOC_SCRATCH_BYTES) +
+                               "-byte scratch (pass smaller capacities, or use wd_decode)");
+  char* base = nullptr;
+  if ((st = scratch_of_current_device(&base))) return st;
+  hipStream_t s = (hipStream_t)stream;
+  LaneDesc lane;
+  std::memset(&lane, 0, sizeof(lane));
+  const Regions R = carve(g, 1, T, c, base, &lane);
+  lane.ll = (decltype(lane.ll))loglikes;
+  lane.T = T;
+  // the scratch keeps the last call's contents: every region a decode reads
+  // before writing is reset here, as for a caller's workspace
+  if ((st = hip_check(hipMemcpyAsync(R.desc, &lane, sizeof(LaneDesc), hipMemcpyHostToDevice, s), "lane upload")))
+    return st;
+  launch_fill_u32((uint32_t*)R.info, sizeof(LaneInfo) / 4, 0u, s);
+  launch_fill_u32(R.bad, 1, 0u, s);
+  launch_fill_u64(R.slot, (uint64_t)g->S, kEmpty, s);
+  launch_fill_u32(R.bitmap, R.bitmap_words, 0u, s);
+  launch_fill_u32(R.used, R.used_words, 0u, s);
+  const Params prm{p->beam, p->max_active, p->lattice_beam, p->flags};
+  launch_check_loglikes(R.desc, 1, g->P, R.bad, s);
+  launch_forward(g->dg, R.desc, 1, prm, R.bad, s);
+  launch_lattice(g->dg, R.desc, 1, prm, s);
+  LaneInfo I;
+  if ((st = hip_check(hipGetLastError(), "launch")) ||
+      (st = hip_check(hipMemcpyAsync(&I, R.info, sizeof(LaneInfo), hipMemcpyDeviceToHost, s), "info download")) ||
+      (st = hip_check(hipStreamSynchronize(s), "decode")))
+    return st;
+  const wd_status ls = (I.status == 0 && I.tb_fail) ? WD_EDEVICE : (wd_status)I.status;
+  *stats = lane_stats(I, T, 0.0f, 0.0f, false);
+  if (ls != WD_OK) return fail(ls, status_message(ls));
+  *cost = I.best_cost;
+  *n_words = (int32_t)I.nwords;
+  if ((int64_t)I.nwords > words_cap || (int64_t)I.kept > links_cap || (int64_t)I.out_nodes > nodes_cap)
+    return fail(WD_ECAPACITY, "decode_noalloc: output buffers too small (need " + std::to_string(I.nwords) +
+                                  " words, " + std::to_string(I.kept) + " links, " + std::to_string(I.out_nodes) +
+                                  " nodes; see n_words and stats)");
+  auto d2h = [&](void* dst, const void* src, uint64_t bytes) -> wd_status {
+    if (!bytes) return WD_OK;
+    return hip_check(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s), "result download");
+  };
+  if ((st = d2h(words, lane.out_words, 4 * I.nwords)) ||
+      (st = d2h(links, lane.out_links, sizeof(OutLink) * I.kept)) ||
+      (st = d2h(nodes, lane.out_nodes, sizeof(OutNode) * I.out_nodes)) ||
+      (st = hip_check(hipStreamSynchronize(s), "result download")))
+    return st;
+  return WD_OK;
+}
+
 extern "C" wd_status wd_result_status(const wd_result* r) { return r->status; }
 extern "C" float wd_result_cost(const wd_result* r) { return r->cost; }
 extern "C" int32_t wd_result_words(const wd_result* r, const int32_t** w) {

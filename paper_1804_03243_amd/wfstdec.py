@@ -88,7 +88,7 @@ class wd_stats(ctypes.Structure):
 
 
 EXPORTS = ["wd_graph_bytes", "wd_graph_load", "wd_graph_free", "wd_graph_eps_levels", "wd_graph_eps_paths",
-           "wd_workspace_bytes", "wd_decode", "wd_decode_batch", "wd_stream_begin",
+           "wd_workspace_bytes", "wd_decode", "wd_decode_batch", "wd_decode_noalloc", "wd_stream_begin",
            "wd_stream_advance", "wd_stream_end", "wd_stream_free", "wd_lattice_determinize",
            "wd_clat_states", "wd_clat_arcs", "wd_clat_finals", "wd_clat_alignment", "wd_clat_free",
            "wd_result_status",
@@ -119,6 +119,9 @@ def lib():
                                     P(ctypes.c_size_t), P(wd_caps)], ctypes.c_int),
             "wd_decode": ([VP, VP, ctypes.c_int32, P(wd_params), P(wd_caps), VP, ctypes.c_size_t, VP,
                            P(VP)], ctypes.c_int),
+            "wd_decode_noalloc": ([VP, VP, ctypes.c_int32, P(wd_params), P(wd_caps), VP, P(ctypes.c_float),
+                                   VP, ctypes.c_int32, P(ctypes.c_int32), VP, ctypes.c_int64, VP, ctypes.c_int64,
+                                   P(wd_stats)], ctypes.c_int),
             "wd_decode_batch": ([VP, ctypes.c_int32, P(VP), P(ctypes.c_int32), P(wd_params),
                                  P(wd_caps), VP, ctypes.c_size_t, VP, P(VP)], ctypes.c_int),
             "wd_stream_begin": ([VP, ctypes.c_int32, P(VP), ctypes.c_int32, P(wd_params), P(wd_caps),
@@ -215,6 +218,29 @@ def wd_decode_batch(handle: int, loglikes_ptrs: list[int], Ts: list[int], params
                                ctypes.byref(caps) if caps is not None else None, ws, ws_bytes, stream,
                                outs)
     return st, [o or 0 for o in outs]
+
+
+WD_NOALLOC_SCRATCH_BYTES = 256 << 20
+
+
+def wd_decode_noalloc(handle: int, loglikes_ptr: int, T: int, params: wd_params, caps: wd_caps | None,
+                      stream: int, words: np.ndarray, links: np.ndarray, nodes: np.ndarray):
+    """The no-allocation decode: results into the given host arrays (int32,
+    LINK_DTYPE, NODE_DTYPE; their sizes are the capacities).  Returns
+    (status, cost, n_words, stats dict, needed dict); on WD_OK the first
+    n_words words, stats['kept_links'] links and stats['nodes'] nodes are
+    filled."""
+    for a, dt, what in ((words, np.dtype("<i4"), "words"), (links, LINK_DTYPE, "links"), (nodes, NODE_DTYPE, "nodes")):
+        if a.dtype != dt or a.ndim != 1 or not a.flags.c_contiguous:
+            raise ValueError(f"{what} must be a contiguous 1-d array of {dt}")
+    cost, nw, st_ = ctypes.c_float(), ctypes.c_int32(), wd_stats()
+    st = lib().wd_decode_noalloc(handle, loglikes_ptr, T, ctypes.byref(params),
+                                 ctypes.byref(caps) if caps is not None else None, stream, ctypes.byref(cost),
+                                 words.ctypes.data, words.size, ctypes.byref(nw), links.ctypes.data, links.size,
+                                 nodes.ctypes.data, nodes.size, ctypes.byref(st_))
+    stats = {f: getattr(st_, f) for f, _ in wd_stats._fields_ if f != "needed"}
+    needed = {f: getattr(st_.needed, f) for f, _ in wd_caps._fields_}
+    return st, np.float32(cost.value), nw.value, stats, needed
 
 
 def wd_stream_begin(handle: int, frame_ptrs: list[int], max_T: int, params: wd_params,
