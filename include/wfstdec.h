@@ -232,8 +232,9 @@ int32_t wd_graph_eps_levels(const wd_graph* g);
  * and last arcs) so that the one-workgroup epsilon closure relaxes all
  * levels in one round (see WD_FLAG_EPS_LEVELS); 0 when the graph has no
  * epsilon arcs, more than 2^27 such paths or one longer than 16 arcs (the
- * closure then goes level by level).  The table takes 20 + 4 * (longest
- * path - 1) bytes per path of device memory (part of wd_graph_bytes). */
+ * closure then goes level by level).  The table takes 16 + 4 * (longest
+ * path - 1) bytes per path of device memory (part of wd_graph_bytes; the
+ * first path of each state sits beside its arc offsets). */
 int64_t wd_graph_eps_paths(const wd_graph* g);
 
 /* ---- decoding --------------------------------------------------------- */

@@ -48,7 +48,8 @@ __host__ __device__ inline uint64_t pack_tok(uint32_t key, uint32_t arc) {
 }
 
 // Device copy of the decoding graph, laid out in one caller-owned buffer.
-//   off[s]  = {first emitting arc, first epsilon arc} of state s (S+1 entries)
+//   off[s]  = {first emitting arc, first epsilon arc, first epsilon path, 0} of
+//             state s (S+1 entries; the path index is 0 without a path table)
 //   earc[i] = {dst, weight bits, ilabel | dst_class << 24, arc id}
 //   xarc[j] = {dst, weight bits, dst_class, arc id}
 //   xnext[j] = epsilon arc range {first, end} of xarc[j]'s destination
@@ -57,7 +58,7 @@ __host__ __device__ inline uint64_t pack_tok(uint32_t key, uint32_t arc) {
 // epsilon out-arcs, else kNoEps.  Epsilon arcs always climb to a strictly
 // higher level, so relaxing levels in order closes a frame exactly.
 struct DevGraph {
-  const uint2* off;
+  const uint4* off;
   const uint4* earc;
   const uint4* xarc;
   const uint2* xnext;
@@ -69,11 +70,10 @@ struct DevGraph {
   const uint32_t* level_base;  // [nlevels + 1] bucket offsets of the epsilon levels
   // Epsilon paths (every path of one or more epsilon arcs out of a state,
   // enumerated when the graph is loaded; npaths = 0 when the graph has too
-  // many or too long ones).  Paths of state s: [pfirst[s], pfirst[s+1]).
+  // many or too long ones).  Paths of state s: [off[s].z, off[s+1].z).
   //   phead[p] = {last state, last arc id, last arc's weight bits, k | xdeg << 8}
   //     k = number of arcs, xdeg = epsilon out-degree of the last state
   //   ptail[p * pstride + i] = weight of arc i < k - 1 (pstride = longest path - 1)
-  const uint32_t* pfirst;
   const uint4* phead;
   const float* ptail;
   uint64_t npaths;

@@ -160,7 +160,7 @@ __device__ __forceinline__ void h_clear(FwdShared& sh, uint32_t used) {
 
 // A first touch in the LDS table of a state with epsilon out-arcs: remember
 // its slot, epsilon arc range and level for the epsilon passes.
-__device__ __forceinline__ void lds_bucket(FwdShared& sh, uint32_t slot, uint2 o0, uint2 o1, uint32_t cls) {
+__device__ __forceinline__ void lds_bucket(FwdShared& sh, uint32_t slot, uint4 o0, uint4 o1, uint32_t cls) {
   const uint32_t b = atomicAdd(&sh.n_bk, 1u);
   if (b < kBkCap) {
     sh.bk[b] = make_uint4(slot, o0.y, o1.y, cls);
@@ -376,8 +376,9 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
             sh.h_val[slot] = pack_tok(cost_key(0.0f), kNoArc);
             const uint32_t c = g.sclass[s0];
             if (c != kNoEps) {
-              if (paths) lds_bucket_paths(sh, slot, g.pfirst[s0], g.pfirst[s0 + 1], g.off[s0 + 1].y - g.off[s0].y);
-              else lds_bucket(sh, slot, g.off[s0], g.off[s0 + 1], c);
+              const uint4 o0 = g.off[s0], o1 = g.off[s0 + 1];
+              if (paths) lds_bucket_paths(sh, slot, o0.z, o1.z, o1.y - o0.y);
+              else lds_bucket(sh, slot, o0, o1, c);
             }
           }
           best_key = cost_key(0.0f);
@@ -395,12 +396,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
             // CSR offsets of the destination: the epsilon range for the bucket,
             // and warm in cache for the degree pass if the token survives;
             // with the path table, the range of its epsilon paths
-            const uint2 o0 = g.off[dst], o1 = g.off[dst + 1];
-            uint32_t p0 = 0, p1 = 0;
-            if (paths && cls != kNoEps) {
-              p0 = g.pfirst[dst];
-              p1 = g.pfirst[dst + 1];
-            }
+            const uint4 o0 = g.off[dst], o1 = g.off[dst + 1];
             const float ac = -row[(r.z & 0xffffffu) - 1u];
             float x = c + ac;
             x = canon(x + __uint_as_float(r.y));
@@ -416,7 +412,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
                   atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
                   if (fresh && cls != kNoEps) {
                     if (paths) {
-                      lds_bucket_paths(sh, slot, p0, p1, o1.y - o0.y);
+                      lds_bucket_paths(sh, slot, o0.z, o1.z, o1.y - o0.y);
                     } else {
                       lds_bucket(sh, slot, o0, o1, cls);
                       // start the state's first epsilon arc on its way for the closure
@@ -552,7 +548,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
             if (r.z != kNoEps) {
               // the destination's level now holds an entry within the cutoff
               atomicOr(&sh.lvl_live, level_bit(r.z));
-              if (fresh) lds_bucket(sh, slot, make_uint2(0, nx.x), make_uint2(0, nx.y), r.z);
+              if (fresh) lds_bucket(sh, slot, make_uint4(0, nx.x, 0, 0), make_uint4(0, nx.y, 0, 0), r.z);
             }
           }
         };
@@ -905,7 +901,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
         if (tid < m && sh.srt[tid] != kNoKey) {
           const uint32_t s = sh.srt[tid];
-          const uint2 o0 = g.off[s], o1 = g.off[s + 1];
+          const uint4 o0 = g.off[s], o1 = g.off[s + 1];
           const uint8_t cls = g.sclass[s];
           const uint4* q4 = reinterpret_cast<const uint4*>(sh.srt);
           uint32_t r = 0;
@@ -1052,7 +1048,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       uint32_t e = 0, x = 0;
       for (uint32_t p = p0; p < p1; ++p) {
         const uint32_t s = f.state[p];
-        const uint2 o0 = g.off[s], o1 = g.off[s + 1];
+        const uint4 o0 = g.off[s], o1 = g.off[s + 1];
         e += o1.x - o0.x;
         x += o1.y - o0.y;
         f.ebeg[p] = o0.x;

@@ -21,21 +21,20 @@ namespace wd {
 namespace {
 
 struct Prepared {
-  std::vector<uint2> off;
+  std::vector<uint4> off;
   std::vector<uint4> earc, xarc;
   std::vector<uint2> xnext;
   std::vector<uint8_t> sclass;
   std::vector<uint32_t> level_base;
   uint32_t nlevels = 0;
-  std::vector<uint32_t> pfirst;  // epsilon path table (empty: none)
+  bool paths = false;            // epsilon path table (its first path per state in off[s].z)
   std::vector<uint4> phead;
   std::vector<float> ptail;
   uint32_t pstride = 0;
 };
 
 struct Layout {
-  uint64_t off, earc, xarc, xnext, sclass, final_w, ilabel, olabel, weight, level_base, pfirst, phead, ptail,
-      total;
+  uint64_t off, earc, xarc, xnext, sclass, final_w, ilabel, olabel, weight, level_base, phead, ptail, total;
 };
 
 Layout layout(int64_t S, int64_t A, uint64_t Ae, uint64_t Ax, uint32_t nlevels, bool finals, uint64_t npaths,
@@ -47,7 +46,7 @@ Layout layout(int64_t S, int64_t A, uint64_t Ae, uint64_t Ax, uint32_t nlevels, 
     p = align_up(p + bytes, 256);
     return at;
   };
-  l.off = take(sizeof(uint2) * (uint64_t)(S + 1));
+  l.off = take(sizeof(uint4) * (uint64_t)(S + 1));
   l.earc = take(sizeof(uint4) * (Ae ? Ae : 1));
   l.xarc = take(sizeof(uint4) * (Ax ? Ax : 1));
   l.xnext = take(sizeof(uint2) * (Ax ? Ax : 1));
@@ -57,7 +56,6 @@ Layout layout(int64_t S, int64_t A, uint64_t Ae, uint64_t Ax, uint32_t nlevels, 
   l.olabel = take(sizeof(int32_t) * (uint64_t)(A ? A : 1));
   l.weight = take(sizeof(float) * (uint64_t)(A ? A : 1));
   l.level_base = take(sizeof(uint32_t) * (uint64_t)(nlevels + 1));
-  l.pfirst = npaths ? take(sizeof(uint32_t) * (uint64_t)(S + 1)) : 0;
   l.phead = npaths ? take(sizeof(uint4) * npaths) : 0;
   l.ptail = npaths && pstride ? take(sizeof(float) * npaths * pstride) : 0;
   l.total = p;
@@ -151,8 +149,8 @@ void eps_paths(const wd_graph_desc* d, const std::vector<uint32_t>& topo, Prepar
   for (int64_t s = 0; s < S; ++s)
     if (xdeg[s] >= (1u << 24)) return;
   p.pstride = longest - 1;
-  p.pfirst.assign((size_t)S + 1, 0);
-  for (int64_t s = 0; s < S; ++s) p.pfirst[s + 1] = p.pfirst[s] + (uint32_t)npath[s];
+  p.paths = true;
+  for (int64_t s = 0; s < S; ++s) p.off[s + 1].z = p.off[s].z + (uint32_t)npath[s];
   p.phead.resize(total);
   p.ptail.assign(total * p.pstride, 0.0f);
   // depth-first walk of the epsilon arcs out of s: stack of (state, next arc)
@@ -160,7 +158,7 @@ void eps_paths(const wd_graph_desc* d, const std::vector<uint32_t>& topo, Prepar
   std::vector<float> wpath;  // weights of the current path's arcs
   for (int64_t s = 0; s < S; ++s) {
     if (!npath[s]) continue;
-    uint64_t at = p.pfirst[s];
+    uint64_t at = p.off[s].z;
     stack.assign(1, {(uint32_t)s, d->row_ptr[s]});
     wpath.clear();
     while (!stack.empty()) {
@@ -203,7 +201,7 @@ wd_status prepare(const wd_graph_desc* d, Prepared& p, uint64_t* Ae_out, uint64_
   uint64_t Ae = 0, Ax = 0;
   p.off.resize((size_t)S + 1);
   for (int64_t s = 0; s < S; ++s) {
-    p.off[s] = make_uint2((uint32_t)Ae, (uint32_t)Ax);
+    p.off[s] = make_uint4((uint32_t)Ae, (uint32_t)Ax, 0, 0);
     uint32_t ne = 0, nx = 0;
     for (uint32_t a = d->row_ptr[s]; a < d->row_ptr[s + 1]; ++a) (d->ilabel[a] ? ne : nx)++;
     Ae += ne;
@@ -217,7 +215,7 @@ wd_status prepare(const wd_graph_desc* d, Prepared& p, uint64_t* Ae_out, uint64_
       any_eps = true;
     }
   }
-  p.off[S] = make_uint2((uint32_t)Ae, (uint32_t)Ax);
+  p.off[S] = make_uint4((uint32_t)Ae, (uint32_t)Ax, 0, 0);
   p.nlevels = any_eps ? maxcls + 1 : 0;
   p.level_base.assign(p.nlevels + 1, 0);
   for (uint32_t l = 0; l < p.nlevels; ++l) p.level_base[l + 1] = p.level_base[l] + count[l];
@@ -283,7 +281,7 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
     if (!bytes) return WD_OK;
     return hip_check(hipMemcpyAsync(base + at, src, bytes, hipMemcpyHostToDevice, s), "graph upload");
   };
-  if ((st = put(l.off, p.off.data(), sizeof(uint2) * (S + 1))) ||
+  if ((st = put(l.off, p.off.data(), sizeof(uint4) * (S + 1))) ||
       (st = put(l.earc, p.earc.data(), sizeof(uint4) * Ae)) ||
       (st = put(l.xarc, p.xarc.data(), sizeof(uint4) * Ax)) ||
       (st = put(l.xnext, p.xnext.data(), sizeof(uint2) * Ax)) ||
@@ -293,7 +291,6 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
       (st = put(l.olabel, d->olabel, sizeof(int32_t) * A)) ||
       (st = put(l.weight, d->weight, sizeof(float) * A)) ||
       (st = put(l.level_base, p.level_base.data(), sizeof(uint32_t) * (p.nlevels + 1))) ||
-      (npaths && (st = put(l.pfirst, p.pfirst.data(), sizeof(uint32_t) * (S + 1)))) ||
       (npaths && (st = put(l.phead, p.phead.data(), sizeof(uint4) * npaths))) ||
       (npaths && p.pstride && (st = put(l.ptail, p.ptail.data(), sizeof(float) * npaths * p.pstride))))
     return st;
@@ -308,7 +305,7 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
   g->level_base = p.level_base;
   g->bytes = l.total;
   DevGraph& dg = g->dg;
-  dg.off = (const uint2*)(base + l.off);
+  dg.off = (const uint4*)(base + l.off);
   dg.earc = (const uint4*)(base + l.earc);
   dg.xarc = (const uint4*)(base + l.xarc);
   dg.xnext = (const uint2*)(base + l.xnext);
@@ -318,7 +315,6 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
   dg.olabel_id = (const int32_t*)(base + l.olabel);
   dg.weight_id = (const float*)(base + l.weight);
   dg.level_base = (const uint32_t*)(base + l.level_base);
-  dg.pfirst = npaths ? (const uint32_t*)(base + l.pfirst) : nullptr;
   dg.phead = npaths ? (const uint4*)(base + l.phead) : nullptr;
   dg.ptail = npaths && p.pstride ? (const float*)(base + l.ptail) : nullptr;
   dg.npaths = npaths;

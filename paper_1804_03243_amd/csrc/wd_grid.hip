@@ -783,7 +783,7 @@ __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* _
       L.f_key[p] = (uint32_t)(v >> 32);
       L.f_arc[p] = (uint32_t)v;
       if ((uint32_t)(v >> 32) == best) atomicMin(&G.best_pos, (uint32_t)p);
-      const uint2 o0 = g.off[st], o1 = g.off[st + 1];
+      const uint4 o0 = g.off[st], o1 = g.off[st + 1];
       deg += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
     }
     pos0 += tot;
@@ -808,14 +808,14 @@ __global__ void __launch_bounds__(kGT) k_g_degrees(DevGraph g, const LaneDesc* _
   unsigned long long c = 0;
   for (uint64_t p = lo; p < hi; ++p) {
     const uint32_t st = L.f_state[p];
-    const uint2 o0 = g.off[st], o1 = g.off[st + 1];
+    const uint4 o0 = g.off[st], o1 = g.off[st + 1];
     c += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
   }
   unsigned long long tot;
   unsigned long long q = G.part[1][blockIdx.x] + gexcl64(c, s, &tot);
   for (uint64_t p = lo; p < hi; ++p) {
     const uint32_t st = L.f_state[p];
-    const uint2 o0 = g.off[st], o1 = g.off[st + 1];
+    const uint4 o0 = g.off[st], o1 = g.off[st + 1];
     L.f_edeg[p] = (uint32_t)q;
     L.f_xdeg[p] = (uint32_t)(q >> 32);
     L.f_ebeg[p] = o0.x;
