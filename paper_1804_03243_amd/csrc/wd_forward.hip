@@ -29,6 +29,9 @@ constexpr int kWaitVm0 = 0x0f70;
 constexpr uint32_t kLdsWork = 3 * kHashMax;  // emitting work above which a frame starts global
 constexpr uint32_t kBkCap = 1024;            // LDS epsilon bucket entries before a frame spills
 constexpr uint32_t kDirectRank = 256;        // survivors ranked directly, without the counting sort
+// the thread that keeps the per-frame counters and records: the last one,
+// whose wavefront is idle in small frames' steps
+constexpr uint32_t kBook = kThreads - 1;
 static_assert(kBkCap == (uint32_t)kThreads, "one bucket entry per thread in the epsilon level scan");
 
 struct FwdShared {
@@ -345,7 +348,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
   for (; t <= T; ++t) {
     stamp(0);
     if (t > 0) {
-      if (tid == 0 && W > sh.c_need_arcs) sh.c_need_arcs = W;
+      if (tid == kBook && W > sh.c_need_arcs) sh.c_need_arcs = W;
       if (W > L.cand_cap) {
         status = 4;  // WD_ECAPACITY
         ovf |= kOvfArcs;
@@ -413,6 +416,8 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
                   if (fresh && cls != kNoEps) {
                     if (paths) {
                       lds_bucket_paths(sh, slot, o0.z, o1.z, o1.y - o0.y);
+                      // start the state's first epsilon paths on their way for the closure
+                      warm = __uint_as_float(g.phead[o0.z].z);
                     } else {
                       lds_bucket(sh, slot, o0, o1, cls);
                       // start the state's first epsilon arc on its way for the closure
@@ -685,7 +690,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         __syncthreads();
         ns = sh.n_surv;
         stamp(3);
-        if (tid == 0 && sh.hcount > sh.c_need_frame) sh.c_need_frame = sh.hcount;
+        if (tid == kBook && sh.hcount > sh.c_need_frame) sh.c_need_frame = sh.hcount;
       } else {
         // --------------------------------------- global per-state slot array
         if (t == 0) {
@@ -763,7 +768,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         }
         stamp(2);
         const uint32_t nt = sh.n_touched;
-        if (tid == 0 && nt > sh.c_need_frame) sh.c_need_frame = nt;
+        if (tid == kBook && nt > sh.c_need_frame) sh.c_need_frame = nt;
         if (nt > L.frame_cap) {
           status = 4;
           ovf |= kOvfFrame;
@@ -799,7 +804,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     }
     if (failed) break;
     my_eps += eps_frame;
-    if (t > 0 && tid == 0) sh.c_arcs += W;
+    if (t > 0 && tid == kBook) sh.c_arcs += W;
     const float best = key_cost(best_key);
     const float cutb = key_cost(kcutb);
     const unsigned long long* spack = lds ? sh.rs_pack : L.surv_pack;
@@ -1084,14 +1089,14 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         const uint32_t k1 = f.edeg[p + 1];
         for (uint32_t k = f.edeg[p]; k < k1; ++k) own_e[k] = (uint16_t)p;
       }
-    if (tid == 0) {
+    if (tid == kBook) {
       L.node_off[t] = node_base;
       L.node_off[t + 1] = node_base + n_keep;
       L.best[t] = best;
       L.cutb[t] = cutb;
       L.cut[t] = key_cost(cut_key);
     }
-    if (tid == 0) {
+    if (tid == kBook) {
       sh.c_tokens += n_keep;
       if (n_keep > sh.c_max_tokens) sh.c_max_tokens = n_keep;
     }
@@ -1222,7 +1227,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       status = kStatusInternal;
       break;
     }
-    if (tid == 0) {
+    if (tid == kBook) {
       L.link_off[t] = link_base;
       L.link_xoff[t] = link_base + nE;
       L.link_off[t + 1] = link_base + nE + nX;
@@ -1264,7 +1269,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     }
   }
   const uint64_t eps = block_sum64(my_eps, sh.bs, par);
-  const uint64_t arcs = sh.c_arcs + eps;  // thread 0's own write; read by thread 0 below
+  const uint64_t arcs = sh.c_arcs + eps;  // (the bookkeeping thread's writes, before the barrier)
   if (tid == 0) {
     LaneInfo* info = L.info;
     if (status == 0 && (ovf & (kOvfNodes | kOvfLinks))) status = 4;
