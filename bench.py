@@ -279,8 +279,8 @@ def batch(wfstdec, graph, n_utts: int = 64, steps: int = 3, cpu: bool = True) ->
     return out
 
 
-PHASE_NAMES = ("expand", "eps_closure", "survivors", "max_active", "compact", "degrees", "link_count",
-               "link_write", "frame_end")
+PHASE_NAMES = ("expand", "eps_closure", "survivors", "max_active", "compact", "degrees_emitting_links",
+               "eps_links", "links_published", "frame_end")
 
 
 def phase_profile(wfstdec, workload: str, reps: int = 3) -> dict:

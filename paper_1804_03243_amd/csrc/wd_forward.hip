@@ -47,6 +47,8 @@ struct FwdShared {
   uint32_t lvl_wide;   // LDS table: first epsilon level the whole workgroup runs
   uint32_t lvl_live;   // LDS table: levels that may hold an entry within the cutoff (level_bit)
   unsigned long long deg_tot;  // frontier out-degree totals (epsilon << 32 | emitting), small frames
+  uint32_t wcnt[kWaves];  // emitting lattice links of the frame per wavefront (one item per thread)
+  uint32_t lnx;        // epsilon lattice links of the frame (one-wavefront epsilon link pass)
   uint32_t hcount;     // LDS table: reserved entries
   uint32_t spill;      // LDS table full: the frame goes global
   uint32_t n_bk;       // LDS table: epsilon bucket entries
@@ -840,6 +842,18 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       cut_key = vkey < kcutb ? vkey : kcutb;
     }
     stamp(4);
+    // Emitting lattice links: a thread's own candidate (work item tid) is a
+    // link when it is within the final cutoff.  With one item per thread,
+    // each wavefront's count goes out with the compaction's barrier and the
+    // links are written right after it, beside the degree prefix sums.
+    const bool early_e = W <= (uint32_t)kThreads;  // (uniform; W = 0 at frame 0)
+    bool e_in = false;
+    if (early_e) {
+      const uint32_t xk = cost_key(__uint_as_float(my_c.w));
+      e_in = t > 0 && tid < W && xk <= cut_key && xk < kInfKey;
+      const uint64_t bal = __ballot(e_in);
+      if (lane_id() == 0) sh.wcnt[wave_id()] = (uint32_t)__popcll(bal);
+    }
     // -------------------------------- compaction into a frontier sorted by state
     const bool fl = n_keep <= (uint32_t)kFrontCap;
     const Front f = front_at(fl, sh, L);
@@ -1009,18 +1023,55 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     }
     __syncthreads();
     stamp(5);
+    // node id of a state that survived frame t
+    auto dst_node = [&](uint32_t s) -> uint64_t {
+      if (lds) {
+        const uint32_t slot = h_find(sh, s);
+        return slot < (uint32_t)kHashCap ? sh.h_val[slot] : kEmpty;
+      }
+      return L.idx[s];
+    };
+    // the emitting links of the frame, when every work item is a thread's own
+    uint32_t nE = 0, bad_idx = 0;
+    auto write_emitting = [&]() {
+      uint32_t before = 0;
+#pragma unroll
+      for (int i = 0; i < kWaves; ++i) {
+        const uint32_t c = sh.wcnt[i];
+        nE += c;
+        before += (uint32_t)i < wave_id() ? c : 0u;
+      }
+      const uint64_t bal = __ballot(e_in);
+      if (!e_in || !hist_ok || link_base + nE > L.link_cap) return;
+      // the thread's own candidate: its insertion left the slot
+      const uint64_t dn = lds && my_slot < (uint32_t)kHashCap ? sh.h_val[my_slot] : dst_node(my_c.z);
+      if (dn < node_base || dn >= node_base + n_keep) {
+        bad_idx = 1;
+        return;
+      }
+      // the frontier reads come before the stores: a wait for a flat load
+      // also waits for every store in flight
+      const uint32_t q = (uint32_t)(dn - node_base);
+      const uint32_t fk = f.key[q], fa = f.arc[q];
+      const uint32_t pos = before + (uint32_t)__popcll(bal & lanemask_lt());
+      L.links[link_base + pos] = make_uint4(my_c.x, my_c.y, (uint32_t)dn, my_c.w);
+      if (fk == cost_key(__uint_as_float(my_c.w)) && fa == my_c.x) L.n_pred[dn] = my_c.y;
+    };
     // ------------------------------- arc offsets and degree prefix sums
     uint32_t W_next, W_eps;
     if (deg_ready) {
-      // at most kDirectRank tokens with their degrees in place: the first
-      // wavefront sums them, four per lane, and publishes the totals
+      // at most kDirectRank tokens with their degrees in place: the last
+      // wavefront (no work items in small frames, which the others write as
+      // emitting links meanwhile) sums them, four per lane, and publishes
+      // the totals
       static_assert(kDirectRank <= 4 * 64, "four tokens per lane");
-      if (tid < 64u) {
+      if (tid >= kThreads - 64u) {
+        const uint32_t lane = lane_id();
         uint32_t de[4], dx[4];
         uint64_t sum = 0;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          const uint32_t p = 4u * tid + (uint32_t)k;
+          const uint32_t p = 4u * lane + (uint32_t)k;
           de[k] = p < n_keep ? f.edeg[p] : 0u;
           dx[k] = p < n_keep ? f.xdeg[p] : 0u;
           sum += ((uint64_t)dx[k] << 32) | de[k];
@@ -1029,7 +1080,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         uint32_t eb = (uint32_t)(inc - sum), xb = (uint32_t)((inc - sum) >> 32);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          const uint32_t p = 4u * tid + (uint32_t)k;
+          const uint32_t p = 4u * lane + (uint32_t)k;
           if (p < n_keep) {
             f.edeg[p] = eb;
             f.xdeg[p] = xb;
@@ -1037,12 +1088,13 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           eb += de[k];
           xb += dx[k];
         }
-        if (tid == 63u) {
+        if (lane == 63u) {
           sh.deg_tot = inc;
           f.edeg[n_keep] = (uint32_t)inc;
           f.xdeg[n_keep] = (uint32_t)(inc >> 32);
         }
       }
+      if (early_e) write_emitting();
       __syncthreads();
       W_next = (uint32_t)sh.deg_tot;
       W_eps = (uint32_t)(sh.deg_tot >> 32);
@@ -1078,6 +1130,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         f.edeg[n_keep] = W_next;
         f.xdeg[n_keep] = W_eps;
       }
+      if (early_e) write_emitting();
       __syncthreads();
     }
     stamp(6);
@@ -1116,19 +1169,49 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       }
     }
     // -------------------------------------------------- lattice links of frame t
-    // node id of a state that survived frame t
-    auto dst_node = [&](uint32_t s) -> uint64_t {
-      if (lds) {
-        const uint32_t slot = h_find(sh, s);
-        return slot < (uint32_t)kHashCap ? sh.h_val[slot] : kEmpty;
+    uint32_t nX = 0, xmask = 0;
+    // With the emitting links written and at most 64 epsilon out-arcs on the
+    // frontier, wavefront 1 writes the epsilon links alone: a wavefront scan
+    // places them, and the frame's closing collective publishes their count.
+    const bool wave_x = early_e && W_eps <= 64u;  // (uniform)
+    if (wave_x) {
+      if (tid >= 64u && tid < 128u) {
+        const uint32_t e = tid - 64u;
+        bool in = false;
+        uint4 r = make_uint4(0, 0, 0, 0);
+        uint32_t p = 0, xk = kNoKey;
+        float x = 0.0f;
+        if (e < W_eps) {
+          p = search_le(f.xdeg, n_keep, e);
+          r = g.xarc[f.xbeg[p] + (e - f.xdeg[p])];
+          x = canon(key_cost(f.key[p]) + __uint_as_float(r.y));
+          xk = cost_key(x);
+          in = xk <= cut_key && xk < kInfKey;
+        }
+        const uint64_t bal = __ballot(in);
+        const uint32_t cntx = (uint32_t)__popcll(bal);
+        if (tid == 64u) sh.lnx = cntx;
+        if (in && hist_ok && link_base + nE + cntx <= L.link_cap) {
+          const uint64_t dn = dst_node(r.x);
+          if (dn < node_base || dn >= node_base + n_keep) {
+            bad_idx = 1;
+          } else {
+            const uint32_t sn = (uint32_t)(node_base + p);
+            const uint64_t at = link_base + nE + (uint32_t)__popcll(bal & lanemask_lt());
+            const uint32_t q = (uint32_t)(dn - node_base);
+            const uint32_t cls = f.cls[p], fk = f.key[q], fa = f.arc[q];  // before the stores
+            L.links[at] = make_uint4(r.w, sn, (uint32_t)dn, __float_as_uint(x));
+            L.link_lvl[at] = (uint8_t)cls;
+            xmask |= 1u << (cls < 31 ? cls : 31);
+            if (fk == xk && fa == r.w) L.n_pred[dn] = sn;
+          }
+        }
       }
-      return L.idx[s];
-    };
-    uint32_t nE = 0, nX = 0;
-    uint32_t bad_idx = 0, xmask = 0;
-    {
-      // emitting run: candidates in work-item order are in arc-id order
-      const uint32_t Wc = t > 0 ? W : 0;
+      stamp(7);
+    } else {
+      // emitting run (unless written above): candidates in work-item order
+      // are in arc-id order
+      const uint32_t Wc = t > 0 && !early_e ? W : 0;
       const uint32_t per = (Wc + kThreads - 1) / kThreads;
       const uint32_t w0 = tid * per < Wc ? tid * per : Wc;
       const uint32_t w1 = w0 + per < Wc ? w0 + per : Wc;
@@ -1160,7 +1243,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       uint64_t tot2;
       const uint64_t ex2 = block_excl_scan64(((uint64_t)cntx << 32) | cnt, sh.bs, par, &tot2);
       uint32_t pos = (uint32_t)ex2, posx = (uint32_t)(ex2 >> 32);
-      nE = (uint32_t)tot2;
+      if (!early_e) nE = (uint32_t)tot2;
       nX = (uint32_t)(tot2 >> 32);
       stamp(7);
       if (hist_ok && link_base + nE + nX > L.link_cap) {
@@ -1221,6 +1304,13 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     const uint32_t h_used_n = sh.hcount < (uint32_t)kHashMax ? sh.hcount : (uint32_t)kHashMax;
     const uint32_t fl_or = block_or((bad_idx ? 0x80000000u : 0u) | xmask, sh.bs, par);
     stamp(8);
+    if (wave_x) {
+      nX = sh.lnx;
+      if (hist_ok && link_base + nE + nX > L.link_cap) {
+        hist_ok = false;
+        ovf |= kOvfLinks;
+      }
+    }
     note(kProfStamps, (lds ? 1ull : 0ull) | ((uint64_t)n_keep << 8) | ((uint64_t)(nE + nX) << 32));
     note(kProfStamps + 1, (t > 0 ? (uint64_t)W : 0ull) | ((uint64_t)(lds ? sh.n_bk : 0u) << 32));
     if (fl_or & 0x80000000u) {
