@@ -13,28 +13,65 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return (lane_id() == 0) ? 0ull : (~0ull >> (64u - lane_id()));
 }
 
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    uint32_t n = __shfl_up(v, o, 64);
-    if ((int)lane_id() >= o) v += n;
-  }
-  return v;
+// Wavefront scans and reductions by DPP (data-parallel primitives of the
+// GFX9 vector ALU: a lane reads another lane's register within the same
+// instruction), which take a few cycles per step where a shuffle through
+// the LDS crossbar takes a round trip.  A wavefront is four rows of 16
+// lanes: row shifts by 1, 2, 4 and 8 scan each row, then lane 15 of rows 0
+// and 2 is broadcast into rows 1 and 3 and lane 31 into rows 2 and 3.
+// Every lane of the wavefront must be active.
+enum : int {
+  kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118,
+  kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143
+};
+
+// Lane i reads the lane its DPP control names; `fill` where that lane is
+// outside the row or the row is not in ROWS.
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ uint32_t dpp32(uint32_t v, uint32_t fill) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)fill, (int)v, CTRL, ROWS, 0xf, false);
 }
 
-__device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int o) {
-  uint32_t lo = __shfl_up((uint32_t)v, o, 64);
-  uint32_t hi = __shfl_up((uint32_t)(v >> 32), o, 64);
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v, uint64_t fill) {
+  const uint32_t lo = dpp32<CTRL, ROWS>((uint32_t)v, (uint32_t)fill);
+  const uint32_t hi = dpp32<CTRL, ROWS>((uint32_t)(v >> 32), (uint32_t)(fill >> 32));
   return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ uint64_t wave_incl_scan64(uint64_t v) {
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    uint64_t n = shfl_up64(v, o);
-    if ((int)lane_id() >= o) v += n;
+// Inclusive scan over the wavefront with an associative op and its identity.
+template <class T, class Op>
+__device__ __forceinline__ T wave_scan_op(T v, T id, Op op) {
+  if constexpr (sizeof(T) == 8) {
+    v = op(v, (T)dpp64<kDppRowShr1>(v, id));
+    v = op(v, (T)dpp64<kDppRowShr2>(v, id));
+    v = op(v, (T)dpp64<kDppRowShr4>(v, id));
+    v = op(v, (T)dpp64<kDppRowShr8>(v, id));
+    v = op(v, (T)dpp64<kDppRowBcast15, 0xa>(v, id));
+    v = op(v, (T)dpp64<kDppRowBcast31, 0xc>(v, id));
+  } else {
+    v = op(v, (T)dpp32<kDppRowShr1>(v, id));
+    v = op(v, (T)dpp32<kDppRowShr2>(v, id));
+    v = op(v, (T)dpp32<kDppRowShr4>(v, id));
+    v = op(v, (T)dpp32<kDppRowShr8>(v, id));
+    v = op(v, (T)dpp32<kDppRowBcast15, 0xa>(v, id));
+    v = op(v, (T)dpp32<kDppRowBcast31, 0xc>(v, id));
   }
   return v;
+}
+
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  return wave_scan_op<uint32_t>(v, 0u, [](uint32_t a, uint32_t b) { return a + b; });
+}
+
+__device__ __forceinline__ uint64_t wave_incl_scan64(uint64_t v) {
+  return wave_scan_op<uint64_t>(v, 0ull, [](uint64_t a, uint64_t b) { return a + b; });
+}
+
+// Value of lane 63 in every lane (a scalar register).
+__device__ __forceinline__ uint32_t lane63(uint32_t v) { return (uint32_t)__builtin_amdgcn_readlane((int)v, 63); }
+__device__ __forceinline__ uint64_t lane63_64(uint64_t v) {
+  return ((uint64_t)lane63((uint32_t)(v >> 32)) << 32) | lane63((uint32_t)v);
 }
 
 __device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int m) {
@@ -97,12 +134,8 @@ template <int NW = kWaves>
 __device__ __forceinline__ uint64_t block_min64(uint64_t v, BlockScratch& bs, uint32_t& par) {
   const uint32_t b = par;
   par ^= 1u;
-#pragma unroll
-  for (int m = 32; m > 0; m >>= 1) {
-    uint64_t o = shfl_xor64(v, m);
-    v = o < v ? o : v;
-  }
-  if (lane_id() == 0) bs.w64[b][wave_id()] = v;
+  v = wave_scan_op<uint64_t>(v, ~0ull, [](uint64_t a, uint64_t c) { return c < a ? c : a; });
+  if (lane_id() == 63) bs.w64[b][wave_id()] = v;
   __syncthreads();
   uint64_t r = bs.w64[b][0];
 #pragma unroll
@@ -114,9 +147,8 @@ template <int NW = kWaves>
 __device__ __forceinline__ uint64_t block_sum64(uint64_t v, BlockScratch& bs, uint32_t& par) {
   const uint32_t b = par;
   par ^= 1u;
-#pragma unroll
-  for (int m = 32; m > 0; m >>= 1) v += shfl_xor64(v, m);
-  if (lane_id() == 0) bs.w64[b][wave_id()] = v;
+  v = wave_incl_scan64(v);
+  if (lane_id() == 63) bs.w64[b][wave_id()] = v;
   __syncthreads();
   uint64_t r = 0;
 #pragma unroll
@@ -125,18 +157,15 @@ __device__ __forceinline__ uint64_t block_sum64(uint64_t v, BlockScratch& bs, ui
 }
 
 __device__ __forceinline__ uint32_t wave_or(uint32_t v) {
-#pragma unroll
-  for (int m = 32; m > 0; m >>= 1) v |= __shfl_xor(v, m, 64);
-  return v;
+  return lane63(wave_scan_op<uint32_t>(v, 0u, [](uint32_t a, uint32_t c) { return a | c; }));
 }
 
 template <int NW = kWaves>
 __device__ __forceinline__ uint32_t block_or(uint32_t v, BlockScratch& bs, uint32_t& par) {
   const uint32_t b = par;
   par ^= 1u;
-#pragma unroll
-  for (int m = 32; m > 0; m >>= 1) v |= __shfl_xor(v, m, 64);
-  if (lane_id() == 0) bs.w32[b][wave_id()] = v;
+  v = wave_scan_op<uint32_t>(v, 0u, [](uint32_t a, uint32_t c) { return a | c; });
+  if (lane_id() == 63) bs.w32[b][wave_id()] = v;
   __syncthreads();
   uint32_t r = 0;
 #pragma unroll
@@ -152,7 +181,7 @@ __device__ __forceinline__ uint32_t wave_append(bool pred, uint32_t* counter) {
   if (m) {
     int leader = __ffsll((unsigned long long)m) - 1;
     if ((int)lane_id() == leader) base = atomicAdd(counter, (uint32_t)__popcll(m));
-    base = __shfl(base, leader, 64);
+    base = (uint32_t)__builtin_amdgcn_readlane((int)base, leader);
   }
   return base + (uint32_t)__popcll(m & lanemask_lt());
 }

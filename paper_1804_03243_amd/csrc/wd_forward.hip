@@ -503,7 +503,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
             // barrier, and when the paths fit its lanes it relaxes them alone
             if (tid < 64u) {
               const uint32_t inc = wave_incl_scan(d), ex = inc - d;
-              const uint32_t all = __shfl(inc, 63, 64);
+              const uint32_t all = lane63(inc);
               sh.xp[tid] = ex;
               if (all <= kOwnCap)
                 for (uint32_t k = 0; k < d; ++k) own[ex + k] = (uint16_t)tid;
@@ -602,7 +602,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
               if (e.w == lvl && (uint32_t)(sh.h_val[e.x] >> 32) <= kcutb) d = e.z - e.y;
             }
             const uint32_t inc = wave_incl_scan(d), ex = inc - d;
-            const uint32_t all = __shfl(inc, 63, 64);
+            const uint32_t all = lane63(inc);
             if (all > 64u) break;  // (nothing of this level done yet)
             eps_frame += d;
             sh.xp[tid] = ex;
@@ -637,7 +637,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
             // workgroup barrier, and one barrier publishes the result
             if (tid < 64u) {
               const uint32_t inc = wave_incl_scan(d), ex = inc - d;
-              const uint32_t all = __shfl(inc, 63, 64);
+              const uint32_t all = lane63(inc);
               sh.xp[tid] = ex;
               if (all <= kOwnCap)
                 for (uint32_t k = 0; k < d; ++k) own[ex + k] = (uint16_t)tid;
