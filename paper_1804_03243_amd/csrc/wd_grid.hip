@@ -80,6 +80,8 @@ struct GridLane {
 
 struct GScratch {
   unsigned long long w[kGW];
+  unsigned long long w2[kGW][2];
+  uint32_t u[4];
 };
 
 __device__ __forceinline__ unsigned long long gsum64(unsigned long long v, GScratch& s) {
@@ -185,6 +187,38 @@ __device__ __forceinline__ void scan_parts(unsigned long long* part, GScratch& s
   if (threadIdx.x == 0) part[kGB] = tot;
 }
 
+// Workgroup b's exclusive prefix among the kGB per-workgroup sums in part
+// (as written by the kernel before: the consumer sums them itself rather
+// than a separate one-workgroup scan launch) and their total.
+__device__ __forceinline__ void part_prefix(const unsigned long long* part, uint32_t b, GScratch& s,
+                                            unsigned long long* before, unsigned long long* total) {
+  constexpr uint32_t per = kGB / kGT;
+  unsigned long long lo = 0, all = 0;
+#pragma unroll
+  for (uint32_t i = 0; i < per; ++i) {
+    const uint32_t j = threadIdx.x * per + i;
+    const unsigned long long v = part[j];
+    all += v;
+    lo += j < b ? v : 0ull;
+  }
+  lo = wave_incl_scan64(lo);
+  all = wave_incl_scan64(all);
+  __syncthreads();
+  if (lane_id() == 63) {
+    s.w2[wave_id()][0] = lo;
+    s.w2[wave_id()][1] = all;
+  }
+  __syncthreads();
+  unsigned long long a = 0, c = 0;
+#pragma unroll
+  for (int i = 0; i < kGW; ++i) {
+    a += s.w2[i][0];
+    c += s.w2[i][1];
+  }
+  *before = a;
+  *total = c;
+}
+
 // Exclusive scan of the kGB partial sums part[which] of each utterance
 // (lattice != 0: after the forward pass has stopped, for utterances whose
 // status is still WD_OK).
@@ -218,18 +252,48 @@ __global__ void k_g_init(const LaneDesc* __restrict__ lanes, GridLane* gl, const
   }
 }
 
-// Frame start: the start token (t = 0), or the emitting work check and the
-// cutoff prefilter bound (t > 0).  The bound (Sec. 4.3 prunes each transition
-// against a beam as it is made): the best emitting candidate of one best token
-// of frame t-1, plus the beam.  That candidate is one of all the frame's
-// candidates, so the exact beam cutoff (best of all, plus the beam) is not
-// above the bound, and a candidate above the bound can never survive or
-// become a lattice link: expansion skips its recombination.  One wavefront.
-__global__ void k_g_begin(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl, Params prm, int t) {
+// Frame 0: the start token.  One wavefront.
+__global__ void k_g_begin(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl) {
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
-  if (G.stop) return;
-  if (t > 0) {
+  if (G.stop || threadIdx.x != 0) return;
+  const uint32_t s0 = g.start;
+  L.slot[s0] = pack_tok(cost_key(0.0f), kNoArc);
+  L.touched[0] = s0;
+  G.n_touched = 1;
+  const uint32_t c = g.sclass[s0];
+  if (c != kNoEps) {
+    L.bucket[g.level_base[c]] = s0;
+    G.nb[c] = 1;
+  }
+  G.best_key = cost_key(0.0f);
+}
+
+// Start of the emitting expansion of frame t > 0, in every workgroup of the
+// expansion kernel: the work capacity check (workgroup 0 records it and the
+// frame's work) and the cutoff prefilter bound, which each workgroup
+// computes for itself from the same inputs.  The bound (Sec. 4.3 prunes each
+// transition against a beam as it is made): the best emitting candidate of
+// one best token of frame t-1, plus the beam.  That candidate is one of all
+// the frame's candidates, so the exact beam cutoff (best of all, plus the
+// beam) is not above the bound, and a candidate above the bound can never
+// survive or become a lattice link: expansion skips its recombination.
+// Returns false when the frame does not fit (every workgroup stops).
+__device__ __forceinline__ bool expand_begin(const DevGraph& g, const LaneDesc& L, GridLane& G, const Params& prm,
+                                             int t, GScratch& s, uint32_t* ub) {
+  const uint32_t W = G.W;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    G.need_arcs = W > G.need_arcs ? W : G.need_arcs;
+    if (W > L.cand_cap) {
+      G.status = 4;  // WD_ECAPACITY
+      G.ovf |= kOvfArcs;
+      G.stop = 1;
+    } else {
+      G.arcs += W;
+    }
+  }
+  if (W > L.cand_cap) return false;
+  if (threadIdx.x < 64u) {
     const uint32_t p = G.best_pos;
     uint32_t m = 0xffffffffu;
     if (p < G.n_prev) {
@@ -245,37 +309,12 @@ __global__ void k_g_begin(DevGraph g, const LaneDesc* __restrict__ lanes, GridLa
         m = xk < m ? xk : m;
       }
     }
-#pragma unroll
-    for (int k = 32; k > 0; k >>= 1) {
-      const uint32_t o = __shfl_xor(m, k, 64);
-      m = o < m ? o : m;
-    }
-    if (threadIdx.x == 0) G.ub = m < kInfKey ? cost_key(key_cost(m) + prm.beam) : 0xffffffffu;
+    m = lane63(wave_scan_op<uint32_t>(m, 0xffffffffu, [](uint32_t a, uint32_t b) { return b < a ? b : a; }));
+    if (threadIdx.x == 0) s.u[0] = m < kInfKey ? cost_key(key_cost(m) + prm.beam) : 0xffffffffu;
   }
-  if (threadIdx.x != 0) return;
-  if (t == 0) {
-    const uint32_t s0 = g.start;
-    L.slot[s0] = pack_tok(cost_key(0.0f), kNoArc);
-    L.touched[0] = s0;
-    G.n_touched = 1;
-    const uint32_t c = g.sclass[s0];
-    if (c != kNoEps) {
-      L.bucket[g.level_base[c]] = s0;
-      G.nb[c] = 1;
-    }
-    G.best_key = cost_key(0.0f);
-    return;
-  }
-  G.need_arcs = G.W > G.need_arcs ? G.W : G.need_arcs;
-  if (G.W > L.cand_cap) {
-    G.status = 4;  // WD_ECAPACITY
-    G.ovf |= kOvfArcs;
-    G.stop = 1;
-    return;
-  }
-  G.arcs += G.W;
-  G.best_key = 0xffffffffu;
-  G.disp = 0;
+  __syncthreads();
+  *ub = s.u[0];
+  return true;
 }
 
 // First touches of a workgroup staged in LDS and published with one global
@@ -350,7 +389,7 @@ __device__ __forceinline__ void stage_flush(TouchStageT<CAP>& ts, GridLane& G, c
 // Emitting expansion of frame t: work item w is arc w - edeg[i] of frontier
 // token i of frame t-1.  Writes the candidate of every work item.
 __global__ void __launch_bounds__(kGT) k_g_expand(DevGraph g, const LaneDesc* __restrict__ lanes,
-                                                  GridLane* gl, int t) {
+                                                  GridLane* gl, Params prm, int t) {
   __shared__ GScratch s;
   __shared__ uint32_t seg[kSeg];
   __shared__ uint32_t rng[2];
@@ -358,7 +397,9 @@ __global__ void __launch_bounds__(kGT) k_g_expand(DevGraph g, const LaneDesc* __
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop || t == 0) return;
-  const uint32_t W = G.W, n_prev = G.n_prev, ub = G.ub;
+  uint32_t ub;
+  if (!expand_begin(g, L, G, prm, t, s, &ub)) return;
+  const uint32_t W = G.W, n_prev = G.n_prev;
   const uint64_t nbp = G.node_base_prev;
   const float* row = L.ll + (size_t)(t - 1) * g.P;
   uint64_t blo, bhi;
@@ -406,13 +447,15 @@ constexpr uint32_t kDynGroup = 8;
 constexpr uint32_t kDynStage = 4096;
 
 __global__ void __launch_bounds__(kGT) k_g_expand_dyn(DevGraph g, const LaneDesc* __restrict__ lanes,
-                                                      GridLane* gl, int t) {
+                                                      GridLane* gl, Params prm, int t) {
   __shared__ GScratch s;
   __shared__ TouchStageT<kDynStage> ts;
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop || t == 0) return;
-  const uint32_t n_prev = G.n_prev, ub = G.ub;
+  uint32_t ub;
+  if (!expand_begin(g, L, G, prm, t, s, &ub)) return;
+  const uint32_t n_prev = G.n_prev;
   const uint64_t nbp = G.node_base_prev;
   const float* row = L.ll + (size_t)(t - 1) * g.P;
   stage_reset(ts, g.nlevels);
@@ -449,26 +492,13 @@ __global__ void __launch_bounds__(kGT) k_g_expand_dyn(DevGraph g, const LaneDesc
   if (threadIdx.x == 0 && my_best != 0xffffffffu) atomicMin(&G.best_key, my_best);
 }
 
-// Beam cutoff from the best emitting candidate (inclusive).
-__global__ void k_g_cut(GridLane* gl, Params prm) {
-  GridLane& G = gl[blockIdx.y];
-  if (G.stop || threadIdx.x != 0) return;
-  G.best_pos = 0xffffffffu;  // set again by this frame's compaction
-  if (G.best_key >= kInfKey) {
-    G.status = 3;  // WD_ENOPATH
-    G.stop = 1;
-    return;
-  }
-  G.kcutb = cost_key(key_cost(G.best_key) + prm.beam);
-}
-
 // Epsilon closure, level `lvl`: states of that level within the cutoff relax
 // their epsilon arcs; destinations sit on higher levels.  Per tile of 256
 // bucket states the workgroup spreads the tile's arcs over its threads (a
 // prefix sum of the states' epsilon degrees in LDS), so a state with many
 // epsilon arcs does not serialise the kernel.
 __global__ void __launch_bounds__(kGT) k_g_level(DevGraph g, const LaneDesc* __restrict__ lanes,
-                                                 GridLane* gl, uint32_t lvl) {
+                                                 GridLane* gl, Params prm, uint32_t lvl) {
   __shared__ GScratch s;
   __shared__ TouchStage ts;
   __shared__ uint32_t t_beg[kGT], t_ex[kGT], t_key[kGT];
@@ -477,7 +507,10 @@ __global__ void __launch_bounds__(kGT) k_g_level(DevGraph g, const LaneDesc* __r
   if (G.stop) return;
   const uint32_t n = G.nb[lvl];
   if (n == 0 || blockIdx.x * kGT >= n) return;
-  const uint32_t kcutb = G.kcutb;
+  // beam cutoff from the best emitting candidate (inclusive); no candidate:
+  // the survivor kernel reports it
+  if (G.best_key >= kInfKey) return;
+  const uint32_t kcutb = cost_key(key_cost(G.best_key) + prm.beam);
   const uint32_t* bk = L.bucket + g.level_base[lvl];
   stage_reset(ts, g.nlevels);
   unsigned long long eps = 0;
@@ -512,24 +545,6 @@ __global__ void __launch_bounds__(kGT) k_g_level(DevGraph g, const LaneDesc* __r
   if (threadIdx.x == 0 && eps) atomicAdd((unsigned long long*)&G.eps_arcs, eps);
 }
 
-// After the closure: frame capacity and the digit layout of the histogram.
-__global__ void k_g_check(const LaneDesc* __restrict__ lanes, GridLane* gl) {
-  const LaneDesc& L = lanes[blockIdx.y];
-  GridLane& G = gl[blockIdx.y];
-  if (G.stop || threadIdx.x != 0) return;
-  const uint32_t nt = G.n_touched;
-  G.need_frame = nt > G.need_frame ? nt : G.need_frame;
-  if (nt > L.frame_cap) {
-    G.status = 4;
-    G.ovf |= kOvfFrame;
-    G.stop = 1;
-    return;
-  }
-  const uint32_t span = G.kcutb - G.best_key;
-  G.nbits = span ? 32u - (uint32_t)__clz(span) : 0u;
-  G.shift = G.nbits > 11u ? G.nbits - 11u : 0u;
-}
-
 // Survivors of the beam cutoff; resets the touched slots; histogram of the
 // top cost-key digit when max-active is on.  Costs never fall below the best
 // emitting candidate (weights are >= 0), so the digit is in range.  Survivors
@@ -544,7 +559,35 @@ __global__ void __launch_bounds__(kGT) k_g_count(const LaneDesc* __restrict__ la
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
-  const uint32_t nt = G.n_touched, kcutb = G.kcutb, best = G.best_key, shift = G.shift;
+  // After the closure: no candidate at all (no path), the frame capacity,
+  // the beam cutoff and the digit layout of the histogram; every workgroup
+  // takes them from the same values, workgroup 0 records them for the
+  // kernels after this one.
+  const uint32_t nt = G.n_touched, best = G.best_key;
+  const bool nopath = best >= kInfKey, over = nt > L.frame_cap;
+  const uint32_t kcutb = nopath ? 0u : cost_key(key_cost(best) + prm.beam);
+  const uint32_t span = kcutb - best;
+  const uint32_t nbits = span ? 32u - (uint32_t)__clz(span) : 0u;
+  const uint32_t shift = nbits > 11u ? nbits - 11u : 0u;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    G.best_pos = 0xffffffffu;  // set again by this frame's compaction
+    if (nopath) {
+      G.status = 3;  // WD_ENOPATH
+      G.stop = 1;
+    } else {
+      G.need_frame = nt > G.need_frame ? nt : G.need_frame;
+      if (over) {
+        G.status = 4;
+        G.ovf |= kOvfFrame;
+        G.stop = 1;
+      } else {
+        G.kcutb = kcutb;
+        G.nbits = nbits;
+        G.shift = shift;
+      }
+    }
+  }
+  if (nopath || over) return;
   if (prm.max_active == 0) {
     // every survivor is kept: mark its state; its token stays in the slot,
     // where the compaction reads and resets it
@@ -700,14 +743,24 @@ __global__ void __launch_bounds__(kGT) k_g_mark(const LaneDesc* __restrict__ lan
 }
 
 // Kept states per workgroup chunk of the bitmap; node capacity check.
-__global__ void __launch_bounds__(kGT) k_g_bits(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl) {
+__global__ void __launch_bounds__(kGT) k_g_bits(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl,
+                                                Params prm) {
   __shared__ GScratch s;
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
-  if (blockIdx.x == 0 && threadIdx.x == 0 && G.hist_ok && G.node_base + G.n_keep > L.node_cap) {
-    G.hist_ok = 0;
-    G.ovf |= kOvfNodes;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    // without max-active every survivor is kept (the select kernels set these
+    // otherwise)
+    if (prm.max_active == 0) {
+      G.cut_key = G.kcutb;
+      G.n_keep = G.n_surv;
+    }
+    const uint32_t n_keep = prm.max_active == 0 ? G.n_surv : G.n_keep;
+    if (G.hist_ok && G.node_base + n_keep > L.node_cap) {
+      G.hist_ok = 0;
+      G.ovf |= kOvfNodes;
+    }
   }
   uint64_t blo, bhi, lo, hi;
   chunk((g.S + 31u) >> 5, blockIdx.x, &blo, &bhi);
@@ -733,7 +786,8 @@ __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* _
   if (G.stop) return;
   uint64_t blo, bhi;
   chunk((g.S + 31u) >> 5, blockIdx.x, &blo, &bhi);
-  uint64_t pos0 = G.part[0][blockIdx.x];
+  unsigned long long pos0, n_all;
+  part_prefix(G.part[0], blockIdx.x, s, &pos0, &n_all);
   const uint64_t nb = G.node_base;
   const bool store = G.hist_ok != 0;
   const uint32_t best = G.best_key;
@@ -801,8 +855,11 @@ __global__ void __launch_bounds__(kGT) k_g_degrees(DevGraph g, const LaneDesc* _
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
-  const uint64_t blo = G.part[0][blockIdx.x], bhi = G.part[0][blockIdx.x + 1];
-  const uint32_t n = (uint32_t)G.part[0][kGB];
+  unsigned long long blo, n_all, d_before, d_all;
+  part_prefix(G.part[0], blockIdx.x, s, &blo, &n_all);
+  part_prefix(G.part[1], blockIdx.x, s, &d_before, &d_all);
+  const uint64_t bhi = blo + G.part[0][blockIdx.x];
+  const uint32_t n = (uint32_t)n_all;
   uint64_t lo, hi;
   sub_chunk(blo, bhi, &lo, &hi);
   unsigned long long c = 0;
@@ -812,7 +869,7 @@ __global__ void __launch_bounds__(kGT) k_g_degrees(DevGraph g, const LaneDesc* _
     c += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
   }
   unsigned long long tot;
-  unsigned long long q = G.part[1][blockIdx.x] + gexcl64(c, s, &tot);
+  unsigned long long q = d_before + gexcl64(c, s, &tot);
   for (uint64_t p = lo; p < hi; ++p) {
     const uint32_t st = L.f_state[p];
     const uint4 o0 = g.off[st], o1 = g.off[st + 1];
@@ -824,7 +881,7 @@ __global__ void __launch_bounds__(kGT) k_g_degrees(DevGraph g, const LaneDesc* _
     q += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
-    const unsigned long long all = G.part[1][kGB];
+    const unsigned long long all = d_all;
     if (n != G.n_keep) G.bad = 1;
     G.W_next = (uint32_t)all;
     G.W_eps = (uint32_t)(all >> 32);
@@ -901,7 +958,8 @@ __global__ void __launch_bounds__(kGT) k_g_link_write(DevGraph g, const LaneDesc
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
   const uint32_t W = t > 0 ? G.W : 0, n = G.n_keep, cut = G.cut_key;
-  const unsigned long long all = G.part[2][kGB];
+  unsigned long long run, all;
+  part_prefix(G.part[2], blockIdx.x, s, &run, &all);
   const uint64_t nE = (uint32_t)all;
   const uint64_t lb = G.link_base, nb = G.node_base;
   if (!G.hist_ok || lb + nE + (all >> 32) > G.slot_hi) return;
@@ -909,7 +967,6 @@ __global__ void __launch_bounds__(kGT) k_g_link_write(DevGraph g, const LaneDesc
   chunk((uint64_t)W + G.W_eps, blockIdx.x, &blo, &bhi);
   if (blo >= bhi) return;
   const Seg sg = link_seg(L, W, n, blo, bhi, seg, rng);
-  unsigned long long run = G.part[2][blockIdx.x];
   uint32_t xm = 0, bad = 0;
   for (uint64_t base = blo; base < bhi; base += kGT) {
     const uint64_t it = base + threadIdx.x;
@@ -945,9 +1002,12 @@ __global__ void __launch_bounds__(kGT) k_g_link_write(DevGraph g, const LaneDesc
 
 // End of frame t: per-frame records, counters, and the state of frame t+1.
 __global__ void __launch_bounds__(kGT) k_g_end(const LaneDesc* __restrict__ lanes, GridLane* gl, int t) {
+  __shared__ GScratch s;
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
+  unsigned long long none, all;
+  part_prefix(G.part[2], 0, s, &none, &all);
   for (uint32_t i = threadIdx.x; i <= (uint32_t)kMaxLevels; i += kGT) G.nb[i] = 0;
   for (uint32_t i = threadIdx.x; i < (uint32_t)kHistBins; i += kGT) G.hist[i] = 0;
   if (threadIdx.x != 0) return;
@@ -957,7 +1017,6 @@ __global__ void __launch_bounds__(kGT) k_g_end(const LaneDesc* __restrict__ lane
     return;
   }
   const uint32_t n = G.n_keep;
-  const unsigned long long all = G.part[2][kGB];
   const uint64_t nE = (uint32_t)all, nX = all >> 32;
   const uint64_t end = G.link_base + nE + nX;
   G.raw_total += nE + nX;
@@ -991,6 +1050,8 @@ __global__ void __launch_bounds__(kGT) k_g_end(const LaneDesc* __restrict__ lane
   G.n_touched = 0;
   G.n_surv = 0;
   G.xmask = 0;
+  G.best_key = 0xffffffffu;  // the next frame's expansion takes the minimum
+  G.disp = 0;
   G.frames = (uint32_t)t + 1u;
   if (t == L.T && !L.open) G.stop = 1;
 }
@@ -1512,27 +1573,26 @@ wd_status grid_frames(GridRun* run, const DevGraph& g, const LaneDesc* lanes, vo
     const int reuse = t / kPruneEvery - 2;
     if (run->q && t % kPruneEvery == 0 && reuse >= 0 && reuse < run->nwin)
       e = hipStreamWaitEvent(st, run->done[reuse % 4], 0);
-    hipLaunchKernelGGL(k_g_begin, one, dim3(64), 0, st, g, lanes, gl, prm, t);
-    if (prm.flags & WD_FLAG_DYNAMIC_LB) hipLaunchKernelGGL(k_g_expand_dyn, all, blk, 0, st, g, lanes, gl, t);
-    else hipLaunchKernelGGL(k_g_expand, all, blk, 0, st, g, lanes, gl, t);
-    hipLaunchKernelGGL(k_g_cut, one, dim3(64), 0, st, gl, prm);
-    for (uint32_t l = 0; l < g.nlevels; ++l) hipLaunchKernelGGL(k_g_level, all, blk, 0, st, g, lanes, gl, l);
-    hipLaunchKernelGGL(k_g_check, one, dim3(64), 0, st, lanes, gl);
+    // per frame: expansion (with the frame's start), epsilon levels,
+    // survivors (with the cutoff and capacity checks), [max-active select],
+    // kept-state counts, compaction, degrees, link counts, links, end
+    if (t == 0) hipLaunchKernelGGL(k_g_begin, one, dim3(64), 0, st, g, lanes, gl);
+    if (prm.flags & WD_FLAG_DYNAMIC_LB) hipLaunchKernelGGL(k_g_expand_dyn, all, blk, 0, st, g, lanes, gl, prm, t);
+    else hipLaunchKernelGGL(k_g_expand, all, blk, 0, st, g, lanes, gl, prm, t);
+    for (uint32_t l = 0; l < g.nlevels; ++l) hipLaunchKernelGGL(k_g_level, all, blk, 0, st, g, lanes, gl, prm, l);
     hipLaunchKernelGGL(k_g_count, all, blk, 0, st, lanes, gl, prm);
-    hipLaunchKernelGGL(k_g_select, one, blk, 0, st, gl, prm, 0);
-    if (prm.max_active > 0)
+    if (prm.max_active > 0) {
+      hipLaunchKernelGGL(k_g_select, one, blk, 0, st, gl, prm, 0);
       for (int step = 1; step < 3; ++step) {
         hipLaunchKernelGGL(k_g_select_hist, all, blk, 0, st, lanes, gl);
         hipLaunchKernelGGL(k_g_select, one, blk, 0, st, gl, prm, step);
       }
-    if (prm.max_active > 0) hipLaunchKernelGGL(k_g_mark, all, blk, 0, st, lanes, gl);
-    hipLaunchKernelGGL(k_g_bits, all, blk, 0, st, g, lanes, gl);
-    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 0, 0);
+      hipLaunchKernelGGL(k_g_mark, all, blk, 0, st, lanes, gl);
+    }
+    hipLaunchKernelGGL(k_g_bits, all, blk, 0, st, g, lanes, gl, prm);
     hipLaunchKernelGGL(k_g_compact, all, blk, 0, st, g, lanes, gl, prm);
-    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 1, 0);
     hipLaunchKernelGGL(k_g_degrees, all, blk, 0, st, g, lanes, gl);
     hipLaunchKernelGGL(k_g_link_count, all, blk, 0, st, g, lanes, gl, t);
-    hipLaunchKernelGGL(k_g_scan, one, blk, 0, st, lanes, gl, 2, 0);
     hipLaunchKernelGGL(k_g_link_write, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_g_end, one, blk, 0, st, lanes, gl, t);
     if (run->q && (t + 1) % kPruneEvery == 0) {
