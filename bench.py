@@ -500,6 +500,8 @@ def main() -> int:
     ap.add_argument("--workload", default=WORKLOAD,
                     help="workload timed (the headline line is hclg_5m; others are for profiling)")
     ap.add_argument("--mode", default="auto", help="execution mode of the timed decodes (for profiling)")
+    ap.add_argument("--frames", type=int, default=0,
+                    help="decode only the first N frames of --workload (for profiling runs)")
     ap.add_argument("--phases", action="store_true",
                     help="only print the step profile of the one-workgroup forward pass on --workload")
     args = ap.parse_args()
@@ -525,6 +527,8 @@ def main() -> int:
     cfg = synth.workload(workload)
     g = synth.make_graph(cfg)
     L = synth.make_loglikes(cfg)
+    if args.frames:
+        L = np.ascontiguousarray(L[:args.frames])
     dev = torch.device("cuda:0")
     graph = wfstdec.Graph(g, cfg["P"], "cuda:0")
     x = torch.from_numpy(L).to(dev)

@@ -99,16 +99,17 @@ typedef struct {
 /* Chip-wide mode prunes the lattice conservatively while decoding, on a
  * second stream of the library's own (Fig. 1 of the paper prunes on a second
  * stream as decoding goes): frames are recorded in windows of 32 into two raw
- * window slots taken in turn; once a window is complete, its links are swept
- * with the lowest possible extra cost (0) on its last frame's tokens, and the
- * links that cannot be kept by the final pruning are dropped while the rest
- * are appended to the compacted region of the link store.  Decoding goes on
- * meanwhile and only waits for a window's pruning before it reuses that
- * window's slot.  The link store then holds the compacted region (capacity
- * `links`) plus the two slots (`window_links` each) instead of every raw
- * link.  The result is identical.  This flag turns it off (A/B).  Never done
- * with WD_FLAG_DEBUG, which returns the raw lattice.  Decodes on one device
- * share the library's pruning stream and are ordered on it by events. */
+ * window slots taken in turn; 8 frames after a window's last frame, its links
+ * (and those of the 8 frames after it) are swept with the lowest possible
+ * extra cost (0) on the 8th frame's tokens, and the window's links that cannot
+ * be kept by the final pruning are dropped while the rest are appended to the
+ * compacted region of the link store.  Decoding goes on meanwhile and only
+ * waits for a window's pruning before it reuses that window's slot.  The link
+ * store then holds the compacted region (capacity `links`) plus the two slots
+ * (`window_links` each) instead of every raw link.  The result is identical.
+ * This flag turns it off (A/B).  Never done with WD_FLAG_DEBUG, which returns
+ * the raw lattice.  Decodes on one device share the library's pruning stream
+ * and are ordered on it by events. */
 #define WD_FLAG_NO_INCREMENTAL_PRUNE 32u
 /* Step profile of the one-workgroup forward pass (a measurement aid, off in
  * timed runs; WD_EINVAL in chip-wide mode): a separately compiled copy of the

@@ -122,7 +122,7 @@ Regions carve(const wd_graph* g, int B, int32_t max_T, const Caps& c, char* base
   char* n_state = take(4 * c.nodes);
   char* n_pack = take(8 * c.nodes);
   char* n_pred = take(4 * c.nodes);
-  const uint64_t nlink = c.links + 2 * c.win;
+  const uint64_t nlink = c.links + grid_window_slots() * c.win;  // compacted region + raw window slots
   char* links = take(16 * nlink);
   char* link_lvl = take(nlink);
   char* node_off = take(8 * T2);

@@ -197,8 +197,8 @@ struct LaneDesc {
   WD_GLOBAL uint32_t* n_state;           // [node_cap]
   WD_GLOBAL unsigned long long* n_pack;  // [node_cap] (cost key, predecessor arc)
   WD_GLOBAL uint32_t* n_pred;            // [node_cap] predecessor node
-  // link store [link_cap + 2*win_cap]: with incremental pruning, the compacted
-  // region [0, link_cap) then two raw window slots of win_cap links each
+  // link store [link_cap + 3*win_cap]: with incremental pruning, the compacted
+  // region [0, link_cap) then three raw window slots of win_cap links each
   WD_GLOBAL uint4* links;                // {arc, src node, dst node, x bits}
   WD_GLOBAL uint8_t* link_lvl;           // epsilon level of the source (epsilon links)
   WD_GLOBAL uint64_t* node_off;          // [T+2]
@@ -211,7 +211,7 @@ struct LaneDesc {
   WD_GLOBAL float* cut;                  // [T+1]
   // lattice pass
   WD_GLOBAL uint32_t* extra_key;         // [node_cap]
-  WD_GLOBAL uint32_t* le_key;            // [link_cap + 2*win_cap]
+  WD_GLOBAL uint32_t* le_key;            // [link_cap + 3*win_cap]
   WD_GLOBAL double* alpha;               // [node_cap]
   WD_GLOBAL double* beta;                // [node_cap]
   WD_GLOBAL uint32_t* used;              // [ceil(node_cap/32)+1] lattice-node bitmap

@@ -27,9 +27,14 @@ constexpr int kGW = kGT / 64;     // wavefronts per workgroup
 constexpr uint32_t kGB = 1024;    // workgroups per utterance
 constexpr uint32_t kSeg = 4096;   // frontier prefix sums a workgroup keeps in LDS
 
-// Incremental pruning runs in windows of this many frames; its sweep kernels
-// use a quarter of the workgroups, leaving room for the decoding kernels.
+// Incremental pruning runs in windows of this many frames, recorded in
+// kSlots raw slots in turn; its sweep kernels use a quarter of the
+// workgroups, leaving room for the decoding kernels.
 constexpr int kPruneEvery = 32;
+// A window is pruned kLookahead frames after its last frame (the sweep runs
+// back from there), in one of kSlots raw slots.
+constexpr int kLookahead = 8;
+constexpr uint32_t kSlots = kLookahead < kPruneEvery ? 2u : 3u;
 constexpr uint32_t kPB = kGB / 4;
 
 // Incremental pruning state of one utterance, written only by the kernels on
@@ -1038,8 +1043,8 @@ __global__ void __launch_bounds__(kGT) k_g_end(const LaneDesc* __restrict__ lane
   G.tokens += n;
   G.max_tokens = n > G.max_tokens ? n : G.max_tokens;
   G.link_base = end;
-  if (L.win_cap && (t + 1) % kPruneEvery == 0) {  // next window: the other slot
-    G.slot_lo = L.link_cap + (((uint32_t)(t + 1) / kPruneEvery) & 1u) * L.win_cap;
+  if (L.win_cap && (t + 1) % kPruneEvery == 0) {  // next window: the next slot
+    G.slot_lo = L.link_cap + (((uint32_t)(t + 1) / kPruneEvery) % kSlots) * L.win_cap;
     G.slot_hi = G.slot_lo + L.win_cap;
     G.link_base = G.slot_lo;
   }
@@ -1324,23 +1329,23 @@ __global__ void __launch_bounds__(kGT) k_gn_write(const LaneDesc* __restrict__ l
 // ------------------------------------------------------ incremental pruning
 //
 // Frames are recorded in windows of kPruneEvery frames, window j in raw slot
-// j mod 2 of the link store.  Once frame t, the last of window [t0, t], is
-// done, the pruning stream sweeps the window while decoding goes on: the
-// nodes of frame t get extra cost 0, the lowest an extra cost can be, and the
-// sweep of Sec. 3.5 over the window then gives every node and link of the
-// window a lower bound of its final extra cost (the recursion is monotone in
-// the frame-t values).  A link whose bound is above the lattice beam (or
-// +inf: it leads nowhere) cannot be kept by the final pruning, and nothing it
-// could decide survives either: a node's final extra cost is the minimum over
-// its out-links, reached by a link within the beam whenever it matters.  The
-// other links are appended, in order, to the compacted region [0, link_cap),
-// and the window's frame offsets move with them.  Decoding waits for window
-// j's pruning only before frame 32 (j + 2) reuses its slot.  At the end, the
-// frames after the last complete window are gathered behind the compacted
-// region, which then holds every frame in order, as the link store does
-// without incremental pruning.  (A window that ends on the last frame is
-// pruned too: the bound holds whether or not frames follow, so a stream can
-// prune each window as soon as it is complete.)
+// j mod kSlots of the link store.  Window j = [t0, t1] is pruned once frame
+// tb = t1 + kLookahead is done too, by the pruning stream while decoding goes
+// on: the nodes of frame tb get extra cost 0, the lowest an extra cost can
+// be, and the sweep of Sec. 3.5 back from tb over window j then gives every
+// node and link of window j a lower bound of its final extra cost (the
+// recursion is monotone in the frame-tb values), one that already knows which
+// paths die or fall behind within the kLookahead frames after the window.  A
+// link of window j whose bound is above the lattice beam (or +inf: it leads
+// nowhere) cannot be kept by the final pruning, and nothing it could decide
+// survives either: a node's final extra cost is the minimum over its
+// out-links, reached by a link within the beam whenever it matters.  Window
+// j's other links are appended, in order, to the compacted region
+// [0, link_cap), and its frame offsets move with them.  Decoding waits for
+// window j's pruning only before window j + kSlots reuses its slot.  At the
+// end, the frames after the last pruned window (at most two windows, the last
+// of them partial) are gathered behind the compacted region, which then holds
+// every frame in order, as the link store does without incremental pruning.
 //
 // Decoding and pruning touch disjoint data while they overlap: the window's
 // links, link offsets, extra costs and le_key belong to the pruning stream;
@@ -1445,46 +1450,56 @@ __global__ void __launch_bounds__(kGT) k_gp_fix(const LaneDesc* __restrict__ lan
   }
 }
 
-// The frames after the last pruned window (t0 .. T, all in one slot; none
-// when the last window ended at T), behind the compacted region.  On the
-// decoding stream, after it has waited for the pruning stream.
-__device__ __forceinline__ bool gather_range(const LaneDesc& L, const GridLane& G, int* t0, uint64_t* src,
-                                             uint64_t* n) {
+// The frames after the last pruned window (t0 .. T; none when it ended at
+// T), behind the compacted region: frames t0 .. a1 of t0's window, then
+// a1 + 1 .. T of the next one (empty when T ends t0's window), each
+// contiguous in its slot.  On the decoding stream, after it has waited for
+// the pruning stream.
+struct Gather {
+  int t0, a1;
+  uint64_t srcA, nA, srcB, nB;
+};
+
+__device__ __forceinline__ bool gather_range(const LaneDesc& L, const GridLane& G, Gather* r) {
   if (!L.win_cap || G.status != 0 || !G.hist_ok) return false;
-  *t0 = (int)G.pr.next;
-  *src = *t0 <= L.T ? L.link_off[*t0] : 0;
-  *n = *t0 <= L.T ? L.link_end[L.T] - *src : 0;
+  const int t0 = (int)G.pr.next, T = L.T;
+  r->t0 = t0;
+  r->a1 = t0 + kPruneEvery - 1 < T ? t0 + kPruneEvery - 1 : T;
+  r->srcA = t0 <= T ? L.link_off[t0] : 0;
+  r->nA = t0 <= T ? L.link_end[r->a1] - r->srcA : 0;
+  r->srcB = r->a1 < T ? L.link_off[r->a1 + 1] : 0;
+  r->nB = r->a1 < T ? L.link_end[T] - r->srcB : 0;
   return true;
 }
 
 __global__ void __launch_bounds__(kGT) k_gp_gather(const LaneDesc* __restrict__ lanes, const GridLane* gl) {
   const LaneDesc& L = lanes[blockIdx.y];
   const GridLane& G = gl[blockIdx.y];
-  int t0;
-  uint64_t src, n;
-  if (!gather_range(L, G, &t0, &src, &n)) return;
-  const uint64_t k0 = G.pr.kend;
+  Gather r;
+  if (!gather_range(L, G, &r)) return;
+  const uint64_t k0 = G.pr.kend, n = r.nA + r.nB;
   if (G.pr.ovf || k0 + n > L.link_cap) return;
   for (uint64_t i = (uint64_t)blockIdx.x * kGT + threadIdx.x; i < n; i += (uint64_t)kGB * kGT) {
-    L.links[k0 + i] = L.links[src + i];
-    L.link_lvl[k0 + i] = L.link_lvl[src + i];
+    const uint64_t src = i < r.nA ? r.srcA + i : r.srcB + (i - r.nA);
+    L.links[k0 + i] = L.links[src];
+    L.link_lvl[k0 + i] = L.link_lvl[src];
   }
 }
 
 __global__ void __launch_bounds__(kGT) k_gp_gather_fix(const LaneDesc* __restrict__ lanes, GridLane* gl) {
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
-  int t0;
-  uint64_t src, n;
-  if (!gather_range(L, G, &t0, &src, &n)) return;
-  const uint64_t k0 = G.pr.kend;
+  Gather r;
+  if (!gather_range(L, G, &r)) return;
+  const uint64_t k0 = G.pr.kend, n = r.nA + r.nB;
   const bool fits = !G.pr.ovf && k0 + n <= L.link_cap;
-  __syncthreads();  // every thread has read link_off[t0] before it moves
+  __syncthreads();  // every thread has read the offsets before they move
   if (fits)
-    for (int f = t0 + (int)threadIdx.x; f <= L.T; f += kGT) {
-      L.link_off[f] = L.link_off[f] - src + k0;
-      L.link_xoff[f] = L.link_xoff[f] - src + k0;
-      L.link_end[f] = L.link_end[f] - src + k0;
+    for (int f = r.t0 + (int)threadIdx.x; f <= L.T; f += kGT) {
+      const uint64_t dst = f <= r.a1 ? k0 - r.srcA : k0 + r.nA - r.srcB;  // (mod 2^64)
+      L.link_off[f] = L.link_off[f] + dst;
+      L.link_xoff[f] = L.link_xoff[f] + dst;
+      L.link_end[f] = L.link_end[f] + dst;
     }
   if (threadIdx.x == 0) {
     if (fits) L.link_off[L.T + 1] = k0 + n;
@@ -1496,6 +1511,8 @@ __global__ void __launch_bounds__(kGT) k_gp_gather_fix(const LaneDesc* __restric
 // -------------------------------------------------------------------- launches
 
 size_t grid_lane_bytes() { return sizeof(GridLane); }
+
+uint32_t grid_window_slots() { return kSlots; }
 
 // Decoding-state update for a stream's utterances: a workgroup per lane.
 __global__ void k_g_bad(const LaneDesc* __restrict__ lanes, GridLane* gl, const uint32_t* __restrict__ bad) {
@@ -1558,10 +1575,11 @@ wd_status grid_begin(GridRun* run, const LaneDesc* lanes, void* glv, int B, bool
   return WD_OK;
 }
 
-// Frames t_from..t_to.  Window j's links go to slot j % 2: the first frame of
-// window j waits for the pruning of window j - 2; after the last frame of a
-// window, an event hands it to the pruning stream (ready[j % 4] / done[j % 4];
-// every wait is enqueued before its event is recorded again).
+// Frames t_from..t_to.  Window u's links go to slot u % kSlots: the first
+// frame of window u waits for the pruning of window u - kSlots; kLookahead
+// frames after the last frame of window j, an event hands window j to the
+// pruning stream (ready[j % 4] / done[j % 4]; every wait is enqueued before
+// its event is recorded again).
 wd_status grid_frames(GridRun* run, const DevGraph& g, const LaneDesc* lanes, void* glv, int B, const Params& prm,
                       const uint32_t* bad, int t_from, int t_to, hipStream_t st) {
   GridLane* gl = (GridLane*)glv;
@@ -1570,7 +1588,7 @@ wd_status grid_frames(GridRun* run, const DevGraph& g, const LaneDesc* lanes, vo
   hipError_t e = hipSuccess;
   hipLaunchKernelGGL(k_g_bad, one, dim3(64), 0, st, lanes, gl, bad);
   for (int t = t_from; t <= t_to && e == hipSuccess; ++t) {
-    const int reuse = t / kPruneEvery - 2;
+    const int reuse = t / kPruneEvery - (int)kSlots;
     if (run->q && t % kPruneEvery == 0 && reuse >= 0 && reuse < run->nwin)
       e = hipStreamWaitEvent(st, run->done[reuse % 4], 0);
     // per frame: expansion (with the frame's start), epsilon levels,
@@ -1595,8 +1613,9 @@ wd_status grid_frames(GridRun* run, const DevGraph& g, const LaneDesc* lanes, vo
     hipLaunchKernelGGL(k_g_link_count, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_g_link_write, all, blk, 0, st, g, lanes, gl, t);
     hipLaunchKernelGGL(k_g_end, one, blk, 0, st, lanes, gl, t);
-    if (run->q && (t + 1) % kPruneEvery == 0) {
-      const int t0 = t + 1 - kPruneEvery, j = run->nwin++;
+    if (run->q && (t + 1 - kLookahead) % kPruneEvery == 0 && t + 1 - kLookahead >= kPruneEvery) {
+      // window j = [t0, t1] against frame t, kLookahead frames after it
+      const int t1 = t - kLookahead, t0 = t1 + 1 - kPruneEvery, j = run->nwin++;
       hipStream_t q = run->q;
       e = hipEventRecord(run->ready[j % 4], st);
       if (e == hipSuccess) e = hipStreamWaitEvent(q, run->ready[j % 4], 0);
@@ -1612,10 +1631,10 @@ wd_status grid_frames(GridRun* run, const DevGraph& g, const LaneDesc* lanes, vo
           for (int l = (int)g.nlevels - 1; l >= 0; --l)
             hipLaunchKernelGGL(k_gs_relax, part, blk, 0, q, lanes, gl, f, 0, l, 1);
       }
-      hipLaunchKernelGGL(k_gp_count, all, blk, 0, q, lanes, gl, t0, t, lb_key);
+      hipLaunchKernelGGL(k_gp_count, all, blk, 0, q, lanes, gl, t0, t1, lb_key);
       hipLaunchKernelGGL(k_gp_scan, one, blk, 0, q, gl);
-      hipLaunchKernelGGL(k_gp_write, all, blk, 0, q, lanes, gl, t0, t, lb_key);
-      hipLaunchKernelGGL(k_gp_fix, one, blk, 0, q, lanes, gl, t0, t);
+      hipLaunchKernelGGL(k_gp_write, all, blk, 0, q, lanes, gl, t0, t1, lb_key);
+      hipLaunchKernelGGL(k_gp_fix, one, blk, 0, q, lanes, gl, t0, t1);
       e = hipEventRecord(run->done[j % 4], q);
     }
   }

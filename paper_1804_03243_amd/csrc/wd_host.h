@@ -28,6 +28,8 @@ void launch_forward(const DevGraph& g, const LaneDesc* lanes, int B, const Param
                     const uint32_t* bad, hipStream_t s);
 void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s);
 size_t grid_lane_bytes();
+// Raw window slots of the link store with incremental pruning.
+uint32_t grid_window_slots();
 // Chip-wide forward pass in three steps, so that a stream can decode frames as
 // they arrive: begin (per-utterance state; with `prune`, incremental lattice
 // pruning on the library's pruning stream of the current device, ordered

@@ -107,8 +107,8 @@ def test_wide_2m_golden(wf, wide_golden, mode):
     candidate links per frame once it has ramped up, epsilon chains of depth
     8), decoded as a whole utterance without the debug flag, so that in
     chip-wide mode the lattice is pruned in 32-frame windows on the second
-    stream while decoding goes on (six windows, then the final pruning of the
-    rest): words, cost, statistics and every lattice link and node must match
+    stream while decoding goes on (windows 0-5, each 8 frames after its end;
+    the last, partial window is gathered for the final pruning): words, cost, statistics and every lattice link and node must match
     the oracle's stored result bit for bit (per-frame digests written by
     tests/golden/make_wide_2m.py from an oracle run), posteriors within 1e-4."""
     gm, name, cfg, graph, x, meta, post = wide_golden
