@@ -53,8 +53,8 @@ BYTES_LINK = 16
 # runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
 # divided by the counter's reading per byte of a plain device copy of known
 # size (bench.py --copy-kernel-bytes).  Valid while k_forward's sources hash to this.
-TRAFFIC = {"sources_sha256": "0dbdd2e84f5520592fdb7831eb4813d9129c420dbcd927a54044f7fbfbdee11d",
-           "bytes_per_launch": 67227156}
+TRAFFIC = {"sources_sha256": "0fbeeb370488047d5f863d3ffcf9d5c592fd49db338f3c5b92d6d48ac074e88a",
+           "bytes_per_launch": 69284271}
 
 
 FORWARD_SOURCES = ("wd_block.h", "wd_common.h", "wd_forward.hip")  # what k_forward is built from
