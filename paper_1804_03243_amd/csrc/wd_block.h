@@ -199,4 +199,15 @@ __device__ __forceinline__ uint32_t search_le(const uint32_t* a, uint32_t n, uin
 
 __device__ __forceinline__ float canon(float x) { return x == 0.0f ? 0.0f : x; }
 
+// Number of entries of the sorted a[0..n) below w.
+__device__ __forceinline__ uint64_t lower_bound64(const uint64_t* a, uint64_t n, uint64_t w) {
+  uint64_t lo = 0, hi = n;
+  while (lo < hi) {
+    uint64_t mid = (lo + hi) >> 1;
+    if (a[mid] < w) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
 }  // namespace wd

@@ -1255,6 +1255,16 @@ __global__ void __launch_bounds__(kGT) k_gs_fill_ab(const LaneDesc* __restrict__
     L.alpha[i] = INFINITY;
     L.beta[i] = INFINITY;
   }
+  // per frame t: kept links start at kframe[2t], kept epsilon links at
+  // kframe[2t+1] (the posterior passes' frame offsets); only when the list
+  // was written
+  const uint64_t nk = L.info->kept;
+  if (nk > L.kept_cap) return;
+  const int T = L.T;
+  for (int t = (int)(blockIdx.x * kGT + threadIdx.x); t <= T + 1; t += kGB * kGT) {
+    L.kframe[2 * t] = lower_bound64(L.kept_idx, nk, L.link_off[t]);
+    L.kframe[2 * t + 1] = t <= T ? lower_bound64(L.kept_idx, nk, L.link_xoff[t]) : nk;
+  }
 }
 
 // The lattice node list: nodes marked in the used bitmap, in node id order,

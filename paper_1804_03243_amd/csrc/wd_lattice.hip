@@ -47,16 +47,6 @@ __device__ __forceinline__ uint64_t search_le64(const uint64_t* a, uint64_t n, u
   return lo;
 }
 
-// Number of entries of the sorted a[0..n) below w.
-__device__ __forceinline__ uint64_t lower_bound64(const uint64_t* a, uint64_t n, uint64_t w) {
-  uint64_t lo = 0, hi = n;
-  while (lo < hi) {
-    uint64_t mid = (lo + hi) >> 1;
-    if (a[mid] < w) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
 
 // -log(exp(-a) + exp(-b)) accumulated atomically into *p (fp64).
 __device__ __forceinline__ void atomic_logadd(double* p, double v) {
@@ -76,6 +66,18 @@ __device__ __forceinline__ void atomic_logadd(double* p, double v) {
 
 __device__ __forceinline__ float node_cost(const LaneDesc& L, uint64_t n) {
   return key_cost((uint32_t)(L.n_pack[n] >> 32));
+}
+
+// Node id of the start token: the start state among frame 0's tokens (sorted
+// by state).
+__device__ __forceinline__ uint64_t start_node_of(const LaneDesc& L, const DevGraph& g) {
+  uint64_t lo = 0, hi = L.node_off[1];
+  while (lo < hi) {
+    const uint64_t mid = (lo + hi) >> 1;
+    if (L.n_state[mid] < g.start) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
 }
 
 struct LinkView {
@@ -161,17 +163,29 @@ __device__ __forceinline__ uint64_t write_nodes(const LaneDesc& L, uint64_t nnod
   const uint64_t per = (nwd + kLT - 1) / kLT;
   const uint64_t w0 = tid * per < nwd ? tid * per : nwd;
   const uint64_t w1 = w0 + per < nwd ? w0 + per : nwd;
+  constexpr int kBatchW = 8;  // bitmap words read together
   uint64_t cnt = 0, n_out;
-  for (uint64_t w = w0; w < w1; ++w) cnt += (uint64_t)__popc(L.used[w]);
+  for (uint64_t wb = w0; wb < w1; wb += kBatchW) {
+    uint32_t v[kBatchW];
+#pragma unroll
+    for (int u = 0; u < kBatchW; ++u) v[u] = wb + u < w1 ? L.used[wb + u] : 0u;
+#pragma unroll
+    for (int u = 0; u < kBatchW; ++u) cnt += (uint64_t)__popc(v[u]);
+  }
   uint64_t pos = block_excl_scan64<kLW>(cnt, bs, par, &n_out);
-  for (uint64_t w = w0; w < w1; ++w) {
+  // the frame of the thread's first node by a search, then walked forward
+  // (node ids ascend in the thread's range)
+  int t = -1;
+  for (uint64_t w = w0; w < w1 && cnt; ++w) {
     uint32_t word = L.used[w];
     while (word) {
       const uint32_t b = (uint32_t)__ffs(word) - 1u;
       word &= word - 1u;
       const uint64_t n = (w << 5) | b;
+      if (t < 0) t = (int)search_le64(L.node_off, (uint64_t)L.T + 2, n);
+      while (L.node_off[t + 1] <= n) ++t;
       OutNode o;
-      o.t = (int32_t)search_le64(L.node_off, (uint64_t)L.T + 2, n);
+      o.t = (int32_t)t;
       o.state = (int32_t)L.n_state[n];
       o.cost = node_cost(L, n);
       o.extra = key_cost(L.extra_key[n]);
@@ -778,6 +792,17 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
     info->tb_fail = ok ? 0u : 1u;
     return;
   }
+  if (blockIdx.y == 2) {
+    // chip-wide mode (links swept, kept links and their frame offsets listed
+    // by the chip-wide kernels), wide lattice: beta here while workgroup 0
+    // computes alpha; Z from it
+    const uint64_t nk = info->kept;
+    if (!swept || nk <= 64 * ((uint64_t)T + 1) || nk > L.kept_cap) return;
+    beta_wave<kLT>(L, g, sh, tid, swept, final_used);
+    __syncthreads();
+    if (tid == 0) info->Z = L.beta[start_node_of(L, g)];
+    return;
+  }
 
   // ------------------------------------------------ backward extra-cost sweep
   if (!swept) sweep_block(L, g, sh, tid, final_used, best_total);
@@ -787,15 +812,30 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   const uint32_t lb_key = cost_key(prm.lattice_beam);
   uint64_t n_kept = info->kept;  // counted and listed by the chip-wide kernels when swept
   if (!swept) {
+    // a contiguous range of links per thread, read kBatchK at a time so that
+    // the loads of a batch are in flight together
+    constexpr int kBatchK = 8;
     const uint64_t per = (nlinks + kLT - 1) / kLT;
     const uint64_t k0 = tid * per < nlinks ? tid * per : nlinks;
     const uint64_t k1 = k0 + per < nlinks ? k0 + per : nlinks;
     uint64_t cnt = 0;
-    for (uint64_t k = k0; k < k1; ++k) cnt += kept(L, k, lb_key);
+    for (uint64_t kb = k0; kb < k1; kb += kBatchK) {
+      uint32_t le[kBatchK];
+#pragma unroll
+      for (int u = 0; u < kBatchK; ++u) le[u] = kb + u < k1 ? L.le_key[kb + u] : kInfKey;
+#pragma unroll
+      for (int u = 0; u < kBatchK; ++u) cnt += le[u] <= lb_key && le[u] < kInfKey;
+    }
     uint64_t pos = block_excl_scan64<kLW>(cnt, sh.bs, par, &n_kept);
-    if (n_kept <= L.kept_cap)
-      for (uint64_t k = k0; k < k1; ++k)
-        if (kept(L, k, lb_key)) L.kept_idx[pos++] = k;
+    if (n_kept <= L.kept_cap && cnt)
+      for (uint64_t kb = k0; kb < k1; kb += kBatchK) {
+        uint32_t le[kBatchK];
+#pragma unroll
+        for (int u = 0; u < kBatchK; ++u) le[u] = kb + u < k1 ? L.le_key[kb + u] : kInfKey;
+#pragma unroll
+        for (int u = 0; u < kBatchK; ++u)
+          if (le[u] <= lb_key && le[u] < kInfKey) L.kept_idx[pos++] = kb + u;
+      }
   }
   const bool debug = (prm.flags & 1u) != 0;
   if (n_kept > L.kept_cap || (debug && nlinks > L.raw_cap)) {
@@ -811,11 +851,13 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   // per frame t: kept links start at kf[2t], kept epsilon links at kf[2t+1];
   // frame t ends where frame t+1 starts
   uint64_t* kf = L.kframe;
-  for (int t = (int)tid; t <= T + 1; t += kLT) {
-    kf[2 * t] = lower_bound64(kid, n_kept, L.link_off[t]);
-    kf[2 * t + 1] = t <= T ? lower_bound64(kid, n_kept, L.link_xoff[t]) : n_kept;
+  if (!swept) {  // (chip-wide mode lists them beside the kept links)
+    for (int t = (int)tid; t <= T + 1; t += kLT) {
+      kf[2 * t] = lower_bound64(kid, n_kept, L.link_off[t]);
+      kf[2 * t + 1] = t <= T ? lower_bound64(kid, n_kept, L.link_xoff[t]) : n_kept;
+    }
+    __syncthreads();
   }
-  __syncthreads();
   if (!swept) {
     // records of the kept links for forward-backward (chip-wide mode writes
     // them while listing the kept links): a thread takes a contiguous range,
@@ -840,30 +882,26 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   }
 
   // ----------------------------------------------------- posteriors (fp64)
-  uint64_t start_node = 0;
-  {
-    // the start state among frame 0's tokens (sorted by state)
-    uint64_t lo = 0, hi = L.node_off[1];
-    while (lo < hi) {
-      const uint64_t mid = (lo + hi) >> 1;
-      if (L.n_state[mid] < g.start) lo = mid + 1;
-      else hi = mid;
-    }
-    start_node = lo;
-  }
+  const uint64_t start_node = start_node_of(L, g);
+  const bool wide = n_kept > 64 * ((uint64_t)T + 1);  // (more than 64 kept links per frame)
   // small kept lattices: alpha on wavefront 0 and beta on wavefront 1,
   // concurrently; large ones (more than 64 kept links per frame on average):
-  // the whole workgroup, alpha then beta
-  if (n_kept <= 64 * ((uint64_t)T + 1)) {
+  // the whole workgroup, alpha then beta, or in chip-wide mode alpha here and
+  // beta on the utterance's third workgroup at the same time
+  if (!wide) {
     if (tid < 64) alpha_wave<64>(L, g, sh, tid, swept, start_node);
     else if (tid < 128) beta_wave<64>(L, g, sh, tid - 64, swept, final_used);
   } else {
     alpha_wave<kLT>(L, g, sh, tid, swept, start_node);
-    __syncthreads();
-    beta_wave<kLT>(L, g, sh, tid, swept, final_used);
+    if (!swept) {
+      __syncthreads();
+      beta_wave<kLT>(L, g, sh, tid, swept, final_used);
+    }
   }
   __syncthreads();
-  const double Z = L.beta[start_node];
+  // (with a wide lattice in chip-wide mode, the third workgroup writes Z;
+  // the merge runs as a chip-wide kernel after this one)
+  const double Z = swept ? 0.0 : L.beta[start_node];
   if (tid == 0) {
     info->final_used = final_used ? 1 : 0;
     info->kept = n_kept;
@@ -871,7 +909,7 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
     info->start_node = (uint32_t)start_node;
     info->best_node = (uint32_t)bnode;
     info->best_cost = best_total;
-    info->Z = Z;
+    if (!(swept && wide)) info->Z = L.beta[start_node];
   }
   // used-node bitmap is zero on entry (cleared by the host before the launch)
   if (tid == 0) atomicOr(&L.used[start_node >> 5], 1u << (start_node & 31u));
@@ -900,7 +938,7 @@ __global__ void __launch_bounds__(256) k_lat_assemble(DevGraph g, const LaneDesc
 }
 
 void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s) {
-  hipLaunchKernelGGL(k_lattice, dim3(B, 2), dim3(kLT), 0, s, g, lanes, prm);
+  hipLaunchKernelGGL(k_lattice, dim3(B, (prm.flags & kFlagSwept) ? 3 : 2), dim3(kLT), 0, s, g, lanes, prm);
   if (prm.flags & kFlagSwept) {
     hipLaunchKernelGGL(k_lat_assemble, dim3(1024, B), dim3(256), 0, s, g, lanes, prm);
   }
