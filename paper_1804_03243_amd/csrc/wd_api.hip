@@ -389,6 +389,41 @@ static const char* status_message(wd_status st) {
 }
 
 // Lattice pass, then the results of every utterance (synchronises).
+// Pinned host memory for result downloads, one buffer per device, grown on
+// demand and kept until the process ends.  Its mutex is held from the copy
+// until the results are unpacked (decodes on one device take turns there).
+struct PinnedBuffer {
+  std::mutex mu;
+  char* p = nullptr;
+  uint64_t cap = 0;
+};
+
+// Locks the current device's buffer (holding at least `bytes`) and returns it
+// locked in *out.
+static wd_status pinned_of_current_device(uint64_t bytes, PinnedBuffer** out) {
+  static PinnedBuffer bufs[64];
+  int dev = 0;
+  wd_status st = hip_check(hipGetDevice(&dev), "device");
+  if (st != WD_OK) return st;
+  if (dev < 0 || dev >= 64) return fail(WD_EINVAL, "pinned buffer: device index out of range");
+  PinnedBuffer& b = bufs[dev];
+  b.mu.lock();
+  if (b.cap < bytes) {
+    if (b.p) (void)hipHostFree(b.p);
+    b.p = nullptr;
+    b.cap = 0;
+    const uint64_t want = std::max<uint64_t>(bytes + bytes / 4, 1ull << 20);
+    if ((st = hip_check(hipHostMalloc((void**)&b.p, want, hipHostMallocDefault), "pinned buffer"))) {
+      b.p = nullptr;
+      b.mu.unlock();
+      return st;
+    }
+    b.cap = want;
+  }
+  *out = &b;
+  return WD_OK;
+}
+
 static wd_status run_finish(wd_stream* run, wd_result** out) {
   const Regions& R = run->R;
   hipStream_t s = run->s;
@@ -432,12 +467,16 @@ static wd_status run_finish(wd_stream* run, wd_result** out) {
     poff[b + 1] = poff[b] + n;
   }
   const bool packed = !debug && poff[B] > 0 && poff[B] <= (uint64_t)B * run->c.arcs * 16;
-  std::vector<char> pack;
+  // the packed results land in the device's pinned download buffer (a DMA
+  // straight into it; pageable memory would be copied through staging)
+  PinnedBuffer* pin = nullptr;
+  std::unique_lock<std::mutex> pin_lock;
   if (packed) {
-    pack.resize(poff[B]);
+    if ((st = pinned_of_current_device(poff[B], &pin))) return st;
+    pin_lock = std::unique_lock<std::mutex>(pin->mu, std::adopt_lock);
     launch_pack_results(R.desc, B, run->lanes[0].cand, s);
     if ((st = hip_check(hipGetLastError(), "launch")) ||
-        (st = hip_check(hipMemcpyAsync(pack.data(), run->lanes[0].cand, poff[B], hipMemcpyDeviceToHost, s),
+        (st = hip_check(hipMemcpyAsync(pin->p, run->lanes[0].cand, poff[B], hipMemcpyDeviceToHost, s),
                         "result download")) ||
         (st = hip_check(hipStreamSynchronize(s), "result download")))
       return st;
@@ -503,7 +542,7 @@ static wd_status run_finish(wd_stream* run, wd_result** out) {
     for (int b = 0; b < B; ++b) {
       wd_result* r = out[b];
       if (!r || r->status != WD_OK) continue;
-      const char* src = pack.data() + poff[b];
+      const char* src = pin->p + poff[b];
       std::memcpy(r->links.data(), src, sizeof(OutLink) * r->links.size());
       src += sizeof(OutLink) * r->links.size();
       std::memcpy(r->nodes.data(), src, sizeof(OutNode) * r->nodes.size());

@@ -328,8 +328,11 @@ def _copy(ptr, n, dtype):
     return out
 
 
-def wd_result_read(r: int) -> SimpleNamespace:
-    """Copy everything out of a result handle (wd_result_* accessors)."""
+def wd_result_read(r: int, debug: bool = True, phases: bool = True) -> SimpleNamespace:
+    """Copy everything out of a result handle (wd_result_* accessors).
+    `debug` / `phases` false: the outputs only WD_FLAG_DEBUG / WD_FLAG_PHASES
+    produce (tokens, raw lattice, cutoffs / step profile) are left empty
+    without asking the library for them."""
     L = lib()
     out = SimpleNamespace()
     out.status = L.wd_result_status(r)
@@ -342,17 +345,26 @@ def wd_result_read(r: int) -> SimpleNamespace:
     out.words = get(L.wd_result_words, np.dtype("<i4"))
     out.links = get(L.wd_result_lattice, LINK_DTYPE)
     out.nodes = get(L.wd_result_nodes, NODE_DTYPE)
-    out.tokens = get(L.wd_result_tokens, TOKEN_DTYPE)
-    out.raw_links = get(L.wd_result_raw_lattice, LINK_DTYPE)
-    b, cb, c = ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_void_p()
-    n = L.wd_result_cutoffs(r, ctypes.byref(b), ctypes.byref(cb), ctypes.byref(c))
     f4 = np.dtype("<f4")
-    out.best, out.cutoff_beam, out.cutoff = (_copy(b.value, n, f4), _copy(cb.value, n, f4),
-                                             _copy(c.value, n, f4))
-    vp, hz = ctypes.c_void_p(), ctypes.c_double()
-    n = L.wd_result_phases(r, ctypes.byref(vp), ctypes.byref(hz))
-    out.phases = _copy(vp.value, n * WD_PHASE_SLOTS, np.dtype("<u8")).reshape(n, WD_PHASE_SLOTS)
-    out.phase_tick_hz = hz.value
+    if debug:
+        out.tokens = get(L.wd_result_tokens, TOKEN_DTYPE)
+        out.raw_links = get(L.wd_result_raw_lattice, LINK_DTYPE)
+        b, cb, c = ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_void_p()
+        n = L.wd_result_cutoffs(r, ctypes.byref(b), ctypes.byref(cb), ctypes.byref(c))
+        out.best, out.cutoff_beam, out.cutoff = (_copy(b.value, n, f4), _copy(cb.value, n, f4),
+                                                 _copy(c.value, n, f4))
+    else:
+        out.tokens = np.zeros(0, TOKEN_DTYPE)
+        out.raw_links = np.zeros(0, LINK_DTYPE)
+        out.best, out.cutoff_beam, out.cutoff = (np.zeros(0, f4), np.zeros(0, f4), np.zeros(0, f4))
+    if phases:
+        vp, hz = ctypes.c_void_p(), ctypes.c_double()
+        n = L.wd_result_phases(r, ctypes.byref(vp), ctypes.byref(hz))
+        out.phases = _copy(vp.value, n * WD_PHASE_SLOTS, np.dtype("<u8")).reshape(n, WD_PHASE_SLOTS)
+        out.phase_tick_hz = hz.value
+    else:
+        out.phases = np.zeros((0, WD_PHASE_SLOTS), np.dtype("<u8"))
+        out.phase_tick_hz = 0.0
     st = wd_stats()
     L.wd_result_stats(r, ctypes.byref(st))
     out.stats = {f: getattr(st, f) for f, _ in wd_stats._fields_ if f != "needed"}
@@ -485,8 +497,9 @@ def decode_batch(graph: Graph, loglikes: list, beam: float, max_active: int, lat
                                       nbytes, _stream(torch))
         outs = []
         err = lib().wd_last_error().decode() if st != WD_OK else ""
+        want_phases = bool(p.flags & WD_FLAG_PHASES)
         for r in res:
-            outs.append(wd_result_read(r) if r else None)
+            outs.append(wd_result_read(r, debug, want_phases) if r else None)
             if r:
                 wd_result_free(r)
         if st == WD_ECAPACITY and attempt < max_retries:
@@ -579,7 +592,7 @@ class Stream:
         self.handle = None
         outs, err = [], lib().wd_last_error().decode() if st != WD_OK else ""
         for r in res:
-            outs.append(wd_result_read(r) if r else None)
+            outs.append(wd_result_read(r, self.debug, False) if r else None)
             if r:
                 wd_result_free(r)
         if st == WD_ECAPACITY:
