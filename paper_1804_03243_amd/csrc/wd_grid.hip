@@ -524,11 +524,14 @@ __global__ void __launch_bounds__(kGT) k_g_level(DevGraph g, const LaneDesc* __r
     uint32_t deg = 0, a0 = 0, k = 0;
     if (i < n) {
       const uint32_t st = bk[i];
-      k = (uint32_t)(L.slot[st] >> 32);
-      if (k <= kcutb) {
-        a0 = g.off[st].y;
-        deg = g.off[st + 1].y - a0;
-      }
+      // the state's epsilon arc range is loaded beside its token, not after
+      // the cutoff test: one round trip instead of two
+      const unsigned long long sv = L.slot[st];
+      const uint32_t x0 = g.off[st].y, x1 = g.off[st + 1].y;
+      k = (uint32_t)(sv >> 32);
+      const bool live = k <= kcutb;  // (selects, so that the loads stay unconditional)
+      a0 = live ? x0 : 0u;
+      deg = live ? x1 - x0 : 0u;
     }
     unsigned long long tot;
     const uint32_t ex = (uint32_t)gexcl64(deg, s, &tot);
