@@ -328,23 +328,53 @@ def _copy(ptr, n, dtype):
     return out
 
 
-def wd_result_read(r: int, debug: bool = True, phases: bool = True) -> SimpleNamespace:
+class _ResultOwner:
+    """Frees a result handle once no array viewing its memory is left."""
+    __slots__ = ("r",)
+
+    def __init__(self, r: int):
+        self.r = r
+
+    def __del__(self):
+        r, self.r = self.r, None
+        if r:
+            try:
+                lib().wd_result_free(r)
+            except Exception:  # (interpreter shutdown)
+                pass
+
+
+def _view(ptr, n, dtype, owner: _ResultOwner):
+    """n records of `dtype` at host address ptr, viewed in place; the view
+    keeps `owner` (and with it the result handle) alive."""
+    n = max(int(n), 0)
+    if n == 0 or not ptr:
+        return np.empty(0, dtype=dtype)
+    buf = (ctypes.c_char * (n * dtype.itemsize)).from_address(ptr)
+    buf._owner = owner
+    return np.frombuffer(buf, dtype=dtype, count=n)
+
+
+def wd_result_read(r: int, debug: bool = True, phases: bool = True,
+                   owner: _ResultOwner | None = None) -> SimpleNamespace:
     """Copy everything out of a result handle (wd_result_* accessors).
     `debug` / `phases` false: the outputs only WD_FLAG_DEBUG / WD_FLAG_PHASES
     produce (tokens, raw lattice, cutoffs / step profile) are left empty
-    without asking the library for them."""
+    without asking the library for them.  With `owner` (which then owns r)
+    the words, lattice and nodes are views of the handle's memory instead of
+    copies, and the handle is freed when the last of them is gone."""
     L = lib()
     out = SimpleNamespace()
     out.status = L.wd_result_status(r)
     out.cost = np.float32(L.wd_result_cost(r))
-    def get(accessor, dtype):
+    def get(accessor, dtype, view=False):
         vp = ctypes.c_void_p()
         n = accessor(r, ctypes.byref(vp))   # sets vp; read it only afterwards
-        return _copy(vp.value, n, dtype)
+        return _view(vp.value, n, dtype, owner) if view and owner is not None else _copy(vp.value, n, dtype)
 
-    out.words = get(L.wd_result_words, np.dtype("<i4"))
-    out.links = get(L.wd_result_lattice, LINK_DTYPE)
-    out.nodes = get(L.wd_result_nodes, NODE_DTYPE)
+    out.words = get(L.wd_result_words, np.dtype("<i4"), True)
+    out.links = get(L.wd_result_lattice, LINK_DTYPE, True)
+    out.nodes = get(L.wd_result_nodes, NODE_DTYPE, True)
     f4 = np.dtype("<f4")
     if debug:
         out.tokens = get(L.wd_result_tokens, TOKEN_DTYPE)
@@ -499,9 +529,8 @@ def decode_batch(graph: Graph, loglikes: list, beam: float, max_active: int, lat
         err = lib().wd_last_error().decode() if st != WD_OK else ""
         want_phases = bool(p.flags & WD_FLAG_PHASES)
         for r in res:
-            outs.append(wd_result_read(r, debug, want_phases) if r else None)
-            if r:
-                wd_result_free(r)
+            # views of the handle's memory, freed with the last of them
+            outs.append(wd_result_read(r, debug, want_phases, _ResultOwner(r)) if r else None)
         if st == WD_ECAPACITY and attempt < max_retries:
             need = {f: max(o.needed[f] for o in outs if o is not None) for f, _ in wd_caps._fields_}
             caps = _grow(used, need)
