@@ -507,7 +507,7 @@ def main() -> int:
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this decoder runs on one GPU; --gpus {args.gpus} is not supported "
-              "(utterances shard across GPUs with no exchange, see DESIGN.md)", file=sys.stderr)
+              "(utterances would shard across GPUs with no exchange between them)", file=sys.stderr)
         return 2
 
     if args.copy_kernel_bytes:
