@@ -283,6 +283,10 @@ PHASE_NAMES = ("expand", "eps_closure", "survivors", "max_active", "compact", "d
                "eps_links", "links_published", "frame_end")
 
 
+LATTICE_PHASE_NAMES = ("final_costs", "pruning_sweep", "kept_links", "kept_offsets_records", "posteriors",
+                       "merge", "node_list")
+
+
 def phase_profile(wfstdec, workload: str, reps: int = 3) -> dict:
     """Step profile of the one-workgroup forward pass (WD_FLAG_PHASES): per
     frame the device wall clock at each step boundary, summarised as the mean
@@ -301,12 +305,13 @@ def phase_profile(wfstdec, workload: str, reps: int = 3) -> dict:
     args = (cfg["beam"], cfg["max_active"], cfg["lattice_beam"])
     plain = [wfstdec.decode(graph, x, *args, timing=True, mode="workgroup").stats["forward_ms"]
              for _ in range(reps + 1)][1:]
-    rows, fwd = [], []
+    rows, fwd, lat = [], [], []
     for _ in range(reps + 1):
         r = wfstdec.decode(graph, x, *args, timing=True, mode="workgroup", flags=wfstdec.WD_FLAG_PHASES)
         rows.append(r.phases[1:])
         fwd.append(r.stats["forward_ms"])
-    rows, fwd = rows[1:], fwd[1:]
+        lat.append(np.diff(r.lattice_phases.astype(np.int64)))
+    rows, fwd, lat = rows[1:], fwd[1:], lat[1:]
     ph = np.concatenate(rows).astype(np.int64)
     hz = r.phase_tick_hz
     S = wfstdec.WD_PHASE_STAMPS
@@ -336,7 +341,10 @@ def phase_profile(wfstdec, workload: str, reps: int = 3) -> dict:
            "forward_ms_profiled": round(float(np.mean(fwd)), 3),
            "all": summary(np.ones(len(lds), bool)), "lds_table": summary(lds),
            "device_table": summary(~lds),
-           "between_frames_us": round(float(gap.mean()), 3) if gap.size else None}
+           "between_frames_us": round(float(gap.mean()), 3) if gap.size else None,
+           # the lattice pass of the same decodes (k_lattice, one workgroup)
+           "lattice_us": {n: round(float(np.mean([v[i] for v in lat])) * 1e6 / hz, 1)
+                          for i, n in enumerate(LATTICE_PHASE_NAMES)}}
     del graph
     torch.cuda.empty_cache()
     return out

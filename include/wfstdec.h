@@ -135,6 +135,13 @@ typedef struct {
  * epsilon arcs). */
 #define WD_PHASE_STAMPS 10
 #define WD_PHASE_SLOTS 12
+/* Stamps of the lattice pass (wd_result_lattice_phases, WD_FLAG_PHASES): at
+ * (0) its start, the end of (1) the final costs and best end token, (2) the
+ * backward pruning sweep (Sec. 3.5), (3) the kept-link list, (4) the kept
+ * links' per-frame offsets and records, (5) the fp64 forward-backward
+ * posteriors, (6) the merge of the kept links into (t, arc id) order, (7) the
+ * node list. */
+#define WD_LATTICE_PHASE_STAMPS 8
 
 /* Workspace capacities (per utterance).  0 selects a default.  A decode that
  * outgrows a capacity fails with WD_ECAPACITY and reports what it needed. */
@@ -405,6 +412,10 @@ int32_t wd_result_cutoffs(const wd_result* r, const float** best, const float** 
  * NULL) receives the stamps' clock rate.  Returns the number of frames (0
  * without the flag). */
 int32_t wd_result_phases(const wd_result* r, const uint64_t** stamps, double* tick_hz);
+/* WD_FLAG_PHASES: the lattice pass's WD_LATTICE_PHASE_STAMPS wall-clock
+ * stamps (same clock as wd_result_phases); returns their number, 0 without
+ * the flag. */
+int32_t wd_result_lattice_phases(const wd_result* r, const uint64_t** stamps);
 void    wd_result_stats(const wd_result* r, wd_stats* s);
 void    wd_result_free(wd_result* r);
 

@@ -67,7 +67,8 @@ Caps resolve_caps(const wd_graph* g, int32_t max_T, const wd_params* p, const wd
   if (incremental_prune(p))
     r.win = (c && c->window_links > 0) ? (uint64_t)c->window_links : std::max<uint64_t>(r.links / 4, 1);
   r.words = T1 * (g->nlevels + 1) + 1;
-  r.prof = (p->flags & WD_FLAG_PHASES) ? T1 * (uint64_t)kProfSlots : 0;
+  // (one row per frame, then one for the lattice pass)
+  r.prof = (p->flags & WD_FLAG_PHASES) ? (T1 + 1) * (uint64_t)kProfSlots : 0;
   return r;
 }
 
@@ -234,12 +235,13 @@ struct wd_result {
   std::vector<wd_lat_node> nodes;
   std::vector<wd_token> tokens;
   std::vector<float> best, cutb, cut;
-  std::vector<uint64_t> prof;  // WD_FLAG_PHASES: (T+1) x WD_PHASE_SLOTS
+  std::vector<uint64_t> prof;  // WD_FLAG_PHASES: (T+2) x WD_PHASE_SLOTS (the last row: the lattice pass)
   double tick_hz = 0.0;
   wd_stats stats{};
 };
 
 static_assert(sizeof(wd_lat_arc) == sizeof(wd::OutLink), "link record layout");
+static_assert(wd::kLatStamps == WD_LATTICE_PHASE_STAMPS && wd::kLatStamps <= wd::kProfSlots, "lattice profile row");
 static_assert(sizeof(wd_lat_node) == sizeof(wd::OutNode), "node record layout");
 
 using namespace wd;
@@ -502,7 +504,7 @@ static wd_status run_finish(wd_stream* run, wd_result** out) {
       return hip_check(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s), "result download");
     };
     if (L.prof) {
-      r->prof.resize(((size_t)Tb + 1) * kProfSlots);
+      r->prof.resize(((size_t)Tb + 2) * kProfSlots);
       int khz = 0, dev = 0;
       if ((st = d2h(r->prof.data(), L.prof, 8 * r->prof.size())) ||
           (st = hip_check(hipGetDevice(&dev), "device")) ||
@@ -771,7 +773,13 @@ extern "C" int32_t wd_result_cutoffs(const wd_result* r, const float** b, const 
 extern "C" int32_t wd_result_phases(const wd_result* r, const uint64_t** stamps, double* tick_hz) {
   *stamps = r->prof.data();
   if (tick_hz) *tick_hz = r->tick_hz;
-  return (int32_t)(r->prof.size() / kProfSlots);
+  const size_t rows = r->prof.size() / kProfSlots;
+  return rows ? (int32_t)(rows - 1) : 0;
+}
+extern "C" int32_t wd_result_lattice_phases(const wd_result* r, const uint64_t** stamps) {
+  const size_t rows = r->prof.size() / kProfSlots;
+  *stamps = rows ? r->prof.data() + (rows - 1) * kProfSlots : nullptr;
+  return rows ? (int32_t)kLatStamps : 0;
 }
 extern "C" void wd_result_stats(const wd_result* r, wd_stats* s) { *s = r->stats; }
 extern "C" void wd_result_free(wd_result* r) { delete r; }

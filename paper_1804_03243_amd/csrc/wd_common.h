@@ -28,6 +28,7 @@ constexpr uint32_t kPathMaxLen = 16;        // epsilon paths longer than this: n
 constexpr uint64_t kPathMax = 1ull << 27;   // more epsilon paths than this: no path table
 constexpr int kProfStamps = 10;             // step boundaries stamped per frame (WD_FLAG_PHASES)
 constexpr int kProfSlots = kProfStamps + 2; // + two words describing the frame
+constexpr int kLatStamps = 8;               // lattice-pass stamps (in the row after the last frame's)
 
 // Order-preserving map of fp32 onto u32 (-0.0 folded onto +0.0): for non-NaN
 // a, b: a < b  <=>  cost_key(a) < cost_key(b).

@@ -712,6 +712,12 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   if (info->status != 0) return;
   const uint32_t tid = threadIdx.x;
   const int T = L.T;
+  // step profile (WD_FLAG_PHASES): the wall clock at the pass's section
+  // boundaries, in the profile row after the last frame's
+  auto lstamp = [&](int k) {
+    if (L.prof && tid == 0 && blockIdx.y == 0) L.prof[(size_t)(T + 1) * kProfSlots + (size_t)k] = wall_clock64();
+  };
+  lstamp(0);
   const uint64_t nT0 = L.node_off[T], nT1 = L.node_off[T + 1];
   const uint64_t nnodes = nT1;
   const uint64_t nlinks = L.link_off[T + 1];
@@ -805,8 +811,10 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   }
 
   // ------------------------------------------------ backward extra-cost sweep
+  lstamp(1);
   if (!swept) sweep_block(L, g, sh, tid, final_used, best_total);
   __syncthreads();
+  lstamp(2);
 
   // ------------------------------------------ kept links (final merge input)
   const uint32_t lb_key = cost_key(prm.lattice_beam);
@@ -847,6 +855,7 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
     return;
   }
   __syncthreads();
+  lstamp(3);
   const uint64_t* kid = L.kept_idx;
   // per frame t: kept links start at kf[2t], kept epsilon links at kf[2t+1];
   // frame t ends where frame t+1 starts
@@ -882,6 +891,7 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   }
 
   // ----------------------------------------------------- posteriors (fp64)
+  lstamp(4);
   const uint64_t start_node = start_node_of(L, g);
   const bool wide = n_kept > 64 * ((uint64_t)T + 1);  // (more than 64 kept links per frame)
   // small kept lattices: alpha on wavefront 0 and beta on wavefront 1,
@@ -899,6 +909,7 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
     }
   }
   __syncthreads();
+  lstamp(5);
   // (with a wide lattice in chip-wide mode, the third workgroup writes Z;
   // the merge runs as a chip-wide kernel after this one)
   const double Z = swept ? 0.0 : L.beta[start_node];
@@ -919,8 +930,13 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   assemble(L, g, false, n_kept, L.out_links, lb_key, Z, true, true, tid, kLT);
   if (debug) assemble(L, g, true, nlinks, L.out_raw, lb_key, Z, true, false, tid, kLT);
   __syncthreads();
+  lstamp(6);
   const uint64_t n_out = write_nodes(L, nnodes, sh.bs, par);
   if (tid == 0) info->out_nodes = n_out;
+  if (L.prof) {
+    __syncthreads();
+    lstamp(7);
+  }
 }
 
 // Chip-wide merge of the kept links (and of every raw link with the debug

@@ -33,6 +33,7 @@ WD_FLAG_PHASES = 64
 WD_FLAG_EPS_LEVELS = 128
 WD_PHASE_STAMPS = 10
 WD_PHASE_SLOTS = 12
+WD_LATTICE_PHASE_STAMPS = 8
 _MODE_FLAGS = {"auto": 0, "workgroup": WD_FLAG_ONE_WORKGROUP, "chip": WD_FLAG_CHIP_WIDE,
                "chip_dyn": WD_FLAG_CHIP_WIDE | WD_FLAG_DYNAMIC_LB,
                "chip_noprune": WD_FLAG_CHIP_WIDE | WD_FLAG_NO_INCREMENTAL_PRUNE,
@@ -94,6 +95,7 @@ EXPORTS = ["wd_graph_bytes", "wd_graph_load", "wd_graph_free", "wd_graph_eps_lev
            "wd_result_status",
            "wd_result_cost", "wd_result_words", "wd_result_lattice", "wd_result_nodes",
            "wd_result_tokens", "wd_result_raw_lattice", "wd_result_cutoffs", "wd_result_phases",
+           "wd_result_lattice_phases",
            "wd_result_stats",
            "wd_result_free", "wd_last_error"]
 
@@ -145,6 +147,7 @@ def lib():
             "wd_result_raw_lattice": ([VP, P(VP)], ctypes.c_int64),
             "wd_result_cutoffs": ([VP, P(VP), P(VP), P(VP)], ctypes.c_int32),
             "wd_result_phases": ([VP, P(VP), P(ctypes.c_double)], ctypes.c_int32),
+            "wd_result_lattice_phases": ([VP, P(VP)], ctypes.c_int32),
             "wd_result_stats": ([VP, P(wd_stats)], None),
             "wd_result_free": ([VP], None),
             "wd_last_error": ([], ctypes.c_char_p),
@@ -392,9 +395,13 @@ def wd_result_read(r: int, debug: bool = True, phases: bool = True,
         n = L.wd_result_phases(r, ctypes.byref(vp), ctypes.byref(hz))
         out.phases = _copy(vp.value, n * WD_PHASE_SLOTS, np.dtype("<u8")).reshape(n, WD_PHASE_SLOTS)
         out.phase_tick_hz = hz.value
+        lp = ctypes.c_void_p()
+        n = L.wd_result_lattice_phases(r, ctypes.byref(lp))
+        out.lattice_phases = _copy(lp.value, n, np.dtype("<u8"))
     else:
         out.phases = np.zeros((0, WD_PHASE_SLOTS), np.dtype("<u8"))
         out.phase_tick_hz = 0.0
+        out.lattice_phases = np.zeros(0, np.dtype("<u8"))
     st = wd_stats()
     L.wd_result_stats(r, ctypes.byref(st))
     out.stats = {f: getattr(st, f) for f, _ in wd_stats._fields_ if f != "needed"}

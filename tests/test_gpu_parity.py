@@ -366,8 +366,11 @@ def test_phase_profile(wf, oracle_mod, tiny10k):
     assert np.array_equal(ntok, counts)
     nlink = ph[:, wf.WD_PHASE_STAMPS] >> 32
     assert np.array_equal(nlink, np.bincount(o.raw_links["t"], minlength=121))
+    lp = r.lattice_phases.astype(np.int64)
+    assert lp.shape == (wf.WD_LATTICE_PHASE_STAMPS,) and np.all(np.diff(lp) >= 0)
+    assert lp[0] >= st[-1, wf.WD_PHASE_STAMPS - 1]  # the lattice pass runs after the last frame
     plain = wf.decode(graph, x, *args, mode="workgroup")
-    assert plain.phases.shape[0] == 0
+    assert plain.phases.shape[0] == 0 and plain.lattice_phases.shape[0] == 0
     with pytest.raises(wf.WdError) as e:
         wf.decode(graph, x, *args, mode="chip", flags=wf.WD_FLAG_PHASES)
     assert e.value.status == wf.WD_EINVAL
