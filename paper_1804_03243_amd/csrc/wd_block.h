@@ -22,7 +22,9 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 // Every lane of the wavefront must be active.
 enum : int {
   kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118,
-  kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143
+  kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143,
+  // within each group of four lanes: swap neighbours (1,0,3,2), swap pairs (2,3,0,1)
+  kDppQuadSwap1 = 0xb1, kDppQuadSwap2 = 0x4e
 };
 
 // Lane i reads the lane its DPP control names; `fill` where that lane is

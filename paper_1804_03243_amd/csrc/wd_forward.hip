@@ -902,10 +902,12 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       const uint32_t m = lds ? ns : n_keep;  // entries in rs_* (<= 2 * kThreads)
       if (m <= kDirectRank) {
         // few entries: each kept state's rank is the number of kept states
-        // below it.  Without a max-active cut the survivor pass has put every
-        // entry into srt already; otherwise the entries it drops read as ~0.
-        // The ranking thread also fills the frontier entry's arc offsets,
-        // degrees and level (its loads overlap the ranking).
+        // below it, counted by four lanes (each a quarter of the entries)
+        // and summed across them.  Without a max-active cut the survivor pass
+        // has put every entry into srt already; otherwise the entries it drops
+        // read as ~0.  The quad's first lane also fills the frontier entry's
+        // arc offsets, degrees and level (its loads overlap the ranking).
+        static_assert(4 * kDirectRank <= kThreads, "four lanes per directly ranked entry");
         deg_ready = true;
         if (!(lds && cut_key == kcutb)) {
           if (tid < m) {
@@ -918,32 +920,50 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         // the frontier's earlier stores have landed by now; saying so lets the
         // ranking loop read LDS without first waiting for the loads below
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
-        if (tid < m && sh.srt[tid] != kNoKey) {
-          const uint32_t s = sh.srt[tid];
-          const uint4 o0 = g.off[s], o1 = g.off[s + 1];
-          const uint8_t cls = g.sclass[s];
+        // (the lane index passes through an empty asm so that the values
+        // derived from it are computed here rather than held in registers
+        // across the whole frame loop)
+        uint32_t lane_q = tid;
+        asm volatile("" : "+v"(lane_q));
+        const uint32_t e = lane_q >> 2, sub = lane_q & 3u;
+        if (e < m && sh.srt[e] != kNoKey) {  // (the same for the four lanes)
+          const uint32_t s = sh.srt[e];
+          uint4 o0 = make_uint4(0, 0, 0, 0), o1 = o0;
+          uint8_t cls = 0;
+          if (sub == 0) {
+            o0 = g.off[s];
+            o1 = g.off[s + 1];
+            cls = g.sclass[s];
+          }
           const uint4* q4 = reinterpret_cast<const uint4*>(sh.srt);
           uint32_t r = 0;
-          for (uint32_t q = 0; q < m / 4u; ++q) {
+          for (uint32_t q = sub; q < m / 4u; q += 4u) {
             const uint4 v = q4[q];
             r += (v.x < s) + (v.y < s) + (v.z < s) + (v.w < s);
           }
-          for (uint32_t q = m & ~3u; q < m; ++q) r += sh.srt[q] < s;
-          place(r, s, sh.rs_pack[tid]);
-          if (lds) sh.h_val[sh.rs_slot[tid]] = node_base + r;  // the table now maps kept states to node ids
-          else L.idx[s] = (uint32_t)(node_base + r);
-          // the link pass reads the token's epsilon arcs
-          if (o1.y > o0.y) warm_x = __uint_as_float(g.xarc[o0.y].y);
-          f.ebeg[r] = o0.x;
-          f.xbeg[r] = o0.y;
-          f.edeg[r] = o1.x - o0.x;  // degrees for now, prefix sums below
-          f.xdeg[r] = o1.y - o0.y;
-          f.cls[r] = cls;
+          const uint32_t qt = (m & ~3u) + sub;
+          if (qt < m) r += sh.srt[qt] < s;
+          r += dpp32<kDppQuadSwap1>(r, 0u);
+          r += dpp32<kDppQuadSwap2>(r, 0u);
+          if (sub == 0) {
+            place(r, s, sh.rs_pack[e]);
+            if (lds) sh.h_val[sh.rs_slot[e]] = node_base + r;  // the table now maps kept states to node ids
+            else L.idx[s] = (uint32_t)(node_base + r);
+            // the link pass reads the token's epsilon arcs
+            if (o1.y > o0.y) warm_x = __uint_as_float(g.xarc[o0.y].y);
+            f.ebeg[r] = o0.x;
+            f.xbeg[r] = o0.y;
+            f.edeg[r] = o1.x - o0.x;  // degrees for now, prefix sums below
+            f.xdeg[r] = o1.y - o0.y;
+            f.cls[r] = cls;
+          }
         }
       } else {
         // counting sort on the top 11 bits of the state, then the few states
         // sharing a bucket are ranked among themselves
-        const uint32_t sbits = 32u - (uint32_t)__clz(g.S > 1 ? g.S - 1 : 1u);
+        uint32_t S = g.S;
+        asm volatile("" : "+v"(S));  // (derived here, not held across the frame loop)
+        const uint32_t sbits = 32u - (uint32_t)__clz(S > 1 ? S - 1 : 1u);
         const uint32_t ssh = sbits > 11u ? sbits - 11u : 0u;
         for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
         __syncthreads();
