@@ -8,6 +8,14 @@
 namespace wd {
 
 __device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & 63u; }
+
+// v, through an empty asm: values derived from the result are computed where
+// they are used instead of being hoisted out of a long loop and held (or
+// spilled) across it.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
 __device__ __forceinline__ uint32_t wave_id() { return threadIdx.x >> 6; }
 __device__ __forceinline__ uint64_t lanemask_lt() {
   return (lane_id() == 0) ? 0ull : (~0ull >> (64u - lane_id()));

@@ -49,6 +49,9 @@ struct FwdShared {
   unsigned long long deg_tot;  // frontier out-degree totals (epsilon << 32 | emitting), small frames
   uint32_t wcnt[kWaves];  // emitting lattice links of the frame per wavefront (one item per thread)
   uint32_t lnx;        // epsilon lattice links of the frame (one-wavefront epsilon link pass)
+  // frontier token whose epsilon out-arcs start at epsilon work item i < 64
+  // (kNoSlot elsewhere), written by the degree scan of small frames
+  uint16_t xo[64];
   uint32_t hcount;     // LDS table: reserved entries
   uint32_t spill;      // LDS table full: the frame goes global
   uint32_t n_bk;       // LDS table: epsilon bucket entries
@@ -276,6 +279,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
 
   for (uint32_t i = tid; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nb[i] = 0;
   for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
+  if (tid < 64u) sh.xo[tid] = kNoSlot;
   h_clear(sh, kHashCap);
   if (tid == 0) {
     sh.n_touched = 0;
@@ -920,11 +924,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         // the frontier's earlier stores have landed by now; saying so lets the
         // ranking loop read LDS without first waiting for the loads below
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
-        // (the lane index passes through an empty asm so that the values
-        // derived from it are computed here rather than held in registers
-        // across the whole frame loop)
-        uint32_t lane_q = tid;
-        asm volatile("" : "+v"(lane_q));
+        const uint32_t lane_q = opaque(tid);
         const uint32_t e = lane_q >> 2, sub = lane_q & 3u;
         if (e < m && sh.srt[e] != kNoKey) {  // (the same for the four lanes)
           const uint32_t s = sh.srt[e];
@@ -961,8 +961,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       } else {
         // counting sort on the top 11 bits of the state, then the few states
         // sharing a bucket are ranked among themselves
-        uint32_t S = g.S;
-        asm volatile("" : "+v"(S));  // (derived here, not held across the frame loop)
+        const uint32_t S = opaque(g.S);
         const uint32_t sbits = 32u - (uint32_t)__clz(S > 1 ? S - 1 : 1u);
         const uint32_t ssh = sbits > 11u ? sbits - 11u : 0u;
         for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
@@ -1104,6 +1103,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           if (p < n_keep) {
             f.edeg[p] = eb;
             f.xdeg[p] = xb;
+            if (dx[k] != 0 && xb < 64u) sh.xo[xb] = (uint16_t)p;
           }
           eb += de[k];
           xb += dx[k];
@@ -1201,8 +1201,19 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         uint4 r = make_uint4(0, 0, 0, 0);
         uint32_t p = 0, xk = kNoKey;
         float x = 0.0f;
+        // the item's token: with the degree scan's start marks, the one
+        // whose epsilon items start at the last mark at or below e (item 0
+        // always starts a token's run)
+        uint64_t starts = 0;
+        if (deg_ready) starts = __ballot(sh.xo[e] != kNoSlot);
         if (e < W_eps) {
-          p = search_le(f.xdeg, n_keep, e);
+          if (deg_ready) {
+            // marks at or below e moved to the top: the last one is e - clz below
+            const uint64_t upto = starts << (63u - opaque(e));
+            p = sh.xo[e - (uint32_t)__clzll(upto)];
+          } else {
+            p = search_le(f.xdeg, n_keep, e);
+          }
           r = g.xarc[f.xbeg[p] + (e - f.xdeg[p])];
           x = canon(key_cost(f.key[p]) + __uint_as_float(r.y));
           xk = cost_key(x);
@@ -1355,6 +1366,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     // pass's closing collective)
     for (uint32_t i = tid; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nb[i] = 0;
     for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
+    if (tid < 64u) sh.xo[tid] = kNoSlot;
     h_clear(sh, h_used_n);
     if (tid == 0) {
       sh.n_touched = 0;
