@@ -48,6 +48,28 @@ __host__ __device__ inline uint64_t pack_tok(uint32_t key, uint32_t arc) {
   return ((uint64_t)key << 32) | arc;
 }
 
+// Forward-backward in the linear domain.  For frame t let b(t) be its best
+// token cost and B the best total cost; the passes carry, per lattice node n
+// of frame t, Sa(n) = exp(b(t) - alpha(n)) and Sb(n) = exp(B - b(t) -
+// beta(n)).  Each kept link then moves mass by one factor, the same for both
+// passes: exp(b(t) - b(t-1) - graph cost - acoustic cost) for an emitting
+// link into frame t, exp(-graph cost) for an epsilon link.  Every term of a
+// kept link lies within exp(-(beam + lattice beam)) .. exp(beam + log of the
+// number of near-best paths), far inside fp64's range.
+#if defined(__HIPCC__)
+__device__ inline double emit_factor(float best_t, float best_prev, float graph, double ac) {
+  return exp((double)best_t - (double)best_prev - (double)graph - ac);
+}
+__device__ inline double eps_factor(float graph) { return exp(-(double)graph); }
+// An epsilon link's record keeps its source level in the factor's lowest 8
+// mantissa bits (a relative change below 2^-44).
+__device__ inline uint2 factor_bits(double f, bool eps, uint32_t lvl) {
+  const uint64_t u = (uint64_t)__double_as_longlong(f);
+  const uint64_t v = eps ? ((u & ~0xffull) | (lvl & 0xffu)) : u;
+  return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+}
+#endif
+
 // Device copy of the decoding graph, laid out in one caller-owned buffer.
 //   off[s]  = {first emitting arc, first epsilon arc, first epsilon path, 0} of
 //             state s (S+1 entries; the path index is 0 without a path table)
@@ -213,12 +235,12 @@ struct LaneDesc {
   // lattice pass
   WD_GLOBAL uint32_t* extra_key;         // [node_cap]
   WD_GLOBAL uint32_t* le_key;            // [link_cap + 3*win_cap]
-  WD_GLOBAL double* alpha;               // [node_cap]
-  WD_GLOBAL double* beta;                // [node_cap]
+  WD_GLOBAL double* alpha;               // [node_cap] forward sums Sa (linear domain)
+  WD_GLOBAL double* beta;                // [node_cap] backward sums Sb (linear domain)
   WD_GLOBAL uint32_t* used;              // [ceil(node_cap/32)+1] lattice-node bitmap
   WD_GLOBAL uint64_t* kept_idx;          // [kept_cap] kept link ids in link order
   WD_GLOBAL uint4* post;                 // [kept_cap] kept links for forward-backward:
-                               //   {src node, dst node, weight bits, -loglike bits | source level}
+                               //   {src node, dst node, factor bits lo, hi (| source level)}
   WD_GLOBAL uint64_t* kframe;            // [2*(T+2)] per frame: first kept link, first kept epsilon link
   // outputs
   WD_GLOBAL OutLink* out_links;          // [kept_cap]

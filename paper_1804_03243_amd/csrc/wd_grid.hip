@@ -1212,8 +1212,8 @@ __global__ void __launch_bounds__(kGT) k_gk_count(const LaneDesc* __restrict__ l
 }
 
 // Also writes each kept link's record for the forward-backward pass: {src
-// node, dst node, graph cost bits, acoustic cost bits (emitting link) or
-// source level (epsilon link)}.
+// node, dst node, the link's fp64 factor as two words (an epsilon link's with
+// its source level in the low bits)}.
 __global__ void __launch_bounds__(kGT) k_gk_write(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl,
                                                   uint32_t lb_key) {
   __shared__ GScratch s;
@@ -1241,22 +1241,25 @@ __global__ void __launch_bounds__(kGT) k_gk_write(DevGraph g, const LaneDesc* __
       else hi = mid;
     }
     const uint4 v = L.links[k];
-    uint32_t aux;
-    if (k >= L.link_xoff[lo]) aux = L.link_lvl[k];
-    else aux = __float_as_uint(-L.ll[(size_t)(lo - 1) * g.P + (g.ilabel_id[v.x] - 1)]);
-    L.post[ex] = make_uint4(v.y, v.z, __float_as_uint(g.weight_id[v.x]), aux);
+    const float w = g.weight_id[v.x];
+    const bool eps = k >= L.link_xoff[lo];
+    const double f = eps ? eps_factor(w)
+                         : emit_factor(L.best[lo], L.best[lo - 1], w,
+                                       -(double)L.ll[(size_t)(lo - 1) * g.P + (g.ilabel_id[v.x] - 1)]);
+    const uint2 fb = factor_bits(f, eps, eps ? L.link_lvl[k] : 0u);
+    L.post[ex] = make_uint4(v.y, v.z, fb.x, fb.y);
   }
 }
 
-// alpha and beta of every node start at +inf (the lattice kernel then only
-// writes the nodes that kept links reach).
+// The linear-domain forward and backward sums of every node start at 0 (the
+// lattice kernel then only adds into the nodes that kept links reach).
 __global__ void __launch_bounds__(kGT) k_gs_fill_ab(const LaneDesc* __restrict__ lanes) {
   const LaneDesc& L = lanes[blockIdx.y];
   if (L.info->status != 0) return;
   const uint64_t n = L.node_off[L.T + 1];
   for (uint64_t i = (uint64_t)blockIdx.x * kGT + threadIdx.x; i < n; i += (uint64_t)kGB * kGT) {
-    L.alpha[i] = INFINITY;
-    L.beta[i] = INFINITY;
+    L.alpha[i] = 0.0;
+    L.beta[i] = 0.0;
   }
   // per frame t: kept links start at kframe[2t], kept epsilon links at
   // kframe[2t+1] (the posterior passes' frame offsets); only when the list
@@ -1367,8 +1370,7 @@ __global__ void __launch_bounds__(kGT) k_gn_write(const LaneDesc* __restrict__ l
 // are decoded (frames only grows), and status and hist_ok still say OK (they
 // only ever change to a failure, whose result is not returned).
 
-__global__ void k_gp_go(const LaneDesc* __restrict__ lanes, GridLane* gl, int t) {
-  const LaneDesc& L = lanes[blockIdx.y];
+__global__ void k_gp_go(GridLane* gl, int t) {
   GridLane& G = gl[blockIdx.y];
   if (threadIdx.x != 0) return;
   const int32_t status = __hip_atomic_load(&G.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1633,7 +1635,7 @@ wd_status grid_frames(GridRun* run, const DevGraph& g, const LaneDesc* lanes, vo
       e = hipEventRecord(run->ready[j % 4], st);
       if (e == hipSuccess) e = hipStreamWaitEvent(q, run->ready[j % 4], 0);
       if (e != hipSuccess) break;
-      hipLaunchKernelGGL(k_gp_go, one, dim3(64), 0, q, lanes, gl, t);
+      hipLaunchKernelGGL(k_gp_go, one, dim3(64), 0, q, gl, t);
       hipLaunchKernelGGL(k_gp_init, part, blk, 0, q, lanes, gl, t0, t);
       // frame f: the emitting links leaving it, then its epsilon levels; down
       // to f = t0 - 1 for the emitting links into t0 (the window's first run;

@@ -48,24 +48,27 @@ __device__ __forceinline__ uint64_t search_le64(const uint64_t* a, uint64_t n, u
 }
 
 
-// -log(exp(-a) + exp(-b)) accumulated atomically into *p (fp64).
-__device__ __forceinline__ void atomic_logadd(double* p, double v) {
-  if (!(v < INFINITY)) return;
-  unsigned long long* a = reinterpret_cast<unsigned long long*>(p);
-  unsigned long long old = *a;
-  while (true) {
-    const double o = __longlong_as_double((long long)old);
-    double n;
-    if (!(o < INFINITY)) n = v;
-    else n = fmin(o, v) - log1p(exp(-fabs(o - v)));
-    const unsigned long long prev = atomicCAS(a, old, (unsigned long long)__double_as_longlong(n));
-    if (prev == old) break;
-    old = prev;
-  }
+// Mass v moved into a node's linear-domain sum (the factor helpers beside
+// cost_key define the sums): LDS windows add with the LDS unit's fp64 add,
+// device-memory frames with the memory-side one.
+__device__ __forceinline__ void mass_add(double* p, double v, bool lds) {
+  if (!(v > 0.0)) return;
+  if (lds) atomicAdd(p, v);
+  else unsafeAtomicAdd(p, v);
 }
 
 __device__ __forceinline__ float node_cost(const LaneDesc& L, uint64_t n) {
   return key_cost((uint32_t)(L.n_pack[n] >> 32));
+}
+
+// The kept lattice's total cost Z = beta(start) = B - b(0) - log Sb(start),
+// and the posteriors' normaliser: posterior = Sa(src) Sb(dst) factor
+// exp(-b(0)) / Sb(start).
+__device__ __forceinline__ double lattice_z(const LaneDesc& L, float best_total, uint64_t start_node) {
+  return (double)best_total - (double)L.best[0] - log(L.beta[start_node]);
+}
+__device__ __forceinline__ double post_norm(const LaneDesc& L, uint64_t start_node) {
+  return exp(-(double)L.best[0]) / L.beta[start_node];
 }
 
 // Node id of the start token: the start state among frame 0's tokens (sorted
@@ -106,7 +109,7 @@ __device__ __forceinline__ double link_ac(const LaneDesc& L, const DevGraph& g, 
 // bounds in selection order are the frame's link offsets (all links) or the
 // per-frame kept-link boundaries kf.
 __device__ __forceinline__ void assemble(const LaneDesc& L, const DevGraph& g, bool all, uint64_t n_sel,
-                         OutLink* out, uint32_t lb_key, double Z, bool with_post, bool mark_nodes,
+                         OutLink* out, uint32_t lb_key, double norm, bool with_post, bool mark_nodes,
                          uint64_t first, uint64_t stride) {
   const int T = L.T;
   const uint64_t* kid = L.kept_idx;
@@ -145,8 +148,11 @@ __device__ __forceinline__ void assemble(const LaneDesc& L, const DevGraph& g, b
     o.fwd_cost = l.x;
     o.extra = key_cost(L.le_key[k]);
     o.posterior = 0.0;
-    if (with_post && kept(L, k, lb_key))
-      o.posterior = exp(Z - L.alpha[l.src] - (double)o.graph_cost - ac - L.beta[l.dst]);
+    if (with_post && kept(L, k, lb_key)) {
+      // exp(Z - alpha(src) - cost - beta(dst)) from the linear-domain sums
+      const double f = eps ? eps_factor(o.graph_cost) : emit_factor(L.best[t], L.best[t - 1], o.graph_cost, ac);
+      o.posterior = L.alpha[l.src] * L.beta[l.dst] * f * norm;
+    }
     out[pos] = o;
     if (mark_nodes) {
       atomicOr(&L.used[l.src >> 5], 1u << (l.src & 31u));
@@ -444,13 +450,24 @@ __device__ __forceinline__ void sweep_block(const LaneDesc& L, const DevGraph& g
 __device__ __forceinline__ uint4 post_link(const LaneDesc& L, uint64_t j) { return L.post[j]; }
 
 // Record of kept link j (link k) of frame t; `eps`: an epsilon link.
+// {src node, dst node, the link's factor (epsilon: with its source level in
+// the low bits) as two words}.
 __device__ __forceinline__ uint4 post_record(const LaneDesc& L, const DevGraph& g, uint64_t k, int t, bool eps) {
   const uint4 v = L.links[k];
-  uint32_t aux;
-  if (eps) aux = L.link_lvl[k];
-  else aux = __float_as_uint(-L.ll[(size_t)(t - 1) * g.P + (g.ilabel_id[v.x] - 1)]);
-  return make_uint4(v.y, v.z, __float_as_uint(g.weight_id[v.x]), aux);
+  const float w = g.weight_id[v.x];
+  double f;
+  uint32_t lvl = 0;
+  if (eps) {
+    f = eps_factor(w);
+    lvl = L.link_lvl[k];
+  } else {
+    f = emit_factor(L.best[t], L.best[t - 1], w, -(double)L.ll[(size_t)(t - 1) * g.P + (g.ilabel_id[v.x] - 1)]);
+  }
+  const uint2 fb = factor_bits(f, eps, lvl);
+  return make_uint4(v.y, v.z, fb.x, fb.y);
 }
+__device__ __forceinline__ double rec_factor(uint4 l) { return __hiloint2double((int)l.w, (int)l.z); }
+__device__ __forceinline__ uint32_t rec_level(uint4 l) { return l.z & 0xffu; }
 
 // Kept links of a run beyond the prefetched ones, kBatch per lane per round
 // trip: the loads of a batch are issued together, then the batch is applied.
@@ -551,7 +568,7 @@ __device__ __forceinline__ void post_items(const LaneDesc& L, const DevGraph& g,
 // `swept`: device-memory alpha is +inf already.
 template <int GS>
 __device__ __forceinline__ void alpha_step(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
-                                           int t, bool swept, uint64_t start_node, const PostFrame& sa_v,
+                                           int t, bool swept, uint64_t start_node, double s_start, const PostFrame& sa_v,
                                            const PostFrame& sn_v, PostFrame& snn, const PostItems& cur,
                                            PostItems& nxt, uint32_t z) {
   const int T = L.T;
@@ -564,15 +581,15 @@ __device__ __forceinline__ void alpha_step(const LaneDesc& L, const DevGraph& g,
   // written once per kind of window, as in the sweep
   auto frame = [&](double* a, const double* ap, bool lds_a, bool lds_ap) {
     if (lds_a || !swept) {
-      for (uint32_t i = lane; i < nt; i += GS) a[i] = (n0 + i == start_node) ? 0.0 : INFINITY;
+      for (uint32_t i = lane; i < nt; i += GS) a[i] = (n0 + i == start_node) ? s_start : 0.0;
     } else if (lane == 0 && start_node >= n0 && start_node < n1) {
-      a[start_node - n0] = 0.0;  // the rest is +inf already
+      a[start_node - n0] = s_start;  // the rest is 0 already
     }
     group_sync<GS>();
     if (pa.e1 > pa.e0) {
       auto emit = [&](uint4 l) {
         const double av = lds_ap ? ap[l.x - m0] : load_fresh(&ap[l.x - m0]);
-        atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w));
+        mass_add(&a[l.y - n0], av * rec_factor(l), lds_a);
       };
 #pragma unroll
       for (int q = 0; q < kAhead; ++q)
@@ -584,9 +601,9 @@ __device__ __forceinline__ void alpha_step(const LaneDesc& L, const DevGraph& g,
       for (uint32_t lvl = 0; lvl < g.nlevels; ++lvl) {
         if (!level_present(pa.mask, lvl)) continue;
         auto eps = [&](uint4 l) {
-          if (l.w != lvl) return;
+          if (rec_level(l) != lvl) return;
           const double av = lds_a ? a[l.x - n0] : load_fresh(&a[l.x - n0]);
-          atomic_logadd(&a[l.y - n0], av + (double)__uint_as_float(l.z));
+          mass_add(&a[l.y - n0], av * rec_factor(l), lds_a);
         };
 #pragma unroll
         for (int q = 0; q < kAhead; ++q)
@@ -614,8 +631,9 @@ __device__ __forceinline__ void alpha_wave(const LaneDesc& L, const DevGraph& g,
   alpha_frame(L, 0, z, sa);
   alpha_frame(L, T >= 1 ? 1 : 0, z, sn);
   post_items<GS>(L, g, uniform(sa), lane, false, cur);
+  const double s_start = exp((double)L.best[0]);  // exp(b(0) - alpha(start)), alpha(start) = 0
   for (int t = 0; t <= T; ++t) {
-    alpha_step<GS>(L, g, sh, lane, t, swept, start_node, sa, sn, snn, cur, nxt, z);
+    alpha_step<GS>(L, g, sh, lane, t, swept, start_node, s_start, sa, sn, snn, cur, nxt, z);
     sa = sn;
     sn = snn;
     cur = nxt;
@@ -627,7 +645,7 @@ __device__ __forceinline__ void alpha_wave(const LaneDesc& L, const DevGraph& g,
 // of frame t (loaded during t+1); those of t-1 are loaded into nxt now.
 template <int GS>
 __device__ __forceinline__ void beta_step(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
-                                          int t, bool swept, bool final_used, const PostFrame& sa_v,
+                                          int t, bool swept, bool final_used, double ref_T, const PostFrame& sa_v,
                                           const PostFrame& sn_v, PostFrame& snn, const PostItems& cur,
                                           PostItems& nxt, uint32_t z) {
   const int T = L.T;
@@ -642,9 +660,11 @@ __device__ __forceinline__ void beta_step(const LaneDesc& L, const DevGraph& g, 
 #pragma unroll
       for (int q = 0; q <= kAhead; ++q)
         for (uint32_t i = lane + (uint32_t)(GS * q); i < nt; i += (q < kAhead ? nt : (uint32_t)GS)) {
-          double v = INFINITY;
+          double v = 0.0;  // exp(B - b(T) - final weight) on the last frame
           if (t == T)
-            v = final_used ? (double)(q < kAhead ? cur.fw[q < kAhead ? q : 0] : g.final_w[L.n_state[n0 + i]]) : 0.0;
+            v = exp(ref_T -
+                    (final_used ? (double)(q < kAhead ? cur.fw[q < kAhead ? q : 0] : g.final_w[L.n_state[n0 + i]])
+                                : 0.0));
           b[i] = v;
         }
     }
@@ -652,7 +672,7 @@ __device__ __forceinline__ void beta_step(const LaneDesc& L, const DevGraph& g, 
     if (pa.e1 > pa.e0) {
       auto emit = [&](uint4 l) {
         const double bv = lds_bn ? bn[l.y - m0] : load_fresh(&bn[l.y - m0]);
-        atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + (double)__uint_as_float(l.w) + bv);
+        mass_add(&b[l.x - n0], rec_factor(l) * bv, lds_b);
       };
 #pragma unroll
       for (int q = 0; q < kAhead; ++q)
@@ -664,9 +684,9 @@ __device__ __forceinline__ void beta_step(const LaneDesc& L, const DevGraph& g, 
       for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
         if (!level_present(pa.mask, (uint32_t)lvl)) continue;
         auto eps = [&](uint4 l) {
-          if (l.w != (uint32_t)lvl) return;
+          if (rec_level(l) != (uint32_t)lvl) return;
           const double bv = lds_b ? b[l.y - n0] : load_fresh(&b[l.y - n0]);
-          atomic_logadd(&b[l.x - n0], (double)__uint_as_float(l.z) + bv);
+          mass_add(&b[l.x - n0], rec_factor(l) * bv, lds_b);
         };
 #pragma unroll
         for (int q = 0; q < kAhead; ++q)
@@ -685,7 +705,7 @@ __device__ __forceinline__ void beta_step(const LaneDesc& L, const DevGraph& g, 
 // highest source level, on GS threads.
 template <int GS>
 __device__ __forceinline__ void beta_wave(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t lane,
-                                          bool swept, bool final_used) {
+                                          bool swept, bool final_used, float best_total) {
   const int T = L.T;
   const uint32_t z = opaque_zero();
   PostFrame sa, sn, snn;
@@ -693,8 +713,9 @@ __device__ __forceinline__ void beta_wave(const LaneDesc& L, const DevGraph& g, 
   beta_frame(L, T, z, sa);
   beta_frame(L, T >= 1 ? T - 1 : 0, z, sn);
   post_items<GS>(L, g, uniform(sa), lane, final_used, cur);
+  const double ref_T = (double)best_total - (double)L.best[T];  // B - b(T)
   for (int t = T; t >= 0; --t) {
-    beta_step<GS>(L, g, sh, lane, t, swept, final_used, sa, sn, snn, cur, nxt, z);
+    beta_step<GS>(L, g, sh, lane, t, swept, final_used, ref_T, sa, sn, snn, cur, nxt, z);
     sa = sn;
     sn = snn;
     cur = nxt;
@@ -804,9 +825,9 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
     // computes alpha; Z from it
     const uint64_t nk = info->kept;
     if (!swept || nk <= 64 * ((uint64_t)T + 1) || nk > L.kept_cap) return;
-    beta_wave<kLT>(L, g, sh, tid, swept, final_used);
+    beta_wave<kLT>(L, g, sh, tid, swept, final_used, best_total);
     __syncthreads();
-    if (tid == 0) info->Z = L.beta[start_node_of(L, g)];
+    if (tid == 0) info->Z = lattice_z(L, best_total, start_node_of(L, g));
     return;
   }
 
@@ -900,19 +921,19 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   // beta on the utterance's third workgroup at the same time
   if (!wide) {
     if (tid < 64) alpha_wave<64>(L, g, sh, tid, swept, start_node);
-    else if (tid < 128) beta_wave<64>(L, g, sh, tid - 64, swept, final_used);
+    else if (tid < 128) beta_wave<64>(L, g, sh, tid - 64, swept, final_used, best_total);
   } else {
     alpha_wave<kLT>(L, g, sh, tid, swept, start_node);
     if (!swept) {
       __syncthreads();
-      beta_wave<kLT>(L, g, sh, tid, swept, final_used);
+      beta_wave<kLT>(L, g, sh, tid, swept, final_used, best_total);
     }
   }
   __syncthreads();
   lstamp(5);
   // (with a wide lattice in chip-wide mode, the third workgroup writes Z;
   // the merge runs as a chip-wide kernel after this one)
-  const double Z = swept ? 0.0 : L.beta[start_node];
+  const double norm = swept ? 0.0 : post_norm(L, start_node);
   if (tid == 0) {
     info->final_used = final_used ? 1 : 0;
     info->kept = n_kept;
@@ -920,15 +941,15 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
     info->start_node = (uint32_t)start_node;
     info->best_node = (uint32_t)bnode;
     info->best_cost = best_total;
-    if (!(swept && wide)) info->Z = L.beta[start_node];
+    if (!(swept && wide)) info->Z = lattice_z(L, best_total, start_node);
   }
   // used-node bitmap is zero on entry (cleared by the host before the launch)
   if (tid == 0) atomicOr(&L.used[start_node >> 5], 1u << (start_node & 31u));
   if (swept) return;  // the merge and the node list run as chip-wide kernels
 
   // ------------------------------------------- final merge of the kept links
-  assemble(L, g, false, n_kept, L.out_links, lb_key, Z, true, true, tid, kLT);
-  if (debug) assemble(L, g, true, nlinks, L.out_raw, lb_key, Z, true, false, tid, kLT);
+  assemble(L, g, false, n_kept, L.out_links, lb_key, norm, true, true, tid, kLT);
+  if (debug) assemble(L, g, true, nlinks, L.out_raw, lb_key, norm, true, false, tid, kLT);
   __syncthreads();
   lstamp(6);
   const uint64_t n_out = write_nodes(L, nnodes, sh.bs, par);
@@ -948,9 +969,10 @@ __global__ void __launch_bounds__(256) k_lat_assemble(DevGraph g, const LaneDesc
   const uint32_t lb_key = cost_key(prm.lattice_beam);
   const uint64_t first = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  assemble(L, g, false, info->kept, L.out_links, lb_key, info->Z, true, true, first, stride);
+  const double norm = post_norm(L, info->start_node);
+  assemble(L, g, false, info->kept, L.out_links, lb_key, norm, true, true, first, stride);
   if (prm.flags & 1u)
-    assemble(L, g, true, L.link_off[L.T + 1], L.out_raw, lb_key, info->Z, true, false, first, stride);
+    assemble(L, g, true, L.link_off[L.T + 1], L.out_raw, lb_key, norm, true, false, first, stride);
 }
 
 void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s) {
