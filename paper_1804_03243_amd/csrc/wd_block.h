@@ -17,8 +17,10 @@ __device__ __forceinline__ uint32_t opaque(uint32_t v) {
   return v;
 }
 __device__ __forceinline__ uint32_t wave_id() { return threadIdx.x >> 6; }
-__device__ __forceinline__ uint64_t lanemask_lt() {
-  return (lane_id() == 0) ? 0ull : (~0ull >> (64u - lane_id()));
+// Set bits of m in the lanes below this one (the mbcnt instructions count
+// them directly, with no lane mask to build or keep).
+__device__ __forceinline__ uint32_t rank_in(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
 // Wavefront scans and reductions by DPP (data-parallel primitives of the
@@ -193,7 +195,7 @@ __device__ __forceinline__ uint32_t wave_append(bool pred, uint32_t* counter) {
     if ((int)lane_id() == leader) base = atomicAdd(counter, (uint32_t)__popcll(m));
     base = (uint32_t)__builtin_amdgcn_readlane((int)base, leader);
   }
-  return base + (uint32_t)__popcll(m & lanemask_lt());
+  return base + rank_in(m);
 }
 
 // Last i in [0, n) with a[i] <= w, for a non-decreasing a with a[0] <= w.

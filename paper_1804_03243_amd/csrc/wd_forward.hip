@@ -98,36 +98,39 @@ __device__ __forceinline__ Front front_at(bool lds, FwdShared& sh, const LaneDes
 
 __device__ __forceinline__ uint32_t h_home(uint32_t s) { return (s * 0x9E3779B1u) >> 20; }  // 12 bits
 
-// Find or insert state s; returns its slot, or kHashCap when the table is full
-// (sh.spill is then set).  *fresh: this call inserted s.  At most kHashMax
-// entries are ever inserted (< kHashCap), so every probe sequence ends.
+// Find or insert state s; returns its slot, or kHashCap when the frame
+// outgrows the table (sh.spill is then set and the frame goes to the global
+// slot array).  *fresh: this call inserted s.  The probe reads up to s or an
+// empty slot, where a compare-and-swap claims it (or finds s, put there
+// meanwhile); the claimed slots are then counted, a wavefront at a time, and
+// recorded for the survivor pass and the clear (the first kHashMax of them:
+// more means a spill, after which the whole table is cleared).  The probe
+// stops after kHashCap positions, so it ends even in a full table.
 __device__ __forceinline__ uint32_t h_insert(FwdShared& sh, uint32_t s, bool* fresh) {
-  *fresh = false;
-  uint32_t i = h_home(s);
-  while (true) {
-    const uint32_t k = sh.h_key[i];
-    if (k == s) return i;
-    if (k == kNoKey) break;
-    i = (i + 1) & (kHashCap - 1);
-  }
-  const uint32_t c = atomicAdd(&sh.hcount, 1u);
-  if (c >= (uint32_t)kHashMax) {
-    sh.spill = 1;
-    return kHashCap;
-  }
-  while (true) {
-    const uint32_t prev = atomicCAS(&sh.h_key[i], kNoKey, s);
-    if (prev == kNoKey) {
-      sh.h_used[c] = (uint16_t)i;
-      *fresh = true;
-      return i;
-    }
-    if (prev == s) {
-      sh.h_used[c] = kNoSlot;
-      return i;
+  uint32_t i = h_home(s), slot = kHashCap;
+  bool ins = false;
+  for (uint32_t n = 0; n < (uint32_t)kHashCap; ++n) {
+    uint32_t k = sh.h_key[i];
+    if (k == kNoKey) k = atomicCAS(&sh.h_key[i], kNoKey, s);
+    if (k == kNoKey || k == s) {
+      ins = k == kNoKey;
+      slot = i;
+      break;
     }
     i = (i + 1) & (kHashCap - 1);
   }
+  const uint32_t c = wave_append(ins, &sh.hcount);
+  if (ins) {
+    if (c < (uint32_t)kHashMax) {
+      sh.h_used[c] = (uint16_t)slot;
+    } else {
+      sh.spill = 1;
+      slot = kHashCap;
+    }
+  }
+  if (slot == kHashCap) sh.spill = 1;
+  *fresh = ins && slot != kHashCap;
+  return slot;
 }
 
 __device__ __forceinline__ uint32_t h_find(const FwdShared& sh, uint32_t s) {
@@ -142,7 +145,7 @@ __device__ __forceinline__ uint32_t h_find(const FwdShared& sh, uint32_t s) {
 
 // Empties the table: every slot (used = kHashCap: its first use), or the
 // slots claimed by the first `used` insertions (the count read before the
-// last barrier; a frame claims at most kHashMax slots).
+// last barrier; a frame that did not spill claims at most kHashMax slots).
 __device__ __forceinline__ void h_clear(FwdShared& sh, uint32_t used) {
   if (used == (uint32_t)kHashCap) {
     for (uint32_t i = threadIdx.x; i < (uint32_t)kHashCap; i += kThreads) {
@@ -1072,7 +1075,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       // also waits for every store in flight
       const uint32_t q = (uint32_t)(dn - node_base);
       const uint32_t fk = f.key[q], fa = f.arc[q];
-      const uint32_t pos = before + (uint32_t)__popcll(bal & lanemask_lt());
+      const uint32_t pos = before + rank_in(bal);
       L.links[link_base + pos] = make_uint4(my_c.x, my_c.y, (uint32_t)dn, my_c.w);
       if (fk == cost_key(__uint_as_float(my_c.w)) && fa == my_c.x) L.n_pred[dn] = my_c.y;
     };
@@ -1228,7 +1231,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
             bad_idx = 1;
           } else {
             const uint32_t sn = (uint32_t)(node_base + p);
-            const uint64_t at = link_base + nE + (uint32_t)__popcll(bal & lanemask_lt());
+            const uint64_t at = link_base + nE + rank_in(bal);
             const uint32_t q = (uint32_t)(dn - node_base);
             const uint32_t cls = f.cls[p], fk = f.key[q], fa = f.arc[q];  // before the stores
             L.links[at] = make_uint4(r.w, sn, (uint32_t)dn, __float_as_uint(x));
@@ -1332,7 +1335,8 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     // warming loads without waiting for them earlier
     if (__float_as_uint(warm) == 0x7fc00001u || __float_as_uint(warm_x) == 0x7fc00001u) bad_idx |= 2u;
     // insertions to undo, read before the barrier after which thread 0 resets the count
-    const uint32_t h_used_n = sh.hcount < (uint32_t)kHashMax ? sh.hcount : (uint32_t)kHashMax;
+    // (a frame that claimed more slots than it could record clears them all)
+    const uint32_t h_used_n = sh.hcount > (uint32_t)kHashMax ? (uint32_t)kHashCap : sh.hcount;
     const uint32_t fl_or = block_or((bad_idx ? 0x80000000u : 0u) | xmask, sh.bs, par);
     stamp(8);
     if (wave_x) {

@@ -230,6 +230,18 @@ def test_wide_2m_dyadic_prefix(wf, oracle_mod, mode):
     assert r.stats["max_tokens"] > 2048
 
 
+def test_lds_table_spill_and_reuse(wf, oracle_mod, hclg5m):
+    """Frames whose expansion touches more states than the LDS token table
+    records (2048): each is redone on the global slot array, and the next
+    one, small again after the max-active cut, starts in the table, which
+    must have been emptied of every slot the spilled frame claimed."""
+    cfg, g, L, graph, _ = hclg5m
+    r, _, _ = _run(wf, oracle_mod, g, L[:30], cfg["P"], 40.0, 1500, 6.0, graph=graph,
+                   case="hclg_5m T=30 beam=40 max_active=1500 (table spills)", mode="workgroup")
+    assert r.needed["frame_tokens"] > 2048
+    assert r.stats["max_tokens"] == 1500
+
+
 @pytest.fixture(scope="module")
 def hclg5m(wf, oracle_mod):
     cfg = synth.workload("hclg_5m")
