@@ -53,8 +53,8 @@ BYTES_LINK = 16
 # runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
 # divided by the counter's reading per byte of a plain device copy of known
 # size (bench.py --copy-kernel-bytes).  Valid while k_forward's sources hash to this.
-TRAFFIC = {"sources_sha256": "c649c5ceb17906a783a1b1bf70fba53bcaa9c94e1b78544e95b7d8fa4a058da5",
-           "bytes_per_launch": 69277657}
+TRAFFIC = {"sources_sha256": "f1b31e73928979c1d4715bbc21a0884b30ae340f5d2492b5446cac1eac9326a5",
+           "bytes_per_launch": 69282132}
 
 
 FORWARD_SOURCES = ("wd_block.h", "wd_common.h", "wd_forward.hip")  # what k_forward is built from
