@@ -498,20 +498,30 @@ __global__ void __launch_bounds__(kGT) k_g_expand_dyn(DevGraph g, const LaneDesc
 }
 
 // Epsilon closure, level `lvl`: states of that level within the cutoff relax
-// their epsilon arcs; destinations sit on higher levels.  Per tile of 256
-// bucket states the workgroup spreads the tile's arcs over its threads (a
-// prefix sum of the states' epsilon degrees in LDS), so a state with many
-// epsilon arcs does not serialise the kernel.
+// their epsilon arcs; destinations sit on higher levels.  Per tile of bucket
+// states the workgroup spreads the tile's arcs over its threads (a prefix sum
+// of the states' epsilon degrees in LDS), so a state with many epsilon arcs
+// does not serialise the kernel.  The tile is the smallest of 64, 128 and 256
+// states that covers the level in one round of the grid: a level of a few
+// thousand states then spreads over a hundred workgroups and more, each
+// thread relaxing one or two arcs, instead of a few workgroups whose threads
+// take several dependent arc-and-atomic round trips in turn (wide-beam frames:
+// a frame 20 µs shorter; tiles of 32 states gain 4 µs less).
+constexpr uint32_t kLvlMinTile = 64;
+
 __global__ void __launch_bounds__(kGT) k_g_level(DevGraph g, const LaneDesc* __restrict__ lanes,
                                                  GridLane* gl, Params prm, uint32_t lvl) {
   __shared__ GScratch s;
   __shared__ TouchStage ts;
   __shared__ uint32_t t_beg[kGT], t_ex[kGT], t_key[kGT];
+  __shared__ uint32_t t_tot;
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
   const uint32_t n = G.nb[lvl];
-  if (n == 0 || blockIdx.x * kGT >= n) return;
+  uint32_t tile = kLvlMinTile;
+  while (tile < (uint32_t)kGT && (uint64_t)tile * kGB < n) tile <<= 1;
+  if (n == 0 || blockIdx.x * tile >= n) return;
   // beam cutoff from the best emitting candidate (inclusive); no candidate:
   // the survivor kernel reports it
   if (G.best_key >= kInfKey) return;
@@ -519,10 +529,10 @@ __global__ void __launch_bounds__(kGT) k_g_level(DevGraph g, const LaneDesc* __r
   const uint32_t* bk = L.bucket + g.level_base[lvl];
   stage_reset(ts, g.nlevels);
   unsigned long long eps = 0;
-  for (uint32_t base = blockIdx.x * kGT; base < n; base += kGB * kGT) {
+  for (uint32_t base = blockIdx.x * tile; base < n; base += kGB * tile) {
     const uint32_t i = base + threadIdx.x;
     uint32_t deg = 0, a0 = 0, k = 0;
-    if (i < n) {
+    if (threadIdx.x < tile && i < n) {
       const uint32_t st = bk[i];
       // the state's epsilon arc range is loaded beside its token, not after
       // the cutoff test: one round trip instead of two
@@ -533,15 +543,34 @@ __global__ void __launch_bounds__(kGT) k_g_level(DevGraph g, const LaneDesc* __r
       a0 = live ? x0 : 0u;
       deg = live ? x1 - x0 : 0u;
     }
-    unsigned long long tot;
-    const uint32_t ex = (uint32_t)gexcl64(deg, s, &tot);
-    t_beg[threadIdx.x] = a0;
-    t_ex[threadIdx.x] = ex;
-    t_key[threadIdx.x] = k;
+    uint32_t tot;
+    if (tile <= 64u) {
+      // the tile is one wavefront's: its scan needs no workgroup collective
+      if (threadIdx.x < 64u) {
+        const uint32_t inc = wave_incl_scan(deg);
+        if (threadIdx.x < tile) {
+          t_beg[threadIdx.x] = a0;
+          t_ex[threadIdx.x] = inc - deg;
+          t_key[threadIdx.x] = k;
+        }
+        if (threadIdx.x == 63u) t_tot = inc;
+      }
+      __syncthreads();
+      tot = t_tot;
+    } else {
+      unsigned long long tt;
+      const uint32_t ex = (uint32_t)gexcl64(deg, s, &tt);
+      tot = (uint32_t)tt;
+      if (threadIdx.x < tile) {
+        t_beg[threadIdx.x] = a0;
+        t_ex[threadIdx.x] = ex;
+        t_key[threadIdx.x] = k;
+      }
+      __syncthreads();
+    }
     eps += tot;
-    __syncthreads();
-    for (uint32_t w = threadIdx.x; w < (uint32_t)tot; w += kGT) {
-      const uint32_t j = search_le(t_ex, kGT, w);
+    for (uint32_t w = threadIdx.x; w < tot; w += kGT) {
+      const uint32_t j = search_le(t_ex, tile, w);
       const uint4 r = g.xarc[t_beg[j] + (w - t_ex[j])];
       const uint32_t xk = cost_key(canon(key_cost(t_key[j]) + __uint_as_float(r.y)));
       if (xk > kcutb || xk >= kInfKey) continue;
@@ -553,11 +582,20 @@ __global__ void __launch_bounds__(kGT) k_g_level(DevGraph g, const LaneDesc* __r
   if (threadIdx.x == 0 && eps) atomicAdd((unsigned long long*)&G.eps_arcs, eps);
 }
 
+// A frame without max-active whose touched states are more than one in 32 of
+// the graph's is dense: its survivors are found by one coalesced pass over
+// the whole slot array (8 bytes per state) instead of a random slot read and
+// a memory-side bitmap atomic per touched state.  Every kernel of the frame
+// takes the same decision from the same values.
+__device__ __forceinline__ bool dense_frame(const Params& prm, uint32_t nt, uint32_t S) {
+  return prm.max_active == 0 && (uint64_t)nt * 32u > (uint64_t)S;
+}
+
 // Survivors of the beam cutoff; resets the touched slots; histogram of the
 // top cost-key digit when max-active is on.  Costs never fall below the best
 // emitting candidate (weights are >= 0), so the digit is in range.  Survivors
 // and histogram counts are staged in LDS per workgroup.
-__global__ void __launch_bounds__(kGT) k_g_count(const LaneDesc* __restrict__ lanes, GridLane* gl,
+__global__ void __launch_bounds__(kGT) k_g_count(DevGraph g, const LaneDesc* __restrict__ lanes, GridLane* gl,
                                                  Params prm) {
   __shared__ uint32_t n_st, gbase;
   __shared__ uint32_t st_state[kStage];
@@ -597,6 +635,9 @@ __global__ void __launch_bounds__(kGT) k_g_count(const LaneDesc* __restrict__ la
   }
   if (nopath || over) return;
   if (prm.max_active == 0) {
+    // dense frames: the state-bitmap kernel finds the survivors in the slot
+    // array itself
+    if (dense_frame(prm, nt, g.S)) return;
     // every survivor is kept: mark its state; its token stays in the slot,
     // where the compaction reads and resets it
     if (blockIdx.x * kGT >= nt) return;
@@ -772,9 +813,32 @@ __global__ void __launch_bounds__(kGT) k_g_bits(DevGraph g, const LaneDesc* __re
   }
   uint64_t blo, bhi, lo, hi;
   chunk((g.S + 31u) >> 5, blockIdx.x, &blo, &bhi);
-  sub_chunk(blo, bhi, &lo, &hi);
   unsigned long long c = 0;
-  for (uint64_t w = lo; w < hi; ++w) c += (uint32_t)__popc(L.bitmap[w]);
+  if (dense_frame(prm, G.n_touched, g.S)) {
+    // the chunk's states in order, one per thread: a state survives when its
+    // slot holds a token within the beam cutoff (other touched slots are
+    // emptied here, the survivors' by the compaction); each half-wavefront's
+    // ballot is one bitmap word, written whole
+    const uint32_t kcutb = G.kcutb;
+    const uint32_t s0 = (uint32_t)blo << 5, s1 = (uint32_t)bhi << 5;
+    for (uint32_t base = s0; base < s1; base += kGT) {
+      const uint32_t st = base + threadIdx.x;
+      bool keep = false;
+      if (st < s1 && st < g.S) {
+        const unsigned long long v = L.slot[st];
+        keep = (uint32_t)(v >> 32) <= kcutb;
+        if (!keep && v != kEmpty) L.slot[st] = kEmpty;
+      }
+      const uint64_t m = __ballot(keep);
+      const uint32_t half = lane_id() & 32u;
+      if ((lane_id() & 31u) == 0 && base + (threadIdx.x & ~31u) < s1)
+        L.bitmap[(base + (threadIdx.x & ~31u)) >> 5] = (uint32_t)(m >> half);
+      if (lane_id() == 0) c += (uint32_t)__popcll(m);
+    }
+  } else {
+    sub_chunk(blo, bhi, &lo, &hi);
+    for (uint64_t w = lo; w < hi; ++w) c += (uint32_t)__popc(L.bitmap[w]);
+  }
   c = gsum64(c, s);
   if (threadIdx.x == 0) G.part[0][blockIdx.x] = c;
 }
@@ -797,7 +861,22 @@ __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* _
   unsigned long long pos0, n_all;
   part_prefix(G.part[0], blockIdx.x, s, &pos0, &n_all);
   const uint64_t nb = G.node_base;
-  const bool store = G.hist_ok != 0;
+  bool store = G.hist_ok != 0;
+  if (dense_frame(prm, G.n_touched, g.S)) {
+    // the survivors were counted by the bitmap kernel's workgroups: the
+    // node capacity check and the frame's kept count happen here (every
+    // workgroup decides alike; workgroup 0 records)
+    const bool fits = nb + n_all <= L.node_cap;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      G.n_surv = (uint32_t)n_all;
+      G.n_keep = (uint32_t)n_all;
+      if (store && !fits) {
+        G.hist_ok = 0;
+        G.ovf |= kOvfNodes;
+      }
+    }
+    store = store && fits;
+  }
   const uint32_t best = G.best_key;
   const bool in_slot = prm.max_active == 0;  // the kept tokens are still in their slots
   unsigned long long deg = 0;
@@ -1613,7 +1692,7 @@ wd_status grid_frames(GridRun* run, const DevGraph& g, const LaneDesc* lanes, vo
     if (prm.flags & WD_FLAG_DYNAMIC_LB) hipLaunchKernelGGL(k_g_expand_dyn, all, blk, 0, st, g, lanes, gl, prm, t);
     else hipLaunchKernelGGL(k_g_expand, all, blk, 0, st, g, lanes, gl, prm, t);
     for (uint32_t l = 0; l < g.nlevels; ++l) hipLaunchKernelGGL(k_g_level, all, blk, 0, st, g, lanes, gl, prm, l);
-    hipLaunchKernelGGL(k_g_count, all, blk, 0, st, lanes, gl, prm);
+    hipLaunchKernelGGL(k_g_count, all, blk, 0, st, g, lanes, gl, prm);
     if (prm.max_active > 0) {
       hipLaunchKernelGGL(k_g_select, one, blk, 0, st, gl, prm, 0);
       for (int step = 1; step < 3; ++step) {
