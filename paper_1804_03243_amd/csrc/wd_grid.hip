@@ -924,7 +924,14 @@ __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* _
       L.f_key[p] = (uint32_t)(v >> 32);
       L.f_arc[p] = (uint32_t)v;
       if ((uint32_t)(v >> 32) == best) atomicMin(&G.best_pos, (uint32_t)p);
+      // the token's arc ranges, its degrees for now (the degree kernel turns
+      // them into prefix sums) and its epsilon level
       const uint4 o0 = g.off[st], o1 = g.off[st + 1];
+      L.f_ebeg[p] = o0.x;
+      L.f_xbeg[p] = o0.y;
+      L.f_edeg[p] = o1.x - o0.x;
+      L.f_xdeg[p] = o1.y - o0.y;
+      L.f_cls[p] = g.sclass[st];
       deg += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
     }
     pos0 += tot;
@@ -934,8 +941,8 @@ __global__ void __launch_bounds__(kGT) k_g_compact(DevGraph g, const LaneDesc* _
   if (threadIdx.x == 0) G.part[1][blockIdx.x] = deg;
 }
 
-// Degree prefix sums of the frontier: each workgroup rescans the frontier range
-// it compacted.
+// Degree prefix sums of the frontier: each workgroup rescans the degrees of
+// the frontier range it compacted.
 __global__ void __launch_bounds__(kGT) k_g_degrees(DevGraph g, const LaneDesc* __restrict__ lanes,
                                                    GridLane* gl) {
   __shared__ GScratch s;
@@ -950,22 +957,14 @@ __global__ void __launch_bounds__(kGT) k_g_degrees(DevGraph g, const LaneDesc* _
   uint64_t lo, hi;
   sub_chunk(blo, bhi, &lo, &hi);
   unsigned long long c = 0;
-  for (uint64_t p = lo; p < hi; ++p) {
-    const uint32_t st = L.f_state[p];
-    const uint4 o0 = g.off[st], o1 = g.off[st + 1];
-    c += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
-  }
+  for (uint64_t p = lo; p < hi; ++p) c += ((unsigned long long)L.f_xdeg[p] << 32) | L.f_edeg[p];
   unsigned long long tot;
   unsigned long long q = d_before + gexcl64(c, s, &tot);
   for (uint64_t p = lo; p < hi; ++p) {
-    const uint32_t st = L.f_state[p];
-    const uint4 o0 = g.off[st], o1 = g.off[st + 1];
+    const unsigned long long d = ((unsigned long long)L.f_xdeg[p] << 32) | L.f_edeg[p];
     L.f_edeg[p] = (uint32_t)q;
     L.f_xdeg[p] = (uint32_t)(q >> 32);
-    L.f_ebeg[p] = o0.x;
-    L.f_xbeg[p] = o0.y;
-    L.f_cls[p] = g.sclass[st];
-    q += ((unsigned long long)(o1.y - o0.y) << 32) | (o1.x - o0.x);
+    q += d;
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     const unsigned long long all = d_all;
@@ -1033,14 +1032,22 @@ __global__ void __launch_bounds__(kGT) k_g_link_count(DevGraph g, const LaneDesc
   if (threadIdx.x == 0) G.part[2][blockIdx.x] = c;
 }
 
-// Writes the links in item order: per 256-item tile a workgroup scan of the
-// (emitting, epsilon) flags.  Sets the predecessor node of each token from
-// the link that produced it (same cost key and arc id).
+// Writes the links in item order.  Items go kLinkBatch tiles of 256 at a time:
+// every item's candidate or epsilon arc is read first, the tiles' (emitting,
+// epsilon) flags are counted by wavefront ballots and one workgroup barrier,
+// then the destinations' node ids and tokens are looked up for all items of
+// the batch before the stores, so a thread has several independent chains of
+// loads in flight instead of one per tile behind a workgroup scan.  Sets the
+// predecessor node of each token from the link that produced it (same cost
+// key and arc id).
+constexpr uint32_t kLinkBatch = 4;
+
 __global__ void __launch_bounds__(kGT) k_g_link_write(DevGraph g, const LaneDesc* __restrict__ lanes,
                                                       GridLane* gl, int t) {
   __shared__ GScratch s;
   __shared__ uint32_t seg[kSeg];
   __shared__ uint32_t rng[2];
+  __shared__ uint32_t wc[2][kLinkBatch][kGW][2];  // (batch parity, tile, wavefront): (emitting, epsilon) flags
   const LaneDesc& L = lanes[blockIdx.y];
   GridLane& G = gl[blockIdx.y];
   if (G.stop) return;
@@ -1054,33 +1061,75 @@ __global__ void __launch_bounds__(kGT) k_g_link_write(DevGraph g, const LaneDesc
   chunk((uint64_t)W + G.W_eps, blockIdx.x, &blo, &bhi);
   if (blo >= bhi) return;
   const Seg sg = link_seg(L, W, n, blo, bhi, seg, rng);
-  uint32_t xm = 0, bad = 0;
-  for (uint64_t base = blo; base < bhi; base += kGT) {
-    const uint64_t it = base + threadIdx.x;
-    LinkItem o;
-    const bool on = it < bhi && link_item(g, L, W, cut, (uint32_t)it, sg, seg, &o);
-    const unsigned long long f = on ? (it < W ? 1ull : (1ull << 32)) : 0ull;
-    unsigned long long tile;
-    const unsigned long long ex = run + gexcl64(f, s, &tile);
-    run += tile;
-    if (!on) continue;
-    const uint32_t dn = L.idx[o.dst];
-    const uint32_t q = dn - (uint32_t)nb;
-    if ((uint64_t)dn < nb || q >= n) {
-      bad = 1;
-      continue;
+  uint32_t xm = 0, bad = 0, par = 0;
+  uint32_t run_e = (uint32_t)run, run_x = (uint32_t)(run >> 32);
+  for (uint64_t base = blo; base < bhi; base += kLinkBatch * kGT) {
+    LinkItem o[kLinkBatch];
+    bool on[kLinkBatch];
+    uint64_t be[kLinkBatch], bx[kLinkBatch];
+#pragma unroll
+    for (uint32_t k = 0; k < kLinkBatch; ++k) {
+      const uint64_t it = base + k * kGT + threadIdx.x;
+      on[k] = it < bhi && link_item(g, L, W, cut, (uint32_t)it, sg, seg, &o[k]);
+      be[k] = __ballot(on[k] && it < W);
+      bx[k] = __ballot(on[k] && it >= W);
+      if (lane_id() == 0) {
+        wc[par][k][wave_id()][0] = (uint32_t)__popcll(be[k]);
+        wc[par][k][wave_id()][1] = (uint32_t)__popcll(bx[k]);
+      }
     }
-    const uint32_t xk = cost_key(__uint_as_float(o.xbits));
-    if (it < W) {
-      L.links[lb + (uint32_t)ex] = make_uint4(o.arc, o.src, dn, o.xbits);
-      if (L.f_key[q] == xk && L.f_arc[q] == o.arc) L.n_pred[dn] = o.src;
-    } else {
-      const uint64_t at = lb + nE + (ex >> 32);
-      const uint32_t sn = (uint32_t)(nb + o.src);
-      L.links[at] = make_uint4(o.arc, sn, dn, o.xbits);
-      L.link_lvl[at] = (uint8_t)o.lvl;
-      xm |= 1u << (o.lvl < 31u ? o.lvl : 31u);
-      if (L.f_key[q] == xk && L.f_arc[q] == o.arc) L.n_pred[dn] = sn;
+    __syncthreads();  // (two count buffers: one barrier per batch)
+    uint32_t pe[kLinkBatch], px[kLinkBatch], te = 0, tx = 0;
+#pragma unroll
+    for (uint32_t k = 0; k < kLinkBatch; ++k) {
+      uint32_t ae = 0, ax = 0, se = 0, sx = 0;
+#pragma unroll
+      for (uint32_t i = 0; i < (uint32_t)kGW; ++i) {
+        const uint32_t ce = wc[par][k][i][0], cx = wc[par][k][i][1];
+        se += ce;
+        sx += cx;
+        ae += i < wave_id() ? ce : 0u;
+        ax += i < wave_id() ? cx : 0u;
+      }
+      pe[k] = run_e + te + ae + rank_in(be[k]);
+      px[k] = run_x + tx + ax + rank_in(bx[k]);
+      te += se;
+      tx += sx;
+    }
+    run_e += te;
+    run_x += tx;
+    par ^= 1u;
+    uint32_t dn[kLinkBatch];
+#pragma unroll
+    for (uint32_t k = 0; k < kLinkBatch; ++k) dn[k] = on[k] ? L.idx[o[k].dst] : 0u;
+    uint32_t fk[kLinkBatch], fa[kLinkBatch];
+#pragma unroll
+    for (uint32_t k = 0; k < kLinkBatch; ++k) {
+      const uint32_t q = dn[k] - (uint32_t)nb;
+      const bool ok = (uint64_t)dn[k] >= nb && q < n;
+      if (on[k] && !ok) {
+        bad = 1;
+        on[k] = false;
+      }
+      fk[k] = on[k] ? L.f_key[q] : 0u;
+      fa[k] = on[k] ? L.f_arc[q] : 0u;
+    }
+#pragma unroll
+    for (uint32_t k = 0; k < kLinkBatch; ++k) {
+      if (!on[k]) continue;
+      const uint64_t it = base + k * kGT + threadIdx.x;
+      const bool pred = fk[k] == cost_key(__uint_as_float(o[k].xbits)) && fa[k] == o[k].arc;
+      if (it < W) {
+        L.links[lb + pe[k]] = make_uint4(o[k].arc, o[k].src, dn[k], o[k].xbits);
+        if (pred) L.n_pred[dn[k]] = o[k].src;
+      } else {
+        const uint64_t at = lb + nE + px[k];
+        const uint32_t sn = (uint32_t)(nb + o[k].src);
+        L.links[at] = make_uint4(o[k].arc, sn, dn[k], o[k].xbits);
+        L.link_lvl[at] = (uint8_t)o[k].lvl;
+        xm |= 1u << (o[k].lvl < 31u ? o[k].lvl : 31u);
+        if (pred) L.n_pred[dn[k]] = sn;
+      }
     }
   }
   if (xm) atomicOr(&G.xmask, xm);
