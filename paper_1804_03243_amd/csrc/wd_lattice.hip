@@ -23,6 +23,14 @@ constexpr int kLW = kLT / 64;
 // Two-frame window of per-node values (frame t and t+1, or t-1 and t): extra
 // costs and costs during the pruning sweep, alpha or beta during the
 // posteriors.  Frames with more nodes use the workspace arrays directly.
+// Small kept lattices (the usual case at a narrow lattice beam: a few kept
+// links per frame) run their forward-backward sums entirely in LDS over the
+// nodes the kept links touch, renumbered 0..K-1 (compact posteriors below).
+constexpr uint32_t kCpNodes = 3584;   // touched nodes
+constexpr uint32_t kCpLinks = 2560;   // kept links
+constexpr uint32_t kCpFrames = 2048;  // frames + 1
+constexpr uint32_t kCpWords = 2 * kCpNodes;  // node bitmap words (the bitmap in a, word ranks in b)
+
 struct LatShared {
   BlockScratch bs;
   union {
@@ -34,6 +42,16 @@ struct LatShared {
       double a[2][kWin];  // alpha (wavefront 0)
       double b[2][kWin];  // beta (wavefront 1, concurrently)
     } ab;
+    struct {
+      // alpha and beta sums of the touched nodes; before them, the bitmap of
+      // touched node ids (in a) and each bitmap word's rank (in b)
+      double a[kCpNodes];
+      double b[kCpNodes];
+      uint4 link[kCpLinks];         // kept link records, source and destination renumbered
+      uint32_t node[kCpNodes];      // node id of each compact number
+      uint16_t kf[2 * kCpFrames];   // per-frame kept-link boundaries
+      uint32_t lmask[kCpFrames];    // source levels of each frame's kept epsilon links
+    } cp;
   } w;
 };
 
@@ -722,6 +740,144 @@ __device__ __forceinline__ void beta_wave(const LaneDesc& L, const DevGraph& g, 
   }
 }
 
+// Compact posteriors.  The nodes that kept links touch (and the start node)
+// are numbered in node id order through a bitmap in LDS; the kept link
+// records, the per-frame kept-link boundaries and each frame's kept epsilon
+// levels are copied into LDS with those numbers; then wavefront 0 runs the
+// alpha sums and wavefront 1 the beta sums frame by frame exactly as the
+// windowed passes do (emitting links, then epsilon links by source level),
+// with every value they read already in LDS.  A node's sums are only ever
+// added to by links in its own frame's step, so starting every node at 0 (the
+// start node at its alpha seed, the last frame's nodes at their final beta)
+// equals the per-frame initialisation.  At the end the touched nodes' sums
+// go to the workspace arrays, where the merge reads them.  Returns false
+// (before touching anything the other path needs) when the lattice does not
+// fit.  Whole workgroup.
+__device__ __forceinline__ bool compact_fits(const LaneDesc& L, const DevGraph& g, uint64_t n_kept, uint64_t nnodes) {
+  return n_kept <= kCpLinks && (uint64_t)L.T + 2 <= kCpFrames && ((nnodes + 31) >> 5) <= kCpWords &&
+         g.nlevels <= 32;
+}
+
+__device__ __forceinline__ bool posteriors_compact(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t tid,
+                                                   uint32_t& par, uint64_t n_kept, uint64_t nnodes,
+                                                   uint64_t start_node, bool final_used, float best_total) {
+  const int T = L.T;
+  uint32_t* bits = reinterpret_cast<uint32_t*>(sh.w.cp.a);
+  uint32_t* rank = reinterpret_cast<uint32_t*>(sh.w.cp.b);
+  const uint32_t nwd = (uint32_t)((nnodes + 31) >> 5);
+  for (uint32_t w = tid; w < nwd; w += kLT) bits[w] = 0;
+  __syncthreads();
+  for (uint64_t j = tid; j < n_kept; j += kLT) {
+    const uint4 r = L.post[j];
+    atomicOr(&bits[r.x >> 5], 1u << (r.x & 31u));
+    atomicOr(&bits[r.y >> 5], 1u << (r.y & 31u));
+  }
+  if (tid == 0) atomicOr(&bits[start_node >> 5], 1u << (start_node & 31u));
+  __syncthreads();
+  // word ranks: a contiguous range of words per thread
+  const uint32_t per = (nwd + kLT - 1) / kLT;
+  const uint32_t w0 = tid * per < nwd ? tid * per : nwd;
+  const uint32_t w1 = w0 + per < nwd ? w0 + per : nwd;
+  uint64_t cnt = 0;
+  for (uint32_t w = w0; w < w1; ++w) cnt += (uint32_t)__popc(bits[w]);
+  uint64_t K;
+  uint32_t r = (uint32_t)block_excl_scan64<kLW>(cnt, sh.bs, par, &K);
+  if (K > kCpNodes) return false;  // (uniform)
+  for (uint32_t w = w0; w < w1; ++w) {
+    rank[w] = r;
+    uint32_t word = bits[w];
+    while (word) {
+      const uint32_t b = (uint32_t)__ffs(word) - 1u;
+      word &= word - 1u;
+      sh.w.cp.node[r++] = (w << 5) | b;
+    }
+  }
+  __syncthreads();
+  auto cid = [&](uint32_t n) -> uint32_t {
+    return rank[n >> 5] + (uint32_t)__popc(bits[n >> 5] & ((1u << (n & 31u)) - 1u));
+  };
+  for (uint64_t j = tid; j < n_kept; j += kLT) {
+    const uint4 l = L.post[j];
+    sh.w.cp.link[j] = make_uint4(cid(l.x), cid(l.y), l.z, l.w);
+  }
+  const uint64_t* kf = L.kframe;
+  for (uint32_t i = tid; i < 2u * (uint32_t)(T + 2); i += kLT) sh.w.cp.kf[i] = (uint16_t)kf[i];
+  for (int t = (int)tid; t <= T; t += kLT) {
+    uint32_t m = 0;
+    for (uint64_t j = kf[2 * t + 1]; j < kf[2 * t + 2]; ++j) m |= 1u << rec_level(L.post[j]);
+    sh.w.cp.lmask[t] = m;
+  }
+  const uint32_t cstart = tid == 0 ? cid((uint32_t)start_node) : 0u;
+  __syncthreads();  // every renumbering read of the bitmap is done
+  const uint64_t nT = L.node_off[T];
+  const double s_start = exp((double)L.best[0]);
+  const double ref_T = (double)best_total - (double)L.best[T];  // B - b(T)
+  for (uint32_t c = tid; c < (uint32_t)K; c += kLT) {
+    const uint32_t n = sh.w.cp.node[c];
+    sh.w.cp.a[c] = 0.0;
+    double b = 0.0;
+    if (n >= nT) b = exp(ref_T - (final_used ? (double)g.final_w[L.n_state[n]] : 0.0));
+    sh.w.cp.b[c] = b;
+  }
+  __syncthreads();
+  if (tid == 0) sh.w.cp.a[cstart] = s_start;
+  __syncthreads();
+  const uint4* lk = sh.w.cp.link;
+  const uint16_t* kfs = sh.w.cp.kf;
+  if (tid < 64) {
+    // alpha, frames ascending; epsilon links from the lowest source level
+    double* a = sh.w.cp.a;
+    for (int t = 0; t <= T; ++t) {
+      const uint32_t e0 = kfs[2 * t], x0 = kfs[2 * t + 1], x1 = kfs[2 * t + 2];
+      for (uint32_t j = e0 + tid; j < x0; j += 64) {
+        const uint4 l = lk[j];
+        mass_add(&a[l.y], a[l.x] * rec_factor(l), true);
+      }
+      wave_sync();
+      uint32_t m = sh.w.cp.lmask[t];
+      while (m) {
+        const uint32_t lvl = (uint32_t)__ffs(m) - 1u;
+        m &= m - 1u;
+        for (uint32_t j = x0 + tid; j < x1; j += 64) {
+          const uint4 l = lk[j];
+          if (rec_level(l) == lvl) mass_add(&a[l.y], a[l.x] * rec_factor(l), true);
+        }
+        wave_sync();
+      }
+    }
+  } else if (tid < 128) {
+    // beta, frames descending; epsilon links from the highest source level
+    const uint32_t lane = tid - 64;
+    double* b = sh.w.cp.b;
+    for (int t = T; t >= 0; --t) {
+      const uint32_t x0 = kfs[2 * t + 1], x1 = kfs[2 * t + 2];
+      const uint32_t e1 = t < T ? kfs[2 * t + 3] : x1;  // emitting links out of t (into t+1)
+      for (uint32_t j = x1 + lane; j < e1; j += 64) {
+        const uint4 l = lk[j];
+        mass_add(&b[l.x], rec_factor(l) * b[l.y], true);
+      }
+      wave_sync();
+      uint32_t m = sh.w.cp.lmask[t];
+      while (m) {
+        const uint32_t lvl = 31u - (uint32_t)__clz(m);
+        m &= ~(1u << lvl);
+        for (uint32_t j = x0 + lane; j < x1; j += 64) {
+          const uint4 l = lk[j];
+          if (rec_level(l) == lvl) mass_add(&b[l.x], rec_factor(l) * b[l.y], true);
+        }
+        wave_sync();
+      }
+    }
+  }
+  __syncthreads();
+  for (uint32_t c = tid; c < (uint32_t)K; c += kLT) {
+    const uint32_t n = sh.w.cp.node[c];
+    L.alpha[n] = sh.w.cp.a[c];
+    L.beta[n] = sh.w.cp.b[c];
+  }
+  return true;
+}
+
 // blockIdx.y == 0: pruning, posteriors and the final merge; blockIdx.y == 1:
 // the 1-best traceback (a serial walk over predecessor pointers, run
 // concurrently by its own workgroup).
@@ -919,7 +1075,11 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   // concurrently; large ones (more than 64 kept links per frame on average):
   // the whole workgroup, alpha then beta, or in chip-wide mode alpha here and
   // beta on the utterance's third workgroup at the same time
-  if (!wide) {
+  if (!wide && !swept && compact_fits(L, g, n_kept, nnodes) &&
+      posteriors_compact(L, g, sh, tid, par, n_kept, nnodes, start_node, final_used, best_total)) {
+    // (done in LDS)
+  } else if (!wide) {
+    __syncthreads();  // (a compact attempt that did not fit has used the LDS)
     if (tid < 64) alpha_wave<64>(L, g, sh, tid, swept, start_node);
     else if (tid < 128) beta_wave<64>(L, g, sh, tid - 64, swept, final_used, best_total);
   } else {
