@@ -30,6 +30,8 @@ constexpr uint32_t kCpNodes = 3584;   // touched nodes
 constexpr uint32_t kCpLinks = 2560;   // kept links
 constexpr uint32_t kCpFrames = 2048;  // frames + 1
 constexpr uint32_t kCpWords = 2 * kCpNodes;  // node bitmap words (the bitmap in a, word ranks in b)
+// Frames (+ 1) whose offsets the final merge and the node list read from LDS.
+constexpr uint32_t kMgFrames = 2048;
 
 struct LatShared {
   BlockScratch bs;
@@ -52,6 +54,11 @@ struct LatShared {
       uint16_t kf[2 * kCpFrames];   // per-frame kept-link boundaries
       uint32_t lmask[kCpFrames];    // source levels of each frame's kept epsilon links
     } cp;
+    struct {
+      // per-frame offsets for the final merge and the node list
+      uint64_t node_off[kMgFrames], link_off[kMgFrames], link_xoff[kMgFrames];
+      uint64_t kf[2 * kMgFrames];
+    } mg;
   } w;
 };
 
@@ -126,21 +133,23 @@ __device__ __forceinline__ double link_ac(const LaneDesc& L, const DevGraph& g, 
 // plus the number of links of the other run with a smaller arc id.  The runs'
 // bounds in selection order are the frame's link offsets (all links) or the
 // per-frame kept-link boundaries kf.
+// lo, xo, kf: the frame offsets (link_off, link_xoff, kframe), in LDS or
+// device memory.
 __device__ __forceinline__ void assemble(const LaneDesc& L, const DevGraph& g, bool all, uint64_t n_sel,
                          OutLink* out, uint32_t lb_key, double norm, bool with_post, bool mark_nodes,
-                         uint64_t first, uint64_t stride) {
+                         uint64_t first, uint64_t stride, const uint64_t* lo_off, const uint64_t* xo_off,
+                         const uint64_t* kf) {
   const int T = L.T;
   const uint64_t* kid = L.kept_idx;
-  const uint64_t* kf = L.kframe;
   auto sel = [&](uint64_t j) -> uint64_t { return all ? j : kid[j]; };
   for (uint64_t j = first; j < n_sel; j += stride) {
     const uint64_t k = sel(j);
-    const int t = (int)search_le64(L.link_off, (uint64_t)T + 2, k);
-    const uint64_t xo = L.link_xoff[t];
+    const int t = (int)search_le64(lo_off, (uint64_t)T + 2, k);
+    const uint64_t xo = xo_off[t];
     const bool eps = k >= xo;
-    const uint64_t s0 = all ? L.link_off[t] : kf[2 * t];
+    const uint64_t s0 = all ? lo_off[t] : kf[2 * t];
     const uint64_t sx = all ? xo : kf[2 * t + 1];
-    const uint64_t s1 = all ? L.link_off[t + 1] : kf[2 * t + 2];
+    const uint64_t s1 = all ? lo_off[t + 1] : kf[2 * t + 2];
     const LinkView l = link_at(L, k);
     // the other run [o0, o1) in selection order
     const uint64_t o0 = eps ? s0 : sx, o1 = eps ? sx : s1;
@@ -181,7 +190,8 @@ __device__ __forceinline__ void assemble(const LaneDesc& L, const DevGraph& g, b
 
 // Lattice nodes (those marked in the used bitmap) in (t, state) order, which
 // is node id order; returns their number.  Whole workgroup.
-__device__ __forceinline__ uint64_t write_nodes(const LaneDesc& L, uint64_t nnodes, BlockScratch& bs, uint32_t& par) {
+__device__ __forceinline__ uint64_t write_nodes(const LaneDesc& L, uint64_t nnodes, BlockScratch& bs, uint32_t& par,
+                                                const uint64_t* no) {
   const uint32_t tid = threadIdx.x;
   const uint64_t nwd = (nnodes + 31) >> 5;
   const uint64_t per = (nwd + kLT - 1) / kLT;
@@ -206,8 +216,8 @@ __device__ __forceinline__ uint64_t write_nodes(const LaneDesc& L, uint64_t nnod
       const uint32_t b = (uint32_t)__ffs(word) - 1u;
       word &= word - 1u;
       const uint64_t n = (w << 5) | b;
-      if (t < 0) t = (int)search_le64(L.node_off, (uint64_t)L.T + 2, n);
-      while (L.node_off[t + 1] <= n) ++t;
+      if (t < 0) t = (int)search_le64(no, (uint64_t)L.T + 2, n);
+      while (no[t + 1] <= n) ++t;
       OutNode o;
       o.t = (int32_t)t;
       o.state = (int32_t)L.n_state[n];
@@ -997,30 +1007,45 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   const uint32_t lb_key = cost_key(prm.lattice_beam);
   uint64_t n_kept = info->kept;  // counted and listed by the chip-wide kernels when swept
   if (!swept) {
-    // a contiguous range of links per thread, read kBatchK at a time so that
-    // the loads of a batch are in flight together
-    constexpr int kBatchK = 8;
-    const uint64_t per = (nlinks + kLT - 1) / kLT;
+    // a contiguous range of links per thread (a multiple of four, so that
+    // whole 16-byte groups of extra-cost keys are read at once), kBatchK
+    // groups in flight together
+    constexpr int kBatchK = 4;
+    const uint64_t per = (((nlinks + kLT - 1) / kLT) + 3) & ~(uint64_t)3;
     const uint64_t k0 = tid * per < nlinks ? tid * per : nlinks;
     const uint64_t k1 = k0 + per < nlinks ? k0 + per : nlinks;
+    // end of the whole groups (none when the lane's key array is not 16-byte aligned)
+    const bool al = ((uintptr_t)L.le_key & 15u) == 0;
+    const uint64_t k4 = al ? k0 + ((k1 - k0) & ~(uint64_t)3) : k0;
+    const uint4* le4 = reinterpret_cast<const uint4*>(L.le_key);
+    auto in = [&](uint32_t le) -> uint32_t { return le <= lb_key && le < kInfKey ? 1u : 0u; };
     uint64_t cnt = 0;
-    for (uint64_t kb = k0; kb < k1; kb += kBatchK) {
-      uint32_t le[kBatchK];
+    for (uint64_t kb = k0; kb < k4; kb += 4 * kBatchK) {
+      uint4 v[kBatchK];
 #pragma unroll
-      for (int u = 0; u < kBatchK; ++u) le[u] = kb + u < k1 ? L.le_key[kb + u] : kInfKey;
+      for (int u = 0; u < kBatchK; ++u) v[u] = kb + 4 * u < k4 ? le4[(kb >> 2) + u] : make_uint4(kInfKey, kInfKey, kInfKey, kInfKey);
 #pragma unroll
-      for (int u = 0; u < kBatchK; ++u) cnt += le[u] <= lb_key && le[u] < kInfKey;
+      for (int u = 0; u < kBatchK; ++u) cnt += in(v[u].x) + in(v[u].y) + in(v[u].z) + in(v[u].w);
     }
+    for (uint64_t k = k4; k < k1; ++k) cnt += in(L.le_key[k]);
     uint64_t pos = block_excl_scan64<kLW>(cnt, sh.bs, par, &n_kept);
-    if (n_kept <= L.kept_cap && cnt)
-      for (uint64_t kb = k0; kb < k1; kb += kBatchK) {
-        uint32_t le[kBatchK];
+    if (n_kept <= L.kept_cap && cnt) {
+      for (uint64_t kb = k0; kb < k4; kb += 4 * kBatchK) {
+        uint4 v[kBatchK];
 #pragma unroll
-        for (int u = 0; u < kBatchK; ++u) le[u] = kb + u < k1 ? L.le_key[kb + u] : kInfKey;
+        for (int u = 0; u < kBatchK; ++u) v[u] = kb + 4 * u < k4 ? le4[(kb >> 2) + u] : make_uint4(kInfKey, kInfKey, kInfKey, kInfKey);
 #pragma unroll
-        for (int u = 0; u < kBatchK; ++u)
-          if (le[u] <= lb_key && le[u] < kInfKey) L.kept_idx[pos++] = kb + u;
+        for (int u = 0; u < kBatchK; ++u) {
+          const uint64_t k = kb + 4 * u;
+          if (in(v[u].x)) L.kept_idx[pos++] = k;
+          if (in(v[u].y)) L.kept_idx[pos++] = k + 1;
+          if (in(v[u].z)) L.kept_idx[pos++] = k + 2;
+          if (in(v[u].w)) L.kept_idx[pos++] = k + 3;
+        }
       }
+      for (uint64_t k = k4; k < k1; ++k)
+        if (in(L.le_key[k])) L.kept_idx[pos++] = k;
+    }
   }
   const bool debug = (prm.flags & 1u) != 0;
   if (n_kept > L.kept_cap || (debug && nlinks > L.raw_cap)) {
@@ -1108,11 +1133,28 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
   if (swept) return;  // the merge and the node list run as chip-wide kernels
 
   // ------------------------------------------- final merge of the kept links
-  assemble(L, g, false, n_kept, L.out_links, lb_key, norm, true, true, tid, kLT);
-  if (debug) assemble(L, g, true, nlinks, L.out_raw, lb_key, norm, true, false, tid, kLT);
+  // (the frame offsets copied to LDS when they fit: each link's and node's
+  // frame is found by a binary search over them)
+  const uint64_t *lo_off = L.link_off, *xo_off = L.link_xoff, *kfo = L.kframe, *no = L.node_off;
+  if ((uint64_t)T + 2 <= kMgFrames) {
+    for (uint32_t i = tid; i < (uint32_t)(T + 2); i += kLT) {
+      sh.w.mg.node_off[i] = L.node_off[i];
+      sh.w.mg.link_off[i] = L.link_off[i];
+      sh.w.mg.link_xoff[i] = L.link_xoff[i];
+      sh.w.mg.kf[2 * i] = L.kframe[2 * i];
+      sh.w.mg.kf[2 * i + 1] = L.kframe[2 * i + 1];
+    }
+    __syncthreads();
+    lo_off = sh.w.mg.link_off;
+    xo_off = sh.w.mg.link_xoff;
+    kfo = sh.w.mg.kf;
+    no = sh.w.mg.node_off;
+  }
+  assemble(L, g, false, n_kept, L.out_links, lb_key, norm, true, true, tid, kLT, lo_off, xo_off, kfo);
+  if (debug) assemble(L, g, true, nlinks, L.out_raw, lb_key, norm, true, false, tid, kLT, lo_off, xo_off, kfo);
   __syncthreads();
   lstamp(6);
-  const uint64_t n_out = write_nodes(L, nnodes, sh.bs, par);
+  const uint64_t n_out = write_nodes(L, nnodes, sh.bs, par, no);
   if (tid == 0) info->out_nodes = n_out;
   if (L.prof) {
     __syncthreads();
@@ -1130,9 +1172,11 @@ __global__ void __launch_bounds__(256) k_lat_assemble(DevGraph g, const LaneDesc
   const uint64_t first = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
   const double norm = post_norm(L, info->start_node);
-  assemble(L, g, false, info->kept, L.out_links, lb_key, norm, true, true, first, stride);
+  assemble(L, g, false, info->kept, L.out_links, lb_key, norm, true, true, first, stride, L.link_off, L.link_xoff,
+           L.kframe);
   if (prm.flags & 1u)
-    assemble(L, g, true, L.link_off[L.T + 1], L.out_raw, lb_key, norm, true, false, first, stride);
+    assemble(L, g, true, L.link_off[L.T + 1], L.out_raw, lb_key, norm, true, false, first, stride, L.link_off,
+             L.link_xoff, L.kframe);
 }
 
 void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s) {
