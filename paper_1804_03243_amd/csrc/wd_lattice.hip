@@ -32,6 +32,13 @@ constexpr uint32_t kCpFrames = 2048;  // frames + 1
 constexpr uint32_t kCpWords = 2 * kCpNodes;  // node bitmap words (the bitmap in a, word ranks in b)
 // Frames (+ 1) whose offsets the final merge and the node list read from LDS.
 constexpr uint32_t kMgFrames = 2048;
+// Staged pruning sweep: blocks of up to kSwK frames; rings of kSwRing links
+// and nodes in LDS hold four blocks (one written back, one swept, one
+// loaded, one loading), so a block may hold at most kSwRing / 4 of each.
+constexpr int kSwK = 4;
+constexpr uint32_t kSwRing = 4096;
+constexpr uint32_t kSwCap = kSwRing / 4;
+constexpr int kSwFrames = 4 * kSwK;  // per-frame table entries (a ring of frames)
 
 struct LatShared {
   BlockScratch bs;
@@ -54,6 +61,19 @@ struct LatShared {
       uint16_t kf[2 * kCpFrames];   // per-frame kept-link boundaries
       uint32_t lmask[kCpFrames];    // source levels of each frame's kept epsilon links
     } cp;
+    struct {
+      uint32_t sd[kSwRing];      // link: source | destination << 16, both as node ring positions
+      float dl[kSwRing];         // link: forward cost minus its destination's cost
+      uint8_t lvl[kSwRing];      // link: source level (epsilon links)
+      uint32_t ex[kSwRing];      // node: extra-cost key
+      uint32_t fm[kSwFrames];    // frame: source levels of its epsilon links
+      // per frame u (u <= T; relative to frame 0's first epsilon link and first
+      // node): first epsilon link, first emitting link out of it, one past its
+      // last link, first node (u = T + 1: one past the last)
+      uint32_t ox[kMgFrames], oe[kMgFrames], oz[kMgFrames], on[kMgFrames];
+      int32_t top[kMgFrames];    // block b's highest frame (then -1)
+      int32_t nblk;              // blocks (-1: a frame does not fit)
+    } sw;
     struct {
       // per-frame offsets for the final merge and the node list
       uint64_t node_off[kMgFrames], link_off[kMgFrames], link_xoff[kMgFrames];
@@ -442,6 +462,149 @@ __device__ __forceinline__ void sweep_step(const LaneDesc& L, const DevGraph& g,
     if (t > 0) sweep_init(L, g, sh, t - 1, sn, tid - 64, kLT - 64, final_used, best_total, cur.c);
   }
   __syncthreads();
+}
+
+// Staged pruning sweep.  Frames are cut, from the last one down, into blocks
+// of at most kSwK frames and kSwCap links and nodes.  The same relaxations
+// as sweep_step, in the same order within each frame, but wavefront 0 walks
+// the frames of a block with every operand already in LDS (links, node costs
+// and extra costs in rings indexed by link and node id), its only global
+// accesses the stores of the links' extra costs; meanwhile the other
+// wavefronts load the block after next into the rings and write the block
+// before back.  One workgroup barrier per block instead of two per frame.
+// Returns false, before touching anything the other sweep needs, when a
+// frame alone does not fit or the utterance is too long.  Whole workgroup.
+__device__ __forceinline__ bool sweep_staged(const LaneDesc& L, const DevGraph& g, LatShared& sh, uint32_t tid,
+                                             uint32_t& par, bool final_used, float best_total) {
+  const int T = L.T;
+  if ((uint64_t)T + 2 > kMgFrames) return false;
+  // the frames' offsets, relative, into LDS
+  const uint64_t kb = L.link_xoff[0], nb = L.node_off[0];
+  for (int u = (int)tid; u <= T + 1; u += kLT) {
+    if (u <= T) {
+      sh.w.sw.ox[u] = (uint32_t)(L.link_xoff[u] - kb);
+      sh.w.sw.oe[u] = (uint32_t)(L.link_off[u + 1] - kb);
+      // one past frame u's last link: its emitting links run to the next
+      // frame's epsilon run; the last frame has none
+      sh.w.sw.oz[u] = (uint32_t)((u < T ? L.link_xoff[u + 1] : L.link_off[T + 1]) - kb);
+    }
+    sh.w.sw.on[u] = (uint32_t)(L.node_off[u] - nb);
+  }
+  __syncthreads();
+  // blocks from the last frame down, cut greedily by one thread
+  if (tid == 0) {
+    int nblk = 0, u = T;
+    bool fits = true;
+    while (u >= 0 && fits) {
+      const int hi = u;
+      sh.w.sw.top[nblk++] = hi;
+      while (u >= 0 && hi - u < kSwK && sh.w.sw.oz[hi] - sh.w.sw.ox[u] <= kSwCap &&
+             sh.w.sw.on[hi + 1] - sh.w.sw.on[u] <= kSwCap)
+        --u;
+      fits = u < hi;  // the block holds at least its first frame
+    }
+    sh.w.sw.top[nblk] = -1;
+    sh.w.sw.nblk = fits ? nblk : -1;
+  }
+  __syncthreads();
+  const int nblk = sh.w.sw.nblk;
+  if (nblk < 0) return false;
+  auto hi_of = [&](int b) { return sh.w.sw.top[b]; };
+  auto lo_of = [&](int b) { return sh.w.sw.top[b + 1] + 1; };
+  constexpr uint32_t kM = kSwRing - 1;
+  // block b into the rings (by the threads first, first + stride, ...)
+  auto load = [&](int b, uint32_t first, uint32_t stride) {
+    const int hi = hi_of(b), lo = lo_of(b);
+    for (int u = lo + (int)first; u <= hi; u += (int)stride) sh.w.sw.fm[u % kSwFrames] = L.xmask[u];
+    const uint64_t k0 = kb + sh.w.sw.ox[lo], k1 = kb + sh.w.sw.oz[hi];
+    for (uint64_t k = k0 + first; k < k1; k += stride) {
+      const uint4 v = L.links[k];
+      const uint32_t r = (uint32_t)k & kM;
+      sh.w.sw.sd[r] = (v.y & kM) | ((v.z & kM) << 16);
+      sh.w.sw.dl[r] = __uint_as_float(v.w) - node_cost(L, v.z);
+      sh.w.sw.lvl[r] = L.link_lvl[k];
+    }
+    const uint64_t n0 = nb + sh.w.sw.on[lo], n1 = nb + sh.w.sw.on[hi + 1], nT = nb + sh.w.sw.on[T];
+    for (uint64_t n = n0 + first; n < n1; n += stride) {
+      const float c = node_cost(L, n);
+      uint32_t e = kInfKey;
+      if (n >= nT) {
+        const float F = final_used ? canon(c + g.final_w[L.n_state[n]]) : c;
+        if (F < INFINITY) e = cost_key(F - best_total);
+      }
+      sh.w.sw.ex[(uint32_t)n & kM] = e;
+    }
+  };
+  auto writeback = [&](int b, uint32_t first, uint32_t stride) {
+    const uint64_t n0 = nb + sh.w.sw.on[lo_of(b)], n1 = nb + sh.w.sw.on[hi_of(b) + 1];
+    for (uint64_t n = n0 + first; n < n1; n += stride) L.extra_key[n] = sh.w.sw.ex[(uint32_t)n & kM];
+  };
+  // link k (ring record sd, dl) relaxed into its source's extra cost (the
+  // key array's address held in a register: a store through the lane
+  // descriptor's field would make the compiler reload the field after every
+  // store)
+  uint32_t* const __restrict__ lek = L.le_key;
+  auto relax_sd = [&](uint64_t k, uint32_t sd, float dl) {
+    const uint32_t le = cost_key(key_cost(sh.w.sw.ex[sd >> 16]) + dl);
+    lek[k] = le;
+    atomicMin(&sh.w.sw.ex[sd & 0xffffu], le);
+  };
+  auto relax = [&](uint64_t k) {
+    const uint32_t r = (uint32_t)k & kM;
+    relax_sd(k, sh.w.sw.sd[r], sh.w.sw.dl[r]);
+  };
+  // levels present in a frame, one bit each (deeper graphs fold levels from
+  // 31 up into bit 31 and take the per-level loop)
+  const bool bitwise_levels = g.nlevels <= 31;
+  load(0, tid, kLT);
+  if (nblk > 1) load(1, tid, kLT);
+  __syncthreads();
+  for (int b = 0; b < nblk; ++b) {
+    if (tid < 64) {
+      for (int u = hi_of(b); u >= lo_of(b); --u) {
+        const uint64_t x0 = kb + sh.w.sw.ox[u], e0 = kb + sh.w.sw.oe[u], z = kb + sh.w.sw.oz[u];
+        const uint32_t mask = sh.w.sw.fm[u % kSwFrames];
+        // emitting links out of the frame (none out of the last one)
+        if (u < T) {
+          for (uint64_t k = e0 + tid; k < z; k += 64) relax(k);
+          wave_sync();
+        }
+        // epsilon links, from the highest source level down: with at most one
+        // per lane, each lane's record is read once and kept for every level
+        if (bitwise_levels && e0 - x0 <= 64) {
+          const uint64_t k = x0 + tid;
+          const bool has = k < e0;
+          uint32_t sd = 0, lv = 0xffu;
+          float dl = 0.0f;
+          if (has) {
+            const uint32_t r = (uint32_t)k & kM;
+            sd = sh.w.sw.sd[r];
+            dl = sh.w.sw.dl[r];
+            lv = sh.w.sw.lvl[r];
+          }
+          for (uint32_t m = mask; m;) {
+            const uint32_t lvl = 31u - (uint32_t)__clz(m);
+            m &= ~(1u << lvl);
+            if (lv == lvl) relax_sd(k, sd, dl);
+            wave_sync();
+          }
+        } else {
+          for (int lvl = (int)g.nlevels - 1; lvl >= 0; --lvl) {
+            if (!level_present(mask, (uint32_t)lvl)) continue;
+            for (uint64_t k = x0 + tid; k < e0; k += 64)
+              if (sh.w.sw.lvl[(uint32_t)k & kM] == (uint8_t)lvl) relax(k);
+            wave_sync();
+          }
+        }
+      }
+    } else {
+      if (b + 2 < nblk) load(b + 2, tid - 64, kLT - 64);
+      if (b >= 1) writeback(b - 1, tid - 64, kLT - 64);
+    }
+    __syncthreads();
+  }
+  writeback(nblk - 1, tid, kLT);
+  return true;
 }
 
 // Backward extra-cost sweep over every frame: four sets of frame offsets and
@@ -999,7 +1162,7 @@ __global__ void __launch_bounds__(kLT) k_lattice(DevGraph g, const LaneDesc* __r
 
   // ------------------------------------------------ backward extra-cost sweep
   lstamp(1);
-  if (!swept) sweep_block(L, g, sh, tid, final_used, best_total);
+  if (!swept && !sweep_staged(L, g, sh, tid, par, final_used, best_total)) sweep_block(L, g, sh, tid, final_used, best_total);
   __syncthreads();
   lstamp(2);
 
