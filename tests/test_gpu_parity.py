@@ -123,6 +123,21 @@ def test_tiny_10k(wf, oracle_mod, tiny10k, beam, ma, lb, mode):
     invariants.check_all(g, L, beam, ma, lb, r)
 
 
+@pytest.mark.parametrize("mode", ["workgroup", "workgroup_levels", "chip"])
+@pytest.mark.parametrize("T", [1800, 2100])
+def test_long_utterance(wf, oracle_mod, tiny10k, T, mode):
+    """Utterances past the lattice pass's LDS limits: 1800 frames keep ~2.9k
+    lattice links (more than the LDS posteriors hold: their per-frame
+    windowed form runs, the staged sweep still fits), 2100 frames are longer
+    than its frame tables (the frame-by-frame sweep and the windowed
+    posteriors)."""
+    cfg, g, _, graph = tiny10k
+    L = synth.make_loglikes(dict(cfg, T=T))
+    r, o, _ = _run(wf, oracle_mod, g, L, cfg["P"], cfg["beam"], cfg["max_active"], cfg["lattice_beam"],
+                   graph=graph, case=f"tiny_10k T={T}", mode=mode)
+    assert o.stats["kept_links"] > 2560
+
+
 @pytest.mark.parametrize("mode", ["chip", "chip_noprune", "chip_dyn"])
 @pytest.mark.parametrize("beam,ma,lb", TINY_PARAMS)
 def test_incremental_prune(wf, oracle_mod, tiny10k, beam, ma, lb, mode):
