@@ -998,48 +998,93 @@ __device__ __forceinline__ bool posteriors_compact(const LaneDesc& L, const DevG
   const uint4* lk = sh.w.cp.link;
   const uint16_t* kfs = sh.w.cp.kf;
   if (tid < 64) {
-    // alpha, frames ascending; epsilon links from the lowest source level
+    // alpha, frames ascending; epsilon links from the lowest source level.
+    // A frame's boundaries, level mask and first emitting and epsilon records
+    // are read during the frame before (off the chain of adds).
     double* a = sh.w.cp.a;
+    const uint4 none = make_uint4(0, 0, 0, 0);
+    uint32_t e0 = kfs[0], x0 = kfs[1], x1 = kfs[2], m0 = sh.w.cp.lmask[0];
+    uint4 le = e0 + tid < x0 ? lk[e0 + tid] : none, lx = x0 + tid < x1 ? lk[x0 + tid] : none;
     for (int t = 0; t <= T; ++t) {
-      const uint32_t e0 = kfs[2 * t], x0 = kfs[2 * t + 1], x1 = kfs[2 * t + 2];
-      for (uint32_t j = e0 + tid; j < x0; j += 64) {
+      uint32_t ne0 = 0, nx0 = 0, nx1 = 0, nm = 0;
+      uint4 nle = none, nlx = none;
+      if (t < T) {
+        ne0 = kfs[2 * t + 2];
+        nx0 = kfs[2 * t + 3];
+        nx1 = kfs[2 * t + 4];
+        nm = sh.w.cp.lmask[t + 1];
+        if (ne0 + tid < nx0) nle = lk[ne0 + tid];
+        if (nx0 + tid < nx1) nlx = lk[nx0 + tid];
+      }
+      if (e0 + tid < x0) mass_add(&a[le.y], a[le.x] * rec_factor(le), true);
+      for (uint32_t j = e0 + tid + 64; j < x0; j += 64) {
         const uint4 l = lk[j];
         mass_add(&a[l.y], a[l.x] * rec_factor(l), true);
       }
       wave_sync();
-      uint32_t m = sh.w.cp.lmask[t];
-      while (m) {
+      for (uint32_t m = m0; m;) {
         const uint32_t lvl = (uint32_t)__ffs(m) - 1u;
         m &= m - 1u;
-        for (uint32_t j = x0 + tid; j < x1; j += 64) {
+        if (x0 + tid < x1 && rec_level(lx) == lvl) mass_add(&a[lx.y], a[lx.x] * rec_factor(lx), true);
+        for (uint32_t j = x0 + tid + 64; j < x1; j += 64) {
           const uint4 l = lk[j];
           if (rec_level(l) == lvl) mass_add(&a[l.y], a[l.x] * rec_factor(l), true);
         }
         wave_sync();
       }
+      e0 = ne0;
+      x0 = nx0;
+      x1 = nx1;
+      m0 = nm;
+      le = nle;
+      lx = nlx;
     }
   } else if (tid < 128) {
-    // beta, frames descending; epsilon links from the highest source level
+    // beta, frames descending; epsilon links from the highest source level;
+    // read ahead like alpha
     const uint32_t lane = tid - 64;
     double* b = sh.w.cp.b;
+    const uint4 none = make_uint4(0, 0, 0, 0);
+    auto bounds = [&](int t, uint32_t& x0, uint32_t& x1, uint32_t& e1) {
+      x0 = kfs[2 * t + 1];
+      x1 = kfs[2 * t + 2];
+      e1 = t < T ? kfs[2 * t + 3] : x1;  // emitting links out of t (into t+1)
+    };
+    uint32_t x0, x1, e1;
+    bounds(T, x0, x1, e1);
+    uint32_t m0 = sh.w.cp.lmask[T];
+    uint4 le = x1 + lane < e1 ? lk[x1 + lane] : none, lx = x0 + lane < x1 ? lk[x0 + lane] : none;
     for (int t = T; t >= 0; --t) {
-      const uint32_t x0 = kfs[2 * t + 1], x1 = kfs[2 * t + 2];
-      const uint32_t e1 = t < T ? kfs[2 * t + 3] : x1;  // emitting links out of t (into t+1)
-      for (uint32_t j = x1 + lane; j < e1; j += 64) {
+      uint32_t nx0 = 0, nx1 = 0, ne1 = 0, nm = 0;
+      uint4 nle = none, nlx = none;
+      if (t > 0) {
+        bounds(t - 1, nx0, nx1, ne1);
+        nm = sh.w.cp.lmask[t - 1];
+        if (nx1 + lane < ne1) nle = lk[nx1 + lane];
+        if (nx0 + lane < nx1) nlx = lk[nx0 + lane];
+      }
+      if (x1 + lane < e1) mass_add(&b[le.x], rec_factor(le) * b[le.y], true);
+      for (uint32_t j = x1 + lane + 64; j < e1; j += 64) {
         const uint4 l = lk[j];
         mass_add(&b[l.x], rec_factor(l) * b[l.y], true);
       }
       wave_sync();
-      uint32_t m = sh.w.cp.lmask[t];
-      while (m) {
+      for (uint32_t m = m0; m;) {
         const uint32_t lvl = 31u - (uint32_t)__clz(m);
         m &= ~(1u << lvl);
-        for (uint32_t j = x0 + lane; j < x1; j += 64) {
+        if (x0 + lane < x1 && rec_level(lx) == lvl) mass_add(&b[lx.x], rec_factor(lx) * b[lx.y], true);
+        for (uint32_t j = x0 + lane + 64; j < x1; j += 64) {
           const uint4 l = lk[j];
           if (rec_level(l) == lvl) mass_add(&b[l.x], rec_factor(l) * b[l.y], true);
         }
         wave_sync();
       }
+      x0 = nx0;
+      x1 = nx1;
+      e1 = ne1;
+      m0 = nm;
+      le = nle;
+      lx = nlx;
     }
   }
   __syncthreads();
