@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB_PATH = os.path.join(HERE, "libwfstdec.so")
-SOURCES = ["wd_graph.hip", "wd_forward.hip", "wd_util.hip", "wd_grid.hip", "wd_lattice.hip", "wd_api.hip",
+SOURCES = ["wd_graph.hip", "wd_forward.hip", "wd_links.hip", "wd_util.hip", "wd_grid.hip", "wd_lattice.hip", "wd_api.hip",
            "wd_det.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -441,6 +441,7 @@ static wd_status run_finish(wd_stream* run, wd_result** out) {
     launch_lattice(run->g->dg, R.desc, B, lp, s);
     launch_grid_nodes(R.desc, R.grid, B, s);
   } else {
+    launch_links(run->g->dg, R.desc, B, s);
     launch_lattice(run->g->dg, R.desc, B, run->prm, s);
   }
   if (run->ev[2]) (void)hipEventRecord(run->ev[2], s);
@@ -715,6 +716,7 @@ extern "C" wd_status wd_decode_noalloc(const wd_graph* g, const float* loglikes,
   const Params prm{p->beam, p->max_active, p->lattice_beam, p->flags};
   launch_check_loglikes(R.desc, 1, g->P, R.bad, s);
   launch_forward(g->dg, R.desc, 1, prm, R.bad, s);
+  launch_links(g->dg, R.desc, 1, s);
   launch_lattice(g->dg, R.desc, 1, prm, s);
   LaneInfo I;
   if ((st = hip_check(hipGetLastError(), "launch")) ||

@@ -47,11 +47,6 @@ struct FwdShared {
   uint32_t lvl_wide;   // LDS table: first epsilon level the whole workgroup runs
   uint32_t lvl_live;   // LDS table: levels that may hold an entry within the cutoff (level_bit)
   unsigned long long deg_tot;  // frontier out-degree totals (epsilon << 32 | emitting), small frames
-  uint32_t wcnt[kWaves];  // emitting lattice links of the frame per wavefront (one item per thread)
-  uint32_t lnx;        // epsilon lattice links of the frame (one-wavefront epsilon link pass)
-  // frontier token whose epsilon out-arcs start at epsilon work item i < 64
-  // (kNoSlot elsewhere), written by the degree scan of small frames
-  uint16_t xo[64];
   uint32_t hcount;     // LDS table: reserved entries
   uint32_t spill;      // LDS table full: the frame goes global
   uint32_t n_bk;       // LDS table: epsilon bucket entries
@@ -282,7 +277,6 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
 
   for (uint32_t i = tid; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nb[i] = 0;
   for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
-  if (tid < 64u) sh.xo[tid] = kNoSlot;
   h_clear(sh, kHashCap);
   if (tid == 0) {
     sh.n_touched = 0;
@@ -294,7 +288,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
   int status = 0;  // WD_OK
   uint32_t ovf = 0;
   uint32_t best_key = cost_key(0.0f);
-  uint64_t node_base = 0, node_base_prev = 0, link_base = 0;
+  uint64_t node_base = 0;
   uint32_t n_prev = 0, W = 0;
   bool front_lds = true;  // where the frontier of the last finished frame is
   bool front_own = false; // its emitting work items' owners are in own_e
@@ -310,7 +304,8 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     sh.c_need_frame = 1;
     sh.c_need_arcs = 0;
   }
-  bool hist_ok = true;  // history (nodes, links) still being stored
+  bool hist_ok = true;  // history (the node store) still being stored
+  uint32_t warm_bad = 0;  // a warming load returned the sentinel payload (never)
   uint32_t par = 0;     // scratch buffer parity of the workgroup collectives
   int t = L.t0;
   // step profile: slot k < kProfStamps of frame t gets the wall clock when
@@ -337,11 +332,9 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     status = __builtin_amdgcn_readfirstlane(go_on ? 0 : I.status);
     if (status != 0) return;
     ovf = __builtin_amdgcn_readfirstlane(I.overflow);
-    hist_ok = (ovf & (kOvfNodes | kOvfLinks)) == 0;
+    hist_ok = (ovf & kOvfNodes) == 0;
     node_base = uniform64(I.tokens);
     n_prev = __builtin_amdgcn_readfirstlane(I.last_tokens);
-    node_base_prev = node_base - n_prev;
-    link_base = uniform64(I.links);
     W = __builtin_amdgcn_readfirstlane(L.f_edeg[n_prev]);
     front_lds = false;
     my_eps = tid == 0 ? I.eps_arcs : 0;
@@ -371,10 +364,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     uint32_t nbits = 0, shift = 0;
     uint64_t eps_frame = 0;
     bool failed = false;
-    uint4 my_c = make_uint4(0, 0, 0, 0);  // this thread's first candidate (work item tid)
-    uint32_t my_slot = kHashCap;          // its destination's slot in the LDS table
     float warm = 0.0f;  // values of cache-warming loads, read at the end of the frame
-    float warm_x = 0.0f;
     // ---------------------------------------------------- token passing
     for (int attempt = 0; attempt < 2; ++attempt) {
       eps_frame = 0;
@@ -413,13 +403,11 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
             float x = c + ac;
             x = canon(x + __uint_as_float(r.y));
             const uint32_t xk = cost_key(x);
-            uint32_t cslot = kHashCap;
             if (xk < kInfKey) {
               my_best = xk < my_best ? xk : my_best;
               if (!sh.spill) {
                 bool fresh;
                 const uint32_t slot = h_insert(sh, dst, &fresh);
-                cslot = slot;
                 if (slot < (uint32_t)kHashCap) {
                   atomicMin(&sh.h_val[slot], pack_tok(xk, r.w));
                   if (fresh && cls != kNoEps) {
@@ -435,12 +423,6 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
                   }
                 }
               }
-            }
-            const uint4 cv = make_uint4(r.w, (uint32_t)(node_base_prev + i), dst, __float_as_uint(x));
-            L.cand[w] = cv;
-            if (base == 0) {
-              my_c = cv;
-              my_slot = cslot;
             }
           }
           // (the collective's barrier also publishes the table writes)
@@ -738,9 +720,6 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
                 first = old == kEmpty;
                 my_best = xk < my_best ? xk : my_best;
               }
-              const uint4 cv = make_uint4(r.w, (uint32_t)(node_base_prev + i), dst, __float_as_uint(x));
-              L.cand[w] = cv;
-              if (base == 0) my_c = cv;
             }
             note_touch(first, dst, cls, sh, g, L);
           }
@@ -849,18 +828,6 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       cut_key = vkey < kcutb ? vkey : kcutb;
     }
     stamp(4);
-    // Emitting lattice links: a thread's own candidate (work item tid) is a
-    // link when it is within the final cutoff.  With one item per thread,
-    // each wavefront's count goes out with the compaction's barrier and the
-    // links are written right after it, beside the degree prefix sums.
-    const bool early_e = W <= (uint32_t)kThreads;  // (uniform; W = 0 at frame 0)
-    bool e_in = false;
-    if (early_e) {
-      const uint32_t xk = cost_key(__uint_as_float(my_c.w));
-      e_in = t > 0 && tid < W && xk <= cut_key && xk < kInfKey;
-      const uint64_t bal = __ballot(e_in);
-      if (lane_id() == 0) sh.wcnt[wave_id()] = (uint32_t)__popcll(bal);
-    }
     // -------------------------------- compaction into a frontier sorted by state
     const bool fl = n_keep <= (uint32_t)kFrontCap;
     const Front f = front_at(fl, sh, L);
@@ -950,10 +917,6 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           r += dpp32<kDppQuadSwap2>(r, 0u);
           if (sub == 0) {
             place(r, s, sh.rs_pack[e]);
-            if (lds) sh.h_val[sh.rs_slot[e]] = node_base + r;  // the table now maps kept states to node ids
-            else L.idx[s] = (uint32_t)(node_base + r);
-            // the link pass reads the token's epsilon arcs
-            if (o1.y > o0.y) warm_x = __uint_as_float(g.xarc[o0.y].y);
             f.ebeg[r] = o0.x;
             f.xbeg[r] = o0.y;
             f.edeg[r] = o1.x - o0.x;  // degrees for now, prefix sums below
@@ -969,7 +932,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         const uint32_t ssh = sbits > 11u ? sbits - 11u : 0u;
         for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
         __syncthreads();
-        uint32_t bb[2] = {0, 0}, loc[2] = {0, 0}, sv[2] = {0, 0}, sl[2] = {0, 0};
+        uint32_t bb[2] = {0, 0}, loc[2] = {0, 0}, sv[2] = {0, 0};
         unsigned long long vv[2] = {0, 0};
         bool kp[2] = {false, false};
         for (int u = 0; u < 2; ++u) {
@@ -979,7 +942,6 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           if ((uint32_t)(vv[u] >> 32) > cut_key) continue;
           kp[u] = true;
           sv[u] = sh.rs_state[j];
-          sl[u] = sh.rs_slot[j];
           bb[u] = sv[u] >> ssh;
           loc[u] = atomicAdd(&sh.hist[bb[u]], 1u);
         }
@@ -1007,8 +969,6 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           uint32_t r = b0;
           for (uint32_t q = b0; q < b1; ++q) r += sh.srt[q] < sv[u];
           place(r, sv[u], vv[u]);
-          if (lds) sh.h_val[sl[u]] = node_base + r;  // the table now maps kept states to node ids
-          else L.idx[sv[u]] = (uint32_t)(node_base + r);
         }
       }
     } else {
@@ -1038,54 +998,20 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           word &= word - 1u;
           const uint32_t s = (w << 5) | b;
           place(p, s, spack[L.idx[s]]);
-          L.idx[s] = (uint32_t)(node_base + p);
           ++p;
         }
       }
     }
     __syncthreads();
     stamp(5);
-    // node id of a state that survived frame t
-    auto dst_node = [&](uint32_t s) -> uint64_t {
-      if (lds) {
-        const uint32_t slot = h_find(sh, s);
-        return slot < (uint32_t)kHashCap ? sh.h_val[slot] : kEmpty;
-      }
-      return L.idx[s];
-    };
-    // the emitting links of the frame, when every work item is a thread's own
-    uint32_t nE = 0, bad_idx = 0;
-    auto write_emitting = [&]() {
-      uint32_t before = 0;
-#pragma unroll
-      for (int i = 0; i < kWaves; ++i) {
-        const uint32_t c = sh.wcnt[i];
-        nE += c;
-        before += (uint32_t)i < wave_id() ? c : 0u;
-      }
-      const uint64_t bal = __ballot(e_in);
-      if (!e_in || !hist_ok || link_base + nE > L.link_cap) return;
-      // the thread's own candidate: its insertion left the slot
-      const uint64_t dn = lds && my_slot < (uint32_t)kHashCap ? sh.h_val[my_slot] : dst_node(my_c.z);
-      if (dn < node_base || dn >= node_base + n_keep) {
-        bad_idx = 1;
-        return;
-      }
-      // the frontier reads come before the stores: a wait for a flat load
-      // also waits for every store in flight
-      const uint32_t q = (uint32_t)(dn - node_base);
-      const uint32_t fk = f.key[q], fa = f.arc[q];
-      const uint32_t pos = before + rank_in(bal);
-      L.links[link_base + pos] = make_uint4(my_c.x, my_c.y, (uint32_t)dn, my_c.w);
-      if (fk == cost_key(__uint_as_float(my_c.w)) && fa == my_c.x) L.n_pred[dn] = my_c.y;
-    };
+    // the table's claimed slots, read before the degree pass's barrier (after
+    // it, the frame end clears them and resets the count)
+    const uint32_t h_used_n = sh.hcount > (uint32_t)kHashMax ? (uint32_t)kHashCap : sh.hcount;
     // ------------------------------- arc offsets and degree prefix sums
     uint32_t W_next, W_eps;
     if (deg_ready) {
       // at most kDirectRank tokens with their degrees in place: the last
-      // wavefront (no work items in small frames, which the others write as
-      // emitting links meanwhile) sums them, four per lane, and publishes
-      // the totals
+      // wavefront sums them, four per lane, and publishes the totals
       static_assert(kDirectRank <= 4 * 64, "four tokens per lane");
       if (tid >= kThreads - 64u) {
         const uint32_t lane = lane_id();
@@ -1106,7 +1032,6 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           if (p < n_keep) {
             f.edeg[p] = eb;
             f.xdeg[p] = xb;
-            if (dx[k] != 0 && xb < 64u) sh.xo[xb] = (uint16_t)p;
           }
           eb += de[k];
           xb += dx[k];
@@ -1117,7 +1042,6 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           f.xdeg[n_keep] = (uint32_t)(inc >> 32);
         }
       }
-      if (early_e) write_emitting();
       __syncthreads();
       W_next = (uint32_t)sh.deg_tot;
       W_eps = (uint32_t)(sh.deg_tot >> 32);
@@ -1153,7 +1077,6 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         f.edeg[n_keep] = W_next;
         f.xdeg[n_keep] = W_eps;
       }
-      if (early_e) write_emitting();
       __syncthreads();
     }
     stamp(6);
@@ -1191,186 +1114,25 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         warm += __uint_as_float(g.earc[f.ebeg[p] + (w - f.edeg[p])].y);
       }
     }
-    // -------------------------------------------------- lattice links of frame t
-    uint32_t nX = 0, xmask = 0;
-    // With the emitting links written and at most 64 epsilon out-arcs on the
-    // frontier, wavefront 1 writes the epsilon links alone: a wavefront scan
-    // places them, and the frame's closing collective publishes their count.
-    const bool wave_x = early_e && W_eps <= 64u;  // (uniform)
-    if (wave_x) {
-      if (tid >= 64u && tid < 128u) {
-        const uint32_t e = tid - 64u;
-        bool in = false;
-        uint4 r = make_uint4(0, 0, 0, 0);
-        uint32_t p = 0, xk = kNoKey;
-        float x = 0.0f;
-        // the item's token: with the degree scan's start marks, the one
-        // whose epsilon items start at the last mark at or below e (item 0
-        // always starts a token's run)
-        uint64_t starts = 0;
-        if (deg_ready) starts = __ballot(sh.xo[e] != kNoSlot);
-        if (e < W_eps) {
-          if (deg_ready) {
-            // marks at or below e moved to the top: the last one is e - clz below
-            const uint64_t upto = starts << (63u - opaque(e));
-            p = sh.xo[e - (uint32_t)__clzll(upto)];
-          } else {
-            p = search_le(f.xdeg, n_keep, e);
-          }
-          r = g.xarc[f.xbeg[p] + (e - f.xdeg[p])];
-          x = canon(key_cost(f.key[p]) + __uint_as_float(r.y));
-          xk = cost_key(x);
-          in = xk <= cut_key && xk < kInfKey;
-        }
-        const uint64_t bal = __ballot(in);
-        const uint32_t cntx = (uint32_t)__popcll(bal);
-        if (tid == 64u) sh.lnx = cntx;
-        if (in && hist_ok && link_base + nE + cntx <= L.link_cap) {
-          const uint64_t dn = dst_node(r.x);
-          if (dn < node_base || dn >= node_base + n_keep) {
-            bad_idx = 1;
-          } else {
-            const uint32_t sn = (uint32_t)(node_base + p);
-            const uint64_t at = link_base + nE + rank_in(bal);
-            const uint32_t q = (uint32_t)(dn - node_base);
-            const uint32_t cls = f.cls[p], fk = f.key[q], fa = f.arc[q];  // before the stores
-            L.links[at] = make_uint4(r.w, sn, (uint32_t)dn, __float_as_uint(x));
-            L.link_lvl[at] = (uint8_t)cls;
-            xmask |= 1u << (cls < 31 ? cls : 31);
-            if (fk == xk && fa == r.w) L.n_pred[dn] = sn;
-          }
-        }
-      }
-      stamp(7);
-    } else {
-      // emitting run (unless written above): candidates in work-item order
-      // are in arc-id order
-      const uint32_t Wc = t > 0 && !early_e ? W : 0;
-      const uint32_t per = (Wc + kThreads - 1) / kThreads;
-      const uint32_t w0 = tid * per < Wc ? tid * per : Wc;
-      const uint32_t w1 = w0 + per < Wc ? w0 + per : Wc;
-      // with one item per thread, the item is the thread's own candidate
-      uint32_t cnt = 0;
-      for (uint32_t w = w0; w < w1; ++w) {
-        const uint32_t xb = per == 1 ? my_c.w : L.cand[w].w;
-        const uint32_t xk = cost_key(__uint_as_float(xb));
-        cnt += xk <= cut_key && xk < kInfKey;
-      }
-      // epsilon run: every epsilon out-arc of the frontier within the cutoff
-      const uint32_t perx = (W_eps + kThreads - 1) / kThreads;
-      const uint32_t e0 = tid * perx < W_eps ? tid * perx : W_eps;
-      const uint32_t e1 = e0 + perx < W_eps ? e0 + perx : W_eps;
-      uint32_t cntx = 0;
-      uint4 rx0 = make_uint4(0, 0, 0, 0);  // the thread's first epsilon arc, reused below
-      uint32_t px0 = 0;
-      if (e0 < e1) {
-        uint32_t p = search_le(f.xdeg, n_keep, e0);
-        px0 = p;
-        for (uint32_t e = e0; e < e1; ++e) {
-          while (f.xdeg[p + 1] <= e) ++p;
-          const uint4 r = g.xarc[f.xbeg[p] + (e - f.xdeg[p])];
-          if (e == e0) rx0 = r;
-          const uint32_t xk = cost_key(canon(key_cost(f.key[p]) + __uint_as_float(r.y)));
-          cntx += xk <= cut_key && xk < kInfKey;
-        }
-      }
-      uint64_t tot2;
-      const uint64_t ex2 = block_excl_scan64(((uint64_t)cntx << 32) | cnt, sh.bs, par, &tot2);
-      uint32_t pos = (uint32_t)ex2, posx = (uint32_t)(ex2 >> 32);
-      if (!early_e) nE = (uint32_t)tot2;
-      nX = (uint32_t)(tot2 >> 32);
-      stamp(7);
-      if (hist_ok && link_base + nE + nX > L.link_cap) {
-        hist_ok = false;
-        ovf |= kOvfLinks;
-      }
-      if (hist_ok) {
-        for (uint32_t w = w0; w < w1; ++w) {
-          uint4 c = my_c;
-          if (per != 1) c = L.cand[w];
-          const uint32_t xk = cost_key(__uint_as_float(c.w));
-          if (!(xk <= cut_key && xk < kInfKey)) continue;
-          // the thread's own candidate: its insertion left the slot
-          const uint64_t dn = per == 1 && lds && my_slot < (uint32_t)kHashCap ? sh.h_val[my_slot] : dst_node(c.z);
-          if (dn < node_base || dn >= node_base + n_keep) {
-            bad_idx = 1;
-            continue;
-          }
-          // the frontier reads come before the stores: a wait for a flat load
-          // also waits for every store in flight
-          const uint32_t q = (uint32_t)(dn - node_base);
-          const uint32_t fk = f.key[q], fa = f.arc[q];
-          L.links[link_base + pos] = make_uint4(c.x, c.y, (uint32_t)dn, c.w);
-          ++pos;
-          if (fk == xk && fa == c.x) L.n_pred[dn] = c.y;
-        }
-        if (e0 < e1) {
-          uint32_t p = px0;
-          for (uint32_t e = e0; e < e1; ++e) {
-            while (f.xdeg[p + 1] <= e) ++p;
-            uint4 r = rx0;
-            if (e != e0) r = g.xarc[f.xbeg[p] + (e - f.xdeg[p])];
-            const float x = canon(key_cost(f.key[p]) + __uint_as_float(r.y));
-            const uint32_t xk = cost_key(x);
-            if (!(xk <= cut_key && xk < kInfKey)) continue;
-            const uint64_t dn = dst_node(r.x);
-            if (dn < node_base || dn >= node_base + n_keep) {
-              bad_idx = 1;
-              continue;
-            }
-            const uint32_t sn = (uint32_t)(node_base + p);
-            const uint64_t at = link_base + nE + posx;
-            const uint32_t q = (uint32_t)(dn - node_base);
-            const uint32_t cls = f.cls[p], fk = f.key[q], fa = f.arc[q];  // before the stores
-            L.links[at] = make_uint4(r.w, sn, (uint32_t)dn, __float_as_uint(x));
-            L.link_lvl[at] = (uint8_t)cls;
-            xmask |= 1u << (cls < 31 ? cls : 31);
-            ++posx;
-            if (fk == xk && fa == r.w) L.n_pred[dn] = sn;
-          }
-        }
-      }
-    }
+    // (the frame's lattice links are formed after the forward pass, from the
+    // node store: every frame at once, off this chain)
+    stamp(7);
     // a payload no sum of a finite weight and a log-likelihood has: keeps the
     // warming loads without waiting for them earlier
-    if (__float_as_uint(warm) == 0x7fc00001u || __float_as_uint(warm_x) == 0x7fc00001u) bad_idx |= 2u;
-    // insertions to undo, read before the barrier after which thread 0 resets the count
-    // (a frame that claimed more slots than it could record clears them all)
-    const uint32_t h_used_n = sh.hcount > (uint32_t)kHashMax ? (uint32_t)kHashCap : sh.hcount;
-    const uint32_t fl_or = block_or((bad_idx ? 0x80000000u : 0u) | xmask, sh.bs, par);
+    warm_bad |= __float_as_uint(warm) == 0x7fc00001u ? 1u : 0u;
     stamp(8);
-    if (wave_x) {
-      nX = sh.lnx;
-      if (hist_ok && link_base + nE + nX > L.link_cap) {
-        hist_ok = false;
-        ovf |= kOvfLinks;
-      }
-    }
-    note(kProfStamps, (lds ? 1ull : 0ull) | ((uint64_t)n_keep << 8) | ((uint64_t)(nE + nX) << 32));
+    note(kProfStamps, (lds ? 1ull : 0ull) | ((uint64_t)n_keep << 8));
     note(kProfStamps + 1, (t > 0 ? (uint64_t)W : 0ull) | ((uint64_t)(lds ? sh.n_bk : 0u) << 32));
-    if (fl_or & 0x80000000u) {
-      status = kStatusInternal;
-      break;
-    }
-    if (tid == kBook) {
-      L.link_off[t] = link_base;
-      L.link_xoff[t] = link_base + nE;
-      L.link_off[t + 1] = link_base + nE + nX;
-      L.xmask[t] = fl_or & 0x7fffffffu;
-    }
-    link_base += nE + nX;
     // ----------------------------------------------------- next frame
-    node_base_prev = node_base;
     node_base += n_keep;
     n_prev = n_keep;
     W = W_next;
     front_lds = fl;
     front_own = own_e_ok;
-    // (the frame's last reads of these counters came before the link
-    // pass's closing collective)
+    // (the frame's last reads of these counters came before the degree
+    // pass's barrier)
     for (uint32_t i = tid; i <= (uint32_t)kMaxLevels; i += kThreads) sh.nb[i] = 0;
     for (uint32_t i = tid; i < (uint32_t)kHistBins; i += kThreads) sh.hist[i] = 0;
-    if (tid < 64u) sh.xo[tid] = kNoSlot;
     h_clear(sh, h_used_n);
     if (tid == 0) {
       sh.n_touched = 0;
@@ -1394,11 +1156,13 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       L.f_cls[i] = sh.f_cls[i];
     }
   }
+  const uint32_t wb = block_or(warm_bad, sh.bs, par);
   const uint64_t eps = block_sum64(my_eps, sh.bs, par);
   const uint64_t arcs = sh.c_arcs + eps;  // (the bookkeeping thread's writes, before the barrier)
   if (tid == 0) {
     LaneInfo* info = L.info;
-    if (status == 0 && (ovf & (kOvfNodes | kOvfLinks))) status = 4;
+    if (status == 0 && wb) status = kStatusInternal;
+    if (status == 0 && (ovf & kOvfNodes)) status = 4;
     info->status = status;
     info->frames_done = t;
     info->overflow = ovf;
@@ -1406,8 +1170,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     info->eps_arcs = eps;
     info->tokens = sh.c_tokens;
     info->max_tokens = sh.c_max_tokens;
-    info->links = link_base;
-    info->need_links = link_base;
+    // (links, need_links: set by the link kernels after the forward pass)
     info->need_frame_tokens = sh.c_need_frame;
     info->need_frame_arcs = sh.c_need_arcs;
     info->last_tokens = n_prev;

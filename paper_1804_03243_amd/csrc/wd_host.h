@@ -26,6 +26,9 @@ wd_status hip_check(hipError_t e, const char* what);
 
 void launch_forward(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm,
                     const uint32_t* bad, hipStream_t s);
+// Lattice links of one-workgroup decodes, from the node store, after the
+// forward pass (all frames at once); before launch_lattice.
+void launch_links(const DevGraph& g, const LaneDesc* lanes, int B, hipStream_t s);
 void launch_lattice(const DevGraph& g, const LaneDesc* lanes, int B, const Params& prm, hipStream_t s);
 size_t grid_lane_bytes();
 // Raw window slots of the link store with incremental pruning.
