@@ -53,8 +53,8 @@ BYTES_LINK = 16
 # runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
 # divided by the counter's reading per byte of a plain device copy of known
 # size (bench.py --copy-kernel-bytes).  Valid while k_forward's sources hash to this.
-TRAFFIC = {"sources_sha256": "f1b31e73928979c1d4715bbc21a0884b30ae340f5d2492b5446cac1eac9326a5",
-           "bytes_per_launch": 69287534}
+TRAFFIC = {"sources_sha256": "e3b0ba4ef44e1d800230ac73f0dc07b2c5266519a6a2045b2c6e0d4b46bcc7b6",
+           "bytes_per_launch": 65986404}
 
 
 FORWARD_SOURCES = ("wd_block.h", "wd_common.h", "wd_forward.hip")  # what k_forward is built from
@@ -279,8 +279,8 @@ def batch(wfstdec, graph, n_utts: int = 64, steps: int = 3, cpu: bool = True) ->
     return out
 
 
-PHASE_NAMES = ("expand", "eps_closure", "survivors", "max_active", "compact", "degrees_emitting_links",
-               "eps_links", "links_published", "frame_end")
+PHASE_NAMES = ("expand", "eps_closure", "survivors", "max_active", "compact", "degrees",
+               "owners_warming", "bookkeeping", "frame_end")
 
 
 LATTICE_PHASE_NAMES = ("final_costs", "pruning_sweep", "kept_links", "kept_offsets_records", "posteriors",

@@ -127,11 +127,12 @@ typedef struct {
  * (0) the frame's start, the end of (1) the emitting expansion and its best
  * cost, (2) the epsilon closure, (3) the survivor pass, (4) the max-active
  * cutoff, (5) the compaction into the state-sorted frontier, (6) the degree
- * prefix sums (and the emitting lattice links), (7) the epsilon lattice
- * links, (8) the frame's links published (a workgroup collective), (9) the
- * frame (table reset); then word 10 = (1 if the frame's token table was in
- * LDS) | surviving tokens << 8 | lattice links << 32, and word 11 = emitting
- * work items | LDS-table epsilon bucket entries << 32 (touched states with
+ * prefix sums, (7) the next frame's work-item owners and cache warming, (8)
+ * the frame's bookkeeping, (9) the frame (table reset); then word 10 = (1 if
+ * the frame's token table was in LDS) | surviving tokens << 8 | lattice
+ * links << 32 (the links are formed after the forward pass, every frame at
+ * once, and their count is filled in then), and word 11 = emitting work
+ * items | LDS-table epsilon bucket entries << 32 (touched states with
  * epsilon arcs). */
 #define WD_PHASE_STAMPS 10
 #define WD_PHASE_SLOTS 12
