@@ -306,6 +306,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
   }
   bool hist_ok = true;  // history (the node store) still being stored
   uint32_t warm_bad = 0;  // a warming load returned the sentinel payload (never)
+  float warm_prev = 0.0f;  // the previous frame's warming values (read a frame late)
   uint32_t par = 0;     // scratch buffer parity of the workgroup collectives
   int t = L.t0;
   // step profile: slot k < kProfStamps of frame t gets the wall clock when
@@ -364,7 +365,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     uint32_t nbits = 0, shift = 0;
     uint64_t eps_frame = 0;
     bool failed = false;
-    float warm = 0.0f;  // values of cache-warming loads, read at the end of the frame
+    float warm = 0.0f;  // values of cache-warming loads, read at the end of the next frame
     // ---------------------------------------------------- token passing
     for (int attempt = 0; attempt < 2; ++attempt) {
       eps_frame = 0;
@@ -1080,14 +1081,12 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       __syncthreads();
     }
     stamp(6);
-    // owners of the next frame's emitting work items, written by threads
-    // 256..511 (idle in the link pass of small frames)
+    // owners of the next frame's emitting work items, one item per thread
+    // of the lower half (each found by a search of the degree prefix sums:
+    // a token's own loop over its arcs would serialise a high out-degree)
     const bool own_e_ok = fl && W_next <= kOwnE;
-    if (own_e_ok && tid >= 256u && tid < 512u)
-      for (uint32_t p = tid - 256u; p < n_keep; p += 256u) {
-        const uint32_t k1 = f.edeg[p + 1];
-        for (uint32_t k = f.edeg[p]; k < k1; ++k) own_e[k] = (uint16_t)p;
-      }
+    if (own_e_ok && tid < 512u)
+      for (uint32_t k = tid; k < W_next; k += 512u) own_e[k] = (uint16_t)search_le(f.edeg, n_keep, k);
     if (tid == kBook) {
       L.node_off[t] = node_base;
       L.node_off[t + 1] = node_base + n_keep;
@@ -1118,8 +1117,10 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     // node store: every frame at once, off this chain)
     stamp(7);
     // a payload no sum of a finite weight and a log-likelihood has: keeps the
-    // warming loads without waiting for them earlier
-    warm_bad |= __float_as_uint(warm) == 0x7fc00001u ? 1u : 0u;
+    // warming loads, whose values are read a frame later, so that no
+    // wavefront waits for them before the frame's last barrier
+    warm_bad |= __float_as_uint(warm_prev) == 0x7fc00001u ? 1u : 0u;
+    warm_prev = warm;
     stamp(8);
     note(kProfStamps, (lds ? 1ull : 0ull) | ((uint64_t)n_keep << 8));
     note(kProfStamps + 1, (t > 0 ? (uint64_t)W : 0ull) | ((uint64_t)(lds ? sh.n_bk : 0u) << 32));
@@ -1156,6 +1157,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       L.f_cls[i] = sh.f_cls[i];
     }
   }
+  warm_bad |= __float_as_uint(warm_prev) == 0x7fc00001u ? 1u : 0u;
   const uint32_t wb = block_or(warm_bad, sh.bs, par);
   const uint64_t eps = block_sum64(my_eps, sh.bs, par);
   const uint64_t arcs = sh.c_arcs + eps;  // (the bookkeeping thread's writes, before the barrier)
