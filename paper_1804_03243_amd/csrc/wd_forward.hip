@@ -89,6 +89,27 @@ __device__ __forceinline__ Front front_at(bool lds, FwdShared& sh, const LaneDes
   return Front{L.f_state, L.f_key, L.f_arc, L.f_edeg, L.f_xdeg, L.f_ebeg, L.f_xbeg, L.f_cls};
 }
 
+// Emitting work item w of the previous frame's frontier: its arc index and
+// (in *c) its token's cost.  With the owners in place the frontier is in
+// LDS, and it is read there by name: accesses through a Front, which may
+// point either way, are flat accesses, whose waits also take in every
+// outstanding global load and store of the wavefront.
+// (The LDS reads go through LDS-qualified pointers: plain ones would let
+// the compiler merge them with the other branch's reads into flat ones.)
+typedef __attribute__((address_space(3))) const uint32_t LdsU32;
+
+__device__ __forceinline__ uint32_t item_arc(bool own, const uint16_t* own_e, FwdShared& sh, const Front& fp,
+                                             uint32_t n_prev, uint32_t w, float* c) {
+  if (own) {
+    const uint32_t i = own_e[w];
+    *c = key_cost(((LdsU32*)sh.f_key)[i]);
+    return ((LdsU32*)sh.f_ebeg)[i] + (w - ((LdsU32*)sh.f_edeg)[i]);
+  }
+  const uint32_t i = search_le(fp.edeg, n_prev, w);
+  *c = key_cost(fp.key[i]);
+  return fp.ebeg[i] + (w - fp.edeg[i]);
+}
+
 // ---------------------------------------------------------------- LDS table
 
 __device__ __forceinline__ uint32_t h_home(uint32_t s) { return (s * 0x9E3779B1u) >> 20; }  // 12 bits
@@ -392,9 +413,8 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           for (uint32_t base = 0; base < W; base += kThreads) {
             const uint32_t w = base + tid;
             if (w >= W) break;
-            const uint32_t i = front_own ? (uint32_t)own_e[w] : search_le(fp.edeg, n_prev, w);
-            const float c = key_cost(fp.key[i]);
-            const uint4 r = g.earc[fp.ebeg[i] + (w - fp.edeg[i])];
+            float c;
+            const uint4 r = g.earc[item_arc(front_own, own_e, sh, fp, n_prev, w, &c)];
             const uint32_t dst = r.x, cls = r.z >> 24;
             // CSR offsets of the destination: the epsilon range for the bucket,
             // and warm in cache for the degree pass if the token survives;
@@ -459,14 +479,16 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           auto relax_path = [&](uint32_t j, uint32_t w) {
             const uint4 e = sh.bk[j];
             const uint32_t pth = e.y + (w - sh.xp[j]);
+            // the first tail weights are loaded beside the head, before the
+            // path's length is known (every row holds pstride weights)
+            const float* tw = g.ptail + (size_t)pth * g.pstride;
+            const float w0 = g.pstride > 0u ? tw[0] : 0.0f;
+            const float w1 = g.pstride > 1u ? tw[1] : 0.0f;
+            const float w2 = g.pstride > 2u ? tw[2] : 0.0f;
             const uint4 h = g.phead[pth];
             const uint32_t k = h.w & 0xffu;
             float x = key_cost((uint32_t)(sh.h_val[e.x] >> 32));
             if (k > 1u) {
-              const float* tw = g.ptail + (size_t)pth * g.pstride;
-              const float w0 = tw[0];
-              const float w1 = k > 2u ? tw[1] : 0.0f;
-              const float w2 = k > 3u ? tw[2] : 0.0f;
               x = canon(x + w0);
               if (k > 2u) x = canon(x + w1);
               if (k > 3u) x = canon(x + w2);
@@ -707,9 +729,8 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
             bool first = false;
             uint32_t dst = 0, cls = kNoEps;
             if (w < W) {
-              const uint32_t i = front_own ? (uint32_t)own_e[w] : search_le(fp.edeg, n_prev, w);
-              const float c = key_cost(fp.key[i]);
-              const uint4 r = g.earc[fp.ebeg[i] + (w - fp.edeg[i])];
+              float c;
+              const uint4 r = g.earc[item_arc(front_own, own_e, sh, fp, n_prev, w, &c)];
               dst = r.x;
               cls = r.z >> 24;
               const float ac = -row[(r.z & 0xffffffu) - 1u];
@@ -832,21 +853,24 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     // -------------------------------- compaction into a frontier sorted by state
     const bool fl = n_keep <= (uint32_t)kFrontCap;
     const Front f = front_at(fl, sh, L);
+    // the LDS frontier by name, for the steps that run only when it is there
+    // (its accesses are then LDS accesses, not flat ones)
+    const Front fs = front_at(true, sh, L);
     bool deg_ready = false;  // the compaction filled the frontier's offsets and degrees
     if (hist_ok && node_base + n_keep > L.node_cap) {
       hist_ok = false;
       ovf |= kOvfNodes;
     }
-    auto place = [&](uint32_t p, uint32_t s, unsigned long long v) {
+    auto place = [&](const Front& F, uint32_t p, uint32_t s, unsigned long long v) {
       const uint64_t node = node_base + p;
       if (hist_ok) {
         L.n_state[node] = s;
         L.n_pack[node] = v;
         L.n_pred[node] = kNoArc;
       }
-      f.state[p] = s;
-      f.key[p] = (uint32_t)(v >> 32);
-      f.arc[p] = (uint32_t)v;
+      F.state[p] = s;
+      F.key[p] = (uint32_t)(v >> 32);
+      F.arc[p] = (uint32_t)v;
     };
     if (lds || n_keep <= (uint32_t)kRankMax) {
       if (!lds) {
@@ -883,6 +907,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         // read as ~0.  The quad's first lane also fills the frontier entry's
         // arc offsets, degrees and level (its loads overlap the ranking).
         static_assert(4 * kDirectRank <= kThreads, "four lanes per directly ranked entry");
+        static_assert(kDirectRank <= kFrontCap, "a directly ranked frontier is in LDS");
         deg_ready = true;
         if (!(lds && cut_key == kcutb)) {
           if (tid < m) {
@@ -917,12 +942,12 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           r += dpp32<kDppQuadSwap1>(r, 0u);
           r += dpp32<kDppQuadSwap2>(r, 0u);
           if (sub == 0) {
-            place(r, s, sh.rs_pack[e]);
-            f.ebeg[r] = o0.x;
-            f.xbeg[r] = o0.y;
-            f.edeg[r] = o1.x - o0.x;  // degrees for now, prefix sums below
-            f.xdeg[r] = o1.y - o0.y;
-            f.cls[r] = cls;
+            place(fs, r, s, sh.rs_pack[e]);  // (at most kDirectRank tokens: in LDS)
+            fs.ebeg[r] = o0.x;
+            fs.xbeg[r] = o0.y;
+            fs.edeg[r] = o1.x - o0.x;  // degrees for now, prefix sums below
+            fs.xdeg[r] = o1.y - o0.y;
+            fs.cls[r] = cls;
           }
         }
       } else {
@@ -969,7 +994,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           const uint32_t b1 = bb[u] + 1 < (uint32_t)kHistBins ? sh.hist[bb[u] + 1] : n_keep;
           uint32_t r = b0;
           for (uint32_t q = b0; q < b1; ++q) r += sh.srt[q] < sv[u];
-          place(r, sv[u], vv[u]);
+          place(f, r, sv[u], vv[u]);
         }
       }
     } else {
@@ -998,7 +1023,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           const uint32_t b = (uint32_t)__ffs(word) - 1u;
           word &= word - 1u;
           const uint32_t s = (w << 5) | b;
-          place(p, s, spack[L.idx[s]]);
+          place(f, p, s, spack[L.idx[s]]);
           ++p;
         }
       }
@@ -1021,8 +1046,8 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           const uint32_t p = 4u * lane + (uint32_t)k;
-          de[k] = p < n_keep ? f.edeg[p] : 0u;
-          dx[k] = p < n_keep ? f.xdeg[p] : 0u;
+          de[k] = p < n_keep ? fs.edeg[p] : 0u;
+          dx[k] = p < n_keep ? fs.xdeg[p] : 0u;
           sum += ((uint64_t)dx[k] << 32) | de[k];
         }
         const uint64_t inc = wave_incl_scan64(sum);
@@ -1031,16 +1056,16 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
         for (int k = 0; k < 4; ++k) {
           const uint32_t p = 4u * lane + (uint32_t)k;
           if (p < n_keep) {
-            f.edeg[p] = eb;
-            f.xdeg[p] = xb;
+            fs.edeg[p] = eb;
+            fs.xdeg[p] = xb;
           }
           eb += de[k];
           xb += dx[k];
         }
         if (lane == 63u) {
           sh.deg_tot = inc;
-          f.edeg[n_keep] = (uint32_t)inc;
-          f.xdeg[n_keep] = (uint32_t)(inc >> 32);
+          fs.edeg[n_keep] = (uint32_t)inc;
+          fs.xdeg[n_keep] = (uint32_t)(inc >> 32);
         }
       }
       __syncthreads();
@@ -1086,7 +1111,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
     // a token's own loop over its arcs would serialise a high out-degree)
     const bool own_e_ok = fl && W_next <= kOwnE;
     if (own_e_ok && tid < 512u)
-      for (uint32_t k = tid; k < W_next; k += 512u) own_e[k] = (uint16_t)search_le(f.edeg, n_keep, k);
+      for (uint32_t k = tid; k < W_next; k += 512u) own_e[k] = (uint16_t)search_le(fs.edeg, n_keep, k);
     if (tid == kBook) {
       L.node_off[t] = node_base;
       L.node_off[t + 1] = node_base + n_keep;
@@ -1108,9 +1133,9 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       if (tid >= 768u) {
         const uint32_t k = (tid - 768u) * 32u;
         if (k < P) warm += L.ll[(size_t)t * P + k];
-      } else if (tid >= 512u && tid - 512u < W_next) {
-        const uint32_t w = tid - 512u, p = search_le(f.edeg, n_keep, w);
-        warm += __uint_as_float(g.earc[f.ebeg[p] + (w - f.edeg[p])].y);
+      } else if (fl && tid >= 512u && tid - 512u < W_next) {
+        const uint32_t w = tid - 512u, p = search_le(fs.edeg, n_keep, w);
+        warm += __uint_as_float(g.earc[fs.ebeg[p] + (w - fs.edeg[p])].y);
       }
     }
     // (the frame's lattice links are formed after the forward pass, from the
