@@ -1123,19 +1123,18 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
       sh.c_tokens += n_keep;
       if (n_keep > sh.c_max_tokens) sh.c_max_tokens = n_keep;
     }
-    // Warm the caches for frame t+1 while the links are written: one load
-    // per 128-byte line of its log-likelihood row and one per work item of
-    // its first 256 emitting arcs.  The upper wavefronts issue them: in small
-    // frames they have no link items, and a wavefront's loads complete in
-    // order, so loads issued by a busy wavefront would make its own link
-    // loads wait for them.  The values are read only after the link pass.
+    // Warm the caches for frame t+1: one load per 128-byte line of its
+    // log-likelihood row and one per work item of its first 256 emitting
+    // arcs, issued by the upper wavefronts (the lower half fills the owners).
+    // Each value replaces the thread's last one rather than adding to it: an
+    // addition would wait for the load here, before the frame's last barrier.
     if (t < T) {
       if (tid >= 768u) {
         const uint32_t k = (tid - 768u) * 32u;
-        if (k < P) warm += L.ll[(size_t)t * P + k];
+        if (k < P) warm = L.ll[(size_t)t * P + k];
       } else if (fl && tid >= 512u && tid - 512u < W_next) {
         const uint32_t w = tid - 512u, p = search_le(fs.edeg, n_keep, w);
-        warm += __uint_as_float(g.earc[fs.ebeg[p] + (w - fs.edeg[p])].y);
+        warm = __uint_as_float(g.earc[fs.ebeg[p] + (w - fs.edeg[p])].y);
       }
     }
     // (the frame's lattice links are formed after the forward pass, from the
