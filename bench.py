@@ -53,8 +53,8 @@ BYTES_LINK = 16
 # runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
 # divided by the counter's reading per byte of a plain device copy of known
 # size (bench.py --copy-kernel-bytes).  Valid while k_forward's sources hash to this.
-TRAFFIC = {"sources_sha256": "e3b0ba4ef44e1d800230ac73f0dc07b2c5266519a6a2045b2c6e0d4b46bcc7b6",
-           "bytes_per_launch": 65986404}
+TRAFFIC = {"sources_sha256": "5290885931a59634b3e7221615f5be5b0fe07f24b2abb056213ee4b629a186cb",
+           "bytes_per_launch": 67017814}
 
 
 FORWARD_SOURCES = ("wd_block.h", "wd_common.h", "wd_forward.hip")  # what k_forward is built from
