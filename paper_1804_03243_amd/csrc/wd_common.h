@@ -94,8 +94,10 @@ struct DevGraph {
   // Epsilon paths (every path of one or more epsilon arcs out of a state,
   // enumerated when the graph is loaded; npaths = 0 when the graph has too
   // many or too long ones).  Paths of state s: [off[s].z, off[s+1].z).
-  //   phead[p] = {last state, last arc id, last arc's weight bits, k | xdeg << 8}
+  //   phead[2p] = {last state, last arc id, last arc's weight bits, k | xdeg << 8}
   //     k = number of arcs, xdeg = epsilon out-degree of the last state
+  //   phead[2p + 1] = bits of the weights of arcs 0..3 (those < k - 1; else 0),
+  //     so that a path of up to five arcs is one 32-byte record
   //   ptail[p * pstride + i] = weight of arc i < k - 1 (pstride = longest path - 1)
   const uint4* phead;
   const float* ptail;

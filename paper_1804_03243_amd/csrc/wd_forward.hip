@@ -435,7 +435,7 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
                     if (paths) {
                       lds_bucket_paths(sh, slot, o0.z, o1.z, o1.y - o0.y);
                       // start the state's first epsilon paths on their way for the closure
-                      warm = __uint_as_float(g.phead[o0.z].z);
+                      warm = __uint_as_float(g.phead[2 * (size_t)o0.z].z);
                     } else {
                       lds_bucket(sh, slot, o0, o1, cls);
                       // start the state's first epsilon arc on its way for the closure
@@ -479,20 +479,17 @@ __device__ __forceinline__ void forward_body(FwdShared& sh, const DevGraph& g, c
           auto relax_path = [&](uint32_t j, uint32_t w) {
             const uint4 e = sh.bk[j];
             const uint32_t pth = e.y + (w - sh.xp[j]);
-            // the first tail weights are loaded beside the head, before the
-            // path's length is known (every row holds pstride weights)
-            const float* tw = g.ptail + (size_t)pth * g.pstride;
-            const float w0 = g.pstride > 0u ? tw[0] : 0.0f;
-            const float w1 = g.pstride > 1u ? tw[1] : 0.0f;
-            const float w2 = g.pstride > 2u ? tw[2] : 0.0f;
-            const uint4 h = g.phead[pth];
+            // the head and the first four tail weights: one 32-byte record
+            const uint4 h = g.phead[2 * (size_t)pth], hw = g.phead[2 * (size_t)pth + 1];
             const uint32_t k = h.w & 0xffu;
             float x = key_cost((uint32_t)(sh.h_val[e.x] >> 32));
             if (k > 1u) {
-              x = canon(x + w0);
-              if (k > 2u) x = canon(x + w1);
-              if (k > 3u) x = canon(x + w2);
-              for (uint32_t i = 3; i + 1 < k; ++i) x = canon(x + tw[i]);
+              x = canon(x + __uint_as_float(hw.x));
+              if (k > 2u) x = canon(x + __uint_as_float(hw.y));
+              if (k > 3u) x = canon(x + __uint_as_float(hw.z));
+              if (k > 4u) x = canon(x + __uint_as_float(hw.w));
+              const float* tw = g.ptail + (size_t)pth * g.pstride;
+              for (uint32_t i = 4; i + 1 < k; ++i) x = canon(x + tw[i]);
             }
             const uint32_t xk = cost_key(canon(x + __uint_as_float(h.z)));
             if (xk > kcutb || xk >= kInfKey || sh.spill) return;

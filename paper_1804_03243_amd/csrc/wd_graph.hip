@@ -56,7 +56,7 @@ Layout layout(int64_t S, int64_t A, uint64_t Ae, uint64_t Ax, uint32_t nlevels, 
   l.olabel = take(sizeof(int32_t) * (uint64_t)(A ? A : 1));
   l.weight = take(sizeof(float) * (uint64_t)(A ? A : 1));
   l.level_base = take(sizeof(uint32_t) * (uint64_t)(nlevels + 1));
-  l.phead = npaths ? take(sizeof(uint4) * npaths) : 0;
+  l.phead = npaths ? take(sizeof(uint4) * 2 * npaths) : 0;
   l.ptail = npaths && pstride ? take(sizeof(float) * npaths * pstride) : 0;
   l.total = p;
   return l;
@@ -151,7 +151,7 @@ void eps_paths(const wd_graph_desc* d, const std::vector<uint32_t>& topo, Prepar
   p.pstride = longest - 1;
   p.paths = true;
   for (int64_t s = 0; s < S; ++s) p.off[s + 1].z = p.off[s].z + (uint32_t)npath[s];
-  p.phead.resize(total);
+  p.phead.assign(2 * total, make_uint4(0, 0, 0, 0));
   p.ptail.assign(total * p.pstride, 0.0f);
   // depth-first walk of the epsilon arcs out of s: stack of (state, next arc)
   std::vector<std::pair<uint32_t, uint32_t>> stack;
@@ -176,7 +176,10 @@ void eps_paths(const wd_graph_desc* d, const std::vector<uint32_t>& topo, Prepar
       const uint32_t k = (uint32_t)wpath.size() + 1;
       uint32_t wbits;
       std::memcpy(&wbits, &d->weight[a], 4);
-      p.phead[at] = make_uint4(v, a, wbits, k | (xdeg[v] << 8));
+      p.phead[2 * at] = make_uint4(v, a, wbits, k | (xdeg[v] << 8));
+      uint32_t tw[4] = {0, 0, 0, 0};  // the first tail weights, beside the head
+      for (uint32_t i = 0; i + 1 < k && i < 4; ++i) std::memcpy(&tw[i], &wpath[i], 4);
+      p.phead[2 * at + 1] = make_uint4(tw[0], tw[1], tw[2], tw[3]);
       for (uint32_t i = 0; i + 1 < k; ++i) p.ptail[at * p.pstride + i] = wpath[i];
       ++at;
       if (xdeg[v]) {
@@ -256,7 +259,7 @@ extern "C" wd_status wd_graph_bytes(const wd_graph_desc* d, size_t* bytes) {
   uint64_t Ae, Ax;
   wd_status st = prepare(d, p, &Ae, &Ax);
   if (st != WD_OK) return st;
-  *bytes = layout(d->num_states, d->num_arcs, Ae, Ax, p.nlevels, d->final_weight != nullptr, p.phead.size(),
+  *bytes = layout(d->num_states, d->num_arcs, Ae, Ax, p.nlevels, d->final_weight != nullptr, p.phead.size() / 2,
                   p.pstride).total;
   return WD_OK;
 }
@@ -272,7 +275,7 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
   if (st != WD_OK) return st;
   const int64_t S = d->num_states, A = d->num_arcs;
   const bool finals = d->final_weight != nullptr;
-  const uint64_t npaths = p.phead.size();
+  const uint64_t npaths = p.phead.size() / 2;
   const Layout l = layout(S, A, Ae, Ax, p.nlevels, finals, npaths, p.pstride);
   if (dev_bytes < l.total) return fail(WD_EINVAL, "graph_load: dev_buf smaller than wd_graph_bytes");
   hipStream_t s = (hipStream_t)stream;
@@ -291,7 +294,7 @@ extern "C" wd_status wd_graph_load(const wd_graph_desc* d, void* dev_buf, size_t
       (st = put(l.olabel, d->olabel, sizeof(int32_t) * A)) ||
       (st = put(l.weight, d->weight, sizeof(float) * A)) ||
       (st = put(l.level_base, p.level_base.data(), sizeof(uint32_t) * (p.nlevels + 1))) ||
-      (npaths && (st = put(l.phead, p.phead.data(), sizeof(uint4) * npaths))) ||
+      (npaths && (st = put(l.phead, p.phead.data(), sizeof(uint4) * 2 * npaths))) ||
       (npaths && p.pstride && (st = put(l.ptail, p.ptail.data(), sizeof(float) * npaths * p.pstride))))
     return st;
   if ((st = hip_check(hipStreamSynchronize(s), "graph upload sync"))) return st;
