@@ -53,11 +53,12 @@ BYTES_LINK = 16
 # runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
 # divided by the counter's reading per byte of a plain device copy of known
 # size (bench.py --copy-kernel-bytes).  Valid while k_forward's sources hash to this.
-TRAFFIC = {"sources_sha256": "5290885931a59634b3e7221615f5be5b0fe07f24b2abb056213ee4b629a186cb",
-           "bytes_per_launch": 67017814}
+TRAFFIC = {"sources_sha256": "939d545fec9ffe3ba92d01c1a49c7271ec731bb32f90926100672b7b1ed07a56",
+           "bytes_per_launch": 65999327}
 
 
-FORWARD_SOURCES = ("wd_block.h", "wd_common.h", "wd_forward.hip")  # what k_forward is built from
+# what k_forward is built from, and the device graph layout it reads
+FORWARD_SOURCES = ("wd_block.h", "wd_common.h", "wd_forward.hip", "wd_graph.hip")
 
 
 def sources_sha256() -> str:
